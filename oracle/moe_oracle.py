@@ -1,0 +1,436 @@
+"""Plain float64 statement of one routed MoE layer (forward, and backward
+through the experts and the permutation).
+
+TEST INFRASTRUCTURE ONLY (see the package docstring): slow on purpose, no
+blocking, fusion or reordering beyond what each definition states.
+
+Notation (paper, Section 1 and Table 2): S tokens, D dispatch dimension,
+E experts, top-K, F per-expert FFN width, H model hidden for a latent
+projection, b_x / b_p bytes per dispatched hidden element / routed
+probability.  R = S*K routed (token, slot) rows.
+
+Precision.  Arithmetic is float64.  Values are rounded only where the paper
+fixes a precision:
+  * router logits and routed probabilities are fp32 (b_p = 4 bytes, Eq. 1);
+  * every hidden-state payload that crosses the dispatch/combine boundary is
+    bf16 (b_x = 2 bytes, Eq. 1): the dispatched activations, the expert
+    outputs sent back for the combine, and in the backward pass the gradients
+    travelling the inverse routes (footnote on q = 6 in Section 4.1).
+Expert-internal values (u, h) and final outputs stay float64.
+
+Pins (each in tests/test_oracle_*.py):
+  round_bf16            library conversion on fp32-exact inputs, hand ties
+  router_logits         exact small-integer products, bias offsets
+  topk_select           brute-force full sort per row; tie / +-0 / -inf / NaN suites
+  routing_probs         closed forms (K=1, equal scores, K=2 logistic), sum = 1,
+                        K-only softmax agreement, hand-worked fixture
+  expert_permutation    brute-force sort of (expert, token) pairs; bijection and
+                        segment invariants; hand-worked fixture; Section 5.3 load
+  dispatch / combine    Eq. 1 byte count, adjoint identity, identity experts, K=1
+  expert_ffn            permutation-matrix experts (closed form), brute-force
+                        triple loop on tiny integer inputs, per-expert scaling
+  latent_down/up        permutation-matrix projections, brute-force loops
+  *_bwd                 float64 central finite differences of the forward;
+                        adjoint identities; dead experts give exactly zero dW
+  ep_volume_per_step    the paper's printed reductions (Section 4.1, 4.3)
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional, Sequence
+
+import numpy as np
+
+B_X = 2  # bytes per dispatched hidden element, bf16 (Eq. 1)
+B_P = 4  # bytes per routed probability, fp32 (Eq. 1)
+
+__all__ = [
+    "B_X", "B_P", "round_bf16", "router_logits", "topk_select", "routing_probs",
+    "route", "expert_permutation", "dispatch", "expert_ffn", "combine",
+    "latent_down", "latent_up", "layer_fwd", "combine_bwd", "expert_ffn_bwd",
+    "dispatch_bwd", "dispatch_payload_bytes", "combine_payload_bytes",
+    "ep_volume_per_step",
+]
+
+
+# ---------------------------------------------------------------------------
+# Rounding to the payload precision
+# ---------------------------------------------------------------------------
+
+def round_bf16(a) -> np.ndarray:
+    """Round to the nearest bfloat16 value (ties to even), returned as float64.
+
+    bf16 keeps 8 significant bits, so a finite value a = m * 2**e with
+    0.5 <= |m| < 1 lies on a grid of spacing 2**(e-8); below the smallest
+    normal (2**-126) the spacing stays at 2**-133.  Rounding is done directly
+    from float64 (no intermediate fp32 step, which could round twice).
+    """
+    a = np.asarray(a, dtype=np.float64)
+    out = a.copy()
+    fin = np.isfinite(a)
+    v = a[fin]
+    _, e = np.frexp(v)
+    e = np.maximum(e, -125)
+    ulp = np.ldexp(np.ones_like(v), e - 8)
+    r = np.rint(v / ulp) * ulp  # np.rint rounds halves to even
+    r = np.where(np.abs(r) >= 2.0 ** 128, np.copysign(np.inf, v), r)
+    out[fin] = r
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Router: logits, top-K selection, routed probabilities
+# ---------------------------------------------------------------------------
+
+def router_logits(x_r, Wr, bias=None) -> np.ndarray:
+    """logits[t, e] = sum_d x_r[t, d] * Wr[d, e] (+ bias[e]), as fp32.
+
+    The router scores every token against every expert (Section 5.2: MoE
+    layers route with a learned router; this workload uses fp32 router
+    logits).  Computed in float64 and rounded once to fp32.  An optional
+    per-expert bias is added to the logits before the softmax, so it changes
+    both which experts are picked and their weights.
+    """
+    z = np.asarray(x_r, np.float64) @ np.asarray(Wr, np.float64)
+    if bias is not None:
+        with np.errstate(invalid="ignore"):
+            z = z + np.asarray(bias, np.float64)[None, :]
+    return z.astype(np.float32)
+
+
+def topk_select(logits, K: int) -> np.ndarray:
+    """Indices of the K highest-scoring experts per token, best first.
+
+    Dropless top-K routing (Section 1): every token keeps exactly K distinct
+    experts.  Selection compares the fp32 scores under one total order:
+    higher score first, equal scores broken towards the lower expert index,
+    -0 equal to +0, NaN below every number including -inf.  The K picks are
+    made one after another, each taking the best expert not yet taken.
+    Returns int32 [S, K].
+    """
+    s = np.asarray(logits, dtype=np.float32)
+    S, E = s.shape
+    if not 1 <= K <= E:
+        raise ValueError("need 1 <= K <= E")
+    vals = s.astype(np.float64) + 0.0          # -0.0 + 0.0 == +0.0
+    nan = np.isnan(vals)
+    taken = np.zeros((S, E), dtype=bool)
+    idx = np.empty((S, K), dtype=np.int32)
+    rows = np.arange(S)
+    for k in range(K):
+        avail = ~taken
+        num = avail & ~nan
+        v = np.where(num, vals, -np.inf)
+        best = v.max(axis=1) if E else None
+        cand = num & (v == best[:, None])
+        only_nan = ~num.any(axis=1)
+        cand[only_nan] = (avail & nan)[only_nan]
+        choice = np.argmax(cand, axis=1)       # first True: the lowest index
+        idx[:, k] = choice
+        taken[rows, choice] = True
+    return idx
+
+
+def routing_probs(logits, idx) -> np.ndarray:
+    """Routed probabilities p[t, k] for the selected experts, as fp32 (b_p).
+
+    Softmax over all E experts, keep the K selected, renormalise them to sum
+    to one: p_k = q_{T_k} / sum_{j<K} q_{T_j} with q = softmax(s).  Each row
+    must hold no NaN and at least one finite score; -inf entries get q = 0.
+    """
+    s = np.asarray(logits, dtype=np.float32).astype(np.float64)
+    idx = np.asarray(idx)
+    if np.isnan(s).any():
+        raise ValueError("routing probabilities are undefined for NaN logits")
+    m = s.max(axis=1, keepdims=True)
+    if not np.isfinite(m).all():
+        raise ValueError("each token needs a finite maximum score")
+    ex = np.exp(s - m)
+    q = ex / ex.sum(axis=1, keepdims=True)
+    sel = np.take_along_axis(q, idx.astype(np.int64), axis=1)
+    p = sel / sel.sum(axis=1, keepdims=True)
+    return p.astype(np.float32)
+
+
+def route(logits, K: int):
+    """topk_select followed by routing_probs: (idx int32 [S,K], p fp32 [S,K])."""
+    idx = topk_select(logits, K)
+    return idx, routing_probs(logits, idx)
+
+
+# ---------------------------------------------------------------------------
+# Permutation into expert-contiguous order
+# ---------------------------------------------------------------------------
+
+def expert_permutation(idx, E: int):
+    """Counting sort of the S*K routed rows by expert.
+
+    Dropless, unpadded (Section 1): the expert-contiguous buffer has exactly
+    S*K rows.  counts[e] is the number of rows routed to e, offsets the
+    exclusive prefix sum (offsets[E] = S*K).  Rows are placed by walking
+    tokens in ascending order and, within a token, slots in ascending order,
+    each taking the next free position of its expert; so inside every expert
+    segment rows appear in ascending token order.
+      perm[pos]        = t*K + k  (which routed row sits at position pos)
+      inv_perm[t*K+k]  = pos
+    """
+    idx = np.asarray(idx)
+    S, K = idx.shape
+    if idx.size and (idx.min() < 0 or idx.max() >= E):
+        raise ValueError("expert index out of range")
+    for t in range(S):
+        if len(set(int(e) for e in idx[t])) != K:
+            raise ValueError("a token's K experts must be distinct")
+    counts = np.bincount(idx.ravel().astype(np.int64), minlength=E).astype(np.int64)
+    offsets = np.zeros(E + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    cursor = offsets[:-1].copy()
+    perm = np.empty(S * K, dtype=np.int64)
+    inv_perm = np.empty(S * K, dtype=np.int64)
+    for t in range(S):
+        for k in range(K):
+            e = int(idx[t, k])
+            pos = int(cursor[e])
+            cursor[e] += 1
+            perm[pos] = t * K + k
+            inv_perm[t * K + k] = pos
+    return counts, offsets, perm, inv_perm
+
+
+# ---------------------------------------------------------------------------
+# Dispatch, experts, combine
+# ---------------------------------------------------------------------------
+
+def dispatch(x, prob, inv_perm, K: int):
+    """The forward dispatch payload (Eq. 1: D*b_x + b_p bytes per routed row).
+
+    Row t*K+k of the token-major expansion goes to position inv_perm[t*K+k]:
+    x_disp[pos] = x[t] (bf16 hidden state, copied unchanged) and
+    p_disp[pos] = prob[t, k] (fp32 routed probability).
+    """
+    x = np.asarray(x, np.float64)
+    S, D = x.shape
+    inv_perm = np.asarray(inv_perm, np.int64)
+    x_disp = np.empty((S * K, D), dtype=np.float64)
+    x_disp[inv_perm] = np.repeat(x, K, axis=0)
+    p_disp = None
+    if prob is not None:
+        p_disp = np.empty(S * K, dtype=np.float32)
+        p_disp[inv_perm] = np.asarray(prob, np.float32).reshape(-1)
+    return x_disp, p_disp
+
+
+def _expert(W, e) -> np.ndarray:
+    return np.asarray(W[e], dtype=np.float64)
+
+
+def expert_ffn(x_disp, offsets, W1, W2, round_payload: bool = True):
+    """Ungated per-expert FFN over each expert's contiguous segment
+    (Section 5.2: grouped GEMM over expert segments; the activation is
+    squared-ReLU for this workload since the paper does not state one).
+
+    For expert e and rows r in [offsets[e], offsets[e+1]):
+        u[r] = x_disp[r] @ W1[e]          W1[e]: [D, F]
+        h[r] = max(u[r], 0)**2
+        y_disp[r] = h[r] @ W2[e]          W2[e]: [F, D]
+    y_disp is the combine payload and is rounded to bf16 (b_x) unless
+    round_payload is False.  W1/W2 may be any object indexable by expert.
+    Returns (u, h, y_disp) as float64.
+    """
+    x_disp = np.asarray(x_disp, np.float64)
+    offsets = np.asarray(offsets, np.int64)
+    R, D = x_disp.shape
+    E = len(offsets) - 1
+    F = None
+    u = h = y = None
+    for e in range(E):
+        a, b = int(offsets[e]), int(offsets[e + 1])
+        if a == b:
+            continue
+        w1 = _expert(W1, e)
+        w2 = _expert(W2, e)
+        if F is None:
+            F = w1.shape[1]
+            u = np.zeros((R, F))
+            h = np.zeros((R, F))
+            y = np.zeros((R, w2.shape[1]))
+        u[a:b] = x_disp[a:b] @ w1
+        h[a:b] = np.maximum(u[a:b], 0.0) ** 2
+        y[a:b] = h[a:b] @ w2
+    if F is None:  # no routed rows at all
+        F = _expert(W1, 0).shape[1] if E else 0
+        u = np.zeros((R, F))
+        h = np.zeros((R, F))
+        y = np.zeros((R, D))
+    if round_payload:
+        y = round_bf16(y)
+    return u, h, y
+
+
+def combine(y_disp, p_disp, inv_perm, S: int, K: int) -> np.ndarray:
+    """Probability-weighted combine back to token order:
+    y[t] = sum_{k<K} p_disp[pos] * y_disp[pos], pos = inv_perm[t*K+k],
+    summed in ascending k.  p_disp None means unit weights.  float64 result.
+    """
+    y_disp = np.asarray(y_disp, np.float64)
+    inv = np.asarray(inv_perm, np.int64).reshape(S, K)
+    y = np.zeros((S, y_disp.shape[1]))
+    for k in range(K):
+        pos = inv[:, k]
+        w = 1.0 if p_disp is None else np.asarray(p_disp, np.float64)[pos][:, None]
+        y = y + w * y_disp[pos]
+    return y
+
+
+def latent_down(x, Wdown, round_payload: bool = True) -> np.ndarray:
+    """LatentMoE-style projection to the dispatch dimension (Section 1, the
+    dispatch-dimension lever; Table 2 d_latent): x_lat = x @ Wdown.  x_lat is
+    what gets dispatched, so it is rounded to bf16 (b_x)."""
+    z = np.asarray(x, np.float64) @ np.asarray(Wdown, np.float64)
+    return round_bf16(z) if round_payload else z
+
+
+def latent_up(y_lat, Wup) -> np.ndarray:
+    """Projection of the combined latent output back to the model hidden:
+    y = y_lat @ Wup (float64)."""
+    return np.asarray(y_lat, np.float64) @ np.asarray(Wup, np.float64)
+
+
+def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
+              logits=None, round_payload: bool = True) -> dict:
+    """One routed MoE layer forward, in the paper's order (Section 4.1
+    footnote: hidden dispatch, probability dispatch, hidden combine):
+    [latent down] -> router logits -> top-K + probabilities -> permutation ->
+    dispatch -> experts -> combine -> [latent up].
+
+    If ``logits`` is given, routing uses those fp32 scores instead of the
+    ones computed here (so a caller can route both sides from identical
+    scores).  Returns every intermediate in a dict.
+    """
+    x = np.asarray(x, np.float64)
+    S = x.shape[0]
+    out = {}
+    x_r = x
+    if Wdown is not None:
+        x_r = latent_down(x, Wdown, round_payload)
+        out["x_lat"] = x_r
+    if logits is None:
+        logits = router_logits(x_r, Wr, bias)
+    out["logits"] = np.asarray(logits, np.float32)
+    E = out["logits"].shape[1]
+    idx, prob = route(out["logits"], K)
+    counts, offsets, perm, inv_perm = expert_permutation(idx, E)
+    x_disp, p_disp = dispatch(x_r, prob, inv_perm, K)
+    u, h, y_disp = expert_ffn(x_disp, offsets, W1, W2, round_payload)
+    y = combine(y_disp, p_disp, inv_perm, S, K)
+    out.update(topk_idx=idx, topk_prob=prob, counts=counts, offsets=offsets, perm=perm,
+               inv_perm=inv_perm, x_disp=x_disp, p_disp=p_disp, u=u, h=h, y_disp=y_disp)
+    if Wup is not None:
+        out["y_lat"] = y
+        y = latent_up(y, Wup)
+    out["y"] = y
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Backward through the combine, the experts and the dispatch
+# ---------------------------------------------------------------------------
+
+def combine_bwd(dy, y_disp, p_disp, inv_perm, K: int, round_payload: bool = True):
+    """Transpose of the weighted combine (the first inverse route of the
+    backward pass, Section 4.1 footnote):
+        dy_disp[pos] = p_disp[pos] * dy[t]         (bf16 payload)
+        dp[t, k]     = <dy[t], y_disp[pos]>        (gradient of the weight)
+    with pos = inv_perm[t*K+k].  Returns (dy_disp, dp) as float64.
+    """
+    dy = np.asarray(dy, np.float64)
+    y_disp = np.asarray(y_disp, np.float64)
+    S, D = dy.shape
+    inv = np.asarray(inv_perm, np.int64).reshape(S, K)
+    dy_disp = np.zeros((S * K, D))
+    dp = np.zeros((S, K))
+    for k in range(K):
+        pos = inv[:, k]
+        w = 1.0 if p_disp is None else np.asarray(p_disp, np.float64)[pos][:, None]
+        dy_disp[pos] = w * dy
+        dp[:, k] = np.sum(dy * y_disp[pos], axis=1)
+    if round_payload:
+        dy_disp = round_bf16(dy_disp)
+    return dy_disp, dp
+
+
+def expert_ffn_bwd(x_disp, u, h, dy_disp, offsets, W1, W2, round_payload: bool = True):
+    """Gradients of expert_ffn along the same expert segments.
+
+    For expert e, rows r in its segment (chain rule of u = x W1,
+    h = max(u,0)^2, y = h W2):
+        dh = dy_disp @ W2[e]^T
+        du = dh * 2*max(u, 0)
+        dx_disp = du @ W1[e]^T                (bf16 payload of the inverse dispatch)
+        dW2[e] = h^T @ dy_disp,  dW1[e] = x_disp^T @ du
+    Experts with no rows get dW = 0 exactly.  Returns (dx_disp, dW1, dW2, du).
+    """
+    x_disp = np.asarray(x_disp, np.float64)
+    u = np.asarray(u, np.float64)
+    h = np.asarray(h, np.float64)
+    dy_disp = np.asarray(dy_disp, np.float64)
+    offsets = np.asarray(offsets, np.int64)
+    R, D = x_disp.shape
+    E = len(offsets) - 1
+    w1_0 = _expert(W1, 0)
+    F = w1_0.shape[1]
+    dx_disp = np.zeros((R, D))
+    du = np.zeros((R, F))
+    dW1 = np.zeros((E, D, F))
+    dW2 = np.zeros((E, F, D))
+    for e in range(E):
+        a, b = int(offsets[e]), int(offsets[e + 1])
+        if a == b:
+            continue
+        w1 = _expert(W1, e)
+        w2 = _expert(W2, e)
+        dh = dy_disp[a:b] @ w2.T
+        du[a:b] = dh * (2.0 * np.maximum(u[a:b], 0.0))
+        dx_disp[a:b] = du[a:b] @ w1.T
+        dW2[e] = h[a:b].T @ dy_disp[a:b]
+        dW1[e] = x_disp[a:b].T @ du[a:b]
+    if round_payload:
+        dx_disp = round_bf16(dx_disp)
+    return dx_disp, dW1, dW2, du
+
+
+def dispatch_bwd(dx_disp, inv_perm, S: int, K: int) -> np.ndarray:
+    """Transpose of the dispatch copy (the last inverse route of the backward
+    pass): dx[t] = sum_{k<K} dx_disp[inv_perm[t*K+k]], ascending k."""
+    dx_disp = np.asarray(dx_disp, np.float64)
+    inv = np.asarray(inv_perm, np.int64).reshape(S, K)
+    dx = np.zeros((S, dx_disp.shape[1]))
+    for k in range(K):
+        dx = dx + dx_disp[inv[:, k]]
+    return dx
+
+
+# ---------------------------------------------------------------------------
+# Eq. 1: expert-parallel communication volume
+# ---------------------------------------------------------------------------
+
+def dispatch_payload_bytes(S: int, K: int, D: int, b_x: int = B_X, b_p: int = B_P) -> int:
+    """Forward dispatch payload: every routed row carries its hidden state
+    and its routed probability, S*K*(D*b_x + b_p) bytes (Eq. 1)."""
+    return S * K * (D * b_x + b_p)
+
+
+def combine_payload_bytes(S: int, K: int, D: int, b_x: int = B_X) -> int:
+    """Forward combine payload: one hidden state per routed row, S*K*D*b_x."""
+    return S * K * D * b_x
+
+
+def ep_volume_per_step(L_E: int, S: int, GBS: int, K: int, D: int,
+                       b_x: int = B_X, b_p: int = B_P) -> int:
+    """Expert-parallel volume over one training step (Eq. 1): forward
+    dispatch + combine and their backward inverses, summed over L_E MoE
+    layers and GBS sequences of S tokens: L_E*S*GBS*K*(4*D*b_x + 2*b_p)."""
+    per_layer_tokens = S * GBS
+    fwd = dispatch_payload_bytes(per_layer_tokens, K, D, b_x, b_p) + \
+        combine_payload_bytes(per_layer_tokens, K, D, b_x)
+    return L_E * 2 * fwd
