@@ -1,0 +1,246 @@
+/*
+ * moe.h -- C ABI of one routed Mixture-of-Experts layer on one MI355X (gfx950).
+ *
+ * The layer is the per-token data path of a routed MoE layer as the paper
+ * trains it (Section 5.2: token dispatch, grouped-GEMM experts, fused
+ * permutation): router logits -> top-K routing -> dispatch of hidden states
+ * and routed probabilities into an expert-contiguous buffer -> per-expert
+ * FFN -> probability-weighted combine back to token order, plus the
+ * backward pass through the experts and the permutation.  On one GPU the
+ * expert-parallel all-to-alls of the paper become the local dispatch and
+ * combine copies; their payloads are exactly what Eq. 1 counts.
+ *
+ * Notation (Section 1, Eq. 1; Table 2):
+ *   S  tokens in this call (sequence length x micro-batch, flattened)
+ *   D  dispatch dimension (hidden width of what is dispatched)
+ *   E  routed experts;  K  experts per token (top-K);  R = S*K routed rows
+ *   F  per-expert FFN width (f_expert);  H  model hidden when a latent
+ *      projection precedes dispatch (d_latent = D)
+ *   b_x = 2 (bf16 hidden elements),  b_p = 4 (fp32 routed probabilities)
+ *
+ * Conventions for every entry point:
+ *   - Tensor pointers are DEVICE pointers to row-major, contiguous arrays.
+ *     bf16 arrays and the probability arrays must be 16-byte aligned;
+ *     int32 arrays 4-byte aligned.
+ *   - The caller allocates and frees every buffer, including the workspace
+ *     sized by the matching *_workspace_bytes query.  The library never
+ *     allocates, frees or synchronises; it keeps no state between calls.
+ *   - Work is enqueued on `stream` (NULL = the null stream) and the call
+ *     returns at once.  Arguments are validated synchronously before any
+ *     launch; on a validation error nothing is enqueued.
+ *   - Outputs must not alias inputs.  Results are deterministic: the same
+ *     inputs give bit-identical outputs on every call.
+ *   - S == 0 (or R == 0) is valid and enqueues nothing.
+ *   - Limits: 1 <= E <= 1024, 1 <= K <= min(E, 32), D and F multiples of 8
+ *     in [8, 65536], S*K < 2^31.
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_ABI_VERSION 1
+
+typedef uint16_t moe_bf16; /* bit pattern of a bfloat16 value (b_x = 2 bytes) */
+
+typedef enum {
+    MOE_OK = 0,
+    MOE_ERR_NULL = -1,        /* a required pointer is NULL */
+    MOE_ERR_SHAPE = -2,       /* a size is out of range or inconsistent */
+    MOE_ERR_ALIGN = -3,       /* a pointer violates its alignment */
+    MOE_ERR_WORKSPACE = -4,   /* workspace missing or smaller than required */
+    MOE_ERR_HIP = -5,         /* a HIP launch failed (see hipGetLastError) */
+    MOE_ERR_UNSUPPORTED = -6  /* valid request this build does not implement */
+} moe_status;
+
+/* ABI version of the loaded library (MOE_ABI_VERSION at build time). */
+int moe_abi_version(void);
+
+/* Static, human-readable text for a moe_status value. Never NULL. */
+const char* moe_status_string(int status);
+
+/* Forward dispatch payload in bytes, S*K*(D*b_x + b_p): every routed row
+ * carries its bf16 hidden state and its fp32 routed probability (Eq. 1).
+ * Returns 0 for negative sizes. Host-only, touches no device. */
+uint64_t moe_payload_bytes(int64_t S, int32_t K, int32_t D);
+
+/* ---------------------------------------------------------------------- */
+/* Router logits (the router scores every token against every expert,     */
+/* Section 5.2).                                                          */
+/* ---------------------------------------------------------------------- */
+/* logits[t,e] = sum_d x_r[t,d] * Wr[d,e] + bias[e], accumulated in fp32.
+ *   x_r    [S, D]  bf16   router input (the dispatch-width activations)
+ *   Wr     [D, E]  fp32   router weight
+ *   bias   [E]     fp32   per-expert logit offset, or NULL for none
+ *   logits [S, E]  fp32   output */
+int moe_router_logits(const moe_bf16* x_r, const float* Wr, const float* bias,
+                      int64_t S, int32_t D, int32_t E, float* logits, hipStream_t stream);
+
+/* ---------------------------------------------------------------------- */
+/* Top-K routing and the expert permutation (dropless, unpadded top-K     */
+/* routing, Section 1; fused permutation, Section 5.2).                   */
+/* ---------------------------------------------------------------------- */
+/* Workspace bytes moe_route_topk needs for these sizes. */
+size_t moe_route_workspace_bytes(int64_t S, int32_t E, int32_t K);
+
+/* Per token t, over the fp32 scores s = logits[t, :]:
+ *   topk_idx[t, 0..K-1]  the K best experts, best first, under the order
+ *                        (score descending, expert index ascending); -0 == +0
+ *                        and NaN ranks below -inf;
+ *   topk_prob[t, k]      softmax over all E, restricted to the K picked and
+ *                        renormalised to sum to 1 (fp32).  Each token needs a
+ *                        finite best score; otherwise its probabilities are
+ *                        unspecified (indices stay well defined).
+ * Over all tokens:
+ *   counts[e]            routed rows per expert, sum = S*K
+ *   offsets[e]           exclusive prefix sum of counts, offsets[E] = S*K
+ *   perm[pos]            = t*K+k of the row stored at position pos of the
+ *                        expert-contiguous order (experts ascending, tokens
+ *                        ascending inside an expert)
+ *   inv_perm[t*K+k]      = pos  (perm and inv_perm are inverse bijections)
+ * Shapes: logits [S,E] fp32; topk_idx, perm, inv_perm int32; topk_prob fp32;
+ * counts [E], offsets [E+1] int32.  ws: >= moe_route_workspace_bytes, 16-byte
+ * aligned, contents need no initialisation. */
+int moe_route_topk(const float* logits, int64_t S, int32_t E, int32_t K,
+                   int32_t* topk_idx, float* topk_prob, int32_t* counts, int32_t* offsets,
+                   int32_t* perm, int32_t* inv_perm, void* ws, size_t ws_bytes,
+                   hipStream_t stream);
+
+/* ---------------------------------------------------------------------- */
+/* Dispatch: the forward dispatch payload of Eq. 1 (D*b_x + b_p per row).  */
+/* ---------------------------------------------------------------------- */
+/* x_disp[inv_perm[t*K+k], :] = x[t, :]   (bf16 copy, bit-exact)
+ * p_disp[inv_perm[t*K+k]]    = topk_prob[t, k]   (fp32 copy)
+ * topk_prob and p_disp may both be NULL to move hidden states only.
+ *   x [S, D] bf16;  inv_perm [S*K] int32;  x_disp [S*K, D] bf16;  p_disp [S*K] fp32 */
+int moe_dispatch(const moe_bf16* x, const float* topk_prob, const int32_t* inv_perm,
+                 int64_t S, int32_t D, int32_t K, moe_bf16* x_disp, float* p_disp,
+                 hipStream_t stream);
+
+/* ---------------------------------------------------------------------- */
+/* Grouped expert FFN (grouped GEMM over expert segments, Section 5.2).    */
+/* ---------------------------------------------------------------------- */
+/* Workspace bytes moe_grouped_ffn needs. */
+size_t moe_grouped_ffn_workspace_bytes(int32_t E, int64_t R, int32_t D, int32_t F);
+
+/* For every expert e and row r in [offsets[e], offsets[e+1]):
+ *   u[r]      = x_disp[r, :] @ W1[e]          (fp32 accumulation)
+ *   h[r]      = bf16(max(u[r], 0)^2)          squared-ReLU, ungated
+ *   y_disp[r] = bf16(h[r] @ W2[e])            (fp32 accumulation)
+ *   x_disp [R, D] bf16;  offsets [E+1] int32 on the device (as produced by
+ *   moe_route_topk, offsets[E] == R);  W1 [E, D, F] bf16;  W2 [E, F, D] bf16;
+ *   h [R, F] bf16 (output, also the down-projection input);
+ *   u_save [R, F] bf16 pre-activation kept for the backward pass, or NULL;
+ *   y_disp [R, D] bf16 output (unweighted expert outputs). */
+int moe_grouped_ffn(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, int64_t R,
+                    int32_t D, int32_t F, const moe_bf16* W1, const moe_bf16* W2,
+                    moe_bf16* h, moe_bf16* u_save, moe_bf16* y_disp,
+                    void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------- */
+/* Combine: probability-weighted sum back to token order (the hidden       */
+/* combine of Section 4.1's footnote; D*b_x per routed row, Eq. 1).        */
+/* ---------------------------------------------------------------------- */
+/* y[t, :] = bf16( sum_{k<K} p_disp[pos] * y_disp[pos, :] ),  pos = inv_perm[t*K+k],
+ * accumulated in fp32 in ascending k, no atomics.  p_disp NULL = unit weights.
+ *   y_disp [S*K, D] bf16;  p_disp [S*K] fp32 or NULL;  y [S, D] bf16 */
+int moe_combine(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_perm,
+                int64_t S, int32_t D, int32_t K, moe_bf16* y, hipStream_t stream);
+
+/* ---------------------------------------------------------------------- */
+/* Dense projection for a LatentMoE-style dispatch dimension (Section 1,   */
+/* dispatch-dimension lever; Table 2 d_latent).                            */
+/* ---------------------------------------------------------------------- */
+/* C = bf16(A @ W) with fp32 accumulation.
+ *   A [M, Kd] bf16;  W [Kd, N] bf16;  C [M, N] bf16.  Kd, N multiples of 8. */
+int moe_latent_proj(const moe_bf16* A, const moe_bf16* W, int64_t M, int32_t Kd, int32_t N,
+                    moe_bf16* C, hipStream_t stream);
+
+/* ---------------------------------------------------------------------- */
+/* Whole layer forward on one stream, no host synchronisation.             */
+/* ---------------------------------------------------------------------- */
+typedef struct {
+    uint32_t struct_size;      /* sizeof(moe_layer_fwd_args) */
+    int64_t S;
+    int32_t H;                 /* 0: no latent projection (x is [S, D]) */
+    int32_t D, E, K, F;
+    const moe_bf16* x;         /* [S, H] if H > 0 else [S, D] */
+    const float* Wr;           /* [D, E] fp32 router weight */
+    const float* router_bias;  /* [E] fp32 or NULL */
+    const moe_bf16* Wdown;     /* [H, D] when H > 0, else NULL */
+    const moe_bf16* W1;        /* [E, D, F] */
+    const moe_bf16* W2;        /* [E, F, D] */
+    const moe_bf16* Wup;       /* [D, H] when H > 0, else NULL */
+    moe_bf16* y;               /* [S, H] if H > 0 else [S, D] */
+    /* Optional exported intermediates: NULL means "keep in workspace". */
+    moe_bf16* x_lat;           /* [S, D]  (H > 0 only) */
+    float* logits;             /* [S, E] */
+    int32_t* topk_idx;         /* [S, K] */
+    float* topk_prob;          /* [S, K] */
+    int32_t* counts;           /* [E] */
+    int32_t* offsets;          /* [E+1] */
+    int32_t* perm;             /* [S*K] */
+    int32_t* inv_perm;         /* [S*K] */
+    moe_bf16* x_disp;          /* [S*K, D] */
+    float* p_disp;             /* [S*K] */
+    moe_bf16* h;               /* [S*K, F] */
+    moe_bf16* u_save;          /* [S*K, F] pre-activation; NULL = not saved */
+    moe_bf16* y_disp;          /* [S*K, D] */
+    moe_bf16* y_lat;           /* [S, D]  (H > 0 only) */
+    void* ws;                  /* workspace, >= moe_layer_fwd_workspace_bytes */
+    size_t ws_bytes;
+} moe_layer_fwd_args;
+
+/* Workspace bytes moe_layer_fwd needs for these arguments (intermediates the
+ * caller does not export are carved from it).  0 if the sizes are invalid. */
+size_t moe_layer_fwd_workspace_bytes(const moe_layer_fwd_args* a);
+
+/* [x_lat = bf16(x @ Wdown)] -> logits -> route -> dispatch -> experts ->
+ * combine -> [y = bf16(y_lat @ Wup)], all enqueued on `stream`. */
+int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream);
+
+/* ---------------------------------------------------------------------- */
+/* Backward through combine, experts and dispatch (the inverse routes of   */
+/* the backward pass, Section 4.1 footnote; Eq. 1's factor of 2).          */
+/* ---------------------------------------------------------------------- */
+/* dy_disp[pos] = bf16(p_disp[pos] * dy[t]),  dp[t,k] = <dy[t], y_disp[pos]> (fp32),
+ * pos = inv_perm[t*K+k].  p_disp NULL = unit weights; dp may be NULL.
+ *   dy [S, D] bf16;  y_disp [S*K, D] bf16;  dy_disp [S*K, D] bf16;  dp [S, K] fp32 */
+int moe_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const float* p_disp,
+                    const int32_t* inv_perm, int64_t S, int32_t D, int32_t K,
+                    moe_bf16* dy_disp, float* dp, hipStream_t stream);
+
+/* Workspace bytes moe_grouped_ffn_bwd needs (includes the [R, F] bf16 du). */
+size_t moe_grouped_ffn_bwd_workspace_bytes(int32_t E, int64_t R, int32_t D, int32_t F);
+
+/* Per expert e over its rows (chain rule of moe_grouped_ffn):
+ *   du      = bf16( (dy_disp @ W2[e]^T) * 2*max(u_save, 0) )
+ *   dx_disp = bf16( du @ W1[e]^T )
+ *   dW2[e]  = h^T @ dy_disp      (fp32)
+ *   dW1[e]  = x_disp^T @ du      (fp32)
+ * Experts with no rows get dW1[e] = dW2[e] = 0.
+ *   x_disp, dy_disp, dx_disp [R, D] bf16;  u_save, h [R, F] bf16;
+ *   dW1 [E, D, F] fp32;  dW2 [E, F, D] fp32 (fully overwritten). */
+int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const moe_bf16* h,
+                        const moe_bf16* dy_disp, const int32_t* offsets, int32_t E, int64_t R,
+                        int32_t D, int32_t F, const moe_bf16* W1, const moe_bf16* W2,
+                        moe_bf16* dx_disp, float* dW1, float* dW2,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* dx[t] = bf16( sum_{k<K} dx_disp[inv_perm[t*K+k]] ), ascending k (the
+ * transpose of moe_dispatch: an unweighted combine).
+ *   dx_disp [S*K, D] bf16;  dx [S, D] bf16 */
+int moe_dispatch_bwd(const moe_bf16* dx_disp, const int32_t* inv_perm, int64_t S, int32_t D,
+                     int32_t K, moe_bf16* dx, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_H */

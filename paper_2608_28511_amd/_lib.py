@@ -1,0 +1,237 @@
+"""ctypes binding of libmoe.so (the C ABI in include/moe.h).
+
+Argument marshalling only: every function here has the name of the C entry
+point it wraps, takes torch tensors (or None where the C argument may be
+NULL), checks that each tensor is a contiguous device tensor of the dtype
+the C side expects (so a host pointer can never reach a kernel), and passes
+raw pointers plus the current HIP stream.  A negative status raises
+``MoeError``.  All arithmetic happens in the HIP kernels; if the library is
+missing this module raises instead of falling back to anything.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from pathlib import Path
+from typing import Optional
+
+import torch
+
+LIB_PATH = Path(__file__).resolve().parent / "libmoe.so"
+
+_lib: Optional[C.CDLL] = None
+
+vp = C.c_void_p
+i32 = C.c_int32
+i64 = C.c_int64
+u32 = C.c_uint32
+sz = C.c_size_t
+
+
+class MoeError(RuntimeError):
+    def __init__(self, code: int, text: str, where: str):
+        super().__init__(f"{where}: {text} (status {code})")
+        self.code = code
+
+
+class LayerFwdArgs(C.Structure):
+    """Mirror of moe_layer_fwd_args."""
+    _fields_ = [
+        ("struct_size", u32), ("S", i64), ("H", i32), ("D", i32), ("E", i32), ("K", i32),
+        ("F", i32),
+        ("x", vp), ("Wr", vp), ("router_bias", vp), ("Wdown", vp), ("W1", vp), ("W2", vp),
+        ("Wup", vp), ("y", vp),
+        ("x_lat", vp), ("logits", vp), ("topk_idx", vp), ("topk_prob", vp), ("counts", vp),
+        ("offsets", vp), ("perm", vp), ("inv_perm", vp), ("x_disp", vp), ("p_disp", vp),
+        ("h", vp), ("u_save", vp), ("y_disp", vp), ("y_lat", vp),
+        ("ws", vp), ("ws_bytes", sz),
+    ]
+
+
+_PROTOS = {
+    "moe_abi_version": (C.c_int, []),
+    "moe_status_string": (C.c_char_p, [C.c_int]),
+    "moe_payload_bytes": (C.c_uint64, [i64, i32, i32]),
+    "moe_router_logits": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp]),
+    "moe_route_workspace_bytes": (sz, [i64, i32, i32]),
+    "moe_route_topk": (C.c_int, [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+    "moe_dispatch": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp, vp]),
+    "moe_grouped_ffn_workspace_bytes": (sz, [i32, i64, i32, i32]),
+    "moe_grouped_ffn": (C.c_int, [vp, vp, i32, i64, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
+    "moe_combine": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp]),
+    "moe_latent_proj": (C.c_int, [vp, vp, i64, i32, i32, vp, vp]),
+    "moe_layer_fwd_workspace_bytes": (sz, [C.POINTER(LayerFwdArgs)]),
+    "moe_layer_fwd": (C.c_int, [C.POINTER(LayerFwdArgs), vp]),
+    "moe_combine_bwd": (C.c_int, [vp, vp, vp, vp, i64, i32, i32, vp, vp, vp]),
+    "moe_grouped_ffn_bwd_workspace_bytes": (sz, [i32, i64, i32, i32]),
+    "moe_grouped_ffn_bwd": (C.c_int, [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp, vp, vp, vp, vp,
+                                      vp, sz, vp]),
+    "moe_dispatch_bwd": (C.c_int, [vp, vp, i64, i32, i32, vp, vp]),
+}
+
+EXPORTED = tuple(_PROTOS)
+
+
+def load(build_if_missing: bool = False) -> C.CDLL:
+    """Load libmoe.so from the package directory (building it first only if
+    asked and absent).  Raises if it cannot be loaded."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not LIB_PATH.exists():
+        if not build_if_missing:
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        from . import build as _build
+        _build.build()
+    lib = C.CDLL(str(LIB_PATH))
+    for name, (res, args) in _PROTOS.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str) -> None:
+    if status != 0:
+        raise MoeError(status, load().moe_status_string(status).decode(), where)
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor], dtype=None, name: str = "tensor"):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.numel() and t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor, got {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    return C.c_void_p(t.data_ptr()) if t.numel() else None
+
+
+BF16, F32, I32 = torch.bfloat16, torch.float32, torch.int32
+
+
+def moe_abi_version() -> int:
+    return load().moe_abi_version()
+
+
+def moe_status_string(status: int) -> str:
+    return load().moe_status_string(status).decode()
+
+
+def moe_payload_bytes(S: int, K: int, D: int) -> int:
+    return load().moe_payload_bytes(S, K, D)
+
+
+def moe_router_logits(x_r, Wr, bias, S, D, E, logits):
+    _check(load().moe_router_logits(_ptr(x_r, BF16, "x_r"), _ptr(Wr, F32, "Wr"),
+                                    _ptr(bias, F32, "bias"), S, D, E,
+                                    _ptr(logits, F32, "logits"), _stream()), "moe_router_logits")
+
+
+def moe_route_workspace_bytes(S, E, K) -> int:
+    return load().moe_route_workspace_bytes(S, E, K)
+
+
+def moe_route_topk(logits, S, E, K, topk_idx, topk_prob, counts, offsets, perm, inv_perm, ws):
+    _check(load().moe_route_topk(
+        _ptr(logits, F32, "logits"), S, E, K, _ptr(topk_idx, I32, "topk_idx"),
+        _ptr(topk_prob, F32, "topk_prob"), _ptr(counts, I32, "counts"),
+        _ptr(offsets, I32, "offsets"), _ptr(perm, I32, "perm"), _ptr(inv_perm, I32, "inv_perm"),
+        _ptr(ws, None, "ws"), 0 if ws is None else ws.numel() * ws.element_size(), _stream()),
+        "moe_route_topk")
+
+
+def moe_dispatch(x, topk_prob, inv_perm, S, D, K, x_disp, p_disp):
+    _check(load().moe_dispatch(_ptr(x, BF16, "x"), _ptr(topk_prob, F32, "topk_prob"),
+                               _ptr(inv_perm, I32, "inv_perm"), S, D, K,
+                               _ptr(x_disp, BF16, "x_disp"), _ptr(p_disp, F32, "p_disp"),
+                               _stream()), "moe_dispatch")
+
+
+def moe_grouped_ffn_workspace_bytes(E, R, D, F) -> int:
+    return load().moe_grouped_ffn_workspace_bytes(E, R, D, F)
+
+
+def moe_grouped_ffn(x_disp, offsets, E, R, D, F, W1, W2, h, u_save, y_disp, ws):
+    _check(load().moe_grouped_ffn(
+        _ptr(x_disp, BF16, "x_disp"), _ptr(offsets, I32, "offsets"), E, R, D, F,
+        _ptr(W1, BF16, "W1"), _ptr(W2, BF16, "W2"), _ptr(h, BF16, "h"),
+        _ptr(u_save, BF16, "u_save"), _ptr(y_disp, BF16, "y_disp"), _ptr(ws, None, "ws"),
+        0 if ws is None else ws.numel() * ws.element_size(), _stream()), "moe_grouped_ffn")
+
+
+def moe_combine(y_disp, p_disp, inv_perm, S, D, K, y):
+    _check(load().moe_combine(_ptr(y_disp, BF16, "y_disp"), _ptr(p_disp, F32, "p_disp"),
+                              _ptr(inv_perm, I32, "inv_perm"), S, D, K, _ptr(y, BF16, "y"),
+                              _stream()), "moe_combine")
+
+
+def moe_latent_proj(A, W, M, Kd, N, Cout):
+    _check(load().moe_latent_proj(_ptr(A, BF16, "A"), _ptr(W, BF16, "W"), M, Kd, N,
+                                  _ptr(Cout, BF16, "C"), _stream()), "moe_latent_proj")
+
+
+_LAYER_TENSORS = {
+    "x": BF16, "Wr": F32, "router_bias": F32, "Wdown": BF16, "W1": BF16, "W2": BF16, "Wup": BF16,
+    "y": BF16, "x_lat": BF16, "logits": F32, "topk_idx": I32, "topk_prob": F32, "counts": I32,
+    "offsets": I32, "perm": I32, "inv_perm": I32, "x_disp": BF16, "p_disp": F32, "h": BF16,
+    "u_save": BF16, "y_disp": BF16, "y_lat": BF16,
+}
+
+
+def layer_fwd_args(S, H, D, E, K, F, ws=None, **tensors) -> LayerFwdArgs:
+    """Fill a moe_layer_fwd_args from sizes and named tensors (None = NULL)."""
+    a = LayerFwdArgs()
+    a.struct_size = C.sizeof(LayerFwdArgs)
+    a.S, a.H, a.D, a.E, a.K, a.F = S, H, D, E, K, F
+    for name, t in tensors.items():
+        if name not in _LAYER_TENSORS:
+            raise KeyError(name)
+        p = _ptr(t, _LAYER_TENSORS[name], name)
+        setattr(a, name, p.value if p is not None else None)
+    if ws is not None:
+        p = _ptr(ws, None, "ws")
+        a.ws = p.value if p is not None else None
+        a.ws_bytes = ws.numel() * ws.element_size()
+    return a
+
+
+def moe_layer_fwd_workspace_bytes(args: LayerFwdArgs) -> int:
+    return load().moe_layer_fwd_workspace_bytes(C.byref(args))
+
+
+def moe_layer_fwd(args: LayerFwdArgs):
+    _check(load().moe_layer_fwd(C.byref(args), _stream()), "moe_layer_fwd")
+
+
+def moe_combine_bwd(dy, y_disp, p_disp, inv_perm, S, D, K, dy_disp, dp):
+    _check(load().moe_combine_bwd(_ptr(dy, BF16, "dy"), _ptr(y_disp, BF16, "y_disp"),
+                                  _ptr(p_disp, F32, "p_disp"), _ptr(inv_perm, I32, "inv_perm"),
+                                  S, D, K, _ptr(dy_disp, BF16, "dy_disp"), _ptr(dp, F32, "dp"),
+                                  _stream()), "moe_combine_bwd")
+
+
+def moe_grouped_ffn_bwd_workspace_bytes(E, R, D, F) -> int:
+    return load().moe_grouped_ffn_bwd_workspace_bytes(E, R, D, F)
+
+
+def moe_grouped_ffn_bwd(x_disp, u_save, h, dy_disp, offsets, E, R, D, F, W1, W2, dx_disp, dW1,
+                        dW2, ws):
+    _check(load().moe_grouped_ffn_bwd(
+        _ptr(x_disp, BF16, "x_disp"), _ptr(u_save, BF16, "u_save"), _ptr(h, BF16, "h"),
+        _ptr(dy_disp, BF16, "dy_disp"), _ptr(offsets, I32, "offsets"), E, R, D, F,
+        _ptr(W1, BF16, "W1"), _ptr(W2, BF16, "W2"), _ptr(dx_disp, BF16, "dx_disp"),
+        _ptr(dW1, F32, "dW1"), _ptr(dW2, F32, "dW2"), _ptr(ws, None, "ws"),
+        0 if ws is None else ws.numel() * ws.element_size(), _stream()), "moe_grouped_ffn_bwd")
+
+
+def moe_dispatch_bwd(dx_disp, inv_perm, S, D, K, dx):
+    _check(load().moe_dispatch_bwd(_ptr(dx_disp, BF16, "dx_disp"), _ptr(inv_perm, I32, "inv_perm"),
+                                   S, D, K, _ptr(dx, BF16, "dx"), _stream()), "moe_dispatch_bwd")

@@ -1,0 +1,373 @@
+// Host side of the C ABI in include/moe.h: synchronous argument validation,
+// workspace sizing and carving, and stream-ordered launch of the kernels.
+// Nothing here allocates, frees or synchronises device memory.
+#include <stdint.h>
+#include <string.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "moe.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int kMaxE = 1024;
+constexpr int kMaxK = 32;
+constexpr int kMaxDim = 65536;
+constexpr int64_t kMaxRows = (int64_t)1 << 31;
+
+bool misaligned(const void* p, size_t a) { return ((uintptr_t)p) % a != 0; }
+
+// A pointer that must address `bytes` bytes: NULL is allowed only for an empty range.
+int need(const void* p, uint64_t bytes, size_t align) {
+    if (bytes == 0) return MOE_OK;
+    if (p == nullptr) return MOE_ERR_NULL;
+    if (misaligned(p, align)) return MOE_ERR_ALIGN;
+    return MOE_OK;
+}
+
+int opt(const void* p, size_t align) {
+    if (p != nullptr && misaligned(p, align)) return MOE_ERR_ALIGN;
+    return MOE_OK;
+}
+
+bool dim_ok(int32_t d) { return d >= 8 && d <= kMaxDim && d % 8 == 0; }
+
+int check_route_shape(int64_t S, int32_t E, int32_t K) {
+    if (S < 0) return MOE_ERR_SHAPE;
+    if (E < 1 || E > kMaxE) return MOE_ERR_SHAPE;
+    if (K < 1 || K > E || K > kMaxK) return MOE_ERR_SHAPE;
+    if (S * (int64_t)K >= kMaxRows) return MOE_ERR_SHAPE;
+    return MOE_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_ERR_HIP; }
+
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+#define MOE_TRY(expr)                 \
+    do {                              \
+        const int _s = (expr);        \
+        if (_s != MOE_OK) return _s;  \
+    } while (0)
+
+#define MOE_HIP(expr)                           \
+    do {                                        \
+        const hipError_t _e = (expr);           \
+        if (_e != hipSuccess) return MOE_ERR_HIP; \
+    } while (0)
+
+}  // namespace
+
+extern "C" {
+
+int moe_abi_version(void) { return MOE_ABI_VERSION; }
+
+const char* moe_status_string(int status) {
+    switch (status) {
+        case MOE_OK: return "ok";
+        case MOE_ERR_NULL: return "a required pointer is NULL";
+        case MOE_ERR_SHAPE: return "a size is out of range or inconsistent";
+        case MOE_ERR_ALIGN: return "a pointer violates its alignment";
+        case MOE_ERR_WORKSPACE: return "workspace missing or too small";
+        case MOE_ERR_HIP: return "a HIP launch failed";
+        case MOE_ERR_UNSUPPORTED: return "request not supported by this build";
+        default: return "unknown status";
+    }
+}
+
+uint64_t moe_payload_bytes(int64_t S, int32_t K, int32_t D) {
+    if (S < 0 || K < 0 || D < 0) return 0;
+    return (uint64_t)S * (uint64_t)K * ((uint64_t)D * 2u + 4u);
+}
+
+int moe_router_logits(const moe_bf16* x_r, const float* Wr, const float* bias, int64_t S, int32_t D,
+                      int32_t E, float* logits, hipStream_t stream) {
+    if (S < 0 || !dim_ok(D) || E < 1 || E > kMaxE) return MOE_ERR_SHAPE;
+    MOE_TRY(need(x_r, (uint64_t)S * D * 2, 16));
+    MOE_TRY(need(Wr, (uint64_t)D * E * 4, 4));
+    MOE_TRY(opt(bias, 4));
+    MOE_TRY(need(logits, (uint64_t)S * E * 4, 4));
+    return hip_status(moe::launch_router_logits(x_r, Wr, bias, S, D, E, logits, stream));
+}
+
+size_t moe_route_workspace_bytes(int64_t S, int32_t E, int32_t K) {
+    if (check_route_shape(S, E, K) != MOE_OK) return 0;
+    return moe::route_ws_bytes(S, E);
+}
+
+int moe_route_topk(const float* logits, int64_t S, int32_t E, int32_t K, int32_t* topk_idx,
+                   float* topk_prob, int32_t* counts, int32_t* offsets, int32_t* perm,
+                   int32_t* inv_perm, void* ws, size_t ws_bytes, hipStream_t stream) {
+    MOE_TRY(check_route_shape(S, E, K));
+    const uint64_t R = (uint64_t)S * K;
+    MOE_TRY(need(logits, (uint64_t)S * E * 4, 4));
+    MOE_TRY(need(topk_idx, R * 4, 4));
+    MOE_TRY(need(topk_prob, R * 4, 4));
+    MOE_TRY(need(counts, (uint64_t)E * 4, 4));
+    MOE_TRY(need(offsets, (uint64_t)(E + 1) * 4, 4));
+    MOE_TRY(need(perm, R * 4, 4));
+    MOE_TRY(need(inv_perm, R * 4, 4));
+    const size_t wsn = moe::route_ws_bytes(S, E);
+    if (wsn > 0 && (ws == nullptr || ws_bytes < wsn)) return MOE_ERR_WORKSPACE;
+    MOE_TRY(opt(ws, 16));
+    return hip_status(moe::launch_route(logits, S, E, K, topk_idx, topk_prob, counts, offsets, perm,
+                                        inv_perm, ws, stream));
+}
+
+int moe_dispatch(const moe_bf16* x, const float* topk_prob, const int32_t* inv_perm, int64_t S,
+                 int32_t D, int32_t K, moe_bf16* x_disp, float* p_disp, hipStream_t stream) {
+    if (S < 0 || !dim_ok(D) || K < 1 || K > kMaxK || S * (int64_t)K >= kMaxRows) return MOE_ERR_SHAPE;
+    if ((topk_prob == nullptr) != (p_disp == nullptr)) return MOE_ERR_NULL;
+    const uint64_t R = (uint64_t)S * K;
+    MOE_TRY(need(x, (uint64_t)S * D * 2, 16));
+    MOE_TRY(need(inv_perm, R * 4, 4));
+    MOE_TRY(need(x_disp, R * D * 2, 16));
+    MOE_TRY(opt(topk_prob, 4));
+    MOE_TRY(opt(p_disp, 4));
+    return hip_status(moe::launch_dispatch(x, topk_prob, inv_perm, S, D, K, x_disp, p_disp, stream));
+}
+
+int moe_combine(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_perm, int64_t S,
+                int32_t D, int32_t K, moe_bf16* y, hipStream_t stream) {
+    if (S < 0 || !dim_ok(D) || K < 1 || K > kMaxK || S * (int64_t)K >= kMaxRows) return MOE_ERR_SHAPE;
+    const uint64_t R = (uint64_t)S * K;
+    MOE_TRY(need(y_disp, R * D * 2, 16));
+    MOE_TRY(opt(p_disp, 4));
+    MOE_TRY(need(inv_perm, R * 4, 4));
+    MOE_TRY(need(y, (uint64_t)S * D * 2, 16));
+    return hip_status(moe::launch_combine(y_disp, p_disp, inv_perm, S, D, K, y, stream));
+}
+
+size_t moe_grouped_ffn_workspace_bytes(int32_t E, int64_t R, int32_t D, int32_t F) {
+    if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(D) || !dim_ok(F)) return 0;
+    return moe::gemm_schedule_bytes(E);
+}
+
+static int check_ffn(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, int64_t R, int32_t D,
+                     int32_t F, const moe_bf16* W1, const moe_bf16* W2) {
+    if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(D) || !dim_ok(F)) return MOE_ERR_SHAPE;
+    MOE_TRY(need(x_disp, (uint64_t)R * D * 2, 16));
+    MOE_TRY(need(offsets, (uint64_t)(E + 1) * 4, 4));
+    MOE_TRY(need(W1, (uint64_t)E * D * F * 2, 16));
+    MOE_TRY(need(W2, (uint64_t)E * F * D * 2, 16));
+    return MOE_OK;
+}
+
+int moe_grouped_ffn(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, int64_t R, int32_t D,
+                    int32_t F, const moe_bf16* W1, const moe_bf16* W2, moe_bf16* h, moe_bf16* u_save,
+                    moe_bf16* y_disp, void* ws, size_t ws_bytes, hipStream_t stream) {
+    MOE_TRY(check_ffn(x_disp, offsets, E, R, D, F, W1, W2));
+    MOE_TRY(need(h, (uint64_t)R * F * 2, 16));
+    MOE_TRY(opt(u_save, 16));
+    MOE_TRY(need(y_disp, (uint64_t)R * D * 2, 16));
+    const size_t wsn = moe::gemm_schedule_bytes(E);
+    if (ws == nullptr || ws_bytes < wsn) return MOE_ERR_WORKSPACE;
+    MOE_TRY(opt(ws, 16));
+    if (R == 0) return MOE_OK;
+    int32_t* mts = (int32_t*)ws;
+    MOE_HIP(moe::launch_tile_schedule(offsets, E, mts, stream));
+    MOE_HIP(moe::launch_grouped_rows(x_disp, D, W1, F, (int64_t)D * F, false, h, F, moe::EPI_RELU2,
+                                     nullptr, u_save, offsets, mts, E, R, F, D, stream));
+    MOE_HIP(moe::launch_grouped_rows(h, F, W2, D, (int64_t)F * D, false, y_disp, D, moe::EPI_BF16,
+                                     nullptr, nullptr, offsets, mts, E, R, D, F, stream));
+    return MOE_OK;
+}
+
+int moe_latent_proj(const moe_bf16* A, const moe_bf16* W, int64_t M, int32_t Kd, int32_t N, moe_bf16* C,
+                    hipStream_t stream) {
+    if (M < 0 || M >= kMaxRows || !dim_ok(Kd) || !dim_ok(N)) return MOE_ERR_SHAPE;
+    MOE_TRY(need(A, (uint64_t)M * Kd * 2, 16));
+    MOE_TRY(need(W, (uint64_t)Kd * N * 2, 16));
+    MOE_TRY(need(C, (uint64_t)M * N * 2, 16));
+    return hip_status(moe::launch_grouped_rows(A, Kd, W, N, 0, false, C, N, moe::EPI_BF16, nullptr,
+                                               nullptr, nullptr, nullptr, 1, M, N, Kd, stream));
+}
+
+// ---------------------------------------------------------------------------
+// Whole layer
+// ---------------------------------------------------------------------------
+
+namespace {
+
+struct Carve {
+    char* base;
+    size_t used;
+    void* take(size_t bytes) {
+        void* p = base ? base + used : nullptr;
+        used += align256(bytes);
+        return p;
+    }
+};
+
+int check_layer_args(const moe_layer_fwd_args* a) {
+    if (a == nullptr) return MOE_ERR_NULL;
+    if (a->struct_size != sizeof(moe_layer_fwd_args)) return MOE_ERR_SHAPE;
+    MOE_TRY(check_route_shape(a->S, a->E, a->K));
+    if (!dim_ok(a->D) || !dim_ok(a->F)) return MOE_ERR_SHAPE;
+    if (a->H != 0 && !dim_ok(a->H)) return MOE_ERR_SHAPE;
+    return MOE_OK;
+}
+
+// Lays the non-exported intermediates out in the workspace (or, with base
+// == nullptr, only counts the bytes).  Pointers the caller exported win.
+struct LayerBufs {
+    moe_bf16* x_lat; float* logits; int32_t* topk_idx; float* topk_prob; int32_t* counts;
+    int32_t* offsets; int32_t* perm; int32_t* inv_perm; moe_bf16* x_disp; float* p_disp;
+    moe_bf16* h; moe_bf16* y_disp; moe_bf16* y_lat; void* route_ws; int32_t* mtile_start;
+};
+
+size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
+    Carve c{base, 0};
+    const int64_t S = a->S, R = S * a->K;
+    const int D = a->D, E = a->E, F = a->F;
+    auto pick = [&](auto* user, size_t bytes) -> decltype(user) {
+        if (user != nullptr) return user;
+        return (decltype(user))c.take(bytes);
+    };
+    b->x_lat = a->H ? pick(a->x_lat, (size_t)S * D * 2) : nullptr;
+    b->logits = pick(a->logits, (size_t)S * E * 4);
+    b->topk_idx = pick(a->topk_idx, (size_t)R * 4);
+    b->topk_prob = pick(a->topk_prob, (size_t)R * 4);
+    b->counts = pick(a->counts, (size_t)E * 4);
+    b->offsets = pick(a->offsets, (size_t)(E + 1) * 4);
+    b->perm = pick(a->perm, (size_t)R * 4);
+    b->inv_perm = pick(a->inv_perm, (size_t)R * 4);
+    b->x_disp = pick(a->x_disp, (size_t)R * D * 2);
+    b->p_disp = pick(a->p_disp, (size_t)R * 4);
+    b->h = pick(a->h, (size_t)R * F * 2);
+    b->y_disp = pick(a->y_disp, (size_t)R * D * 2);
+    b->y_lat = a->H ? pick(a->y_lat, (size_t)S * D * 2) : nullptr;
+    b->route_ws = c.take(moe::route_ws_bytes(S, E));
+    b->mtile_start = (int32_t*)c.take(moe::gemm_schedule_bytes(E));
+    return c.used;
+}
+
+}  // namespace
+
+size_t moe_layer_fwd_workspace_bytes(const moe_layer_fwd_args* a) {
+    if (check_layer_args(a) != MOE_OK) return 0;
+    LayerBufs b;
+    return layer_layout(a, nullptr, &b);
+}
+
+int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
+    MOE_TRY(check_layer_args(a));
+    const int64_t S = a->S, R = S * a->K;
+    const int H = a->H, D = a->D, E = a->E, K = a->K, F = a->F;
+    const int in_w = H ? H : D;
+    MOE_TRY(need(a->x, (uint64_t)S * in_w * 2, 16));
+    MOE_TRY(need(a->Wr, (uint64_t)D * E * 4, 4));
+    MOE_TRY(opt(a->router_bias, 4));
+    MOE_TRY(need(a->W1, (uint64_t)E * D * F * 2, 16));
+    MOE_TRY(need(a->W2, (uint64_t)E * F * D * 2, 16));
+    MOE_TRY(need(a->y, (uint64_t)S * in_w * 2, 16));
+    if (H) {
+        MOE_TRY(need(a->Wdown, (uint64_t)H * D * 2, 16));
+        MOE_TRY(need(a->Wup, (uint64_t)D * H * 2, 16));
+    } else if (a->Wdown != nullptr || a->Wup != nullptr) {
+        return MOE_ERR_SHAPE;
+    }
+    const void* bf16_ptrs[] = {a->x_lat, a->x_disp, a->h, a->u_save, a->y_disp, a->y_lat};
+    for (const void* p : bf16_ptrs) MOE_TRY(opt(p, 16));
+    const void* word_ptrs[] = {a->logits, a->topk_idx, a->topk_prob, a->counts, a->offsets,
+                               a->perm, a->inv_perm, a->p_disp};
+    for (const void* p : word_ptrs) MOE_TRY(opt(p, 4));
+
+    LayerBufs b;
+    const size_t need_ws = layer_layout(a, nullptr, &b);
+    if (a->ws == nullptr || a->ws_bytes < need_ws) return MOE_ERR_WORKSPACE;
+    MOE_TRY(opt(a->ws, 256));
+    layer_layout(a, (char*)a->ws, &b);
+
+    const moe_bf16* x_r = a->x;
+    if (H) {
+        MOE_HIP(moe::launch_grouped_rows(a->x, H, a->Wdown, D, 0, false, b.x_lat, D, moe::EPI_BF16,
+                                         nullptr, nullptr, nullptr, nullptr, 1, S, D, H, stream));
+        x_r = b.x_lat;
+    }
+    MOE_HIP(moe::launch_router_logits(x_r, a->Wr, a->router_bias, S, D, E, b.logits, stream));
+    MOE_HIP(moe::launch_route(b.logits, S, E, K, b.topk_idx, b.topk_prob, b.counts, b.offsets, b.perm,
+                              b.inv_perm, b.route_ws, stream));
+    MOE_HIP(moe::launch_dispatch(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_disp, b.p_disp, stream));
+    if (R > 0) {
+        MOE_HIP(moe::launch_tile_schedule(b.offsets, E, b.mtile_start, stream));
+        MOE_HIP(moe::launch_grouped_rows(b.x_disp, D, a->W1, F, (int64_t)D * F, false, b.h, F,
+                                         moe::EPI_RELU2, nullptr, a->u_save, b.offsets, b.mtile_start,
+                                         E, R, F, D, stream));
+        MOE_HIP(moe::launch_grouped_rows(b.h, F, a->W2, D, (int64_t)F * D, false, b.y_disp, D,
+                                         moe::EPI_BF16, nullptr, nullptr, b.offsets, b.mtile_start, E,
+                                         R, D, F, stream));
+    }
+    moe_bf16* comb_out = H ? b.y_lat : a->y;
+    MOE_HIP(moe::launch_combine(b.y_disp, b.p_disp, b.inv_perm, S, D, K, comb_out, stream));
+    if (H) {
+        MOE_HIP(moe::launch_grouped_rows(b.y_lat, D, a->Wup, H, 0, false, a->y, H, moe::EPI_BF16,
+                                         nullptr, nullptr, nullptr, nullptr, 1, S, H, D, stream));
+    }
+    return MOE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Backward
+// ---------------------------------------------------------------------------
+
+int moe_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const float* p_disp,
+                    const int32_t* inv_perm, int64_t S, int32_t D, int32_t K, moe_bf16* dy_disp,
+                    float* dp, hipStream_t stream) {
+    if (S < 0 || !dim_ok(D) || K < 1 || K > kMaxK || S * (int64_t)K >= kMaxRows) return MOE_ERR_SHAPE;
+    const uint64_t R = (uint64_t)S * K;
+    MOE_TRY(need(dy, (uint64_t)S * D * 2, 16));
+    MOE_TRY(need(y_disp, R * D * 2, 16));
+    MOE_TRY(opt(p_disp, 4));
+    MOE_TRY(need(inv_perm, R * 4, 4));
+    MOE_TRY(need(dy_disp, R * D * 2, 16));
+    MOE_TRY(opt(dp, 4));
+    return hip_status(moe::launch_combine_bwd(dy, y_disp, p_disp, inv_perm, S, D, K, dy_disp, dp, stream));
+}
+
+size_t moe_grouped_ffn_bwd_workspace_bytes(int32_t E, int64_t R, int32_t D, int32_t F) {
+    if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(D) || !dim_ok(F)) return 0;
+    return align256((size_t)R * F * 2) + moe::gemm_schedule_bytes(E);
+}
+
+int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const moe_bf16* h,
+                        const moe_bf16* dy_disp, const int32_t* offsets, int32_t E, int64_t R, int32_t D,
+                        int32_t F, const moe_bf16* W1, const moe_bf16* W2, moe_bf16* dx_disp,
+                        float* dW1, float* dW2, void* ws, size_t ws_bytes, hipStream_t stream) {
+    MOE_TRY(check_ffn(x_disp, offsets, E, R, D, F, W1, W2));
+    MOE_TRY(need(u_save, (uint64_t)R * F * 2, 16));
+    MOE_TRY(need(h, (uint64_t)R * F * 2, 16));
+    MOE_TRY(need(dy_disp, (uint64_t)R * D * 2, 16));
+    MOE_TRY(need(dx_disp, (uint64_t)R * D * 2, 16));
+    MOE_TRY(need(dW1, (uint64_t)E * D * F * 4, 16));
+    MOE_TRY(need(dW2, (uint64_t)E * F * D * 4, 16));
+    const size_t du_bytes = align256((size_t)R * F * 2);
+    const size_t wsn = du_bytes + moe::gemm_schedule_bytes(E);
+    if (ws == nullptr || ws_bytes < wsn) return MOE_ERR_WORKSPACE;
+    MOE_TRY(opt(ws, 256));
+    moe_bf16* du = (moe_bf16*)ws;
+    int32_t* mts = (int32_t*)((char*)ws + du_bytes);
+    if (R > 0) {
+        MOE_HIP(moe::launch_tile_schedule(offsets, E, mts, stream));
+        // du = (dy_disp @ W2[e]^T) * 2 max(u, 0): W2[e] is [F, D], read K(=D)-contiguous
+        MOE_HIP(moe::launch_grouped_rows(dy_disp, D, W2, D, (int64_t)F * D, true, du, F, moe::EPI_DRELU2,
+                                         u_save, nullptr, offsets, mts, E, R, F, D, stream));
+        // dx_disp = du @ W1[e]^T: W1[e] is [D, F], read K(=F)-contiguous
+        MOE_HIP(moe::launch_grouped_rows(du, F, W1, F, (int64_t)D * F, true, dx_disp, D, moe::EPI_BF16,
+                                         nullptr, nullptr, offsets, mts, E, R, D, F, stream));
+    }
+    // dW2[e] = h_e^T @ dy_disp_e  ([F, D]);  dW1[e] = x_disp_e^T @ du_e  ([D, F])
+    MOE_HIP(moe::launch_grouped_wgrad(h, F, dy_disp, D, dW2, D, (int64_t)F * D, offsets, E, F, D,
+                                      R, stream));
+    MOE_HIP(moe::launch_grouped_wgrad(x_disp, D, du, F, dW1, F, (int64_t)D * F, offsets, E, D, F,
+                                      R, stream));
+    return MOE_OK;
+}
+
+int moe_dispatch_bwd(const moe_bf16* dx_disp, const int32_t* inv_perm, int64_t S, int32_t D, int32_t K,
+                     moe_bf16* dx, hipStream_t stream) {
+    return moe_combine(dx_disp, nullptr, inv_perm, S, D, K, dx, stream);
+}
+
+}  // extern "C"

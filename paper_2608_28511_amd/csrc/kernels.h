@@ -1,0 +1,45 @@
+// Launchers of the gfx950 kernels (internal to the library; the public
+// surface is include/moe.h).  Each returns the HIP error of its launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "moe.h"
+
+namespace moe {
+
+enum { EPI_BF16 = 0, EPI_RELU2 = 1, EPI_DRELU2 = 2, EPI_F32 = 3 };
+
+hipError_t launch_router_logits(const moe_bf16* x, const float* Wr, const float* bias, int64_t S,
+                                int D, int E, float* logits, hipStream_t st);
+
+size_t route_ws_bytes(int64_t S, int E);
+hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* topk_idx,
+                        float* topk_prob, int32_t* counts, int32_t* offsets, int32_t* perm,
+                        int32_t* inv_perm, void* ws, hipStream_t st);
+
+hipError_t launch_dispatch(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S,
+                           int D, int K, moe_bf16* x_disp, float* p_disp, hipStream_t st);
+hipError_t launch_combine(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_perm,
+                          int64_t S, int D, int K, moe_bf16* y, hipStream_t st);
+hipError_t launch_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const float* p_disp,
+                              const int32_t* inv_perm, int64_t S, int D, int K, moe_bf16* dy_disp,
+                              float* dp, hipStream_t st);
+
+int gemm_tile_m();
+size_t gemm_schedule_bytes(int E);
+hipError_t launch_tile_schedule(const int32_t* offsets, int E, int32_t* mtile_start, hipStream_t st);
+// ROWS mode: C[r, :] = A[r, :] @ B_e (per expert segment) or dense when offsets == nullptr.
+// b_kmajor: B_e stored [N, Kd] (product with its transpose) instead of [Kd, N].
+hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
+                               int64_t b_stride, bool b_kmajor, void* C, int64_t ldc, int epi,
+                               const moe_bf16* aux_in, moe_bf16* aux_out, const int32_t* offsets,
+                               const int32_t* mtile_start, int E, int64_t R, int N, int Kd,
+                               hipStream_t st);
+// KGRP mode: C_e[m, n] = sum over expert e's rows r of A[r, m] * B[r, n]  (fp32 out).
+hipError_t launch_grouped_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
+                                float* C, int64_t ldc, int64_t c_stride, const int32_t* offsets,
+                                int E, int M, int N, int64_t R, hipStream_t st);
+
+}  // namespace moe

@@ -1,0 +1,146 @@
+"""Convenience wrappers that allocate outputs and workspace with torch and
+call the C ABI through ``_lib``.  Plumbing only: no arithmetic of the layer
+happens here."""
+from __future__ import annotations
+
+from typing import Dict, Optional
+
+import torch
+
+from . import _lib as L
+
+BF16, F32, I32 = torch.bfloat16, torch.float32, torch.int32
+
+
+def _empty(shape, dtype, device):
+    return torch.empty(shape, dtype=dtype, device=device)
+
+
+def _ws(nbytes: int, device) -> torch.Tensor:
+    return torch.empty((max(int(nbytes), 1),), dtype=torch.uint8, device=device)
+
+
+def router_logits(x_r: torch.Tensor, Wr: torch.Tensor, bias: Optional[torch.Tensor] = None):
+    S, D = x_r.shape
+    E = Wr.shape[1]
+    out = _empty((S, E), F32, x_r.device)
+    L.moe_router_logits(x_r, Wr, bias, S, D, E, out)
+    return out
+
+
+def route(logits: torch.Tensor, K: int) -> Dict[str, torch.Tensor]:
+    S, E = logits.shape
+    dev = logits.device
+    R = S * K
+    o = dict(topk_idx=_empty((S, K), I32, dev), topk_prob=_empty((S, K), F32, dev),
+             counts=_empty((E,), I32, dev), offsets=_empty((E + 1,), I32, dev),
+             perm=_empty((R,), I32, dev), inv_perm=_empty((R,), I32, dev))
+    ws = _ws(L.moe_route_workspace_bytes(S, E, K), dev)
+    L.moe_route_topk(logits, S, E, K, o["topk_idx"], o["topk_prob"], o["counts"], o["offsets"],
+                     o["perm"], o["inv_perm"], ws)
+    return o
+
+
+def dispatch(x: torch.Tensor, topk_prob: Optional[torch.Tensor], inv_perm: torch.Tensor, K: int):
+    S, D = x.shape
+    x_disp = _empty((S * K, D), BF16, x.device)
+    p_disp = _empty((S * K,), F32, x.device) if topk_prob is not None else None
+    L.moe_dispatch(x, topk_prob, inv_perm, S, D, K, x_disp, p_disp)
+    return x_disp, p_disp
+
+
+def grouped_ffn(x_disp: torch.Tensor, offsets: torch.Tensor, W1: torch.Tensor, W2: torch.Tensor,
+                save_u: bool = False):
+    R, D = x_disp.shape
+    E, _, F = W1.shape
+    dev = x_disp.device
+    h = _empty((R, F), BF16, dev)
+    u = _empty((R, F), BF16, dev) if save_u else None
+    y_disp = _empty((R, D), BF16, dev)
+    ws = _ws(L.moe_grouped_ffn_workspace_bytes(E, R, D, F), dev)
+    L.moe_grouped_ffn(x_disp, offsets, E, R, D, F, W1, W2, h, u, y_disp, ws)
+    return h, u, y_disp
+
+
+def combine(y_disp: torch.Tensor, p_disp: Optional[torch.Tensor], inv_perm: torch.Tensor, S: int,
+            K: int):
+    D = y_disp.shape[1]
+    y = _empty((S, D), BF16, y_disp.device)
+    L.moe_combine(y_disp, p_disp, inv_perm, S, D, K, y)
+    return y
+
+
+def latent_proj(A: torch.Tensor, W: torch.Tensor):
+    M, Kd = A.shape
+    N = W.shape[1]
+    C = _empty((M, N), BF16, A.device)
+    L.moe_latent_proj(A, W, M, Kd, N, C)
+    return C
+
+
+def combine_bwd(dy, y_disp, p_disp, inv_perm, K: int, want_dp: bool = True):
+    S, D = dy.shape
+    dy_disp = _empty((S * K, D), BF16, dy.device)
+    dp = _empty((S, K), F32, dy.device) if want_dp else None
+    L.moe_combine_bwd(dy, y_disp, p_disp, inv_perm, S, D, K, dy_disp, dp)
+    return dy_disp, dp
+
+
+def grouped_ffn_bwd(x_disp, u_save, h, dy_disp, offsets, W1, W2):
+    R, D = x_disp.shape
+    E, _, F = W1.shape
+    dev = x_disp.device
+    dx_disp = _empty((R, D), BF16, dev)
+    dW1 = _empty((E, D, F), F32, dev)
+    dW2 = _empty((E, F, D), F32, dev)
+    ws = _ws(L.moe_grouped_ffn_bwd_workspace_bytes(E, R, D, F), dev)
+    L.moe_grouped_ffn_bwd(x_disp, u_save, h, dy_disp, offsets, E, R, D, F, W1, W2, dx_disp, dW1,
+                          dW2, ws)
+    return dx_disp, dW1, dW2
+
+
+def dispatch_bwd(dx_disp, inv_perm, S: int, K: int):
+    D = dx_disp.shape[1]
+    dx = _empty((S, D), BF16, dx_disp.device)
+    L.moe_dispatch_bwd(dx_disp, inv_perm, S, D, K, dx)
+    return dx
+
+
+class LayerFwd:
+    """Preallocated buffers for repeated moe_layer_fwd calls on one shape.
+
+    With export=True every intermediate is a torch tensor owned here (for
+    parity checks); otherwise intermediates live in the workspace.
+    """
+
+    def __init__(self, S, D, E, K, F, H=0, device="cuda", export=True, save_u=False):
+        self.S, self.D, self.E, self.K, self.F, self.H = S, D, E, K, F, H
+        dev = torch.device(device)
+        R = S * K
+        self.out: Dict[str, Optional[torch.Tensor]] = {}
+        self.out["y"] = _empty((S, H if H else D), BF16, dev)
+        if export:
+            if H:
+                self.out["x_lat"] = _empty((S, D), BF16, dev)
+                self.out["y_lat"] = _empty((S, D), BF16, dev)
+            self.out.update(
+                logits=_empty((S, E), F32, dev), topk_idx=_empty((S, K), I32, dev),
+                topk_prob=_empty((S, K), F32, dev), counts=_empty((E,), I32, dev),
+                offsets=_empty((E + 1,), I32, dev), perm=_empty((R,), I32, dev),
+                inv_perm=_empty((R,), I32, dev), x_disp=_empty((R, D), BF16, dev),
+                p_disp=_empty((R,), F32, dev), h=_empty((R, F), BF16, dev),
+                y_disp=_empty((R, D), BF16, dev))
+        if save_u:
+            self.out["u_save"] = _empty((R, F), BF16, dev)
+        probe = L.layer_fwd_args(S, H, D, E, K, F, **{k: v for k, v in self.out.items()})
+        self.ws_bytes = L.moe_layer_fwd_workspace_bytes(probe)
+        if self.ws_bytes == 0:
+            raise ValueError("invalid layer shape")
+        self.ws = _ws(self.ws_bytes, dev)
+
+    def __call__(self, x, Wr, W1, W2, bias=None, Wdown=None, Wup=None):
+        a = L.layer_fwd_args(self.S, self.H, self.D, self.E, self.K, self.F, ws=self.ws, x=x, Wr=Wr,
+                             router_bias=bias, Wdown=Wdown, W1=W1, W2=W2, Wup=Wup,
+                             **self.out)
+        L.moe_layer_fwd(a)
+        return self.out

@@ -167,7 +167,8 @@ def make_logits(kind: str, S: int, E: int, seed: int, device="cpu") -> torch.Ten
     quantised  integers in {-2..2}: many exact ties
     equal      every row constant: selection must be experts 0..K-1
     signed0    entries drawn from {-0.0, +0.0, -1, 1}
-    masked     N(0,1) with ~half the entries set to -inf (at least 32 finite per row)
+    masked     N(0,1) with ~half the entries set to -inf (entry t % E of row t
+               always finite, so every row has a finite best score)
     nan        N(0,1) with a few NaN entries per row
     """
     g = _gen(device, seed)
@@ -185,8 +186,8 @@ def make_logits(kind: str, S: int, E: int, seed: int, device="cpu") -> torch.Ten
     if kind == "masked":
         v = torch.randn((S, E), generator=g, device=device)
         drop = torch.rand((S, E), generator=g, device=device) < 0.5
-        keep = torch.arange(E, device=device) % max(1, E // 32) == 0
-        drop &= ~keep[None, :]
+        rows = torch.arange(S, device=device)
+        drop[rows, rows % E] = False
         v[drop] = float("-inf")
         return v
     if kind == "nan":
@@ -204,3 +205,34 @@ def make_topk_indices(S: int, E: int, K: int, seed: int, device="cpu",
     w = torch.ones((E,), device=device) if weights is None else weights.to(device)
     idx = torch.multinomial(w.expand(S, E), K, replacement=False, generator=g)
     return idx.to(torch.int32)
+
+
+def make_segments(R: int, E: int, seed: int, empty: int = 0, skew: float = 0.0) -> torch.Tensor:
+    """Random expert segment boundaries: int32 [E+1] with offsets[0] = 0,
+    offsets[E] = R, non-decreasing.  ``empty`` experts (chosen at random)
+    get no rows; ``skew`` > 0 makes segment lengths Zipf-like."""
+    g = _gen("cpu", seed)
+    w = torch.rand((E,), generator=g, dtype=torch.float64) + 0.05
+    if skew > 0:
+        order = torch.randperm(E, generator=g).to(torch.float64) + 1.0
+        w = order ** (-skew)
+    if empty:
+        dead = torch.randperm(E, generator=g)[:empty]
+        w[dead] = 0.0
+    cut = torch.floor(torch.cumsum(w, 0) / w.sum() * R).to(torch.int64)
+    cut[-1] = R
+    off = torch.zeros((E + 1,), dtype=torch.int64)
+    off[1:] = cut
+    return off.to(torch.int32)
+
+
+def make_sparse_sign_rows(R: int, D: int, nnz: int, seed: int) -> torch.Tensor:
+    """[R, D] float32 rows holding exactly min(nnz, D) entries of +-1 at random
+    columns and zeros elsewhere (exact-arithmetic GEMM inputs)."""
+    g = _gen("cpu", seed)
+    out = torch.zeros((R, D), dtype=torch.float32)
+    n = min(nnz, D)
+    cols = torch.argsort(torch.rand((R, D), generator=g), dim=1)[:, :n]
+    signs = torch.randint(0, 2, (R, n), generator=g).to(torch.float32) * 2 - 1
+    out.scatter_(1, cols, signs)
+    return out

@@ -1,0 +1,125 @@
+"""CPU checks of the C ABI boundary: the library loads, exports every entry
+point include/moe.h declares, and rejects bad arguments synchronously.
+
+Only host-side paths run here: every call below fails validation (or is a
+pure size query) before anything is enqueued, so no GPU is touched.
+"""
+import ctypes as C
+import re
+from pathlib import Path
+
+import pytest
+
+from paper_2608_28511_amd import _lib as L
+
+ROOT = Path(__file__).resolve().parents[1]
+FAKE = C.c_void_p(0x10000)        # 16-byte aligned, never dereferenced
+ODD = C.c_void_p(0x10002)         # misaligned for 4- and 16-byte rules
+
+
+def _declared():
+    text = (ROOT / "include" / "moe.h").read_text()
+    return sorted(set(re.findall(r"^\s*(?:int|size_t|uint64_t|const char\*)\s+(moe_\w+)\(",
+                                 text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return L.load(build_if_missing=True)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert len(names) >= 17
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(L.EXPORTED)
+
+
+def test_version_status_payload(lib):
+    assert L.moe_abi_version() == 1
+    assert L.moe_status_string(0) == "ok"
+    for code in range(-6, 0):
+        assert L.moe_status_string(code) not in ("ok", "unknown status")
+    assert L.moe_status_string(-99) == "unknown status"
+    # Eq. 1: S*K*(D*b_x + b_p)
+    assert L.moe_payload_bytes(8192, 6, 2048) == 8192 * 6 * (2048 * 2 + 4) == 201_523_200
+    assert L.moe_payload_bytes(16384, 8, 2048) == 16384 * 8 * (2048 * 2 + 4)
+    assert L.moe_payload_bytes(-1, 2, 8) == 0
+
+
+def test_workspace_queries(lib):
+    assert lib.moe_route_workspace_bytes(16384, 128, 8) >= (16384 // 32) * 128 * 4
+    assert lib.moe_route_workspace_bytes(10, 4, 5) == 0          # K > E
+    assert lib.moe_route_workspace_bytes(10, 2048, 2) == 0       # E > 1024
+    assert lib.moe_route_workspace_bytes(10, 64, 33) == 0        # K > 32
+    assert lib.moe_route_workspace_bytes(2 ** 28, 64, 8) == 0    # S*K >= 2^31
+    assert lib.moe_grouped_ffn_workspace_bytes(64, 49152, 2048, 1024) > 0
+    assert lib.moe_grouped_ffn_workspace_bytes(64, 49152, 2044, 1024) == 0   # D % 8
+    assert lib.moe_grouped_ffn_bwd_workspace_bytes(8, 100, 64, 64) >= 100 * 64 * 2
+
+
+def test_layer_struct_layout_matches(lib):
+    a = L.LayerFwdArgs()
+    a.struct_size = C.sizeof(L.LayerFwdArgs)
+    a.S, a.H, a.D, a.E, a.K, a.F = 512, 0, 256, 8, 2, 512
+    n = L.moe_layer_fwd_workspace_bytes(a)
+    R = 512 * 2
+    assert n >= R * 256 * 2 * 2 + R * 512 * 2   # x_disp + y_disp + h at least
+    a.struct_size += 8
+    assert L.moe_layer_fwd_workspace_bytes(a) == 0
+    a.struct_size -= 8
+    a.H = 12                                      # not a multiple of 8
+    assert L.moe_layer_fwd_workspace_bytes(a) == 0
+
+
+def test_validation_errors_return_before_launch(lib):
+    st = None
+    # route: bad shapes, null and misaligned pointers, short workspace
+    assert lib.moe_route_topk(FAKE, 4, 8, 9, *[FAKE] * 6, FAKE, 1 << 20, st) == -2
+    assert lib.moe_route_topk(None, 4, 8, 2, *[FAKE] * 6, FAKE, 1 << 20, st) == -1
+    assert lib.moe_route_topk(FAKE, 4, 8, 2, ODD, *[FAKE] * 5, FAKE, 1 << 20, st) == -3
+    assert lib.moe_route_topk(FAKE, 4, 8, 2, *[FAKE] * 6, FAKE, 4, st) == -4
+    assert lib.moe_route_topk(FAKE, 4, 8, 2, *[FAKE] * 6, None, 1 << 20, st) == -4
+    assert lib.moe_route_topk(FAKE, -1, 8, 2, *[FAKE] * 6, FAKE, 1 << 20, st) == -2
+    # dispatch: D % 8, prob / p_disp must be both given or both NULL, alignment
+    assert lib.moe_dispatch(FAKE, FAKE, FAKE, 4, 12, 2, FAKE, FAKE, st) == -2
+    assert lib.moe_dispatch(FAKE, None, FAKE, 4, 16, 2, FAKE, FAKE, st) == -1
+    assert lib.moe_dispatch(C.c_void_p(0x10008), FAKE, FAKE, 4, 16, 2, FAKE, FAKE, st) == -3
+    # combine / grouped ffn / latent / backward
+    assert lib.moe_combine(FAKE, None, FAKE, 4, 16, 0, FAKE, st) == -2
+    assert lib.moe_combine(FAKE, None, None, 4, 16, 2, FAKE, st) == -1
+    assert lib.moe_grouped_ffn(FAKE, FAKE, 0, 4, 16, 16, FAKE, FAKE, FAKE, None, FAKE, FAKE, 4096, st) == -2
+    assert lib.moe_grouped_ffn(FAKE, FAKE, 2, 4, 16, 16, FAKE, FAKE, FAKE, None, FAKE, FAKE, 0, st) == -4
+    assert lib.moe_grouped_ffn(FAKE, FAKE, 2, 4, 16, 16, FAKE, FAKE, FAKE, ODD, FAKE, FAKE, 4096, st) == -3
+    assert lib.moe_latent_proj(FAKE, FAKE, 4, 20, 16, FAKE, st) == -2
+    assert lib.moe_router_logits(FAKE, FAKE, None, 4, 16, 0, FAKE, st) == -2
+    assert lib.moe_router_logits(FAKE, FAKE, ODD, 4, 16, 4, FAKE, st) == -3
+    assert lib.moe_combine_bwd(FAKE, FAKE, None, FAKE, 4, 16, 33, FAKE, None, st) == -2
+    assert lib.moe_grouped_ffn_bwd(FAKE, None, FAKE, FAKE, FAKE, 2, 4, 16, 16, FAKE, FAKE, FAKE,
+                                   FAKE, FAKE, FAKE, 1 << 20, st) == -1
+    assert lib.moe_grouped_ffn_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 4, 16, 16, FAKE, FAKE, FAKE,
+                                   FAKE, FAKE, FAKE, 8, st) == -4
+    assert lib.moe_dispatch_bwd(FAKE, FAKE, 4, 16, 40, FAKE, st) == -2
+    # layer: null args, wrong struct size, latent weights without H
+    assert lib.moe_layer_fwd(None, st) == -1
+    a = L.LayerFwdArgs()
+    a.struct_size = 4
+    assert lib.moe_layer_fwd(C.byref(a), st) == -2
+    a.struct_size = C.sizeof(L.LayerFwdArgs)
+    a.S, a.H, a.D, a.E, a.K, a.F = 4, 0, 16, 4, 2, 16
+    for f in ("x", "Wr", "W1", "W2", "y", "Wdown"):
+        setattr(a, f, 0x10000)
+    a.ws, a.ws_bytes = 0x10000, 1 << 30
+    assert lib.moe_layer_fwd(C.byref(a), st) == -2       # Wdown given with H == 0
+    a.Wdown = None
+    a.ws_bytes = 16
+    assert lib.moe_layer_fwd(C.byref(a), st) == -4       # workspace too small
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        L._ptr(torch.zeros(4), torch.float32, "x")
+    with pytest.raises(TypeError):
+        L._ptr([1, 2], torch.float32, "x")

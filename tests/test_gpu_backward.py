@@ -1,0 +1,122 @@
+"""GPU parity of the backward pass through combine, experts and dispatch.
+
+Routing comes from generated logits on both sides (bit-identical routes), the
+GPU runs its own forward (dispatch, grouped FFN with u saved) and backward
+(combine^T, grouped dgrad + wgrad, dispatch^T); the oracle runs the same
+chain in float64.  dx and du-derived bf16 outputs are held to the bf16 bar;
+the fp32 weight gradients to the same two metrics per tensor with the
+mean-absolute term taken relative to the tensor's rms.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+from paper_2608_28511_amd import layer
+from paper_2608_28511_amd.workloads import WORKLOADS, make_inputs
+
+from gpu_helpers import LazyExperts, assert_bf16_close, np64, npi
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def gpu_chain(x, logits, W1, W2, dy, K):
+    S = x.shape[0]
+    r = layer.route(logits, K)
+    x_disp, p_disp = layer.dispatch(x, r["topk_prob"], r["inv_perm"], K)
+    h, u, yd = layer.grouped_ffn(x_disp, r["offsets"], W1, W2, save_u=True)
+    y = layer.combine(yd, p_disp, r["inv_perm"], S, K)
+    dyd, dp = layer.combine_bwd(dy, yd, p_disp, r["inv_perm"], K)
+    dxd, dW1, dW2 = layer.grouped_ffn_bwd(x_disp, u, h, dyd, r["offsets"], W1, W2)
+    dx = layer.dispatch_bwd(dxd, r["inv_perm"], S, K)
+    torch.cuda.synchronize()
+    return dict(r=r, y=y, dp=dp, dx=dx, dW1=dW1, dW2=dW2, dxd=dxd)
+
+
+def oracle_chain(x, logits, W1, W2, dy, K, E):
+    S = x.shape[0]
+    idx, p = O.route(logits, K)
+    counts, off, perm, inv = O.expert_permutation(idx, E)
+    xd, pd = O.dispatch(x, p, inv, K)
+    u, h, yd = O.expert_ffn(xd, off, W1, W2)
+    y = O.combine(yd, pd, inv, S, K)
+    dyd, dp = O.combine_bwd(dy, yd, pd, inv, K)
+    dxd, dW1, dW2, du = O.expert_ffn_bwd(xd, u, h, dyd, off, W1, W2)
+    dx = O.dispatch_bwd(dxd, inv, S, K)
+    return dict(counts=counts, y=y, dp=dp, dx=dx, dW1=dW1, dW2=dW2)
+
+
+def assert_grad_close(got, ref, what):
+    assert_bf16_close(got, ref, what, mean_abs=1e-2, mean_rel_to_rms=True)
+
+
+@pytest.mark.parametrize("S,D,E,K,F", [(64, 64, 4, 2, 64), (300, 136, 9, 3, 200), (512, 256, 8, 2, 512),
+                                       (1024, 512, 32, 8, 256)])
+def test_backward_small(S, D, E, K, F):
+    g = torch.Generator().manual_seed(S + D + E)
+    x = torch.randn((S, D), generator=g).to(torch.bfloat16)
+    logits = torch.randn((S, E), generator=g)
+    logits[:, E - 1] = float("-inf")          # one dead expert
+    W1 = (torch.randn((E, D, F), generator=g) / np.sqrt(D)).to(torch.bfloat16)
+    W2 = (torch.randn((E, F, D), generator=g) / np.sqrt(F)).to(torch.bfloat16)
+    dy = torch.randn((S, D), generator=g).to(torch.bfloat16)
+    G = gpu_chain(x.to(DEV), logits.to(DEV), W1.to(DEV), W2.to(DEV), dy.to(DEV), K)
+    R = oracle_chain(np64(x), logits.numpy(), np64(W1), np64(W2), np64(dy), K, E)
+    assert np.array_equal(npi(G["r"]["counts"]), R["counts"])
+    assert_bf16_close(np64(G["y"]), R["y"], "y")
+    assert_bf16_close(np64(G["dx"]), R["dx"], "dx")
+    assert_grad_close(np64(G["dp"]), R["dp"], "dp")
+    assert_grad_close(np64(G["dW1"]), R["dW1"], "dW1")
+    assert_grad_close(np64(G["dW2"]), R["dW2"], "dW2")
+    assert torch.all(G["dW1"][E - 1] == 0) and torch.all(G["dW2"][E - 1] == 0)
+
+
+def test_backward_full_size_sampled():
+    """Zipf-skewed 16384-token workload: dx / dp on sampled tokens, dW on the
+    busiest, a median and a dead expert, against the oracle."""
+    s = WORKLOADS["skew_s16384_d2048_e128_k8_bwd"]
+    inp = make_inputs(s, device=DEV)
+    logits = torch.randn((s.S, s.E), device=DEV,
+                         generator=torch.Generator(device=DEV).manual_seed(2)) + inp["bias"][None, :]
+    G = gpu_chain(inp["x"], logits, inp["W1"], inp["W2"], inp["dy"], s.K)
+    lg = logits.cpu().numpy()
+    idx, p = O.route(lg, s.K)
+    counts = np.bincount(idx.ravel(), minlength=s.E)
+    assert np.array_equal(npi(G["r"]["counts"]), counts)
+    W1, W2 = LazyExperts(inp["W1"]), LazyExperts(inp["W2"])
+    x = np64(inp["x"])
+    dy = np64(inp["dy"])
+    # sampled tokens: every per-row quantity of the backward
+    tok = np.sort(np.random.default_rng(5).choice(s.S, 24, replace=False))
+    sub_idx, sub_p = idx[tok], p[tok]
+    _, off, perm, inv = O.expert_permutation(sub_idx, s.E)
+    xd, pd = O.dispatch(x[tok], sub_p, inv, s.K)
+    u, h, yd = O.expert_ffn(xd, off, W1, W2)
+    dyd, dp = O.combine_bwd(dy[tok], yd, pd, inv, s.K)
+    dxd, _, _, _ = O.expert_ffn_bwd(xd, u, h, dyd, off, W1, W2)
+    dx = O.dispatch_bwd(dxd, inv, len(tok), s.K)
+    sel = torch.as_tensor(tok, device=DEV)
+    assert_bf16_close(np64(G["dx"][sel]), dx, "dx sampled")
+    assert_grad_close(np64(G["dp"][sel]), dp, "dp sampled")
+    # sampled experts: busiest, median, dead
+    order = np.argsort(-counts, kind="stable")
+    dead = np.nonzero(counts == 0)[0]
+    assert dead.size >= 4
+    for e in (int(order[0]), int(order[len(order) // 2])):
+        t_e, k_e = np.nonzero(idx == e)
+        p_e = p[t_e, k_e].reshape(-1, 1)
+        n = len(t_e)
+        one = np.zeros((n, 1), np.int64)
+        off1 = np.array([0, n])
+        inv1 = np.arange(n)
+        xd1, pd1 = O.dispatch(x[t_e], p_e, inv1, 1)
+        w1, w2 = [W1[e]], [W2[e]]
+        u1, h1, yd1 = O.expert_ffn(xd1, off1, w1, w2)
+        dyd1, _ = O.combine_bwd(dy[t_e], yd1, pd1, inv1, 1)
+        _, dW1, dW2, _ = O.expert_ffn_bwd(xd1, u1, h1, dyd1, off1, w1, w2)
+        assert_grad_close(np64(G["dW1"][e]), dW1[0], f"dW1[{e}] ({n} rows)")
+        assert_grad_close(np64(G["dW2"][e]), dW2[0], f"dW2[{e}] ({n} rows)")
+        del one
+    for e in dead[:2]:
+        assert torch.all(G["dW1"][int(e)] == 0) and torch.all(G["dW2"][int(e)] == 0)

@@ -1,0 +1,106 @@
+"""GPU parity: grouped expert FFN (MFMA grouped GEMM + fused squared-ReLU)
+and the dense latent projection.
+
+Exact-arithmetic inputs (+-1 entries, at most 16 non-zeros per row, so every
+product, sum and u^2 is exact) require bit-exact outputs; these pin the MFMA
+lane layouts, the in-register transposes, the expert-segment mapping and the
+ragged row / k / n tails.  Random inputs are held to the bf16 bar.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+from paper_2608_28511_amd import layer
+from paper_2608_28511_amd.workloads import (WORKLOADS, make_inputs, make_logits, make_segments,
+                                            make_sparse_sign_rows)
+
+from gpu_helpers import LazyExperts, assert_bf16_close, np64, npi
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+# (R, D, F, E, empty experts, skew)
+SHAPES = [(1, 8, 8, 1, 0, 0.0), (100, 16, 24, 3, 0, 0.0), (1000, 264, 200, 5, 1, 0.0),
+          (777, 136, 392, 9, 2, 1.5), (4096, 256, 512, 8, 0, 0.0), (300, 512, 128, 64, 20, 0.0),
+          (2500, 192, 64, 2, 0, 2.0)]
+
+
+def _sign_weights(E, a, b, seed, density):
+    g = torch.Generator().manual_seed(seed)
+    v = torch.randint(-1, 2, (E, a, b), generator=g).to(torch.float32)
+    keep = torch.rand((E, a, b), generator=g) < density
+    return (v * keep).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("R,D,F,E,empty,skew", SHAPES)
+def test_grouped_ffn_exact(R, D, F, E, empty, skew):
+    off = make_segments(R, E, seed=R + E, empty=empty, skew=skew)
+    x = make_sparse_sign_rows(R, D, 16, seed=R).to(torch.bfloat16)
+    W1 = _sign_weights(E, D, F, seed=D, density=1.0)
+    # y = sum_f h_f W2[f, d] with h <= 256: keep one non-zero per W2 column block small
+    W2 = _sign_weights(E, F, D, seed=F, density=min(1.0, 4.0 / F))
+    h, u, yd = layer.grouped_ffn(x.to(DEV), off.to(DEV), W1.to(DEV), W2.to(DEV), save_u=True)
+    torch.cuda.synchronize()
+    u_ref, h_ref, y_ref = O.expert_ffn(np64(x), npi(off), np64(W1), np64(W2))
+    assert np.array_equal(np64(u), u_ref)
+    assert np.array_equal(np64(h), h_ref)
+    assert np.array_equal(np64(yd), y_ref)
+
+
+@pytest.mark.parametrize("R,D,F,E,empty,skew", SHAPES)
+def test_grouped_ffn_random(R, D, F, E, empty, skew):
+    g = torch.Generator().manual_seed(R * 3 + D)
+    off = make_segments(R, E, seed=R + 2 * E, empty=empty, skew=skew)
+    x = torch.randn((R, D), generator=g).to(torch.bfloat16)
+    W1 = (torch.randn((E, D, F), generator=g) / np.sqrt(D)).to(torch.bfloat16)
+    W2 = (torch.randn((E, F, D), generator=g) / np.sqrt(F)).to(torch.bfloat16)
+    h, u, yd = layer.grouped_ffn(x.to(DEV), off.to(DEV), W1.to(DEV), W2.to(DEV), save_u=True)
+    u_ref, h_ref, y_ref = O.expert_ffn(np64(x), npi(off), np64(W1), np64(W2))
+    assert_bf16_close(np64(u), u_ref, "u")
+    assert_bf16_close(np64(h), h_ref, "h")
+    assert_bf16_close(np64(yd), y_ref, "y_disp")
+
+
+@pytest.mark.parametrize("M,Kd,N", [(1, 8, 8), (300, 264, 136), (4096, 4096, 1024), (1000, 1024, 4096)])
+def test_latent_proj(M, Kd, N):
+    g = torch.Generator().manual_seed(M + Kd + N)
+    A = torch.randn((M, Kd), generator=g).to(torch.bfloat16)
+    W = (torch.randn((Kd, N), generator=g) / np.sqrt(Kd)).to(torch.bfloat16)
+    C = layer.latent_proj(A.to(DEV), W.to(DEV))
+    assert_bf16_close(np64(C), O.latent_down(np64(A), np64(W), round_payload=False), "latent")
+    # exact arithmetic: +-1 rows with 16 non-zeros times a +-1/0 weight
+    Ae = make_sparse_sign_rows(M, Kd, 16, seed=M).to(torch.bfloat16)
+    We = _sign_weights(1, Kd, N, seed=Kd, density=1.0)[0]
+    Ce = layer.latent_proj(Ae.to(DEV), We.to(DEV))
+    torch.cuda.synchronize()
+    assert np.array_equal(np64(Ce), O.latent_down(np64(Ae), np64(We)))
+
+
+@pytest.mark.parametrize("name", [n for n in WORKLOADS if not n.startswith("tiny")])
+def test_grouped_ffn_full_size_sampled(name):
+    """Full-size experts and routing; 96 sampled routed rows against the oracle."""
+    s = WORKLOADS[name]
+    inp = make_inputs(s.scaled(H=0), device=DEV)
+    x = inp["x"][:, : s.D].contiguous()
+    logits = torch.randn((s.S, s.E), device=DEV, generator=torch.Generator(device=DEV).manual_seed(1))
+    if inp["bias"] is not None:
+        logits = logits + inp["bias"][None, :]
+    r = layer.route(logits, s.K)
+    x_disp, p_disp = layer.dispatch(x, r["topk_prob"], r["inv_perm"], s.K)
+    h, u, yd = layer.grouped_ffn(x_disp, r["offsets"], inp["W1"], inp["W2"], save_u=True)
+    torch.cuda.synchronize()
+    idx, _ = O.route(logits.cpu().numpy(), s.K)
+    rng = np.random.default_rng(s.seed)
+    tok = rng.choice(s.S, 96 // s.K + 1, replace=False)
+    sub_idx = idx[tok]
+    _, off_sub, perm_sub, inv_sub = O.expert_permutation(sub_idx, s.E)
+    xs = np64(x[torch.as_tensor(tok, device=DEV)])
+    xd_sub, _ = O.dispatch(xs, None, inv_sub, s.K)
+    u_ref, h_ref, y_ref = O.expert_ffn(xd_sub, off_sub, LazyExperts(inp["W1"]), LazyExperts(inp["W2"]))
+    gpu_pos = npi(r["inv_perm"]).reshape(s.S, s.K)[tok].reshape(-1)
+    sel = torch.as_tensor(gpu_pos, device=DEV)
+    ref_order = inv_sub  # row i*K+k of the sub-problem sits at inv_sub[i*K+k]
+    assert_bf16_close(np64(h[sel]), h_ref[ref_order], f"{name} h")
+    assert_bf16_close(np64(u[sel]), u_ref[ref_order], f"{name} u")
+    assert_bf16_close(np64(yd[sel]), y_ref[ref_order], f"{name} y_disp")

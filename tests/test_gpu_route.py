@@ -1,0 +1,114 @@
+"""GPU parity: router logits, top-K routing and the expert permutation.
+
+Indices, counts, offsets, perm and inv_perm must match the oracle bit for
+bit from the same fp32 logits; probabilities within 1e-5 relative; logits
+within 1e-5 * max(|ref|, 1).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+from paper_2608_28511_amd import layer
+from paper_2608_28511_amd.workloads import WORKLOADS, make_inputs, make_logits
+
+from gpu_helpers import LOGIT_RTOL, assert_probs_close, np64, npi
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _route_and_compare(logits_cpu: torch.Tensor, K: int, probs: bool = True):
+    S, E = logits_cpu.shape
+    out = layer.route(logits_cpu.to(DEV), K)
+    torch.cuda.synchronize()
+    lg = logits_cpu.numpy()
+    ref_idx = O.topk_select(lg, K)
+    got_idx = npi(out["topk_idx"])
+    bad = np.nonzero(np.any(got_idx != ref_idx, axis=1))[0]
+    assert bad.size == 0, f"top-K differs on {bad.size} tokens, first {bad[:3]}: " \
+                          f"got {got_idx[bad[:1]]} ref {ref_idx[bad[:1]]}"
+    if probs:
+        assert_probs_close(np64(out["topk_prob"]), O.routing_probs(lg, ref_idx))
+    counts, offsets, perm, inv = O.expert_permutation(ref_idx, E)
+    assert np.array_equal(npi(out["counts"]), counts)
+    assert np.array_equal(npi(out["offsets"]), offsets)
+    assert np.array_equal(npi(out["perm"]), perm)
+    assert np.array_equal(npi(out["inv_perm"]), inv)
+    return out
+
+
+SHAPES = [(1, 1, 1), (31, 8, 2), (33, 8, 8), (512, 8, 2), (1000, 64, 6), (777, 256, 8),
+          (300, 1024, 32), (2049, 37, 5), (64, 128, 1), (95, 65, 3)]
+
+
+@pytest.mark.parametrize("kind", ["normal", "quantised", "equal", "signed0", "masked"])
+@pytest.mark.parametrize("S,E,K", SHAPES)
+def test_route_suites(kind, S, E, K):
+    _route_and_compare(make_logits(kind, S, E, seed=S * 7 + E + K), K)
+
+
+@pytest.mark.parametrize("S,E,K", [(64, 8, 2), (300, 128, 8), (129, 1024, 4)])
+def test_route_nan_logits_indices(S, E, K):
+    """NaN ranks below -inf: indices and the permutation stay exact (the
+    probabilities of a row holding NaN are unspecified)."""
+    _route_and_compare(make_logits("nan", S, E, seed=11 + E), K, probs=False)
+
+
+@pytest.mark.parametrize("name", list(WORKLOADS))
+def test_route_full_size(name):
+    """Full-size S, E, K with the workload's logit distribution (unit-variance
+    scores plus the workload's per-expert bias)."""
+    s = WORKLOADS[name]
+    g = torch.Generator().manual_seed(100 + s.seed)
+    logits = torch.randn((s.S, s.E), generator=g)
+    inp = make_inputs(s.scaled(S=1), device="cpu", with_experts=False)
+    if inp["bias"] is not None:
+        logits = logits + inp["bias"][None, :]
+    out = _route_and_compare(logits, s.K)
+    if s.bias == "zipf":
+        assert (npi(out["counts"]) == 0).sum() >= 4     # masked experts receive nothing
+
+
+def test_route_deterministic_and_empty():
+    logits = make_logits("quantised", 4097, 64, seed=5).to(DEV)
+    a = layer.route(logits, 6)
+    b = layer.route(logits, 6)
+    torch.cuda.synchronize()
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+    z = layer.route(torch.empty((0, 16), device=DEV), 4)
+    torch.cuda.synchronize()
+    assert npi(z["counts"]).tolist() == [0] * 16 and npi(z["offsets"]).tolist() == [0] * 17
+
+
+@pytest.mark.parametrize("S,D,E,bias", [(1, 8, 1, False), (100, 264, 37, True), (512, 256, 8, False),
+                                        (1000, 2048, 64, False), (777, 2048, 256, True),
+                                        (513, 1024, 128, False)])
+def test_router_logits(S, D, E, bias):
+    g = torch.Generator().manual_seed(S + D + E)
+    x = torch.randn((S, D), generator=g).to(torch.bfloat16)
+    Wr = torch.randn((D, E), generator=g) / np.sqrt(D)
+    b = torch.randn((E,), generator=g) if bias else None
+    if bias:
+        b[::7] = float("-inf")
+    got = np64(layer.router_logits(x.to(DEV), Wr.to(DEV), None if b is None else b.to(DEV)))
+    ref = O.router_logits(np64(x), np64(Wr), None if b is None else np64(b)).astype(np.float64)
+    fin = np.isfinite(ref)
+    assert np.array_equal(np.isfinite(got), fin) and np.all(got[~fin] == ref[~fin])
+    err = np.abs(got[fin] - ref[fin]) / np.maximum(np.abs(ref[fin]), 1.0)
+    assert err.max() <= LOGIT_RTOL, err.max()
+
+
+@pytest.mark.parametrize("name", list(WORKLOADS))
+def test_router_logits_full_size(name):
+    s = WORKLOADS[name]
+    inp = make_inputs(s, device=DEV, with_experts=False)
+    x_r = inp["x"] if not s.H else torch.randn((s.S, s.D), device=DEV).to(torch.bfloat16)
+    got = np64(layer.router_logits(x_r, inp["Wr"], inp["bias"]))
+    ref = O.router_logits(np64(x_r), np64(inp["Wr"]),
+                          None if inp["bias"] is None else np64(inp["bias"])).astype(np.float64)
+    fin = np.isfinite(ref)
+    assert np.array_equal(np.isfinite(got), fin)
+    err = np.abs(got[fin] - ref[fin]) / np.maximum(np.abs(ref[fin]), 1.0)
+    assert err.max() <= LOGIT_RTOL, err.max()
