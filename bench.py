@@ -1,0 +1,243 @@
+"""Benchmark of one routed MoE layer forward on one MI355X.
+
+Prints ONE JSON line on stdout (progress goes to stderr):
+  value        routed token-slots per second of moe_layer_fwd (S*K / layer time),
+               inputs resident in HBM, input sets rotated between steps so the
+               256 MB last-level cache cannot hold a step's weights
+  roofline     the dominant kernel (the larger of the two grouped GEMMs), timed
+               with HIP events on the stream it is launched on, against the
+               dense bf16 MFMA peak
+  stages       per-stage times and algorithmic GB/s or TFLOP/s
+  cpu_baseline the CPU oracle on a bounded sample of the same workload
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+from pathlib import Path
+
+ROOT = Path(__file__).resolve().parent
+sys.path.insert(0, str(ROOT))
+
+METRIC = ("routed token-slots/sec per MoE layer fwd; HBM GB/s (route/dispatch/combine), "
+          "MFMA % peak")
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, GB/s
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
+PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 vector, TFLOP/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="base_s8192_d2048_e64_k6")
+    p.add_argument("--sets", type=int, default=3, help="rotating input sets")
+    p.add_argument("--stage-reps", type=int, default=20)
+    p.add_argument("--cpu-tokens", type=int, default=1024)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--calib-bytes", type=int, default=1 << 30,
+                   help="size of the plain copy run once for counter calibration")
+    return p.parse_args()
+
+
+def stage_bytes(s):
+    S, D, E, K, F, R = s.S, s.D, s.E, s.K, s.F, s.R
+    return {
+        "router_logits": S * D * 2 + D * E * 4 + S * E * 4,
+        "route": S * E * 4 + R * 16 + (2 * E + 1) * 4,
+        "dispatch": S * D * 2 + R * 8 + R * (2 * D + 4),
+        "combine": R * (2 * D + 8) + S * D * 2,
+    }
+
+
+def time_region(fn, reps, stream):
+    """Average duration of fn() over reps back-to-back launches, bracketed by
+    HIP events recorded on `stream` (the stream the kernels run on)."""
+    import torch
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(reps):
+        fn(i)
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / reps * 1e-3   # seconds
+
+
+def cpu_baseline(s, inp, tokens):
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from oracle import moe_oracle as O
+
+    T = min(tokens, s.S)
+    x = inp["x"][:T].cpu().to(torch.float64).numpy()
+    Wr = inp["Wr"].cpu().to(torch.float64).numpy()
+    bias = None if inp["bias"] is None else inp["bias"].cpu().to(torch.float64).numpy()
+    W1c, W2c = inp["W1"].cpu(), inp["W2"].cpu()
+
+    class Experts:
+        def __init__(self, W):
+            self.W = W
+
+        def __getitem__(self, e):
+            return self.W[int(e)].to(torch.float64).numpy()
+
+    extra = {}
+    if s.H:
+        extra = dict(Wdown=inp["Wdown"].cpu().to(torch.float64).numpy(),
+                     Wup=inp["Wup"].cpu().to(torch.float64).numpy())
+    t0 = time.perf_counter()
+    O.layer_fwd(x, Wr, Experts(W1c), Experts(W2c), s.K, bias=bias, **extra)
+    dt = time.perf_counter() - t0
+    blas = [d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"]
+    return {
+        "value": T * s.K / dt, "unit": "slots/s", "cores": int(max(blas) if blas else 1),
+        "kind": "oracle",
+        "sample": f"first {T} of {s.S} tokens of the same workload through the float64 oracle "
+                  f"layer forward ({T * s.K} routed rows, {dt:.1f} s; BLAS matmuls threaded, "
+                  f"routing and permutation single-threaded Python)",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2608_28511_amd import _lib, layer
+    from paper_2608_28511_amd.workloads import WORKLOADS, make_inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        sys.exit(1)
+    _lib.load(build_if_missing=True)
+    s = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+
+    log(f"generating {args.sets} input sets for {s.name}")
+    sets = [make_inputs(s, device=dev, seed=s.seed + 1000 * i) for i in range(args.sets)]
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True)
+
+    # a plain device copy of known size, once, so hardware byte counters can be
+    # calibrated against it in profiler runs of this same command
+    n = args.calib_bytes // 2
+    a = torch.empty(n, dtype=torch.bfloat16, device=dev).fill_(1.0)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    del a, b
+    torch.cuda.synchronize()
+
+    def step(i):
+        inp = sets[i % len(sets)]
+        lf(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"], Wdown=inp.get("Wdown"),
+           Wup=inp.get("Wup"))
+
+    log(f"warmup {args.warmup}, timed {args.steps}")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t_layer = time_region(step, args.steps, stream)
+    slots = s.S * s.K
+    value = slots / t_layer
+
+    # ---- per-stage timings on the same stream, same launch configuration ----
+    out = lf.out
+    reps = args.stage_reps
+    st = {}
+    st["router_logits"] = time_region(
+        lambda i: _lib.moe_router_logits(sets[i % len(sets)]["x"] if not s.H else out["x_lat"],
+                                         sets[i % len(sets)]["Wr"], sets[i % len(sets)]["bias"],
+                                         s.S, s.D, s.E, out["logits"]), reps, stream)
+    ws_route = torch.empty(max(1, _lib.moe_route_workspace_bytes(s.S, s.E, s.K)), dtype=torch.uint8,
+                           device=dev)
+    r_bufs = {k: torch.empty_like(out[k]) for k in ("topk_idx", "topk_prob", "counts", "offsets",
+                                                      "perm", "inv_perm")}
+    st["route"] = time_region(
+        lambda i: _lib.moe_route_topk(out["logits"], s.S, s.E, s.K, r_bufs["topk_idx"],
+                                      r_bufs["topk_prob"], r_bufs["counts"], r_bufs["offsets"],
+                                      r_bufs["perm"], r_bufs["inv_perm"], ws_route), reps, stream)
+    xd2 = torch.empty_like(out["x_disp"])
+    pd2 = torch.empty_like(out["p_disp"])
+    x_r = [(st_["x"] if not s.H else out["x_lat"]) for st_ in sets]
+    st["dispatch"] = time_region(
+        lambda i: _lib.moe_dispatch(x_r[i % len(x_r)], out["topk_prob"], out["inv_perm"], s.S, s.D,
+                                    s.K, xd2, pd2), reps, stream)
+    sched = layer.grouped_schedule(out["offsets"], s.E)
+    h2 = torch.empty_like(out["h"])
+    yd2 = torch.empty_like(out["y_disp"])
+    st["grouped_up"] = time_region(
+        lambda i: _lib.moe_grouped_gemm(out["x_disp"], out["offsets"], sched, s.E, s.R, s.D, s.F,
+                                        sets[i % len(sets)]["W1"], 1, h2, None), reps, stream)
+    st["grouped_down"] = time_region(
+        lambda i: _lib.moe_grouped_gemm(out["h"], out["offsets"], sched, s.E, s.R, s.F, s.D,
+                                        sets[i % len(sets)]["W2"], 0, yd2, None), reps, stream)
+    y2 = torch.empty((s.S, s.D), dtype=torch.bfloat16, device=dev)
+    st["combine"] = time_region(
+        lambda i: _lib.moe_combine(out["y_disp"], out["p_disp"], out["inv_perm"], s.S, s.D, s.K, y2),
+        reps, stream)
+    if s.H:
+        st["latent_down"] = time_region(
+            lambda i: _lib.moe_latent_proj(sets[i % len(sets)]["x"], sets[i % len(sets)]["Wdown"],
+                                           s.S, s.H, s.D, out["x_lat"]), reps, stream)
+
+    bytes_ = stage_bytes(s)
+    gemm_flops = 2.0 * s.R * s.D * s.F
+    stages = {}
+    for k, t in st.items():
+        e = {"us": round(t * 1e6, 2)}
+        if k in ("route", "dispatch", "combine"):
+            gbs = bytes_[k] / t / 1e9
+            e.update(bytes=bytes_[k], GBps=round(gbs, 1), hbm_frac=round(gbs / PEAK_HBM_GBS, 4))
+        elif k == "router_logits":
+            tf = 2.0 * s.S * s.D * s.E / t / 1e12
+            e.update(TFLOPs=round(tf, 2), fp32_frac=round(tf / PEAK_FP32_TFLOPS, 4))
+        else:
+            fl = gemm_flops if k.startswith("grouped") else 2.0 * s.S * s.H * s.D
+            tf = fl / t / 1e12
+            e.update(flops=fl, TFLOPs=round(tf, 1), mfma_frac=round(tf / PEAK_BF16_TFLOPS, 4))
+        stages[k] = e
+
+    dom = max(("grouped_up", "grouped_down"), key=lambda k: st[k])
+    achieved = gemm_flops / st[dom] / 1e12
+    roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": None,
+                "per_launch": f"2*R*D*F = {gemm_flops:.4g} flop per launch (R = S*K = {s.R})"}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle on {args.cpu_tokens} tokens")
+        cpu = cpu_baseline(s, sets[0], args.cpu_tokens)
+
+    rec = {
+        "metric": METRIC, "value": round(value, 1), "unit": "slots/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t_layer * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": s.name, "S": s.S, "D": s.D, "E": s.E, "K": s.K, "F": s.F,
+                   "H": s.H, "rotating_input_sets": args.sets, "parallelism": "none (1 GPU)"},
+        "roofline": roofline, "stages": stages, "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

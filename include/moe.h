@@ -143,6 +143,25 @@ int moe_grouped_ffn(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, i
                     moe_bf16* h, moe_bf16* u_save, moe_bf16* y_disp,
                     void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* The two products of moe_grouped_ffn as separate launches (for callers that
+ * schedule or time them individually).
+ *
+ * moe_grouped_schedule: sched[0] = 0, sched[e+1] = sched[e] + ceil(counts[e] /
+ * 128), counts[e] = offsets[e+1] - offsets[e]: the per-expert 128-row tile
+ * schedule the grouped GEMM reads on the device.  sched [E+1] int32. */
+int moe_grouped_schedule(const int32_t* offsets, int32_t E, int32_t* sched, hipStream_t stream);
+
+/* One grouped GEMM over expert segments, one kernel launch:
+ *   C[r, :] = epi( A[r, :] @ W[e] ),  r in [offsets[e], offsets[e+1])
+ *   A [R, Kd] bf16;  W [E, Kd, N] bf16;  C [R, N] bf16;  sched from
+ *   moe_grouped_schedule for the same offsets.
+ *   epilogue 0: C = bf16(acc)                        (down projection)
+ *   epilogue 1: C = bf16(max(acc,0)^2), u_save = bf16(acc) if u_save != NULL
+ *                                                    (up projection)  */
+int moe_grouped_gemm(const moe_bf16* A, const int32_t* offsets, const int32_t* sched, int32_t E,
+                     int64_t R, int32_t Kd, int32_t N, const moe_bf16* W, int32_t epilogue,
+                     moe_bf16* C, moe_bf16* u_save, hipStream_t stream);
+
 /* ---------------------------------------------------------------------- */
 /* Combine: probability-weighted sum back to token order (the hidden       */
 /* combine of Section 4.1's footnote; D*b_x per routed row, Eq. 1).        */

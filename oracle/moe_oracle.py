@@ -297,22 +297,23 @@ def latent_up(y_lat, Wup) -> np.ndarray:
 
 
 def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
-              logits=None, round_payload: bool = True) -> dict:
+              logits=None, round_payload: bool = True, round_latent: bool = True) -> dict:
     """One routed MoE layer forward, in the paper's order (Section 4.1
     footnote: hidden dispatch, probability dispatch, hidden combine):
     [latent down] -> router logits -> top-K + probabilities -> permutation ->
     dispatch -> experts -> combine -> [latent up].
 
     If ``logits`` is given, routing uses those fp32 scores instead of the
-    ones computed here (so a caller can route both sides from identical
-    scores).  Returns every intermediate in a dict.
+    ones computed here.  ``round_latent`` rounds the projected activations
+    (the dispatched, routed input) to bf16; ``round_payload`` rounds the
+    expert outputs sent back for the combine.  Returns every intermediate.
     """
     x = np.asarray(x, np.float64)
     S = x.shape[0]
     out = {}
     x_r = x
     if Wdown is not None:
-        x_r = latent_down(x, Wdown, round_payload)
+        x_r = latent_down(x, Wdown, round_latent)
         out["x_lat"] = x_r
     if logits is None:
         logits = router_logits(x_r, Wr, bias)

@@ -174,6 +174,31 @@ int moe_grouped_ffn(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, i
     return MOE_OK;
 }
 
+int moe_grouped_schedule(const int32_t* offsets, int32_t E, int32_t* sched, hipStream_t stream) {
+    if (E < 1 || E > kMaxE) return MOE_ERR_SHAPE;
+    MOE_TRY(need(offsets, (uint64_t)(E + 1) * 4, 4));
+    MOE_TRY(need(sched, (uint64_t)(E + 1) * 4, 4));
+    return hip_status(moe::launch_tile_schedule(offsets, E, sched, stream));
+}
+
+int moe_grouped_gemm(const moe_bf16* A, const int32_t* offsets, const int32_t* sched, int32_t E,
+                     int64_t R, int32_t Kd, int32_t N, const moe_bf16* W, int32_t epilogue,
+                     moe_bf16* C, moe_bf16* u_save, hipStream_t stream) {
+    if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(Kd) || !dim_ok(N)) return MOE_ERR_SHAPE;
+    if (epilogue != 0 && epilogue != 1) return MOE_ERR_UNSUPPORTED;
+    if (epilogue == 0 && u_save != nullptr) return MOE_ERR_SHAPE;
+    MOE_TRY(need(A, (uint64_t)R * Kd * 2, 16));
+    MOE_TRY(need(offsets, (uint64_t)(E + 1) * 4, 4));
+    MOE_TRY(need(sched, (uint64_t)(E + 1) * 4, 4));
+    MOE_TRY(need(W, (uint64_t)E * Kd * N * 2, 16));
+    MOE_TRY(need(C, (uint64_t)R * N * 2, 16));
+    MOE_TRY(opt(u_save, 16));
+    if (R == 0) return MOE_OK;
+    return hip_status(moe::launch_grouped_rows(A, Kd, W, N, (int64_t)Kd * N, false, C, N,
+                                               epilogue == 1 ? moe::EPI_RELU2 : moe::EPI_BF16, nullptr,
+                                               u_save, offsets, sched, E, R, N, Kd, stream));
+}
+
 int moe_latent_proj(const moe_bf16* A, const moe_bf16* W, int64_t M, int32_t Kd, int32_t N, moe_bf16* C,
                     hipStream_t stream) {
     if (M < 0 || M >= kMaxRows || !dim_ok(Kd) || !dim_ok(N)) return MOE_ERR_SHAPE;

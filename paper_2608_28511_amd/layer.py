@@ -62,6 +62,21 @@ def grouped_ffn(x_disp: torch.Tensor, offsets: torch.Tensor, W1: torch.Tensor, W
     return h, u, y_disp
 
 
+def grouped_schedule(offsets: torch.Tensor, E: int):
+    sched = _empty((E + 1,), I32, offsets.device)
+    L.moe_grouped_schedule(offsets, E, sched)
+    return sched
+
+
+def grouped_gemm(A: torch.Tensor, offsets: torch.Tensor, sched: torch.Tensor, W: torch.Tensor,
+                 epilogue: int, out: Optional[torch.Tensor] = None, u_save: Optional[torch.Tensor] = None):
+    R, Kd = A.shape
+    E, _, N = W.shape
+    C = out if out is not None else _empty((R, N), BF16, A.device)
+    L.moe_grouped_gemm(A, offsets, sched, E, R, Kd, N, W, epilogue, C, u_save)
+    return C
+
+
 def combine(y_disp: torch.Tensor, p_disp: Optional[torch.Tensor], inv_perm: torch.Tensor, S: int,
             K: int):
     D = y_disp.shape[1]
