@@ -11,38 +11,63 @@
 //   KGRP mode   C_e[m, n] = sum_{r in segment e} A[r, m] * B[r, n]  (wgrad:
 //               the contraction runs over the expert's ragged rows).
 //
-// Tiles are BM x BN x BK = 128 x 128 x 64 on 256 threads (4 wavefronts in a
-// 2 x 2 grid, 64 x 64 outputs each, 16 v_mfma_f32_16x16x32_bf16 per 32-wide k
-// step).  Both operands live in LDS as "rows of K-contiguous 16-byte chunks"
-// with an XOR swizzle on the chunk index, which is the layout the MFMA
-// operand reads want.  An operand whose source is K-contiguous is copied
-// straight in; one whose source is M/N-contiguous (weights stored [D, F] or
-// [F, D], and both wgrad operands) is read as 4x8 bf16 blocks with 16-byte
-// loads and transposed in registers before the LDS write.  LDS is double
-// buffered with the next tile's global loads issued before the current
-// tile's MFMAs.
+// Block tile BM x BN x BK = 128 x 256 x 64 on 512 threads: 8 wavefronts in a
+// 2 x 4 grid, 64 x 64 outputs each (4 x 4 v_mfma_f32_16x16x32_bf16 per
+// 32-wide k step).  One workgroup fills a CU's LDS, so each SIMD runs two
+// wavefronts: one wave's address arithmetic, barrier and LDS latency overlap
+// the other's MFMAs.
 //
-// The MFMA is issued with the weight tile as its first operand, so each
+// Operands never pass through registers on their way to LDS: every 16-byte
+// chunk is copied by global_load_lds_dwordx4 into a 3-stage LDS ring (48 KB
+// per stage), two stages in flight while the third is consumed.  Each
+// operand keeps the layout it has in HBM:
+//   K-contiguous source  -> LDS rows of 64 k (8 chunks, XOR-swizzled by row),
+//                           MFMA fragments read with ds_read_b128;
+//   M/N-contiguous source (weights stored [D, F] / [F, D], both wgrad
+//                           operands) -> LDS k-rows of BM or BN elements
+//                           (chunk pairs XOR-swizzled by k), fragments read
+//                           with two ds_read_b64_tr_b16, the gfx950 LDS
+//                           transpose read, so no VALU transposition at all.
+// A DMA lane's LDS destination is fixed by its lane id, so the swizzles are
+// applied by permuting which global chunk each lane fetches.  Lanes whose
+// chunk lies outside the operand (ragged expert rows, k / n tails) fetch a
+// zero chunk instead, so partial tiles need no special path.
+//
+// The MFMA takes the weight-side fragment as its first operand, so each
 // lane's four accumulators hold four consecutive output columns of one row:
-// the epilogue stores 8 bytes (bf16) or 16 bytes (fp32) per lane directly,
-// after fusing squared-ReLU (up), its derivative (dgrad), or nothing.
+// the epilogue stores 8 bytes (bf16) or 16 bytes (fp32) per lane, after
+// fusing squared-ReLU (up), its derivative (dgrad) or nothing.
 //
-// Workgroups of one expert segment are found from a device-side tile
-// schedule (prefix sum of per-expert tile counts), so no host ever reads the
-// routing counts; workgroup ids are remapped so that consecutive tiles land
-// on the same XCD and share its L2.
+// Workgroups of an expert segment are located through a device-side tile
+// schedule (prefix sum of per-expert 128-row tile counts): no host reads the
+// routing counts.  Workgroup ids are remapped so that consecutive tiles run
+// on the same XCD and share its L2, and tiles are grouped 8 m-tiles at a time.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace moe {
 
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int kGemmThreads = 256;
-constexpr int kChunks = BK / 8;     // 16-byte chunks per LDS row
-constexpr int kGroupM = 8;          // m-tiles per scheduling group
+constexpr int BM = 128, BN = 256, BK = 64;
+constexpr int kGemmThreads = 512;
+constexpr int kWaves = kGemmThreads / 64;
+constexpr int kStages = 3;
+constexpr int kABytes = BM * BK * 2;            // 16 KB
+constexpr int kBBytes = BN * BK * 2;            // 32 KB
+constexpr int kStageBytes = kABytes + kBBytes;  // 48 KB
+constexpr int kGroupM = 8;
 constexpr int kXcds = 8;
 
 enum { MODE_ROWS = 0, MODE_KGRP = 1 };
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) char lds_char;
+
+// One zero chunk: the source of every out-of-range DMA lane.
+__device__ __attribute__((aligned(16))) uint4 g_zero_chunk[1];
 
 struct GemmArgs {
     const uint16_t* A;
@@ -61,103 +86,133 @@ struct GemmArgs {
     int m_tiles, n_tiles;
 };
 
-__device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & (kChunks - 1); }
+// ---- row layout: [rows][64 k], 8 chunks per row; chunk c of row r stored at
+// c ^ rswz(r).  rswz has period 16 in r, so the fragments of rows r and r + 16
+// sit a constant 2 KB apart (an immediate offset); within any 16 consecutive
+// rows the 16-byte reads of one ds_read_b128 hit distinct banks.
+__device__ __forceinline__ int rswz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-// Byte offset of chunk c of LDS row r.
-__device__ __forceinline__ int lds_off(int r, int c) { return (r * kChunks + (c ^ swz(r))) * 16; }
+// ---- col layout: [64 k][cols], cols/8 chunks per k-row; chunk pairs XOR-swizzled
+// so the 8 rows {k..k+3, k+8..k+11} read together by ds_read_b64_tr_b16 hit
+// distinct 32-byte bank groups.  cswz depends on k mod 16 only, so rows k + 4
+// and k + 32 sit constant offsets away.
+__device__ __forceinline__ int cswz(int k) { return 2 * ((k & 3) | (((k >> 3) & 1) << 2)); }
 
-// Tile rows [r0, r0+ROWS) x k [k0, k0+BK) from a K-contiguous source:
-// element (r, k) at src[r*ld + k]; rows >= r_hi and k >= k_hi read as zero.
-template <int ROWS>
-struct KMajorTile {
-    static constexpr int kPer = ROWS * kChunks / kGemmThreads;
-    uint4 v[kPer];
-    __device__ __forceinline__ void load(const uint16_t* __restrict__ src, int64_t ld, int64_t r0,
-                                         int64_t r_hi, int64_t k0, int64_t k_hi, int tid) {
+// 16-byte global -> LDS copy for the whole wave: lane l's chunk lands at LDS
+// byte lds_addr + 16*l (lds_addr wave-uniform).  Issued as inline assembly so
+// that the compiler does not treat it as an LDS write that every later LDS
+// read must wait for; the kernel orders it with explicit vmcnt waits and
+// barriers instead.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(g), "s"(lds_addr)
+                 : "memory", "m0");
+}
+
+// Workgroup barrier without the memory fence of __syncthreads (whose release
+// fence would drain every in-flight DMA stage).  Callers wait for their own
+// DMA stage with wait_vmcnt first; every LDS read of the previous stage has
+// been consumed by an MFMA before a wave can arrive here.
+__device__ __forceinline__ void stage_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else if constexpr (N == 6) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
+    else static_assert(N == 0, "unsupported vmcnt");
+}
+
+// Per-lane DMA slots of one operand tile.  Slot i of a wave covers LDS bytes
+// [(wave*kSlots + i)*1024, +1024) of the tile; each lane's 16-byte chunk has a
+// fixed global row / column for the whole k loop, so its pointer advances by
+// one k tile per stage (by zero for chunks outside the operand, which keep
+// pointing at the zero chunk).  Only a tile that crosses the end of the
+// contraction re-checks the k coordinate.
+//
+// Row layout (K-contiguous source, element (r, k) at src[r*ld + k]).
+// Col layout (M/N-contiguous source, element (k, c) at src[k*ld + c]).
+template <bool ROWL, int EXT>
+struct DmaTile {
+    static constexpr int kCPR = ROWL ? 8 : EXT / 8;       // chunks per LDS row
+    static constexpr int kSlots = EXT * 8 / 64 / kWaves;  // 1 KB slots per wave
+    const uint16_t* ptr[kSlots];
+    int64_t step[kSlots];
+    int kpos[kSlots];      // k offset of the chunk inside the tile
+    bool ok[kSlots];
+
+    __device__ __forceinline__ void init(const uint16_t* __restrict__ src, int64_t ld, int64_t x0,
+                                         int64_t x_hi, int64_t k_begin, int wave, int lane) {
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-            const int q = tid + kGemmThreads * i;
-            const int r = q / kChunks, c = q % kChunks;
-            const int64_t gr = r0 + r, gk = k0 + c * 8;
-            if (gr < r_hi && gk < k_hi)
-                v[i] = *(const uint4*)(src + gr * ld + gk);
+        for (int i = 0; i < kSlots; ++i) {
+            const int p = (wave * kSlots + i) * 64 + lane;
+            const int row = p / kCPR;
+            int c = p % kCPR;
+            if (ROWL) {
+                c ^= rswz(row);
+                ok[i] = x0 + row < x_hi;
+                kpos[i] = c * 8;
+                ptr[i] = ok[i] ? src + (x0 + row) * ld + k_begin + c * 8 : (const uint16_t*)g_zero_chunk;
+                step[i] = ok[i] ? (int64_t)BK : 0;
+            } else {
+                c ^= cswz(row);
+                ok[i] = x0 + c * 8 < x_hi;
+                kpos[i] = row;
+                ptr[i] = ok[i] ? src + (k_begin + row) * ld + x0 + c * 8 : (const uint16_t*)g_zero_chunk;
+                step[i] = ok[i] ? (int64_t)BK * ld : 0;
+            }
+        }
+    }
+    // Issue this wave's slots [I0, I1) of the next tile in k order, then
+    // advance.  KTAIL: the contraction length may end inside a tile, so chunks
+    // at or past k_rem are replaced by the zero chunk.
+    template <bool KTAIL, int I0, int I1>
+    __device__ __forceinline__ void issue(uint32_t tile_lds, int64_t k_rem, int wave) {
+#pragma unroll
+        for (int i = I0; i < I1; ++i) {
+            const uint32_t dst = tile_lds + (uint32_t)(wave * kSlots + i) * 1024u;
+            if constexpr (KTAIL)
+                dma16(kpos[i] < k_rem ? (const void*)ptr[i] : (const void*)g_zero_chunk, dst);
             else
-                v[i] = make_uint4(0, 0, 0, 0);
-        }
-    }
-    __device__ __forceinline__ void store(char* lds, int tid) const {
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-            const int q = tid + kGemmThreads * i;
-            const int r = q / kChunks, c = q % kChunks;
-            *(uint4*)(lds + lds_off(r, c)) = v[i];
+                dma16(ptr[i], dst);
+            ptr[i] += step[i];
         }
     }
 };
 
-// Tile rows [r0, r0+ROWS) x k [k0, k0+BK) from a row(M/N)-contiguous source:
-// element (r, k) at src[k*ld + r].  Each thread loads a 4(k) x 8(r) block
-// with four 16-byte loads and writes it transposed as eight 8-byte pieces.
-template <int ROWS>
-struct MNMajorTile {
-    static constexpr int kRB = ROWS / 8;                       // 8-row blocks
-    static constexpr int kBlocks = (BK / 4) * kRB;
-    static constexpr int kPer = kBlocks / kGemmThreads;
-    uint4 v[kPer][4];
-    __device__ __forceinline__ void load(const uint16_t* __restrict__ src, int64_t ld, int64_t r0,
-                                         int64_t r_hi, int64_t k0, int64_t k_hi, int tid) {
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-            const int b = tid + kGemmThreads * i;
-            const int kb = b / kRB, rb = b % kRB;
-            const int64_t gr = r0 + rb * 8;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int64_t gk = k0 + kb * 4 + q;
-                if (gr < r_hi && gk < k_hi)
-                    v[i][q] = *(const uint4*)(src + gk * ld + gr);
-                else
-                    v[i][q] = make_uint4(0, 0, 0, 0);
-            }
-        }
-    }
-    __device__ __forceinline__ void store(char* lds, int tid) const {
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-            const int b = tid + kGemmThreads * i;
-            const int kb = b / kRB, rb = b % kRB;
-            const uint32_t* w0 = (const uint32_t*)&v[i][0];
-            const uint32_t* w1 = (const uint32_t*)&v[i][1];
-            const uint32_t* w2 = (const uint32_t*)&v[i][2];
-            const uint32_t* w3 = (const uint32_t*)&v[i][3];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int wd = j >> 1;
-                uint32_t lo, hi;
-                if (j & 1) {
-                    lo = (w0[wd] >> 16) | (w1[wd] & 0xffff0000u);
-                    hi = (w2[wd] >> 16) | (w3[wd] & 0xffff0000u);
-                } else {
-                    lo = (w0[wd] & 0xffffu) | (w1[wd] << 16);
-                    hi = (w2[wd] & 0xffffu) | (w3[wd] << 16);
-                }
-                const int r = rb * 8 + j;
-                *(uint2*)(lds + lds_off(r, kb >> 1) + (kb & 1) * 8) = make_uint2(lo, hi);
-            }
-        }
-    }
-};
+// Fragment addressing.  A fragment is 16 rows x 8 k per lane group; the lane
+// base offsets below are computed once, everything else is an immediate.
+//
+// Row layout: lane reads row (row0 + lane%16), chunk (4*kk + lane/16) ^ rswz.
+__device__ __forceinline__ uint32_t row_base(int row0, int kk, int lane) {
+    const int r = row0 + (lane & 15);
+    const int c = kk * 4 + (lane >> 4);
+    return (uint32_t)((r * 8 + (c ^ rswz(r))) * 16);
+}
+// Col layout: lane 16g + 4r + q points at k-row 8g + r (+32 kk, +4 for the
+// second read), columns col0 + 4q .. +3; each 16-lane group then receives one
+// column each from ds_read_b64_tr_b16.
+template <int COLS>
+__device__ __forceinline__ uint32_t col_base(int col0, int lane) {
+    constexpr int kCPR = COLS / 8;
+    const int g = lane >> 4, rq = (lane >> 2) & 3, q = lane & 3;
+    const int k = g * 8 + rq;
+    const int c = (col0 >> 3) + (q >> 1);
+    return (uint32_t)((k * kCPR + (c ^ cswz(k))) * 16 + (q & 1) * 8);
+}
 
-template <bool KMAJOR, int ROWS>
-struct TileSel;
-template <int ROWS>
-struct TileSel<true, ROWS> {
-    using type = KMajorTile<ROWS>;
-};
-template <int ROWS>
-struct TileSel<false, ROWS> {
-    using type = MNMajorTile<ROWS>;
-};
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+
+__device__ __forceinline__ bf16x8 lds_b128(uint32_t addr) { return *(const lds_bf16x8*)(uintptr_t)addr; }
+
+__device__ __forceinline__ bf16x8 lds_tr_pair(uint32_t addr, uint32_t hi_off) {
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(uintptr_t)addr);
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(uintptr_t)(addr + hi_off));
+    const v8i16 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
 
 __device__ __forceinline__ int xcd_remap(int pid, int n) {
     const int q = n / kXcds, r = n % kXcds;
@@ -165,15 +220,13 @@ __device__ __forceinline__ int xcd_remap(int pid, int n) {
     return xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
 }
 
-template <int MODE, bool A_K, bool B_K, int EPI>
-__global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs p) {
-    __shared__ __attribute__((aligned(16))) char smem[2 * (BM + BN) * BK * 2];
-    char* const As0 = smem;
-    char* const Bs0 = smem + BM * BK * 2;
-    constexpr int kBufBytes = (BM + BN) * BK * 2;
+template <int MODE, bool A_K, bool B_K, int EPI, bool KTAIL>
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(GemmArgs p) {
+    __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];  // 144 KB
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar LDS offsets
+    const int wm = wave >> 2, wn = wave & 3;
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
 
     int e = 0, mt, nt;
@@ -222,8 +275,31 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs p) {
     const int64_t n0 = (int64_t)nt * BN;
     const uint16_t* Bsrc = p.B + (MODE == MODE_ROWS ? (int64_t)e * p.b_stride : 0);
 
-    typename TileSel<A_K, BM>::type ta;
-    typename TileSel<B_K, BN>::type tb;
+    // LDS: B tiles of the 3 stages first, then the A tiles.
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char*)smem;
+    const uint32_t ldsB = lds0, ldsA = lds0 + kStages * kBBytes;
+
+    DmaTile<A_K, BM> da;
+    DmaTile<B_K, BN> db;
+    da.init(p.A, p.lda, row0, row_hi, k_begin, wave, lane);
+    db.init(Bsrc, p.ldb, n0, (int64_t)p.N, k_begin, wave, lane);
+    constexpr int kSA = DmaTile<A_K, BM>::kSlots, kSB = DmaTile<B_K, BN>::kSlots;
+    constexpr int kPerStage = kSA + kSB;  // DMA instructions per wave per stage: 2 + 4
+
+    // Per-lane fragment bases; stage, k-step and tile offsets are immediates.
+    // B tiles of stages 0/1 are reached from bbase[0], stage 2 from bbase[1]
+    // (the immediate offset field holds at most 64 KB).
+    constexpr int kNA = A_K ? 2 : 4, kNB = B_K ? 2 : 4;
+    uint32_t abase[kNA], bbase[2][kNB];
+#pragma unroll
+    for (int i = 0; i < kNA; ++i)
+        abase[i] = ldsA + (A_K ? row_base(wm * 64, i, lane) : col_base<BM>(wm * 64 + i * 16, lane));
+#pragma unroll
+    for (int j = 0; j < kNB; ++j) {
+        const uint32_t o = B_K ? row_base(wn * 64, j, lane) : col_base<BN>(wn * 64 + j * 16, lane);
+        bbase[0][j] = ldsB + o;
+        bbase[1][j] = ldsB + 2 * kBBytes + o;
+    }
 
     f32x4 acc[4][4];
 #pragma unroll
@@ -234,53 +310,55 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs p) {
     const int64_t klen = k_end - k_begin;
     const int nk = (int)((klen + BK - 1) / BK);
 
-    // Row ranges of the two operand tiles: A rows are activation rows (ROWS)
-    // or output rows m (KGRP); B rows are output columns n.
-    auto load_tiles = [&](int kt) {
-        const int64_t k0 = k_begin + (int64_t)kt * BK;
-        if (MODE == MODE_ROWS) {
-            ta.load(p.A, p.lda, row0, row_hi, k0, k_end, tid);
-        } else {
-            ta.load(p.A, p.lda, row0, row_hi, k0, k_end, tid);
+    auto step = [&](auto stage_c, int kt) {
+        constexpr int S = decltype(stage_c)::value;
+        constexpr int NS = (S + 2) % kStages;
+        if (kt + 1 < nk) wait_vmcnt<kPerStage>(); else wait_vmcnt<0>();
+        stage_barrier();
+        const bool next = kt + 2 < nk;
+        const int64_t nrem = klen - (int64_t)(kt + 2) * BK;
+#pragma unroll
+        for (int kk = 0; kk < BK / 32; ++kk) {
+            bf16x8 af[4], bfg[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if constexpr (A_K) af[i] = lds_b128(abase[kk] + S * kABytes + i * 2048);
+                else af[i] = lds_tr_pair(abase[i] + S * kABytes + kk * 64 * BM, 8 * BM);
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                constexpr uint32_t so = (S & 1) * kBBytes;
+                if constexpr (B_K) bfg[j] = lds_b128(bbase[S >> 1][kk] + so + j * 2048);
+                else bfg[j] = lds_tr_pair(bbase[S >> 1][j] + so + kk * 64 * BN, 8 * BN);
+            }
+            // the next-but-one stage's copies go out between the MFMA blocks
+            if (next) {
+                if (kk == 0) {
+                    da.template issue<KTAIL, 0, kSA>(ldsA + NS * kABytes, nrem, wave);
+                    db.template issue<KTAIL, 0, kSB / 2>(ldsB + NS * kBBytes, nrem, wave);
+                } else {
+                    db.template issue<KTAIL, kSB / 2, kSB>(ldsB + NS * kBBytes, nrem, wave);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfg[j], af[i], acc[i][j], 0, 0, 0);
         }
-        tb.load(Bsrc, p.ldb, n0, (int64_t)p.N, k0, k_end, tid);
     };
 
     if (nk > 0) {
-        load_tiles(0);
-        ta.store(As0, tid);
-        tb.store(Bs0, tid);
-        __syncthreads();
-        for (int kt = 0; kt < nk; ++kt) {
-            const int cur = kt & 1;
-            if (kt + 1 < nk) load_tiles(kt + 1);
-            const char* As = As0 + cur * kBufBytes;
-            const char* Bs = Bs0 + cur * kBufBytes;
-#pragma unroll
-            for (int kk = 0; kk < BK / 32; ++kk) {
-                const int c = kk * 4 + (lane >> 4);
-                bf16x8 af[4], bfg[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int r = wm * 64 + i * 16 + (lane & 15);
-                    af[i] = *(const bf16x8*)(As + lds_off(r, c));
-                }
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int r = wn * 64 + j * 16 + (lane & 15);
-                    bfg[j] = *(const bf16x8*)(Bs + lds_off(r, c));
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfg[j], af[i], acc[i][j], 0, 0, 0);
-            }
-            if (kt + 1 < nk) {
-                ta.store(As0 + (cur ^ 1) * kBufBytes, tid);
-                tb.store(Bs0 + (cur ^ 1) * kBufBytes, tid);
-            }
-            __syncthreads();
+        da.template issue<KTAIL, 0, kSA>(ldsA, klen, wave);
+        db.template issue<KTAIL, 0, kSB>(ldsB, klen, wave);
+        if (nk > 1) {
+            da.template issue<KTAIL, 0, kSA>(ldsA + kABytes, klen - BK, wave);
+            db.template issue<KTAIL, 0, kSB>(ldsB + kBBytes, klen - BK, wave);
+        }
+        for (int kt = 0; kt < nk; kt += kStages) {
+            step(std::integral_constant<int, 0>{}, kt);
+            if (kt + 1 < nk) step(std::integral_constant<int, 1>{}, kt + 1);
+            if (kt + 2 < nk) step(std::integral_constant<int, 2>{}, kt + 2);
         }
     }
 
@@ -296,11 +374,11 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs p) {
             if (n >= p.N) continue;
             const f32x4 a = acc[i][j];
             const int64_t off = c_base + m * p.ldc + n;
-            if (EPI == EPI_F32) {
+            if constexpr (EPI == EPI_F32) {
                 *(float4*)((float*)p.C + off) = make_float4(a[0], a[1], a[2], a[3]);
-            } else if (EPI == EPI_BF16) {
+            } else if constexpr (EPI == EPI_BF16) {
                 *(uint2*)((uint16_t*)p.C + off) = make_uint2(pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]));
-            } else if (EPI == EPI_RELU2) {
+            } else if constexpr (EPI == EPI_RELU2) {
                 const float r0 = fmaxf(a[0], 0.f), r1 = fmaxf(a[1], 0.f);
                 const float r2 = fmaxf(a[2], 0.f), r3 = fmaxf(a[3], 0.f);
                 *(uint2*)((uint16_t*)p.C + off) =
@@ -350,8 +428,14 @@ template <int MODE, bool A_K, bool B_K, int EPI>
 static hipError_t launch(const GemmArgs& a, int64_t n_wg, hipStream_t st) {
     if (n_wg <= 0) return hipSuccess;
     if (n_wg > 0x7fffffff) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((gemm_kernel<MODE, A_K, B_K, EPI>), dim3((unsigned)n_wg), dim3(kGemmThreads), 0,
-                       st, a);
+    // ROWS mode contracts over a fixed width: a partial last k tile only when
+    // it is not a multiple of BK.  KGRP contracts over ragged expert rows.
+    if (MODE == MODE_KGRP || a.Kd % BK != 0)
+        hipLaunchKernelGGL((gemm_kernel<MODE, A_K, B_K, EPI, true>), dim3((unsigned)n_wg),
+                           dim3(kGemmThreads), 0, st, a);
+    else
+        hipLaunchKernelGGL((gemm_kernel<MODE, A_K, B_K, EPI, false>), dim3((unsigned)n_wg),
+                           dim3(kGemmThreads), 0, st, a);
     return hipGetLastError();
 }
 
