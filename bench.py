@@ -180,14 +180,14 @@ def main():
     st["dispatch"] = time_region(
         lambda i: _lib.moe_dispatch(x_r[i % len(x_r)], out["topk_prob"], out["inv_perm"], s.S, s.D,
                                     s.K, xd2, pd2), reps, stream)
-    sched = layer.grouped_schedule(out["offsets"], s.E)
+    sched = layer.grouped_schedule(out["offsets"], s.E, s.R)
     h2 = torch.empty_like(out["h"])
     yd2 = torch.empty_like(out["y_disp"])
     st["grouped_up"] = time_region(
-        lambda i: _lib.moe_grouped_gemm(out["x_disp"], out["offsets"], sched, s.E, s.R, s.D, s.F,
+        lambda i: _lib.moe_grouped_gemm(out["x_disp"], sched, s.E, s.R, s.D, s.F,
                                         sets[i % len(sets)]["W1"], 1, h2, None), reps, stream)
     st["grouped_down"] = time_region(
-        lambda i: _lib.moe_grouped_gemm(out["h"], out["offsets"], sched, s.E, s.R, s.F, s.D,
+        lambda i: _lib.moe_grouped_gemm(out["h"], sched, s.E, s.R, s.F, s.D,
                                         sets[i % len(sets)]["W2"], 0, yd2, None), reps, stream)
     y2 = torch.empty((s.S, s.D), dtype=torch.bfloat16, device=dev)
     st["combine"] = time_region(

@@ -146,21 +146,26 @@ int moe_grouped_ffn(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, i
 /* The two products of moe_grouped_ffn as separate launches (for callers that
  * schedule or time them individually).
  *
- * moe_grouped_schedule: sched[0] = 0, sched[e+1] = sched[e] + ceil(counts[e] /
- * 128), counts[e] = offsets[e+1] - offsets[e]: the per-expert 128-row tile
- * schedule the grouped GEMM reads on the device.  sched [E+1] int32. */
-int moe_grouped_schedule(const int32_t* offsets, int32_t E, int32_t* sched, hipStream_t stream);
+ * moe_grouped_schedule builds, on the device, the tile schedule the grouped
+ * GEMM reads for expert segments offsets[0..E] over R rows: per-expert counts
+ * of 128-row tiles (sched starts with mtile_start[E+1] int32: mtile_start[0] =
+ * 0, mtile_start[e+1] = mtile_start[e] + ceil(count[e] / 128)) followed by one
+ * entry per tile.  Segments are clamped to [0, R).  sched: device buffer of at
+ * least moe_grouped_schedule_bytes(E, R) bytes, 16-byte aligned. */
+size_t moe_grouped_schedule_bytes(int32_t E, int64_t R);
+int moe_grouped_schedule(const int32_t* offsets, int32_t E, int64_t R, void* sched, size_t sched_bytes,
+                         hipStream_t stream);
 
 /* One grouped GEMM over expert segments, one kernel launch:
- *   C[r, :] = epi( A[r, :] @ W[e] ),  r in [offsets[e], offsets[e+1])
+ *   C[r, :] = epi( A[r, :] @ W[e] ),  r in expert e's segment
  *   A [R, Kd] bf16;  W [E, Kd, N] bf16;  C [R, N] bf16;  sched from
- *   moe_grouped_schedule for the same offsets.
+ *   moe_grouped_schedule for the same offsets, E and R.
  *   epilogue 0: C = bf16(acc)                        (down projection)
  *   epilogue 1: C = bf16(max(acc,0)^2), u_save = bf16(acc) if u_save != NULL
  *                                                    (up projection)  */
-int moe_grouped_gemm(const moe_bf16* A, const int32_t* offsets, const int32_t* sched, int32_t E,
-                     int64_t R, int32_t Kd, int32_t N, const moe_bf16* W, int32_t epilogue,
-                     moe_bf16* C, moe_bf16* u_save, hipStream_t stream);
+int moe_grouped_gemm(const moe_bf16* A, const void* sched, int32_t E, int64_t R, int32_t Kd, int32_t N,
+                     const moe_bf16* W, int32_t epilogue, moe_bf16* C, moe_bf16* u_save,
+                     hipStream_t stream);
 
 /* ---------------------------------------------------------------------- */
 /* Combine: probability-weighted sum back to token order (the hidden       */

@@ -57,8 +57,9 @@ _PROTOS = {
     "moe_dispatch": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp, vp]),
     "moe_grouped_ffn_workspace_bytes": (sz, [i32, i64, i32, i32]),
     "moe_grouped_ffn": (C.c_int, [vp, vp, i32, i64, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
-    "moe_grouped_schedule": (C.c_int, [vp, i32, vp, vp]),
-    "moe_grouped_gemm": (C.c_int, [vp, vp, vp, i32, i64, i32, i32, vp, i32, vp, vp, vp]),
+    "moe_grouped_schedule_bytes": (sz, [i32, i64]),
+    "moe_grouped_schedule": (C.c_int, [vp, i32, i64, vp, sz, vp]),
+    "moe_grouped_gemm": (C.c_int, [vp, vp, i32, i64, i32, i32, vp, i32, vp, vp, vp]),
     "moe_combine": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp]),
     "moe_latent_proj": (C.c_int, [vp, vp, i64, i32, i32, vp, vp]),
     "moe_layer_fwd_workspace_bytes": (sz, [C.POINTER(LayerFwdArgs)]),
@@ -169,16 +170,20 @@ def moe_grouped_ffn(x_disp, offsets, E, R, D, F, W1, W2, h, u_save, y_disp, ws):
         0 if ws is None else ws.numel() * ws.element_size(), _stream()), "moe_grouped_ffn")
 
 
-def moe_grouped_schedule(offsets, E, sched):
-    _check(load().moe_grouped_schedule(_ptr(offsets, I32, "offsets"), E, _ptr(sched, I32, "sched"),
-                                       _stream()), "moe_grouped_schedule")
+def moe_grouped_schedule_bytes(E, R) -> int:
+    return load().moe_grouped_schedule_bytes(E, R)
 
 
-def moe_grouped_gemm(A, offsets, sched, E, R, Kd, N, W, epilogue, Cout, u_save):
-    _check(load().moe_grouped_gemm(_ptr(A, BF16, "A"), _ptr(offsets, I32, "offsets"),
-                                   _ptr(sched, I32, "sched"), E, R, Kd, N, _ptr(W, BF16, "W"),
-                                   epilogue, _ptr(Cout, BF16, "C"), _ptr(u_save, BF16, "u_save"),
-                                   _stream()), "moe_grouped_gemm")
+def moe_grouped_schedule(offsets, E, R, sched):
+    _check(load().moe_grouped_schedule(_ptr(offsets, I32, "offsets"), E, R, _ptr(sched, None, "sched"),
+                                       sched.numel() * sched.element_size(), _stream()),
+           "moe_grouped_schedule")
+
+
+def moe_grouped_gemm(A, sched, E, R, Kd, N, W, epilogue, Cout, u_save):
+    _check(load().moe_grouped_gemm(_ptr(A, BF16, "A"), _ptr(sched, None, "sched"), E, R, Kd, N,
+                                   _ptr(W, BF16, "W"), epilogue, _ptr(Cout, BF16, "C"),
+                                   _ptr(u_save, BF16, "u_save"), _stream()), "moe_grouped_gemm")
 
 
 def moe_combine(y_disp, p_disp, inv_perm, S, D, K, y):

@@ -141,7 +141,7 @@ int moe_combine(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_
 
 size_t moe_grouped_ffn_workspace_bytes(int32_t E, int64_t R, int32_t D, int32_t F) {
     if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(D) || !dim_ok(F)) return 0;
-    return moe::gemm_schedule_bytes(E);
+    return moe::gemm_schedule_bytes(E, R);
 }
 
 static int check_ffn(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, int64_t R, int32_t D,
@@ -161,42 +161,48 @@ int moe_grouped_ffn(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, i
     MOE_TRY(need(h, (uint64_t)R * F * 2, 16));
     MOE_TRY(opt(u_save, 16));
     MOE_TRY(need(y_disp, (uint64_t)R * D * 2, 16));
-    const size_t wsn = moe::gemm_schedule_bytes(E);
+    const size_t wsn = moe::gemm_schedule_bytes(E, R);
     if (ws == nullptr || ws_bytes < wsn) return MOE_ERR_WORKSPACE;
     MOE_TRY(opt(ws, 16));
     if (R == 0) return MOE_OK;
-    int32_t* mts = (int32_t*)ws;
-    MOE_HIP(moe::launch_tile_schedule(offsets, E, mts, stream));
+    MOE_HIP(moe::launch_tile_schedule(offsets, E, R, ws, stream));
     MOE_HIP(moe::launch_grouped_rows(x_disp, D, W1, F, (int64_t)D * F, false, h, F, moe::EPI_RELU2,
-                                     nullptr, u_save, offsets, mts, E, R, F, D, stream));
+                                     nullptr, u_save, ws, E, R, F, D, stream));
     MOE_HIP(moe::launch_grouped_rows(h, F, W2, D, (int64_t)F * D, false, y_disp, D, moe::EPI_BF16,
-                                     nullptr, nullptr, offsets, mts, E, R, D, F, stream));
+                                     nullptr, nullptr, ws, E, R, D, F, stream));
     return MOE_OK;
 }
 
-int moe_grouped_schedule(const int32_t* offsets, int32_t E, int32_t* sched, hipStream_t stream) {
-    if (E < 1 || E > kMaxE) return MOE_ERR_SHAPE;
-    MOE_TRY(need(offsets, (uint64_t)(E + 1) * 4, 4));
-    MOE_TRY(need(sched, (uint64_t)(E + 1) * 4, 4));
-    return hip_status(moe::launch_tile_schedule(offsets, E, sched, stream));
+size_t moe_grouped_schedule_bytes(int32_t E, int64_t R) {
+    if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows) return 0;
+    return moe::gemm_schedule_bytes(E, R);
 }
 
-int moe_grouped_gemm(const moe_bf16* A, const int32_t* offsets, const int32_t* sched, int32_t E,
-                     int64_t R, int32_t Kd, int32_t N, const moe_bf16* W, int32_t epilogue,
-                     moe_bf16* C, moe_bf16* u_save, hipStream_t stream) {
+int moe_grouped_schedule(const int32_t* offsets, int32_t E, int64_t R, void* sched, size_t sched_bytes,
+                         hipStream_t stream) {
+    if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows) return MOE_ERR_SHAPE;
+    MOE_TRY(need(offsets, (uint64_t)(E + 1) * 4, 4));
+    if (sched == nullptr || sched_bytes < moe::gemm_schedule_bytes(E, R)) return MOE_ERR_WORKSPACE;
+    MOE_TRY(opt(sched, 16));
+    return hip_status(moe::launch_tile_schedule(offsets, E, R, sched, stream));
+}
+
+int moe_grouped_gemm(const moe_bf16* A, const void* sched, int32_t E, int64_t R, int32_t Kd, int32_t N,
+                     const moe_bf16* W, int32_t epilogue, moe_bf16* C, moe_bf16* u_save,
+                     hipStream_t stream) {
     if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(Kd) || !dim_ok(N)) return MOE_ERR_SHAPE;
     if (epilogue != 0 && epilogue != 1) return MOE_ERR_UNSUPPORTED;
     if (epilogue == 0 && u_save != nullptr) return MOE_ERR_SHAPE;
     MOE_TRY(need(A, (uint64_t)R * Kd * 2, 16));
-    MOE_TRY(need(offsets, (uint64_t)(E + 1) * 4, 4));
-    MOE_TRY(need(sched, (uint64_t)(E + 1) * 4, 4));
+    if (sched == nullptr) return MOE_ERR_NULL;
+    MOE_TRY(opt(sched, 16));
     MOE_TRY(need(W, (uint64_t)E * Kd * N * 2, 16));
     MOE_TRY(need(C, (uint64_t)R * N * 2, 16));
     MOE_TRY(opt(u_save, 16));
     if (R == 0) return MOE_OK;
     return hip_status(moe::launch_grouped_rows(A, Kd, W, N, (int64_t)Kd * N, false, C, N,
                                                epilogue == 1 ? moe::EPI_RELU2 : moe::EPI_BF16, nullptr,
-                                               u_save, offsets, sched, E, R, N, Kd, stream));
+                                               u_save, sched, E, R, N, Kd, stream));
 }
 
 int moe_latent_proj(const moe_bf16* A, const moe_bf16* W, int64_t M, int32_t Kd, int32_t N, moe_bf16* C,
@@ -206,7 +212,7 @@ int moe_latent_proj(const moe_bf16* A, const moe_bf16* W, int64_t M, int32_t Kd,
     MOE_TRY(need(W, (uint64_t)Kd * N * 2, 16));
     MOE_TRY(need(C, (uint64_t)M * N * 2, 16));
     return hip_status(moe::launch_grouped_rows(A, Kd, W, N, 0, false, C, N, moe::EPI_BF16, nullptr,
-                                               nullptr, nullptr, nullptr, 1, M, N, Kd, stream));
+                                               nullptr, nullptr, 1, M, N, Kd, stream));
 }
 
 // ---------------------------------------------------------------------------
@@ -239,7 +245,7 @@ int check_layer_args(const moe_layer_fwd_args* a) {
 struct LayerBufs {
     moe_bf16* x_lat; float* logits; int32_t* topk_idx; float* topk_prob; int32_t* counts;
     int32_t* offsets; int32_t* perm; int32_t* inv_perm; moe_bf16* x_disp; float* p_disp;
-    moe_bf16* h; moe_bf16* y_disp; moe_bf16* y_lat; void* route_ws; int32_t* mtile_start;
+    moe_bf16* h; moe_bf16* y_disp; moe_bf16* y_lat; void* route_ws; void* sched;
 };
 
 size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
@@ -264,7 +270,7 @@ size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
     b->y_disp = pick(a->y_disp, (size_t)R * D * 2);
     b->y_lat = a->H ? pick(a->y_lat, (size_t)S * D * 2) : nullptr;
     b->route_ws = c.take(moe::route_ws_bytes(S, E));
-    b->mtile_start = (int32_t*)c.take(moe::gemm_schedule_bytes(E));
+    b->sched = c.take(moe::gemm_schedule_bytes(E, R));
     return c.used;
 }
 
@@ -308,7 +314,7 @@ int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
     const moe_bf16* x_r = a->x;
     if (H) {
         MOE_HIP(moe::launch_grouped_rows(a->x, H, a->Wdown, D, 0, false, b.x_lat, D, moe::EPI_BF16,
-                                         nullptr, nullptr, nullptr, nullptr, 1, S, D, H, stream));
+                                         nullptr, nullptr, nullptr, 1, S, D, H, stream));
         x_r = b.x_lat;
     }
     MOE_HIP(moe::launch_router_logits(x_r, a->Wr, a->router_bias, S, D, E, b.logits, stream));
@@ -316,19 +322,17 @@ int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
                               b.inv_perm, b.route_ws, stream));
     MOE_HIP(moe::launch_dispatch(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_disp, b.p_disp, stream));
     if (R > 0) {
-        MOE_HIP(moe::launch_tile_schedule(b.offsets, E, b.mtile_start, stream));
+        MOE_HIP(moe::launch_tile_schedule(b.offsets, E, R, b.sched, stream));
         MOE_HIP(moe::launch_grouped_rows(b.x_disp, D, a->W1, F, (int64_t)D * F, false, b.h, F,
-                                         moe::EPI_RELU2, nullptr, a->u_save, b.offsets, b.mtile_start,
-                                         E, R, F, D, stream));
+                                         moe::EPI_RELU2, nullptr, a->u_save, b.sched, E, R, F, D, stream));
         MOE_HIP(moe::launch_grouped_rows(b.h, F, a->W2, D, (int64_t)F * D, false, b.y_disp, D,
-                                         moe::EPI_BF16, nullptr, nullptr, b.offsets, b.mtile_start, E,
-                                         R, D, F, stream));
+                                         moe::EPI_BF16, nullptr, nullptr, b.sched, E, R, D, F, stream));
     }
     moe_bf16* comb_out = H ? b.y_lat : a->y;
     MOE_HIP(moe::launch_combine(b.y_disp, b.p_disp, b.inv_perm, S, D, K, comb_out, stream));
     if (H) {
         MOE_HIP(moe::launch_grouped_rows(b.y_lat, D, a->Wup, H, 0, false, a->y, H, moe::EPI_BF16,
-                                         nullptr, nullptr, nullptr, nullptr, 1, S, H, D, stream));
+                                         nullptr, nullptr, nullptr, 1, S, H, D, stream));
     }
     return MOE_OK;
 }
@@ -353,7 +357,7 @@ int moe_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const float* p_d
 
 size_t moe_grouped_ffn_bwd_workspace_bytes(int32_t E, int64_t R, int32_t D, int32_t F) {
     if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(D) || !dim_ok(F)) return 0;
-    return align256((size_t)R * F * 2) + moe::gemm_schedule_bytes(E);
+    return align256((size_t)R * F * 2) + moe::gemm_schedule_bytes(E, R);
 }
 
 int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const moe_bf16* h,
@@ -368,19 +372,19 @@ int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const mo
     MOE_TRY(need(dW1, (uint64_t)E * D * F * 4, 16));
     MOE_TRY(need(dW2, (uint64_t)E * F * D * 4, 16));
     const size_t du_bytes = align256((size_t)R * F * 2);
-    const size_t wsn = du_bytes + moe::gemm_schedule_bytes(E);
+    const size_t wsn = du_bytes + moe::gemm_schedule_bytes(E, R);
     if (ws == nullptr || ws_bytes < wsn) return MOE_ERR_WORKSPACE;
     MOE_TRY(opt(ws, 256));
     moe_bf16* du = (moe_bf16*)ws;
-    int32_t* mts = (int32_t*)((char*)ws + du_bytes);
+    void* sched = (char*)ws + du_bytes;
     if (R > 0) {
-        MOE_HIP(moe::launch_tile_schedule(offsets, E, mts, stream));
+        MOE_HIP(moe::launch_tile_schedule(offsets, E, R, sched, stream));
         // du = (dy_disp @ W2[e]^T) * 2 max(u, 0): W2[e] is [F, D], read K(=D)-contiguous
         MOE_HIP(moe::launch_grouped_rows(dy_disp, D, W2, D, (int64_t)F * D, true, du, F, moe::EPI_DRELU2,
-                                         u_save, nullptr, offsets, mts, E, R, F, D, stream));
+                                         u_save, nullptr, sched, E, R, F, D, stream));
         // dx_disp = du @ W1[e]^T: W1[e] is [D, F], read K(=F)-contiguous
         MOE_HIP(moe::launch_grouped_rows(du, F, W1, F, (int64_t)D * F, true, dx_disp, D, moe::EPI_BF16,
-                                         nullptr, nullptr, offsets, mts, E, R, D, F, stream));
+                                         nullptr, nullptr, sched, E, R, D, F, stream));
     }
     // dW2[e] = h_e^T @ dy_disp_e  ([F, D]);  dW1[e] = x_disp_e^T @ du_e  ([D, F])
     MOE_HIP(moe::launch_grouped_wgrad(h, F, dy_disp, D, dW2, D, (int64_t)F * D, offsets, E, F, D,

@@ -39,8 +39,9 @@
 // fusing squared-ReLU (up), its derivative (dgrad) or nothing.
 //
 // Workgroups of an expert segment are located through a device-side tile
-// schedule (prefix sum of per-expert 128-row tile counts): no host reads the
-// routing counts.  Workgroup ids are remapped so that consecutive tiles run
+// table (expert, first row, end row of every 128-row tile, built from the
+// routing offsets on the device): no host reads the routing counts, and a
+// workgroup finds its rows with one 16-byte load.  Workgroup ids are remapped so that consecutive tiles run
 // on the same XCD and share its L2, and tiles are grouped 8 m-tiles at a time.
 #include <type_traits>
 
@@ -75,8 +76,8 @@ struct GemmArgs {
     void* C;
     const uint16_t* aux_in;   // EPI_DRELU2: pre-activation u, same layout as C
     uint16_t* aux_out;        // EPI_RELU2: pre-activation u (may be null)
-    const int32_t* offsets;   // [E+1] expert row segments; null = one dense segment
-    const int32_t* mtile_start;  // [E+1] ROWS mode with offsets
+    const int32_t* offsets;   // [E+1] expert row segments (KGRP mode)
+    const int4* tiles;        // ROWS mode: per 128-row tile {expert, row0, row_end, 0}; null = dense
     int64_t lda, ldb, ldc;
     int64_t b_stride;         // elements between experts' B (ROWS mode)
     int64_t c_stride;         // elements between experts' C (KGRP mode)
@@ -239,19 +240,12 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(GemmArgs p) {
         const int in = lid - group * width;
         mt = first_m + in % gsz;
         nt = in / gsz;
-        if (p.offsets != nullptr) {
-            if (mt >= p.mtile_start[p.E]) return;
-            int lo = 0, hi = p.E;  // last e with mtile_start[e] <= mt
-            while (hi - lo > 1) {
-                const int mid = (lo + hi) >> 1;
-                if (p.mtile_start[mid] <= mt) lo = mid; else hi = mid;
-            }
-            e = lo;
-            row0 = (int64_t)p.offsets[e] + (int64_t)(mt - p.mtile_start[e]) * BM;
-            if (row0 < 0 || row0 >= p.R) return;
-            int64_t seg_end = p.offsets[e + 1];
-            if (seg_end > p.R) seg_end = p.R;
-            row_hi = (row0 + BM) < seg_end ? (row0 + BM) : seg_end;
+        if (p.tiles != nullptr) {
+            const int4 ti = p.tiles[mt];  // one uniform 16-byte load: expert and rows
+            if (ti.x < 0) return;
+            e = ti.x;
+            row0 = ti.y;
+            row_hi = ti.z;
         } else {
             row0 = (int64_t)mt * BM;
             if (row0 >= p.M) return;
@@ -397,12 +391,28 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(GemmArgs p) {
     }
 }
 
-// mtile_start[0] = 0, mtile_start[e+1] = sum_{e' <= e} ceil(count[e'] / BM).
+// Device-side tile schedule of the grouped GEMM for expert segments
+// offsets[0..E] (clamped to [0, R)):
+//   mtile_start[0] = 0, mtile_start[e+1] = sum_{e' <= e} ceil(count[e'] / BM)
+//   tiles[mt] = {e, row0, row_end, 0} for every 128-row tile mt of expert e,
+//               {-1, 0, 0, 0} for mt in [total, max_tiles) (the static grid bound).
 __global__ __launch_bounds__(1024) void tile_schedule_kernel(const int32_t* __restrict__ offsets, int E,
-                                                              int32_t* __restrict__ mtile_start) {
+                                                              int R, int max_tiles,
+                                                              int32_t* __restrict__ mtile_start,
+                                                              int4* __restrict__ tiles) {
     __shared__ int32_t s[1024];
+    __shared__ int32_t seg_lo[1024], seg_hi[1024];
     const int tid = threadIdx.x;
-    s[tid] = tid < E ? (offsets[tid + 1] - offsets[tid] + BM - 1) / BM : 0;
+    int lo = 0, hi = 0;
+    if (tid < E) {
+        lo = offsets[tid];
+        hi = offsets[tid + 1];
+        lo = lo < 0 ? 0 : (lo > R ? R : lo);
+        hi = hi < lo ? lo : (hi > R ? R : hi);
+    }
+    seg_lo[tid] = lo;
+    seg_hi[tid] = hi;
+    s[tid] = (hi - lo + BM - 1) / BM;
     __syncthreads();
     for (int d = 1; d < 1024; d <<= 1) {
         const int add = tid >= d ? s[tid - d] : 0;
@@ -412,16 +422,36 @@ __global__ __launch_bounds__(1024) void tile_schedule_kernel(const int32_t* __re
     }
     if (tid < E) mtile_start[tid + 1] = s[tid];
     if (tid == 0) mtile_start[0] = 0;
+    const int total = s[E - 1];
+    for (int mt = tid; mt < max_tiles; mt += 1024) {
+        int4 v = make_int4(-1, 0, 0, 0);
+        if (mt < total) {
+            int a = 0, b = E - 1;  // first e with s[e] > mt
+            while (a < b) {
+                const int m = (a + b) >> 1;
+                if (s[m] > mt) b = m; else a = m + 1;
+            }
+            const int row0 = seg_lo[a] + (mt - (a ? s[a - 1] : 0)) * BM;
+            const int row_end = row0 + BM < seg_hi[a] ? row0 + BM : seg_hi[a];
+            v = make_int4(a, row0, row_end, 0);
+        }
+        tiles[mt] = v;
+    }
 }
 
 int gemm_tile_m() { return BM; }
-
-size_t gemm_schedule_bytes(int E) { return (size_t)((E + 1) * 4 + 255) / 256 * 256; }
 
 static int64_t mtiles_bound(int64_t R, int E) {
     // sum_e ceil(c_e / BM) <= ceil(R / BM) + (number of non-empty experts)
     const int64_t nonempty = R < E ? R : E;
     return (R + BM - 1) / BM + nonempty;
+}
+
+// Schedule buffer: mtile_start [E+1] int32, then (16-byte aligned) the tile table.
+static size_t sched_table_offset(int E) { return (size_t)((E + 1) * 4 + 15) / 16 * 16; }
+
+size_t gemm_schedule_bytes(int E, int64_t R) {
+    return (sched_table_offset(E) + (size_t)mtiles_bound(R, E) * 16 + 255) / 256 * 256;
 }
 
 template <int MODE, bool A_K, bool B_K, int EPI>
@@ -439,23 +469,24 @@ static hipError_t launch(const GemmArgs& a, int64_t n_wg, hipStream_t st) {
     return hipGetLastError();
 }
 
-hipError_t launch_tile_schedule(const int32_t* offsets, int E, int32_t* mtile_start, hipStream_t st) {
-    hipLaunchKernelGGL(tile_schedule_kernel, dim3(1), dim3(1024), 0, st, offsets, E, mtile_start);
+hipError_t launch_tile_schedule(const int32_t* offsets, int E, int64_t R, void* sched, hipStream_t st) {
+    const int max_tiles = (int)mtiles_bound(R, E);
+    hipLaunchKernelGGL(tile_schedule_kernel, dim3(1), dim3(1024), 0, st, offsets, E, (int)R, max_tiles,
+                       (int32_t*)sched, (int4*)((char*)sched + sched_table_offset(E)));
     return hipGetLastError();
 }
 
 hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
                                int64_t b_stride, bool b_kmajor, void* C, int64_t ldc, int epi,
-                               const moe_bf16* aux_in, moe_bf16* aux_out, const int32_t* offsets,
-                               const int32_t* mtile_start, int E, int64_t R, int N, int Kd,
-                               hipStream_t st) {
+                               const moe_bf16* aux_in, moe_bf16* aux_out, const void* sched,
+                               int E, int64_t R, int N, int Kd, hipStream_t st) {
     GemmArgs a{};
     a.A = A; a.B = B; a.C = C; a.aux_in = aux_in; a.aux_out = aux_out;
-    a.offsets = offsets; a.mtile_start = mtile_start;
+    a.tiles = sched ? (const int4*)((const char*)sched + sched_table_offset(E)) : nullptr;
     a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.b_stride = b_stride;
     a.M = R; a.R = R; a.N = N; a.Kd = Kd; a.E = E;
     a.n_tiles = (N + BN - 1) / BN;
-    a.m_tiles = (int)(offsets ? mtiles_bound(R, E) : (R + BM - 1) / BM);
+    a.m_tiles = (int)(sched ? mtiles_bound(R, E) : (R + BM - 1) / BM);
     const int64_t n_wg = (int64_t)a.m_tiles * a.n_tiles;
     if (R == 0) return hipSuccess;
     if (!b_kmajor) {

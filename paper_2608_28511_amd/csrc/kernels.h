@@ -28,15 +28,16 @@ hipError_t launch_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const 
                               float* dp, hipStream_t st);
 
 int gemm_tile_m();
-size_t gemm_schedule_bytes(int E);
-hipError_t launch_tile_schedule(const int32_t* offsets, int E, int32_t* mtile_start, hipStream_t st);
-// ROWS mode: C[r, :] = A[r, :] @ B_e (per expert segment) or dense when offsets == nullptr.
+// Schedule buffer of the grouped GEMM: mtile_start [E+1] then the per-tile table.
+size_t gemm_schedule_bytes(int E, int64_t R);
+hipError_t launch_tile_schedule(const int32_t* offsets, int E, int64_t R, void* sched, hipStream_t st);
+// ROWS mode: C[r, :] = A[r, :] @ B_e per expert segment (sched from launch_tile_schedule
+// for the same offsets, E and R), or dense over R rows when sched == nullptr.
 // b_kmajor: B_e stored [N, Kd] (product with its transpose) instead of [Kd, N].
 hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
                                int64_t b_stride, bool b_kmajor, void* C, int64_t ldc, int epi,
-                               const moe_bf16* aux_in, moe_bf16* aux_out, const int32_t* offsets,
-                               const int32_t* mtile_start, int E, int64_t R, int N, int Kd,
-                               hipStream_t st);
+                               const moe_bf16* aux_in, moe_bf16* aux_out, const void* sched,
+                               int E, int64_t R, int N, int Kd, hipStream_t st);
 // KGRP mode: C_e[m, n] = sum over expert e's rows r of A[r, m] * B[r, n]  (fp32 out).
 hipError_t launch_grouped_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
                                 float* C, int64_t ldc, int64_t c_stride, const int32_t* offsets,

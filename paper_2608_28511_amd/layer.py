@@ -62,18 +62,19 @@ def grouped_ffn(x_disp: torch.Tensor, offsets: torch.Tensor, W1: torch.Tensor, W
     return h, u, y_disp
 
 
-def grouped_schedule(offsets: torch.Tensor, E: int):
-    sched = _empty((E + 1,), I32, offsets.device)
-    L.moe_grouped_schedule(offsets, E, sched)
+def grouped_schedule(offsets: torch.Tensor, E: int, R: int) -> torch.Tensor:
+    """Device tile schedule; its first E+1 int32 are the per-expert tile starts."""
+    sched = _empty((L.moe_grouped_schedule_bytes(E, R) // 4,), I32, offsets.device)
+    L.moe_grouped_schedule(offsets, E, R, sched)
     return sched
 
 
-def grouped_gemm(A: torch.Tensor, offsets: torch.Tensor, sched: torch.Tensor, W: torch.Tensor,
-                 epilogue: int, out: Optional[torch.Tensor] = None, u_save: Optional[torch.Tensor] = None):
+def grouped_gemm(A: torch.Tensor, sched: torch.Tensor, W: torch.Tensor, epilogue: int,
+                 out: Optional[torch.Tensor] = None, u_save: Optional[torch.Tensor] = None):
     R, Kd = A.shape
     E, _, N = W.shape
     C = out if out is not None else _empty((R, N), BF16, A.device)
-    L.moe_grouped_gemm(A, offsets, sched, E, R, Kd, N, W, epilogue, C, u_save)
+    L.moe_grouped_gemm(A, sched, E, R, Kd, N, W, epilogue, C, u_save)
     return C
 
 

@@ -57,6 +57,9 @@ def test_workspace_queries(lib):
     assert lib.moe_grouped_ffn_workspace_bytes(64, 49152, 2048, 1024) > 0
     assert lib.moe_grouped_ffn_workspace_bytes(64, 49152, 2044, 1024) == 0   # D % 8
     assert lib.moe_grouped_ffn_bwd_workspace_bytes(8, 100, 64, 64) >= 100 * 64 * 2
+    # schedule: E+1 tile starts plus one 16-byte entry per possible 128-row tile
+    assert lib.moe_grouped_schedule_bytes(64, 49152) >= 65 * 4 + (384 + 64) * 16
+    assert lib.moe_grouped_schedule_bytes(0, 10) == 0
 
 
 def test_layer_struct_layout_matches(lib):
@@ -93,6 +96,9 @@ def test_validation_errors_return_before_launch(lib):
     assert lib.moe_grouped_ffn(FAKE, FAKE, 2, 4, 16, 16, FAKE, FAKE, FAKE, None, FAKE, FAKE, 0, st) == -4
     assert lib.moe_grouped_ffn(FAKE, FAKE, 2, 4, 16, 16, FAKE, FAKE, FAKE, ODD, FAKE, FAKE, 4096, st) == -3
     assert lib.moe_latent_proj(FAKE, FAKE, 4, 20, 16, FAKE, st) == -2
+    assert lib.moe_grouped_schedule(FAKE, 4, 100, FAKE, 16, st) == -4
+    assert lib.moe_grouped_gemm(FAKE, None, 2, 4, 16, 16, FAKE, 1, FAKE, None, st) == -1
+    assert lib.moe_grouped_gemm(FAKE, FAKE, 2, 4, 16, 16, FAKE, 2, FAKE, None, st) == -6
     assert lib.moe_router_logits(FAKE, FAKE, None, 4, 16, 0, FAKE, st) == -2
     assert lib.moe_router_logits(FAKE, FAKE, ODD, 4, 16, 4, FAKE, st) == -3
     assert lib.moe_combine_bwd(FAKE, FAKE, None, FAKE, 4, 16, 33, FAKE, None, st) == -2

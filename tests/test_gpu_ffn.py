@@ -117,11 +117,11 @@ def test_grouped_gemm_single_launches_match_ffn(R, D, F, E, empty, skew):
     W1 = (torch.randn((E, D, F), generator=g) / np.sqrt(D)).to(torch.bfloat16).to(DEV)
     W2 = (torch.randn((E, F, D), generator=g) / np.sqrt(F)).to(torch.bfloat16).to(DEV)
     h, u, yd = layer.grouped_ffn(x, off, W1, W2, save_u=True)
-    sched = layer.grouped_schedule(off, E)
+    sched = layer.grouped_schedule(off, E, R)
     u2 = torch.empty_like(u)
-    h2 = layer.grouped_gemm(x, off, sched, W1, 1, u_save=u2)
-    y2 = layer.grouped_gemm(h2, off, sched, W2, 0)
+    h2 = layer.grouped_gemm(x, sched, W1, 1, u_save=u2)
+    y2 = layer.grouped_gemm(h2, sched, W2, 0)
     torch.cuda.synchronize()
     counts = np.diff(npi(off))
-    assert np.array_equal(np.diff(npi(sched)), (counts + 127) // 128)
+    assert np.array_equal(np.diff(npi(sched[: E + 1])), (counts + 127) // 128)
     assert torch.equal(h, h2) and torch.equal(u, u2) and torch.equal(yd, y2)
