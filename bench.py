@@ -44,11 +44,97 @@ def parse():
     p.add_argument("--workload", default="base_s8192_d2048_e64_k6")
     p.add_argument("--sets", type=int, default=3, help="rotating input sets")
     p.add_argument("--stage-reps", type=int, default=20)
-    p.add_argument("--cpu-tokens", type=int, default=1024)
+    p.add_argument("--cpu-tokens", type=int, default=3072,
+                   help="tokens of the batch the CPU oracle runs (about 10-30 s on 16 cores)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--calib-bytes", type=int, default=1 << 30,
                    help="size of the plain copy run once for counter calibration")
+    p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="summarise two rocprofv3 counter passes into profiles/ and exit")
+    p.add_argument("--traffic-kernel", default="grouped_down", choices=sorted(KERNEL_NAME))
     return p.parse_args()
+
+
+# ---- HBM traffic of the dominant kernel, from hardware counters ----------------
+# Two profiler passes of this same command, one per counter:
+#   rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir_fetch> -o p -- python bench.py --no-cpu-baseline
+#   rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir_write> -o p -- python bench.py --no-cpu-baseline
+# then `python bench.py --traffic-from <dir_fetch> <dir_write>` writes the summary
+# profiles/traffic_<kernel>_<workload>.txt.  Each counter (KiB per dispatch) is
+# scaled by what it reads for the plain 1 GiB device copy this script runs at
+# start-up (a copy reads and writes exactly 1 GiB).  The summary records a
+# digest of the GEMM sources; once they change, `traffic` is reported as null.
+GEMM_SOURCES = ("gemm.hip", "kernels.h", "common.h")
+KERNEL_NAME = {"grouped_up": "gemm_kernel<0, true, false, 1, false>",
+               "grouped_down": "gemm_kernel<0, true, false, 0, false>"}
+
+
+def gemm_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        h.update((ROOT / "paper_2608_28511_amd" / "csrc" / f).read_bytes())
+    return h.hexdigest()
+
+
+def traffic_path(kernel, workload):
+    return ROOT / "profiles" / f"traffic_{kernel}_{workload}.txt"
+
+
+def load_traffic(kernel, workload):
+    p = traffic_path(kernel, workload)
+    if not p.exists():
+        return None
+    rec = json.loads(p.read_text().split("\n", 1)[1])
+    if rec.get("gemm_sources_sha256") != gemm_digest():
+        log(f"{p.name}: GEMM sources changed since the counters were taken; traffic null")
+        return None
+    return rec["bytes_per_launch"]
+
+
+def counter_rows(d):
+    import csv
+    files = sorted(Path(d).rglob("*counter_collection.csv"))
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    rows = []
+    for f in files:
+        rows += list(csv.DictReader(open(f)))
+    return rows
+
+
+def per_dispatch(rows, counter, match):
+    vals = {}
+    for r in rows:
+        if r["Counter_Name"] == counter and match(r["Kernel_Name"]):
+            vals[r["Dispatch_Id"]] = vals.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    return list(vals.values())
+
+
+def write_traffic(d_fetch, d_write, workload, kernel, calib_bytes):
+    out = {"kernel": kernel, "kernel_symbol": KERNEL_NAME[kernel], "workload": workload,
+           "gemm_sources_sha256": gemm_digest()}
+    total = 0.0
+    for d, counter in ((d_fetch, "FETCH_SIZE"), (d_write, "WRITE_SIZE")):
+        rows = counter_rows(d)
+        cal = per_dispatch(rows, counter, lambda n: "copyBuffer" in n)
+        if not cal:
+            raise SystemExit(f"{d}: no device copy dispatch to calibrate {counter}")
+        factor = calib_bytes / (max(cal) * 1024.0)
+        ks = per_dispatch(rows, counter, lambda n: KERNEL_NAME[kernel] in n)
+        if not ks:
+            raise SystemExit(f"{d}: no {KERNEL_NAME[kernel]} dispatches")
+        kib = sum(ks) / len(ks)
+        out[counter] = {"kib_per_dispatch": round(kib, 1), "dispatches": len(ks),
+                        "copy_kib": round(max(cal), 1), "factor": round(factor, 4),
+                        "bytes": round(kib * 1024.0 * factor)}
+        total += kib * 1024.0 * factor
+    out["bytes_per_launch"] = round(total)
+    p = traffic_path(kernel, workload)
+    p.write_text(f"HBM traffic of {kernel} on {workload} from rocprofv3 FETCH_SIZE / WRITE_SIZE "
+                 f"passes of `python bench.py --no-cpu-baseline --workload {workload}`, scaled by "
+                 f"a 1 GiB device copy (see bench.py)\n" + json.dumps(out, indent=1) + "\n")
+    print(p.read_text())
 
 
 def stage_bytes(s):
@@ -115,6 +201,9 @@ def cpu_baseline(s, inp, tokens):
 
 def main():
     args = parse()
+    if args.traffic_from:
+        write_traffic(*args.traffic_from, args.workload, args.traffic_kernel, args.calib_bytes)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
               f"(--gpus {args.gpus} requested).", file=sys.stderr)
@@ -219,7 +308,7 @@ def main():
     achieved = gemm_flops / st[dom] / 1e12
     roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": None,
+                "traffic": load_traffic(dom, s.name),
                 "per_launch": f"2*R*D*F = {gemm_flops:.4g} flop per launch (R = S*K = {s.R})"}
 
     cpu = None

@@ -34,15 +34,28 @@
 // zero chunk instead, so partial tiles need no special path.
 //
 // The MFMA takes the weight-side fragment as its first operand, so each
-// lane's four accumulators hold four consecutive output columns of one row:
-// the epilogue stores 8 bytes (bf16) or 16 bytes (fp32) per lane, after
-// fusing squared-ReLU (up), its derivative (dgrad) or nothing.
+// lane's four accumulators hold four consecutive output columns of one row.
 //
-// Workgroups of an expert segment are located through a device-side tile
-// table (expert, first row, end row of every 128-row tile, built from the
-// routing offsets on the device): no host reads the routing counts, and a
-// workgroup finds its rows with one 16-byte load.  Workgroup ids are remapped so that consecutive tiles run
-// on the same XCD and share its L2, and tiles are grouped 8 m-tiles at a time.
+// ROWS mode runs persistently: one workgroup per CU walks its share of the
+// output tiles, and the DMA ring runs over the flattened sequence of (tile,
+// k step) pairs, so the first two k steps of a workgroup's next tile are
+// already loading while it finishes the current one.  Output tiles are
+// written through a 16 KB LDS slice (16 x 64 bf16 per wave) so that every
+// store is 16 contiguous bytes and one store instruction covers 8 whole
+// 128-byte rows; stores go through a range-checked buffer descriptor, so
+// rows past the tile's end and columns past N are dropped by the hardware.
+// Squared-ReLU (up projection) is fused there; the dgrad epilogue that
+// multiplies by the activation derivative reads the saved pre-activation
+// directly.
+//
+// Expert segments are located through a device-side tile table (expert,
+// first row, end row of every 128-row tile, built from the routing offsets
+// on the device): no host reads the routing counts.  Work item w of the
+// grid-wide order is tile (m, n) of an ordering that takes 8 m-tiles at a
+// time across all n-tiles, and the items a round of workgroups processes
+// together on one XCD are consecutive, so they share A rows and expert
+// weights in that XCD's L2.
+#include <mutex>
 #include <type_traits>
 
 #include "common.h"
@@ -57,10 +70,11 @@ constexpr int kStages = 3;
 constexpr int kABytes = BM * BK * 2;            // 16 KB
 constexpr int kBBytes = BN * BK * 2;            // 32 KB
 constexpr int kStageBytes = kABytes + kBBytes;  // 48 KB
+constexpr int kRingBytes = kStages * kStageBytes;  // 144 KB
+constexpr int kEpiWaveBytes = 16 * 64 * 2;      // 16 x 64 bf16 staging block per wave
+constexpr int kEpiBytes = kWaves * kEpiWaveBytes;  // 16 KB
 constexpr int kGroupM = 8;
 constexpr int kXcds = 8;
-
-enum { MODE_ROWS = 0, MODE_KGRP = 1 };
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef short v8i16 __attribute__((ext_vector_type(8)));
@@ -78,6 +92,7 @@ struct GemmArgs {
     uint16_t* aux_out;        // EPI_RELU2: pre-activation u (may be null)
     const int32_t* offsets;   // [E+1] expert row segments (KGRP mode)
     const int4* tiles;        // ROWS mode: per 128-row tile {expert, row0, row_end, 0}; null = dense
+    const int32_t* mtile_total;  // ROWS mode with tiles: device count of valid m-tiles
     int64_t lda, ldb, ldc;
     int64_t b_stride;         // elements between experts' B (ROWS mode)
     int64_t c_stride;         // elements between experts' C (KGRP mode)
@@ -88,10 +103,13 @@ struct GemmArgs {
 };
 
 // ---- row layout: [rows][64 k], 8 chunks per row; chunk c of row r stored at
-// c ^ rswz(r).  rswz has period 16 in r, so the fragments of rows r and r + 16
-// sit a constant 2 KB apart (an immediate offset); within any 16 consecutive
-// rows the 16-byte reads of one ds_read_b128 hit distinct banks.
-__device__ __forceinline__ int rswz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+// c ^ (r & 7).  The fragments of rows r and r + 16 then sit a constant 2 KB
+// apart (an immediate offset).  A ds_read_b128 of 16 consecutive rows is
+// conflict-free with this swizzle: rows r and r + 8 (1 KB apart) already fall
+// in different banks on gfx950, and XOR-ing r >> 3 into the chunk as well
+// measured as a 2-way conflict (LDS bank-conflict counter, 16-row fragment
+// read pattern).
+__device__ __forceinline__ int rswz(int r) { return r & 7; }
 
 // ---- col layout: [64 k][cols], cols/8 chunks per k-row; chunk pairs XOR-swizzled
 // so the 8 rows {k..k+3, k+8..k+11} read together by ds_read_b64_tr_b16 hit
@@ -221,133 +239,123 @@ __device__ __forceinline__ int xcd_remap(int pid, int n) {
     return xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
 }
 
-template <int MODE, bool A_K, bool B_K, int EPI, bool KTAIL>
-__global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(GemmArgs p) {
-    __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];  // 144 KB
+// One BK-wide stage of the main loop for stage slot S of the ring: read the
+// fragments of both 32-wide k steps, send the next-but-one stage's copies out
+// between the two MFMA blocks, and accumulate.  `next` says whether there is
+// a stage to copy; nrem is the contraction length left from its start.
+template <bool A_K, bool B_K, bool KTAIL, int S, class DA, class DB, int NA, int NB>
+__device__ __forceinline__ void mma_stage(f32x4 (&acc)[4][4], const uint32_t (&abase)[NA],
+                                          const uint32_t (&bbase)[2][NB], DA& da, DB& db, bool next,
+                                          int64_t nrem, uint32_t ldsA, uint32_t ldsB, int wave) {
+    constexpr int NS = (S + 2) % kStages;
+    constexpr int kSA = DA::kSlots, kSB = DB::kSlots;
+#pragma unroll
+    for (int kk = 0; kk < BK / 32; ++kk) {
+        bf16x8 af[4], bfg[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (A_K) af[i] = lds_b128(abase[kk] + S * kABytes + i * 2048);
+            else af[i] = lds_tr_pair(abase[i] + S * kABytes + kk * 64 * BM, 8 * BM);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            constexpr uint32_t so = (S & 1) * kBBytes;
+            if constexpr (B_K) bfg[j] = lds_b128(bbase[S >> 1][kk] + so + j * 2048);
+            else bfg[j] = lds_tr_pair(bbase[S >> 1][j] + so + kk * 64 * BN, 8 * BN);
+        }
+        if (next) {
+            if (kk == 0) {
+                da.template issue<KTAIL, 0, kSA>(ldsA + NS * kABytes, nrem, wave);
+                db.template issue<KTAIL, 0, kSB / 2>(ldsB + NS * kBBytes, nrem, wave);
+            } else {
+                db.template issue<KTAIL, kSB / 2, kSB>(ldsB + NS * kBBytes, nrem, wave);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfg[j], af[i], acc[i][j], 0, 0, 0);
+    }
+}
+
+// Per-lane fragment bases of the A (BM-wide) and B (BN-wide) operands.
+template <bool A_K, bool B_K, int NA, int NB>
+__device__ __forceinline__ void frag_bases(uint32_t (&abase)[NA], uint32_t (&bbase)[2][NB], uint32_t ldsA,
+                                           uint32_t ldsB, int wm, int wn, int lane) {
+#pragma unroll
+    for (int i = 0; i < NA; ++i)
+        abase[i] = ldsA + (A_K ? row_base(wm * 64, i, lane) : col_base<BM>(wm * 64 + i * 16, lane));
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        const uint32_t o = B_K ? row_base(wn * 64, j, lane) : col_base<BN>(wn * 64 + j * 16, lane);
+        bbase[0][j] = ldsB + o;          // stages 0 and 1
+        bbase[1][j] = ldsB + 2 * kBBytes + o;  // stage 2 (immediate offsets reach 64 KB)
+    }
+}
+
+__device__ __forceinline__ void zero_acc(f32x4 (&acc)[4][4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// ---------------------------------------------------------------------------
+// KGRP mode (wgrad): C_e[m, n] = sum over expert e's rows r of A[r, m] B[r, n],
+// fp32 output.  One workgroup per (expert, m-tile, n-tile).
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) {
+    __shared__ __attribute__((aligned(1024))) char smem[kRingBytes];  // 144 KB
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar LDS offsets
     const int wm = wave >> 2, wn = wave & 3;
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
 
-    int e = 0, mt, nt;
-    int64_t row0, row_hi, k_begin, k_end;
-    if (MODE == MODE_ROWS) {
-        const int width = kGroupM * p.n_tiles;
-        const int group = lid / width;
-        const int first_m = group * kGroupM;
-        const int gsz = (p.m_tiles - first_m) < kGroupM ? (p.m_tiles - first_m) : kGroupM;
-        const int in = lid - group * width;
-        mt = first_m + in % gsz;
-        nt = in / gsz;
-        if (p.tiles != nullptr) {
-            const int4 ti = p.tiles[mt];  // one uniform 16-byte load: expert and rows
-            if (ti.x < 0) return;
-            e = ti.x;
-            row0 = ti.y;
-            row_hi = ti.z;
-        } else {
-            row0 = (int64_t)mt * BM;
-            if (row0 >= p.M) return;
-            row_hi = (row0 + BM) < p.M ? (row0 + BM) : p.M;
-        }
-        k_begin = 0;
-        k_end = p.Kd;
-    } else {
-        const int per = p.m_tiles * p.n_tiles;
-        e = lid / per;
-        const int in = lid - e * per;
-        mt = in % p.m_tiles;
-        nt = in / p.m_tiles;
-        row0 = (int64_t)mt * BM;
-        row_hi = (row0 + BM) < p.M ? (row0 + BM) : p.M;
-        k_begin = p.offsets[e];
-        k_end = p.offsets[e + 1];
-        k_begin = k_begin < 0 ? 0 : (k_begin > p.R ? p.R : k_begin);
-        k_end = k_end < k_begin ? k_begin : (k_end > p.R ? p.R : k_end);
-    }
+    const int per = p.m_tiles * p.n_tiles;
+    const int e = lid / per;
+    const int in = lid - e * per;
+    const int mt = in % p.m_tiles, nt = in / p.m_tiles;
+    const int64_t row0 = (int64_t)mt * BM;
+    const int64_t row_hi = (row0 + BM) < p.M ? (row0 + BM) : p.M;
+    int64_t k_begin = p.offsets[e];
+    int64_t k_end = p.offsets[e + 1];
+    k_begin = k_begin < 0 ? 0 : (k_begin > p.R ? p.R : k_begin);
+    k_end = k_end < k_begin ? k_begin : (k_end > p.R ? p.R : k_end);
     const int64_t n0 = (int64_t)nt * BN;
-    const uint16_t* Bsrc = p.B + (MODE == MODE_ROWS ? (int64_t)e * p.b_stride : 0);
 
-    // LDS: B tiles of the 3 stages first, then the A tiles.
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char*)smem;
     const uint32_t ldsB = lds0, ldsA = lds0 + kStages * kBBytes;
 
-    DmaTile<A_K, BM> da;
-    DmaTile<B_K, BN> db;
+    DmaTile<false, BM> da;
+    DmaTile<false, BN> db;
     da.init(p.A, p.lda, row0, row_hi, k_begin, wave, lane);
-    db.init(Bsrc, p.ldb, n0, (int64_t)p.N, k_begin, wave, lane);
-    constexpr int kSA = DmaTile<A_K, BM>::kSlots, kSB = DmaTile<B_K, BN>::kSlots;
-    constexpr int kPerStage = kSA + kSB;  // DMA instructions per wave per stage: 2 + 4
+    db.init(p.B, p.ldb, n0, (int64_t)p.N, k_begin, wave, lane);
+    constexpr int kPerStage = DmaTile<false, BM>::kSlots + DmaTile<false, BN>::kSlots;
 
-    // Per-lane fragment bases; stage, k-step and tile offsets are immediates.
-    // B tiles of stages 0/1 are reached from bbase[0], stage 2 from bbase[1]
-    // (the immediate offset field holds at most 64 KB).
-    constexpr int kNA = A_K ? 2 : 4, kNB = B_K ? 2 : 4;
-    uint32_t abase[kNA], bbase[2][kNB];
-#pragma unroll
-    for (int i = 0; i < kNA; ++i)
-        abase[i] = ldsA + (A_K ? row_base(wm * 64, i, lane) : col_base<BM>(wm * 64 + i * 16, lane));
-#pragma unroll
-    for (int j = 0; j < kNB; ++j) {
-        const uint32_t o = B_K ? row_base(wn * 64, j, lane) : col_base<BN>(wn * 64 + j * 16, lane);
-        bbase[0][j] = ldsB + o;
-        bbase[1][j] = ldsB + 2 * kBBytes + o;
-    }
+    uint32_t abase[4], bbase[2][4];
+    frag_bases<false, false>(abase, bbase, ldsA, ldsB, wm, wn, lane);
 
     f32x4 acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    zero_acc(acc);
 
     const int64_t klen = k_end - k_begin;
     const int nk = (int)((klen + BK - 1) / BK);
 
     auto step = [&](auto stage_c, int kt) {
         constexpr int S = decltype(stage_c)::value;
-        constexpr int NS = (S + 2) % kStages;
         if (kt + 1 < nk) wait_vmcnt<kPerStage>(); else wait_vmcnt<0>();
         stage_barrier();
-        const bool next = kt + 2 < nk;
-        const int64_t nrem = klen - (int64_t)(kt + 2) * BK;
-#pragma unroll
-        for (int kk = 0; kk < BK / 32; ++kk) {
-            bf16x8 af[4], bfg[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                if constexpr (A_K) af[i] = lds_b128(abase[kk] + S * kABytes + i * 2048);
-                else af[i] = lds_tr_pair(abase[i] + S * kABytes + kk * 64 * BM, 8 * BM);
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                constexpr uint32_t so = (S & 1) * kBBytes;
-                if constexpr (B_K) bfg[j] = lds_b128(bbase[S >> 1][kk] + so + j * 2048);
-                else bfg[j] = lds_tr_pair(bbase[S >> 1][j] + so + kk * 64 * BN, 8 * BN);
-            }
-            // the next-but-one stage's copies go out between the MFMA blocks
-            if (next) {
-                if (kk == 0) {
-                    da.template issue<KTAIL, 0, kSA>(ldsA + NS * kABytes, nrem, wave);
-                    db.template issue<KTAIL, 0, kSB / 2>(ldsB + NS * kBBytes, nrem, wave);
-                } else {
-                    db.template issue<KTAIL, kSB / 2, kSB>(ldsB + NS * kBBytes, nrem, wave);
-                }
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfg[j], af[i], acc[i][j], 0, 0, 0);
-        }
+        mma_stage<false, false, true, S>(acc, abase, bbase, da, db, kt + 2 < nk,
+                                         klen - (int64_t)(kt + 2) * BK, ldsA, ldsB, wave);
     };
 
     if (nk > 0) {
-        da.template issue<KTAIL, 0, kSA>(ldsA, klen, wave);
-        db.template issue<KTAIL, 0, kSB>(ldsB, klen, wave);
+        da.template issue<true, 0, DmaTile<false, BM>::kSlots>(ldsA, klen, wave);
+        db.template issue<true, 0, DmaTile<false, BN>::kSlots>(ldsB, klen, wave);
         if (nk > 1) {
-            da.template issue<KTAIL, 0, kSA>(ldsA + kABytes, klen - BK, wave);
-            db.template issue<KTAIL, 0, kSB>(ldsB + kBBytes, klen - BK, wave);
+            da.template issue<true, 0, DmaTile<false, BM>::kSlots>(ldsA + kABytes, klen - BK, wave);
+            db.template issue<true, 0, DmaTile<false, BN>::kSlots>(ldsB + kBBytes, klen - BK, wave);
         }
         for (int kt = 0; kt < nk; kt += kStages) {
             step(std::integral_constant<int, 0>{}, kt);
@@ -356,8 +364,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(GemmArgs p) {
         }
     }
 
-    // Epilogue: lane holds C[m][n .. n+3] for each (i, j).
-    const int64_t c_base = (MODE == MODE_KGRP) ? (int64_t)e * p.c_stride : 0;
+    // lane holds C[m][n .. n+3] for each (i, j)
+    const int64_t c_base = (int64_t)e * p.c_stride;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int64_t m = row0 + wm * 64 + i * 16 + (lane & 15);
@@ -367,27 +375,228 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(GemmArgs p) {
             const int64_t n = n0 + wn * 64 + j * 16 + 4 * (lane >> 4);
             if (n >= p.N) continue;
             const f32x4 a = acc[i][j];
-            const int64_t off = c_base + m * p.ldc + n;
-            if constexpr (EPI == EPI_F32) {
-                *(float4*)((float*)p.C + off) = make_float4(a[0], a[1], a[2], a[3]);
-            } else if constexpr (EPI == EPI_BF16) {
-                *(uint2*)((uint16_t*)p.C + off) = make_uint2(pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]));
-            } else if constexpr (EPI == EPI_RELU2) {
-                const float r0 = fmaxf(a[0], 0.f), r1 = fmaxf(a[1], 0.f);
-                const float r2 = fmaxf(a[2], 0.f), r3 = fmaxf(a[3], 0.f);
-                *(uint2*)((uint16_t*)p.C + off) =
-                    make_uint2(pack_bf16x2(r0 * r0, r1 * r1), pack_bf16x2(r2 * r2, r3 * r3));
-                if (p.aux_out != nullptr)
-                    *(uint2*)(p.aux_out + off) = make_uint2(pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]));
-            } else {  // EPI_DRELU2
-                const uint2 u = *(const uint2*)(p.aux_in + off);
-                const float g0 = a[0] * 2.f * fmaxf(bf16_lo(u.x), 0.f);
-                const float g1 = a[1] * 2.f * fmaxf(bf16_hi(u.x), 0.f);
-                const float g2 = a[2] * 2.f * fmaxf(bf16_lo(u.y), 0.f);
-                const float g3 = a[3] * 2.f * fmaxf(bf16_hi(u.y), 0.f);
-                *(uint2*)((uint16_t*)p.C + off) = make_uint2(pack_bf16x2(g0, g1), pack_bf16x2(g2, g3));
-            }
+            *(float4*)((float*)p.C + c_base + m * p.ldc + n) = make_float4(a[0], a[1], a[2], a[3]);
         }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// ROWS mode, persistent.
+
+struct RowsTile {
+    int e;
+    int64_t row0, row_hi, n0;
+};
+
+// Work item w -> output tile: 8 m-tiles at a time across all n-tiles.
+__device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, int m_total, int64_t w) {
+    const int64_t width = (int64_t)kGroupM * p.n_tiles;
+    const int64_t group = w / width;
+    const int first_m = (int)(group * kGroupM);
+    const int gsz = (m_total - first_m) < kGroupM ? (m_total - first_m) : kGroupM;
+    const int in = (int)(w - group * width);
+    const int mt = __builtin_amdgcn_readfirstlane(first_m + in % gsz);
+    const int nt = in / gsz;
+    RowsTile t;
+    if (p.tiles != nullptr) {
+        // the table is written by an earlier launch and read-only here: a
+        // scalar load through the constant address space
+        const __attribute__((address_space(4))) int32_t* ti =
+            (const __attribute__((address_space(4))) int32_t*)(p.tiles + mt);
+        t.e = ti[0];
+        t.row0 = ti[1];
+        t.row_hi = ti[2];
+    } else {
+        t.e = 0;
+        t.row0 = (int64_t)mt * BM;
+        t.row_hi = (t.row0 + BM) < p.M ? (t.row0 + BM) : p.M;
+    }
+    t.n0 = (int64_t)nt * BN;
+    return t;
+}
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+
+// Buffer descriptor over rows [row0, row0 + nrows) of a row-major bf16 matrix:
+// accesses at byte offsets >= nrows * ldc * 2 are dropped (stores) or read as
+// zero (loads) by the hardware.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void* base, int64_t row0, int64_t nrows,
+                                                            int64_t ldc) {
+    const uint16_t* b = (const uint16_t*)base + row0 * ldc;
+    const int32_t bytes = nrows > 0 ? (int32_t)(nrows * ldc * 2) : 0;
+    return __builtin_amdgcn_make_buffer_rsrc((void*)b, 0, bytes, 0x00020000);
+}
+
+constexpr uint32_t kDropOffset = 0x80000000u;  // beyond any descriptor's range
+
+// Staged epilogue of one 64 x 64 wave tile (EPI_BF16 / EPI_RELU2): per 16-row
+// block, the accumulators go to the wave's LDS slice as bf16 (chunk c of row
+// r at c ^ (r & 7)), come back as 16-byte row pieces and leave as two
+// buffer_store_dwordx4 of 8 rows x 128 bytes each.  OUT: 0 = the product
+// (squared-ReLU applied for EPI_RELU2), 1 = the raw product (pre-activation).
+template <int EPI, int OUT>
+__device__ __forceinline__ void staged_store(const f32x4 (&acc)[4][4], void* C, int64_t ldc, int N,
+                                             int64_t rbase, int64_t nrows, int64_t cbase,
+                                             uint32_t ep, int lane) {
+    const __amdgpu_buffer_rsrc_t rs = rows_rsrc(C, rbase, nrows, ldc);
+    const int r = lane & 15;
+    const uint32_t wr = ep + (uint32_t)(r * 128 + (lane >> 4 & 1) * 8);
+    const int rr0 = lane >> 3, c = lane & 7;
+    const bool col_ok = cbase + c * 8 < N;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const f32x4 a = acc[i][j];
+            float v0 = a[0], v1 = a[1], v2 = a[2], v3 = a[3];
+            if constexpr (EPI == EPI_RELU2 && OUT == 0) {
+                v0 = fmaxf(v0, 0.f); v1 = fmaxf(v1, 0.f); v2 = fmaxf(v2, 0.f); v3 = fmaxf(v3, 0.f);
+                v0 *= v0; v1 *= v1; v2 *= v2; v3 *= v3;
+            }
+            const int ch = 2 * j + (lane >> 5);
+            const u32x2 w = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+            *(lds_u32x2*)(uintptr_t)(wr + (uint32_t)((ch ^ (r & 7)) * 16)) = w;
+        }
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int rr = q * 8 + rr0;
+            const u32x4 v = *(const lds_u32x4*)(uintptr_t)(ep + (uint32_t)(rr * 128 + ((c ^ (rr & 7)) * 16)));
+            const int64_t row = i * 16 + rr;
+            const uint32_t off = (row < nrows && col_ok) ? (uint32_t)((row * ldc + cbase + c * 8) * 2) : kDropOffset;
+            __builtin_amdgcn_raw_buffer_store_b128(v, rs, off, 0, 0);
+        }
+    }
+}
+
+// dgrad epilogue: C = bf16(acc * 2 max(u, 0)) with u read from aux_in at the
+// accumulator's own positions (8 bytes per lane and fragment).
+__device__ __forceinline__ void drelu2_store(const f32x4 (&acc)[4][4], void* C, const uint16_t* aux_in,
+                                             int64_t ldc, int N, int64_t rbase, int64_t nrows,
+                                             int64_t cbase, int lane) {
+    const __amdgpu_buffer_rsrc_t rc = rows_rsrc(C, rbase, nrows, ldc);
+    const __amdgpu_buffer_rsrc_t ru = rows_rsrc(aux_in, rbase, nrows, ldc);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t row = i * 16 + (lane & 15);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t col = cbase + j * 16 + 4 * (lane >> 4);
+            const uint32_t off = (row < nrows && col < N) ? (uint32_t)((row * ldc + col) * 2) : kDropOffset;
+            const u32x2 u = __builtin_amdgcn_raw_buffer_load_b64(ru, off, 0, 0);
+            const f32x4 a = acc[i][j];
+            const float g0 = a[0] * 2.f * fmaxf(bf16_lo(u[0]), 0.f);
+            const float g1 = a[1] * 2.f * fmaxf(bf16_hi(u[0]), 0.f);
+            const float g2 = a[2] * 2.f * fmaxf(bf16_lo(u[1]), 0.f);
+            const float g3 = a[3] * 2.f * fmaxf(bf16_hi(u[1]), 0.f);
+            const u32x2 w = {pack_bf16x2(g0, g1), pack_bf16x2(g2, g3)};
+            __builtin_amdgcn_raw_buffer_store_b64(w, rc, off, 0, 0);
+        }
+    }
+}
+
+// C[r, n] = sum_k A[r, k] B_e[k, n] over the grid-wide list of output tiles
+// (expert segments from the tile table, or all M rows when it is null).
+// A is K-contiguous (ROW layout); B is N-contiguous (B_K false: weights stored
+// [Kd, N]) or K-contiguous (B_K true: transposed weights of the dgrads).
+template <bool B_K, int EPI, bool KTAIL>
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) {
+    __shared__ __attribute__((aligned(1024))) char smem[kRingBytes + kEpiBytes];  // 160 KB
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 2, wn = wave & 3;
+
+    // This workgroup's work items: w = first + j * G, j = 0 .. n_mine - 1,
+    // where the G / 8 workgroups of one XCD take consecutive items.
+    const int m_total = p.mtile_total != nullptr
+                            ? *(const __attribute__((address_space(4))) int32_t*)p.mtile_total
+                            : p.m_tiles;
+    const int64_t n_work = (int64_t)m_total * p.n_tiles;
+    const int G = gridDim.x;
+    const int first = (int)(blockIdx.x % kXcds) * (G / kXcds) + (int)(blockIdx.x / kXcds);
+    const int64_t n_mine = first < n_work ? (n_work - first + G - 1) / G : 0;
+    const int nk = (p.Kd + BK - 1) / BK;
+    const int64_t g_total = n_mine * nk;  // (tile, k step) pairs
+    if (g_total == 0) return;
+
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char*)smem;
+    const uint32_t ldsB = lds0, ldsA = lds0 + kStages * kBBytes;
+    const uint32_t ep = lds0 + kRingBytes + (uint32_t)wave * kEpiWaveBytes;
+
+    DmaTile<true, BM> da;
+    DmaTile<B_K, BN> db;
+    constexpr int kSA = DmaTile<true, BM>::kSlots, kSB = DmaTile<B_K, BN>::kSlots;
+    constexpr int kPerStage = kSA + kSB;
+    auto dma_tile = [&](int64_t j) {
+        const RowsTile t = rows_tile(p, m_total, first + j * G);
+        da.init(p.A, p.lda, t.row0, t.row_hi, 0, wave, lane);
+        db.init(p.B + (int64_t)t.e * p.b_stride, p.ldb, t.n0, (int64_t)p.N, 0, wave, lane);
+    };
+
+    constexpr int kNB = B_K ? 2 : 4;
+    uint32_t abase[2], bbase[2][kNB];
+    frag_bases<true, B_K>(abase, bbase, ldsA, ldsB, wm, wn, lane);
+
+    f32x4 acc[4][4];
+    zero_acc(acc);
+
+    // DMA of the first two steps; kd / jd track the step two ahead.
+    dma_tile(0);
+    da.template issue<KTAIL, 0, kSA>(ldsA, p.Kd, wave);
+    db.template issue<KTAIL, 0, kSB>(ldsB, p.Kd, wave);
+    int kd = 1 % nk;
+    int64_t jd = 1 / nk;
+    if (g_total > 1) {
+        if (kd == 0) dma_tile(jd);
+        const int64_t rem = (int64_t)p.Kd - (int64_t)kd * BK;
+        da.template issue<KTAIL, 0, kSA>(ldsA + kABytes, rem, wave);
+        db.template issue<KTAIL, 0, kSB>(ldsB + kBBytes, rem, wave);
+    }
+    if (++kd == nk) { kd = 0; ++jd; }
+
+    int kc = 0;        // k step of the tile being computed
+    int64_t jc = 0;    // its index in this workgroup's list
+    RowsTile cur = rows_tile(p, m_total, first);
+
+    auto step = [&](auto stage_c, int64_t g) {
+        constexpr int S = decltype(stage_c)::value;
+        // Stores of an epilogue may still be in flight; they are not counted,
+        // so the wait covers this stage's copies whichever way they complete.
+        if (g + 1 < g_total) wait_vmcnt<kPerStage>(); else wait_vmcnt<0>();
+        stage_barrier();
+        const bool next = g + 2 < g_total;
+        if (next && kd == 0) dma_tile(jd);
+        mma_stage<true, B_K, KTAIL, S>(acc, abase, bbase, da, db, next,
+                                       (int64_t)p.Kd - (int64_t)kd * BK, ldsA, ldsB, wave);
+        if (++kd == nk) { kd = 0; ++jd; }
+        if (kc == nk - 1) {
+            const int64_t rbase = cur.row0 + wm * 64;
+            const int64_t nrows = cur.row_hi - rbase;
+            const int64_t cbase = cur.n0 + wn * 64;
+            if constexpr (EPI == EPI_DRELU2) {
+                drelu2_store(acc, p.C, p.aux_in, p.ldc, p.N, rbase, nrows, cbase, lane);
+            } else {
+                staged_store<EPI, 0>(acc, p.C, p.ldc, p.N, rbase, nrows, cbase, ep, lane);
+                if constexpr (EPI == EPI_RELU2)
+                    if (p.aux_out != nullptr)
+                        staged_store<EPI, 1>(acc, p.aux_out, p.ldc, p.N, rbase, nrows, cbase, ep, lane);
+            }
+            zero_acc(acc);
+            kc = 0;
+            ++jc;
+            if (jc < n_mine) cur = rows_tile(p, m_total, first + jc * G);
+        } else {
+            ++kc;
+        }
+    };
+
+    for (int64_t g = 0; g < g_total; g += kStages) {
+        step(std::integral_constant<int, 0>{}, g);
+        if (g + 1 < g_total) step(std::integral_constant<int, 1>{}, g + 1);
+        if (g + 2 < g_total) step(std::integral_constant<int, 2>{}, g + 2);
     }
 }
 
@@ -454,18 +663,35 @@ size_t gemm_schedule_bytes(int E, int64_t R) {
     return (sched_table_offset(E) + (size_t)mtiles_bound(R, E) * 16 + 255) / 256 * 256;
 }
 
-template <int MODE, bool A_K, bool B_K, int EPI>
-static hipError_t launch(const GemmArgs& a, int64_t n_wg, hipStream_t st) {
-    if (n_wg <= 0) return hipSuccess;
-    if (n_wg > 0x7fffffff) return hipErrorInvalidConfiguration;
-    // ROWS mode contracts over a fixed width: a partial last k tile only when
-    // it is not a multiple of BK.  KGRP contracts over ragged expert rows.
-    if (MODE == MODE_KGRP || a.Kd % BK != 0)
-        hipLaunchKernelGGL((gemm_kernel<MODE, A_K, B_K, EPI, true>), dim3((unsigned)n_wg),
-                           dim3(kGemmThreads), 0, st, a);
+// Compute units of the current device, read once per device.
+static int cu_count() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    static std::once_flag once[64];
+    static int cus[64];
+    std::call_once(once[dev], [dev] {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+        cus[dev] = n;
+    });
+    return cus[dev];
+}
+
+template <bool B_K, int EPI>
+static hipError_t launch_rows(const GemmArgs& a, hipStream_t st) {
+    // one workgroup per CU (a multiple of the XCD count), never more than the
+    // static bound on the number of output tiles
+    const int64_t bound = (int64_t)a.m_tiles * a.n_tiles;
+    if (bound <= 0) return hipSuccess;
+    int64_t G = (cu_count() / kXcds) * kXcds;
+    if (G < kXcds) G = kXcds;
+    const int64_t need = (bound + kXcds - 1) / kXcds * kXcds;
+    if (need < G) G = need;
+    if (a.Kd % BK != 0)
+        hipLaunchKernelGGL((gemm_rows_kernel<B_K, EPI, true>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
     else
-        hipLaunchKernelGGL((gemm_kernel<MODE, A_K, B_K, EPI, false>), dim3((unsigned)n_wg),
-                           dim3(kGemmThreads), 0, st, a);
+        hipLaunchKernelGGL((gemm_rows_kernel<B_K, EPI, false>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
     return hipGetLastError();
 }
 
@@ -482,19 +708,21 @@ hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B
                                int E, int64_t R, int N, int Kd, hipStream_t st) {
     GemmArgs a{};
     a.A = A; a.B = B; a.C = C; a.aux_in = aux_in; a.aux_out = aux_out;
-    a.tiles = sched ? (const int4*)((const char*)sched + sched_table_offset(E)) : nullptr;
+    if (sched != nullptr) {
+        a.tiles = (const int4*)((const char*)sched + sched_table_offset(E));
+        a.mtile_total = (const int32_t*)sched + E;  // mtile_start[E]
+    }
     a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.b_stride = b_stride;
     a.M = R; a.R = R; a.N = N; a.Kd = Kd; a.E = E;
     a.n_tiles = (N + BN - 1) / BN;
     a.m_tiles = (int)(sched ? mtiles_bound(R, E) : (R + BM - 1) / BM);
-    const int64_t n_wg = (int64_t)a.m_tiles * a.n_tiles;
     if (R == 0) return hipSuccess;
     if (!b_kmajor) {
-        if (epi == EPI_BF16) return launch<MODE_ROWS, true, false, EPI_BF16>(a, n_wg, st);
-        if (epi == EPI_RELU2) return launch<MODE_ROWS, true, false, EPI_RELU2>(a, n_wg, st);
+        if (epi == EPI_BF16) return launch_rows<false, EPI_BF16>(a, st);
+        if (epi == EPI_RELU2) return launch_rows<false, EPI_RELU2>(a, st);
     } else {
-        if (epi == EPI_BF16) return launch<MODE_ROWS, true, true, EPI_BF16>(a, n_wg, st);
-        if (epi == EPI_DRELU2) return launch<MODE_ROWS, true, true, EPI_DRELU2>(a, n_wg, st);
+        if (epi == EPI_BF16) return launch_rows<true, EPI_BF16>(a, st);
+        if (epi == EPI_DRELU2) return launch_rows<true, EPI_DRELU2>(a, st);
     }
     return hipErrorInvalidValue;
 }
@@ -509,7 +737,10 @@ hipError_t launch_grouped_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* 
     a.m_tiles = (M + BM - 1) / BM;
     a.n_tiles = (N + BN - 1) / BN;
     const int64_t n_wg = (int64_t)E * a.m_tiles * a.n_tiles;
-    return launch<MODE_KGRP, false, false, EPI_F32>(a, n_wg, st);
+    if (n_wg <= 0) return hipSuccess;
+    if (n_wg > 0x7fffffff) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(gemm_kgrp_kernel, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a);
+    return hipGetLastError();
 }
 
 }  // namespace moe

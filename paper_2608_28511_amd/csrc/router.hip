@@ -26,7 +26,8 @@ constexpr int kRK = 64;       // d per stage
 constexpr int kRChunks = kRK / 8;
 constexpr int kRTile = kRT * kRK * 2;   // bytes of one bf16 64x64 tile
 
-__device__ __forceinline__ int rswz(int row) { return (row ^ (row >> 3)) & (kRChunks - 1); }
+// chunk c of row r stored at c ^ (r & 7): conflict-free 16-row ds_read_b128 on gfx950
+__device__ __forceinline__ int rswz(int row) { return row & (kRChunks - 1); }
 __device__ __forceinline__ int roff(int r, int c) { return (r * kRChunks + (c ^ rswz(r))) * 16; }
 
 __device__ __forceinline__ float bf16_round_f32(float f, uint32_t* bits) {
