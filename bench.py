@@ -251,10 +251,12 @@ def main():
     out = lf.out
     reps = args.stage_reps
     st = {}
+    ws_router = torch.empty(max(1, _lib.moe_router_logits_workspace_bytes(s.D, s.E)), dtype=torch.uint8,
+                            device=dev)
     st["router_logits"] = time_region(
         lambda i: _lib.moe_router_logits(sets[i % len(sets)]["x"] if not s.H else out["x_lat"],
                                          sets[i % len(sets)]["Wr"], sets[i % len(sets)]["bias"],
-                                         s.S, s.D, s.E, out["logits"]), reps, stream)
+                                         s.S, s.D, s.E, out["logits"], ws_router), reps, stream)
     ws_route = torch.empty(max(1, _lib.moe_route_workspace_bytes(s.S, s.E, s.K)), dtype=torch.uint8,
                            device=dev)
     r_bufs = {k: torch.empty_like(out[k]) for k in ("topk_idx", "topk_prob", "counts", "offsets",

@@ -74,13 +74,27 @@ uint64_t moe_payload_bytes(int64_t S, int32_t K, int32_t D);
 /* Router logits (the router scores every token against every expert,     */
 /* Section 5.2).                                                          */
 /* ---------------------------------------------------------------------- */
+/* Workspace bytes moe_router_logits needs (3 * E * D * 2 rounded up to
+ * 256: the router weight split into three bf16 planes); 0 for invalid sizes. */
+size_t moe_router_logits_workspace_bytes(int32_t D, int32_t E);
+
 /* logits[t,e] = sum_d x_r[t,d] * Wr[d,e] + bias[e], accumulated in fp32.
  *   x_r    [S, D]  bf16   router input (the dispatch-width activations)
- *   Wr     [D, E]  fp32   router weight
+ *   Wr     [D, E]  fp32   router weight (4-byte aligned)
  *   bias   [E]     fp32   per-expert logit offset, or NULL for none
- *   logits [S, E]  fp32   output */
+ *   logits [S, E]  fp32   output
+ *   ws, ws_bytes          device scratch of at least
+ *                         moe_router_logits_workspace_bytes(D, E) bytes,
+ *                         16-byte aligned; overwritten by the call.
+ * Each fp32 weight is used as the sum of three bf16 terms (its bf16
+ * rounding and the bf16 roundings of the two successive remainders), which
+ * equals it to within 2^-24 relative, so the logits carry fp32 accuracy.
+ * Errors: MOE_ERR_SHAPE (S < 0, D not a multiple of 8 in [8, 65536], E not
+ * in [1, 1024]), MOE_ERR_NULL / MOE_ERR_ALIGN for missing or misaligned
+ * buffers, MOE_ERR_WORKSPACE for a missing or short ws. */
 int moe_router_logits(const moe_bf16* x_r, const float* Wr, const float* bias,
-                      int64_t S, int32_t D, int32_t E, float* logits, hipStream_t stream);
+                      int64_t S, int32_t D, int32_t E, float* logits,
+                      void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------- */
 /* Top-K routing and the expert permutation (dropless, unpadded top-K     */

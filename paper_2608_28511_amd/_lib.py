@@ -51,7 +51,8 @@ _PROTOS = {
     "moe_abi_version": (C.c_int, []),
     "moe_status_string": (C.c_char_p, [C.c_int]),
     "moe_payload_bytes": (C.c_uint64, [i64, i32, i32]),
-    "moe_router_logits": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp]),
+    "moe_router_logits_workspace_bytes": (sz, [i32, i32]),
+    "moe_router_logits": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp, sz, vp]),
     "moe_route_workspace_bytes": (sz, [i64, i32, i32]),
     "moe_route_topk": (C.c_int, [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
     "moe_dispatch": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp, vp]),
@@ -132,10 +133,16 @@ def moe_payload_bytes(S: int, K: int, D: int) -> int:
     return load().moe_payload_bytes(S, K, D)
 
 
-def moe_router_logits(x_r, Wr, bias, S, D, E, logits):
+def moe_router_logits_workspace_bytes(D, E) -> int:
+    return load().moe_router_logits_workspace_bytes(D, E)
+
+
+def moe_router_logits(x_r, Wr, bias, S, D, E, logits, ws):
     _check(load().moe_router_logits(_ptr(x_r, BF16, "x_r"), _ptr(Wr, F32, "Wr"),
-                                    _ptr(bias, F32, "bias"), S, D, E,
-                                    _ptr(logits, F32, "logits"), _stream()), "moe_router_logits")
+                                    _ptr(bias, F32, "bias"), S, D, E, _ptr(logits, F32, "logits"),
+                                    _ptr(ws, None, "ws"),
+                                    0 if ws is None else ws.numel() * ws.element_size(), _stream()),
+           "moe_router_logits")
 
 
 def moe_route_workspace_bytes(S, E, K) -> int:

@@ -81,14 +81,21 @@ uint64_t moe_payload_bytes(int64_t S, int32_t K, int32_t D) {
     return (uint64_t)S * (uint64_t)K * ((uint64_t)D * 2u + 4u);
 }
 
+size_t moe_router_logits_workspace_bytes(int32_t D, int32_t E) {
+    if (!dim_ok(D) || E < 1 || E > kMaxE) return 0;
+    return moe::router_ws_bytes(D, E);
+}
+
 int moe_router_logits(const moe_bf16* x_r, const float* Wr, const float* bias, int64_t S, int32_t D,
-                      int32_t E, float* logits, hipStream_t stream) {
+                      int32_t E, float* logits, void* ws, size_t ws_bytes, hipStream_t stream) {
     if (S < 0 || !dim_ok(D) || E < 1 || E > kMaxE) return MOE_ERR_SHAPE;
     MOE_TRY(need(x_r, (uint64_t)S * D * 2, 16));
     MOE_TRY(need(Wr, (uint64_t)D * E * 4, 4));
     MOE_TRY(opt(bias, 4));
     MOE_TRY(need(logits, (uint64_t)S * E * 4, 4));
-    return hip_status(moe::launch_router_logits(x_r, Wr, bias, S, D, E, logits, stream));
+    if (ws == nullptr || ws_bytes < moe::router_ws_bytes(D, E)) return MOE_ERR_WORKSPACE;
+    MOE_TRY(opt(ws, 16));
+    return hip_status(moe::launch_router_logits(x_r, Wr, bias, S, D, E, logits, ws, stream));
 }
 
 size_t moe_route_workspace_bytes(int64_t S, int32_t E, int32_t K) {
@@ -245,7 +252,7 @@ int check_layer_args(const moe_layer_fwd_args* a) {
 struct LayerBufs {
     moe_bf16* x_lat; float* logits; int32_t* topk_idx; float* topk_prob; int32_t* counts;
     int32_t* offsets; int32_t* perm; int32_t* inv_perm; moe_bf16* x_disp; float* p_disp;
-    moe_bf16* h; moe_bf16* y_disp; moe_bf16* y_lat; void* route_ws; void* sched;
+    moe_bf16* h; moe_bf16* y_disp; moe_bf16* y_lat; void* route_ws; void* sched; void* router_ws;
 };
 
 size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
@@ -271,6 +278,7 @@ size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
     b->y_lat = a->H ? pick(a->y_lat, (size_t)S * D * 2) : nullptr;
     b->route_ws = c.take(moe::route_ws_bytes(S, E));
     b->sched = c.take(moe::gemm_schedule_bytes(E, R));
+    b->router_ws = c.take(moe::router_ws_bytes(D, E));
     return c.used;
 }
 
@@ -317,7 +325,7 @@ int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
                                          nullptr, nullptr, nullptr, 1, S, D, H, stream));
         x_r = b.x_lat;
     }
-    MOE_HIP(moe::launch_router_logits(x_r, a->Wr, a->router_bias, S, D, E, b.logits, stream));
+    MOE_HIP(moe::launch_router_logits(x_r, a->Wr, a->router_bias, S, D, E, b.logits, b.router_ws, stream));
     MOE_HIP(moe::launch_route(b.logits, S, E, K, b.topk_idx, b.topk_prob, b.counts, b.offsets, b.perm,
                               b.inv_perm, b.route_ws, stream));
     MOE_HIP(moe::launch_dispatch(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_disp, b.p_disp, stream));

@@ -11,8 +11,10 @@ namespace moe {
 
 enum { EPI_BF16 = 0, EPI_RELU2 = 1, EPI_DRELU2 = 2, EPI_F32 = 3 };
 
+// Router workspace: the three bf16 planes [3][E][D] of the split router weight.
+size_t router_ws_bytes(int D, int E);
 hipError_t launch_router_logits(const moe_bf16* x, const float* Wr, const float* bias, int64_t S,
-                                int D, int E, float* logits, hipStream_t st);
+                                int D, int E, float* logits, void* ws, hipStream_t st);
 
 size_t route_ws_bytes(int64_t S, int E);
 hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* topk_idx,

@@ -3,142 +3,152 @@
 //
 // The router weight is fp32 while x is bf16.  Each fp32 weight w is split
 // into three bf16 terms, hi = bf16(w), mid = bf16(w - hi), lo = bf16(w - hi -
-// mid), whose sum equals w to within 2^-27 |w|.  Products of bf16 values are
+// mid), whose sum equals w to within 2^-24 |w|.  Products of bf16 values are
 // exact in fp32, so three bf16 MFMAs (x*lo + x*mid + x*hi, accumulated in
 // fp32) reproduce the fp32 product to fp32 accuracy while running on the
 // matrix cores (bf16 splitting as in Henry, Tang and Heinecke, "Leveraging
 // the bfloat16 artificial intelligence datatype for higher-precision
 // computations", ARITH 2019).
 //
-// Tiles: 64 tokens x 64 experts x 64 d per 256-thread block, 4 wavefronts of
-// 32 x 32 outputs; the split happens while the fp32 weight tile is written
-// to LDS (transposed to expert rows of d-contiguous chunks, the MFMA operand
-// layout), double buffered.  Every output is one fixed-order fp32 MFMA chain,
-// so results are deterministic.
+// Two launches:
+//   router_split_kernel   Wr [D, E] fp32 -> three bf16 planes [3][E][D]
+//                         (transposed through LDS, so each plane is
+//                         K-contiguous like x);
+//   router_logits_kernel  64 tokens x 64 experts per workgroup, 8 waves of
+//                         32 tokens x 16 experts; x and the three planes are
+//                         copied global -> LDS by a 4-stage DMA ring (32 KB
+//                         per 64-wide d step), every fragment is one
+//                         conflict-free ds_read_b128, and every output is one
+//                         fixed-order fp32 MFMA chain (lo, mid, hi per 32-wide
+//                         d step), so results are deterministic.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
+#include "tile_dma.h"
 
 namespace moe {
 
-constexpr int kRT = 64;       // tokens per block
-constexpr int kRE = 64;       // experts per block
-constexpr int kRK = 64;       // d per stage
-constexpr int kRChunks = kRK / 8;
-constexpr int kRTile = kRT * kRK * 2;   // bytes of one bf16 64x64 tile
+constexpr int kRT = 64;                      // tokens per workgroup
+constexpr int kRE = 64;                      // experts per workgroup
+constexpr int kRStages = 4;
+constexpr int kRTile = 64 * BK * 2;          // one 64 x 64 bf16 tile: 8 KB
+constexpr int kRStage = 4 * kRTile;          // x, hi, mid, lo: 32 KB
 
-// chunk c of row r stored at c ^ (r & 7): conflict-free 16-row ds_read_b128 on gfx950
-__device__ __forceinline__ int rswz(int row) { return row & (kRChunks - 1); }
-__device__ __forceinline__ int roff(int r, int c) { return (r * kRChunks + (c ^ rswz(r))) * 16; }
-
-__device__ __forceinline__ float bf16_round_f32(float f, uint32_t* bits) {
-    const uint32_t b = f32_to_bf16(f);
-    *bits = b;
-    return __uint_as_float(b << 16);
+// ---- split: one 64 (d) x 64 (e) block per 256-thread workgroup ----------
+__global__ __launch_bounds__(256) void router_split_kernel(const float* __restrict__ Wr, int D, int E,
+                                                           uint16_t* __restrict__ w3) {
+    __shared__ float t[64][65];
+    const int tid = threadIdx.x;
+    const int d0 = blockIdx.x * 64, e0 = blockIdx.y * 64;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+        const int dl = (tid >> 6) + 4 * q, el = tid & 63;
+        const int d = d0 + dl, e = e0 + el;
+        t[dl][el] = (d < D && e < E) ? Wr[(int64_t)d * E + e] : 0.f;
+    }
+    __syncthreads();
+    const int el = tid >> 2, seg = (tid & 3) * 16;
+    const int e = e0 + el;
+    if (e >= E) return;
+    const int64_t plane = (int64_t)E * D;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {          // two 8-wide chunks of d
+        const int d = d0 + seg + 8 * h;
+        if (d >= D) break;                 // D is a multiple of 8: chunks are whole
+        uint32_t hb[4], mb[4], lb[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            uint32_t p[3][2];
+#pragma unroll
+            for (int v = 0; v < 2; ++v) {
+                const float w = t[seg + 8 * h + 2 * u + v][el];
+                const uint32_t hi = f32_to_bf16(w);
+                const float r1 = w - __uint_as_float(hi << 16);
+                const uint32_t mid = f32_to_bf16(r1);
+                const uint32_t lo = f32_to_bf16(r1 - __uint_as_float(mid << 16));
+                p[0][v] = hi; p[1][v] = mid; p[2][v] = lo;
+            }
+            hb[u] = p[0][0] | (p[0][1] << 16);
+            mb[u] = p[1][0] | (p[1][1] << 16);
+            lb[u] = p[2][0] | (p[2][1] << 16);
+        }
+        uint16_t* dst = w3 + (int64_t)e * D + d;
+        *(uint4*)dst = make_uint4(hb[0], hb[1], hb[2], hb[3]);
+        *(uint4*)(dst + plane) = make_uint4(mb[0], mb[1], mb[2], mb[3]);
+        *(uint4*)(dst + 2 * plane) = make_uint4(lb[0], lb[1], lb[2], lb[3]);
+    }
 }
 
-__global__ __launch_bounds__(256, 2) void router_logits_kernel(const uint16_t* __restrict__ x,
-                                                               const float* __restrict__ Wr,
-                                                               const float* __restrict__ bias,
-                                                               int64_t S, int D, int E,
-                                                               float* __restrict__ logits,
-                                                               bool vec_w, bool vec_out) {
-    // per stage: A [64 tok][64 d], B_hi, B_mid, B_lo [64 exp][64 d]
-    __shared__ __attribute__((aligned(16))) char smem[2 * 4 * kRTile];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+// ---- logits --------------------------------------------------------------
+template <bool KTAIL>
+__global__ __launch_bounds__(kWaves * 64, 1) void router_logits_kernel(const uint16_t* __restrict__ x,
+                                                                       const uint16_t* __restrict__ w3,
+                                                                       const float* __restrict__ bias,
+                                                                       int64_t S, int D, int E,
+                                                                       float* __restrict__ logits,
+                                                                       bool vec_out) {
+    __shared__ __attribute__((aligned(1024))) char smem[kRStages * kRStage];  // 128 KB
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 2, wn = wave & 3;
     const int64_t t0 = (int64_t)blockIdx.x * kRT;
     const int e0 = blockIdx.y * kRE;
+    const int64_t plane = (int64_t)E * D;
 
-    uint4 av[2];
-    float bw[4][4];  // [k row][expert] of this thread's 4x4 weight block
-    const int eg = tid & 15, kg = tid >> 4;
+    DmaTile<true, 64> dx, dw[3];
+    dx.init(x, D, t0, S, 0, wave, lane);
+#pragma unroll
+    for (int s = 0; s < 3; ++s) dw[s].init(w3 + s * plane, D, e0, E, 0, wave, lane);
 
-    auto load = [&](int d0) {
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char*)smem;
+    auto issue = [&](int stage, int64_t rem) {
+        const uint32_t b = lds0 + (uint32_t)stage * kRStage;
+        dx.template issue<KTAIL, 0, 1>(b, rem, wave);
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int q = tid + 256 * i;
-            const int r = q >> 3, c = q & 7;
-            const int64_t t = t0 + r;
-            const int d = d0 + c * 8;
-            av[i] = (t < S && d < D) ? *(const uint4*)(x + t * D + d) : make_uint4(0, 0, 0, 0);
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int d = d0 + kg * 4 + q;
-            const int e = e0 + eg * 4;
-            if (d < D && vec_w && e + 3 < E) {
-                const float4 v = *(const float4*)(Wr + (int64_t)d * E + e);
-                bw[q][0] = v.x; bw[q][1] = v.y; bw[q][2] = v.z; bw[q][3] = v.w;
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    bw[q][j] = (d < D && e + j < E) ? Wr[(int64_t)d * E + e + j] : 0.f;
-            }
-        }
-    };
-    auto store = [&](char* st) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int q = tid + 256 * i;
-            *(uint4*)(st + roff(q >> 3, q & 7)) = av[i];
-        }
-        char* bh = st + kRTile;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            uint32_t hb[4], mb[4], lb[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const float w = bw[q][j];
-                const float h = bf16_round_f32(w, &hb[q]);
-                const float r1 = w - h;
-                const float m = bf16_round_f32(r1, &mb[q]);
-                lb[q] = f32_to_bf16(r1 - m);
-            }
-            const int r = eg * 4 + j;
-            const int off = roff(r, kg >> 1) + (kg & 1) * 8;
-            *(uint2*)(bh + off) = make_uint2(hb[0] | (hb[1] << 16), hb[2] | (hb[3] << 16));
-            *(uint2*)(bh + kRTile + off) = make_uint2(mb[0] | (mb[1] << 16), mb[2] | (mb[3] << 16));
-            *(uint2*)(bh + 2 * kRTile + off) = make_uint2(lb[0] | (lb[1] << 16), lb[2] | (lb[3] << 16));
-        }
+        for (int s = 0; s < 3; ++s) dw[s].template issue<KTAIL, 0, 1>(b + (1 + s) * kRTile, rem, wave);
     };
 
-    f32x4 acc[2][2];
+    uint32_t xb[2], wb[2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < 2; ++kk) {
+        xb[kk] = lds0 + row_base(wm * 32, kk, lane);
+        wb[kk] = lds0 + kRTile + row_base(wn * 16, kk, lane);
+    }
 
-    const int nk = (D + kRK - 1) / kRK;
-    load(0);
-    store(smem);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < nk) load((kt + 1) * kRK);
-        const char* st = smem + cur * 4 * kRTile;
+    f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+    const int nk = (D + BK - 1) / BK;
+
+    auto step = [&](auto stage_c, int kt) {
+        constexpr int S = decltype(stage_c)::value;
+        if (kt + 2 < nk) wait_vmcnt<8>();
+        else if (kt + 1 < nk) wait_vmcnt<4>();
+        else wait_vmcnt<0>();
+        stage_barrier();
+        if (kt + 3 < nk) issue((S + 3) % kRStages, (int64_t)D - (int64_t)(kt + 3) * BK);
 #pragma unroll
-        for (int kk = 0; kk < kRK / 32; ++kk) {
-            const int c = kk * 4 + (lane >> 4);
-            bf16x8 af[2], bf[3][2];
+        for (int kk = 0; kk < 2; ++kk) {
+            bf16x8 af[2], wf[3];
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-                af[i] = *(const bf16x8*)(st + roff(wm * 32 + i * 16 + (lane & 15), c));
+            for (int i = 0; i < 2; ++i) af[i] = lds_b128(xb[kk] + S * kRStage + i * 2048);
 #pragma unroll
-            for (int s = 0; s < 3; ++s)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    bf[s][j] = *(const bf16x8*)(st + (1 + s) * kRTile +
-                                                roff(wn * 32 + j * 16 + (lane & 15), c));
+            for (int s = 0; s < 3; ++s) wf[s] = lds_b128(wb[kk] + S * kRStage + s * kRTile);
 #pragma unroll
             for (int s = 2; s >= 0; --s)   // lo, mid, hi: smaller terms first
 #pragma unroll
                 for (int i = 0; i < 2; ++i)
-#pragma unroll
-                    for (int j = 0; j < 2; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bf[s][j], af[i], acc[i][j], 0, 0, 0);
+                    acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[s], af[i], acc[i], 0, 0, 0);
         }
-        if (kt + 1 < nk) store(smem + (cur ^ 1) * 4 * kRTile);
-        __syncthreads();
+    };
+
+    issue(0, D);
+    if (nk > 1) issue(1, (int64_t)D - BK);
+    if (nk > 2) issue(2, (int64_t)D - 2 * BK);
+    for (int kt = 0; kt < nk; kt += kRStages) {
+        step(std::integral_constant<int, 0>{}, kt);
+        if (kt + 1 < nk) step(std::integral_constant<int, 1>{}, kt + 1);
+        if (kt + 2 < nk) step(std::integral_constant<int, 2>{}, kt + 2);
+        if (kt + 3 < nk) step(std::integral_constant<int, 3>{}, kt + 3);
     }
 
     // lane holds logits[t][e .. e+3]
@@ -146,36 +156,42 @@ __global__ __launch_bounds__(256, 2) void router_logits_kernel(const uint16_t* _
     for (int i = 0; i < 2; ++i) {
         const int64_t t = t0 + wm * 32 + i * 16 + (lane & 15);
         if (t >= S) continue;
+        const int e = e0 + wn * 16 + 4 * (lane >> 4);
+        float v[4] = {acc[i][0], acc[i][1], acc[i][2], acc[i][3]};
+        if (bias != nullptr) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int e = e0 + wn * 32 + j * 16 + 4 * (lane >> 4);
-            float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-            if (bias != nullptr) {
+            for (int q = 0; q < 4; ++q)
+                if (e + q < E) v[q] += bias[e + q];
+        }
+        float* dst = logits + t * E + e;
+        if (vec_out && e + 3 < E) {
+            *(float4*)dst = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    if (e + q < E) v[q] += bias[e + q];
-            }
-            float* dst = logits + t * E + e;
-            if (vec_out && e + 3 < E) {
-                *(float4*)dst = make_float4(v[0], v[1], v[2], v[3]);
-            } else {
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    if (e + q < E) dst[q] = v[q];
-            }
+            for (int q = 0; q < 4; ++q)
+                if (e + q < E) dst[q] = v[q];
         }
     }
 }
 
+size_t router_ws_bytes(int D, int E) { return ((size_t)3 * E * D * 2 + 255) / 256 * 256; }
+
 hipError_t launch_router_logits(const moe_bf16* x, const float* Wr, const float* bias, int64_t S,
-                                int D, int E, float* logits, hipStream_t st) {
-    if (S == 0) return hipSuccess;
+                                int D, int E, float* logits, void* ws, hipStream_t st) {
+    uint16_t* w3 = (uint16_t*)ws;
+    hipLaunchKernelGGL(router_split_kernel, dim3((unsigned)((D + 63) / 64), (unsigned)((E + 63) / 64)),
+                       dim3(256), 0, st, Wr, D, E, w3);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess || S == 0) return err;
     dim3 grid(grid_for(S, kRT), (unsigned)((E + kRE - 1) / kRE));
-    // 16-byte vector access only where every row start is 16-byte aligned
-    const bool vec_w = (E % 4) == 0 && ((uintptr_t)Wr % 16) == 0;
+    // 16-byte output stores only where every row start is 16-byte aligned
     const bool vec_out = (E % 4) == 0 && ((uintptr_t)logits % 16) == 0;
-    hipLaunchKernelGGL(router_logits_kernel, grid, dim3(256), 0, st, (const uint16_t*)x, Wr, bias, S,
-                       D, E, logits, vec_w, vec_out);
+    if (D % BK != 0)
+        hipLaunchKernelGGL(router_logits_kernel<true>, grid, dim3(kWaves * 64), 0, st, (const uint16_t*)x,
+                           w3, bias, S, D, E, logits, vec_out);
+    else
+        hipLaunchKernelGGL(router_logits_kernel<false>, grid, dim3(kWaves * 64), 0, st, (const uint16_t*)x,
+                           w3, bias, S, D, E, logits, vec_out);
     return hipGetLastError();
 }
 

@@ -24,7 +24,8 @@ def router_logits(x_r: torch.Tensor, Wr: torch.Tensor, bias: Optional[torch.Tens
     S, D = x_r.shape
     E = Wr.shape[1]
     out = _empty((S, E), F32, x_r.device)
-    L.moe_router_logits(x_r, Wr, bias, S, D, E, out)
+    ws = _ws(L.moe_router_logits_workspace_bytes(D, E), x_r.device)
+    L.moe_router_logits(x_r, Wr, bias, S, D, E, out, ws)
     return out
 
 

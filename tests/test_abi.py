@@ -54,6 +54,10 @@ def test_workspace_queries(lib):
     assert lib.moe_route_workspace_bytes(10, 2048, 2) == 0       # E > 1024
     assert lib.moe_route_workspace_bytes(10, 64, 33) == 0        # K > 32
     assert lib.moe_route_workspace_bytes(2 ** 28, 64, 8) == 0    # S*K >= 2^31
+    assert lib.moe_router_logits_workspace_bytes(2048, 64) == 3 * 2048 * 64 * 2
+    assert lib.moe_router_logits_workspace_bytes(1032, 37) == (3 * 1032 * 37 * 2 + 255) // 256 * 256
+    assert lib.moe_router_logits_workspace_bytes(2044, 64) == 0   # D % 8
+    assert lib.moe_router_logits_workspace_bytes(64, 0) == 0
     assert lib.moe_grouped_ffn_workspace_bytes(64, 49152, 2048, 1024) > 0
     assert lib.moe_grouped_ffn_workspace_bytes(64, 49152, 2044, 1024) == 0   # D % 8
     assert lib.moe_grouped_ffn_bwd_workspace_bytes(8, 100, 64, 64) >= 100 * 64 * 2
@@ -99,8 +103,10 @@ def test_validation_errors_return_before_launch(lib):
     assert lib.moe_grouped_schedule(FAKE, 4, 100, FAKE, 16, st) == -4
     assert lib.moe_grouped_gemm(FAKE, None, 2, 4, 16, 16, FAKE, 1, FAKE, None, st) == -1
     assert lib.moe_grouped_gemm(FAKE, FAKE, 2, 4, 16, 16, FAKE, 2, FAKE, None, st) == -6
-    assert lib.moe_router_logits(FAKE, FAKE, None, 4, 16, 0, FAKE, st) == -2
-    assert lib.moe_router_logits(FAKE, FAKE, ODD, 4, 16, 4, FAKE, st) == -3
+    assert lib.moe_router_logits(FAKE, FAKE, None, 4, 16, 0, FAKE, FAKE, 4096, st) == -2
+    assert lib.moe_router_logits(FAKE, FAKE, ODD, 4, 16, 4, FAKE, FAKE, 4096, st) == -3
+    assert lib.moe_router_logits(FAKE, FAKE, None, 4, 16, 4, FAKE, None, 4096, st) == -4
+    assert lib.moe_router_logits(FAKE, FAKE, None, 4, 16, 4, FAKE, FAKE, 8, st) == -4
     assert lib.moe_combine_bwd(FAKE, FAKE, None, FAKE, 4, 16, 33, FAKE, None, st) == -2
     assert lib.moe_grouped_ffn_bwd(FAKE, None, FAKE, FAKE, FAKE, 2, 4, 16, 16, FAKE, FAKE, FAKE,
                                    FAKE, FAKE, FAKE, 1 << 20, st) == -1
