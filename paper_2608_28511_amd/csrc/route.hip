@@ -4,17 +4,23 @@
 // experts; the grouped-GEMM experts then need the S*K routed rows in
 // expert-contiguous order (fused permutation, Section 5.2).  Three launches:
 //
-//   route_topk     one wavefront per token: K rounds of a wave-wide max over
-//                  64-bit keys (orderable fp32 score | inverted expert id), so
-//                  ties resolve to the lower expert id with no data-dependent
-//                  order; renormalised softmax over the K winners; a per-block
-//                  LDS bitmask per expert gives each (token, slot) its rank
-//                  among the block's rows of that expert and the block's
+//   route_topk     32 tokens per workgroup, 8 per wavefront, all loaded up
+//                  front.  Per token, K rounds of: wave-wide max of the
+//                  orderable 32-bit score codes of the experts not yet picked
+//                  (DPP within rows of 16 lanes, then the 4 row maxima), and
+//                  a ballot for the lowest expert id holding that code (ties
+//                  go to the lower id, NaN ranks below -inf).  Then the
+//                  softmax renormalised over the K winners, and a per-block
+//                  LDS bitmask per expert that gives each (token, slot) its
+//                  rank among the block's rows of that expert and the block's
 //                  per-expert count.
-//   route_scan     one workgroup: exclusive scan of the block counts along
-//                  blocks (per expert) and of the totals along experts.
-//   route_scatter  one thread per routed row: pos = offsets[e] + block base
-//                  + rank; writes perm and inv_perm.
+//   route_colscan  per expert (parallel over experts): exclusive scan of the
+//                  block counts along blocks, in place; the total is
+//                  counts[e].
+//   route_scatter  one thread per routed row; every workgroup first rebuilds
+//                  offsets = exclusive scan of counts in LDS (the first one
+//                  also stores it), then pos = offsets[e] + block base + rank
+//                  gives perm and inv_perm.
 //
 // No step depends on the order in which atomics land (the LDS OR is
 // commutative and ranks come from popcounts), so the permutation is
@@ -26,14 +32,9 @@ namespace moe {
 
 constexpr int kRouteTok = 32;  // tokens per block (one bit each in the masks)
 constexpr int kRouteThreads = 256;
-constexpr int kScanThreads = 1024;
-
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
-    uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
-    lo = __shfl_xor(lo, m);
-    hi = __shfl_xor(hi, m);
-    return ((uint64_t)hi << 32) | lo;
-}
+constexpr int kTokPerWave = kRouteTok / (kRouteThreads / kWave);  // 8
+constexpr int kScanCols = 4;    // experts per route_colscan workgroup
+constexpr int kScanThreads = 256;
 
 // Monotone map of an fp32 score to uint32 (larger score -> larger code).
 // -0 is folded onto +0 and NaN maps to 0, below the code of -inf.
@@ -49,6 +50,18 @@ __device__ __forceinline__ float code_score(uint32_t c) {
     return __uint_as_float(u);
 }
 
+// Maximum of v over the 64 lanes (all active), returned wave-uniform.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    // pairs, quads, half rows, rows of 16 lanes: full permutations within a row
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xf, 0xf, false));   // quad_perm 1,0,3,2
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xf, 0xf, false));   // quad_perm 2,3,0,1
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xf, 0xf, false));  // row_half_mirror
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xf, 0xf, false));  // row_mirror
+    const uint32_t a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);
+    const uint32_t c = __builtin_amdgcn_readlane(v, 32), d = __builtin_amdgcn_readlane(v, 48);
+    return max(max(a, b), max(c, d));
+}
+
 template <int EPL>
 __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
     const float* __restrict__ logits, int64_t S, int E, int K, int32_t* __restrict__ topk_idx,
@@ -58,48 +71,62 @@ __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t t_base = (int64_t)blockIdx.x * kRouteTok;
     for (int e = tid; e < E; e += kRouteThreads) mask[e] = 0u;
-    __syncthreads();
 
-    for (int j = wave; j < kRouteTok; j += kRouteThreads / kWave) {
-        const int64_t t = t_base + j;
-        if (t >= S) break;
-        const float* row = logits + t * E;
-        uint64_t key[EPL];
+    // this wave's tokens t_base + wave*8 + j: every score code loaded up front
+    uint32_t code[kTokPerWave][EPL];
+#pragma unroll
+    for (int j = 0; j < kTokPerWave; ++j) {
+        const int64_t t = t_base + wave * kTokPerWave + j;
 #pragma unroll
         for (int i = 0; i < EPL; ++i) {
             const int e = lane + kWave * i;
-            key[i] = (e < E) ? (((uint64_t)score_code(row[e]) << 32) | (uint32_t)(0xffffu - e)) : 0ull;
+            code[j][i] = (t < S && e < E) ? score_code(logits[t * E + e]) : 0u;
         }
+    }
+    __syncthreads();
+
+#pragma unroll
+    for (int j = 0; j < kTokPerWave; ++j) {
+        const int jt = wave * kTokPerWave + j;
+        const int64_t t = t_base + jt;
+        if (t >= S) break;
+        uint32_t taken = 0;  // bit i: expert lane + 64 i picked (or beyond E)
+#pragma unroll
+        for (int i = 0; i < EPL; ++i)
+            if (lane + kWave * i >= E) taken |= 1u << i;
         int my_e = 0;
         float my_s = 0.f;
         for (int k = 0; k < K; ++k) {
-            uint64_t best = key[0];
-#pragma unroll
-            for (int i = 1; i < EPL; ++i) best = key[i] > best ? key[i] : best;
-#pragma unroll
-            for (int m = 32; m > 0; m >>= 1) {
-                const uint64_t o = shfl_xor_u64(best, m);
-                best = o > best ? o : best;
-            }
-            const int e = 0xffff - (int)(uint32_t)(best & 0xffffffffu);
+            uint32_t m = 0;
 #pragma unroll
             for (int i = 0; i < EPL; ++i)
-                if (lane + kWave * i == e) key[i] = 0ull;
+                if (!(taken >> i & 1u)) m = max(m, code[j][i]);
+            m = wave_max_u32(m);
+            int e_sel = 0;
+#pragma unroll
+            for (int i = 0; i < EPL; ++i) {
+                const uint64_t b = __ballot(!(taken >> i & 1u) && code[j][i] == m);
+                if (b != 0) {
+                    e_sel = kWave * i + (__ffsll((unsigned long long)b) - 1);
+                    break;
+                }
+            }
+            if (lane == (e_sel & (kWave - 1))) taken |= 1u << (e_sel / kWave);
             if (lane == k) {
-                my_e = e;
-                my_s = code_score((uint32_t)(best >> 32));
+                my_e = e_sel;
+                my_s = code_score(m);
             }
         }
         const float s0 = __shfl(my_s, 0);
         float z = (lane < K) ? expf(my_s - s0) : 0.f;
         float sum = z;
 #pragma unroll
-        for (int m = 32; m > 0; m >>= 1) sum += __shfl_xor(sum, m);
+        for (int msk = 32; msk > 0; msk >>= 1) sum += __shfl_xor(sum, msk);
         if (lane < K) {
             topk_idx[t * K + lane] = my_e;
             topk_prob[t * K + lane] = z / sum;
-            sel[j][lane] = (int16_t)my_e;
-            atomicOr(&mask[my_e], 1u << j);
+            sel[jt][lane] = (int16_t)my_e;
+            atomicOr(&mask[my_e], 1u << jt);
         }
     }
     __syncthreads();
@@ -114,77 +141,87 @@ __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
         blkcnt[(int64_t)blockIdx.x * E + e] = __popc(mask[e]);
 }
 
-// One workgroup. blkcnt[b*E+e] (per-block counts) is replaced in place by the
-// number of rows of expert e in blocks before b.  counts[e] = total rows of
-// e; offsets = exclusive scan of counts with offsets[E] = total.
-__global__ __launch_bounds__(kScanThreads) void route_scan_kernel(int32_t* __restrict__ blkcnt, int nblk,
-                                                                  int E, int32_t* __restrict__ counts,
-                                                                  int32_t* __restrict__ offsets) {
-    __shared__ int32_t part[kScanThreads];
-    __shared__ int32_t tot[kScanThreads];
+// blkcnt[b*E+e] (rows of expert e in token block b) is replaced in place by
+// the rows of e in blocks before b; counts[e] = all rows of e.  A workgroup
+// takes kScanCols experts; its 256 threads split the blocks into 64 chunks.
+__global__ __launch_bounds__(kScanThreads) void route_colscan_kernel(int32_t* __restrict__ blkcnt, int nblk,
+                                                                     int E, int32_t* __restrict__ counts) {
+    constexpr int kChunks = kScanThreads / kScanCols;  // 64
+    __shared__ int32_t part[kChunks][kScanCols];
     const int tid = threadIdx.x;
-    int P = kScanThreads / E;
-    if (P > 32) P = 32;
-    if (P < 1) P = 1;
-    const int chunk = (nblk + P - 1) / P;
-    for (int e0 = 0; e0 < E; e0 += kScanThreads) {
-        // lanes: e = e0 + tid % Ew, part index tid / Ew (Ew experts handled per pass)
-        const int Ew = (E - e0) < kScanThreads / P ? (E - e0) : kScanThreads / P;
-        const int e = e0 + tid % Ew;
-        const int pi = tid / Ew;
-        const bool active = pi < P && (tid < Ew * P);
-        const int b0 = pi * chunk;
-        const int b1 = (b0 + chunk) < nblk ? (b0 + chunk) : nblk;
-        int s = 0;
-        if (active)
-            for (int b = b0; b < b1; ++b) s += blkcnt[(int64_t)b * E + e];
-        part[tid] = s;
-        __syncthreads();
-        int before = 0, total = 0;
-        if (active) {
-            for (int q = 0; q < P; ++q) {
-                const int v = part[q * Ew + (tid % Ew)];
-                if (q < pi) before += v;
-                total += v;
-            }
-            int run = before;
-            for (int b = b0; b < b1; ++b) {
-                const int64_t ix = (int64_t)b * E + e;
-                const int c = blkcnt[ix];
-                blkcnt[ix] = run;
-                run += c;
-            }
-            if (pi == 0) tot[e] = total;
-        }
-        __syncthreads();
-    }
-    // exclusive scan of tot[0..E) (Hillis-Steele over 1024 slots)
-    int v = tid < E ? tot[tid] : 0;
-    if (tid < E) counts[tid] = v;
-    part[tid] = v;
+    const int c = tid % kScanCols, q = tid / kScanCols;
+    const int e = blockIdx.x * kScanCols + c;
+    const int chunk = (nblk + kChunks - 1) / kChunks;
+    const int b0 = q * chunk;
+    const int b1 = (b0 + chunk) < nblk ? (b0 + chunk) : nblk;
+    int s = 0;
+    if (e < E)
+        for (int b = b0; b < b1; ++b) s += blkcnt[(int64_t)b * E + e];
+    part[q][c] = s;
     __syncthreads();
-    for (int d = 1; d < kScanThreads; d <<= 1) {
-        const int add = tid >= d ? part[tid - d] : 0;
-        __syncthreads();
-        part[tid] += add;
-        __syncthreads();
+    if (e >= E) return;
+    int before = 0, total = 0;
+    for (int r = 0; r < kChunks; ++r) {
+        const int v = part[r][c];
+        before += r < q ? v : 0;
+        total += v;
     }
-    if (tid < E) offsets[tid + 1] = part[tid];
-    if (tid == 0) offsets[0] = 0;
+    int run = before;
+    for (int b = b0; b < b1; ++b) {
+        const int64_t ix = (int64_t)b * E + e;
+        const int v = blkcnt[ix];
+        blkcnt[ix] = run;
+        run += v;
+    }
+    if (q == 0) counts[e] = total;
 }
 
 __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __restrict__ topk_idx,
                                                             const int32_t* __restrict__ blkbase,
-                                                            const int32_t* __restrict__ offsets,
+                                                            const int32_t* __restrict__ counts,
+                                                            int32_t* __restrict__ offsets,
                                                             int32_t* __restrict__ inv_perm,
                                                             int32_t* __restrict__ perm, int64_t R,
                                                             int K, int E) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    __shared__ int32_t off[1024];
+    __shared__ int32_t wsum[4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // exclusive scan of counts[0..E): each thread owns 4 consecutive experts
+    int v[4], run = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int e = tid * 4 + u;
+        v[u] = e < E ? counts[e] : 0;
+        run += v[u];
+    }
+    int incl = run;  // inclusive scan of the per-thread sums within the wave
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const int o = __shfl_up(incl, d);
+        if (lane >= d) incl += o;
+    }
+    if (lane == kWave - 1) wsum[wave] = incl;
+    __syncthreads();
+    int base = incl - run;
+    for (int w = 0; w < wave; ++w) base += wsum[w];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int e = tid * 4 + u;
+        if (e < E) off[e] = base;
+        base += v[u];
+    }
+    __syncthreads();
+    if (blockIdx.x == 0) {
+        for (int e = tid; e < E; e += 256) offsets[e] = off[e];
+        if (tid == 0) offsets[E] = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    }
+
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + tid;
     if (i >= R) return;
     const int64_t t = i / K;
     const int e = topk_idx[i];
     const int64_t b = t / kRouteTok;
-    const int pos = offsets[e] + blkbase[b * E + e] + inv_perm[i];
+    const int pos = off[e] + blkbase[b * E + e] + inv_perm[i];
     if ((uint32_t)pos >= (uint64_t)R) return;  // unreachable for consistent counts
     perm[pos] = (int32_t)i;
     inv_perm[i] = pos;
@@ -212,13 +249,12 @@ hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* t
         else MOE_ROUTE_CASE(16);
 #undef MOE_ROUTE_CASE
     }
-    hipLaunchKernelGGL(route_scan_kernel, dim3(1), dim3(kScanThreads), 0, st, blkcnt, nblk, E,
-                       counts, offsets);
-    if (S > 0) {
-        const int64_t R = S * K;
-        hipLaunchKernelGGL(route_scatter_kernel, dim3(grid_for(R, 256)), dim3(256), 0, st, topk_idx,
-                           blkcnt, offsets, inv_perm, perm, R, K, E);
-    }
+    hipLaunchKernelGGL(route_colscan_kernel, dim3((unsigned)((E + kScanCols - 1) / kScanCols)),
+                       dim3(kScanThreads), 0, st, blkcnt, nblk, E, counts);
+    const int64_t R = S * K;
+    // at least one workgroup, so that offsets are written even for S == 0
+    hipLaunchKernelGGL(route_scatter_kernel, dim3(R > 0 ? grid_for(R, 256) : 1u), dim3(256), 0, st,
+                       topk_idx, blkcnt, counts, offsets, inv_perm, perm, R, K, E);
     return hipGetLastError();
 }
 
