@@ -183,8 +183,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) 
 
     DmaTile<false, BM> da;
     DmaTile<false, BN> db;
-    da.init(p.A, p.lda, row0, row_hi, k_begin, wave, lane);
-    db.init(p.B, p.ldb, n0, (int64_t)p.N, k_begin, wave, lane);
+    da.init(p.A, p.lda, row0, row_hi, k_begin, k_end, wave, lane);
+    db.init(p.B, p.ldb, n0, (int64_t)p.N, k_begin, k_end, wave, lane);
     constexpr int kPerStage = DmaTile<false, BM>::kSlots + DmaTile<false, BN>::kSlots;
 
     uint32_t abase[4], bbase[2][4];
@@ -238,17 +238,16 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) 
 // ROWS mode, persistent.
 
 struct RowsTile {
-    int e;
-    int64_t row0, row_hi, n0;
+    int e, row0, row_hi, n0;  // rows and columns are below 2^31
 };
 
 // Work item w -> output tile: 8 m-tiles at a time across all n-tiles.
-__device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, int m_total, int64_t w) {
-    const int64_t width = (int64_t)kGroupM * p.n_tiles;
-    const int64_t group = w / width;
-    const int first_m = (int)(group * kGroupM);
+__device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, int m_total, int w) {
+    const int width = kGroupM * p.n_tiles;
+    const int group = w / width;
+    const int first_m = group * kGroupM;
     const int gsz = (m_total - first_m) < kGroupM ? (m_total - first_m) : kGroupM;
-    const int in = (int)(w - group * width);
+    const int in = w - group * width;
     const int mt = __builtin_amdgcn_readfirstlane(first_m + in % gsz);
     const int nt = in / gsz;
     RowsTile t;
@@ -262,10 +261,10 @@ __device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, int m_total, in
         t.row_hi = ti[2];
     } else {
         t.e = 0;
-        t.row0 = (int64_t)mt * BM;
-        t.row_hi = (t.row0 + BM) < p.M ? (t.row0 + BM) : p.M;
+        t.row0 = mt * BM;
+        t.row_hi = (t.row0 + BM) < p.M ? (t.row0 + BM) : (int)p.M;
     }
-    t.n0 = (int64_t)nt * BN;
+    t.n0 = nt * BN;
     return t;
 }
 
@@ -368,12 +367,12 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     const int m_total = p.mtile_total != nullptr
                             ? *(const __attribute__((address_space(4))) int32_t*)p.mtile_total
                             : p.m_tiles;
-    const int64_t n_work = (int64_t)m_total * p.n_tiles;
+    const int n_work = m_total * p.n_tiles;
     const int G = gridDim.x;
     const int first = (int)(blockIdx.x % kXcds) * (G / kXcds) + (int)(blockIdx.x / kXcds);
-    const int64_t n_mine = first < n_work ? (n_work - first + G - 1) / G : 0;
+    const int n_mine = first < n_work ? (n_work - first + G - 1) / G : 0;
     const int nk = (p.Kd + BK - 1) / BK;
-    const int64_t g_total = n_mine * nk;  // (tile, k step) pairs
+    const int g_total = n_mine * nk;  // (tile, k step) pairs
     if (g_total == 0) return;
 
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char*)smem;
@@ -384,10 +383,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     DmaTile<B_K, BN> db;
     constexpr int kSA = DmaTile<true, BM>::kSlots, kSB = DmaTile<B_K, BN>::kSlots;
     constexpr int kPerStage = kSA + kSB;
-    auto dma_tile = [&](int64_t j) {
+    auto dma_tile = [&](int j) {
         const RowsTile t = rows_tile(p, m_total, first + j * G);
-        da.init(p.A, p.lda, t.row0, t.row_hi, 0, wave, lane);
-        db.init(p.B + (int64_t)t.e * p.b_stride, p.ldb, t.n0, (int64_t)p.N, 0, wave, lane);
+        da.init(p.A, p.lda, t.row0, t.row_hi, 0, p.Kd, wave, lane);
+        db.init(p.B + (int64_t)t.e * p.b_stride, p.ldb, t.n0, (int64_t)p.N, 0, p.Kd, wave, lane);
     };
 
     constexpr int kNB = B_K ? 2 : 4;
@@ -402,20 +401,20 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     da.template issue<KTAIL, 0, kSA>(ldsA, p.Kd, wave);
     db.template issue<KTAIL, 0, kSB>(ldsB, p.Kd, wave);
     int kd = 1 % nk;
-    int64_t jd = 1 / nk;
+    int jd = 1 / nk;
     if (g_total > 1) {
         if (kd == 0) dma_tile(jd);
-        const int64_t rem = (int64_t)p.Kd - (int64_t)kd * BK;
+        const int rem = p.Kd - kd * BK;
         da.template issue<KTAIL, 0, kSA>(ldsA + kABytes, rem, wave);
         db.template issue<KTAIL, 0, kSB>(ldsB + kBBytes, rem, wave);
     }
     if (++kd == nk) { kd = 0; ++jd; }
 
-    int kc = 0;        // k step of the tile being computed
-    int64_t jc = 0;    // its index in this workgroup's list
+    int kc = 0;   // k step of the tile being computed
+    int jc = 0;   // its index in this workgroup's list
     RowsTile cur = rows_tile(p, m_total, first);
 
-    auto step = [&](auto stage_c, int64_t g) {
+    auto step = [&](auto stage_c, int g) {
         constexpr int S = decltype(stage_c)::value;
         // Stores of an epilogue may still be in flight; they are not counted,
         // so the wait covers this stage's copies whichever way they complete.
@@ -423,13 +422,12 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
         stage_barrier();
         const bool next = g + 2 < g_total;
         if (next && kd == 0) dma_tile(jd);
-        mma_stage<true, B_K, KTAIL, S>(acc, abase, bbase, da, db, next,
-                                       (int64_t)p.Kd - (int64_t)kd * BK, ldsA, ldsB, wave);
+        mma_stage<true, B_K, KTAIL, S>(acc, abase, bbase, da, db, next, p.Kd - kd * BK, ldsA, ldsB, wave);
         if (++kd == nk) { kd = 0; ++jd; }
         if (kc == nk - 1) {
-            const int64_t rbase = cur.row0 + wm * 64;
-            const int64_t nrows = cur.row_hi - rbase;
-            const int64_t cbase = cur.n0 + wn * 64;
+            const int rbase = cur.row0 + wm * 64;
+            const int nrows = cur.row_hi - rbase;
+            const int cbase = cur.n0 + wn * 64;
             if constexpr (EPI == EPI_DRELU2) {
                 drelu2_store(acc, p.C, p.aux_in, p.ldc, p.N, rbase, nrows, cbase, lane);
             } else {
@@ -447,7 +445,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
         }
     };
 
-    for (int64_t g = 0; g < g_total; g += kStages) {
+    for (int g = 0; g < g_total; g += kStages) {
         step(std::integral_constant<int, 0>{}, g);
         if (g + 1 < g_total) step(std::integral_constant<int, 1>{}, g + 1);
         if (g + 2 < g_total) step(std::integral_constant<int, 2>{}, g + 2);
@@ -571,6 +569,8 @@ hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B
     a.n_tiles = (N + BN - 1) / BN;
     a.m_tiles = (int)(sched ? mtiles_bound(R, E) : (R + BM - 1) / BM);
     if (R == 0) return hipSuccess;
+    // the DMA descriptor of an N-contiguous B spans its whole contraction
+    if (!b_kmajor && (int64_t)Kd * ldb * 2 >= kMaxDmaBytes) return hipErrorInvalidValue;
     if (!b_kmajor) {
         if (epi == EPI_BF16) return launch_rows<false, EPI_BF16>(a, st);
         if (epi == EPI_RELU2) return launch_rows<false, EPI_RELU2>(a, st);
@@ -592,6 +592,8 @@ hipError_t launch_grouped_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* 
     a.n_tiles = (N + BN - 1) / BN;
     const int64_t n_wg = (int64_t)E * a.m_tiles * a.n_tiles;
     if (n_wg <= 0) return hipSuccess;
+    // DMA descriptors span an expert's rows of both operands
+    if (R * (lda > ldb ? lda : ldb) * 2 >= kMaxDmaBytes) return hipErrorInvalidValue;
     if (n_wg > 0x7fffffff) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(gemm_kgrp_kernel, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a);
     return hipGetLastError();

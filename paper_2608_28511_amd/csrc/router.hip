@@ -97,9 +97,9 @@ __global__ __launch_bounds__(kWaves * 64, 1) void router_logits_kernel(const uin
     const int64_t plane = (int64_t)E * D;
 
     DmaTile<true, 64> dx, dw[3];
-    dx.init(x, D, t0, S, 0, wave, lane);
+    dx.init(x, D, t0, S, 0, D, wave, lane);
 #pragma unroll
-    for (int s = 0; s < 3; ++s) dw[s].init(w3 + s * plane, D, e0, E, 0, wave, lane);
+    for (int s = 0; s < 3; ++s) dw[s].init(w3 + s * plane, D, e0, E, 0, D, wave, lane);
 
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char*)smem;
     auto issue = [&](int stage, int64_t rem) {

@@ -23,8 +23,7 @@ typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 typedef __attribute__((address_space(3))) char lds_char;
 
-// One zero chunk: the source of every out-of-range DMA lane.
-static __device__ __attribute__((aligned(16))) uint4 g_zero_chunk[1];
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 // ---- row layout: [rows][64 k], 8 chunks per row; chunk c of row r stored at
 // c ^ (r & 7).  The fragments of rows r and r + 16 then sit a constant 2 KB
@@ -41,15 +40,32 @@ __device__ __forceinline__ int rswz(int r) { return r & 7; }
 // and k + 32 sit constant offsets away.
 __device__ __forceinline__ int cswz(int k) { return 2 * ((k & 3) | (((k >> 3) & 1) << 2)); }
 
-// 16-byte global -> LDS copy for the whole wave: lane l's chunk lands at LDS
-// byte lds_addr + 16*l (lds_addr wave-uniform).  Issued as inline assembly so
+// Range-checked buffer descriptor over [base, base + bytes): every access at
+// or past `bytes` reads as zero without touching memory.  bytes < 2^31.
+__device__ __forceinline__ i32x4 buf_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t a = (uint64_t)(uintptr_t)base;
+    return i32x4{(int)(uint32_t)a, (int)((uint32_t)(a >> 32) & 0xffffu), (int)bytes, 0x00020000};
+}
+
+// An offset beyond every descriptor's range, with room to advance by a whole
+// operand (< 2^31 bytes) without wrapping.
+constexpr uint32_t kDmaDrop = 0x80000000u;
+constexpr int64_t kMaxDmaBytes = (int64_t)1 << 31;  // descriptor ranges stay below this
+
+// 16-byte buffer -> LDS copy for the whole wave: lane l's chunk (byte offset
+// `off` in the descriptor's range, zero if outside it) lands at LDS byte
+// lds_addr + 16*l (lds_addr wave-uniform).  Issued as inline assembly so
 // that the compiler does not treat it as an LDS write that every later LDS
-// read must wait for; the kernel orders it with explicit vmcnt waits and
+// read must wait for; the kernels order it with explicit vmcnt waits and
 // barriers instead.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+__device__ __forceinline__ void dma16(const i32x4& rs, uint32_t off, uint32_t lds_addr) {
+    // descriptor and LDS base are wave-uniform: pin them to scalar registers
+    const i32x4 srs = {__builtin_amdgcn_readfirstlane(rs[0]), __builtin_amdgcn_readfirstlane(rs[1]),
+                       __builtin_amdgcn_readfirstlane(rs[2]), __builtin_amdgcn_readfirstlane(rs[3])};
+    const uint32_t sdst = __builtin_amdgcn_readfirstlane(lds_addr);
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
                  :
-                 : "v"(g), "s"(lds_addr)
+                 : "v"(off), "s"(srs), "s"(sdst)
                  : "memory", "m0");
 }
 
@@ -72,24 +88,38 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // Per-lane DMA slots of one operand tile.  Slot i of a wave covers LDS bytes
 // [(wave*kSlots + i)*1024, +1024) of the tile; each lane's 16-byte chunk has a
-// fixed global row / column for the whole k loop, so its pointer advances by
-// one k tile per stage (by zero for chunks outside the operand, which keep
-// pointing at the zero chunk).  Only a tile that crosses the end of the
-// contraction re-checks the k coordinate.
+// fixed row / column for the whole k loop, so its byte offset advances by one
+// k tile per stage.  The descriptor spans only the tile's part of the operand,
+// so chunks past its rows (ragged expert segments, the end of the contraction
+// for the column layout) read as zero; chunks past its columns start at
+// kDmaDrop.
 //
-// Row layout (K-contiguous source, element (r, k) at src[r*ld + k]).
-// Col layout (M/N-contiguous source, element (k, c) at src[k*ld + c]).
+// Row layout (K-contiguous source, element (r, k) at src[r*ld + k]): rows
+//   [x0, min(x_hi, x0 + EXT)), k from k_begin.  A contraction that ends inside
+//   a k tile (KTAIL) is cut per chunk at issue time.
+// Col layout (M/N-contiguous source, element (k, c) at src[k*ld + c]): k rows
+//   [k_begin, k_end), columns [x0, x_hi).
 template <bool ROWL, int EXT>
 struct DmaTile {
     static constexpr int kCPR = ROWL ? 8 : EXT / 8;       // chunks per LDS row
     static constexpr int kSlots = EXT * 8 / 64 / kWaves;  // 1 KB slots per wave
-    const uint16_t* ptr[kSlots];
-    int64_t step[kSlots];
-    int kpos[kSlots];      // k offset of the chunk inside the tile
-    bool ok[kSlots];
+    i32x4 rs;                // wave-uniform
+    uint32_t kstep;          // bytes per k tile, wave-uniform
+    uint32_t off[kSlots];
+    int kpos[kSlots];        // row layout: k offset of the chunk inside the tile
 
     __device__ __forceinline__ void init(const uint16_t* __restrict__ src, int64_t ld, int64_t x0,
-                                         int64_t x_hi, int64_t k_begin, int wave, int lane) {
+                                         int64_t x_hi, int64_t k_begin, int64_t k_end, int wave, int lane) {
+        if (ROWL) {
+            const int64_t x_end = (x0 + EXT) < x_hi ? (x0 + EXT) : x_hi;
+            const int64_t rows = x_end > x0 ? x_end - x0 : 0;
+            rs = buf_rsrc(src + x0 * ld + k_begin, (uint32_t)(rows * ld * 2));
+            kstep = BK * 2;
+        } else {
+            const int64_t krows = k_end > k_begin ? k_end - k_begin : 0;
+            rs = buf_rsrc(src + k_begin * ld + x0, (uint32_t)(krows > 0 ? krows * ld * 2 - x0 * 2 : 0));
+            kstep = (uint32_t)(BK * ld * 2);
+        }
 #pragma unroll
         for (int i = 0; i < kSlots; ++i) {
             const int p = (wave * kSlots + i) * 64 + lane;
@@ -97,32 +127,27 @@ struct DmaTile {
             int c = p % kCPR;
             if (ROWL) {
                 c ^= rswz(row);
-                ok[i] = x0 + row < x_hi;
                 kpos[i] = c * 8;
-                ptr[i] = ok[i] ? src + (x0 + row) * ld + k_begin + c * 8 : (const uint16_t*)g_zero_chunk;
-                step[i] = ok[i] ? (int64_t)BK : 0;
+                off[i] = (uint32_t)((row * ld + c * 8) * 2);
             } else {
                 c ^= cswz(row);
-                ok[i] = x0 + c * 8 < x_hi;
                 kpos[i] = row;
-                ptr[i] = ok[i] ? src + (k_begin + row) * ld + x0 + c * 8 : (const uint16_t*)g_zero_chunk;
-                step[i] = ok[i] ? (int64_t)BK * ld : 0;
+                off[i] = x0 + c * 8 < x_hi ? (uint32_t)((row * ld + c * 8) * 2) : kDmaDrop;
             }
         }
     }
     // Issue this wave's slots [I0, I1) of the next tile in k order, then
-    // advance.  KTAIL: the contraction length may end inside a tile, so chunks
-    // at or past k_rem are replaced by the zero chunk.
+    // advance.  KTAIL (row layout): chunks at or past k_rem, the contraction
+    // left from this tile's start, read as zero.
     template <bool KTAIL, int I0, int I1>
     __device__ __forceinline__ void issue(uint32_t tile_lds, int64_t k_rem, int wave) {
 #pragma unroll
         for (int i = I0; i < I1; ++i) {
             const uint32_t dst = tile_lds + (uint32_t)(wave * kSlots + i) * 1024u;
-            if constexpr (KTAIL)
-                dma16(kpos[i] < k_rem ? (const void*)ptr[i] : (const void*)g_zero_chunk, dst);
-            else
-                dma16(ptr[i], dst);
-            ptr[i] += step[i];
+            uint32_t o = off[i];
+            if constexpr (KTAIL && ROWL) o = kpos[i] < k_rem ? o : kDmaDrop;
+            dma16(rs, o, dst);
+            off[i] += kstep;
         }
     }
 };
