@@ -44,8 +44,8 @@ def parse():
     p.add_argument("--workload", default="base_s8192_d2048_e64_k6")
     p.add_argument("--sets", type=int, default=3, help="rotating input sets")
     p.add_argument("--stage-reps", type=int, default=20)
-    p.add_argument("--cpu-tokens", type=int, default=3072,
-                   help="tokens of the batch the CPU oracle runs (about 10-30 s on 16 cores)")
+    p.add_argument("--cpu-tokens", type=int, default=0,
+                   help="tokens of the batch the CPU oracle runs (0: the whole batch)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--calib-bytes", type=int, default=1 << 30,
                    help="size of the plain copy run once for counter calibration")
@@ -64,9 +64,9 @@ def parse():
 # scaled by what it reads for the plain 1 GiB device copy this script runs at
 # start-up (a copy reads and writes exactly 1 GiB).  The summary records a
 # digest of the GEMM sources; once they change, `traffic` is reported as null.
-GEMM_SOURCES = ("gemm.hip", "kernels.h", "common.h")
-KERNEL_NAME = {"grouped_up": "gemm_kernel<0, true, false, 1, false>",
-               "grouped_down": "gemm_kernel<0, true, false, 0, false>"}
+GEMM_SOURCES = ("gemm.hip", "tile_dma.h", "kernels.h", "common.h")
+KERNEL_NAME = {"grouped_up": "gemm_rows_kernel<false, 1, false>",
+               "grouped_down": "gemm_rows_kernel<false, 0, false>"}
 
 
 def gemm_digest():
@@ -93,14 +93,14 @@ def load_traffic(kernel, workload):
 
 
 def counter_rows(d):
+    """Rows of the newest counter_collection.csv under d (one profiler run)."""
     import csv
-    files = sorted(Path(d).rglob("*counter_collection.csv"))
+    files = sorted(Path(d).rglob("*counter_collection.csv"), key=lambda f: f.stat().st_mtime)
     if not files:
         raise SystemExit(f"no counter_collection.csv under {d}")
-    rows = []
-    for f in files:
-        rows += list(csv.DictReader(open(f)))
-    return rows
+    if len(files) > 1:
+        log(f"{d}: {len(files)} counter files, using the newest ({files[-1].name})")
+    return list(csv.DictReader(open(files[-1])))
 
 
 def per_dispatch(rows, counter, match):
@@ -140,10 +140,15 @@ def write_traffic(d_fetch, d_write, workload, kernel, calib_bytes):
 def stage_bytes(s):
     S, D, E, K, F, R = s.S, s.D, s.E, s.K, s.F, s.R
     return {
-        "router_logits": S * D * 2 + D * E * 4 + S * E * 4,
+        # x read, Wr read and split into three bf16 planes, planes re-read per
+        # 64-token tile from L2 (not counted), logits written
+        "router_logits": S * D * 2 + D * E * 4 + 3 * D * E * 2 + S * E * 4,
         "route": S * E * 4 + R * 16 + (2 * E + 1) * 4,
         "dispatch": S * D * 2 + R * 8 + R * (2 * D + 4),
         "combine": R * (2 * D + 8) + S * D * 2,
+        # dy read once per slot, y_disp and p read, dy_disp written, dp written
+        "combine_bwd": S * D * 2 + R * (2 * D + 8) + R * 2 * D + R * 4,
+        "dispatch_bwd": R * (2 * D + 4) + S * D * 2,
     }
 
 
@@ -169,7 +174,7 @@ def cpu_baseline(s, inp, tokens):
 
     from oracle import moe_oracle as O
 
-    T = min(tokens, s.S)
+    T = s.S if tokens <= 0 else min(tokens, s.S)
     x = inp["x"][:T].cpu().to(torch.float64).numpy()
     Wr = inp["Wr"].cpu().to(torch.float64).numpy()
     bias = None if inp["bias"] is None else inp["bias"].cpu().to(torch.float64).numpy()
@@ -289,19 +294,49 @@ def main():
             lambda i: _lib.moe_latent_proj(sets[i % len(sets)]["x"], sets[i % len(sets)]["Wdown"],
                                            s.S, s.H, s.D, out["x_lat"]), reps, stream)
 
+    if s.backward:
+        # backward stages (reported per stage; `value` stays the forward rate)
+        lb = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, save_u=True)
+        ob = lb(sets[0]["x"], sets[0]["Wr"], sets[0]["W1"], sets[0]["W2"], bias=sets[0]["bias"])
+        dy = sets[0]["dy"]
+        dy_disp = torch.empty_like(ob["x_disp"])
+        dp = torch.empty((s.S, s.K), dtype=torch.float32, device=dev)
+        dx_disp = torch.empty_like(ob["x_disp"])
+        dW1 = torch.empty((s.E, s.D, s.F), dtype=torch.float32, device=dev)
+        dW2 = torch.empty((s.E, s.F, s.D), dtype=torch.float32, device=dev)
+        dx = torch.empty((s.S, s.D), dtype=torch.bfloat16, device=dev)
+        ws_bwd = torch.empty(max(1, _lib.moe_grouped_ffn_bwd_workspace_bytes(s.E, s.R, s.D, s.F)),
+                             dtype=torch.uint8, device=dev)
+        st["combine_bwd"] = time_region(
+            lambda i: _lib.moe_combine_bwd(dy, ob["y_disp"], ob["p_disp"], ob["inv_perm"], s.S, s.D, s.K,
+                                           dy_disp, dp), reps, stream)
+        st["grouped_ffn_bwd"] = time_region(
+            lambda i: _lib.moe_grouped_ffn_bwd(ob["x_disp"], ob["u_save"], ob["h"], dy_disp, ob["offsets"],
+                                               s.E, s.R, s.D, s.F, sets[0]["W1"], sets[0]["W2"], dx_disp,
+                                               dW1, dW2, ws_bwd), max(2, reps // 4), stream)
+        st["dispatch_bwd"] = time_region(
+            lambda i: _lib.moe_dispatch_bwd(dx_disp, ob["inv_perm"], s.S, s.D, s.K, dx), reps, stream)
+        del lb, ob, dy_disp, dx_disp, dW1, dW2, ws_bwd
+
     bytes_ = stage_bytes(s)
     gemm_flops = 2.0 * s.R * s.D * s.F
     stages = {}
     for k, t in st.items():
         e = {"us": round(t * 1e6, 2)}
-        if k in ("route", "dispatch", "combine"):
+        if k in ("route", "dispatch", "combine", "combine_bwd", "dispatch_bwd"):
             gbs = bytes_[k] / t / 1e9
             e.update(bytes=bytes_[k], GBps=round(gbs, 1), hbm_frac=round(gbs / PEAK_HBM_GBS, 4))
         elif k == "router_logits":
+            # fp32 products computed as three bf16 MFMAs; bounded by HBM
             tf = 2.0 * s.S * s.D * s.E / t / 1e12
-            e.update(TFLOPs=round(tf, 2), fp32_frac=round(tf / PEAK_FP32_TFLOPS, 4))
+            gbs = bytes_[k] / t / 1e9
+            e.update(TFLOPs_fp32_equiv=round(tf, 2), bytes=bytes_[k], GBps=round(gbs, 1),
+                     hbm_frac=round(gbs / PEAK_HBM_GBS, 4))
         else:
-            fl = gemm_flops if k.startswith("grouped") else 2.0 * s.S * s.H * s.D
+            if k == "grouped_ffn_bwd":
+                fl = 4.0 * gemm_flops      # dgrad and wgrad of both projections
+            else:
+                fl = gemm_flops if k.startswith("grouped") else 2.0 * s.S * s.H * s.D
             tf = fl / t / 1e12
             e.update(flops=fl, TFLOPs=round(tf, 1), mfma_frac=round(tf / PEAK_BF16_TFLOPS, 4))
         stages[k] = e

@@ -32,7 +32,11 @@
  *     inputs give bit-identical outputs on every call.
  *   - S == 0 (or R == 0) is valid and enqueues nothing.
  *   - Limits: 1 <= E <= 1024, 1 <= K <= min(E, 32), D and F multiples of 8
- *     in [8, 65536], S*K < 2^31.
+ *     in [8, 65536], S*K < 2^31.  The grouped GEMM copies its
+ *     operands through range-checked buffer descriptors of at most 2^31
+ *     bytes, so one expert's weight (D*F*2 bytes; H*D*2 for the latent
+ *     projections) and, for the weight gradients, S*K*max(D, F)*2 must stay
+ *     below 2^31; larger requests return MOE_ERR_UNSUPPORTED.
  */
 #ifndef MOE_H
 #define MOE_H

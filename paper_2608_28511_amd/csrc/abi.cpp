@@ -33,6 +33,12 @@ int opt(const void* p, size_t align) {
 
 bool dim_ok(int32_t d) { return d >= 8 && d <= kMaxDim && d % 8 == 0; }
 
+// The grouped GEMM copies operands through buffer descriptors whose range is
+// below 2^31 bytes: one expert's (or the dense) [Kd, N] bf16 weight, and for
+// the weight gradients each operand's rows.
+constexpr int64_t kMaxOperandBytes = (int64_t)1 << 31;
+bool weight_ok(int64_t kd, int64_t n) { return kd * n * 2 < kMaxOperandBytes; }
+
 int check_route_shape(int64_t S, int32_t E, int32_t K) {
     if (S < 0) return MOE_ERR_SHAPE;
     if (E < 1 || E > kMaxE) return MOE_ERR_SHAPE;
@@ -154,6 +160,7 @@ size_t moe_grouped_ffn_workspace_bytes(int32_t E, int64_t R, int32_t D, int32_t 
 static int check_ffn(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, int64_t R, int32_t D,
                      int32_t F, const moe_bf16* W1, const moe_bf16* W2) {
     if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(D) || !dim_ok(F)) return MOE_ERR_SHAPE;
+    if (!weight_ok(D, F)) return MOE_ERR_UNSUPPORTED;
     MOE_TRY(need(x_disp, (uint64_t)R * D * 2, 16));
     MOE_TRY(need(offsets, (uint64_t)(E + 1) * 4, 4));
     MOE_TRY(need(W1, (uint64_t)E * D * F * 2, 16));
@@ -199,6 +206,7 @@ int moe_grouped_gemm(const moe_bf16* A, const void* sched, int32_t E, int64_t R,
                      hipStream_t stream) {
     if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(Kd) || !dim_ok(N)) return MOE_ERR_SHAPE;
     if (epilogue != 0 && epilogue != 1) return MOE_ERR_UNSUPPORTED;
+    if (!weight_ok(Kd, N)) return MOE_ERR_UNSUPPORTED;
     if (epilogue == 0 && u_save != nullptr) return MOE_ERR_SHAPE;
     MOE_TRY(need(A, (uint64_t)R * Kd * 2, 16));
     if (sched == nullptr) return MOE_ERR_NULL;
@@ -215,6 +223,7 @@ int moe_grouped_gemm(const moe_bf16* A, const void* sched, int32_t E, int64_t R,
 int moe_latent_proj(const moe_bf16* A, const moe_bf16* W, int64_t M, int32_t Kd, int32_t N, moe_bf16* C,
                     hipStream_t stream) {
     if (M < 0 || M >= kMaxRows || !dim_ok(Kd) || !dim_ok(N)) return MOE_ERR_SHAPE;
+    if (!weight_ok(Kd, N)) return MOE_ERR_UNSUPPORTED;
     MOE_TRY(need(A, (uint64_t)M * Kd * 2, 16));
     MOE_TRY(need(W, (uint64_t)Kd * N * 2, 16));
     MOE_TRY(need(C, (uint64_t)M * N * 2, 16));
@@ -244,6 +253,7 @@ int check_layer_args(const moe_layer_fwd_args* a) {
     MOE_TRY(check_route_shape(a->S, a->E, a->K));
     if (!dim_ok(a->D) || !dim_ok(a->F)) return MOE_ERR_SHAPE;
     if (a->H != 0 && !dim_ok(a->H)) return MOE_ERR_SHAPE;
+    if (!weight_ok(a->D, a->F) || (a->H != 0 && !weight_ok(a->H, a->D))) return MOE_ERR_UNSUPPORTED;
     return MOE_OK;
 }
 
@@ -373,6 +383,7 @@ int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const mo
                         int32_t F, const moe_bf16* W1, const moe_bf16* W2, moe_bf16* dx_disp,
                         float* dW1, float* dW2, void* ws, size_t ws_bytes, hipStream_t stream) {
     MOE_TRY(check_ffn(x_disp, offsets, E, R, D, F, W1, W2));
+    if (!weight_ok(R, D > F ? D : F)) return MOE_ERR_UNSUPPORTED;  // wgrad operand rows
     MOE_TRY(need(u_save, (uint64_t)R * F * 2, 16));
     MOE_TRY(need(h, (uint64_t)R * F * 2, 16));
     MOE_TRY(need(dy_disp, (uint64_t)R * D * 2, 16));

@@ -100,6 +100,13 @@ def test_validation_errors_return_before_launch(lib):
     assert lib.moe_grouped_ffn(FAKE, FAKE, 2, 4, 16, 16, FAKE, FAKE, FAKE, None, FAKE, FAKE, 0, st) == -4
     assert lib.moe_grouped_ffn(FAKE, FAKE, 2, 4, 16, 16, FAKE, FAKE, FAKE, ODD, FAKE, FAKE, 4096, st) == -3
     assert lib.moe_latent_proj(FAKE, FAKE, 4, 20, 16, FAKE, st) == -2
+    # operands whose DMA descriptor range would reach 2^31 bytes
+    assert lib.moe_latent_proj(FAKE, FAKE, 4, 65536, 16384, FAKE, st) == -6
+    assert lib.moe_grouped_gemm(FAKE, FAKE, 2, 4, 65536, 16384, FAKE, 0, FAKE, None, st) == -6
+    assert lib.moe_grouped_ffn(FAKE, FAKE, 2, 4, 65536, 16384, FAKE, FAKE, FAKE, None, FAKE, FAKE,
+                               4096, st) == -6
+    assert lib.moe_grouped_ffn_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 1 << 20, 2048, 1024, FAKE, FAKE, FAKE,
+                                   FAKE, FAKE, FAKE, 1 << 40, st) == -6
     assert lib.moe_grouped_schedule(FAKE, 4, 100, FAKE, 16, st) == -4
     assert lib.moe_grouped_gemm(FAKE, None, 2, 4, 16, 16, FAKE, 1, FAKE, None, st) == -1
     assert lib.moe_grouped_gemm(FAKE, FAKE, 2, 4, 16, 16, FAKE, 2, FAKE, None, st) == -6
