@@ -32,6 +32,10 @@ Pins (each in tests/test_oracle_*.py):
   latent_down/up        permutation-matrix projections, brute-force loops
   *_bwd                 float64 central finite differences of the forward;
                         adjoint identities; dead experts give exactly zero dW
+  router_bwd            central finite differences of routing_probs and
+                        router_logits; rows of ds sum to zero; K = 1 gives 0
+  layer_bwd             directional finite differences of the whole layer_fwd
+                        (plain and latent, with bias) for every input
   ep_volume_per_step    the paper's printed reductions (Section 4.1, 4.3)
 """
 from __future__ import annotations
@@ -409,6 +413,82 @@ def dispatch_bwd(dx_disp, inv_perm, S: int, K: int) -> np.ndarray:
     for k in range(K):
         dx = dx + dx_disp[inv[:, k]]
     return dx
+
+
+# ---------------------------------------------------------------------------
+# Backward through the router and the latent projections
+# ---------------------------------------------------------------------------
+
+def router_bwd(x_r, Wr, topk_idx, topk_prob, dp):
+    """Gradient of the routed probabilities with respect to the router
+    (the learned router of Section 5.2), with the expert selection held
+    fixed: top-K is piecewise constant in the scores, so no gradient flows
+    through which experts are picked.
+
+    The routed probability p_k is the softmax of the K selected scores (the
+    full-E denominator cancels in routing_probs' renormalisation), so per
+    token, with dp the gradient of the routed probabilities,
+        ds[T_k] = p_k * (dp_k - sum_{j<K} p_j dp_j),    ds = 0 elsewhere,
+    and through logits = x_r @ Wr + bias:
+        dWr = x_r^T ds,   dbias = sum_t ds[t],   dx_r = ds @ Wr^T.
+    Returns (ds [S,E], dWr [D,E], dbias [E], dx_r [S,D]) as float64.
+    """
+    x_r = np.asarray(x_r, np.float64)
+    Wr = np.asarray(Wr, np.float64)
+    idx = np.asarray(topk_idx, np.int64)
+    p = np.asarray(topk_prob, np.float64)
+    dp = np.asarray(dp, np.float64)
+    S, K = idx.shape
+    E = Wr.shape[1]
+    ds = np.zeros((S, E))
+    mean = np.sum(p * dp, axis=1)
+    for t in range(S):
+        for k in range(K):
+            ds[t, idx[t, k]] = p[t, k] * (dp[t, k] - mean[t])
+    return ds, x_r.T @ ds, ds.sum(axis=0), ds @ Wr.T
+
+
+def latent_bwd(x_in, W, dout):
+    """Gradients of a latent projection out = x_in @ W (latent_down with
+    x_in = x, W = Wdown; latent_up with x_in = y_lat, W = Wup):
+        dx_in = dout @ W^T,   dW = x_in^T @ dout      (float64)."""
+    x_in = np.asarray(x_in, np.float64)
+    W = np.asarray(W, np.float64)
+    dout = np.asarray(dout, np.float64)
+    return dout @ W.T, x_in.T @ dout
+
+
+def layer_bwd(fwd: dict, x, Wr, W1, W2, K: int, dy, Wdown=None, Wup=None,
+              round_payload: bool = True) -> dict:
+    """Backward of layer_fwd for the loss gradient dy = dL/dy, from the
+    intermediates ``fwd`` that layer_fwd returned, in reverse order:
+    [latent up] -> combine^T -> experts -> dispatch^T, plus the router path
+    (router_bwd on the combine's probability gradient) -> [latent down].
+    The input's gradient is the sum of the dispatch^T and router paths.
+    ``round_payload`` rounds the gradients that travel the inverse routes
+    (dy_disp, dx_disp) to bf16, as the forward payloads are.
+    Returns dx, dWr, dbias, dW1, dW2 (and dWdown, dWup, dx_lat, dy_lat for a
+    latent layer), plus dp and ds, as float64.
+    """
+    x = np.asarray(x, np.float64)
+    S = x.shape[0]
+    out = {}
+    g = np.asarray(dy, np.float64)
+    if Wup is not None:
+        g, out["dWup"] = latent_bwd(fwd["y_lat"], Wup, g)
+        out["dy_lat"] = g
+    dy_disp, dp = combine_bwd(g, fwd["y_disp"], fwd["p_disp"], fwd["inv_perm"], K, round_payload)
+    dx_disp, dW1, dW2, _ = expert_ffn_bwd(fwd["x_disp"], fwd["u"], fwd["h"], dy_disp, fwd["offsets"],
+                                          W1, W2, round_payload)
+    x_r = fwd["x_lat"] if Wdown is not None else x
+    ds, dWr, dbias, dx_router = router_bwd(x_r, Wr, fwd["topk_idx"], fwd["topk_prob"], dp)
+    dx_r = dispatch_bwd(dx_disp, fwd["inv_perm"], S, K) + dx_router
+    if Wdown is not None:
+        out["dx_lat"] = dx_r
+        dx_r, out["dWdown"] = latent_bwd(x, Wdown, dx_r)
+    out.update(dx=dx_r, dWr=dWr, dbias=dbias, dW1=dW1, dW2=dW2, dp=dp, ds=ds,
+               dy_disp=dy_disp, dx_disp=dx_disp)
+    return out
 
 
 # ---------------------------------------------------------------------------
