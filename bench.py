@@ -315,7 +315,7 @@ def main():
                                                s.E, s.R, s.D, s.F, sets[0]["W1"], sets[0]["W2"], dx_disp,
                                                dW1, dW2, ws_bwd), max(2, reps // 4), stream)
         st["dispatch_bwd"] = time_region(
-            lambda i: _lib.moe_dispatch_bwd(dx_disp, ob["inv_perm"], s.S, s.D, s.K, dx), reps, stream)
+            lambda i: _lib.moe_dispatch_bwd(dx_disp, ob["inv_perm"], None, s.S, s.D, s.K, dx), reps, stream)
         del lb, ob, dy_disp, dx_disp, dW1, dW2, ws_bwd
 
     bytes_ = stage_bytes(s)

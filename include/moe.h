@@ -275,11 +275,62 @@ int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const mo
                         moe_bf16* dx_disp, float* dW1, float* dW2,
                         void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* dx[t] = bf16( sum_{k<K} dx_disp[inv_perm[t*K+k]] ), ascending k (the
- * transpose of moe_dispatch: an unweighted combine).
- *   dx_disp [S*K, D] bf16;  dx [S, D] bf16 */
-int moe_dispatch_bwd(const moe_bf16* dx_disp, const int32_t* inv_perm, int64_t S, int32_t D,
-                     int32_t K, moe_bf16* dx, hipStream_t stream);
+/* dx[t] = bf16( sum_{k<K} dx_disp[inv_perm[t*K+k]]  (+ dx_add[t]) ), the
+ * transpose of moe_dispatch (an unweighted combine): the K rows are summed in
+ * fp32 in ascending k, the optional fp32 addend (the router's contribution
+ * to the input gradient, moe_router_bwd's dx_r) is added after them, and the
+ * result is rounded once.
+ *   dx_disp [S*K, D] bf16;  dx_add [S, D] fp32 (16-byte aligned) or NULL;
+ *   dx [S, D] bf16 */
+int moe_dispatch_bwd(const moe_bf16* dx_disp, const int32_t* inv_perm, const float* dx_add,
+                     int64_t S, int32_t D, int32_t K, moe_bf16* dx, hipStream_t stream);
+
+/* ---------------------------------------------------------------------- */
+/* Router backward (the learned router of Section 5.2) with the expert     */
+/* selection held fixed: top-K is piecewise constant in the scores, so no  */
+/* gradient flows through which experts are picked.                        */
+/* ---------------------------------------------------------------------- */
+/* Workspace bytes moe_router_bwd needs; 0 for invalid sizes. */
+size_t moe_router_bwd_workspace_bytes(int64_t S, int32_t D, int32_t E);
+
+/* From the gradient dp[t,k] of the routed probabilities (moe_combine_bwd's
+ * dp), with p = topk_prob (the softmax of the K selected scores):
+ *   dlogits[t, T_k] = p_k (dp_k - sum_j p_j dp_j),  0 for unselected experts
+ *   dWr   = x_r^T dlogits        [D, E] fp32 (fp32 accuracy: dlogits enters
+ *                                the MFMA as three bf16 terms)
+ *   dbias = sum_t dlogits[t]     [E] fp32, or NULL
+ *   dx_r  = dlogits Wr^T         [S, D] fp32 (the K nonzero terms, fp32 FMA),
+ *                                or NULL; pass it to moe_dispatch_bwd as dx_add
+ * Every sum has a fixed order (deterministic).
+ *   x_r [S, D] bf16;  Wr [D, E] fp32;  topk_idx, topk_prob, dp [S, K];
+ *   dlogits [S, E] fp32 or NULL (then kept in the workspace).
+ * Errors: as moe_route_topk's shapes, D a multiple of 8 in [8, 65536],
+ * MOE_ERR_UNSUPPORTED if S*max(D, 3E)*2 >= 2^31, MOE_ERR_WORKSPACE. */
+int moe_router_bwd(const moe_bf16* x_r, const float* Wr, const int32_t* topk_idx,
+                   const float* topk_prob, const float* dp, int64_t S, int32_t D, int32_t E,
+                   int32_t K, float* dlogits, float* dWr, float* dbias, float* dx_r,
+                   void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------- */
+/* Latent projection backward (LatentMoE-style dispatch dimension,         */
+/* Section 1; Table 2 d_latent).                                           */
+/* ---------------------------------------------------------------------- */
+/* Workspace bytes moe_latent_proj_bwd needs for dW; 0 for invalid sizes. */
+size_t moe_latent_proj_bwd_workspace_bytes(int64_t M, int32_t Kd, int32_t N);
+
+/* For out = x_in @ W (moe_latent_proj) and its gradient dout:
+ *   dx_in = bf16(dout @ W^T)   [M, Kd] bf16, or NULL
+ *   dW    = x_in^T @ dout      [Kd, N] fp32 (fixed-order sum over row
+ *                              chunks), or NULL
+ * Covers both projections: (x_in, W, dout) = (x, Wdown, dx_lat) gives dx and
+ * dWdown; (y_lat, Wup, dy) gives dy_lat and dWup.
+ *   x_in [M, Kd] bf16 (needed for dW);  W [Kd, N] bf16 (needed for dx_in);
+ *   dout [M, N] bf16.
+ * Errors: M in [0, 2^31), Kd and N multiples of 8 in [8, 65536],
+ * MOE_ERR_UNSUPPORTED if Kd*N*2 or (with dW) M*max(Kd, N)*2 reaches 2^31. */
+int moe_latent_proj_bwd(const moe_bf16* x_in, const moe_bf16* W, const moe_bf16* dout,
+                        int64_t M, int32_t Kd, int32_t N, moe_bf16* dx_in, float* dW,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

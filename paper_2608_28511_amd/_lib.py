@@ -69,7 +69,11 @@ _PROTOS = {
     "moe_grouped_ffn_bwd_workspace_bytes": (sz, [i32, i64, i32, i32]),
     "moe_grouped_ffn_bwd": (C.c_int, [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp, vp, vp, vp, vp,
                                       vp, sz, vp]),
-    "moe_dispatch_bwd": (C.c_int, [vp, vp, i64, i32, i32, vp, vp]),
+    "moe_dispatch_bwd": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp]),
+    "moe_router_bwd_workspace_bytes": (sz, [i64, i32, i32]),
+    "moe_router_bwd": (C.c_int, [vp, vp, vp, vp, vp, i64, i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
+    "moe_latent_proj_bwd_workspace_bytes": (sz, [i64, i32, i32]),
+    "moe_latent_proj_bwd": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp, vp, sz, vp]),
 }
 
 EXPORTED = tuple(_PROTOS)
@@ -258,6 +262,30 @@ def moe_grouped_ffn_bwd(x_disp, u_save, h, dy_disp, offsets, E, R, D, F, W1, W2,
         0 if ws is None else ws.numel() * ws.element_size(), _stream()), "moe_grouped_ffn_bwd")
 
 
-def moe_dispatch_bwd(dx_disp, inv_perm, S, D, K, dx):
+def moe_dispatch_bwd(dx_disp, inv_perm, dx_add, S, D, K, dx):
     _check(load().moe_dispatch_bwd(_ptr(dx_disp, BF16, "dx_disp"), _ptr(inv_perm, I32, "inv_perm"),
-                                   S, D, K, _ptr(dx, BF16, "dx"), _stream()), "moe_dispatch_bwd")
+                                   _ptr(dx_add, F32, "dx_add"), S, D, K, _ptr(dx, BF16, "dx"), _stream()),
+           "moe_dispatch_bwd")
+
+
+def moe_router_bwd_workspace_bytes(S, D, E) -> int:
+    return load().moe_router_bwd_workspace_bytes(S, D, E)
+
+
+def moe_router_bwd(x_r, Wr, topk_idx, topk_prob, dp, S, D, E, K, dlogits, dWr, dbias, dx_r, ws):
+    _check(load().moe_router_bwd(
+        _ptr(x_r, BF16, "x_r"), _ptr(Wr, F32, "Wr"), _ptr(topk_idx, I32, "topk_idx"),
+        _ptr(topk_prob, F32, "topk_prob"), _ptr(dp, F32, "dp"), S, D, E, K, _ptr(dlogits, F32, "dlogits"),
+        _ptr(dWr, F32, "dWr"), _ptr(dbias, F32, "dbias"), _ptr(dx_r, F32, "dx_r"), _ptr(ws, None, "ws"),
+        0 if ws is None else ws.numel() * ws.element_size(), _stream()), "moe_router_bwd")
+
+
+def moe_latent_proj_bwd_workspace_bytes(M, Kd, N) -> int:
+    return load().moe_latent_proj_bwd_workspace_bytes(M, Kd, N)
+
+
+def moe_latent_proj_bwd(x_in, W, dout, M, Kd, N, dx_in, dW, ws):
+    _check(load().moe_latent_proj_bwd(
+        _ptr(x_in, BF16, "x_in"), _ptr(W, BF16, "W"), _ptr(dout, BF16, "dout"), M, Kd, N,
+        _ptr(dx_in, BF16, "dx_in"), _ptr(dW, F32, "dW"), _ptr(ws, None, "ws"),
+        0 if ws is None else ws.numel() * ws.element_size(), _stream()), "moe_latent_proj_bwd")

@@ -149,7 +149,7 @@ int moe_combine(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_
     MOE_TRY(opt(p_disp, 4));
     MOE_TRY(need(inv_perm, R * 4, 4));
     MOE_TRY(need(y, (uint64_t)S * D * 2, 16));
-    return hip_status(moe::launch_combine(y_disp, p_disp, inv_perm, S, D, K, y, stream));
+    return hip_status(moe::launch_combine(y_disp, p_disp, inv_perm, S, D, K, nullptr, y, stream));
 }
 
 size_t moe_grouped_ffn_workspace_bytes(int32_t E, int64_t R, int32_t D, int32_t F) {
@@ -347,7 +347,7 @@ int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
                                          moe::EPI_BF16, nullptr, nullptr, b.sched, E, R, D, F, stream));
     }
     moe_bf16* comb_out = H ? b.y_lat : a->y;
-    MOE_HIP(moe::launch_combine(b.y_disp, b.p_disp, b.inv_perm, S, D, K, comb_out, stream));
+    MOE_HIP(moe::launch_combine(b.y_disp, b.p_disp, b.inv_perm, S, D, K, nullptr, comb_out, stream));
     if (H) {
         MOE_HIP(moe::launch_grouped_rows(b.y_lat, D, a->Wup, H, 0, false, a->y, H, moe::EPI_BF16,
                                          nullptr, nullptr, nullptr, 1, S, H, D, stream));
@@ -413,9 +413,80 @@ int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const mo
     return MOE_OK;
 }
 
-int moe_dispatch_bwd(const moe_bf16* dx_disp, const int32_t* inv_perm, int64_t S, int32_t D, int32_t K,
-                     moe_bf16* dx, hipStream_t stream) {
-    return moe_combine(dx_disp, nullptr, inv_perm, S, D, K, dx, stream);
+int moe_dispatch_bwd(const moe_bf16* dx_disp, const int32_t* inv_perm, const float* dx_add, int64_t S,
+                     int32_t D, int32_t K, moe_bf16* dx, hipStream_t stream) {
+    if (S < 0 || !dim_ok(D) || K < 1 || K > kMaxK || S * (int64_t)K >= kMaxRows) return MOE_ERR_SHAPE;
+    const uint64_t R = (uint64_t)S * K;
+    MOE_TRY(need(dx_disp, R * D * 2, 16));
+    MOE_TRY(need(inv_perm, R * 4, 4));
+    MOE_TRY(opt(dx_add, 16));
+    MOE_TRY(need(dx, (uint64_t)S * D * 2, 16));
+    return hip_status(moe::launch_combine(dx_disp, nullptr, inv_perm, S, D, K, dx_add, dx, stream));
+}
+
+size_t moe_router_bwd_workspace_bytes(int64_t S, int32_t D, int32_t E) {
+    if (S < 0 || S >= kMaxRows || !dim_ok(D) || E < 1 || E > kMaxE) return 0;
+    return moe::router_bwd_ws_bytes(S, D, E);
+}
+
+int moe_router_bwd(const moe_bf16* x_r, const float* Wr, const int32_t* topk_idx, const float* topk_prob,
+                   const float* dp, int64_t S, int32_t D, int32_t E, int32_t K, float* dlogits, float* dWr,
+                   float* dbias, float* dx_r, void* ws, size_t ws_bytes, hipStream_t stream) {
+    MOE_TRY(check_route_shape(S, E, K));
+    if (!dim_ok(D)) return MOE_ERR_SHAPE;
+    const int32_t E3 = 3 * ((E + 7) / 8 * 8);  // the three bf16 planes of dlogits, rows padded to 8
+    if (!weight_ok(S, D > E3 ? D : E3)) return MOE_ERR_UNSUPPORTED;  // dWr operand rows
+    const uint64_t R = (uint64_t)S * K;
+    MOE_TRY(need(x_r, (uint64_t)S * D * 2, 16));
+    MOE_TRY(need(Wr, (uint64_t)D * E * 4, 4));
+    MOE_TRY(need(topk_idx, R * 4, 4));
+    MOE_TRY(need(topk_prob, R * 4, 4));
+    MOE_TRY(need(dp, R * 4, 4));
+    MOE_TRY(opt(dlogits, 4));
+    MOE_TRY(need(dWr, (uint64_t)D * E * 4, 4));
+    MOE_TRY(opt(dbias, 4));
+    MOE_TRY(opt(dx_r, 16));
+    if (ws == nullptr || ws_bytes < moe::router_bwd_ws_bytes(S, D, E)) return MOE_ERR_WORKSPACE;
+    MOE_TRY(opt(ws, 256));
+    return hip_status(moe::launch_router_bwd(x_r, Wr, topk_idx, topk_prob, dp, S, D, E, K, dlogits, dWr,
+                                             dbias, dx_r, ws, stream));
+}
+
+size_t moe_latent_proj_bwd_workspace_bytes(int64_t M, int32_t Kd, int32_t N) {
+    if (M < 0 || M >= kMaxRows || !dim_ok(Kd) || !dim_ok(N)) return 0;
+    return align256((size_t)moe::wgrad_chunks(M, Kd, N) * Kd * N * 4);
+}
+
+int moe_latent_proj_bwd(const moe_bf16* x_in, const moe_bf16* W, const moe_bf16* dout, int64_t M, int32_t Kd,
+                        int32_t N, moe_bf16* dx_in, float* dW, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (M < 0 || M >= kMaxRows || !dim_ok(Kd) || !dim_ok(N)) return MOE_ERR_SHAPE;
+    if (!weight_ok(Kd, N)) return MOE_ERR_UNSUPPORTED;
+    if (dW != nullptr && !weight_ok(M, Kd > N ? Kd : N)) return MOE_ERR_UNSUPPORTED;
+    MOE_TRY(need(dout, (uint64_t)M * N * 2, 16));
+    if (dx_in != nullptr) {
+        MOE_TRY(need(W, (uint64_t)Kd * N * 2, 16));
+        MOE_TRY(need(dx_in, (uint64_t)M * Kd * 2, 16));
+    }
+    if (dW != nullptr) {
+        MOE_TRY(need(x_in, (uint64_t)M * Kd * 2, 16));
+        MOE_TRY(need(dW, (uint64_t)Kd * N * 4, 4));
+        if (ws == nullptr || ws_bytes < moe_latent_proj_bwd_workspace_bytes(M, Kd, N)) return MOE_ERR_WORKSPACE;
+        MOE_TRY(opt(ws, 256));
+    }
+    if (dx_in != nullptr && M > 0) {
+        // dx_in[m, kd] = sum_n dout[m, n] W[kd, n]: W read N-contiguous per output column
+        MOE_HIP(moe::launch_grouped_rows(dout, N, W, N, 0, true, dx_in, Kd, moe::EPI_BF16, nullptr, nullptr,
+                                         nullptr, 1, M, Kd, N, stream));
+    }
+    if (dW != nullptr) {
+        const int nch = moe::wgrad_chunks(M, Kd, N);
+        const int64_t kchunk = M > 0 ? (M + nch - 1) / nch : 1;
+        float* part = (float*)ws;
+        MOE_HIP(moe::launch_chunked_wgrad(x_in, Kd, dout, N, part, N, (int64_t)Kd * N, nch, kchunk, Kd, N, M,
+                                          stream));
+        MOE_HIP(moe::launch_sum_planes(part, nch, Kd, N, 1, N, dW, stream));
+    }
+    return MOE_OK;
 }
 
 }  // extern "C"

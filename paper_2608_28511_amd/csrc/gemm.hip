@@ -87,6 +87,7 @@ struct GemmArgs {
     int64_t lda, ldb, ldc;
     int64_t b_stride;         // elements between experts' B (ROWS mode)
     int64_t c_stride;         // elements between experts' C (KGRP mode)
+    int64_t kchunk;           // KGRP mode without offsets: group e contracts rows [e*kchunk, (e+1)*kchunk)
     int64_t M;                // dense rows (ROWS, no offsets) or output rows (KGRP)
     int64_t R;                // rows of the activation buffers: segments are clamped to [0, R)
     int N, Kd, E;
@@ -172,8 +173,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) 
     const int mt = in % p.m_tiles, nt = in / p.m_tiles;
     const int64_t row0 = (int64_t)mt * BM;
     const int64_t row_hi = (row0 + BM) < p.M ? (row0 + BM) : p.M;
-    int64_t k_begin = p.offsets[e];
-    int64_t k_end = p.offsets[e + 1];
+    int64_t k_begin = p.offsets != nullptr ? (int64_t)p.offsets[e] : (int64_t)e * p.kchunk;
+    int64_t k_end = p.offsets != nullptr ? (int64_t)p.offsets[e + 1] : k_begin + p.kchunk;
     k_begin = k_begin < 0 ? 0 : (k_begin > p.R ? p.R : k_begin);
     k_end = k_end < k_begin ? k_begin : (k_end > p.R ? p.R : k_end);
     const int64_t n0 = (int64_t)nt * BN;
@@ -579,6 +580,22 @@ hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B
         if (epi == EPI_DRELU2) return launch_rows<true, EPI_DRELU2>(a, st);
     }
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_chunked_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb, float* C,
+                                int64_t ldc, int64_t c_stride, int nchunk, int64_t kchunk, int M, int N,
+                                int64_t R, hipStream_t st) {
+    GemmArgs a{};
+    a.A = A; a.B = B; a.C = C; a.offsets = nullptr; a.kchunk = kchunk;
+    a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.c_stride = c_stride;
+    a.M = M; a.R = R; a.N = N; a.E = nchunk;
+    a.m_tiles = (M + BM - 1) / BM;
+    a.n_tiles = (N + BN - 1) / BN;
+    const int64_t n_wg = (int64_t)nchunk * a.m_tiles * a.n_tiles;
+    if (n_wg <= 0) return hipSuccess;
+    if (R * (lda > ldb ? lda : ldb) * 2 >= kMaxDmaBytes) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(gemm_kgrp_kernel, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a);
+    return hipGetLastError();
 }
 
 hipError_t launch_grouped_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,

@@ -16,6 +16,17 @@ size_t router_ws_bytes(int D, int E);
 hipError_t launch_router_logits(const moe_bf16* x, const float* Wr, const float* bias, int64_t S,
                                 int D, int E, float* logits, void* ws, hipStream_t st);
 
+// Router backward (selection held fixed): dlogits (optional; else internal),
+// dWr [D,E], dbias [E] (optional), dx_r [S,D] fp32 (optional).
+size_t router_bwd_ws_bytes(int64_t S, int D, int E);
+hipError_t launch_router_bwd(const moe_bf16* x_r, const float* Wr, const int32_t* topk_idx, const float* topk_prob,
+                             const float* dp, int64_t S, int D, int E, int K, float* dlogits, float* dWr,
+                             float* dbias, float* dx_r, void* ws, hipStream_t st);
+// out[m,n] = sum_c sum_{s=P-1..0} part[c][m][s*ldp+n] (fixed order; rows of part hold P*ldp)
+hipError_t launch_sum_planes(const float* part, int nchunk, int M, int N, int P, int ldp, float* out,
+                             hipStream_t st);
+int wgrad_chunks(int64_t rows, int M, int N);
+
 size_t route_ws_bytes(int64_t S, int E);
 hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* topk_idx,
                         float* topk_prob, int32_t* counts, int32_t* offsets, int32_t* perm,
@@ -23,8 +34,9 @@ hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* t
 
 hipError_t launch_dispatch(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S,
                            int D, int K, moe_bf16* x_disp, float* p_disp, hipStream_t st);
+// y[t] = bf16(sum_k w_k y_disp[pos_k] (+ add[t], fp32 [S,D], after the sum; NULL for none))
 hipError_t launch_combine(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_perm,
-                          int64_t S, int D, int K, moe_bf16* y, hipStream_t st);
+                          int64_t S, int D, int K, const float* add, moe_bf16* y, hipStream_t st);
 hipError_t launch_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const float* p_disp,
                               const int32_t* inv_perm, int64_t S, int D, int K, moe_bf16* dy_disp,
                               float* dp, hipStream_t st);
@@ -41,6 +53,11 @@ hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B
                                const moe_bf16* aux_in, moe_bf16* aux_out, const void* sched,
                                int E, int64_t R, int N, int Kd, hipStream_t st);
 // KGRP mode: C_e[m, n] = sum over expert e's rows r of A[r, m] * B[r, n]  (fp32 out).
+// KGRP over a dense contraction cut into nchunk row ranges of kchunk rows:
+// C + c*c_stride = A[rows of chunk c]^T @ B[rows of chunk c]  (fp32 partials).
+hipError_t launch_chunked_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb, float* C,
+                                int64_t ldc, int64_t c_stride, int nchunk, int64_t kchunk, int M, int N,
+                                int64_t R, hipStream_t st);
 hipError_t launch_grouped_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
                                 float* C, int64_t ldc, int64_t c_stride, const int32_t* offsets,
                                 int E, int M, int N, int64_t R, hipStream_t st);

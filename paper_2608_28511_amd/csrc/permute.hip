@@ -76,6 +76,7 @@ __global__ __launch_bounds__(kRowThreads) void combine_kernel(const uint4* __res
                                                               const float* __restrict__ p_disp,
                                                               const int32_t* __restrict__ inv_perm,
                                                               int64_t S, int D8, int K,
+                                                              const float4* __restrict__ add,
                                                               uint4* __restrict__ y) {
     const int lane = threadIdx.x & 63;
     const int64_t t = (int64_t)blockIdx.x * kRowTok + (threadIdx.x >> 6);
@@ -108,7 +109,13 @@ __global__ __launch_bounds__(kRowThreads) void combine_kernel(const uint4* __res
 #pragma unroll
         for (int i = 0; i < kCPL; ++i) {
             const int c = c0 + lane + kWave * i;
-            if (c < D8) y[t * D8 + c] = pack8(acc[i]);
+            if (c >= D8) continue;
+            if (add != nullptr) {  // fp32 addend, summed after the K rows, before the rounding
+                const float4 a0 = add[(t * D8 + c) * 2], a1 = add[(t * D8 + c) * 2 + 1];
+                acc[i][0] += a0.x; acc[i][1] += a0.y; acc[i][2] += a0.z; acc[i][3] += a0.w;
+                acc[i][4] += a1.x; acc[i][5] += a1.y; acc[i][6] += a1.z; acc[i][7] += a1.w;
+            }
+            y[t * D8 + c] = pack8(acc[i]);
         }
     }
 }
@@ -180,10 +187,10 @@ hipError_t launch_dispatch(const moe_bf16* x, const float* prob, const int32_t* 
 }
 
 hipError_t launch_combine(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_perm,
-                          int64_t S, int D, int K, moe_bf16* y, hipStream_t st) {
+                          int64_t S, int D, int K, const float* add, moe_bf16* y, hipStream_t st) {
     if (S == 0) return hipSuccess;
     hipLaunchKernelGGL(combine_kernel, dim3(grid_for(S, kRowTok)), dim3(kRowThreads), 0, st,
-                       (const uint4*)y_disp, p_disp, inv_perm, S, D / 8, K, (uint4*)y);
+                       (const uint4*)y_disp, p_disp, inv_perm, S, D / 8, K, (const float4*)add, (uint4*)y);
     return hipGetLastError();
 }
 

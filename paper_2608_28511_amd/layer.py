@@ -116,11 +116,40 @@ def grouped_ffn_bwd(x_disp, u_save, h, dy_disp, offsets, W1, W2):
     return dx_disp, dW1, dW2
 
 
-def dispatch_bwd(dx_disp, inv_perm, S: int, K: int):
+def dispatch_bwd(dx_disp, inv_perm, S: int, K: int, dx_add: Optional[torch.Tensor] = None):
     D = dx_disp.shape[1]
     dx = _empty((S, D), BF16, dx_disp.device)
-    L.moe_dispatch_bwd(dx_disp, inv_perm, S, D, K, dx)
+    L.moe_dispatch_bwd(dx_disp, inv_perm, dx_add, S, D, K, dx)
     return dx
+
+
+def router_bwd(x_r, Wr, topk_idx, topk_prob, dp, want_dlogits: bool = True, want_dbias: bool = True,
+               want_dx: bool = True) -> Dict[str, torch.Tensor]:
+    """Router gradients with the selection held fixed: dlogits, dWr, dbias, dx_r (fp32)."""
+    S, D = x_r.shape
+    E = Wr.shape[1]
+    K = topk_idx.shape[1]
+    dev = x_r.device
+    o = dict(dWr=_empty((D, E), F32, dev))
+    o["dlogits"] = _empty((S, E), F32, dev) if want_dlogits else None
+    o["dbias"] = _empty((E,), F32, dev) if want_dbias else None
+    o["dx_r"] = _empty((S, D), F32, dev) if want_dx else None
+    ws = _ws(L.moe_router_bwd_workspace_bytes(S, D, E), dev)
+    L.moe_router_bwd(x_r, Wr, topk_idx, topk_prob, dp, S, D, E, K, o["dlogits"], o["dWr"], o["dbias"],
+                     o["dx_r"], ws)
+    return o
+
+
+def latent_proj_bwd(x_in, W, dout, want_dx: bool = True, want_dW: bool = True):
+    """Gradients of out = x_in @ W: (dx_in bf16 or None, dW fp32 or None)."""
+    M, N = dout.shape
+    Kd = W.shape[0]
+    dev = dout.device
+    dx = _empty((M, Kd), BF16, dev) if want_dx else None
+    dW = _empty((Kd, N), F32, dev) if want_dW else None
+    ws = _ws(L.moe_latent_proj_bwd_workspace_bytes(M, Kd, N), dev) if want_dW else None
+    L.moe_latent_proj_bwd(x_in, W, dout, M, Kd, N, dx, dW, ws)
+    return dx, dW
 
 
 class LayerFwd:

@@ -58,6 +58,10 @@ def test_workspace_queries(lib):
     assert lib.moe_router_logits_workspace_bytes(1032, 37) == (3 * 1032 * 37 * 2 + 255) // 256 * 256
     assert lib.moe_router_logits_workspace_bytes(2044, 64) == 0   # D % 8
     assert lib.moe_router_logits_workspace_bytes(64, 0) == 0
+    assert lib.moe_router_bwd_workspace_bytes(8192, 2048, 64) >= 8192 * 64 * 4 + 8192 * 192 * 2
+    assert lib.moe_router_bwd_workspace_bytes(8192, 2044, 64) == 0
+    assert lib.moe_latent_proj_bwd_workspace_bytes(16384, 4096, 1024) >= 4096 * 1024 * 4
+    assert lib.moe_latent_proj_bwd_workspace_bytes(16384, 4096, 1020) == 0
     assert lib.moe_grouped_ffn_workspace_bytes(64, 49152, 2048, 1024) > 0
     assert lib.moe_grouped_ffn_workspace_bytes(64, 49152, 2044, 1024) == 0   # D % 8
     assert lib.moe_grouped_ffn_bwd_workspace_bytes(8, 100, 64, 64) >= 100 * 64 * 2
@@ -119,7 +123,18 @@ def test_validation_errors_return_before_launch(lib):
                                    FAKE, FAKE, FAKE, 1 << 20, st) == -1
     assert lib.moe_grouped_ffn_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 4, 16, 16, FAKE, FAKE, FAKE,
                                    FAKE, FAKE, FAKE, 8, st) == -4
-    assert lib.moe_dispatch_bwd(FAKE, FAKE, 4, 16, 40, FAKE, st) == -2
+    assert lib.moe_dispatch_bwd(FAKE, FAKE, None, 4, 16, 40, FAKE, st) == -2
+    assert lib.moe_dispatch_bwd(FAKE, FAKE, ODD, 4, 16, 2, FAKE, st) == -3
+    # router / latent backward
+    assert lib.moe_router_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, 4, 16, 8, 9, None, FAKE, None, None, FAKE,
+                              1 << 20, st) == -2                       # K > E
+    assert lib.moe_router_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, 4, 16, 8, 2, None, FAKE, None, None, FAKE,
+                              8, st) == -4                             # workspace too small
+    assert lib.moe_router_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, 4, 16, 8, 2, None, FAKE, None, ODD, FAKE,
+                              1 << 20, st) == -3                       # dx_r must be 16-byte aligned
+    assert lib.moe_latent_proj_bwd(FAKE, FAKE, FAKE, 4, 16, 12, FAKE, None, None, 0, st) == -2
+    assert lib.moe_latent_proj_bwd(FAKE, FAKE, FAKE, 4, 16, 16, None, FAKE, None, 0, st) == -4
+    assert lib.moe_latent_proj_bwd(FAKE, FAKE, FAKE, 4, 65536, 16384, FAKE, None, None, 0, st) == -6
     # layer: null args, wrong struct size, latent weights without H
     assert lib.moe_layer_fwd(None, st) == -1
     a = L.LayerFwdArgs()
