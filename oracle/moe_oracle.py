@@ -36,6 +36,18 @@ Pins (each in tests/test_oracle_*.py):
                         router_logits; rows of ds sum to zero; K = 1 gives 0
   layer_bwd             directional finite differences of the whole layer_fwd
                         (plain and latent, with bias) for every input
+  sigmoid_topk_select   zero bias equals topk_select on the logits; equal
+                        logits rank by bias; brute-force sort; hand fixture
+  sigmoid_gates         K = 1 -> 1; equal scores -> 1/K; K = 2 with opposite
+                        logits -> sigmoid(l0); sum = 1; bias-independent;
+                        hand fixture (exact fractions)
+  seq_aux_loss          uniform scores -> coeff exactly; hand fixture;
+                        per-sequence mean (not batch-level); token-order
+                        invariance; linear in coeff
+  *_bwd (sigmoid, aux)  float64 central finite differences, selection fixed
+  expert_bias_update    closed form on a hand example
+  shared_expert         one expert over all rows of expert_ffn; identity
+                        weights give relu(x)^2; finite differences of the bwd
   ep_volume_per_step    the paper's printed reductions (Section 4.1, 4.3)
 """
 from __future__ import annotations
@@ -52,8 +64,11 @@ __all__ = [
     "B_X", "B_P", "round_bf16", "router_logits", "topk_select", "routing_probs",
     "route", "expert_permutation", "dispatch", "expert_ffn", "combine",
     "latent_down", "latent_up", "layer_fwd", "combine_bwd", "expert_ffn_bwd",
-    "dispatch_bwd", "dispatch_payload_bytes", "combine_payload_bytes",
-    "ep_volume_per_step",
+    "dispatch_bwd", "router_bwd", "latent_bwd", "layer_bwd", "sigmoid_scores",
+    "sigmoid_topk_select", "sigmoid_gates", "sigmoid_route", "seq_aux_loss",
+    "seq_aux_loss_bwd", "sigmoid_gate_bwd", "router_linear_bwd", "expert_bias_update",
+    "shared_expert", "shared_expert_bwd", "dispatch_payload_bytes",
+    "combine_payload_bytes", "ep_volume_per_step",
 ]
 
 
@@ -301,7 +316,9 @@ def latent_up(y_lat, Wup) -> np.ndarray:
 
 
 def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
-              logits=None, round_payload: bool = True, round_latent: bool = True) -> dict:
+              logits=None, round_payload: bool = True, round_latent: bool = True,
+              score: str = "softmax", sel_bias=None, Ws1=None, Ws2=None,
+              seq_len: Optional[int] = None, aux_coeff: float = 0.0) -> dict:
     """One routed MoE layer forward, in the paper's order (Section 4.1
     footnote: hidden dispatch, probability dispatch, hidden combine):
     [latent down] -> router logits -> top-K + probabilities -> permutation ->
@@ -310,7 +327,13 @@ def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
     If ``logits`` is given, routing uses those fp32 scores instead of the
     ones computed here.  ``round_latent`` rounds the projected activations
     (the dispatched, routed input) to bf16; ``round_payload`` rounds the
-    expert outputs sent back for the combine.  Returns every intermediate.
+    expert outputs sent back for the combine.
+
+    The production variant of Section 5.2: ``score="sigmoid"`` routes with
+    sigmoid_route (``sel_bias`` steering selection only); ``Ws1``/``Ws2`` add
+    the shared expert on the layer input to the layer output; ``aux_coeff``
+    (sigmoid scores, batch of whole ``seq_len``-token sequences) adds the
+    balance loss as ``aux_loss``.  Returns every intermediate.
     """
     x = np.asarray(x, np.float64)
     S = x.shape[0]
@@ -323,7 +346,12 @@ def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
         logits = router_logits(x_r, Wr, bias)
     out["logits"] = np.asarray(logits, np.float32)
     E = out["logits"].shape[1]
-    idx, prob = route(out["logits"], K)
+    if score == "sigmoid":
+        idx, prob = sigmoid_route(out["logits"], K, sel_bias)
+    elif score == "softmax" and sel_bias is None:
+        idx, prob = route(out["logits"], K)
+    else:
+        raise ValueError("score is 'softmax' (no selection bias) or 'sigmoid'")
     counts, offsets, perm, inv_perm = expert_permutation(idx, E)
     x_disp, p_disp = dispatch(x_r, prob, inv_perm, K)
     u, h, y_disp = expert_ffn(x_disp, offsets, W1, W2, round_payload)
@@ -333,6 +361,13 @@ def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
     if Wup is not None:
         out["y_lat"] = y
         y = latent_up(y, Wup)
+    if Ws1 is not None:
+        out["u_s"], out["h_s"], out["y_shared"] = shared_expert(x, Ws1, Ws2)
+        y = y + out["y_shared"]
+    if aux_coeff:
+        if score != "sigmoid":
+            raise ValueError("the sequence balance loss is defined on sigmoid scores")
+        out["aux_loss"] = seq_aux_loss(out["logits"], idx, seq_len, aux_coeff)
     out["y"] = y
     return out
 
@@ -459,7 +494,8 @@ def latent_bwd(x_in, W, dout):
 
 
 def layer_bwd(fwd: dict, x, Wr, W1, W2, K: int, dy, Wdown=None, Wup=None,
-              round_payload: bool = True) -> dict:
+              round_payload: bool = True, score: str = "softmax", Ws1=None, Ws2=None,
+              seq_len: Optional[int] = None, aux_coeff: float = 0.0) -> dict:
     """Backward of layer_fwd for the loss gradient dy = dL/dy, from the
     intermediates ``fwd`` that layer_fwd returned, in reverse order:
     [latent up] -> combine^T -> experts -> dispatch^T, plus the router path
@@ -467,13 +503,19 @@ def layer_bwd(fwd: dict, x, Wr, W1, W2, K: int, dy, Wdown=None, Wup=None,
     The input's gradient is the sum of the dispatch^T and router paths.
     ``round_payload`` rounds the gradients that travel the inverse routes
     (dy_disp, dx_disp) to bf16, as the forward payloads are.
+    With the production variant (same arguments as layer_fwd) the loss is
+    <dy, y> + aux_loss: the router path differentiates the sigmoid weights
+    (and the balance loss), and the shared expert adds its input gradient.
     Returns dx, dWr, dbias, dW1, dW2 (and dWdown, dWup, dx_lat, dy_lat for a
-    latent layer), plus dp and ds, as float64.
+    latent layer; dWs1, dWs2 with a shared expert), plus dp and ds (the
+    gradient of the logits), as float64.
     """
     x = np.asarray(x, np.float64)
     S = x.shape[0]
     out = {}
     g = np.asarray(dy, np.float64)
+    if Ws1 is not None:
+        dx_shared, out["dWs1"], out["dWs2"] = shared_expert_bwd(x, fwd["u_s"], fwd["h_s"], g, Ws1, Ws2)
     if Wup is not None:
         g, out["dWup"] = latent_bwd(fwd["y_lat"], Wup, g)
         out["dy_lat"] = g
@@ -481,14 +523,193 @@ def layer_bwd(fwd: dict, x, Wr, W1, W2, K: int, dy, Wdown=None, Wup=None,
     dx_disp, dW1, dW2, _ = expert_ffn_bwd(fwd["x_disp"], fwd["u"], fwd["h"], dy_disp, fwd["offsets"],
                                           W1, W2, round_payload)
     x_r = fwd["x_lat"] if Wdown is not None else x
-    ds, dWr, dbias, dx_router = router_bwd(x_r, Wr, fwd["topk_idx"], fwd["topk_prob"], dp)
+    if score == "sigmoid":
+        ds = sigmoid_gate_bwd(fwd["logits"], fwd["topk_idx"], dp)
+        if aux_coeff:
+            ds = ds + seq_aux_loss_bwd(fwd["logits"], fwd["topk_idx"], seq_len, aux_coeff)
+        dWr, dbias, dx_router = router_linear_bwd(x_r, Wr, ds)
+    else:
+        ds, dWr, dbias, dx_router = router_bwd(x_r, Wr, fwd["topk_idx"], fwd["topk_prob"], dp)
     dx_r = dispatch_bwd(dx_disp, fwd["inv_perm"], S, K) + dx_router
     if Wdown is not None:
         out["dx_lat"] = dx_r
         dx_r, out["dWdown"] = latent_bwd(x, Wdown, dx_r)
+    if Ws1 is not None:
+        dx_r = dx_r + dx_shared
     out.update(dx=dx_r, dWr=dWr, dbias=dbias, dW1=dW1, dW2=dW2, dp=dp, ds=ds,
                dy_disp=dy_disp, dx_disp=dx_disp)
     return out
+
+
+# ---------------------------------------------------------------------------
+# The paper's production router (Section 5.2): sigmoid scores with a
+# selection-only expert bias, sequence-level balance loss, shared expert
+# ---------------------------------------------------------------------------
+#
+# The paper names these parts but does not write them out.  They are read as
+# the published forms they come from (sigmoid gating with a bias that only
+# steers selection and a complementary per-sequence balance loss, as in
+# DeepSeek-V3, arXiv:2412.19437, Section 2.1):
+#   s[t, e]   = sigmoid(logit[t, e])
+#   T_t       = top-K experts of s[t, e] + b[e]   (b: selection bias only)
+#   g[t, k]   = s[t, T_k] / sum_{j<K} s[t, T_j]   (the routed weight, b_p)
+#   loss      = coeff * mean over sequences of sum_e f_e * P_e, per sequence
+#               f_e = E / (K * T) * #{tokens of the sequence routed to e},
+#               P_e = (1 / T) * sum_t s[t, e] / sum_e' s[t, e'].
+# The shared expert is one ungated squared-ReLU MLP on every token, its
+# output added to the combined routed output.
+
+def sigmoid_scores(logits) -> np.ndarray:
+    """s = 1 / (1 + exp(-logit)) in float64 from the fp32 logits (-inf -> 0)."""
+    z = np.asarray(logits, dtype=np.float32).astype(np.float64)
+    if np.isnan(z).any():
+        raise ValueError("sigmoid routing is undefined for NaN logits")
+    with np.errstate(over="ignore"):
+        return 1.0 / (1.0 + np.exp(-z))
+
+
+def sigmoid_topk_select(logits, K: int, sel_bias=None) -> np.ndarray:
+    """Top-K experts per token by the selection score s + b (float64), best
+    first; equal selection scores go to the lower expert index.  The bias
+    steers which experts are picked and nothing else."""
+    s = sigmoid_scores(logits)
+    S, E = s.shape
+    if not 1 <= K <= E:
+        raise ValueError("need 1 <= K <= E")
+    key = s if sel_bias is None else s + np.asarray(sel_bias, np.float64)[None, :]
+    idx = np.empty((S, K), dtype=np.int32)
+    experts = np.arange(E)
+    for t in range(S):
+        order = np.lexsort((experts, -key[t]))   # score descending, then index ascending
+        idx[t] = order[:K]
+    return idx
+
+
+def sigmoid_gates(logits, idx) -> np.ndarray:
+    """Routed weights g[t, k] = s[t, T_k] / sum_j s[t, T_j], as fp32 (b_p).
+    The selection bias does not enter.  A row whose selected scores are all
+    zero (every selected logit -inf) has no defined weights."""
+    s = sigmoid_scores(logits)
+    sel = np.take_along_axis(s, np.asarray(idx, np.int64), axis=1)
+    tot = sel.sum(axis=1, keepdims=True)
+    if np.any(tot <= 0.0):
+        raise ValueError("every token needs a selected expert with a non-zero score")
+    return (sel / tot).astype(np.float32)
+
+
+def sigmoid_route(logits, K: int, sel_bias=None):
+    """sigmoid_topk_select then sigmoid_gates: (idx int32 [S,K], g fp32 [S,K])."""
+    idx = sigmoid_topk_select(logits, K, sel_bias)
+    return idx, sigmoid_gates(logits, idx)
+
+
+def _sequences(S: int, seq_len: int) -> int:
+    if seq_len <= 0 or S % seq_len:
+        raise ValueError("the batch must hold whole sequences (S % seq_len == 0)")
+    return S // seq_len
+
+
+def seq_aux_loss(logits, topk_idx, seq_len: int, coeff: float) -> float:
+    """Sequence-level balance loss (Section 5.2, coefficient 1e-4 there):
+    per sequence of seq_len tokens, sum_e f_e * P_e with f_e the expert's
+    share of the sequence's routed slots scaled by E / K (1 when balanced)
+    and P_e its mean normalised sigmoid score; averaged over the sequences
+    of the batch and scaled by coeff.  The selection is the routed one."""
+    s = sigmoid_scores(logits)
+    idx = np.asarray(topk_idx, np.int64)
+    S, E = s.shape
+    K = idx.shape[1]
+    B = _sequences(S, seq_len)
+    sn = s / s.sum(axis=1, keepdims=True)
+    total = 0.0
+    for b in range(B):
+        rows = slice(b * seq_len, (b + 1) * seq_len)
+        f = np.bincount(idx[rows].ravel(), minlength=E) * (E / (K * seq_len))
+        P = sn[rows].sum(axis=0) / seq_len
+        total += float(np.sum(f * P))
+    return coeff * total / B
+
+
+def seq_aux_loss_bwd(logits, topk_idx, seq_len: int, coeff: float) -> np.ndarray:
+    """d(seq_aux_loss)/d(logits) [S,E] with the selection (f) held fixed.
+    Through sn = s / sum(s) and s = sigmoid(logit), per token with
+    a_e = coeff * f_e / (B * T) of its sequence:
+        d sn_e      = a_e
+        d s_e       = (a_e - sum_e' a_e' sn_e') / sum_e' s_e'
+        d logit_e   = d s_e * s_e * (1 - s_e)."""
+    s = sigmoid_scores(logits)
+    idx = np.asarray(topk_idx, np.int64)
+    S, E = s.shape
+    K = idx.shape[1]
+    B = _sequences(S, seq_len)
+    tot = s.sum(axis=1, keepdims=True)
+    sn = s / tot
+    a = np.zeros((S, E))
+    for b in range(B):
+        rows = slice(b * seq_len, (b + 1) * seq_len)
+        f = np.bincount(idx[rows].ravel(), minlength=E) * (E / (K * seq_len))
+        a[rows] = coeff * f / (B * seq_len)
+    ds = (a - np.sum(a * sn, axis=1, keepdims=True)) / tot
+    return ds * s * (1.0 - s)
+
+
+def sigmoid_gate_bwd(logits, topk_idx, dg) -> np.ndarray:
+    """d(loss)/d(logits) [S,E] from dg = d(loss)/d(g) [S,K], selection held
+    fixed: with sel_k = s[T_k] and Z = sum_j sel_j,
+        d sel_k = (dg_k - sum_j dg_j g_j) / Z,   d logit = d s * s (1 - s)
+    on the selected experts, 0 elsewhere."""
+    s = sigmoid_scores(logits)
+    idx = np.asarray(topk_idx, np.int64)
+    dg = np.asarray(dg, np.float64)
+    S, E = s.shape
+    K = idx.shape[1]
+    sel = np.take_along_axis(s, idx, axis=1)
+    Z = sel.sum(axis=1, keepdims=True)
+    g = sel / Z
+    dsel = (dg - np.sum(dg * g, axis=1, keepdims=True)) / Z
+    out = np.zeros((S, E))
+    for t in range(S):
+        for k in range(K):
+            e = idx[t, k]
+            out[t, e] = dsel[t, k] * s[t, e] * (1.0 - s[t, e])
+    return out
+
+
+def router_linear_bwd(x_r, Wr, dlogits):
+    """Through logits = x_r @ Wr + bias: (dWr = x_r^T dl, dbias = sum_t dl,
+    dx_r = dl @ Wr^T), float64."""
+    x_r = np.asarray(x_r, np.float64)
+    Wr = np.asarray(Wr, np.float64)
+    dl = np.asarray(dlogits, np.float64)
+    return x_r.T @ dl, dl.sum(axis=0), dl @ Wr.T
+
+
+def expert_bias_update(sel_bias, counts, rate: float) -> np.ndarray:
+    """Load-driven update of the selection bias (the bias is not trained by
+    gradient): b_e += rate * sign(mean_e' counts - counts_e), i.e. an
+    overloaded expert is made less attractive, an underloaded one more."""
+    c = np.asarray(counts, np.float64)
+    return np.asarray(sel_bias, np.float64) + rate * np.sign(c.mean() - c)
+
+
+def shared_expert(x, Ws1, Ws2):
+    """The ungated shared expert on every token (Section 5.2):
+    u = x @ Ws1, h = max(u, 0)**2, y_s = h @ Ws2.  Returns (u, h, y_s)."""
+    x = np.asarray(x, np.float64)
+    u = x @ np.asarray(Ws1, np.float64)
+    h = np.maximum(u, 0.0) ** 2
+    return u, h, h @ np.asarray(Ws2, np.float64)
+
+
+def shared_expert_bwd(x, u, h, dy, Ws1, Ws2):
+    """Gradients of shared_expert: dh = dy Ws2^T, du = dh * 2 max(u, 0),
+    dx = du Ws1^T, dWs1 = x^T du, dWs2 = h^T dy.  Returns (dx, dWs1, dWs2)."""
+    x = np.asarray(x, np.float64)
+    dy = np.asarray(dy, np.float64)
+    Ws1 = np.asarray(Ws1, np.float64)
+    Ws2 = np.asarray(Ws2, np.float64)
+    du = (dy @ Ws2.T) * (2.0 * np.maximum(np.asarray(u, np.float64), 0.0))
+    return du @ Ws1.T, x.T @ du, np.asarray(h, np.float64).T @ dy
 
 
 # ---------------------------------------------------------------------------
