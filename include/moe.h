@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 1
+#define MOE_ABI_VERSION 2
 
 typedef uint16_t moe_bf16; /* bit pattern of a bfloat16 value (b_x = 2 bytes) */
 
@@ -237,14 +237,35 @@ typedef struct {
     moe_bf16* y_lat;           /* [S, D]  (H > 0 only) */
     void* ws;                  /* workspace, >= moe_layer_fwd_workspace_bytes */
     size_t ws_bytes;
+    /* The paper's production variant (Section 5.2); all zero / NULL gives
+     * the softmax layer above.  See the production-router section below. */
+    int32_t score_fn;          /* MOE_SCORE_SOFTMAX or MOE_SCORE_SIGMOID */
+    int32_t Fs;                /* shared-expert width (multiple of 8); 0 = none (H must be 0) */
+    const float* sel_bias;     /* [E] selection-only bias (sigmoid scores only) or NULL */
+    const moe_bf16* Ws1;       /* [D, Fs] when Fs > 0 */
+    const moe_bf16* Ws2;       /* [Fs, D] when Fs > 0 */
+    int64_t seq_len;           /* balance loss over sequences of seq_len tokens; 0 = none */
+    float aux_coeff;           /* balance-loss coefficient (the paper trains with 1e-4) */
+    float* aux_loss;           /* [1] fp32, required when seq_len > 0 */
+    int32_t* seq_counts;       /* [S / seq_len, E] routed counts per sequence, or NULL */
+    moe_bf16* h_s;             /* [S, Fs] shared-expert activation, or NULL */
+    moe_bf16* u_s;             /* [S, Fs] its pre-activation (saved only if given) */
+    float* y_s;                /* [S, D] fp32 shared-expert output, or NULL */
 } moe_layer_fwd_args;
+
+enum { MOE_SCORE_SOFTMAX = 0, MOE_SCORE_SIGMOID = 1 };
 
 /* Workspace bytes moe_layer_fwd needs for these arguments (intermediates the
  * caller does not export are carved from it).  0 if the sizes are invalid. */
 size_t moe_layer_fwd_workspace_bytes(const moe_layer_fwd_args* a);
 
 /* [x_lat = bf16(x @ Wdown)] -> logits -> route -> dispatch -> experts ->
- * combine -> [y = bf16(y_lat @ Wup)], all enqueued on `stream`. */
+ * combine -> [y = bf16(y_lat @ Wup)], all enqueued on `stream`.
+ * With score_fn = MOE_SCORE_SIGMOID the route is moe_route_sigmoid (with
+ * sel_bias); seq_len > 0 adds moe_seq_aux_loss; Fs > 0 runs the shared
+ * expert and adds its fp32 output in the combine, before the one bf16
+ * rounding of y (moe_combine_add).  A shared expert with a latent
+ * projection (H > 0) returns MOE_ERR_UNSUPPORTED. */
 int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream);
 
 /* ---------------------------------------------------------------------- */
@@ -331,6 +352,107 @@ size_t moe_latent_proj_bwd_workspace_bytes(int64_t M, int32_t Kd, int32_t N);
 int moe_latent_proj_bwd(const moe_bf16* x_in, const moe_bf16* W, const moe_bf16* dout,
                         int64_t M, int32_t Kd, int32_t N, moe_bf16* dx_in, float* dW,
                         void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------- */
+/* The paper's production router and shared expert (Section 5.2): sigmoid  */
+/* router scores with a selection-only expert bias, sequence-level         */
+/* auxiliary load balancing, and an ungated shared expert whose output is  */
+/* added to the combined routed output.  The paper names these parts; the  */
+/* formulas are the published sigmoid gating with a selection-only bias    */
+/* and its per-sequence balance loss:                                      */
+/*   s = sigmoid(logit);  T_t = top-K of s + sel_bias;                     */
+/*   g_k = s[T_k] / sum_j s[T_j]  (the routed weight, b_p);               */
+/*   loss = coeff / B * sum_b sum_e f_be P_be,  f_be = E/(K T) n_be,       */
+/*   P_be = mean over the sequence's tokens of s[t,e] / sum_e' s[t,e'].    */
+/* ---------------------------------------------------------------------- */
+/* Sigmoid routing: like moe_route_topk (same outputs, same ordering rules
+ * on the selection score s + sel_bias computed in fp32, same workspace
+ * moe_route_workspace_bytes), with topk_gate = the routed weights g.
+ * sel_bias [E] fp32 or NULL (zero).  Rows whose selected scores are all 0
+ * (every selected logit -inf) and NaN logits give unspecified weights. */
+int moe_route_sigmoid(const float* logits, const float* sel_bias, int64_t S, int32_t E, int32_t K,
+                      int32_t* topk_idx, float* topk_gate, int32_t* counts, int32_t* offsets,
+                      int32_t* perm, int32_t* inv_perm, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Workspace bytes moe_seq_aux_loss needs; 0 for invalid sizes. */
+size_t moe_seq_aux_loss_workspace_bytes(int64_t S, int32_t E, int64_t seq_len);
+
+/* The sequence balance loss of the sigmoid scores of `logits` for the
+ * routing topk_idx, over the S / seq_len sequences of seq_len tokens:
+ *   loss [1] fp32 (fixed-order sums, fp64 across chunks);
+ *   seq_counts [S / seq_len, E] int32 routed rows per sequence and expert,
+ *   or NULL (moe_router_bwd_sigmoid needs them for the loss gradient).
+ * Errors: route shapes, seq_len >= 1 dividing S (MOE_ERR_SHAPE),
+ * MOE_ERR_WORKSPACE. */
+int moe_seq_aux_loss(const float* logits, const int32_t* topk_idx, int64_t S, int32_t E, int32_t K,
+                     int64_t seq_len, float coeff, float* loss, int32_t* seq_counts, void* ws,
+                     size_t ws_bytes, hipStream_t stream);
+
+/* Workspace bytes moe_router_bwd_sigmoid needs; 0 for invalid sizes. */
+size_t moe_router_bwd_sigmoid_workspace_bytes(int64_t S, int32_t D, int32_t E);
+
+/* Backward of the sigmoid router with the selection held fixed, for the
+ * loss  <dg, g> + balance loss:
+ *   dlogits = s (1 - s) * ( on the picked experts (dg_k - sum_j g_j dg_j) / Z,
+ *                           Z = sum_j s[T_j];
+ *                           plus, with seq_counts, the balance-loss gradient
+ *                           (a_e - sum_e' a_e' s_e'/sum s) / sum s,
+ *                           a_e = coeff E n_be / (K seq_len^2 B) )
+ *   dWr, dbias, dx_r as for moe_router_bwd.  Without the balance loss dx_r
+ *   is the K nonzero terms in fp32; with it, dlogits is dense and dx_r is
+ *   one MFMA product of three-term bf16 splits of dlogits and Wr (error
+ *   within a few 2^-24 of |dlogits| |Wr|^T).
+ *   logits [S, E] fp32 (the router's output);  topk_idx, topk_gate, dg [S, K];
+ *   seq_counts [S / seq_len, E] from moe_seq_aux_loss, or NULL (no loss);
+ *   dlogits [S, E] fp32 or NULL (kept in the workspace);  dWr [D, E];
+ *   dbias [E] or NULL;  dx_r [S, D] fp32 (16-byte aligned) or NULL.
+ * Errors: as moe_router_bwd; seq_len must divide S when seq_counts is given. */
+int moe_router_bwd_sigmoid(const moe_bf16* x_r, const float* Wr, const float* logits,
+                           const int32_t* topk_idx, const float* topk_gate, const float* dg,
+                           const int32_t* seq_counts, int64_t seq_len, float coeff, int64_t S,
+                           int32_t D, int32_t E, int32_t K, float* dlogits, float* dWr, float* dbias,
+                           float* dx_r, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Load-driven update of the selection-only bias (it is not trained by
+ * gradient): sel_bias[e] += rate * sign(mean(counts) - counts[e]), the sign
+ * taken exactly in integers.  counts [E] (moe_route_sigmoid's), sel_bias [E]
+ * fp32 updated in place. */
+int moe_expert_bias_update(const int32_t* counts, int32_t E, float rate, float* sel_bias,
+                           hipStream_t stream);
+
+/* y[t] = bf16( sum_{k<K} p_disp[pos] y_disp[pos] + y_add[t] ): moe_combine
+ * with an fp32 addend (the shared expert's output) added after the K-term
+ * sum and before the one rounding.  y_add [S, D] fp32, 16-byte aligned. */
+int moe_combine_add(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_perm,
+                    const float* y_add, int64_t S, int32_t D, int32_t K, moe_bf16* y,
+                    hipStream_t stream);
+
+/* Shared expert forward on every token (ungated, squared-ReLU):
+ *   u_s = x @ Ws1 (bf16, saved if u_s != NULL);  h_s = bf16(max(u_s, 0)^2);
+ *   y_s = h_s @ Ws2  (fp32, for moe_combine_add).
+ *   x [S, D] bf16;  Ws1 [D, Fs];  Ws2 [Fs, D];  h_s [S, Fs];  y_s [S, D] fp32.
+ * Errors: D, Fs multiples of 8 in [8, 65536]; MOE_ERR_UNSUPPORTED if D*Fs*2
+ * reaches 2^31. */
+int moe_shared_expert_fwd(const moe_bf16* x, const moe_bf16* Ws1, const moe_bf16* Ws2, int64_t S,
+                          int32_t D, int32_t Fs, moe_bf16* h_s, moe_bf16* u_s, float* y_s,
+                          hipStream_t stream);
+
+/* Workspace bytes moe_shared_expert_bwd needs; 0 for invalid sizes. */
+size_t moe_shared_expert_bwd_workspace_bytes(int64_t S, int32_t D, int32_t Fs);
+
+/* Shared expert backward for the layer-output gradient dy:
+ *   du   = bf16( (dy @ Ws2^T) * 2 max(u_s, 0) )      (workspace)
+ *   dx   = du @ Ws1^T  fp32 [S, D]; with accumulate_dx, added to what dx
+ *          holds (e.g. moe_router_bwd*'s dx_r, then pass it as dx_add to
+ *          moe_dispatch_bwd); dx may be NULL
+ *   dWs1 = x^T du  [D, Fs] fp32;   dWs2 = h_s^T dy  [Fs, D] fp32
+ *   (fixed-order sums over row chunks).
+ * Errors: as moe_shared_expert_fwd; MOE_ERR_UNSUPPORTED if S*max(D, Fs)*2
+ * reaches 2^31; MOE_ERR_WORKSPACE. */
+int moe_shared_expert_bwd(const moe_bf16* x, const moe_bf16* u_s, const moe_bf16* h_s,
+                          const moe_bf16* dy, const moe_bf16* Ws1, const moe_bf16* Ws2, int64_t S,
+                          int32_t D, int32_t Fs, float* dx, int32_t accumulate_dx, float* dWs1,
+                          float* dWs2, void* ws, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

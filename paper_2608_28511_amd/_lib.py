@@ -44,7 +44,13 @@ class LayerFwdArgs(C.Structure):
         ("offsets", vp), ("perm", vp), ("inv_perm", vp), ("x_disp", vp), ("p_disp", vp),
         ("h", vp), ("u_save", vp), ("y_disp", vp), ("y_lat", vp),
         ("ws", vp), ("ws_bytes", sz),
+        ("score_fn", i32), ("Fs", i32), ("sel_bias", vp), ("Ws1", vp), ("Ws2", vp),
+        ("seq_len", i64), ("aux_coeff", C.c_float), ("aux_loss", vp), ("seq_counts", vp),
+        ("h_s", vp), ("u_s", vp), ("y_s", vp),
     ]
+
+
+SCORE_SOFTMAX, SCORE_SIGMOID = 0, 1
 
 
 _PROTOS = {
@@ -74,6 +80,17 @@ _PROTOS = {
     "moe_router_bwd": (C.c_int, [vp, vp, vp, vp, vp, i64, i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
     "moe_latent_proj_bwd_workspace_bytes": (sz, [i64, i32, i32]),
     "moe_latent_proj_bwd": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp, vp, sz, vp]),
+    "moe_route_sigmoid": (C.c_int, [vp, vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+    "moe_seq_aux_loss_workspace_bytes": (sz, [i64, i32, i64]),
+    "moe_seq_aux_loss": (C.c_int, [vp, vp, i64, i32, i32, i64, C.c_float, vp, vp, vp, sz, vp]),
+    "moe_router_bwd_sigmoid_workspace_bytes": (sz, [i64, i32, i32]),
+    "moe_router_bwd_sigmoid": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, i64, C.c_float, i64, i32, i32, i32,
+                                         vp, vp, vp, vp, vp, sz, vp]),
+    "moe_expert_bias_update": (C.c_int, [vp, i32, C.c_float, vp, vp]),
+    "moe_combine_add": (C.c_int, [vp, vp, vp, vp, i64, i32, i32, vp, vp]),
+    "moe_shared_expert_fwd": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp, vp, vp]),
+    "moe_shared_expert_bwd_workspace_bytes": (sz, [i64, i32, i32]),
+    "moe_shared_expert_bwd": (C.c_int, [vp, vp, vp, vp, vp, vp, i64, i32, i32, vp, i32, vp, vp, vp, sz, vp]),
 }
 
 EXPORTED = tuple(_PROTOS)
@@ -212,15 +229,18 @@ _LAYER_TENSORS = {
     "x": BF16, "Wr": F32, "router_bias": F32, "Wdown": BF16, "W1": BF16, "W2": BF16, "Wup": BF16,
     "y": BF16, "x_lat": BF16, "logits": F32, "topk_idx": I32, "topk_prob": F32, "counts": I32,
     "offsets": I32, "perm": I32, "inv_perm": I32, "x_disp": BF16, "p_disp": F32, "h": BF16,
-    "u_save": BF16, "y_disp": BF16, "y_lat": BF16,
+    "u_save": BF16, "y_disp": BF16, "y_lat": BF16, "sel_bias": F32, "Ws1": BF16, "Ws2": BF16,
+    "aux_loss": F32, "seq_counts": I32, "h_s": BF16, "u_s": BF16, "y_s": F32,
 }
 
 
-def layer_fwd_args(S, H, D, E, K, F, ws=None, **tensors) -> LayerFwdArgs:
+def layer_fwd_args(S, H, D, E, K, F, ws=None, score_fn=SCORE_SOFTMAX, Fs=0, seq_len=0, aux_coeff=0.0,
+                   **tensors) -> LayerFwdArgs:
     """Fill a moe_layer_fwd_args from sizes and named tensors (None = NULL)."""
     a = LayerFwdArgs()
     a.struct_size = C.sizeof(LayerFwdArgs)
     a.S, a.H, a.D, a.E, a.K, a.F = S, H, D, E, K, F
+    a.score_fn, a.Fs, a.seq_len, a.aux_coeff = score_fn, Fs, seq_len, aux_coeff
     for name, t in tensors.items():
         if name not in _LAYER_TENSORS:
             raise KeyError(name)
@@ -289,3 +309,68 @@ def moe_latent_proj_bwd(x_in, W, dout, M, Kd, N, dx_in, dW, ws):
         _ptr(x_in, BF16, "x_in"), _ptr(W, BF16, "W"), _ptr(dout, BF16, "dout"), M, Kd, N,
         _ptr(dx_in, BF16, "dx_in"), _ptr(dW, F32, "dW"), _ptr(ws, None, "ws"),
         0 if ws is None else ws.numel() * ws.element_size(), _stream()), "moe_latent_proj_bwd")
+
+
+def _wsz(ws):
+    return 0 if ws is None else ws.numel() * ws.element_size()
+
+
+def moe_route_sigmoid(logits, sel_bias, S, E, K, topk_idx, topk_gate, counts, offsets, perm, inv_perm, ws):
+    _check(load().moe_route_sigmoid(
+        _ptr(logits, F32, "logits"), _ptr(sel_bias, F32, "sel_bias"), S, E, K, _ptr(topk_idx, I32, "topk_idx"),
+        _ptr(topk_gate, F32, "topk_gate"), _ptr(counts, I32, "counts"), _ptr(offsets, I32, "offsets"),
+        _ptr(perm, I32, "perm"), _ptr(inv_perm, I32, "inv_perm"), _ptr(ws, None, "ws"), _wsz(ws), _stream()),
+        "moe_route_sigmoid")
+
+
+def moe_seq_aux_loss_workspace_bytes(S, E, seq_len) -> int:
+    return load().moe_seq_aux_loss_workspace_bytes(S, E, seq_len)
+
+
+def moe_seq_aux_loss(logits, topk_idx, S, E, K, seq_len, coeff, loss, seq_counts, ws):
+    _check(load().moe_seq_aux_loss(
+        _ptr(logits, F32, "logits"), _ptr(topk_idx, I32, "topk_idx"), S, E, K, seq_len, coeff,
+        _ptr(loss, F32, "loss"), _ptr(seq_counts, I32, "seq_counts"), _ptr(ws, None, "ws"), _wsz(ws), _stream()),
+        "moe_seq_aux_loss")
+
+
+def moe_router_bwd_sigmoid_workspace_bytes(S, D, E) -> int:
+    return load().moe_router_bwd_sigmoid_workspace_bytes(S, D, E)
+
+
+def moe_router_bwd_sigmoid(x_r, Wr, logits, topk_idx, topk_gate, dg, seq_counts, seq_len, coeff, S, D, E, K,
+                           dlogits, dWr, dbias, dx_r, ws):
+    _check(load().moe_router_bwd_sigmoid(
+        _ptr(x_r, BF16, "x_r"), _ptr(Wr, F32, "Wr"), _ptr(logits, F32, "logits"), _ptr(topk_idx, I32, "topk_idx"),
+        _ptr(topk_gate, F32, "topk_gate"), _ptr(dg, F32, "dg"), _ptr(seq_counts, I32, "seq_counts"), seq_len,
+        coeff, S, D, E, K, _ptr(dlogits, F32, "dlogits"), _ptr(dWr, F32, "dWr"), _ptr(dbias, F32, "dbias"),
+        _ptr(dx_r, F32, "dx_r"), _ptr(ws, None, "ws"), _wsz(ws), _stream()), "moe_router_bwd_sigmoid")
+
+
+def moe_expert_bias_update(counts, E, rate, sel_bias):
+    _check(load().moe_expert_bias_update(_ptr(counts, I32, "counts"), E, rate, _ptr(sel_bias, F32, "sel_bias"),
+                                         _stream()), "moe_expert_bias_update")
+
+
+def moe_combine_add(y_disp, p_disp, inv_perm, y_add, S, D, K, y):
+    _check(load().moe_combine_add(_ptr(y_disp, BF16, "y_disp"), _ptr(p_disp, F32, "p_disp"),
+                                  _ptr(inv_perm, I32, "inv_perm"), _ptr(y_add, F32, "y_add"), S, D, K,
+                                  _ptr(y, BF16, "y"), _stream()), "moe_combine_add")
+
+
+def moe_shared_expert_fwd(x, Ws1, Ws2, S, D, Fs, h_s, u_s, y_s):
+    _check(load().moe_shared_expert_fwd(_ptr(x, BF16, "x"), _ptr(Ws1, BF16, "Ws1"), _ptr(Ws2, BF16, "Ws2"), S, D,
+                                        Fs, _ptr(h_s, BF16, "h_s"), _ptr(u_s, BF16, "u_s"), _ptr(y_s, F32, "y_s"),
+                                        _stream()), "moe_shared_expert_fwd")
+
+
+def moe_shared_expert_bwd_workspace_bytes(S, D, Fs) -> int:
+    return load().moe_shared_expert_bwd_workspace_bytes(S, D, Fs)
+
+
+def moe_shared_expert_bwd(x, u_s, h_s, dy, Ws1, Ws2, S, D, Fs, dx, accumulate_dx, dWs1, dWs2, ws):
+    _check(load().moe_shared_expert_bwd(
+        _ptr(x, BF16, "x"), _ptr(u_s, BF16, "u_s"), _ptr(h_s, BF16, "h_s"), _ptr(dy, BF16, "dy"),
+        _ptr(Ws1, BF16, "Ws1"), _ptr(Ws2, BF16, "Ws2"), S, D, Fs, _ptr(dx, F32, "dx"), int(bool(accumulate_dx)),
+        _ptr(dWs1, F32, "dWs1"), _ptr(dWs2, F32, "dWs2"), _ptr(ws, None, "ws"), _wsz(ws), _stream()),
+        "moe_shared_expert_bwd")

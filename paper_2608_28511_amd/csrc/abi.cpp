@@ -247,6 +247,22 @@ struct Carve {
     }
 };
 
+// coeff * E / (K T^2 B): the balance loss and its gradient per routed count.
+double aux_coef(float coeff, int64_t S, int32_t E, int32_t K, int64_t T) {
+    const double B = (double)(S / T);
+    return (double)coeff * E / ((double)K * (double)T * (double)T * B);
+}
+
+int shared_fwd(const moe_bf16* x, const moe_bf16* Ws1, const moe_bf16* Ws2, int64_t S, int32_t D, int32_t Fs,
+               moe_bf16* h_s, moe_bf16* u_s, float* y_s, hipStream_t stream) {
+    // h_s = bf16(max(x Ws1, 0)^2) (u_s = bf16(x Ws1) if wanted), y_s = h_s Ws2 in fp32
+    MOE_HIP(moe::launch_grouped_rows(x, D, Ws1, Fs, 0, false, h_s, Fs, moe::EPI_RELU2, nullptr, u_s, nullptr, 1,
+                                     S, Fs, D, stream));
+    MOE_HIP(moe::launch_grouped_rows(h_s, Fs, Ws2, D, 0, false, y_s, D, moe::EPI_F32, nullptr, nullptr, nullptr,
+                                     1, S, D, Fs, stream));
+    return MOE_OK;
+}
+
 int check_layer_args(const moe_layer_fwd_args* a) {
     if (a == nullptr) return MOE_ERR_NULL;
     if (a->struct_size != sizeof(moe_layer_fwd_args)) return MOE_ERR_SHAPE;
@@ -254,6 +270,14 @@ int check_layer_args(const moe_layer_fwd_args* a) {
     if (!dim_ok(a->D) || !dim_ok(a->F)) return MOE_ERR_SHAPE;
     if (a->H != 0 && !dim_ok(a->H)) return MOE_ERR_SHAPE;
     if (!weight_ok(a->D, a->F) || (a->H != 0 && !weight_ok(a->H, a->D))) return MOE_ERR_UNSUPPORTED;
+    if (a->score_fn != MOE_SCORE_SOFTMAX && a->score_fn != MOE_SCORE_SIGMOID) return MOE_ERR_SHAPE;
+    if (a->score_fn == MOE_SCORE_SOFTMAX && a->sel_bias != nullptr) return MOE_ERR_SHAPE;
+    if (a->seq_len < 0 || (a->seq_len > 0 && (a->score_fn != MOE_SCORE_SIGMOID || a->S % a->seq_len != 0)))
+        return MOE_ERR_SHAPE;
+    if (a->Fs != 0) {
+        if (!dim_ok(a->Fs)) return MOE_ERR_SHAPE;
+        if (a->H != 0 || !weight_ok(a->D, a->Fs)) return MOE_ERR_UNSUPPORTED;
+    }
     return MOE_OK;
 }
 
@@ -263,6 +287,7 @@ struct LayerBufs {
     moe_bf16* x_lat; float* logits; int32_t* topk_idx; float* topk_prob; int32_t* counts;
     int32_t* offsets; int32_t* perm; int32_t* inv_perm; moe_bf16* x_disp; float* p_disp;
     moe_bf16* h; moe_bf16* y_disp; moe_bf16* y_lat; void* route_ws; void* sched; void* router_ws;
+    void* aux_ws; int32_t* seq_counts; moe_bf16* h_s; float* y_s;
 };
 
 size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
@@ -289,6 +314,14 @@ size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
     b->route_ws = c.take(moe::route_ws_bytes(S, E));
     b->sched = c.take(moe::gemm_schedule_bytes(E, R));
     b->router_ws = c.take(moe::router_ws_bytes(D, E));
+    b->aux_ws = nullptr;
+    b->seq_counts = nullptr;
+    if (a->seq_len > 0) {
+        b->aux_ws = c.take(moe::seq_aux_ws_bytes(S, E, a->seq_len));
+        b->seq_counts = pick(a->seq_counts, (size_t)(S / a->seq_len) * E * 4);
+    }
+    b->h_s = a->Fs ? pick(a->h_s, (size_t)S * a->Fs * 2) : nullptr;
+    b->y_s = a->Fs ? pick(a->y_s, (size_t)S * D * 4) : nullptr;
     return c.used;
 }
 
@@ -317,10 +350,18 @@ int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
     } else if (a->Wdown != nullptr || a->Wup != nullptr) {
         return MOE_ERR_SHAPE;
     }
-    const void* bf16_ptrs[] = {a->x_lat, a->x_disp, a->h, a->u_save, a->y_disp, a->y_lat};
+    if (a->Fs) {
+        MOE_TRY(need(a->Ws1, (uint64_t)D * a->Fs * 2, 16));
+        MOE_TRY(need(a->Ws2, (uint64_t)a->Fs * D * 2, 16));
+    } else if (a->Ws1 != nullptr || a->Ws2 != nullptr) {
+        return MOE_ERR_SHAPE;
+    }
+    if (a->seq_len > 0) MOE_TRY(need(a->aux_loss, 4, 4));
+    const void* bf16_ptrs[] = {a->x_lat, a->x_disp, a->h, a->u_save, a->y_disp, a->y_lat, a->h_s, a->u_s,
+                               a->y_s};
     for (const void* p : bf16_ptrs) MOE_TRY(opt(p, 16));
     const void* word_ptrs[] = {a->logits, a->topk_idx, a->topk_prob, a->counts, a->offsets,
-                               a->perm, a->inv_perm, a->p_disp};
+                               a->perm, a->inv_perm, a->p_disp, a->sel_bias, a->seq_counts};
     for (const void* p : word_ptrs) MOE_TRY(opt(p, 4));
 
     LayerBufs b;
@@ -336,8 +377,14 @@ int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
         x_r = b.x_lat;
     }
     MOE_HIP(moe::launch_router_logits(x_r, a->Wr, a->router_bias, S, D, E, b.logits, b.router_ws, stream));
+    const bool sig = a->score_fn == MOE_SCORE_SIGMOID;
     MOE_HIP(moe::launch_route(b.logits, S, E, K, b.topk_idx, b.topk_prob, b.counts, b.offsets, b.perm,
-                              b.inv_perm, b.route_ws, stream));
+                              b.inv_perm, b.route_ws, stream, sig, a->sel_bias));
+    if (a->seq_len > 0) {
+        MOE_HIP(moe::launch_seq_aux_loss(b.logits, b.topk_idx, S, E, K, a->seq_len,
+                                         aux_coef(a->aux_coeff, S, E, K, a->seq_len), a->aux_loss,
+                                         b.seq_counts, b.aux_ws, stream));
+    }
     MOE_HIP(moe::launch_dispatch(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_disp, b.p_disp, stream));
     if (R > 0) {
         MOE_HIP(moe::launch_tile_schedule(b.offsets, E, R, b.sched, stream));
@@ -346,8 +393,9 @@ int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
         MOE_HIP(moe::launch_grouped_rows(b.h, F, a->W2, D, (int64_t)F * D, false, b.y_disp, D,
                                          moe::EPI_BF16, nullptr, nullptr, b.sched, E, R, D, F, stream));
     }
+    if (a->Fs && S > 0) MOE_TRY(shared_fwd(a->x, a->Ws1, a->Ws2, S, D, a->Fs, b.h_s, a->u_s, b.y_s, stream));
     moe_bf16* comb_out = H ? b.y_lat : a->y;
-    MOE_HIP(moe::launch_combine(b.y_disp, b.p_disp, b.inv_perm, S, D, K, nullptr, comb_out, stream));
+    MOE_HIP(moe::launch_combine(b.y_disp, b.p_disp, b.inv_perm, S, D, K, b.y_s, comb_out, stream));
     if (H) {
         MOE_HIP(moe::launch_grouped_rows(b.y_lat, D, a->Wup, H, 0, false, a->y, H, moe::EPI_BF16,
                                          nullptr, nullptr, nullptr, 1, S, H, D, stream));
@@ -486,6 +534,173 @@ int moe_latent_proj_bwd(const moe_bf16* x_in, const moe_bf16* W, const moe_bf16*
                                           stream));
         MOE_HIP(moe::launch_sum_planes(part, nch, Kd, N, 1, N, dW, stream));
     }
+    return MOE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Production router (sigmoid scores, selection-only bias, balance loss) and
+// the shared expert
+// ---------------------------------------------------------------------------
+
+int moe_route_sigmoid(const float* logits, const float* sel_bias, int64_t S, int32_t E, int32_t K,
+                      int32_t* topk_idx, float* topk_gate, int32_t* counts, int32_t* offsets, int32_t* perm,
+                      int32_t* inv_perm, void* ws, size_t ws_bytes, hipStream_t stream) {
+    MOE_TRY(check_route_shape(S, E, K));
+    const uint64_t R = (uint64_t)S * K;
+    MOE_TRY(need(logits, (uint64_t)S * E * 4, 4));
+    MOE_TRY(opt(sel_bias, 4));
+    MOE_TRY(need(topk_idx, R * 4, 4));
+    MOE_TRY(need(topk_gate, R * 4, 4));
+    MOE_TRY(need(counts, (uint64_t)E * 4, 4));
+    MOE_TRY(need(offsets, (uint64_t)(E + 1) * 4, 4));
+    MOE_TRY(need(perm, R * 4, 4));
+    MOE_TRY(need(inv_perm, R * 4, 4));
+    const size_t wsn = moe::route_ws_bytes(S, E);
+    if (wsn > 0 && (ws == nullptr || ws_bytes < wsn)) return MOE_ERR_WORKSPACE;
+    MOE_TRY(opt(ws, 16));
+    return hip_status(moe::launch_route(logits, S, E, K, topk_idx, topk_gate, counts, offsets, perm, inv_perm,
+                                        ws, stream, true, sel_bias));
+}
+
+size_t moe_seq_aux_loss_workspace_bytes(int64_t S, int32_t E, int64_t seq_len) {
+    if (S < 0 || S >= kMaxRows || E < 1 || E > kMaxE || seq_len < 1 || S % seq_len != 0) return 0;
+    return moe::seq_aux_ws_bytes(S, E, seq_len);
+}
+
+int moe_seq_aux_loss(const float* logits, const int32_t* topk_idx, int64_t S, int32_t E, int32_t K,
+                     int64_t seq_len, float coeff, float* loss, int32_t* seq_counts, void* ws, size_t ws_bytes,
+                     hipStream_t stream) {
+    MOE_TRY(check_route_shape(S, E, K));
+    if (seq_len < 1 || S % seq_len != 0) return MOE_ERR_SHAPE;
+    MOE_TRY(need(logits, (uint64_t)S * E * 4, 4));
+    MOE_TRY(need(topk_idx, (uint64_t)S * K * 4, 4));
+    MOE_TRY(need(loss, 4, 4));
+    MOE_TRY(opt(seq_counts, 4));
+    const size_t wsn = moe::seq_aux_ws_bytes(S, E, seq_len);
+    if (wsn > 0 && (ws == nullptr || ws_bytes < wsn)) return MOE_ERR_WORKSPACE;
+    MOE_TRY(opt(ws, 16));
+    return hip_status(moe::launch_seq_aux_loss(logits, topk_idx, S, E, K, seq_len, aux_coef(coeff, S, E, K, seq_len),
+                                               loss, seq_counts, ws, stream));
+}
+
+size_t moe_router_bwd_sigmoid_workspace_bytes(int64_t S, int32_t D, int32_t E) {
+    if (S < 0 || S >= kMaxRows || !dim_ok(D) || E < 1 || E > kMaxE) return 0;
+    return moe::router_bwd_ws_bytes(S, D, E, true);
+}
+
+int moe_router_bwd_sigmoid(const moe_bf16* x_r, const float* Wr, const float* logits, const int32_t* topk_idx,
+                           const float* topk_gate, const float* dg, const int32_t* seq_counts, int64_t seq_len,
+                           float coeff, int64_t S, int32_t D, int32_t E, int32_t K, float* dlogits, float* dWr,
+                           float* dbias, float* dx_r, void* ws, size_t ws_bytes, hipStream_t stream) {
+    MOE_TRY(check_route_shape(S, E, K));
+    if (!dim_ok(D)) return MOE_ERR_SHAPE;
+    if (seq_counts != nullptr && (seq_len < 1 || S % seq_len != 0)) return MOE_ERR_SHAPE;
+    const int32_t E6 = 6 * ((E + 7) / 8 * 8);  // widest bf16 plane rows of dlogits
+    if (!weight_ok(S, D > E6 ? D : E6)) return MOE_ERR_UNSUPPORTED;
+    const uint64_t R = (uint64_t)S * K;
+    MOE_TRY(need(x_r, (uint64_t)S * D * 2, 16));
+    MOE_TRY(need(Wr, (uint64_t)D * E * 4, 4));
+    MOE_TRY(need(logits, (uint64_t)S * E * 4, 4));
+    MOE_TRY(need(topk_idx, R * 4, 4));
+    MOE_TRY(need(topk_gate, R * 4, 4));
+    MOE_TRY(need(dg, R * 4, 4));
+    MOE_TRY(opt(seq_counts, 4));
+    MOE_TRY(opt(dlogits, 4));
+    MOE_TRY(need(dWr, (uint64_t)D * E * 4, 4));
+    MOE_TRY(opt(dbias, 4));
+    MOE_TRY(opt(dx_r, 16));
+    if (ws == nullptr || ws_bytes < moe::router_bwd_ws_bytes(S, D, E, true)) return MOE_ERR_WORKSPACE;
+    MOE_TRY(opt(ws, 256));
+    const float coef = seq_counts != nullptr ? (float)aux_coef(coeff, S, E, K, seq_len) : 0.f;
+    return hip_status(moe::launch_router_bwd_sigmoid(x_r, Wr, logits, topk_idx, topk_gate, dg, seq_counts,
+                                                     seq_counts != nullptr ? seq_len : 1, coef, S, D, E, K,
+                                                     dlogits, dWr, dbias, dx_r, ws, stream));
+}
+
+int moe_expert_bias_update(const int32_t* counts, int32_t E, float rate, float* sel_bias, hipStream_t stream) {
+    if (E < 1 || E > kMaxE) return MOE_ERR_SHAPE;
+    MOE_TRY(need(counts, (uint64_t)E * 4, 4));
+    MOE_TRY(need(sel_bias, (uint64_t)E * 4, 4));
+    return hip_status(moe::launch_expert_bias_update(counts, E, rate, sel_bias, stream));
+}
+
+int moe_combine_add(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_perm, const float* y_add,
+                    int64_t S, int32_t D, int32_t K, moe_bf16* y, hipStream_t stream) {
+    if (S < 0 || !dim_ok(D) || K < 1 || K > kMaxK || S * (int64_t)K >= kMaxRows) return MOE_ERR_SHAPE;
+    const uint64_t R = (uint64_t)S * K;
+    MOE_TRY(need(y_disp, R * D * 2, 16));
+    MOE_TRY(opt(p_disp, 4));
+    MOE_TRY(need(inv_perm, R * 4, 4));
+    MOE_TRY(need(y_add, (uint64_t)S * D * 4, 16));
+    MOE_TRY(need(y, (uint64_t)S * D * 2, 16));
+    return hip_status(moe::launch_combine(y_disp, p_disp, inv_perm, S, D, K, y_add, y, stream));
+}
+
+static int check_shared(int64_t S, int32_t D, int32_t Fs) {
+    if (S < 0 || S >= kMaxRows || !dim_ok(D) || !dim_ok(Fs)) return MOE_ERR_SHAPE;
+    if (!weight_ok(D, Fs)) return MOE_ERR_UNSUPPORTED;
+    return MOE_OK;
+}
+
+int moe_shared_expert_fwd(const moe_bf16* x, const moe_bf16* Ws1, const moe_bf16* Ws2, int64_t S, int32_t D,
+                          int32_t Fs, moe_bf16* h_s, moe_bf16* u_s, float* y_s, hipStream_t stream) {
+    MOE_TRY(check_shared(S, D, Fs));
+    MOE_TRY(need(x, (uint64_t)S * D * 2, 16));
+    MOE_TRY(need(Ws1, (uint64_t)D * Fs * 2, 16));
+    MOE_TRY(need(Ws2, (uint64_t)Fs * D * 2, 16));
+    MOE_TRY(need(h_s, (uint64_t)S * Fs * 2, 16));
+    MOE_TRY(opt(u_s, 16));
+    MOE_TRY(need(y_s, (uint64_t)S * D * 4, 16));
+    if (S == 0) return MOE_OK;
+    return shared_fwd(x, Ws1, Ws2, S, D, Fs, h_s, u_s, y_s, stream);
+}
+
+static size_t shared_bwd_ws(int64_t S, int32_t D, int32_t Fs) {
+    const int nch = moe::wgrad_chunks(S, D > Fs ? D : Fs, D > Fs ? Fs : D);
+    return align256((size_t)S * Fs * 2) + align256((size_t)nch * D * Fs * 4);
+}
+
+size_t moe_shared_expert_bwd_workspace_bytes(int64_t S, int32_t D, int32_t Fs) {
+    if (check_shared(S, D, Fs) != MOE_OK) return 0;
+    return shared_bwd_ws(S, D, Fs);
+}
+
+int moe_shared_expert_bwd(const moe_bf16* x, const moe_bf16* u_s, const moe_bf16* h_s, const moe_bf16* dy,
+                          const moe_bf16* Ws1, const moe_bf16* Ws2, int64_t S, int32_t D, int32_t Fs, float* dx,
+                          int32_t accumulate_dx, float* dWs1, float* dWs2, void* ws, size_t ws_bytes,
+                          hipStream_t stream) {
+    MOE_TRY(check_shared(S, D, Fs));
+    if (!weight_ok(S, D > Fs ? D : Fs)) return MOE_ERR_UNSUPPORTED;  // wgrad operand rows
+    MOE_TRY(need(x, (uint64_t)S * D * 2, 16));
+    MOE_TRY(need(u_s, (uint64_t)S * Fs * 2, 16));
+    MOE_TRY(need(h_s, (uint64_t)S * Fs * 2, 16));
+    MOE_TRY(need(dy, (uint64_t)S * D * 2, 16));
+    MOE_TRY(need(Ws1, (uint64_t)D * Fs * 2, 16));
+    MOE_TRY(need(Ws2, (uint64_t)Fs * D * 2, 16));
+    MOE_TRY(opt(dx, 16));
+    MOE_TRY(need(dWs1, (uint64_t)D * Fs * 4, 4));
+    MOE_TRY(need(dWs2, (uint64_t)Fs * D * 4, 4));
+    if (ws == nullptr || ws_bytes < shared_bwd_ws(S, D, Fs)) return MOE_ERR_WORKSPACE;
+    MOE_TRY(opt(ws, 256));
+    moe_bf16* du = (moe_bf16*)ws;
+    float* part = (float*)((char*)ws + align256((size_t)S * Fs * 2));
+    if (S > 0) {
+        // du = (dy Ws2^T) * 2 max(u, 0): Ws2 [Fs, D] read D-contiguous per output column
+        MOE_HIP(moe::launch_grouped_rows(dy, D, Ws2, D, 0, true, du, Fs, moe::EPI_DRELU2, u_s, nullptr, nullptr, 1,
+                                         S, Fs, D, stream));
+        if (dx != nullptr) {
+            // dx (+)= du Ws1^T: Ws1 [D, Fs] read Fs-contiguous per output column
+            MOE_HIP(moe::launch_grouped_rows(du, Fs, Ws1, Fs, 0, true, dx, D, moe::EPI_F32, nullptr, nullptr,
+                                             nullptr, 1, S, D, Fs, stream, accumulate_dx != 0));
+        }
+    }
+    const int nch = moe::wgrad_chunks(S, D > Fs ? D : Fs, D > Fs ? Fs : D);
+    const int64_t kchunk = S > 0 ? (S + nch - 1) / nch : 1;
+    // dWs2 [Fs, D] = h_s^T dy;  dWs1 [D, Fs] = x^T du  (the partial buffer is reused in stream order)
+    MOE_HIP(moe::launch_chunked_wgrad(h_s, Fs, dy, D, part, D, (int64_t)Fs * D, nch, kchunk, Fs, D, S, stream));
+    MOE_HIP(moe::launch_sum_planes(part, nch, Fs, D, 1, D, dWs2, stream));
+    MOE_HIP(moe::launch_chunked_wgrad(x, D, du, Fs, part, Fs, (int64_t)D * Fs, nch, kchunk, D, Fs, S, stream));
+    MOE_HIP(moe::launch_sum_planes(part, nch, D, Fs, 1, Fs, dWs1, stream));
     return MOE_OK;
 }
 

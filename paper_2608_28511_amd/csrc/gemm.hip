@@ -92,6 +92,7 @@ struct GemmArgs {
     int64_t R;                // rows of the activation buffers: segments are clamped to [0, R)
     int N, Kd, E;
     int m_tiles, n_tiles;
+    int accumulate;           // EPI_F32: C += product instead of C = product
 };
 
 // One BK-wide stage of the main loop for stage slot S of the ring: read the
@@ -351,6 +352,39 @@ __device__ __forceinline__ void drelu2_store(const f32x4 (&acc)[4][4], void* C, 
     }
 }
 
+// fp32 epilogue: each lane's four accumulators of a fragment are four
+// consecutive columns of one row, stored as one 16-byte buffer store (with
+// `accumulate`, added to what C holds there).  The descriptor spans only this
+// wave's rows, so rows past the tile and columns past N are dropped.
+__device__ __forceinline__ void f32_store(const f32x4 (&acc)[4][4], float* C, int64_t ldc, int N,
+                                          int64_t rbase, int64_t nrows, int64_t cbase, bool accumulate,
+                                          int lane) {
+    const int64_t rows = nrows < 64 ? nrows : 64;
+    const int32_t bytes = rows > 0 ? (int32_t)(rows * ldc * 4) : 0;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)(C + rbase * ldc), 0, bytes,
+                                                                        0x00020000);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t row = i * 16 + (lane & 15);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t col = cbase + j * 16 + 4 * (lane >> 4);
+            const uint32_t off = (row < rows && col < N) ? (uint32_t)((row * ldc + col) * 4) : kDropOffset;
+            f32x4 v = acc[i][j];
+            if (accumulate) {
+                const u32x4 o = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+                v[0] += __uint_as_float(o[0]);
+                v[1] += __uint_as_float(o[1]);
+                v[2] += __uint_as_float(o[2]);
+                v[3] += __uint_as_float(o[3]);
+            }
+            const u32x4 w = {__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                             __float_as_uint(v[3])};
+            __builtin_amdgcn_raw_buffer_store_b128(w, rs, off, 0, 0);
+        }
+    }
+}
+
 // C[r, n] = sum_k A[r, k] B_e[k, n] over the grid-wide list of output tiles
 // (expert segments from the tile table, or all M rows when it is null).
 // A is K-contiguous (ROW layout); B is N-contiguous (B_K false: weights stored
@@ -431,6 +465,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
             const int cbase = cur.n0 + wn * 64;
             if constexpr (EPI == EPI_DRELU2) {
                 drelu2_store(acc, p.C, p.aux_in, p.ldc, p.N, rbase, nrows, cbase, lane);
+            } else if constexpr (EPI == EPI_F32) {
+                f32_store(acc, (float*)p.C, p.ldc, p.N, rbase, nrows, cbase, p.accumulate != 0, lane);
             } else {
                 staged_store<EPI, 0>(acc, p.C, p.ldc, p.N, rbase, nrows, cbase, ep, lane);
                 if constexpr (EPI == EPI_RELU2)
@@ -558,9 +594,10 @@ hipError_t launch_tile_schedule(const int32_t* offsets, int E, int64_t R, void* 
 hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
                                int64_t b_stride, bool b_kmajor, void* C, int64_t ldc, int epi,
                                const moe_bf16* aux_in, moe_bf16* aux_out, const void* sched,
-                               int E, int64_t R, int N, int Kd, hipStream_t st) {
+                               int E, int64_t R, int N, int Kd, hipStream_t st, bool accumulate) {
     GemmArgs a{};
     a.A = A; a.B = B; a.C = C; a.aux_in = aux_in; a.aux_out = aux_out;
+    a.accumulate = accumulate ? 1 : 0;
     if (sched != nullptr) {
         a.tiles = (const int4*)((const char*)sched + sched_table_offset(E));
         a.mtile_total = (const int32_t*)sched + E;  // mtile_start[E]
@@ -575,9 +612,11 @@ hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B
     if (!b_kmajor) {
         if (epi == EPI_BF16) return launch_rows<false, EPI_BF16>(a, st);
         if (epi == EPI_RELU2) return launch_rows<false, EPI_RELU2>(a, st);
+        if (epi == EPI_F32) return launch_rows<false, EPI_F32>(a, st);
     } else {
         if (epi == EPI_BF16) return launch_rows<true, EPI_BF16>(a, st);
         if (epi == EPI_DRELU2) return launch_rows<true, EPI_DRELU2>(a, st);
+        if (epi == EPI_F32) return launch_rows<true, EPI_F32>(a, st);
     }
     return hipErrorInvalidValue;
 }

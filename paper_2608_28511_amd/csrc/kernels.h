@@ -18,19 +18,39 @@ hipError_t launch_router_logits(const moe_bf16* x, const float* Wr, const float*
 
 // Router backward (selection held fixed): dlogits (optional; else internal),
 // dWr [D,E], dbias [E] (optional), dx_r [S,D] fp32 (optional).
-size_t router_bwd_ws_bytes(int64_t S, int D, int E);
+// dense: the sigmoid router with the balance loss (ds dense over E).
+size_t router_bwd_ws_bytes(int64_t S, int D, int E, bool dense = false);
 hipError_t launch_router_bwd(const moe_bf16* x_r, const float* Wr, const int32_t* topk_idx, const float* topk_prob,
                              const float* dp, int64_t S, int D, int E, int K, float* dlogits, float* dWr,
                              float* dbias, float* dx_r, void* ws, hipStream_t st);
+// Sigmoid router backward: dg is the gradient of the routed weights; with
+// seq_counts (per sequence of seq_len tokens and expert) the balance-loss
+// gradient coef * count is added (coef = coeff * E / (K * T^2 * B)).
+hipError_t launch_router_bwd_sigmoid(const moe_bf16* x_r, const float* Wr, const float* logits,
+                                     const int32_t* topk_idx, const float* topk_gate, const float* dg,
+                                     const int32_t* seq_counts, int64_t seq_len, float coef, int64_t S, int D,
+                                     int E, int K, float* dlogits, float* dWr, float* dbias, float* dx_r,
+                                     void* ws, hipStream_t st);
+// Sequence balance loss forward: loss[0] (fp32) and seq_counts [B, E] (may be null).
+size_t seq_aux_ws_bytes(int64_t S, int E, int64_t seq_len);
+hipError_t launch_seq_aux_loss(const float* logits, const int32_t* topk_idx, int64_t S, int E, int K,
+                               int64_t seq_len, double coef, float* loss, int32_t* seq_counts, void* ws,
+                               hipStream_t st);
+// sel_bias[e] += rate * sign(mean(counts) - counts[e])
+hipError_t launch_expert_bias_update(const int32_t* counts, int E, float rate, float* sel_bias, hipStream_t st);
 // out[m,n] = sum_c sum_{s=P-1..0} part[c][m][s*ldp+n] (fixed order; rows of part hold P*ldp)
 hipError_t launch_sum_planes(const float* part, int nchunk, int M, int N, int P, int ldp, float* out,
                              hipStream_t st);
 int wgrad_chunks(int64_t rows, int M, int N);
 
 size_t route_ws_bytes(int64_t S, int E);
+// sigmoid: the production router (sigmoid scores, selection by score +
+// sel_bias (nullable), weights = picked sigmoids over their sum); otherwise
+// the softmax router.
 hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* topk_idx,
                         float* topk_prob, int32_t* counts, int32_t* offsets, int32_t* perm,
-                        int32_t* inv_perm, void* ws, hipStream_t st);
+                        int32_t* inv_perm, void* ws, hipStream_t st, bool sigmoid = false,
+                        const float* sel_bias = nullptr);
 
 hipError_t launch_dispatch(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S,
                            int D, int K, moe_bf16* x_disp, float* p_disp, hipStream_t st);
@@ -48,10 +68,11 @@ hipError_t launch_tile_schedule(const int32_t* offsets, int E, int64_t R, void* 
 // ROWS mode: C[r, :] = A[r, :] @ B_e per expert segment (sched from launch_tile_schedule
 // for the same offsets, E and R), or dense over R rows when sched == nullptr.
 // b_kmajor: B_e stored [N, Kd] (product with its transpose) instead of [Kd, N].
+// EPI_F32 writes fp32 C (ldc in floats); with accumulate, C += product.
 hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
                                int64_t b_stride, bool b_kmajor, void* C, int64_t ldc, int epi,
                                const moe_bf16* aux_in, moe_bf16* aux_out, const void* sched,
-                               int E, int64_t R, int N, int Kd, hipStream_t st);
+                               int E, int64_t R, int N, int Kd, hipStream_t st, bool accumulate = false);
 // KGRP mode: C_e[m, n] = sum over expert e's rows r of A[r, m] * B[r, n]  (fp32 out).
 // KGRP over a dense contraction cut into nchunk row ranges of kchunk rows:
 // C + c*c_stride = A[rows of chunk c]^T @ B[rows of chunk c]  (fp32 partials).

@@ -10,7 +10,8 @@
 //                  (DPP within rows of 16 lanes, then the 4 row maxima), and
 //                  a ballot for the lowest expert id holding that code (ties
 //                  go to the lower id, NaN ranks below -inf).  Then the
-//                  softmax renormalised over the K winners, and a per-block
+//                  softmax renormalised over the K winners (or, for sigmoid
+//                  scores, the winners' sigmoids over their sum), and a per-block
 //                  LDS bitmask per expert that gives each (token, slot) its
 //                  rank among the block's rows of that expert and the block's
 //                  per-expert count.
@@ -50,6 +51,10 @@ __device__ __forceinline__ float code_score(uint32_t c) {
     return __uint_as_float(u);
 }
 
+// Router score of the production variant (Section 5.2): the logistic
+// sigmoid in fp32 (-inf -> 0, +inf -> 1).
+__device__ __forceinline__ float sigmoid_f32(float l) { return 1.f / (1.f + expf(-l)); }
+
 // Maximum of v over the 64 lanes (all active), returned wave-uniform.
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     // pairs, quads, half rows, rows of 16 lanes: full permutations within a row
@@ -62,10 +67,14 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     return max(max(a, b), max(c, d));
 }
 
-template <int EPL>
+// SIG false: selection by the logits, weights = softmax over the K picked.
+// SIG true: selection by sigmoid(logit) + sel_bias (bias may be null), weights
+// = the picked sigmoids over their sum; the bias only steers selection.
+template <int EPL, bool SIG>
 __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
-    const float* __restrict__ logits, int64_t S, int E, int K, int32_t* __restrict__ topk_idx,
-    float* __restrict__ topk_prob, int32_t* __restrict__ blkcnt, int32_t* __restrict__ rank_out) {
+    const float* __restrict__ logits, const float* __restrict__ sel_bias, int64_t S, int E, int K,
+    int32_t* __restrict__ topk_idx, float* __restrict__ topk_prob, int32_t* __restrict__ blkcnt,
+    int32_t* __restrict__ rank_out) {
     __shared__ uint32_t mask[1024];
     __shared__ int16_t sel[kRouteTok][32];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -74,13 +83,24 @@ __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
 
     // this wave's tokens t_base + wave*8 + j: every score code loaded up front
     uint32_t code[kTokPerWave][EPL];
+    float bias[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+        const int e = lane + kWave * i;
+        bias[i] = (SIG && sel_bias != nullptr && e < E) ? sel_bias[e] : 0.f;
+    }
 #pragma unroll
     for (int j = 0; j < kTokPerWave; ++j) {
         const int64_t t = t_base + wave * kTokPerWave + j;
 #pragma unroll
         for (int i = 0; i < EPL; ++i) {
             const int e = lane + kWave * i;
-            code[j][i] = (t < S && e < E) ? score_code(logits[t * E + e]) : 0u;
+            if (t < S && e < E) {
+                const float l = logits[t * E + e];
+                code[j][i] = score_code(SIG ? sigmoid_f32(l) + bias[i] : l);
+            } else {
+                code[j][i] = 0u;
+            }
         }
     }
     __syncthreads();
@@ -117,8 +137,13 @@ __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
                 my_s = code_score(m);
             }
         }
-        const float s0 = __shfl(my_s, 0);
-        float z = (lane < K) ? expf(my_s - s0) : 0.f;
+        float z;
+        if constexpr (SIG) {
+            z = (lane < K) ? sigmoid_f32(logits[t * E + my_e]) : 0.f;
+        } else {
+            const float s0 = __shfl(my_s, 0);
+            z = (lane < K) ? expf(my_s - s0) : 0.f;
+        }
         float sum = z;
 #pragma unroll
         for (int msk = 32; msk > 0; msk >>= 1) sum += __shfl_xor(sum, msk);
@@ -232,22 +257,31 @@ size_t route_ws_bytes(int64_t S, int E) {
     return (size_t)(((nblk * E * 4) + 255) / 256 * 256);
 }
 
+template <bool SIG>
+static void launch_topk(const float* logits, const float* sel_bias, int64_t S, int E, int K, int32_t* topk_idx,
+                        float* topk_prob, int32_t* blkcnt, int32_t* rank, int nblk, hipStream_t st) {
+    const int epl = (E + kWave - 1) / kWave;
+#define MOE_ROUTE_CASE(N)                                                                          \
+    hipLaunchKernelGGL((route_topk_kernel<N, SIG>), dim3(nblk), dim3(kRouteThreads), 0, st, logits, \
+                       sel_bias, S, E, K, topk_idx, topk_prob, blkcnt, rank)
+    if (epl <= 1) MOE_ROUTE_CASE(1);
+    else if (epl <= 2) MOE_ROUTE_CASE(2);
+    else if (epl <= 4) MOE_ROUTE_CASE(4);
+    else if (epl <= 8) MOE_ROUTE_CASE(8);
+    else MOE_ROUTE_CASE(16);
+#undef MOE_ROUTE_CASE
+}
+
 hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* topk_idx,
                         float* topk_prob, int32_t* counts, int32_t* offsets, int32_t* perm,
-                        int32_t* inv_perm, void* ws, hipStream_t st) {
+                        int32_t* inv_perm, void* ws, hipStream_t st, bool sigmoid, const float* sel_bias) {
     const int nblk = (int)((S + kRouteTok - 1) / kRouteTok);
     int32_t* blkcnt = (int32_t*)ws;
     if (S > 0) {
-        const int epl = (E + kWave - 1) / kWave;
-#define MOE_ROUTE_CASE(N)                                                                      \
-    hipLaunchKernelGGL(route_topk_kernel<N>, dim3(nblk), dim3(kRouteThreads), 0, st, logits, S, \
-                       E, K, topk_idx, topk_prob, blkcnt, inv_perm)
-        if (epl <= 1) MOE_ROUTE_CASE(1);
-        else if (epl <= 2) MOE_ROUTE_CASE(2);
-        else if (epl <= 4) MOE_ROUTE_CASE(4);
-        else if (epl <= 8) MOE_ROUTE_CASE(8);
-        else MOE_ROUTE_CASE(16);
-#undef MOE_ROUTE_CASE
+        if (sigmoid)
+            launch_topk<true>(logits, sel_bias, S, E, K, topk_idx, topk_prob, blkcnt, inv_perm, nblk, st);
+        else
+            launch_topk<false>(logits, nullptr, S, E, K, topk_idx, topk_prob, blkcnt, inv_perm, nblk, st);
     }
     hipLaunchKernelGGL(route_colscan_kernel, dim3((unsigned)((E + kScanCols - 1) / kScanCols)),
                        dim3(kScanThreads), 0, st, blkcnt, nblk, E, counts);

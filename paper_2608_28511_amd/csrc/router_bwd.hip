@@ -20,12 +20,67 @@
 //   router_dx_kernel      one wavefront per token: the K nonzero terms of
 //                         ds Wr^T in fp32 from a transposed copy of Wr.
 // Every reduction has a fixed order, so results are deterministic.
+//
+// The production router (sigmoid scores s = sigmoid(logit), weights
+// g_k = s[T_k] / sum_j s[T_j], Section 5.2) differs only in the first step:
+//   router_ds_sigmoid_kernel   d logit = s (1 - s) (d s), with, on the picked
+//                              experts, d s[T_k] = (dg_k - sum_j g_j dg_j) / Z,
+//                              Z = sum_j s[T_j]; with the sequence balance
+//                              loss, every expert also gets
+//                              d s_e += (a_e - sum_e' a_e' s_e' / sum s) / sum s,
+//                              a_e = coef * count[seq, e].
+// The balance term makes ds dense, so dx_r = ds Wr^T becomes an MFMA product
+// over E: six bf16 plane products (hi, mid, lo of ds against hi, mid, lo of
+// Wr, dropping the three below 2^-24 relative) in one rows-GEMM launch.
 #include "common.h"
 #include "kernels.h"
 
 namespace moe {
 
 constexpr int kRbTok = 4;  // tokens (wavefronts) per 256-thread block
+
+__device__ __forceinline__ float sigmoid_score(float l) { return 1.f / (1.f + expf(-l)); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int msk = 32; msk > 0; msk >>= 1) v += __shfl_xor(v, msk);
+    return v;  // the xor butterfly leaves the same bits in every lane
+}
+
+// hi + mid + lo == w within 2^-24 |w| (three successive bf16 roundings).
+__device__ __forceinline__ void split3(float w, uint32_t& hi, uint32_t& mid, uint32_t& lo) {
+    hi = f32_to_bf16(w);
+    const float r1 = w - __uint_as_float(hi << 16);
+    mid = f32_to_bf16(r1);
+    lo = f32_to_bf16(r1 - __uint_as_float(mid << 16));
+}
+
+// Row t of ds (fp32, E wide), of ds3 (planes hi | mid | lo, each Ep wide) and,
+// when ds6 is not null, of ds6 (planes hi hi hi mid mid lo, matching the
+// weight planes Wh Wm Wl Wh Wm Wh of wr_split6_kernel).
+template <int EPL>
+__device__ __forceinline__ void store_ds_row(const float (&v)[EPL], int64_t t, int E, int Ep, int lane,
+                                             float* __restrict__ ds, uint16_t* __restrict__ ds3,
+                                             uint16_t* __restrict__ ds6) {
+    const int64_t E3 = 3 * (int64_t)Ep, E6 = 6 * (int64_t)Ep;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+        const int e = lane + 64 * i;
+        if (e >= Ep) break;
+        const float w = e < E ? v[i] : 0.f;
+        if (e < E) ds[t * E + e] = w;
+        uint32_t hi, mid, lo;
+        split3(w, hi, mid, lo);
+        ds3[t * E3 + e] = (uint16_t)hi;
+        ds3[t * E3 + Ep + e] = (uint16_t)mid;
+        ds3[t * E3 + 2 * Ep + e] = (uint16_t)lo;
+        if (ds6 != nullptr) {
+            uint16_t* r = ds6 + t * E6 + e;
+            r[0] = (uint16_t)hi; r[Ep] = (uint16_t)hi; r[2 * Ep] = (uint16_t)hi;
+            r[3 * Ep] = (uint16_t)mid; r[4 * Ep] = (uint16_t)mid; r[5 * Ep] = (uint16_t)lo;
+        }
+    }
+}
 
 template <int EPL>
 __global__ __launch_bounds__(256) void router_ds_kernel(const int32_t* __restrict__ topk_idx,
@@ -60,21 +115,82 @@ __global__ __launch_bounds__(256) void router_ds_kernel(const int32_t* __restric
     }
     // planes of Ep >= E columns (a multiple of 8, so every plane row starts
     // 16-byte aligned for the DMA); columns E .. Ep-1 are zero
-    const int64_t E3 = 3 * (int64_t)Ep;
+    store_ds_row<EPL>(v, t, E, Ep, lane, ds, ds3, nullptr);
+}
+
+// Sigmoid router: one wavefront per token.  seq_counts (per sequence of T
+// tokens and expert, from the balance-loss forward) null = no balance loss.
+template <int EPL>
+__global__ __launch_bounds__(256) void router_ds_sigmoid_kernel(
+    const float* __restrict__ logits, const int32_t* __restrict__ topk_idx, const float* __restrict__ topk_gate,
+    const float* __restrict__ dg, const int32_t* __restrict__ seq_counts, int64_t S, int E, int Ep, int K,
+    int64_t T, float coef, float* __restrict__ ds, uint16_t* __restrict__ ds3, uint16_t* __restrict__ ds6) {
+    const int lane = threadIdx.x & 63;
+    const int64_t t = (int64_t)blockIdx.x * kRbTok + (threadIdx.x >> 6);
+    if (t >= S) return;
+    int e_l = -1;
+    float g_l = 0.f, dg_l = 0.f, s_l = 0.f;
+    if (lane < K) {
+        e_l = topk_idx[t * K + lane];
+        if (e_l < 0 || e_l >= E) e_l = -1;  // malformed index: no contribution
+        g_l = topk_gate[t * K + lane];
+        dg_l = dg[t * K + lane];
+        s_l = e_l >= 0 ? sigmoid_score(logits[t * E + e_l]) : 0.f;
+    }
+    const float m = wave_sum(g_l * dg_l);
+    const float Z = wave_sum(s_l);
+    const float dsel_l = lane < K ? (dg_l - m) / Z : 0.f;
+    float sg[EPL], v[EPL];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
         const int e = lane + 64 * i;
-        if (e >= Ep) break;
-        const float w = e < E ? v[i] : 0.f;
-        if (e < E) ds[t * E + e] = w;
-        const uint32_t hi = f32_to_bf16(w);
-        const float r1 = w - __uint_as_float(hi << 16);
-        const uint32_t mid = f32_to_bf16(r1);
-        const uint32_t lo = f32_to_bf16(r1 - __uint_as_float(mid << 16));
-        ds3[t * E3 + e] = (uint16_t)hi;
-        ds3[t * E3 + Ep + e] = (uint16_t)mid;
-        ds3[t * E3 + 2 * Ep + e] = (uint16_t)lo;
+        sg[i] = e < E ? sigmoid_score(logits[t * E + e]) : 0.f;
+        v[i] = 0.f;
     }
+    for (int k = 0; k < K; ++k) {
+        const int ek = __shfl(e_l, k);
+        const float dk = __shfl(dsel_l, k);
+        if (ek < 0) continue;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i)
+            if (lane + 64 * i == ek) v[i] = dk;
+    }
+    if (seq_counts != nullptr) {
+        const int32_t* cnt = seq_counts + (t / T) * E;
+        float part = 0.f;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) part += sg[i];
+        const float tot = wave_sum(part);
+        float a[EPL], ap = 0.f;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) {
+            const int e = lane + 64 * i;
+            a[i] = e < E ? coef * (float)cnt[e] : 0.f;
+            ap += a[i] * (sg[i] / tot);
+        }
+        const float A = wave_sum(ap);
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) v[i] += (a[i] - A) / tot;
+    }
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) v[i] *= sg[i] * (1.f - sg[i]);
+    store_ds_row<EPL>(v, t, E, Ep, lane, ds, ds3, ds6);
+}
+
+// W6[d][p*Ep + e] = plane p of Wr[d, e], planes (hi, mid, lo, hi, mid, hi);
+// columns E .. Ep-1 zero.  K-contiguous rows of 6*Ep, the transposed weight
+// of the dx product.
+__global__ __launch_bounds__(256) void wr_split6_kernel(const float* __restrict__ Wr, int D, int E, int Ep,
+                                                        uint16_t* __restrict__ W6) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (int64_t)D * Ep) return;
+    const int64_t d = i / Ep;
+    const int e = (int)(i - d * Ep);
+    uint32_t hi, mid, lo;
+    split3(e < E ? Wr[d * E + e] : 0.f, hi, mid, lo);
+    uint16_t* r = W6 + d * 6 * (int64_t)Ep + e;
+    r[0] = (uint16_t)hi; r[Ep] = (uint16_t)mid; r[2 * Ep] = (uint16_t)lo;
+    r[3 * Ep] = (uint16_t)hi; r[4 * Ep] = (uint16_t)mid; r[5 * Ep] = (uint16_t)hi;
 }
 
 // dbias[e] = sum_t ds[t, e]: one wavefront per expert, lane l adds rows
@@ -172,12 +288,14 @@ int wgrad_chunks(int64_t rows, int M, int N) {
 }
 
 struct RouterBwdWs {
-    float* ds; uint16_t* ds3; float* WrT; float* part; size_t bytes; int nchunk;
+    float* ds; uint16_t* ds3; float* WrT; float* part; uint16_t* ds6; uint16_t* W6; size_t bytes; int nchunk;
 };
 
 static int pad8(int e) { return (e + 7) / 8 * 8; }
 
-static RouterBwdWs router_bwd_layout(char* base, int64_t S, int D, int E) {
+// dense: room for the six-plane dx product of the sigmoid router with the
+// balance loss (ds6 [S, 6 Ep], W6 [D, 6 Ep] bf16).
+static RouterBwdWs router_bwd_layout(char* base, int64_t S, int D, int E, bool dense) {
     RouterBwdWs w{};
     size_t off = 0;
     auto take = [&](size_t bytes) { void* p = base ? base + off : nullptr; off += (bytes + 255) / 256 * 256; return p; };
@@ -187,16 +305,62 @@ static RouterBwdWs router_bwd_layout(char* base, int64_t S, int D, int E) {
     w.ds3 = (uint16_t*)take((size_t)S * 3 * Ep * 2);
     w.WrT = (float*)take((size_t)E * D * 4);
     w.part = (float*)take((size_t)w.nchunk * D * 3 * Ep * 4);
+    if (dense) {
+        w.ds6 = (uint16_t*)take((size_t)S * 6 * Ep * 2);
+        w.W6 = (uint16_t*)take((size_t)D * 6 * Ep * 2);
+    }
     w.bytes = off;
     return w;
 }
 
-size_t router_bwd_ws_bytes(int64_t S, int D, int E) { return router_bwd_layout(nullptr, S, D, E).bytes; }
+size_t router_bwd_ws_bytes(int64_t S, int D, int E, bool dense) {
+    return router_bwd_layout(nullptr, S, D, E, dense).bytes;
+}
+
+// dWr, dbias and dx_r from ds (and its planes) already in the workspace.
+static hipError_t router_linear_bwd(const moe_bf16* x_r, const float* Wr, const int32_t* topk_idx,
+                                    const float* ds, const RouterBwdWs& w, int64_t S, int D, int E, int K,
+                                    float* dWr, float* dbias, float* dx_r, hipStream_t st);
+
+hipError_t launch_router_bwd_sigmoid(const moe_bf16* x_r, const float* Wr, const float* logits,
+                                     const int32_t* topk_idx, const float* topk_gate, const float* dg,
+                                     const int32_t* seq_counts, int64_t seq_len, float coef, int64_t S, int D,
+                                     int E, int K, float* dlogits, float* dWr, float* dbias, float* dx_r,
+                                     void* ws, hipStream_t st) {
+    const bool dense = seq_counts != nullptr;
+    RouterBwdWs w = router_bwd_layout((char*)ws, S, D, E, dense);
+    float* ds = dlogits != nullptr ? dlogits : w.ds;
+    const int Ep = pad8(E);
+    uint16_t* ds6 = dense && dx_r != nullptr ? w.ds6 : nullptr;
+    if (S > 0) {
+        const int epl = (Ep + 63) / 64;
+#define MOE_DS_CASE(N)                                                                                       \
+    hipLaunchKernelGGL(router_ds_sigmoid_kernel<N>, dim3(grid_for(S, kRbTok)), dim3(256), 0, st, logits,       \
+                       topk_idx, topk_gate, dg, seq_counts, S, E, Ep, K, seq_len, coef, ds, w.ds3, ds6)
+        if (epl <= 1) MOE_DS_CASE(1);
+        else if (epl <= 2) MOE_DS_CASE(2);
+        else if (epl <= 4) MOE_DS_CASE(4);
+        else if (epl <= 8) MOE_DS_CASE(8);
+        else MOE_DS_CASE(16);
+#undef MOE_DS_CASE
+        hipError_t err = hipGetLastError();
+        if (err != hipSuccess) return err;
+    }
+    if (!dense) return router_linear_bwd(x_r, Wr, topk_idx, ds, w, S, D, E, K, dWr, dbias, dx_r, st);
+    hipError_t err = router_linear_bwd(x_r, Wr, topk_idx, ds, w, S, D, E, K, dWr, dbias, nullptr, st);
+    if (err != hipSuccess || dx_r == nullptr || S == 0) return err;
+    // dense dx_r [S, D] = ds6 [S, 6 Ep] . W6 [D, 6 Ep]^T, fp32 out
+    hipLaunchKernelGGL(wr_split6_kernel, dim3(grid_for((int64_t)D * Ep, 256)), dim3(256), 0, st, Wr, D, E, Ep,
+                       w.W6);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    return launch_grouped_rows((const moe_bf16*)ds6, 6 * (int64_t)Ep, (const moe_bf16*)w.W6, 6 * (int64_t)Ep, 0,
+                               true, dx_r, D, EPI_F32, nullptr, nullptr, nullptr, 1, S, D, 6 * Ep, st);
+}
 
 hipError_t launch_router_bwd(const moe_bf16* x_r, const float* Wr, const int32_t* topk_idx, const float* topk_prob,
                              const float* dp, int64_t S, int D, int E, int K, float* dlogits, float* dWr,
                              float* dbias, float* dx_r, void* ws, hipStream_t st) {
-    RouterBwdWs w = router_bwd_layout((char*)ws, S, D, E);
+    RouterBwdWs w = router_bwd_layout((char*)ws, S, D, E, false);
     float* ds = dlogits != nullptr ? dlogits : w.ds;
     const int Ep = pad8(E);
     hipError_t err;
@@ -213,6 +377,14 @@ hipError_t launch_router_bwd(const moe_bf16* x_r, const float* Wr, const int32_t
 #undef MOE_DS_CASE
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
+    return router_linear_bwd(x_r, Wr, topk_idx, ds, w, S, D, E, K, dWr, dbias, dx_r, st);
+}
+
+static hipError_t router_linear_bwd(const moe_bf16* x_r, const float* Wr, const int32_t* topk_idx,
+                                    const float* ds, const RouterBwdWs& w, int64_t S, int D, int E, int K,
+                                    float* dWr, float* dbias, float* dx_r, hipStream_t st) {
+    const int Ep = pad8(E);
+    hipError_t err;
     // dWr [D, E] = x_r^T [hi | mid | lo](ds), fp32 partials per row chunk
     const int64_t kchunk = S > 0 ? (S + w.nchunk - 1) / w.nchunk : 1;
     if ((err = launch_chunked_wgrad(x_r, D, (const moe_bf16*)w.ds3, 3 * (int64_t)Ep, w.part, 3 * (int64_t)Ep,

@@ -152,15 +152,109 @@ def latent_proj_bwd(x_in, W, dout, want_dx: bool = True, want_dW: bool = True):
     return dx, dW
 
 
+def route_sigmoid(logits: torch.Tensor, K: int, sel_bias: Optional[torch.Tensor] = None) -> Dict[str, torch.Tensor]:
+    """Sigmoid routing with a selection-only bias; ``topk_prob`` holds the gates."""
+    S, E = logits.shape
+    dev = logits.device
+    R = S * K
+    o = dict(topk_idx=_empty((S, K), I32, dev), topk_prob=_empty((S, K), F32, dev),
+             counts=_empty((E,), I32, dev), offsets=_empty((E + 1,), I32, dev),
+             perm=_empty((R,), I32, dev), inv_perm=_empty((R,), I32, dev))
+    ws = _ws(L.moe_route_workspace_bytes(S, E, K), dev)
+    L.moe_route_sigmoid(logits, sel_bias, S, E, K, o["topk_idx"], o["topk_prob"], o["counts"], o["offsets"],
+                        o["perm"], o["inv_perm"], ws)
+    return o
+
+
+def seq_aux_loss(logits: torch.Tensor, topk_idx: torch.Tensor, seq_len: int, coeff: float):
+    """(loss [1] fp32, seq_counts [S/seq_len, E] int32)."""
+    S, E = logits.shape
+    K = topk_idx.shape[1]
+    dev = logits.device
+    loss = _empty((1,), F32, dev)
+    counts = _empty((S // seq_len, E), I32, dev)
+    ws = _ws(L.moe_seq_aux_loss_workspace_bytes(S, E, seq_len), dev)
+    L.moe_seq_aux_loss(logits, topk_idx, S, E, K, seq_len, coeff, loss, counts, ws)
+    return loss, counts
+
+
+def router_bwd_sigmoid(x_r, Wr, logits, topk_idx, topk_gate, dg, seq_counts=None, seq_len: int = 0,
+                       coeff: float = 0.0, want_dlogits: bool = True, want_dbias: bool = True,
+                       want_dx: bool = True) -> Dict[str, torch.Tensor]:
+    """Sigmoid-router gradients (selection fixed), plus the balance loss's when
+    seq_counts is given: dlogits, dWr, dbias, dx_r (fp32)."""
+    S, D = x_r.shape
+    E = Wr.shape[1]
+    K = topk_idx.shape[1]
+    dev = x_r.device
+    o = dict(dWr=_empty((D, E), F32, dev))
+    o["dlogits"] = _empty((S, E), F32, dev) if want_dlogits else None
+    o["dbias"] = _empty((E,), F32, dev) if want_dbias else None
+    o["dx_r"] = _empty((S, D), F32, dev) if want_dx else None
+    ws = _ws(L.moe_router_bwd_sigmoid_workspace_bytes(S, D, E), dev)
+    L.moe_router_bwd_sigmoid(x_r, Wr, logits, topk_idx, topk_gate, dg, seq_counts, seq_len, coeff, S, D, E, K,
+                             o["dlogits"], o["dWr"], o["dbias"], o["dx_r"], ws)
+    return o
+
+
+def expert_bias_update(counts: torch.Tensor, sel_bias: torch.Tensor, rate: float) -> torch.Tensor:
+    """In place on sel_bias; returns it."""
+    L.moe_expert_bias_update(counts, counts.shape[0], rate, sel_bias)
+    return sel_bias
+
+
+def combine_add(y_disp, p_disp, inv_perm, y_add, S: int, K: int):
+    D = y_disp.shape[1]
+    y = _empty((S, D), BF16, y_disp.device)
+    L.moe_combine_add(y_disp, p_disp, inv_perm, y_add, S, D, K, y)
+    return y
+
+
+def shared_expert_fwd(x, Ws1, Ws2, save_u: bool = True):
+    """(h_s bf16, u_s bf16 or None, y_s fp32)."""
+    S, D = x.shape
+    Fs = Ws1.shape[1]
+    dev = x.device
+    h = _empty((S, Fs), BF16, dev)
+    u = _empty((S, Fs), BF16, dev) if save_u else None
+    y = _empty((S, D), F32, dev)
+    L.moe_shared_expert_fwd(x, Ws1, Ws2, S, D, Fs, h, u, y)
+    return h, u, y
+
+
+def shared_expert_bwd(x, u_s, h_s, dy, Ws1, Ws2, dx: Optional[torch.Tensor] = None, accumulate_dx: bool = False,
+                      want_dx: bool = True):
+    """(dx fp32 or None, dWs1, dWs2); with accumulate_dx the product is added to ``dx``."""
+    S, D = x.shape
+    Fs = Ws1.shape[1]
+    dev = x.device
+    if dx is None and want_dx:
+        dx = _empty((S, D), F32, dev)
+        accumulate_dx = False
+    dW1 = _empty((D, Fs), F32, dev)
+    dW2 = _empty((Fs, D), F32, dev)
+    ws = _ws(L.moe_shared_expert_bwd_workspace_bytes(S, D, Fs), dev)
+    L.moe_shared_expert_bwd(x, u_s, h_s, dy, Ws1, Ws2, S, D, Fs, dx, accumulate_dx, dW1, dW2, ws)
+    return dx, dW1, dW2
+
+
 class LayerFwd:
     """Preallocated buffers for repeated moe_layer_fwd calls on one shape.
 
     With export=True every intermediate is a torch tensor owned here (for
     parity checks); otherwise intermediates live in the workspace.
+
+    With ``score="sigmoid"``, ``Fs`` and ``seq_len`` it runs the production
+    variant (sigmoid routing with a selection-only bias, shared expert,
+    sequence balance loss; exported as ``aux_loss``, ``seq_counts``, ``h_s``,
+    ``u_s`` and ``y_s``).
     """
 
-    def __init__(self, S, D, E, K, F, H=0, device="cuda", export=True, save_u=False):
+    def __init__(self, S, D, E, K, F, H=0, device="cuda", export=True, save_u=False, score="softmax",
+                 Fs=0, seq_len=0, aux_coeff=0.0):
         self.S, self.D, self.E, self.K, self.F, self.H = S, D, E, K, F, H
+        self.score_fn = {"softmax": L.SCORE_SOFTMAX, "sigmoid": L.SCORE_SIGMOID}[score]
+        self.Fs, self.seq_len, self.aux_coeff = Fs, seq_len, aux_coeff
         dev = torch.device(device)
         R = S * K
         self.out: Dict[str, Optional[torch.Tensor]] = {}
@@ -178,15 +272,28 @@ class LayerFwd:
                 y_disp=_empty((R, D), BF16, dev))
         if save_u:
             self.out["u_save"] = _empty((R, F), BF16, dev)
-        probe = L.layer_fwd_args(S, H, D, E, K, F, **{k: v for k, v in self.out.items()})
+        if seq_len:
+            self.out["aux_loss"] = _empty((1,), F32, dev)
+            if export:
+                self.out["seq_counts"] = _empty((S // seq_len, E), I32, dev)
+        if Fs:
+            if export:
+                self.out["h_s"] = _empty((S, Fs), BF16, dev)
+                self.out["y_s"] = _empty((S, D), F32, dev)
+            if save_u:
+                self.out["u_s"] = _empty((S, Fs), BF16, dev)
+        probe = L.layer_fwd_args(S, H, D, E, K, F, **self._modes(), **{k: v for k, v in self.out.items()})
         self.ws_bytes = L.moe_layer_fwd_workspace_bytes(probe)
         if self.ws_bytes == 0:
             raise ValueError("invalid layer shape")
         self.ws = _ws(self.ws_bytes, dev)
 
-    def __call__(self, x, Wr, W1, W2, bias=None, Wdown=None, Wup=None):
+    def _modes(self):
+        return dict(score_fn=self.score_fn, Fs=self.Fs, seq_len=self.seq_len, aux_coeff=self.aux_coeff)
+
+    def __call__(self, x, Wr, W1, W2, bias=None, Wdown=None, Wup=None, sel_bias=None, Ws1=None, Ws2=None):
         a = L.layer_fwd_args(self.S, self.H, self.D, self.E, self.K, self.F, ws=self.ws, x=x, Wr=Wr,
-                             router_bias=bias, Wdown=Wdown, W1=W1, W2=W2, Wup=Wup,
-                             **self.out)
+                             router_bias=bias, Wdown=Wdown, W1=W1, W2=W2, Wup=Wup, sel_bias=sel_bias,
+                             Ws1=Ws1, Ws2=Ws2, **self._modes(), **self.out)
         L.moe_layer_fwd(a)
         return self.out

@@ -9,7 +9,8 @@ dimension, E experts, top-K routing, F per-expert FFN width (f_expert in
 Table 2), H model hidden when a LatentMoE-style projection precedes dispatch
 (Section 1 "dispatch dimension" lever; Table 2 d_latent).
 
-Draw order per workload is fixed (x, Wr, bias, Wdown, W1, W2, Wup, dy) from
+Draw order per workload is fixed (x, Wr, bias, Wdown, W1, W2, Wup, dy, then
+for the production variant sel_bias, Ws1, Ws2) from
 one ``torch.Generator`` seeded with the workload's seed, on the requested
 device.  CPU and GPU generators produce different streams; a test always
 feeds the same bytes to both sides, so cross-device stream parity is never
@@ -34,6 +35,11 @@ class MoEShape:
       "zipf"      b_e = -1.1 * ln(r_e), r a seeded rank permutation of 1..E,
                   and the 4 lowest-ranked experts masked to -inf so that some
                   experts receive no rows at all
+
+    The production variant of Section 5.2 (score "sigmoid"): a selection-only
+    expert bias ~ N(0, sel_bias_std^2) (the state a load-driven update leaves
+    it in: small, of either sign), a shared expert of width Fs, and the
+    sequence balance loss over sequences of seq_len tokens.
     """
 
     name: str
@@ -46,6 +52,11 @@ class MoEShape:
     bias: str = "none"
     backward: bool = False
     seed: int = 0
+    score: str = "softmax"
+    sel_bias_std: float = 0.0
+    Fs: int = 0
+    seq_len: int = 0
+    aux_coeff: float = 0.0
 
     @property
     def R(self) -> int:
@@ -79,6 +90,22 @@ WORKLOADS: Dict[str, MoEShape] = {
                                               E=128, K=8, F=1024, bias="zipf", backward=True,
                                               seed=5),
 }
+
+# The production layer of Section 5.2 (sigmoid scores with a selection-only
+# bias, shared expert, sequence balance loss with coefficient 1e-4): a tiny
+# one for full oracle parity, and the 31.5B CE-MoE layer shape of Table 2 and
+# Section 4.3 (hidden 2688, 192 experts top-7, expert and shared width 3520)
+# over two sequences of 8192 tokens, with the backward pass.
+PRODUCTION: Dict[str, MoEShape] = {
+    "prod_tiny_s512_d256_e8_k2": MoEShape("prod_tiny_s512_d256_e8_k2", S=512, D=256, E=8, K=2, F=512,
+                                          backward=True, seed=6, score="sigmoid", sel_bias_std=0.05,
+                                          Fs=256, seq_len=128, aux_coeff=1e-4),
+    "prod_s16384_d2688_e192_k7": MoEShape("prod_s16384_d2688_e192_k7", S=16384, D=2688, E=192, K=7,
+                                          F=3520, backward=True, seed=7, score="sigmoid",
+                                          sel_bias_std=0.05, Fs=3520, seq_len=8192, aux_coeff=1e-4),
+}
+PROD_TINY = PRODUCTION["prod_tiny_s512_d256_e8_k2"]
+PROD = PRODUCTION["prod_s16384_d2688_e192_k7"]
 
 TINY = WORKLOADS["tiny_s512_d256_e8_k2"]
 BASE = WORKLOADS["base_s8192_d2048_e64_k6"]
@@ -135,6 +162,9 @@ def make_inputs(shape: MoEShape, device="cpu", seed: Optional[int] = None,
     W2     [E, F, D] bf16 ~ N(0, 1/F)
     Wup    [D, H]    bf16 ~ N(0, 1/D)     (latent workloads only)
     dy     [S, D_in] bf16 ~ N(0,1)        (backward workloads only)
+    sel_bias [E]     fp32 ~ N(0, sel_bias_std^2)   (sigmoid-score workloads)
+    Ws1    [D, Fs]   bf16 ~ N(0, 1/D)     (shared expert)
+    Ws2    [Fs, D]   bf16 ~ N(0, 1/Fs)
     """
     s = shape
     g = _gen(device, s.seed if seed is None else seed)
@@ -153,6 +183,11 @@ def make_inputs(shape: MoEShape, device="cpu", seed: Optional[int] = None,
         out["Wup"] = _normal((s.D, s.H), 1.0 / math.sqrt(s.D), g, device, torch.bfloat16)
     if s.backward:
         out["dy"] = _normal((s.S, s.D_in), 1.0, g, device, torch.bfloat16, chunk_dim0=4096)
+    if s.score == "sigmoid":
+        out["sel_bias"] = _normal((s.E,), s.sel_bias_std, g, device, torch.float32)
+    if s.Fs:
+        out["Ws1"] = _normal((s.D_in, s.Fs), 1.0 / math.sqrt(s.D_in), g, device, torch.bfloat16)
+        out["Ws2"] = _normal((s.Fs, s.D_in), 1.0 / math.sqrt(s.Fs), g, device, torch.bfloat16)
     return out
 
 

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_status_payload(lib):
-    assert L.moe_abi_version() == 1
+    assert L.moe_abi_version() == 2
     assert L.moe_status_string(0) == "ok"
     for code in range(-6, 0):
         assert L.moe_status_string(code) not in ("ok", "unknown status")
@@ -68,6 +68,15 @@ def test_workspace_queries(lib):
     # schedule: E+1 tile starts plus one 16-byte entry per possible 128-row tile
     assert lib.moe_grouped_schedule_bytes(64, 49152) >= 65 * 4 + (384 + 64) * 16
     assert lib.moe_grouped_schedule_bytes(0, 10) == 0
+    # production router: balance-loss partials per 64-token chunk; the sigmoid
+    # backward also holds the six-plane dx operands
+    assert lib.moe_seq_aux_loss_workspace_bytes(16384, 192, 8192) >= 2 * 128 * 192 * 8
+    assert lib.moe_seq_aux_loss_workspace_bytes(1000, 8, 300) == 0          # seq_len must divide S
+    assert lib.moe_seq_aux_loss_workspace_bytes(1000, 8, 0) == 0
+    assert (lib.moe_router_bwd_sigmoid_workspace_bytes(8192, 2048, 64)
+            >= lib.moe_router_bwd_workspace_bytes(8192, 2048, 64) + 8192 * 384 * 2 + 2048 * 384 * 2)
+    assert lib.moe_shared_expert_bwd_workspace_bytes(1024, 256, 512) >= 1024 * 512 * 2 + 256 * 512 * 4
+    assert lib.moe_shared_expert_bwd_workspace_bytes(1024, 256, 500) == 0   # Fs % 8
 
 
 def test_layer_struct_layout_matches(lib):
@@ -149,6 +158,54 @@ def test_validation_errors_return_before_launch(lib):
     a.Wdown = None
     a.ws_bytes = 16
     assert lib.moe_layer_fwd(C.byref(a), st) == -4       # workspace too small
+    a.ws_bytes = 1 << 30
+    a.sel_bias = 0x10000
+    assert lib.moe_layer_fwd(C.byref(a), st) == -2       # selection bias with softmax scores
+    a.score_fn = 1
+    a.seq_len = 3
+    assert lib.moe_layer_fwd(C.byref(a), st) == -2       # seq_len does not divide S
+    a.seq_len = 2
+    assert lib.moe_layer_fwd(C.byref(a), st) == -1       # balance loss without its output
+    a.seq_len = 0
+    a.Fs = 12
+    assert lib.moe_layer_fwd(C.byref(a), st) == -2       # shared width not a multiple of 8
+    a.Fs, a.H = 16, 16
+    assert lib.moe_layer_fwd_workspace_bytes(C.byref(a)) == 0  # shared expert with a latent layer
+    a.H = 0
+    assert lib.moe_layer_fwd(C.byref(a), st) == -1       # shared expert without its weights
+    a.score_fn = 7
+    assert lib.moe_layer_fwd(C.byref(a), st) == -2
+
+
+def test_production_validation_errors(lib):
+    st = None
+    assert lib.moe_route_sigmoid(FAKE, None, 4, 8, 9, *[FAKE] * 6, FAKE, 1 << 20, st) == -2
+    assert lib.moe_route_sigmoid(FAKE, ODD, 4, 8, 2, *[FAKE] * 6, FAKE, 1 << 20, st) == -3
+    assert lib.moe_route_sigmoid(FAKE, None, 4, 8, 2, *[FAKE] * 6, FAKE, 4, st) == -4
+    assert lib.moe_seq_aux_loss(FAKE, FAKE, 10, 8, 2, 3, 1e-4, FAKE, None, FAKE, 1 << 20, st) == -2
+    assert lib.moe_seq_aux_loss(FAKE, FAKE, 10, 8, 2, 5, 1e-4, None, None, FAKE, 1 << 20, st) == -1
+    assert lib.moe_seq_aux_loss(FAKE, FAKE, 10, 8, 2, 5, 1e-4, FAKE, None, FAKE, 8, st) == -4
+    args = [FAKE] * 7 + [5, 1e-4, 10, 16, 8, 2, None, FAKE, None, None, FAKE, 1 << 24, st]
+    bad = list(args)
+    bad[7] = 3                                              # seq_len does not divide S
+    assert lib.moe_router_bwd_sigmoid(*bad) == -2
+    bad = list(args)
+    bad[-2] = 8                                             # workspace too small
+    assert lib.moe_router_bwd_sigmoid(*bad) == -4
+    bad = list(args)
+    bad[12] = 9                                             # K > E
+    assert lib.moe_router_bwd_sigmoid(*bad) == -2
+    assert lib.moe_expert_bias_update(FAKE, 0, 1e-3, FAKE, st) == -2
+    assert lib.moe_expert_bias_update(FAKE, 8, 1e-3, None, st) == -1
+    assert lib.moe_combine_add(FAKE, None, FAKE, ODD, 4, 16, 2, FAKE, st) == -3
+    assert lib.moe_combine_add(FAKE, None, FAKE, None, 4, 16, 2, FAKE, st) == -1
+    assert lib.moe_shared_expert_fwd(FAKE, FAKE, FAKE, 4, 16, 12, FAKE, None, FAKE, st) == -2
+    assert lib.moe_shared_expert_fwd(FAKE, FAKE, FAKE, 4, 65536, 16384, FAKE, None, FAKE, st) == -6
+    assert lib.moe_shared_expert_fwd(FAKE, FAKE, FAKE, 4, 16, 16, FAKE, ODD, FAKE, st) == -3
+    assert lib.moe_shared_expert_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 16, 16, None, 0, FAKE, FAKE,
+                                     FAKE, 8, st) == -4
+    assert lib.moe_shared_expert_bwd(FAKE, None, FAKE, FAKE, FAKE, FAKE, 4, 16, 16, None, 0, FAKE, FAKE,
+                                     FAKE, 1 << 20, st) == -1
 
 
 def test_binding_refuses_host_tensors():
