@@ -145,10 +145,14 @@ def stage_bytes(s):
         "router_logits": S * D * 2 + D * E * 4 + 3 * D * E * 2 + S * E * 4,
         "route": S * E * 4 + R * 16 + (2 * E + 1) * 4,
         "dispatch": S * D * 2 + R * 8 + R * (2 * D + 4),
-        "combine": R * (2 * D + 8) + S * D * 2,
+        # with a shared expert its fp32 output is read as the addend
+        "combine": R * (2 * D + 8) + S * D * 2 + (S * D * 4 if s.Fs else 0),
         # dy read once per slot, y_disp and p read, dy_disp written, dp written
         "combine_bwd": S * D * 2 + R * (2 * D + 8) + R * 2 * D + R * 4,
-        "dispatch_bwd": R * (2 * D + 4) + S * D * 2,
+        # plus the router's fp32 input gradient read as the addend
+        "dispatch_bwd": R * (2 * D + 4) + S * D * 2 + S * D * 4,
+        # logits read once per 64-token chunk, topk_idx read, partials written
+        "seq_aux_loss": S * E * 4 + R * 4,
     }
 
 
@@ -187,10 +191,16 @@ def cpu_baseline(s, inp, tokens):
         def __getitem__(self, e):
             return self.W[int(e)].to(torch.float64).numpy()
 
+    f64 = lambda t: t.cpu().to(torch.float64).numpy()
     extra = {}
     if s.H:
-        extra = dict(Wdown=inp["Wdown"].cpu().to(torch.float64).numpy(),
-                     Wup=inp["Wup"].cpu().to(torch.float64).numpy())
+        extra = dict(Wdown=f64(inp["Wdown"]), Wup=f64(inp["Wup"]))
+    if s.score == "sigmoid":
+        extra.update(score="sigmoid", sel_bias=f64(inp["sel_bias"]))
+        if s.seq_len and T % s.seq_len == 0:   # the balance loss needs whole sequences
+            extra.update(seq_len=s.seq_len, aux_coeff=s.aux_coeff)
+    if s.Fs:
+        extra.update(Ws1=f64(inp["Ws1"]), Ws2=f64(inp["Ws2"]))
     t0 = time.perf_counter()
     O.layer_fwd(x, Wr, Experts(W1c), Experts(W2c), s.K, bias=bias, **extra)
     dt = time.perf_counter() - t0
@@ -216,19 +226,21 @@ def main():
     import torch
 
     from paper_2608_28511_amd import _lib, layer
-    from paper_2608_28511_amd.workloads import WORKLOADS, make_inputs
+    from paper_2608_28511_amd.workloads import PRODUCTION, WORKLOADS, make_inputs
 
     if not torch.cuda.is_available():
         print("bench.py needs a HIP device", file=sys.stderr)
         sys.exit(1)
     _lib.load(build_if_missing=True)
-    s = WORKLOADS[args.workload]
+    s = {**WORKLOADS, **PRODUCTION}[args.workload]
+    prod = s.score == "sigmoid"
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
 
     log(f"generating {args.sets} input sets for {s.name}")
     sets = [make_inputs(s, device=dev, seed=s.seed + 1000 * i) for i in range(args.sets)]
-    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True)
+    modes = dict(score=s.score, Fs=s.Fs, seq_len=s.seq_len, aux_coeff=s.aux_coeff)
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, **modes)
 
     # a plain device copy of known size, once, so hardware byte counters can be
     # calibrated against it in profiler runs of this same command
@@ -242,7 +254,7 @@ def main():
     def step(i):
         inp = sets[i % len(sets)]
         lf(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"], Wdown=inp.get("Wdown"),
-           Wup=inp.get("Wup"))
+           Wup=inp.get("Wup"), sel_bias=inp.get("sel_bias"), Ws1=inp.get("Ws1"), Ws2=inp.get("Ws2"))
 
     log(f"warmup {args.warmup}, timed {args.steps}")
     for i in range(args.warmup):
@@ -266,10 +278,25 @@ def main():
                            device=dev)
     r_bufs = {k: torch.empty_like(out[k]) for k in ("topk_idx", "topk_prob", "counts", "offsets",
                                                       "perm", "inv_perm")}
-    st["route"] = time_region(
-        lambda i: _lib.moe_route_topk(out["logits"], s.S, s.E, s.K, r_bufs["topk_idx"],
-                                      r_bufs["topk_prob"], r_bufs["counts"], r_bufs["offsets"],
-                                      r_bufs["perm"], r_bufs["inv_perm"], ws_route), reps, stream)
+    if prod:
+        st["route"] = time_region(
+            lambda i: _lib.moe_route_sigmoid(out["logits"], sets[i % len(sets)]["sel_bias"], s.S, s.E, s.K,
+                                             r_bufs["topk_idx"], r_bufs["topk_prob"], r_bufs["counts"],
+                                             r_bufs["offsets"], r_bufs["perm"], r_bufs["inv_perm"], ws_route),
+            reps, stream)
+    else:
+        st["route"] = time_region(
+            lambda i: _lib.moe_route_topk(out["logits"], s.S, s.E, s.K, r_bufs["topk_idx"],
+                                          r_bufs["topk_prob"], r_bufs["counts"], r_bufs["offsets"],
+                                          r_bufs["perm"], r_bufs["inv_perm"], ws_route), reps, stream)
+    if s.seq_len:
+        ws_aux = torch.empty(max(1, _lib.moe_seq_aux_loss_workspace_bytes(s.S, s.E, s.seq_len)),
+                             dtype=torch.uint8, device=dev)
+        loss2 = torch.empty(1, dtype=torch.float32, device=dev)
+        cnt2 = torch.empty((s.S // s.seq_len, s.E), dtype=torch.int32, device=dev)
+        st["seq_aux_loss"] = time_region(
+            lambda i: _lib.moe_seq_aux_loss(out["logits"], out["topk_idx"], s.S, s.E, s.K, s.seq_len, s.aux_coeff,
+                                            loss2, cnt2, ws_aux), reps, stream)
     xd2 = torch.empty_like(out["x_disp"])
     pd2 = torch.empty_like(out["p_disp"])
     x_r = [(st_["x"] if not s.H else out["x_lat"]) for st_ in sets]
@@ -286,9 +313,20 @@ def main():
         lambda i: _lib.moe_grouped_gemm(out["h"], sched, s.E, s.R, s.F, s.D,
                                         sets[i % len(sets)]["W2"], 0, yd2, None), reps, stream)
     y2 = torch.empty((s.S, s.D), dtype=torch.bfloat16, device=dev)
-    st["combine"] = time_region(
-        lambda i: _lib.moe_combine(out["y_disp"], out["p_disp"], out["inv_perm"], s.S, s.D, s.K, y2),
-        reps, stream)
+    if s.Fs:
+        hs2 = torch.empty_like(out["h_s"])
+        ys2 = torch.empty_like(out["y_s"])
+        st["shared_fwd"] = time_region(
+            lambda i: _lib.moe_shared_expert_fwd(sets[i % len(sets)]["x"], sets[i % len(sets)]["Ws1"],
+                                                 sets[i % len(sets)]["Ws2"], s.S, s.D, s.Fs, hs2, None, ys2),
+            reps, stream)
+        st["combine"] = time_region(
+            lambda i: _lib.moe_combine_add(out["y_disp"], out["p_disp"], out["inv_perm"], out["y_s"], s.S, s.D,
+                                           s.K, y2), reps, stream)
+    else:
+        st["combine"] = time_region(
+            lambda i: _lib.moe_combine(out["y_disp"], out["p_disp"], out["inv_perm"], s.S, s.D, s.K, y2),
+            reps, stream)
     if s.H:
         st["latent_down"] = time_region(
             lambda i: _lib.moe_latent_proj(sets[i % len(sets)]["x"], sets[i % len(sets)]["Wdown"],
@@ -296,8 +334,10 @@ def main():
 
     if s.backward:
         # backward stages (reported per stage; `value` stays the forward rate)
-        lb = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, save_u=True)
-        ob = lb(sets[0]["x"], sets[0]["Wr"], sets[0]["W1"], sets[0]["W2"], bias=sets[0]["bias"])
+        lb = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, save_u=True, **modes)
+        i0 = sets[0]
+        ob = lb(i0["x"], i0["Wr"], i0["W1"], i0["W2"], bias=i0["bias"], sel_bias=i0.get("sel_bias"),
+                Ws1=i0.get("Ws1"), Ws2=i0.get("Ws2"))
         dy = sets[0]["dy"]
         dy_disp = torch.empty_like(ob["x_disp"])
         dp = torch.empty((s.S, s.K), dtype=torch.float32, device=dev)
@@ -314,8 +354,35 @@ def main():
             lambda i: _lib.moe_grouped_ffn_bwd(ob["x_disp"], ob["u_save"], ob["h"], dy_disp, ob["offsets"],
                                                s.E, s.R, s.D, s.F, sets[0]["W1"], sets[0]["W2"], dx_disp,
                                                dW1, dW2, ws_bwd), max(2, reps // 4), stream)
+        dWr = torch.empty((s.D, s.E), dtype=torch.float32, device=dev)
+        dbias = torch.empty((s.E,), dtype=torch.float32, device=dev)
+        dx_r = torch.empty((s.S, s.D), dtype=torch.float32, device=dev)
+        if prod:
+            ws_rb = torch.empty(max(1, _lib.moe_router_bwd_sigmoid_workspace_bytes(s.S, s.D, s.E)), dtype=torch.uint8,
+                                device=dev)
+            st["router_bwd"] = time_region(
+                lambda i: _lib.moe_router_bwd_sigmoid(i0["x"], i0["Wr"], ob["logits"], ob["topk_idx"],
+                                                      ob["topk_prob"], dp, ob["seq_counts"], s.seq_len, s.aux_coeff,
+                                                      s.S, s.D, s.E, s.K, None, dWr, dbias, dx_r, ws_rb),
+                reps, stream)
+        else:
+            ws_rb = torch.empty(max(1, _lib.moe_router_bwd_workspace_bytes(s.S, s.D, s.E)), dtype=torch.uint8,
+                                device=dev)
+            st["router_bwd"] = time_region(
+                lambda i: _lib.moe_router_bwd(i0["x"], i0["Wr"], ob["topk_idx"], ob["topk_prob"], dp, s.S, s.D,
+                                              s.E, s.K, None, dWr, None if i0["bias"] is None else dbias, dx_r,
+                                              ws_rb), reps, stream)
+        if s.Fs:
+            dWs1 = torch.empty((s.D, s.Fs), dtype=torch.float32, device=dev)
+            dWs2 = torch.empty((s.Fs, s.D), dtype=torch.float32, device=dev)
+            ws_sb = torch.empty(max(1, _lib.moe_shared_expert_bwd_workspace_bytes(s.S, s.D, s.Fs)),
+                                dtype=torch.uint8, device=dev)
+            st["shared_bwd"] = time_region(
+                lambda i: _lib.moe_shared_expert_bwd(i0["x"], ob["u_s"], ob["h_s"], dy, i0["Ws1"], i0["Ws2"], s.S,
+                                                     s.D, s.Fs, dx_r, True, dWs1, dWs2, ws_sb),
+                max(2, reps // 4), stream)
         st["dispatch_bwd"] = time_region(
-            lambda i: _lib.moe_dispatch_bwd(dx_disp, ob["inv_perm"], None, s.S, s.D, s.K, dx), reps, stream)
+            lambda i: _lib.moe_dispatch_bwd(dx_disp, ob["inv_perm"], dx_r, s.S, s.D, s.K, dx), reps, stream)
         del lb, ob, dy_disp, dx_disp, dW1, dW2, ws_bwd
 
     bytes_ = stage_bytes(s)
@@ -323,7 +390,7 @@ def main():
     stages = {}
     for k, t in st.items():
         e = {"us": round(t * 1e6, 2)}
-        if k in ("route", "dispatch", "combine", "combine_bwd", "dispatch_bwd"):
+        if k in ("route", "dispatch", "combine", "combine_bwd", "dispatch_bwd", "seq_aux_loss"):
             gbs = bytes_[k] / t / 1e9
             e.update(bytes=bytes_[k], GBps=round(gbs, 1), hbm_frac=round(gbs / PEAK_HBM_GBS, 4))
         elif k == "router_logits":
@@ -332,9 +399,17 @@ def main():
             gbs = bytes_[k] / t / 1e9
             e.update(TFLOPs_fp32_equiv=round(tf, 2), bytes=bytes_[k], GBps=round(gbs, 1),
                      hbm_frac=round(gbs / PEAK_HBM_GBS, 4))
+        elif k == "router_bwd":
+            # dWr (x^T against three bf16 planes of dlogits) and dx_r, in fp32-equivalent flops
+            tf = 4.0 * s.S * s.D * s.E / t / 1e12
+            e.update(TFLOPs_fp32_equiv=round(tf, 2))
         else:
             if k == "grouped_ffn_bwd":
                 fl = 4.0 * gemm_flops      # dgrad and wgrad of both projections
+            elif k == "shared_fwd":
+                fl = 4.0 * s.S * s.D * s.Fs
+            elif k == "shared_bwd":
+                fl = 8.0 * s.S * s.D * s.Fs  # two dgrads, two wgrads
             else:
                 fl = gemm_flops if k.startswith("grouped") else 2.0 * s.S * s.H * s.D
             tf = fl / t / 1e12
@@ -359,7 +434,9 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": s.name, "S": s.S, "D": s.D, "E": s.E, "K": s.K, "F": s.F,
-                   "H": s.H, "rotating_input_sets": args.sets, "parallelism": "none (1 GPU)"},
+                   "H": s.H, "rotating_input_sets": args.sets, "parallelism": "none (1 GPU)",
+                   **({"score": s.score, "Fs": s.Fs, "seq_len": s.seq_len, "aux_coeff": s.aux_coeff}
+                      if prod else {})},
         "roofline": roofline, "stages": stages, "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)

@@ -15,9 +15,10 @@
 //                           four waves' sums are added in wave order, and the
 //                           chunk's routed counts are an LDS histogram
 //                           (integer, so the order of its atomics is moot);
-//   seq_aux_final_kernel    one workgroup: chunks summed in order (fp64),
-//                           n_be * P_be summed over sequences per expert,
-//                           then a fixed tree over experts.
+//   seq_aux_expert_kernel   one workgroup per expert: per sequence the chunk
+//                           partials in a fixed tree (fp64) and the routed
+//                           count, summed n_be * P_be over sequences;
+//   seq_aux_final_kernel    one workgroup: a fixed tree over experts.
 // Every sum has a fixed order, so the loss is deterministic.
 #include "common.h"
 #include "kernels.h"
@@ -77,27 +78,49 @@ __global__ __launch_bounds__(256) void seq_aux_partial_kernel(const float* __res
     }
 }
 
-__global__ __launch_bounds__(1024) void seq_aux_final_kernel(const float* __restrict__ partP,
+// Per expert (one workgroup each): for every sequence, the chunk partials in
+// a fixed tree (fp64), the routed count, and term[e] = sum_b n_be P_be.
+__global__ __launch_bounds__(256) void seq_aux_expert_kernel(const float* __restrict__ partP,
                                                              const int32_t* __restrict__ partC, int64_t B,
-                                                             int nck, int E, double coef, float* __restrict__ loss,
+                                                             int nck, int E, double* __restrict__ term,
                                                              int32_t* __restrict__ seq_counts) {
+    __shared__ double rp[256];
+    __shared__ long long rc[256];
+    const int tid = threadIdx.x, e = blockIdx.x;
+    double t_e = 0.0;
+    for (int64_t b = 0; b < B; ++b) {
+        double P = 0.0;
+        long long n = 0;
+        for (int c = tid; c < nck; c += 256) {
+            const int64_t ix = (b * nck + c) * E + e;
+            P += (double)partP[ix];
+            n += partC[ix];
+        }
+        rp[tid] = P;
+        rc[tid] = n;
+        __syncthreads();
+        for (int w = 128; w > 0; w >>= 1) {
+            if (tid < w) {
+                rp[tid] += rp[tid + w];
+                rc[tid] += rc[tid + w];
+            }
+            __syncthreads();
+        }
+        if (tid == 0) {
+            if (seq_counts != nullptr) seq_counts[b * E + e] = (int32_t)rc[0];
+            t_e += (double)rc[0] * rp[0];
+        }
+        __syncthreads();
+    }
+    if (tid == 0) term[e] = t_e;
+}
+
+// loss = coef * sum_e term[e], a fixed tree over the experts.
+__global__ __launch_bounds__(1024) void seq_aux_final_kernel(const double* __restrict__ term, int E, double coef,
+                                                             float* __restrict__ loss) {
     __shared__ double red[1024];
     const int tid = threadIdx.x;
-    double term = 0.0;
-    if (tid < E) {
-        for (int64_t b = 0; b < B; ++b) {
-            double P = 0.0;
-            int64_t n = 0;
-            for (int c = 0; c < nck; ++c) {
-                const int64_t ix = (b * nck + c) * E + tid;
-                P += (double)partP[ix];
-                n += partC[ix];
-            }
-            if (seq_counts != nullptr) seq_counts[b * E + tid] = (int32_t)n;
-            term += (double)n * P;
-        }
-    }
-    red[tid] = term;
+    red[tid] = tid < E ? term[tid] : 0.0;
     __syncthreads();
     for (int w = 512; w > 0; w >>= 1) {
         if (tid < w) red[tid] += red[tid + w];
@@ -107,7 +130,7 @@ __global__ __launch_bounds__(1024) void seq_aux_final_kernel(const float* __rest
 }
 
 struct AuxWs {
-    float* partP; int32_t* partC; size_t bytes; int nck;
+    float* partP; int32_t* partC; double* term; size_t bytes; int nck;
 };
 
 static AuxWs aux_layout(char* base, int64_t S, int E, int64_t T) {
@@ -118,6 +141,7 @@ static AuxWs aux_layout(char* base, int64_t S, int E, int64_t T) {
     w.nck = (int)((T + kAuxTok - 1) / kAuxTok);
     w.partP = (float*)take((size_t)(B * w.nck * E * 4));
     w.partC = (int32_t*)take((size_t)(B * w.nck * E * 4));
+    w.term = (double*)take((size_t)E * 8);
     w.bytes = off;
     return w;
 }
@@ -144,8 +168,9 @@ hipError_t launch_seq_aux_loss(const float* logits, const int32_t* topk_idx, int
         hipError_t err = hipGetLastError();
         if (err != hipSuccess) return err;
     }
-    hipLaunchKernelGGL(seq_aux_final_kernel, dim3(1), dim3(1024), 0, st, w.partP, w.partC, B, w.nck, E, coef, loss,
-                       seq_counts);
+    hipLaunchKernelGGL(seq_aux_expert_kernel, dim3((unsigned)E), dim3(256), 0, st, w.partP, w.partC, B, w.nck, E,
+                       w.term, seq_counts);
+    hipLaunchKernelGGL(seq_aux_final_kernel, dim3(1), dim3(1024), 0, st, w.term, E, coef, loss);
     return hipGetLastError();
 }
 

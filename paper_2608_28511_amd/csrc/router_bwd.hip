@@ -16,7 +16,7 @@
 //                         over row chunks of S into fp32 partials, then
 //                         sum_planes_kernel adds planes (lo, mid, hi) and
 //                         chunks in a fixed order;
-//   router_dbias_kernel   one wavefront per expert, fixed-order column sum;
+//   colsum kernels        dbias: fixed-order column sums in two passes;
 //   router_dx_kernel      one wavefront per token: the K nonzero terms of
 //                         ds Wr^T in fp32 from a transposed copy of Wr.
 // Every reduction has a fixed order, so results are deterministic.
@@ -193,18 +193,57 @@ __global__ __launch_bounds__(256) void wr_split6_kernel(const float* __restrict_
     r[3 * Ep] = (uint16_t)hi; r[4 * Ep] = (uint16_t)mid; r[5 * Ep] = (uint16_t)hi;
 }
 
-// dbias[e] = sum_t ds[t, e]: one wavefront per expert, lane l adds rows
-// l, l + 64, ... in order, then a fixed butterfly.
-__global__ __launch_bounds__(256) void router_dbias_kernel(const float* __restrict__ ds, int64_t S, int E,
-                                                           float* __restrict__ dbias) {
-    const int lane = threadIdx.x & 63;
-    const int e = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (e >= E) return;
+// dbias[e] = sum_t ds[t, e] in two fixed-order passes.  Pass 1: workgroup
+// (column block of 64, row chunk) with 4 row lanes per column, each adding
+// its rows in order (loads issued 8 at a time so they overlap), then the 4
+// lanes in order.  Pass 2: one thread per column adds the chunks in order.
+constexpr int kColChunkRows = 256;
+
+static int colsum_chunks(int64_t rows) {
+    int64_t n = (rows + kColChunkRows - 1) / kColChunkRows;
+    return (int)(n < 1 ? 1 : (n > 64 ? 64 : n));
+}
+
+__global__ __launch_bounds__(256) void colsum_partial_kernel(const float* __restrict__ src, int64_t rows, int cols,
+                                                             int64_t chunk_rows, float* __restrict__ part) {
+    __shared__ float red[4][64];
+    const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
+    const int col = blockIdx.x * 64 + c;
+    const int64_t r0 = (int64_t)blockIdx.y * chunk_rows;
+    const int64_t r1 = (r0 + chunk_rows) < rows ? (r0 + chunk_rows) : rows;
     float s = 0.f;
-    for (int64_t t = lane; t < S; t += 64) s += ds[t * E + e];
+    if (col < cols) {
+        int64_t r = r0 + q;
+        for (; r + 28 < r1; r += 32) {
+            float v[8];
 #pragma unroll
-    for (int msk = 32; msk > 0; msk >>= 1) s += __shfl_xor(s, msk);
-    if (lane == 0) dbias[e] = s;
+            for (int u = 0; u < 8; ++u) v[u] = src[(r + 4 * u) * cols + col];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; r < r1; r += 4) s += src[r * cols + col];
+    }
+    red[q][c] = s;
+    __syncthreads();
+    if (q == 0 && col < cols)
+        part[(int64_t)blockIdx.y * cols + col] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+}
+
+__global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restrict__ part, int nchunk, int cols,
+                                                           float* __restrict__ out) {
+    const int col = blockIdx.x * 256 + threadIdx.x;
+    if (col >= cols) return;
+    float s = 0.f;
+    int c = 0;
+    for (; c + 8 <= nchunk; c += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(c + u) * cols + col];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; c < nchunk; ++c) s += part[(int64_t)c * cols + col];
+    out[col] = s;
 }
 
 // WrT[e, d] = Wr[d, e] through a 32 x 33 LDS tile.
@@ -288,7 +327,8 @@ int wgrad_chunks(int64_t rows, int M, int N) {
 }
 
 struct RouterBwdWs {
-    float* ds; uint16_t* ds3; float* WrT; float* part; uint16_t* ds6; uint16_t* W6; size_t bytes; int nchunk;
+    float* ds; uint16_t* ds3; float* WrT; float* part; float* colpart; uint16_t* ds6; uint16_t* W6; size_t bytes;
+    int nchunk;
 };
 
 static int pad8(int e) { return (e + 7) / 8 * 8; }
@@ -305,6 +345,7 @@ static RouterBwdWs router_bwd_layout(char* base, int64_t S, int D, int E, bool d
     w.ds3 = (uint16_t*)take((size_t)S * 3 * Ep * 2);
     w.WrT = (float*)take((size_t)E * D * 4);
     w.part = (float*)take((size_t)w.nchunk * D * 3 * Ep * 4);
+    w.colpart = (float*)take((size_t)colsum_chunks(S) * E * 4);
     if (dense) {
         w.ds6 = (uint16_t*)take((size_t)S * 6 * Ep * 2);
         w.W6 = (uint16_t*)take((size_t)D * 6 * Ep * 2);
@@ -393,7 +434,12 @@ static hipError_t router_linear_bwd(const moe_bf16* x_r, const float* Wr, const 
     // (an empty row range contributes zero partials: the k-grouped kernel writes its zero accumulators)
     if ((err = launch_sum_planes(w.part, w.nchunk, D, E, 3, Ep, dWr, st)) != hipSuccess) return err;
     if (dbias != nullptr) {
-        hipLaunchKernelGGL(router_dbias_kernel, dim3((unsigned)((E + 3) / 4)), dim3(256), 0, st, ds, S, E, dbias);
+        const int nch = colsum_chunks(S);
+        const int64_t chunk_rows = (S + nch - 1) / nch;
+        hipLaunchKernelGGL(colsum_partial_kernel, dim3((unsigned)((E + 63) / 64), (unsigned)nch), dim3(256), 0, st,
+                           ds, S, E, chunk_rows > 0 ? chunk_rows : 1, w.colpart);
+        hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)((E + 255) / 256)), dim3(256), 0, st, w.colpart,
+                           nch, E, dbias);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     if (dx_r != nullptr && S > 0) {
