@@ -48,6 +48,13 @@ Pins (each in tests/test_oracle_*.py):
   expert_bias_update    closed form on a hand example
   shared_expert         one expert over all rows of expert_ffn; identity
                         weights give relu(x)^2; finite differences of the bwd
+  e4m3_encode/decode    the library fp8 (E4M3) conversion on every in-range
+                        value, codes and midpoints; hand codes of the OCP
+                        format; saturation; round trip of all 254 codes
+  mx_shared_exponent    closed forms (powers of two, zero, clamping)
+  mxfp8_(de)quantize    error bound per element, power-of-two equivariance,
+                        block independence, exact round trip of encoded values
+  dispatch_mxfp8        rows equal the token's encoding; Eq. 1 byte count
   ep_volume_per_step    the paper's printed reductions (Section 4.1, 4.3)
 """
 from __future__ import annotations
@@ -67,7 +74,9 @@ __all__ = [
     "dispatch_bwd", "router_bwd", "latent_bwd", "layer_bwd", "sigmoid_scores",
     "sigmoid_topk_select", "sigmoid_gates", "sigmoid_route", "seq_aux_loss",
     "seq_aux_loss_bwd", "sigmoid_gate_bwd", "router_linear_bwd", "expert_bias_update",
-    "shared_expert", "shared_expert_bwd", "dispatch_payload_bytes",
+    "shared_expert", "shared_expert_bwd", "MX_BLOCK", "E4M3_MAX", "e4m3_encode", "e4m3_decode",
+    "mx_shared_exponent", "mxfp8_quantize", "mxfp8_dequantize", "dispatch_mxfp8", "mx_payload_bytes",
+    "dispatch_payload_bytes",
     "combine_payload_bytes", "ep_volume_per_step",
 ]
 
@@ -318,7 +327,7 @@ def latent_up(y_lat, Wup) -> np.ndarray:
 def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
               logits=None, round_payload: bool = True, round_latent: bool = True,
               score: str = "softmax", sel_bias=None, Ws1=None, Ws2=None,
-              seq_len: Optional[int] = None, aux_coeff: float = 0.0) -> dict:
+              seq_len: Optional[int] = None, aux_coeff: float = 0.0, payload: str = "bf16") -> dict:
     """One routed MoE layer forward, in the paper's order (Section 4.1
     footnote: hidden dispatch, probability dispatch, hidden combine):
     [latent down] -> router logits -> top-K + probabilities -> permutation ->
@@ -333,7 +342,9 @@ def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
     sigmoid_route (``sel_bias`` steering selection only); ``Ws1``/``Ws2`` add
     the shared expert on the layer input to the layer output; ``aux_coeff``
     (sigmoid scores, batch of whole ``seq_len``-token sequences) adds the
-    balance loss as ``aux_loss``.  Returns every intermediate.
+    balance loss as ``aux_loss``.  ``payload="mxfp8"`` sends the dispatched
+    hidden states as MX-FP8 (dispatch_mxfp8) and the experts read their
+    decoded values.  Returns every intermediate.
     """
     x = np.asarray(x, np.float64)
     S = x.shape[0]
@@ -353,7 +364,14 @@ def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
     else:
         raise ValueError("score is 'softmax' (no selection bias) or 'sigmoid'")
     counts, offsets, perm, inv_perm = expert_permutation(idx, E)
-    x_disp, p_disp = dispatch(x_r, prob, inv_perm, K)
+    if payload == "mxfp8":
+        xq, xs, p_disp = dispatch_mxfp8(x_r, prob, inv_perm, K)
+        x_disp = mxfp8_dequantize(xq, xs)
+        out.update(x_q=xq, x_scale=xs)
+    elif payload == "bf16":
+        x_disp, p_disp = dispatch(x_r, prob, inv_perm, K)
+    else:
+        raise ValueError("payload is 'bf16' or 'mxfp8'")
     u, h, y_disp = expert_ffn(x_disp, offsets, W1, W2, round_payload)
     y = combine(y_disp, p_disp, inv_perm, S, K)
     out.update(topk_idx=idx, topk_prob=prob, counts=counts, offsets=offsets, perm=perm,
@@ -710,6 +728,125 @@ def shared_expert_bwd(x, u, h, dy, Ws1, Ws2):
     Ws2 = np.asarray(Ws2, np.float64)
     du = (dy @ Ws2.T) * (2.0 * np.maximum(np.asarray(u, np.float64), 0.0))
     return du @ Ws1.T, x.T @ du, np.asarray(h, np.float64).T @ dy
+
+
+# ---------------------------------------------------------------------------
+# Lower-precision dispatch payload (Section 1, the precision lever on b_x)
+# ---------------------------------------------------------------------------
+#
+# The payload format is OCP Microscaling (MX v1.0) with FP8 E4M3 elements:
+# every block of 32 consecutive elements of a row shares one power-of-two
+# scale X = 2^s stored as an E8M0 byte (s + 127), and each element is the
+# E4M3 value nearest to x / X.  E4M3 (OCP 8-bit floating point): 1 sign,
+# 4 exponent (bias 7) and 3 mantissa bits, no infinities, S.1111.111 = NaN,
+# largest finite 448, smallest normal 2^-6, subnormals m * 2^-9.
+# The shared exponent is floor(log2(max |x|)) - 8 (8 = the exponent of
+# E4M3's largest power of two), so x / X of the block maximum lies in
+# [256, 512); element values beyond 448 saturate to +-448.  Readings where
+# the specification leaves a choice: an all-zero block (or one whose maximum
+# is below 2^-119) takes the smallest scale 2^-127; NaN and infinite inputs
+# are not defined here.
+
+MX_BLOCK = 32
+E4M3_MAX = 448.0
+E4M3_EMAX = 8        # exponent of the largest power of two below E4M3_MAX
+E8M0_BIAS = 127
+
+
+def e4m3_encode(v) -> np.ndarray:
+    """Round each value to the nearest E4M3 number (ties to even mantissa),
+    saturating finite values beyond 448 to +-448; uint8 codes.  -0.0 keeps
+    its sign bit."""
+    v = np.asarray(v, np.float64)
+    if not np.all(np.isfinite(v)):
+        raise ValueError("E4M3 encoding is defined here for finite values only")
+    sign = np.signbit(v).astype(np.uint8) << 7
+    a = np.minimum(np.abs(v), E4M3_MAX)
+    code = np.zeros(a.shape, np.int64)
+    sub = a < 2.0 ** -6
+    # subnormals (and zero): multiples of 2^-9; 8 * 2^-9 is the smallest normal
+    code[sub] = np.rint(a[sub] / 2.0 ** -9).astype(np.int64)
+    n = ~sub
+    if np.any(n):
+        _, ex = np.frexp(a[n])               # a = f * 2^ex, f in [0.5, 1)
+        e = ex - 1                           # floor(log2 a), in [-6, 8]
+        ulp = np.ldexp(1.0, e - 3)
+        r = np.rint(a[n] / ulp) * ulp        # may carry into the next binade
+        _, ex2 = np.frexp(r)
+        e2 = ex2 - 1
+        mant = np.rint((r / np.ldexp(1.0, e2) - 1.0) * 8).astype(np.int64)
+        code[n] = ((e2 + 7) << 3) | mant
+    return (sign | code.astype(np.uint8)).astype(np.uint8)
+
+
+def e4m3_decode(codes) -> np.ndarray:
+    """Value of each E4M3 code (float64); NaN codes raise."""
+    c = np.asarray(codes, np.uint8).astype(np.int64)
+    mag = c & 0x7F
+    if np.any(mag == 0x7F):
+        raise ValueError("NaN code")
+    e = mag >> 3
+    m = mag & 7
+    val = np.where(e == 0, m * 2.0 ** -9, (1.0 + m / 8.0) * np.ldexp(1.0, e - 7))
+    return np.where(c & 0x80, -val, val)
+
+
+def mx_shared_exponent(amax) -> np.ndarray:
+    """Block exponent s = floor(log2(amax)) - 8, clamped to E8M0's [-127, 127]
+    (amax 0 -> -127)."""
+    amax = np.asarray(amax, np.float64)
+    _, ex = np.frexp(amax)
+    s = np.where(amax > 0, ex - 1 - E4M3_EMAX, -E8M0_BIAS)
+    return np.clip(s, -E8M0_BIAS, E8M0_BIAS).astype(np.int64)
+
+
+def mxfp8_quantize(x):
+    """MX-FP8 (E4M3) encoding of the rows of x [R, D], D a multiple of 32:
+    (codes uint8 [R, D], scales uint8 [R, D/32] holding s + 127)."""
+    x = np.asarray(x, np.float64)
+    R, D = x.shape
+    if D % MX_BLOCK:
+        raise ValueError("row length must be a multiple of the MX block (32)")
+    blocks = x.reshape(R, D // MX_BLOCK, MX_BLOCK)
+    s = mx_shared_exponent(np.max(np.abs(blocks), axis=2))
+    codes = e4m3_encode(blocks / np.ldexp(1.0, s)[:, :, None])
+    return codes.reshape(R, D), (s + E8M0_BIAS).astype(np.uint8)
+
+
+def mxfp8_dequantize(codes, scales) -> np.ndarray:
+    """Values of an MX-FP8 payload, float64 [R, D]."""
+    codes = np.asarray(codes, np.uint8)
+    R, D = codes.shape
+    s = np.asarray(scales, np.uint8).astype(np.int64) - E8M0_BIAS
+    v = e4m3_decode(codes).reshape(R, D // MX_BLOCK, MX_BLOCK)
+    return (v * np.ldexp(1.0, s)[:, :, None]).reshape(R, D)
+
+
+def dispatch_mxfp8(x, prob, inv_perm, K: int):
+    """Dispatch with an MX-FP8 hidden payload: each token row is encoded once
+    and its codes and scales are copied to the token's K routed rows (the
+    sender encodes, the payload travels); the probability stays fp32 (b_p).
+    Returns (codes [S*K, D], scales [S*K, D/32], p_disp [S*K] or None)."""
+    codes, scales = mxfp8_quantize(x)
+    S = codes.shape[0]
+    inv = np.asarray(inv_perm, np.int64).reshape(S, K)
+    R = S * K
+    cd = np.zeros((R, codes.shape[1]), np.uint8)
+    sc = np.zeros((R, scales.shape[1]), np.uint8)
+    pd = None if prob is None else np.zeros(R, np.float32)
+    for k in range(K):
+        cd[inv[:, k]] = codes
+        sc[inv[:, k]] = scales
+        if prob is not None:
+            pd[inv[:, k]] = np.asarray(prob, np.float32)[:, k]
+    return cd, sc, pd
+
+
+def mx_payload_bytes(S: int, K: int, D: int, b_p: int = B_P) -> int:
+    """Forward dispatch payload with MX-FP8 hidden elements: per routed row D
+    one-byte elements, D/32 one-byte scales and the routed probability
+    (Eq. 1 with b_x = 1 + 1/32)."""
+    return S * K * (D + D // MX_BLOCK + b_p)
 
 
 # ---------------------------------------------------------------------------
