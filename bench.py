@@ -43,6 +43,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="base_s8192_d2048_e64_k6")
     p.add_argument("--sets", type=int, default=3, help="rotating input sets")
+    p.add_argument("--payload", default="bf16", choices=("bf16", "mxfp8"),
+                   help="dispatch payload of the timed layer (MX-FP8: b_x = 1 + 1/32)")
     p.add_argument("--stage-reps", type=int, default=20)
     p.add_argument("--cpu-tokens", type=int, default=0,
                    help="tokens of the batch the CPU oracle runs (0: the whole batch)")
@@ -153,6 +155,9 @@ def stage_bytes(s):
         "dispatch_bwd": R * (2 * D + 4) + S * D * 2 + S * D * 4,
         # logits read once per 64-token chunk, topk_idx read, partials written
         "seq_aux_loss": S * E * 4 + R * 4,
+        # MX-FP8 payload: x read once, codes + scales + p written per routed row
+        "dispatch_mxfp8": S * D * 2 + R * 8 + R * (D + D // 32 + 4),
+        "mxfp8_dequant": R * (D + D // 32) + R * D * 2,
     }
 
 
@@ -171,7 +176,7 @@ def time_region(fn, reps, stream):
     return start.elapsed_time(end) / reps * 1e-3   # seconds
 
 
-def cpu_baseline(s, inp, tokens):
+def cpu_baseline(s, inp, tokens, payload="bf16", min_seconds=10.0, max_runs=8):
     import numpy as np
     import torch
     from threadpoolctl import threadpool_info
@@ -201,16 +206,22 @@ def cpu_baseline(s, inp, tokens):
             extra.update(seq_len=s.seq_len, aux_coeff=s.aux_coeff)
     if s.Fs:
         extra.update(Ws1=f64(inp["Ws1"]), Ws2=f64(inp["Ws2"]))
-    t0 = time.perf_counter()
-    O.layer_fwd(x, Wr, Experts(W1c), Experts(W2c), s.K, bias=bias, **extra)
-    dt = time.perf_counter() - t0
+    if payload != "bf16":
+        extra["payload"] = payload
+    # whole passes over the sample until about min_seconds of CPU work
+    runs, dt = 0, 0.0
+    while runs < max_runs and (runs == 0 or dt < min_seconds):
+        t0 = time.perf_counter()
+        O.layer_fwd(x, Wr, Experts(W1c), Experts(W2c), s.K, bias=bias, **extra)
+        dt += time.perf_counter() - t0
+        runs += 1
     blas = [d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"]
     return {
-        "value": T * s.K / dt, "unit": "slots/s", "cores": int(max(blas) if blas else 1),
+        "value": runs * T * s.K / dt, "unit": "slots/s", "cores": int(max(blas) if blas else 1),
         "kind": "oracle",
-        "sample": f"first {T} of {s.S} tokens of the same workload through the float64 oracle "
-                  f"layer forward ({T * s.K} routed rows, {dt:.1f} s; BLAS matmuls threaded, "
-                  f"routing and permutation single-threaded Python)",
+        "sample": f"{runs} passes over the first {T} of {s.S} tokens of the same workload through the "
+                  f"float64 oracle layer forward ({T * s.K} routed rows per pass, {dt:.1f} s in all; BLAS "
+                  f"matmuls threaded, routing and permutation single-threaded Python)",
     }
 
 
@@ -240,7 +251,7 @@ def main():
     log(f"generating {args.sets} input sets for {s.name}")
     sets = [make_inputs(s, device=dev, seed=s.seed + 1000 * i) for i in range(args.sets)]
     modes = dict(score=s.score, Fs=s.Fs, seq_len=s.seq_len, aux_coeff=s.aux_coeff)
-    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, **modes)
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, payload=args.payload, **modes)
 
     # a plain device copy of known size, once, so hardware byte counters can be
     # calibrated against it in profiler runs of this same command
@@ -303,6 +314,13 @@ def main():
     st["dispatch"] = time_region(
         lambda i: _lib.moe_dispatch(x_r[i % len(x_r)], out["topk_prob"], out["inv_perm"], s.S, s.D,
                                     s.K, xd2, pd2), reps, stream)
+    if s.D % 32 == 0:
+        xq2 = torch.empty((s.R, s.D), dtype=torch.uint8, device=dev)
+        xs2 = torch.empty((s.R, s.D // 32), dtype=torch.uint8, device=dev)
+        st["dispatch_mxfp8"] = time_region(
+            lambda i: _lib.moe_dispatch_mxfp8(x_r[i % len(x_r)], out["topk_prob"], out["inv_perm"], s.S, s.D, s.K,
+                                              xq2, xs2, pd2), reps, stream)
+        st["mxfp8_dequant"] = time_region(lambda i: _lib.moe_mxfp8_dequant(xq2, xs2, s.R, s.D, xd2), reps, stream)
     sched = layer.grouped_schedule(out["offsets"], s.E, s.R)
     h2 = torch.empty_like(out["h"])
     yd2 = torch.empty_like(out["y_disp"])
@@ -390,7 +408,8 @@ def main():
     stages = {}
     for k, t in st.items():
         e = {"us": round(t * 1e6, 2)}
-        if k in ("route", "dispatch", "combine", "combine_bwd", "dispatch_bwd", "seq_aux_loss"):
+        if k in ("route", "dispatch", "combine", "combine_bwd", "dispatch_bwd", "seq_aux_loss", "dispatch_mxfp8",
+                 "mxfp8_dequant"):
             gbs = bytes_[k] / t / 1e9
             e.update(bytes=bytes_[k], GBps=round(gbs, 1), hbm_frac=round(gbs / PEAK_HBM_GBS, 4))
         elif k == "router_logits":
@@ -426,7 +445,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log(f"cpu baseline: oracle on {args.cpu_tokens} tokens")
-        cpu = cpu_baseline(s, sets[0], args.cpu_tokens)
+        cpu = cpu_baseline(s, sets[0], args.cpu_tokens, args.payload)
 
     rec = {
         "metric": METRIC, "value": round(value, 1), "unit": "slots/s", "n_gpus": 1,
@@ -435,9 +454,15 @@ def main():
         "data": "synthetic",
         "config": {"workload": s.name, "S": s.S, "D": s.D, "E": s.E, "K": s.K, "F": s.F,
                    "H": s.H, "rotating_input_sets": args.sets, "parallelism": "none (1 GPU)",
+                   **({"payload": "mxfp8"} if args.payload == "mxfp8" else {}),
                    **({"score": s.score, "Fs": s.Fs, "seq_len": s.seq_len, "aux_coeff": s.aux_coeff}
                       if prod else {})},
         "roofline": roofline, "stages": stages, "cpu_baseline": cpu,
+        # Eq. 1: forward dispatch payload with bf16 and with MX-FP8 hidden elements
+        "payload": {"timed": args.payload, "eq1_dispatch_bytes_bf16": _lib.moe_payload_bytes(s.S, s.K, s.D),
+                    "eq1_dispatch_bytes_mxfp8": _lib.moe_mx_payload_bytes(s.S, s.K, s.D),
+                    "mxfp8_over_bf16": round(_lib.moe_mx_payload_bytes(s.S, s.K, s.D)
+                                             / _lib.moe_payload_bytes(s.S, s.K, s.D), 4)},
     }
     print(json.dumps(rec), flush=True)
 

@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 2
+#define MOE_ABI_VERSION 3
 
 typedef uint16_t moe_bf16; /* bit pattern of a bfloat16 value (b_x = 2 bytes) */
 
@@ -251,7 +251,13 @@ typedef struct {
     moe_bf16* h_s;             /* [S, Fs] shared-expert activation, or NULL */
     moe_bf16* u_s;             /* [S, Fs] its pre-activation (saved only if given) */
     float* y_s;                /* [S, D] fp32 shared-expert output, or NULL */
+    /* Dispatch payload precision (Section 1's precision lever on b_x). */
+    int32_t payload;           /* MOE_PAYLOAD_BF16 or MOE_PAYLOAD_MXFP8 (D a multiple of 32) */
+    uint8_t* x_q;              /* [S*K, D] MX-FP8 codes, exported or NULL */
+    uint8_t* x_scale;          /* [S*K, D/32] their E8M0 block scales, exported or NULL */
 } moe_layer_fwd_args;
+
+enum { MOE_PAYLOAD_BF16 = 0, MOE_PAYLOAD_MXFP8 = 1 };
 
 enum { MOE_SCORE_SOFTMAX = 0, MOE_SCORE_SIGMOID = 1 };
 
@@ -261,6 +267,9 @@ size_t moe_layer_fwd_workspace_bytes(const moe_layer_fwd_args* a);
 
 /* [x_lat = bf16(x @ Wdown)] -> logits -> route -> dispatch -> experts ->
  * combine -> [y = bf16(y_lat @ Wup)], all enqueued on `stream`.
+ * With payload = MOE_PAYLOAD_MXFP8 the dispatch sends MX-FP8 rows
+ * (moe_dispatch_mxfp8) and the experts read their decoded bf16 values
+ * (moe_mxfp8_dequant into x_disp).
  * With score_fn = MOE_SCORE_SIGMOID the route is moe_route_sigmoid (with
  * sel_bias); seq_len > 0 adds moe_seq_aux_loss; Fs > 0 runs the shared
  * expert and adds its fp32 output in the combine, before the one bf16
@@ -352,6 +361,33 @@ size_t moe_latent_proj_bwd_workspace_bytes(int64_t M, int32_t Kd, int32_t N);
 int moe_latent_proj_bwd(const moe_bf16* x_in, const moe_bf16* W, const moe_bf16* dout,
                         int64_t M, int32_t Kd, int32_t N, moe_bf16* dx_in, float* dW,
                         void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------- */
+/* Lower-precision dispatch payload (Section 1: the precision lever on b_x */
+/* in Eq. 1).  Format: OCP microscaling (MX) with FP8 E4M3 elements -- per  */
+/* block of 32 consecutive elements of a row one E8M0 scale byte s + 127,  */
+/* s = floor(log2 max|x|) - 8 clamped to [-127, 127] (all-zero block:      */
+/* -127), and per element the E4M3 code nearest to x * 2^-s (ties to even, */
+/* saturated to +-448).  b_x becomes 1 + 1/32 bytes.                       */
+/* ---------------------------------------------------------------------- */
+/* Forward dispatch payload bytes with MX-FP8 hidden elements:
+ * S*K*(D + D/32 + 4) (Eq. 1 with b_x = 1 + 1/32, b_p = 4). */
+uint64_t moe_mx_payload_bytes(int64_t S, int32_t K, int32_t D);
+
+/* moe_dispatch with the MX-FP8 payload: each token row of x is encoded once
+ * (bit-exact to the format above) and its codes and scales are written to
+ * the token's K routed rows; p_disp as in moe_dispatch.
+ *   x [S, D] bf16 (finite);  x_q [S*K, D] uint8 (8-byte aligned);
+ *   x_scale [S*K, D/32] uint8.
+ * Errors: as moe_dispatch, plus D % 32 != 0 (MOE_ERR_SHAPE). */
+int moe_dispatch_mxfp8(const moe_bf16* x, const float* topk_prob, const int32_t* inv_perm, int64_t S,
+                       int32_t D, int32_t K, uint8_t* x_q, uint8_t* x_scale, float* p_disp,
+                       hipStream_t stream);
+
+/* Receive side: out = bf16 of the decoded payload (exact; values below
+ * bf16's normal range rounded to nearest even).  out [R, D] bf16. */
+int moe_mxfp8_dequant(const uint8_t* x_q, const uint8_t* x_scale, int64_t R, int32_t D, moe_bf16* out,
+                      hipStream_t stream);
 
 /* ---------------------------------------------------------------------- */
 /* The paper's production router and shared expert (Section 5.2): sigmoid  */

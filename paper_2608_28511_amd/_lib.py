@@ -47,10 +47,13 @@ class LayerFwdArgs(C.Structure):
         ("score_fn", i32), ("Fs", i32), ("sel_bias", vp), ("Ws1", vp), ("Ws2", vp),
         ("seq_len", i64), ("aux_coeff", C.c_float), ("aux_loss", vp), ("seq_counts", vp),
         ("h_s", vp), ("u_s", vp), ("y_s", vp),
+        ("payload", i32), ("x_q", vp), ("x_scale", vp),
     ]
 
 
 SCORE_SOFTMAX, SCORE_SIGMOID = 0, 1
+PAYLOAD_BF16, PAYLOAD_MXFP8 = 0, 1
+U8 = torch.uint8
 
 
 _PROTOS = {
@@ -90,6 +93,9 @@ _PROTOS = {
     "moe_combine_add": (C.c_int, [vp, vp, vp, vp, i64, i32, i32, vp, vp]),
     "moe_shared_expert_fwd": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp, vp, vp]),
     "moe_shared_expert_bwd_workspace_bytes": (sz, [i64, i32, i32]),
+    "moe_mx_payload_bytes": (C.c_uint64, [i64, i32, i32]),
+    "moe_dispatch_mxfp8": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp, vp, vp]),
+    "moe_mxfp8_dequant": (C.c_int, [vp, vp, i64, i32, vp, vp]),
     "moe_shared_expert_bwd": (C.c_int, [vp, vp, vp, vp, vp, vp, i64, i32, i32, vp, i32, vp, vp, vp, sz, vp]),
 }
 
@@ -231,16 +237,18 @@ _LAYER_TENSORS = {
     "offsets": I32, "perm": I32, "inv_perm": I32, "x_disp": BF16, "p_disp": F32, "h": BF16,
     "u_save": BF16, "y_disp": BF16, "y_lat": BF16, "sel_bias": F32, "Ws1": BF16, "Ws2": BF16,
     "aux_loss": F32, "seq_counts": I32, "h_s": BF16, "u_s": BF16, "y_s": F32,
+    "x_q": torch.uint8, "x_scale": torch.uint8,
 }
 
 
 def layer_fwd_args(S, H, D, E, K, F, ws=None, score_fn=SCORE_SOFTMAX, Fs=0, seq_len=0, aux_coeff=0.0,
-                   **tensors) -> LayerFwdArgs:
+                   payload=PAYLOAD_BF16, **tensors) -> LayerFwdArgs:
     """Fill a moe_layer_fwd_args from sizes and named tensors (None = NULL)."""
     a = LayerFwdArgs()
     a.struct_size = C.sizeof(LayerFwdArgs)
     a.S, a.H, a.D, a.E, a.K, a.F = S, H, D, E, K, F
     a.score_fn, a.Fs, a.seq_len, a.aux_coeff = score_fn, Fs, seq_len, aux_coeff
+    a.payload = payload
     for name, t in tensors.items():
         if name not in _LAYER_TENSORS:
             raise KeyError(name)
@@ -374,3 +382,19 @@ def moe_shared_expert_bwd(x, u_s, h_s, dy, Ws1, Ws2, S, D, Fs, dx, accumulate_dx
         _ptr(Ws1, BF16, "Ws1"), _ptr(Ws2, BF16, "Ws2"), S, D, Fs, _ptr(dx, F32, "dx"), int(bool(accumulate_dx)),
         _ptr(dWs1, F32, "dWs1"), _ptr(dWs2, F32, "dWs2"), _ptr(ws, None, "ws"), _wsz(ws), _stream()),
         "moe_shared_expert_bwd")
+
+
+def moe_mx_payload_bytes(S, K, D) -> int:
+    return load().moe_mx_payload_bytes(S, K, D)
+
+
+def moe_dispatch_mxfp8(x, topk_prob, inv_perm, S, D, K, x_q, x_scale, p_disp):
+    _check(load().moe_dispatch_mxfp8(_ptr(x, BF16, "x"), _ptr(topk_prob, F32, "topk_prob"),
+                                     _ptr(inv_perm, I32, "inv_perm"), S, D, K, _ptr(x_q, U8, "x_q"),
+                                     _ptr(x_scale, U8, "x_scale"), _ptr(p_disp, F32, "p_disp"), _stream()),
+           "moe_dispatch_mxfp8")
+
+
+def moe_mxfp8_dequant(x_q, x_scale, R, D, out):
+    _check(load().moe_mxfp8_dequant(_ptr(x_q, U8, "x_q"), _ptr(x_scale, U8, "x_scale"), R, D,
+                                    _ptr(out, BF16, "out"), _stream()), "moe_mxfp8_dequant")

@@ -87,6 +87,35 @@ uint64_t moe_payload_bytes(int64_t S, int32_t K, int32_t D) {
     return (uint64_t)S * (uint64_t)K * ((uint64_t)D * 2u + 4u);
 }
 
+uint64_t moe_mx_payload_bytes(int64_t S, int32_t K, int32_t D) {
+    if (S < 0 || K < 0 || D < 0 || D % 32 != 0) return 0;
+    return (uint64_t)S * (uint64_t)K * ((uint64_t)D + (uint64_t)D / 32u + 4u);
+}
+
+int moe_dispatch_mxfp8(const moe_bf16* x, const float* topk_prob, const int32_t* inv_perm, int64_t S, int32_t D,
+                       int32_t K, uint8_t* x_q, uint8_t* x_scale, float* p_disp, hipStream_t stream) {
+    if (S < 0 || !dim_ok(D) || D % 32 != 0 || K < 1 || K > kMaxK || S * (int64_t)K >= kMaxRows)
+        return MOE_ERR_SHAPE;
+    if ((topk_prob == nullptr) != (p_disp == nullptr)) return MOE_ERR_NULL;
+    const uint64_t R = (uint64_t)S * K;
+    MOE_TRY(need(x, (uint64_t)S * D * 2, 16));
+    MOE_TRY(need(inv_perm, R * 4, 4));
+    MOE_TRY(need(x_q, R * D, 8));
+    MOE_TRY(need(x_scale, R * (D / 32), 1));
+    MOE_TRY(opt(topk_prob, 4));
+    MOE_TRY(opt(p_disp, 4));
+    return hip_status(moe::launch_dispatch_mx(x, topk_prob, inv_perm, S, D, K, x_q, x_scale, p_disp, stream));
+}
+
+int moe_mxfp8_dequant(const uint8_t* x_q, const uint8_t* x_scale, int64_t R, int32_t D, moe_bf16* out,
+                      hipStream_t stream) {
+    if (R < 0 || R >= kMaxRows || !dim_ok(D) || D % 32 != 0) return MOE_ERR_SHAPE;
+    MOE_TRY(need(x_q, (uint64_t)R * D, 8));
+    MOE_TRY(need(x_scale, (uint64_t)R * (D / 32), 1));
+    MOE_TRY(need(out, (uint64_t)R * D * 2, 16));
+    return hip_status(moe::launch_dequant_mx(x_q, x_scale, R, D, out, stream));
+}
+
 size_t moe_router_logits_workspace_bytes(int32_t D, int32_t E) {
     if (!dim_ok(D) || E < 1 || E > kMaxE) return 0;
     return moe::router_ws_bytes(D, E);
@@ -278,6 +307,8 @@ int check_layer_args(const moe_layer_fwd_args* a) {
         if (!dim_ok(a->Fs)) return MOE_ERR_SHAPE;
         if (a->H != 0 || !weight_ok(a->D, a->Fs)) return MOE_ERR_UNSUPPORTED;
     }
+    if (a->payload != MOE_PAYLOAD_BF16 && a->payload != MOE_PAYLOAD_MXFP8) return MOE_ERR_SHAPE;
+    if (a->payload == MOE_PAYLOAD_MXFP8 && a->D % 32 != 0) return MOE_ERR_SHAPE;
     return MOE_OK;
 }
 
@@ -287,7 +318,7 @@ struct LayerBufs {
     moe_bf16* x_lat; float* logits; int32_t* topk_idx; float* topk_prob; int32_t* counts;
     int32_t* offsets; int32_t* perm; int32_t* inv_perm; moe_bf16* x_disp; float* p_disp;
     moe_bf16* h; moe_bf16* y_disp; moe_bf16* y_lat; void* route_ws; void* sched; void* router_ws;
-    void* aux_ws; int32_t* seq_counts; moe_bf16* h_s; float* y_s;
+    void* aux_ws; int32_t* seq_counts; moe_bf16* h_s; float* y_s; uint8_t* x_q; uint8_t* x_scale;
 };
 
 size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
@@ -320,6 +351,9 @@ size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
         b->aux_ws = c.take(moe::seq_aux_ws_bytes(S, E, a->seq_len));
         b->seq_counts = pick(a->seq_counts, (size_t)(S / a->seq_len) * E * 4);
     }
+    const bool mx = a->payload == MOE_PAYLOAD_MXFP8;
+    b->x_q = mx ? pick(a->x_q, (size_t)R * D) : nullptr;
+    b->x_scale = mx ? pick(a->x_scale, (size_t)R * (D / 32)) : nullptr;
     b->h_s = a->Fs ? pick(a->h_s, (size_t)S * a->Fs * 2) : nullptr;
     b->y_s = a->Fs ? pick(a->y_s, (size_t)S * D * 4) : nullptr;
     return c.used;
@@ -358,7 +392,7 @@ int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
     }
     if (a->seq_len > 0) MOE_TRY(need(a->aux_loss, 4, 4));
     const void* bf16_ptrs[] = {a->x_lat, a->x_disp, a->h, a->u_save, a->y_disp, a->y_lat, a->h_s, a->u_s,
-                               a->y_s};
+                               a->y_s, a->x_q};
     for (const void* p : bf16_ptrs) MOE_TRY(opt(p, 16));
     const void* word_ptrs[] = {a->logits, a->topk_idx, a->topk_prob, a->counts, a->offsets,
                                a->perm, a->inv_perm, a->p_disp, a->sel_bias, a->seq_counts};
@@ -385,7 +419,12 @@ int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
                                          aux_coef(a->aux_coeff, S, E, K, a->seq_len), a->aux_loss,
                                          b.seq_counts, b.aux_ws, stream));
     }
-    MOE_HIP(moe::launch_dispatch(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_disp, b.p_disp, stream));
+    if (a->payload == MOE_PAYLOAD_MXFP8) {
+        MOE_HIP(moe::launch_dispatch_mx(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_q, b.x_scale, b.p_disp, stream));
+        MOE_HIP(moe::launch_dequant_mx(b.x_q, b.x_scale, R, D, b.x_disp, stream));
+    } else {
+        MOE_HIP(moe::launch_dispatch(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_disp, b.p_disp, stream));
+    }
     if (R > 0) {
         MOE_HIP(moe::launch_tile_schedule(b.offsets, E, R, b.sched, stream));
         MOE_HIP(moe::launch_grouped_rows(b.x_disp, D, a->W1, F, (int64_t)D * F, false, b.h, F,

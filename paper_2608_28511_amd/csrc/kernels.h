@@ -54,6 +54,12 @@ hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* t
 
 hipError_t launch_dispatch(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S,
                            int D, int K, moe_bf16* x_disp, float* p_disp, hipStream_t st);
+// MX-FP8 payload (D a multiple of 32): codes [S*K, D] and E8M0 scales
+// [S*K, D/32] of each token row at its K routed rows; decode to bf16.
+hipError_t launch_dispatch_mx(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S, int D,
+                              int K, uint8_t* x_q, uint8_t* x_scale, float* p_disp, hipStream_t st);
+hipError_t launch_dequant_mx(const uint8_t* x_q, const uint8_t* x_scale, int64_t R, int D, moe_bf16* out,
+                             hipStream_t st);
 // y[t] = bf16(sum_k w_k y_disp[pos_k] (+ add[t], fp32 [S,D], after the sum; NULL for none))
 hipError_t launch_combine(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_perm,
                           int64_t S, int D, int K, const float* add, moe_bf16* y, hipStream_t st);

@@ -51,6 +51,136 @@ __global__ __launch_bounds__(kRowThreads) void dispatch_kernel(const uint4* __re
     }
 }
 
+// ---- MX-FP8 dispatch payload (the precision lever on b_x, Eq. 1) ----------
+// OCP microscaling with FP8 E4M3 elements: per block of 32 elements of a row
+// one E8M0 scale byte s + 127, s = floor(log2 max|x|) - 8 clamped to
+// [-127, 127] (an all-zero block takes -127), and per element the E4M3 code
+// nearest to x * 2^-s (ties to even), saturated to +-448.  A lane's 16-byte
+// chunk is 8 elements, so one block is 4 adjacent lanes.
+
+// E4M3 code of a finite fp32 value (round to nearest even, saturating).
+__device__ __forceinline__ uint32_t e4m3_rne_sat(float v) {
+    const uint32_t u = __float_as_uint(v);
+    const uint32_t sign = (u >> 24) & 0x80u;
+    const uint32_t a = u & 0x7fffffffu;
+    if (a >= 0x43e00000u) return sign | 0x7eu;          // |v| >= 448
+    if (a < 0x3c800000u) {                              // |v| < 2^-6: multiples of 2^-9
+        const float q = rintf(__uint_as_float(a) * 512.f);  // exact scaling, ties to even
+        return sign | (uint32_t)q;                      // 8 -> 0x08, the smallest normal
+    }
+    // normal: keep 3 mantissa bits of the fp32 value, ties to even
+    const uint32_t r = (a + 0x7ffffu + ((a >> 20) & 1u)) & 0xfff00000u;
+    const uint32_t e = (r >> 23) - 120u;                // fp32 exponent 121..135 -> E4M3 field 1..15
+    return sign | (e << 3) | ((r >> 20) & 7u);
+}
+
+// bf16 bits of q * 2^t for an integer q in [0, 15] (exact, or rounded to
+// nearest even below bf16's smallest normal), with the given sign bit.
+__device__ __forceinline__ uint32_t bf16_of_scaled(uint32_t q, int t, uint32_t sign16) {
+    if (q == 0) return sign16;
+    const int L = 31 - __builtin_clz(q);                // q in [2^L, 2^(L+1))
+    const int E = t + L;                                // exponent of the value
+    if (E >= -126) return sign16 | ((uint32_t)(E + 127) << 7) | ((q << (7 - L)) & 0x7fu);
+    const int sh = t + 133;                             // value = q * 2^sh * 2^-133
+    uint32_t m;
+    if (sh >= 0) {
+        m = q << sh;
+    } else {
+        const int n = -sh;
+        m = q >> n;
+        const uint32_t rem = q & ((1u << n) - 1u), half = 1u << (n - 1);
+        if (rem > half || (rem == half && (m & 1u))) ++m;
+    }
+    return sign16 | m;                                  // m == 128 encodes 2^-126 itself
+}
+
+// bf16 bits of one E4M3 code times 2^s.
+__device__ __forceinline__ uint32_t e4m3_scaled_to_bf16(uint32_t c, int s) {
+    const uint32_t sign16 = (c & 0x80u) << 8;
+    const uint32_t e = (c >> 3) & 15u, m = c & 7u;
+    return e == 0 ? bf16_of_scaled(m, s - 9, sign16) : bf16_of_scaled(8u | m, (int)e - 10 + s, sign16);
+}
+
+__device__ __forceinline__ uint32_t bf16_mag_max8(const uint4& v) {
+    uint32_t m = max(max(v.x & 0x7fffu, v.x >> 16 & 0x7fffu), max(v.y & 0x7fffu, v.y >> 16 & 0x7fffu));
+    return max(m, max(max(v.z & 0x7fffu, v.z >> 16 & 0x7fffu), max(v.w & 0x7fffu, v.w >> 16 & 0x7fffu)));
+}
+
+// One wavefront per token: the row is encoded once and its codes and block
+// scales are written to the token's K routed rows.
+__global__ __launch_bounds__(kRowThreads) void dispatch_mx_kernel(const uint4* __restrict__ x,
+                                                                  const float* __restrict__ prob,
+                                                                  const int32_t* __restrict__ inv_perm,
+                                                                  int64_t S, int D8, int K,
+                                                                  uint2* __restrict__ x_q,
+                                                                  uint8_t* __restrict__ x_scale,
+                                                                  float* __restrict__ p_disp) {
+    const int lane = threadIdx.x & 63;
+    const int64_t t = (int64_t)blockIdx.x * kRowTok + (threadIdx.x >> 6);
+    if (t >= S) return;
+    const int64_t R = S * K;
+    const int D32 = D8 / 4;
+    int pos_l = lane < K ? inv_perm[t * K + lane] : 0;
+    if ((uint32_t)pos_l >= (uint64_t)R) pos_l = -1;  // out-of-range entries are not written
+    if (p_disp != nullptr && lane < K && pos_l >= 0) p_disp[pos_l] = prob[t * K + lane];
+    const uint4* src = x + t * D8;
+    for (int c0 = 0; c0 < D8; c0 += kWave * kCPL) {
+        uint2 q[kCPL];
+        uint32_t sc[kCPL];
+#pragma unroll
+        for (int i = 0; i < kCPL; ++i) {
+            const int c = c0 + lane + kWave * i;      // D8 is a multiple of 4: whole blocks per lane group
+            const uint4 v = c < D8 ? src[c] : make_uint4(0, 0, 0, 0);
+            uint32_t am = bf16_mag_max8(v);
+            am = max(am, (uint32_t)__shfl_xor((int)am, 1));
+            am = max(am, (uint32_t)__shfl_xor((int)am, 2));
+            const int ef = (int)(am >> 7);            // bf16 exponent field of the block maximum
+            const int sh = ef == 0 ? -127 : max(ef - 127 - 8, -127);
+            sc[i] = (uint32_t)(sh + 127);
+            const float inv = __uint_as_float((uint32_t)(127 - sh) << 23);  // 2^-s, a normal fp32
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+            uint32_t b[2] = {0u, 0u};
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+                const uint32_t lo = e4m3_rne_sat(bf16_lo(w[h]) * inv);
+                const uint32_t hi = e4m3_rne_sat(bf16_hi(w[h]) * inv);
+                b[h >> 1] |= (lo | (hi << 8)) << (16 * (h & 1));
+            }
+            q[i] = make_uint2(b[0], b[1]);
+        }
+        for (int k = 0; k < K; ++k) {
+            const int64_t pos = __shfl(pos_l, k);
+            if (pos < 0) continue;
+#pragma unroll
+            for (int i = 0; i < kCPL; ++i) {
+                const int c = c0 + lane + kWave * i;
+                if (c >= D8) continue;
+                x_q[pos * D8 + c] = q[i];
+                if ((lane & 3) == 0) x_scale[pos * D32 + c / 4] = (uint8_t)sc[i];
+            }
+        }
+    }
+}
+
+// out[r, :] = bf16 of the decoded MX-FP8 row (exact: 4 significant bits
+// times a power of two), one thread per 8 elements.
+__global__ __launch_bounds__(256) void dequant_mx_kernel(const uint2* __restrict__ x_q,
+                                                         const uint8_t* __restrict__ x_scale, int64_t n8,
+                                                         uint4* __restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n8) return;
+    const uint2 q = x_q[i];
+    const int s = (int)x_scale[i / 4] - 127;
+    const uint32_t b[2] = {q.x, q.y};
+    uint32_t o[4];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+        const uint32_t w = b[h >> 1] >> (16 * (h & 1));
+        o[h] = e4m3_scaled_to_bf16(w & 0xffu, s) | (e4m3_scaled_to_bf16((w >> 8) & 0xffu, s) << 16);
+    }
+    out[i] = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
 __device__ __forceinline__ void fma8(float* acc, float w, const uint4& v) {
     acc[0] = fmaf(w, bf16_lo(v.x), acc[0]);
     acc[1] = fmaf(w, bf16_hi(v.x), acc[1]);
@@ -201,6 +331,27 @@ hipError_t launch_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const 
     hipLaunchKernelGGL(combine_bwd_kernel, dim3(grid_for(S, kRowTok)), dim3(kRowThreads), 0, st,
                        (const uint4*)dy, (const uint4*)y_disp, p_disp, inv_perm, S, D / 8, K,
                        (uint4*)dy_disp, dp);
+    return hipGetLastError();
+}
+
+}  // namespace moe
+
+namespace moe {
+
+hipError_t launch_dispatch_mx(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S, int D,
+                              int K, uint8_t* x_q, uint8_t* x_scale, float* p_disp, hipStream_t st) {
+    if (S == 0) return hipSuccess;
+    hipLaunchKernelGGL(dispatch_mx_kernel, dim3(grid_for(S, kRowTok)), dim3(kRowThreads), 0, st, (const uint4*)x,
+                       prob, inv_perm, S, D / 8, K, (uint2*)x_q, x_scale, p_disp);
+    return hipGetLastError();
+}
+
+hipError_t launch_dequant_mx(const uint8_t* x_q, const uint8_t* x_scale, int64_t R, int D, moe_bf16* out,
+                             hipStream_t st) {
+    const int64_t n8 = R * (D / 8);
+    if (n8 == 0) return hipSuccess;
+    hipLaunchKernelGGL(dequant_mx_kernel, dim3(grid_for(n8, 256)), dim3(256), 0, st, (const uint2*)x_q, x_scale, n8,
+                       (uint4*)out);
     return hipGetLastError();
 }
 

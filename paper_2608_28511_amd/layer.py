@@ -50,6 +50,24 @@ def dispatch(x: torch.Tensor, topk_prob: Optional[torch.Tensor], inv_perm: torch
     return x_disp, p_disp
 
 
+def dispatch_mxfp8(x: torch.Tensor, topk_prob: Optional[torch.Tensor], inv_perm: torch.Tensor, K: int):
+    """(x_q uint8 [S*K, D], x_scale uint8 [S*K, D/32], p_disp fp32 or None)."""
+    S, D = x.shape
+    dev = x.device
+    x_q = _empty((S * K, D), torch.uint8, dev)
+    x_scale = _empty((S * K, D // 32), torch.uint8, dev)
+    p_disp = _empty((S * K,), F32, dev) if topk_prob is not None else None
+    L.moe_dispatch_mxfp8(x, topk_prob, inv_perm, S, D, K, x_q, x_scale, p_disp)
+    return x_q, x_scale, p_disp
+
+
+def mxfp8_dequant(x_q: torch.Tensor, x_scale: torch.Tensor) -> torch.Tensor:
+    R, D = x_q.shape
+    out = _empty((R, D), BF16, x_q.device)
+    L.moe_mxfp8_dequant(x_q, x_scale, R, D, out)
+    return out
+
+
 def grouped_ffn(x_disp: torch.Tensor, offsets: torch.Tensor, W1: torch.Tensor, W2: torch.Tensor,
                 save_u: bool = False):
     R, D = x_disp.shape
@@ -251,8 +269,9 @@ class LayerFwd:
     """
 
     def __init__(self, S, D, E, K, F, H=0, device="cuda", export=True, save_u=False, score="softmax",
-                 Fs=0, seq_len=0, aux_coeff=0.0):
+                 Fs=0, seq_len=0, aux_coeff=0.0, payload="bf16"):
         self.S, self.D, self.E, self.K, self.F, self.H = S, D, E, K, F, H
+        self.payload = {"bf16": L.PAYLOAD_BF16, "mxfp8": L.PAYLOAD_MXFP8}[payload]
         self.score_fn = {"softmax": L.SCORE_SOFTMAX, "sigmoid": L.SCORE_SIGMOID}[score]
         self.Fs, self.seq_len, self.aux_coeff = Fs, seq_len, aux_coeff
         dev = torch.device(device)
@@ -276,6 +295,9 @@ class LayerFwd:
             self.out["aux_loss"] = _empty((1,), F32, dev)
             if export:
                 self.out["seq_counts"] = _empty((S // seq_len, E), I32, dev)
+        if payload == "mxfp8" and export:
+            self.out["x_q"] = _empty((R, D), torch.uint8, dev)
+            self.out["x_scale"] = _empty((R, D // 32), torch.uint8, dev)
         if Fs:
             if export:
                 self.out["h_s"] = _empty((S, Fs), BF16, dev)
@@ -289,7 +311,8 @@ class LayerFwd:
         self.ws = _ws(self.ws_bytes, dev)
 
     def _modes(self):
-        return dict(score_fn=self.score_fn, Fs=self.Fs, seq_len=self.seq_len, aux_coeff=self.aux_coeff)
+        return dict(score_fn=self.score_fn, Fs=self.Fs, seq_len=self.seq_len, aux_coeff=self.aux_coeff,
+                    payload=self.payload)
 
     def __call__(self, x, Wr, W1, W2, bias=None, Wdown=None, Wup=None, sel_bias=None, Ws1=None, Ws2=None):
         a = L.layer_fwd_args(self.S, self.H, self.D, self.E, self.K, self.F, ws=self.ws, x=x, Wr=Wr,

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_status_payload(lib):
-    assert L.moe_abi_version() == 2
+    assert L.moe_abi_version() == 3
     assert L.moe_status_string(0) == "ok"
     for code in range(-6, 0):
         assert L.moe_status_string(code) not in ("ok", "unknown status")
@@ -46,6 +46,9 @@ def test_version_status_payload(lib):
     assert L.moe_payload_bytes(8192, 6, 2048) == 8192 * 6 * (2048 * 2 + 4) == 201_523_200
     assert L.moe_payload_bytes(16384, 8, 2048) == 16384 * 8 * (2048 * 2 + 4)
     assert L.moe_payload_bytes(-1, 2, 8) == 0
+    # MX-FP8 hidden payload: b_x = 1 + 1/32
+    assert L.moe_mx_payload_bytes(8192, 6, 2048) == 8192 * 6 * (2048 + 64 + 4) == 104_005_632
+    assert L.moe_mx_payload_bytes(8192, 6, 2040) == 0
 
 
 def test_workspace_queries(lib):
@@ -175,10 +178,22 @@ def test_validation_errors_return_before_launch(lib):
     assert lib.moe_layer_fwd(C.byref(a), st) == -1       # shared expert without its weights
     a.score_fn = 7
     assert lib.moe_layer_fwd(C.byref(a), st) == -2
+    a.score_fn, a.Fs = 0, 0
+    a.payload = 2
+    assert lib.moe_layer_fwd(C.byref(a), st) == -2       # unknown payload format
+    a.payload = 1                                         # MX-FP8 needs D % 32 == 0 (D = 16 here)
+    assert lib.moe_layer_fwd(C.byref(a), st) == -2
 
 
 def test_production_validation_errors(lib):
     st = None
+    # MX-FP8 payload: D a multiple of 32, x_q 8-byte aligned, both outputs required
+    assert lib.moe_dispatch_mxfp8(FAKE, FAKE, FAKE, 4, 48, 2, FAKE, FAKE, FAKE, st) == -2
+    assert lib.moe_dispatch_mxfp8(FAKE, FAKE, FAKE, 4, 64, 2, FAKE, None, FAKE, st) == -1
+    assert lib.moe_dispatch_mxfp8(FAKE, FAKE, FAKE, 4, 64, 2, C.c_void_p(0x10004), FAKE, FAKE, st) == -3
+    assert lib.moe_dispatch_mxfp8(FAKE, None, FAKE, 4, 64, 2, FAKE, FAKE, FAKE, st) == -1
+    assert lib.moe_mxfp8_dequant(FAKE, FAKE, 4, 40, FAKE, st) == -2
+    assert lib.moe_mxfp8_dequant(FAKE, None, 4, 64, FAKE, st) == -1
     assert lib.moe_route_sigmoid(FAKE, None, 4, 8, 9, *[FAKE] * 6, FAKE, 1 << 20, st) == -2
     assert lib.moe_route_sigmoid(FAKE, ODD, 4, 8, 2, *[FAKE] * 6, FAKE, 1 << 20, st) == -3
     assert lib.moe_route_sigmoid(FAKE, None, 4, 8, 2, *[FAKE] * 6, FAKE, 4, st) == -4

@@ -1,0 +1,111 @@
+"""GPU parity of the MX-FP8 dispatch payload (Section 1's precision lever on
+b_x): codes, block scales and the decoded rows are integer/byte work and
+must match the oracle bit for bit; the layer with the MX payload is held to
+the bf16 output bar against the oracle's chain on the same payload."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+from paper_2608_28511_amd import layer
+from paper_2608_28511_amd.workloads import WORKLOADS, make_inputs
+
+from gpu_helpers import LazyExperts, assert_bf16_close, np64, npi
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _rows(kind, S, D, seed):
+    g = torch.Generator().manual_seed(seed)
+    x = torch.randn((S, D), generator=g)
+    if kind == "wide":        # per-row scales over ~2^-40 .. 2^40
+        x = x * torch.exp2(torch.randint(-40, 40, (S, 1), generator=g).float())
+    elif kind == "tiny":      # bf16 subnormals and blocks near the bottom of the range
+        x = x * 2.0 ** -128
+    elif kind == "edge":      # zero blocks, -0, block maxima just below a power of two (saturation)
+        x[:, :32] = 0.0
+        x[::2, 32:64] = -0.0
+        x[:, 64] = 1.99 * torch.sign(x[:, 64] + 0.5)
+        x[1::3, 96:128] = 0.0
+        x[1::3, 97] = 2.0 ** 100
+    return x.to(torch.bfloat16)
+
+
+def _random_inv(S, K, seed):
+    g = torch.Generator().manual_seed(seed)
+    return torch.randperm(S * K, generator=g).to(torch.int32)
+
+
+@pytest.mark.parametrize("kind", ["normal", "wide", "tiny", "edge"])
+@pytest.mark.parametrize("S,D,K", [(1, 32, 1), (37, 96, 3), (256, 2048, 6), (100, 2688, 7), (513, 128, 8)])
+def test_dispatch_mxfp8_bit_exact(kind, S, D, K):
+    if kind == "edge" and D < 128:
+        pytest.skip("edge rows need four blocks")
+    x = _rows(kind, S, D, S + D + K)
+    inv = _random_inv(S, K, S * K)
+    g = torch.Generator().manual_seed(S)
+    p = torch.rand((S, K), generator=g)
+    xq, xs, pd = layer.dispatch_mxfp8(x.to(DEV), p.to(DEV), inv.to(DEV), K)
+    torch.cuda.synchronize()
+    cd, sc, pref = O.dispatch_mxfp8(np64(x), p.numpy(), inv.numpy(), K)
+    assert np.array_equal(xq.cpu().numpy(), cd), "codes"
+    assert np.array_equal(xs.cpu().numpy(), sc), "scales"
+    assert np.array_equal(pd.cpu().numpy(), pref), "p_disp"
+    # receive side: the decoded bf16 rows are exact
+    out = layer.mxfp8_dequant(xq, xs)
+    torch.cuda.synchronize()
+    want = O.round_bf16(O.mxfp8_dequantize(cd, sc))
+    got = np64(out)
+    assert np.array_equal(got, want) and np.array_equal(np.signbit(got), np.signbit(want)), "dequant"
+
+
+def test_dequant_every_code_and_scale():
+    # all 254 finite codes at every scale from 2^-127 to 2^119 (the bottom of
+    # the range rounds below bf16's smallest normal)
+    codes = np.array([c for c in range(256) if c & 0x7F != 0x7F], np.uint8)
+    s = np.arange(-127, 120)
+    R = len(s)
+    cq = np.zeros((R, 256), np.uint8)
+    cq[:, :254] = codes[None, :]
+    sc = np.repeat((s + 127).astype(np.uint8)[:, None], 8, axis=1)
+    out = layer.mxfp8_dequant(torch.as_tensor(cq).to(DEV), torch.as_tensor(sc).to(DEV))
+    torch.cuda.synchronize()
+    want = O.round_bf16(O.mxfp8_dequantize(cq, sc))
+    got = np64(out)
+    assert np.array_equal(got, want) and np.array_equal(np.signbit(got), np.signbit(want))
+
+
+def test_mx_payload_bytes():
+    from paper_2608_28511_amd import _lib as L
+    for S, K, D in [(8192, 6, 2048), (16384, 7, 2688), (1, 1, 32)]:
+        assert L.moe_mx_payload_bytes(S, K, D) == O.mx_payload_bytes(S, K, D)
+    assert L.moe_mx_payload_bytes(8, 2, 48) == 0
+
+
+@pytest.mark.parametrize("name,n_samples", [("tiny_s512_d256_e8_k2", None), ("base_s8192_d2048_e64_k6", 32)])
+def test_layer_fwd_mxfp8(name, n_samples):
+    s = WORKLOADS[name]
+    inp = make_inputs(s, device=DEV)
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, export=True, payload="mxfp8")
+    out = lf(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"])
+    torch.cuda.synchronize()
+    x = np64(inp["x"])
+    # the payload: each routed row holds its token's encoding, bit for bit
+    c, sc = O.mxfp8_quantize(x)
+    inv = npi(out["inv_perm"]).reshape(s.S, s.K)
+    xq, xs = out["x_q"].cpu().numpy(), out["x_scale"].cpu().numpy()
+    for k in range(s.K):
+        assert np.array_equal(xq[inv[:, k]], c) and np.array_equal(xs[inv[:, k]], sc)
+    assert np.array_equal(np64(out["x_disp"])[inv[:, 0]], O.round_bf16(O.mxfp8_dequantize(c, sc)))
+    # outputs against the oracle's chain on the same MX payload (routing is
+    # unchanged by the payload: the router reads x itself)
+    rng = np.random.default_rng(s.seed)
+    tok = np.arange(s.S) if n_samples is None else np.sort(rng.choice(s.S, n_samples, replace=False))
+    ref = O.layer_fwd(x[tok], np64(inp["Wr"]), LazyExperts(inp["W1"]), LazyExperts(inp["W2"]), s.K,
+                      bias=None if inp["bias"] is None else np64(inp["bias"]), payload="mxfp8",
+                      round_payload=False)
+    idx = npi(out["topk_idx"])[tok]
+    ok = np.all(idx == ref["topk_idx"], axis=1)
+    assert ok.mean() > 0.99
+    assert_bf16_close(np64(out["y"][torch.as_tensor(tok[ok], device=DEV)]), ref["y"][ok], f"{name} y (mxfp8)")
