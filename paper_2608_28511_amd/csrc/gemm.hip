@@ -65,6 +65,7 @@
 namespace moe {
 
 constexpr int BM = 128, BN = 256;
+constexpr int MI = BM / 32;                     // A fragments (16 rows) per wave: waves cover BM/2 rows
 constexpr int kGemmThreads = kWaves * 64;
 constexpr int kStages = 3;
 constexpr int kABytes = BM * BK * 2;            // 16 KB
@@ -100,16 +101,16 @@ struct GemmArgs {
 // between the two MFMA blocks, and accumulate.  `next` says whether there is
 // a stage to copy; nrem is the contraction length left from its start.
 template <bool A_K, bool B_K, bool KTAIL, int S, class DA, class DB, int NA, int NB>
-__device__ __forceinline__ void mma_stage(f32x4 (&acc)[4][4], const uint32_t (&abase)[NA],
+__device__ __forceinline__ void mma_stage(f32x4 (&acc)[MI][4], const uint32_t (&abase)[NA],
                                           const uint32_t (&bbase)[2][NB], DA& da, DB& db, bool next,
                                           int64_t nrem, uint32_t ldsA, uint32_t ldsB, int wave) {
-    constexpr int NS = (S + 2) % kStages;
+    constexpr int NS = (S + kStages - 1) % kStages;
     constexpr int kSA = DA::kSlots, kSB = DB::kSlots;
 #pragma unroll
     for (int kk = 0; kk < BK / 32; ++kk) {
-        bf16x8 af[4], bfg[4];
+        bf16x8 af[MI], bfg[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < MI; ++i) {
             if constexpr (A_K) af[i] = lds_b128(abase[kk] + S * kABytes + i * 2048);
             else af[i] = lds_tr_pair(abase[i] + S * kABytes + kk * 64 * BM, 8 * BM);
         }
@@ -128,10 +129,13 @@ __device__ __forceinline__ void mma_stage(f32x4 (&acc)[4][4], const uint32_t (&a
             }
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfg[j], af[i], acc[i][j], 0, 0, 0);
+        // keep the two k halves' fragment sets from being live at once (the
+        // other wave on the SIMD covers the second half's read latency)
+        if constexpr (MI > 4) __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -141,18 +145,18 @@ __device__ __forceinline__ void frag_bases(uint32_t (&abase)[NA], uint32_t (&bba
                                            uint32_t ldsB, int wm, int wn, int lane) {
 #pragma unroll
     for (int i = 0; i < NA; ++i)
-        abase[i] = ldsA + (A_K ? row_base(wm * 64, i, lane) : col_base<BM>(wm * 64 + i * 16, lane));
+        abase[i] = ldsA + (A_K ? row_base(wm * (BM / 2), i, lane) : col_base<BM>(wm * (BM / 2) + i * 16, lane));
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
         const uint32_t o = B_K ? row_base(wn * 64, j, lane) : col_base<BN>(wn * 64 + j * 16, lane);
         bbase[0][j] = ldsB + o;          // stages 0 and 1
-        bbase[1][j] = ldsB + 2 * kBBytes + o;  // stage 2 (immediate offsets reach 64 KB)
+        bbase[1][j] = ldsB + 2 * kBBytes + o;  // stage 2 of a 3-stage ring (immediate offsets reach 64 KB)
     }
 }
 
-__device__ __forceinline__ void zero_acc(f32x4 (&acc)[4][4]) {
+__device__ __forceinline__ void zero_acc(f32x4 (&acc)[MI][4]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 }
@@ -189,10 +193,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) 
     db.init(p.B, p.ldb, n0, (int64_t)p.N, k_begin, k_end, wave, lane);
     constexpr int kPerStage = DmaTile<false, BM>::kSlots + DmaTile<false, BN>::kSlots;
 
-    uint32_t abase[4], bbase[2][4];
+    uint32_t abase[MI], bbase[2][4];
     frag_bases<false, false>(abase, bbase, ldsA, ldsB, wm, wn, lane);
 
-    f32x4 acc[4][4];
+    f32x4 acc[MI][4];
     zero_acc(acc);
 
     const int64_t klen = k_end - k_begin;
@@ -200,31 +204,31 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) 
 
     auto step = [&](auto stage_c, int kt) {
         constexpr int S = decltype(stage_c)::value;
-        if (kt + 1 < nk) wait_vmcnt<kPerStage>(); else wait_vmcnt<0>();
+        // stages kt .. kt + kStages - 2 are in flight; stage kt must have landed
+        if (kStages == 3 && kt + 1 < nk) wait_vmcnt<kPerStage>(); else wait_vmcnt<0>();
         stage_barrier();
-        mma_stage<false, false, true, S>(acc, abase, bbase, da, db, kt + 2 < nk,
-                                         klen - (int64_t)(kt + 2) * BK, ldsA, ldsB, wave);
+        mma_stage<false, false, true, S>(acc, abase, bbase, da, db, kt + kStages - 1 < nk,
+                                         klen - (int64_t)(kt + kStages - 1) * BK, ldsA, ldsB, wave);
     };
 
     if (nk > 0) {
-        da.template issue<true, 0, DmaTile<false, BM>::kSlots>(ldsA, klen, wave);
-        db.template issue<true, 0, DmaTile<false, BN>::kSlots>(ldsB, klen, wave);
-        if (nk > 1) {
-            da.template issue<true, 0, DmaTile<false, BM>::kSlots>(ldsA + kABytes, klen - BK, wave);
-            db.template issue<true, 0, DmaTile<false, BN>::kSlots>(ldsB + kBBytes, klen - BK, wave);
+        for (int q = 0; q < kStages - 1 && q < nk; ++q) {
+            da.template issue<true, 0, DmaTile<false, BM>::kSlots>(ldsA + q * kABytes, klen - (int64_t)q * BK, wave);
+            db.template issue<true, 0, DmaTile<false, BN>::kSlots>(ldsB + q * kBBytes, klen - (int64_t)q * BK, wave);
         }
         for (int kt = 0; kt < nk; kt += kStages) {
             step(std::integral_constant<int, 0>{}, kt);
             if (kt + 1 < nk) step(std::integral_constant<int, 1>{}, kt + 1);
-            if (kt + 2 < nk) step(std::integral_constant<int, 2>{}, kt + 2);
+            if constexpr (kStages == 3)
+                if (kt + 2 < nk) step(std::integral_constant<int, 2 % kStages>{}, kt + 2);
         }
     }
 
     // lane holds C[m][n .. n+3] for each (i, j)
     const int64_t c_base = (int64_t)e * p.c_stride;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t m = row0 + wm * 64 + i * 16 + (lane & 15);
+    for (int i = 0; i < MI; ++i) {
+        const int64_t m = row0 + wm * (BM / 2) + i * 16 + (lane & 15);
         if (m >= row_hi) continue;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -293,7 +297,7 @@ constexpr uint32_t kDropOffset = 0x80000000u;  // beyond any descriptor's range
 // buffer_store_dwordx4 of 8 rows x 128 bytes each.  OUT: 0 = the product
 // (squared-ReLU applied for EPI_RELU2), 1 = the raw product (pre-activation).
 template <int EPI, int OUT>
-__device__ __forceinline__ void staged_store(const f32x4 (&acc)[4][4], void* C, int64_t ldc, int N,
+__device__ __forceinline__ void staged_store(const f32x4 (&acc)[MI][4], void* C, int64_t ldc, int N,
                                              int64_t rbase, int64_t nrows, int64_t cbase,
                                              uint32_t ep, int lane) {
     const __amdgpu_buffer_rsrc_t rs = rows_rsrc(C, rbase, nrows, ldc);
@@ -302,7 +306,7 @@ __device__ __forceinline__ void staged_store(const f32x4 (&acc)[4][4], void* C, 
     const int rr0 = lane >> 3, c = lane & 7;
     const bool col_ok = cbase + c * 8 < N;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < MI; ++i) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const f32x4 a = acc[i][j];
@@ -327,20 +331,38 @@ __device__ __forceinline__ void staged_store(const f32x4 (&acc)[4][4], void* C, 
 }
 
 // dgrad epilogue: C = bf16(acc * 2 max(u, 0)) with u read from aux_in at the
-// accumulator's own positions (8 bytes per lane and fragment).
-__device__ __forceinline__ void drelu2_store(const f32x4 (&acc)[4][4], void* C, const uint16_t* aux_in,
-                                             int64_t ldc, int N, int64_t rbase, int64_t nrows,
-                                             int64_t cbase, int lane) {
-    const __amdgpu_buffer_rsrc_t rc = rows_rsrc(C, rbase, nrows, ldc);
+// accumulators' own positions (8 bytes per lane and fragment).  The sixteen
+// u loads are issued by drelu2_load at the tile's first k step (right after
+// its barrier, before that step's operand copies), so they have long
+// completed when drelu2_store uses them: its waits never reach the copies
+// in flight at the tile's end.
+__device__ __forceinline__ void drelu2_load(u32x2 (&uu)[MI][4], const uint16_t* aux_in, int64_t ldc, int N,
+                                            int64_t rbase, int64_t nrows, int64_t cbase, int lane) {
     const __amdgpu_buffer_rsrc_t ru = rows_rsrc(aux_in, rbase, nrows, ldc);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < MI; ++i) {
         const int64_t row = i * 16 + (lane & 15);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int64_t col = cbase + j * 16 + 4 * (lane >> 4);
             const uint32_t off = (row < nrows && col < N) ? (uint32_t)((row * ldc + col) * 2) : kDropOffset;
-            const u32x2 u = __builtin_amdgcn_raw_buffer_load_b64(ru, off, 0, 0);
+            uu[i][j] = __builtin_amdgcn_raw_buffer_load_b64(ru, off, 0, 0);
+        }
+    }
+}
+
+__device__ __forceinline__ void drelu2_store(const f32x4 (&acc)[MI][4], const u32x2 (&uu)[MI][4], void* C,
+                                             int64_t ldc, int N, int64_t rbase, int64_t nrows, int64_t cbase,
+                                             int lane) {
+    const __amdgpu_buffer_rsrc_t rc = rows_rsrc(C, rbase, nrows, ldc);
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+        const int64_t row = i * 16 + (lane & 15);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t col = cbase + j * 16 + 4 * (lane >> 4);
+            const uint32_t off = (row < nrows && col < N) ? (uint32_t)((row * ldc + col) * 2) : kDropOffset;
+            const u32x2 u = uu[i][j];
             const f32x4 a = acc[i][j];
             const float g0 = a[0] * 2.f * fmaxf(bf16_lo(u[0]), 0.f);
             const float g1 = a[1] * 2.f * fmaxf(bf16_hi(u[0]), 0.f);
@@ -356,15 +378,15 @@ __device__ __forceinline__ void drelu2_store(const f32x4 (&acc)[4][4], void* C, 
 // consecutive columns of one row, stored as one 16-byte buffer store (with
 // `accumulate`, added to what C holds there).  The descriptor spans only this
 // wave's rows, so rows past the tile and columns past N are dropped.
-__device__ __forceinline__ void f32_store(const f32x4 (&acc)[4][4], float* C, int64_t ldc, int N,
+__device__ __forceinline__ void f32_store(const f32x4 (&acc)[MI][4], float* C, int64_t ldc, int N,
                                           int64_t rbase, int64_t nrows, int64_t cbase, bool accumulate,
                                           int lane) {
-    const int64_t rows = nrows < 64 ? nrows : 64;
+    const int64_t rows = nrows < BM / 2 ? nrows : BM / 2;
     const int32_t bytes = rows > 0 ? (int32_t)(rows * ldc * 4) : 0;
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)(C + rbase * ldc), 0, bytes,
                                                                         0x00020000);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < MI; ++i) {
         const int64_t row = i * 16 + (lane & 15);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -428,43 +450,47 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     uint32_t abase[2], bbase[2][kNB];
     frag_bases<true, B_K>(abase, bbase, ldsA, ldsB, wm, wn, lane);
 
-    f32x4 acc[4][4];
+    f32x4 acc[MI][4];
     zero_acc(acc);
 
-    // DMA of the first two steps; kd / jd track the step two ahead.
-    dma_tile(0);
-    da.template issue<KTAIL, 0, kSA>(ldsA, p.Kd, wave);
-    db.template issue<KTAIL, 0, kSB>(ldsB, p.Kd, wave);
-    int kd = 1 % nk;
-    int jd = 1 / nk;
-    if (g_total > 1) {
+    // DMA of the first kStages - 1 steps; kd / jd track the next step to send.
+    int kd = 0, jd = 0;
+    for (int q = 0; q < kStages - 1 && q < g_total; ++q) {
         if (kd == 0) dma_tile(jd);
         const int rem = p.Kd - kd * BK;
-        da.template issue<KTAIL, 0, kSA>(ldsA + kABytes, rem, wave);
-        db.template issue<KTAIL, 0, kSB>(ldsB + kBBytes, rem, wave);
+        da.template issue<KTAIL, 0, kSA>(ldsA + q * kABytes, rem, wave);
+        db.template issue<KTAIL, 0, kSB>(ldsB + q * kBBytes, rem, wave);
+        if (++kd == nk) { kd = 0; ++jd; }
     }
-    if (++kd == nk) { kd = 0; ++jd; }
 
     int kc = 0;   // k step of the tile being computed
     int jc = 0;   // its index in this workgroup's list
     RowsTile cur = rows_tile(p, m_total, first);
+    u32x2 uu[MI][4];   // dgrad: the tile's pre-activations
 
     auto step = [&](auto stage_c, int g) {
         constexpr int S = decltype(stage_c)::value;
-        // Stores of an epilogue may still be in flight; they are not counted,
-        // so the wait covers this stage's copies whichever way they complete.
-        if (g + 1 < g_total) wait_vmcnt<kPerStage>(); else wait_vmcnt<0>();
+        // Stages g .. g + kStages - 2 are in flight and stage g must have
+        // landed.  Stores of an epilogue may still be in flight; they are
+        // not counted, so the wait covers this stage's copies whichever way
+        // they complete (loads complete in order among themselves).
+        if (kStages == 3 && g + 1 < g_total) wait_vmcnt<kPerStage>(); else wait_vmcnt<0>();
         stage_barrier();
-        const bool next = g + 2 < g_total;
+        if constexpr (EPI == EPI_DRELU2 && MI <= 4)   // with taller tiles: loaded in the epilogue
+            if (kc == 0)
+                drelu2_load(uu, p.aux_in, p.ldc, p.N, cur.row0 + wm * (BM / 2),
+                            cur.row_hi - (cur.row0 + wm * (BM / 2)), cur.n0 + wn * 64, lane);
+        const bool next = g + kStages - 1 < g_total;
         if (next && kd == 0) dma_tile(jd);
         mma_stage<true, B_K, KTAIL, S>(acc, abase, bbase, da, db, next, p.Kd - kd * BK, ldsA, ldsB, wave);
         if (++kd == nk) { kd = 0; ++jd; }
         if (kc == nk - 1) {
-            const int rbase = cur.row0 + wm * 64;
+            const int rbase = cur.row0 + wm * (BM / 2);
             const int nrows = cur.row_hi - rbase;
             const int cbase = cur.n0 + wn * 64;
             if constexpr (EPI == EPI_DRELU2) {
-                drelu2_store(acc, p.C, p.aux_in, p.ldc, p.N, rbase, nrows, cbase, lane);
+                if constexpr (MI > 4) drelu2_load(uu, p.aux_in, p.ldc, p.N, rbase, nrows, cbase, lane);
+                drelu2_store(acc, uu, p.C, p.ldc, p.N, rbase, nrows, cbase, lane);
             } else if constexpr (EPI == EPI_F32) {
                 f32_store(acc, (float*)p.C, p.ldc, p.N, rbase, nrows, cbase, p.accumulate != 0, lane);
             } else {
@@ -485,7 +511,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     for (int g = 0; g < g_total; g += kStages) {
         step(std::integral_constant<int, 0>{}, g);
         if (g + 1 < g_total) step(std::integral_constant<int, 1>{}, g + 1);
-        if (g + 2 < g_total) step(std::integral_constant<int, 2>{}, g + 2);
+        if constexpr (kStages == 3)
+            if (g + 2 < g_total) step(std::integral_constant<int, 2 % kStages>{}, g + 2);
     }
 }
 
