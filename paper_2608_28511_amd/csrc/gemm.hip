@@ -11,17 +11,23 @@
 //   KGRP mode   C_e[m, n] = sum_{r in segment e} A[r, m] * B[r, n]  (wgrad:
 //               the contraction runs over the expert's ragged rows).
 //
-// Block tile BM x BN x BK = 128 x 256 x 64 on 512 threads: 8 wavefronts in a
-// 2 x 4 grid, 64 x 64 outputs each (4 x 4 v_mfma_f32_16x16x32_bf16 per
-// 32-wide k step).  One workgroup fills a CU's LDS, so each SIMD runs two
-// wavefronts: one wave's address arithmetic, barrier and LDS latency overlap
-// the other's MFMAs.
+// Two block tiles, chosen per launch (Tile below), on 512 threads: 8
+// wavefronts in a 2 x 4 grid, each (BM/2) x 64 outputs (v_mfma_f32_16x16x32_bf16):
+//   128 x 256, 64 k per stage, 3-stage ring of 48 KB stages;
+//   256 x 256, 32 k per stage, 4-stage ring of 32 KB stages -- one third
+//   fewer operand bytes per product, for launches long enough that the
+//   coarser tile count does not leave the last round of CUs half idle.
+// The operand copies into LDS, not the MFMAs, bound the 128-row tile (the
+// per-CU texture-data return path measured 82% busy at 0.42 of the MFMA
+// rate); the 256-row tile moves a third less per flop.  One workgroup fills
+// a CU's LDS, so each SIMD runs two wavefronts: one wave's address
+// arithmetic, barrier and LDS latency overlap the other's MFMAs.
 //
 // Operands never pass through registers on their way to LDS: every 16-byte
-// chunk is copied by global_load_lds_dwordx4 into a 3-stage LDS ring (48 KB
-// per stage), two stages in flight while the third is consumed.  Each
-// operand keeps the layout it has in HBM:
-//   K-contiguous source  -> LDS rows of 64 k (8 chunks, XOR-swizzled by row),
+// chunk is copied by a buffer load with an LDS destination into the LDS
+// ring, all but one stage in flight while one is consumed.  Each operand
+// keeps the layout it has in HBM:
+//   K-contiguous source  -> LDS rows of 64 or 32 k (XOR-swizzled by row),
 //                           MFMA fragments read with ds_read_b128;
 //   M/N-contiguous source (weights stored [D, F] / [F, D], both wgrad
 //                           operands) -> LDS k-rows of BM or BN elements
@@ -48,9 +54,9 @@
 // multiplies by the activation derivative reads the saved pre-activation
 // directly.
 //
-// Expert segments are located through a device-side tile table (expert,
-// first row, end row of every 128-row tile, built from the routing offsets
-// on the device): no host reads the routing counts.  Work item w of the
+// Expert segments are located through device-side tile tables (expert,
+// first row, end row of every 128-row and every 256-row tile, built from the
+// routing offsets on the device): no host reads the routing counts.  Work item w of the
 // grid-wide order is tile (m, n) of an ordering that takes 8 m-tiles at a
 // time across all n-tiles, and the items a round of workgroups processes
 // together on one XCD are consecutive, so they share A rows and expert
@@ -64,17 +70,28 @@
 
 namespace moe {
 
-constexpr int BM = 128, BN = 256;
-constexpr int MI = BM / 32;                     // A fragments (16 rows) per wave: waves cover BM/2 rows
+constexpr int BN = 256;
 constexpr int kGemmThreads = kWaves * 64;
-constexpr int kStages = 3;
-constexpr int kABytes = BM * BK * 2;            // 16 KB
-constexpr int kBBytes = BN * BK * 2;            // 32 KB
-constexpr int kStageBytes = kABytes + kBBytes;  // 48 KB
-constexpr int kRingBytes = kStages * kStageBytes;  // 144 KB
 constexpr int kEpiWaveBytes = 16 * 64 * 2;      // 16 x 64 bf16 staging block per wave
 constexpr int kEpiBytes = kWaves * kEpiWaveBytes;  // 16 KB
 constexpr int kGroupM = 8;
+
+// Block tile BM x BN with KD contraction elements per ring stage and a ring
+// of STAGES stages.
+template <int BM_, int KD_, int STAGES_>
+struct Tile {
+    static constexpr int BM = BM_, KD = KD_, kStages = STAGES_;
+    static constexpr int MI = BM / 32;          // A fragments (16 rows) per wave: waves cover BM/2 rows
+    static constexpr int kKK = KD / 32;         // MFMA k steps per stage
+    static constexpr int kABytes = BM * KD * 2, kBBytes = BN * KD * 2;
+    static constexpr int kStageBytes = kABytes + kBBytes;
+    static constexpr int kRingBytes = kStages * kStageBytes;
+    static constexpr int kFrag = 16 * KD * 2;   // bytes between 16-row fragments of the row layout
+};
+using TileS = Tile<128, 64, 3>;   // 144 KB ring (+16 KB epilogue staging)
+using TileL = Tile<256, 32, 4>;   // 128 KB ring
+static_assert(TileS::kRingBytes + kEpiBytes <= 160 * 1024 && TileL::kRingBytes + kEpiBytes <= 160 * 1024,
+              "LDS budget");
 
 struct GemmArgs {
     const uint16_t* A;
@@ -83,7 +100,7 @@ struct GemmArgs {
     const uint16_t* aux_in;   // EPI_DRELU2: pre-activation u, same layout as C
     uint16_t* aux_out;        // EPI_RELU2: pre-activation u (may be null)
     const int32_t* offsets;   // [E+1] expert row segments (KGRP mode)
-    const int4* tiles;        // ROWS mode: per 128-row tile {expert, row0, row_end, 0}; null = dense
+    const int4* tiles;        // ROWS mode: per BM-row tile {expert, row0, row_end, 0}; null = dense
     const int32_t* mtile_total;  // ROWS mode with tiles: device count of valid m-tiles
     int64_t lda, ldb, ldc;
     int64_t b_stride;         // elements between experts' B (ROWS mode)
@@ -96,64 +113,82 @@ struct GemmArgs {
     int accumulate;           // EPI_F32: C += product instead of C = product
 };
 
-// One BK-wide stage of the main loop for stage slot S of the ring: read the
-// fragments of both 32-wide k steps, send the next-but-one stage's copies out
-// between the two MFMA blocks, and accumulate.  `next` says whether there is
-// a stage to copy; nrem is the contraction length left from its start.
-template <bool A_K, bool B_K, bool KTAIL, int S, class DA, class DB, int NA, int NB>
-__device__ __forceinline__ void mma_stage(f32x4 (&acc)[MI][4], const uint32_t (&abase)[NA],
+// Wait until stage `cur` of `total` has landed when stages cur + 1 ..
+// cur + T::kStages - 2 (those that exist) may still be in flight: copies
+// complete in order, so at most that many stages' worth may be outstanding.
+template <class T, int kPerStage>
+__device__ __forceinline__ void wait_stage(int cur, int total) {
+    const int ahead = total - 1 - cur;
+    if constexpr (T::kStages >= 4) {
+        if (ahead >= 2) { wait_vmcnt<2 * kPerStage>(); return; }
+    }
+    if constexpr (T::kStages >= 3) {
+        if (ahead >= 1) { wait_vmcnt<kPerStage>(); return; }
+    }
+    wait_vmcnt<0>();
+}
+
+// One KD-wide stage of the main loop for stage slot S of the ring: read the
+// fragments of each 32-wide k step, send the copies of the stage kStages - 1
+// ahead (half of B after the second k step's reads when a stage has two),
+// and accumulate.  `next` says whether there is a stage to copy; nrem is the
+// contraction length left from its start.
+template <class T, bool A_K, bool B_K, bool KTAIL, int S, class DA, class DB, int NA, int NB>
+__device__ __forceinline__ void mma_stage(f32x4 (&acc)[T::MI][4], const uint32_t (&abase)[NA],
                                           const uint32_t (&bbase)[2][NB], DA& da, DB& db, bool next,
                                           int64_t nrem, uint32_t ldsA, uint32_t ldsB, int wave) {
-    constexpr int NS = (S + kStages - 1) % kStages;
+    constexpr int NS = (S + T::kStages - 1) % T::kStages;
     constexpr int kSA = DA::kSlots, kSB = DB::kSlots;
 #pragma unroll
-    for (int kk = 0; kk < BK / 32; ++kk) {
-        bf16x8 af[MI], bfg[4];
+    for (int kk = 0; kk < T::kKK; ++kk) {
+        bf16x8 af[T::MI], bfg[4];
 #pragma unroll
-        for (int i = 0; i < MI; ++i) {
-            if constexpr (A_K) af[i] = lds_b128(abase[kk] + S * kABytes + i * 2048);
-            else af[i] = lds_tr_pair(abase[i] + S * kABytes + kk * 64 * BM, 8 * BM);
+        for (int i = 0; i < T::MI; ++i) {
+            if constexpr (A_K) af[i] = lds_b128(abase[kk] + S * T::kABytes + i * T::kFrag);
+            else af[i] = lds_tr_pair(abase[i] + S * T::kABytes + kk * 64 * T::BM, 8 * T::BM);
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            constexpr uint32_t so = (S & 1) * kBBytes;
-            if constexpr (B_K) bfg[j] = lds_b128(bbase[S >> 1][kk] + so + j * 2048);
+            constexpr uint32_t so = (S & 1) * T::kBBytes;
+            if constexpr (B_K) bfg[j] = lds_b128(bbase[S >> 1][kk] + so + j * T::kFrag);
             else bfg[j] = lds_tr_pair(bbase[S >> 1][j] + so + kk * 64 * BN, 8 * BN);
         }
         if (next) {
-            if (kk == 0) {
-                da.template issue<KTAIL, 0, kSA>(ldsA + NS * kABytes, nrem, wave);
-                db.template issue<KTAIL, 0, kSB / 2>(ldsB + NS * kBBytes, nrem, wave);
+            if (T::kKK == 1) {
+                da.template issue<KTAIL, 0, kSA>(ldsA + NS * T::kABytes, nrem, wave);
+                db.template issue<KTAIL, 0, kSB>(ldsB + NS * T::kBBytes, nrem, wave);
+            } else if (kk == 0) {
+                da.template issue<KTAIL, 0, kSA>(ldsA + NS * T::kABytes, nrem, wave);
+                db.template issue<KTAIL, 0, kSB / 2>(ldsB + NS * T::kBBytes, nrem, wave);
             } else {
-                db.template issue<KTAIL, kSB / 2, kSB>(ldsB + NS * kBBytes, nrem, wave);
+                db.template issue<KTAIL, kSB / 2, kSB>(ldsB + NS * T::kBBytes, nrem, wave);
             }
         }
 #pragma unroll
-        for (int i = 0; i < MI; ++i)
+        for (int i = 0; i < T::MI; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfg[j], af[i], acc[i][j], 0, 0, 0);
-        // keep the two k halves' fragment sets from being live at once (the
-        // other wave on the SIMD covers the second half's read latency)
-        if constexpr (MI > 4) __builtin_amdgcn_sched_barrier(0);
     }
 }
 
 // Per-lane fragment bases of the A (BM-wide) and B (BN-wide) operands.
-template <bool A_K, bool B_K, int NA, int NB>
+template <class T, bool A_K, bool B_K, int NA, int NB>
 __device__ __forceinline__ void frag_bases(uint32_t (&abase)[NA], uint32_t (&bbase)[2][NB], uint32_t ldsA,
                                            uint32_t ldsB, int wm, int wn, int lane) {
 #pragma unroll
     for (int i = 0; i < NA; ++i)
-        abase[i] = ldsA + (A_K ? row_base(wm * (BM / 2), i, lane) : col_base<BM>(wm * (BM / 2) + i * 16, lane));
+        abase[i] = ldsA + (A_K ? row_base<T::KD>(wm * (T::BM / 2), i, lane)
+                               : col_base<T::BM>(wm * (T::BM / 2) + i * 16, lane));
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-        const uint32_t o = B_K ? row_base(wn * 64, j, lane) : col_base<BN>(wn * 64 + j * 16, lane);
-        bbase[0][j] = ldsB + o;          // stages 0 and 1
-        bbase[1][j] = ldsB + 2 * kBBytes + o;  // stage 2 of a 3-stage ring (immediate offsets reach 64 KB)
+        const uint32_t o = B_K ? row_base<T::KD>(wn * 64, j, lane) : col_base<BN>(wn * 64 + j * 16, lane);
+        bbase[0][j] = ldsB + o;                    // stages 0 and 1
+        bbase[1][j] = ldsB + 2 * T::kBBytes + o;   // stages 2 and 3 (immediate offsets reach 64 KB)
     }
 }
 
+template <int MI>
 __device__ __forceinline__ void zero_acc(f32x4 (&acc)[MI][4]) {
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -161,11 +196,24 @@ __device__ __forceinline__ void zero_acc(f32x4 (&acc)[MI][4]) {
         for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
+// Calls step(integral_constant<S>, g) for g = g0 .. g0 + kStages - 1 (those
+// below total), S the ring slot of step g.
+template <int kStages, class F>
+__device__ __forceinline__ void ring_round(F&& step, int g0, int total) {
+    step(std::integral_constant<int, 0>{}, g0);
+    if (g0 + 1 < total) step(std::integral_constant<int, 1 % kStages>{}, g0 + 1);
+    if constexpr (kStages >= 3)
+        if (g0 + 2 < total) step(std::integral_constant<int, 2 % kStages>{}, g0 + 2);
+    if constexpr (kStages >= 4)
+        if (g0 + 3 < total) step(std::integral_constant<int, 3 % kStages>{}, g0 + 3);
+}
+
 // ---------------------------------------------------------------------------
 // KGRP mode (wgrad): C_e[m, n] = sum over expert e's rows r of A[r, m] B[r, n],
 // fp32 output.  One workgroup per (expert, m-tile, n-tile).
+template <class T>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) {
-    __shared__ __attribute__((aligned(1024))) char smem[kRingBytes];  // 144 KB
+    __shared__ __attribute__((aligned(1024))) char smem[T::kRingBytes];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar LDS offsets
@@ -176,8 +224,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) 
     const int e = lid / per;
     const int in = lid - e * per;
     const int mt = in % p.m_tiles, nt = in / p.m_tiles;
-    const int64_t row0 = (int64_t)mt * BM;
-    const int64_t row_hi = (row0 + BM) < p.M ? (row0 + BM) : p.M;
+    const int64_t row0 = (int64_t)mt * T::BM;
+    const int64_t row_hi = (row0 + T::BM) < p.M ? (row0 + T::BM) : p.M;
     int64_t k_begin = p.offsets != nullptr ? (int64_t)p.offsets[e] : (int64_t)e * p.kchunk;
     int64_t k_end = p.offsets != nullptr ? (int64_t)p.offsets[e + 1] : k_begin + p.kchunk;
     k_begin = k_begin < 0 ? 0 : (k_begin > p.R ? p.R : k_begin);
@@ -185,50 +233,45 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) 
     const int64_t n0 = (int64_t)nt * BN;
 
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char*)smem;
-    const uint32_t ldsB = lds0, ldsA = lds0 + kStages * kBBytes;
+    const uint32_t ldsB = lds0, ldsA = lds0 + T::kStages * T::kBBytes;
 
-    DmaTile<false, BM> da;
-    DmaTile<false, BN> db;
+    DmaTile<false, T::BM, T::KD> da;
+    DmaTile<false, BN, T::KD> db;
     da.init(p.A, p.lda, row0, row_hi, k_begin, k_end, wave, lane);
     db.init(p.B, p.ldb, n0, (int64_t)p.N, k_begin, k_end, wave, lane);
-    constexpr int kPerStage = DmaTile<false, BM>::kSlots + DmaTile<false, BN>::kSlots;
+    constexpr int kSA = DmaTile<false, T::BM, T::KD>::kSlots, kSB = DmaTile<false, BN, T::KD>::kSlots;
+    constexpr int kPerStage = kSA + kSB;
 
-    uint32_t abase[MI], bbase[2][4];
-    frag_bases<false, false>(abase, bbase, ldsA, ldsB, wm, wn, lane);
+    uint32_t abase[T::MI], bbase[2][4];
+    frag_bases<T, false, false>(abase, bbase, ldsA, ldsB, wm, wn, lane);
 
-    f32x4 acc[MI][4];
+    f32x4 acc[T::MI][4];
     zero_acc(acc);
 
     const int64_t klen = k_end - k_begin;
-    const int nk = (int)((klen + BK - 1) / BK);
+    const int nk = (int)((klen + T::KD - 1) / T::KD);
 
     auto step = [&](auto stage_c, int kt) {
         constexpr int S = decltype(stage_c)::value;
-        // stages kt .. kt + kStages - 2 are in flight; stage kt must have landed
-        if (kStages == 3 && kt + 1 < nk) wait_vmcnt<kPerStage>(); else wait_vmcnt<0>();
+        wait_stage<T, kPerStage>(kt, nk);
         stage_barrier();
-        mma_stage<false, false, true, S>(acc, abase, bbase, da, db, kt + kStages - 1 < nk,
-                                         klen - (int64_t)(kt + kStages - 1) * BK, ldsA, ldsB, wave);
+        mma_stage<T, false, false, true, S>(acc, abase, bbase, da, db, kt + T::kStages - 1 < nk,
+                                            klen - (int64_t)(kt + T::kStages - 1) * T::KD, ldsA, ldsB, wave);
     };
 
     if (nk > 0) {
-        for (int q = 0; q < kStages - 1 && q < nk; ++q) {
-            da.template issue<true, 0, DmaTile<false, BM>::kSlots>(ldsA + q * kABytes, klen - (int64_t)q * BK, wave);
-            db.template issue<true, 0, DmaTile<false, BN>::kSlots>(ldsB + q * kBBytes, klen - (int64_t)q * BK, wave);
+        for (int q = 0; q < T::kStages - 1 && q < nk; ++q) {
+            da.template issue<true, 0, kSA>(ldsA + q * T::kABytes, klen - (int64_t)q * T::KD, wave);
+            db.template issue<true, 0, kSB>(ldsB + q * T::kBBytes, klen - (int64_t)q * T::KD, wave);
         }
-        for (int kt = 0; kt < nk; kt += kStages) {
-            step(std::integral_constant<int, 0>{}, kt);
-            if (kt + 1 < nk) step(std::integral_constant<int, 1>{}, kt + 1);
-            if constexpr (kStages == 3)
-                if (kt + 2 < nk) step(std::integral_constant<int, 2 % kStages>{}, kt + 2);
-        }
+        for (int kt = 0; kt < nk; kt += T::kStages) ring_round<T::kStages>(step, kt, nk);
     }
 
     // lane holds C[m][n .. n+3] for each (i, j)
     const int64_t c_base = (int64_t)e * p.c_stride;
 #pragma unroll
-    for (int i = 0; i < MI; ++i) {
-        const int64_t m = row0 + wm * (BM / 2) + i * 16 + (lane & 15);
+    for (int i = 0; i < T::MI; ++i) {
+        const int64_t m = row0 + wm * (T::BM / 2) + i * 16 + (lane & 15);
         if (m >= row_hi) continue;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -247,7 +290,7 @@ struct RowsTile {
     int e, row0, row_hi, n0;  // rows and columns are below 2^31
 };
 
-// Work item w -> output tile: 8 m-tiles at a time across all n-tiles.
+template <int BM>
 __device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, int m_total, int w) {
     const int width = kGroupM * p.n_tiles;
     const int group = w / width;
@@ -296,7 +339,7 @@ constexpr uint32_t kDropOffset = 0x80000000u;  // beyond any descriptor's range
 // r at c ^ (r & 7)), come back as 16-byte row pieces and leave as two
 // buffer_store_dwordx4 of 8 rows x 128 bytes each.  OUT: 0 = the product
 // (squared-ReLU applied for EPI_RELU2), 1 = the raw product (pre-activation).
-template <int EPI, int OUT>
+template <int EPI, int OUT, int MI>
 __device__ __forceinline__ void staged_store(const f32x4 (&acc)[MI][4], void* C, int64_t ldc, int N,
                                              int64_t rbase, int64_t nrows, int64_t cbase,
                                              uint32_t ep, int lane) {
@@ -336,6 +379,7 @@ __device__ __forceinline__ void staged_store(const f32x4 (&acc)[MI][4], void* C,
 // its barrier, before that step's operand copies), so they have long
 // completed when drelu2_store uses them: its waits never reach the copies
 // in flight at the tile's end.
+template <int MI>
 __device__ __forceinline__ void drelu2_load(u32x2 (&uu)[MI][4], const uint16_t* aux_in, int64_t ldc, int N,
                                             int64_t rbase, int64_t nrows, int64_t cbase, int lane) {
     const __amdgpu_buffer_rsrc_t ru = rows_rsrc(aux_in, rbase, nrows, ldc);
@@ -351,6 +395,7 @@ __device__ __forceinline__ void drelu2_load(u32x2 (&uu)[MI][4], const uint16_t* 
     }
 }
 
+template <int MI>
 __device__ __forceinline__ void drelu2_store(const f32x4 (&acc)[MI][4], const u32x2 (&uu)[MI][4], void* C,
                                              int64_t ldc, int N, int64_t rbase, int64_t nrows, int64_t cbase,
                                              int lane) {
@@ -378,10 +423,11 @@ __device__ __forceinline__ void drelu2_store(const f32x4 (&acc)[MI][4], const u3
 // consecutive columns of one row, stored as one 16-byte buffer store (with
 // `accumulate`, added to what C holds there).  The descriptor spans only this
 // wave's rows, so rows past the tile and columns past N are dropped.
+template <int MI>
 __device__ __forceinline__ void f32_store(const f32x4 (&acc)[MI][4], float* C, int64_t ldc, int N,
                                           int64_t rbase, int64_t nrows, int64_t cbase, bool accumulate,
                                           int lane) {
-    const int64_t rows = nrows < BM / 2 ? nrows : BM / 2;
+    const int64_t rows = nrows < MI * 16 ? nrows : MI * 16;
     const int32_t bytes = rows > 0 ? (int32_t)(rows * ldc * 4) : 0;
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)(C + rbase * ldc), 0, bytes,
                                                                         0x00020000);
@@ -411,9 +457,10 @@ __device__ __forceinline__ void f32_store(const f32x4 (&acc)[MI][4], float* C, i
 // (expert segments from the tile table, or all M rows when it is null).
 // A is K-contiguous (ROW layout); B is N-contiguous (B_K false: weights stored
 // [Kd, N]) or K-contiguous (B_K true: transposed weights of the dgrads).
-template <bool B_K, int EPI, bool KTAIL>
+template <class T, bool B_K, int EPI, bool KTAIL>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) {
-    __shared__ __attribute__((aligned(1024))) char smem[kRingBytes + kEpiBytes];  // 160 KB
+    __shared__ __attribute__((aligned(1024))) char smem[T::kRingBytes + kEpiBytes];
+    constexpr int BM = T::BM, MI = T::MI, KD = T::KD, kStages = T::kStages;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -428,27 +475,27 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     const int G = gridDim.x;
     const int first = (int)(blockIdx.x % kXcds) * (G / kXcds) + (int)(blockIdx.x / kXcds);
     const int n_mine = first < n_work ? (n_work - first + G - 1) / G : 0;
-    const int nk = (p.Kd + BK - 1) / BK;
+    const int nk = (p.Kd + KD - 1) / KD;
     const int g_total = n_mine * nk;  // (tile, k step) pairs
     if (g_total == 0) return;
 
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char*)smem;
-    const uint32_t ldsB = lds0, ldsA = lds0 + kStages * kBBytes;
-    const uint32_t ep = lds0 + kRingBytes + (uint32_t)wave * kEpiWaveBytes;
+    const uint32_t ldsB = lds0, ldsA = lds0 + kStages * T::kBBytes;
+    const uint32_t ep = lds0 + T::kRingBytes + (uint32_t)wave * kEpiWaveBytes;
 
-    DmaTile<true, BM> da;
-    DmaTile<B_K, BN> db;
-    constexpr int kSA = DmaTile<true, BM>::kSlots, kSB = DmaTile<B_K, BN>::kSlots;
+    DmaTile<true, BM, KD> da;
+    DmaTile<B_K, BN, KD> db;
+    constexpr int kSA = DmaTile<true, BM, KD>::kSlots, kSB = DmaTile<B_K, BN, KD>::kSlots;
     constexpr int kPerStage = kSA + kSB;
     auto dma_tile = [&](int j) {
-        const RowsTile t = rows_tile(p, m_total, first + j * G);
+        const RowsTile t = rows_tile<BM>(p, m_total, first + j * G);
         da.init(p.A, p.lda, t.row0, t.row_hi, 0, p.Kd, wave, lane);
         db.init(p.B + (int64_t)t.e * p.b_stride, p.ldb, t.n0, (int64_t)p.N, 0, p.Kd, wave, lane);
     };
 
-    constexpr int kNB = B_K ? 2 : 4;
-    uint32_t abase[2], bbase[2][kNB];
-    frag_bases<true, B_K>(abase, bbase, ldsA, ldsB, wm, wn, lane);
+    constexpr int kNB = B_K ? T::kKK : 4;
+    uint32_t abase[T::kKK], bbase[2][kNB];
+    frag_bases<T, true, B_K>(abase, bbase, ldsA, ldsB, wm, wn, lane);
 
     f32x4 acc[MI][4];
     zero_acc(acc);
@@ -457,15 +504,15 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     int kd = 0, jd = 0;
     for (int q = 0; q < kStages - 1 && q < g_total; ++q) {
         if (kd == 0) dma_tile(jd);
-        const int rem = p.Kd - kd * BK;
-        da.template issue<KTAIL, 0, kSA>(ldsA + q * kABytes, rem, wave);
-        db.template issue<KTAIL, 0, kSB>(ldsB + q * kBBytes, rem, wave);
+        const int rem = p.Kd - kd * KD;
+        da.template issue<KTAIL, 0, kSA>(ldsA + q * T::kABytes, rem, wave);
+        db.template issue<KTAIL, 0, kSB>(ldsB + q * T::kBBytes, rem, wave);
         if (++kd == nk) { kd = 0; ++jd; }
     }
 
     int kc = 0;   // k step of the tile being computed
     int jc = 0;   // its index in this workgroup's list
-    RowsTile cur = rows_tile(p, m_total, first);
+    RowsTile cur = rows_tile<BM>(p, m_total, first);
     u32x2 uu[MI][4];   // dgrad: the tile's pre-activations
 
     auto step = [&](auto stage_c, int g) {
@@ -474,7 +521,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
         // landed.  Stores of an epilogue may still be in flight; they are
         // not counted, so the wait covers this stage's copies whichever way
         // they complete (loads complete in order among themselves).
-        if (kStages == 3 && g + 1 < g_total) wait_vmcnt<kPerStage>(); else wait_vmcnt<0>();
+        wait_stage<T, kPerStage>(g, g_total);
         stage_barrier();
         if constexpr (EPI == EPI_DRELU2 && MI <= 4)   // with taller tiles: loaded in the epilogue
             if (kc == 0)
@@ -482,7 +529,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
                             cur.row_hi - (cur.row0 + wm * (BM / 2)), cur.n0 + wn * 64, lane);
         const bool next = g + kStages - 1 < g_total;
         if (next && kd == 0) dma_tile(jd);
-        mma_stage<true, B_K, KTAIL, S>(acc, abase, bbase, da, db, next, p.Kd - kd * BK, ldsA, ldsB, wave);
+        mma_stage<T, true, B_K, KTAIL, S>(acc, abase, bbase, da, db, next, p.Kd - kd * KD, ldsA, ldsB, wave);
         if (++kd == nk) { kd = 0; ++jd; }
         if (kc == nk - 1) {
             const int rbase = cur.row0 + wm * (BM / 2);
@@ -494,37 +541,66 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
             } else if constexpr (EPI == EPI_F32) {
                 f32_store(acc, (float*)p.C, p.ldc, p.N, rbase, nrows, cbase, p.accumulate != 0, lane);
             } else {
-                staged_store<EPI, 0>(acc, p.C, p.ldc, p.N, rbase, nrows, cbase, ep, lane);
+                staged_store<EPI, 0, MI>(acc, p.C, p.ldc, p.N, rbase, nrows, cbase, ep, lane);
                 if constexpr (EPI == EPI_RELU2)
                     if (p.aux_out != nullptr)
-                        staged_store<EPI, 1>(acc, p.aux_out, p.ldc, p.N, rbase, nrows, cbase, ep, lane);
+                        staged_store<EPI, 1, MI>(acc, p.aux_out, p.ldc, p.N, rbase, nrows, cbase, ep, lane);
             }
             zero_acc(acc);
             kc = 0;
             ++jc;
-            if (jc < n_mine) cur = rows_tile(p, m_total, first + jc * G);
+            if (jc < n_mine) cur = rows_tile<BM>(p, m_total, first + jc * G);
         } else {
             ++kc;
         }
     };
 
-    for (int g = 0; g < g_total; g += kStages) {
-        step(std::integral_constant<int, 0>{}, g);
-        if (g + 1 < g_total) step(std::integral_constant<int, 1>{}, g + 1);
-        if constexpr (kStages == 3)
-            if (g + 2 < g_total) step(std::integral_constant<int, 2 % kStages>{}, g + 2);
-    }
+    for (int g = 0; g < g_total; g += kStages) ring_round<kStages>(step, g, g_total);
 }
 
-// Device-side tile schedule of the grouped GEMM for expert segments
-// offsets[0..E] (clamped to [0, R)):
+// Device-side tile schedules of the grouped GEMM for expert segments
+// offsets[0..E] (clamped to [0, R)), one per tile height BM in {128, 256}:
 //   mtile_start[0] = 0, mtile_start[e+1] = sum_{e' <= e} ceil(count[e'] / BM)
-//   tiles[mt] = {e, row0, row_end, 0} for every 128-row tile mt of expert e,
+//   tiles[mt] = {e, row0, row_end, 0} for every BM-row tile mt of expert e,
 //               {-1, 0, 0, 0} for mt in [total, max_tiles) (the static grid bound).
-__global__ __launch_bounds__(1024) void tile_schedule_kernel(const int32_t* __restrict__ offsets, int E,
-                                                              int R, int max_tiles,
-                                                              int32_t* __restrict__ mtile_start,
-                                                              int4* __restrict__ tiles) {
+struct SchedPart {
+    int32_t* mtile_start;
+    int4* tiles;
+    int max_tiles;
+};
+
+__device__ void fill_schedule(const int32_t* seg_lo, const int32_t* seg_hi, int32_t* s, int E, int BMr,
+                              const SchedPart& sp, int tid) {
+    s[tid] = (seg_hi[tid] - seg_lo[tid] + BMr - 1) / BMr;
+    __syncthreads();
+    for (int d = 1; d < 1024; d <<= 1) {
+        const int add = tid >= d ? s[tid - d] : 0;
+        __syncthreads();
+        s[tid] += add;
+        __syncthreads();
+    }
+    if (tid < E) sp.mtile_start[tid + 1] = s[tid];
+    if (tid == 0) sp.mtile_start[0] = 0;
+    const int total = s[E - 1];
+    for (int mt = tid; mt < sp.max_tiles; mt += 1024) {
+        int4 v = make_int4(-1, 0, 0, 0);
+        if (mt < total) {
+            int a = 0, b = E - 1;  // first e with s[e] > mt
+            while (a < b) {
+                const int m = (a + b) >> 1;
+                if (s[m] > mt) b = m; else a = m + 1;
+            }
+            const int row0 = seg_lo[a] + (mt - (a ? s[a - 1] : 0)) * BMr;
+            const int row_end = row0 + BMr < seg_hi[a] ? row0 + BMr : seg_hi[a];
+            v = make_int4(a, row0, row_end, 0);
+        }
+        sp.tiles[mt] = v;
+    }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(1024) void tile_schedule_kernel(const int32_t* __restrict__ offsets, int E, int R,
+                                                              SchedPart small, SchedPart large) {
     __shared__ int32_t s[1024];
     __shared__ int32_t seg_lo[1024], seg_hi[1024];
     const int tid = threadIdx.x;
@@ -537,46 +613,33 @@ __global__ __launch_bounds__(1024) void tile_schedule_kernel(const int32_t* __re
     }
     seg_lo[tid] = lo;
     seg_hi[tid] = hi;
-    s[tid] = (hi - lo + BM - 1) / BM;
-    __syncthreads();
-    for (int d = 1; d < 1024; d <<= 1) {
-        const int add = tid >= d ? s[tid - d] : 0;
-        __syncthreads();
-        s[tid] += add;
-        __syncthreads();
-    }
-    if (tid < E) mtile_start[tid + 1] = s[tid];
-    if (tid == 0) mtile_start[0] = 0;
-    const int total = s[E - 1];
-    for (int mt = tid; mt < max_tiles; mt += 1024) {
-        int4 v = make_int4(-1, 0, 0, 0);
-        if (mt < total) {
-            int a = 0, b = E - 1;  // first e with s[e] > mt
-            while (a < b) {
-                const int m = (a + b) >> 1;
-                if (s[m] > mt) b = m; else a = m + 1;
-            }
-            const int row0 = seg_lo[a] + (mt - (a ? s[a - 1] : 0)) * BM;
-            const int row_end = row0 + BM < seg_hi[a] ? row0 + BM : seg_hi[a];
-            v = make_int4(a, row0, row_end, 0);
-        }
-        tiles[mt] = v;
-    }
+    fill_schedule(seg_lo, seg_hi, s, E, TileS::BM, small, tid);
+    fill_schedule(seg_lo, seg_hi, s, E, TileL::BM, large, tid);
 }
 
-int gemm_tile_m() { return BM; }
+int gemm_tile_m() { return TileS::BM; }
 
-static int64_t mtiles_bound(int64_t R, int E) {
+static int64_t mtiles_bound(int64_t R, int E, int BMr) {
     // sum_e ceil(c_e / BM) <= ceil(R / BM) + (number of non-empty experts)
     const int64_t nonempty = R < E ? R : E;
-    return (R + BM - 1) / BM + nonempty;
+    return (R + BMr - 1) / BMr + nonempty;
 }
 
-// Schedule buffer: mtile_start [E+1] int32, then (16-byte aligned) the tile table.
+// Schedule buffer: for 128-row then 256-row tiles, mtile_start [E+1] int32
+// then (16-byte aligned) the tile table; each part 256-byte aligned.
 static size_t sched_table_offset(int E) { return (size_t)((E + 1) * 4 + 15) / 16 * 16; }
+static size_t sched_part_bytes(int E, int64_t R, int BMr) {
+    return (sched_table_offset(E) + (size_t)mtiles_bound(R, E, BMr) * 16 + 255) / 256 * 256;
+}
 
 size_t gemm_schedule_bytes(int E, int64_t R) {
-    return (sched_table_offset(E) + (size_t)mtiles_bound(R, E) * 16 + 255) / 256 * 256;
+    return sched_part_bytes(E, R, TileS::BM) + sched_part_bytes(E, R, TileL::BM);
+}
+
+static SchedPart sched_part(void* sched, int E, int64_t R, bool large) {
+    char* base = (char*)sched + (large ? sched_part_bytes(E, R, TileS::BM) : 0);
+    return SchedPart{(int32_t*)base, (int4*)(base + sched_table_offset(E)),
+                     (int)mtiles_bound(R, E, large ? TileL::BM : TileS::BM)};
 }
 
 // Compute units of the current device, read once per device.
@@ -594,27 +657,47 @@ static int cu_count() {
     return cus[dev];
 }
 
-template <bool B_K, int EPI>
+// The persistent grid: one workgroup per CU (a multiple of the XCD count).
+static int64_t persistent_grid() {
+    int64_t G = (cu_count() / kXcds) * kXcds;
+    return G < kXcds ? kXcds : G;
+}
+
+// Tall tiles only when the launch holds at least this many rounds of them.
+constexpr int64_t kMinRoundsLarge = 6;
+
+template <class T, bool B_K, int EPI>
 static hipError_t launch_rows(const GemmArgs& a, hipStream_t st) {
-    // one workgroup per CU (a multiple of the XCD count), never more than the
-    // static bound on the number of output tiles
+    // never more workgroups than the static bound on the number of output tiles
     const int64_t bound = (int64_t)a.m_tiles * a.n_tiles;
     if (bound <= 0) return hipSuccess;
-    int64_t G = (cu_count() / kXcds) * kXcds;
-    if (G < kXcds) G = kXcds;
+    int64_t G = persistent_grid();
     const int64_t need = (bound + kXcds - 1) / kXcds * kXcds;
     if (need < G) G = need;
-    if (a.Kd % BK != 0)
-        hipLaunchKernelGGL((gemm_rows_kernel<B_K, EPI, true>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
+    if (a.Kd % T::KD != 0)
+        hipLaunchKernelGGL((gemm_rows_kernel<T, B_K, EPI, true>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
     else
-        hipLaunchKernelGGL((gemm_rows_kernel<B_K, EPI, false>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
+        hipLaunchKernelGGL((gemm_rows_kernel<T, B_K, EPI, false>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
     return hipGetLastError();
 }
 
+template <class T>
+static hipError_t launch_rows_epi(const GemmArgs& a, bool b_kmajor, int epi, hipStream_t st) {
+    if (!b_kmajor) {
+        if (epi == EPI_BF16) return launch_rows<T, false, EPI_BF16>(a, st);
+        if (epi == EPI_RELU2) return launch_rows<T, false, EPI_RELU2>(a, st);
+        if (epi == EPI_F32) return launch_rows<T, false, EPI_F32>(a, st);
+    } else {
+        if (epi == EPI_BF16) return launch_rows<T, true, EPI_BF16>(a, st);
+        if (epi == EPI_DRELU2) return launch_rows<T, true, EPI_DRELU2>(a, st);
+        if (epi == EPI_F32) return launch_rows<T, true, EPI_F32>(a, st);
+    }
+    return hipErrorInvalidValue;
+}
+
 hipError_t launch_tile_schedule(const int32_t* offsets, int E, int64_t R, void* sched, hipStream_t st) {
-    const int max_tiles = (int)mtiles_bound(R, E);
-    hipLaunchKernelGGL(tile_schedule_kernel, dim3(1), dim3(1024), 0, st, offsets, E, (int)R, max_tiles,
-                       (int32_t*)sched, (int4*)((char*)sched + sched_table_offset(E)));
+    hipLaunchKernelGGL(tile_schedule_kernel, dim3(1), dim3(1024), 0, st, offsets, E, (int)R,
+                       sched_part(sched, E, R, false), sched_part(sched, E, R, true));
     return hipGetLastError();
 }
 
@@ -622,30 +705,47 @@ hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B
                                int64_t b_stride, bool b_kmajor, void* C, int64_t ldc, int epi,
                                const moe_bf16* aux_in, moe_bf16* aux_out, const void* sched,
                                int E, int64_t R, int N, int Kd, hipStream_t st, bool accumulate) {
-    GemmArgs a{};
-    a.A = A; a.B = B; a.C = C; a.aux_in = aux_in; a.aux_out = aux_out;
-    a.accumulate = accumulate ? 1 : 0;
-    if (sched != nullptr) {
-        a.tiles = (const int4*)((const char*)sched + sched_table_offset(E));
-        a.mtile_total = (const int32_t*)sched + E;  // mtile_start[E]
-    }
-    a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.b_stride = b_stride;
-    a.M = R; a.R = R; a.N = N; a.Kd = Kd; a.E = E;
-    a.n_tiles = (N + BN - 1) / BN;
-    a.m_tiles = (int)(sched ? mtiles_bound(R, E) : (R + BM - 1) / BM);
     if (R == 0) return hipSuccess;
     // the DMA descriptor of an N-contiguous B spans its whole contraction
     if (!b_kmajor && (int64_t)Kd * ldb * 2 >= kMaxDmaBytes) return hipErrorInvalidValue;
-    if (!b_kmajor) {
-        if (epi == EPI_BF16) return launch_rows<false, EPI_BF16>(a, st);
-        if (epi == EPI_RELU2) return launch_rows<false, EPI_RELU2>(a, st);
-        if (epi == EPI_F32) return launch_rows<false, EPI_F32>(a, st);
+    GemmArgs a{};
+    a.A = A; a.B = B; a.C = C; a.aux_in = aux_in; a.aux_out = aux_out;
+    a.accumulate = accumulate ? 1 : 0;
+    a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.b_stride = b_stride;
+    a.M = R; a.R = R; a.N = N; a.Kd = Kd; a.E = E;
+    a.n_tiles = (N + BN - 1) / BN;
+    // tall tiles when the launch is long enough (bound on their count)
+    const int64_t large_tiles =
+        (sched ? mtiles_bound(R, E, TileL::BM) : (R + TileL::BM - 1) / TileL::BM) * a.n_tiles;
+    const bool large = large_tiles >= kMinRoundsLarge * persistent_grid();
+    const int BMr = large ? TileL::BM : TileS::BM;
+    if (sched != nullptr) {
+        const SchedPart sp = sched_part((void*)sched, E, R, large);
+        a.tiles = sp.tiles;
+        a.mtile_total = sp.mtile_start + E;  // mtile_start[E]
+        a.m_tiles = sp.max_tiles;
     } else {
-        if (epi == EPI_BF16) return launch_rows<true, EPI_BF16>(a, st);
-        if (epi == EPI_DRELU2) return launch_rows<true, EPI_DRELU2>(a, st);
-        if (epi == EPI_F32) return launch_rows<true, EPI_F32>(a, st);
+        a.m_tiles = (int)((R + BMr - 1) / BMr);
     }
-    return hipErrorInvalidValue;
+    return large ? launch_rows_epi<TileL>(a, b_kmajor, epi, st) : launch_rows_epi<TileS>(a, b_kmajor, epi, st);
+}
+
+// KGRP launches: tall tiles when there are enough workgroups to fill the
+// device a few times over.
+static hipError_t launch_kgrp(GemmArgs a, int64_t groups, hipStream_t st) {
+    const int64_t nt = (a.N + BN - 1) / BN;
+    const int64_t mt_l = (a.M + TileL::BM - 1) / TileL::BM;
+    const bool large = groups * mt_l * nt >= 2 * persistent_grid();
+    a.m_tiles = (int)(large ? mt_l : (a.M + TileS::BM - 1) / TileS::BM);
+    a.n_tiles = (int)nt;
+    const int64_t n_wg = groups * a.m_tiles * a.n_tiles;
+    if (n_wg <= 0) return hipSuccess;
+    if (n_wg > 0x7fffffff) return hipErrorInvalidConfiguration;
+    if (large)
+        hipLaunchKernelGGL(gemm_kgrp_kernel<TileL>, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a);
+    else
+        hipLaunchKernelGGL(gemm_kgrp_kernel<TileS>, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a);
+    return hipGetLastError();
 }
 
 hipError_t launch_chunked_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb, float* C,
@@ -655,13 +755,8 @@ hipError_t launch_chunked_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* 
     a.A = A; a.B = B; a.C = C; a.offsets = nullptr; a.kchunk = kchunk;
     a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.c_stride = c_stride;
     a.M = M; a.R = R; a.N = N; a.E = nchunk;
-    a.m_tiles = (M + BM - 1) / BM;
-    a.n_tiles = (N + BN - 1) / BN;
-    const int64_t n_wg = (int64_t)nchunk * a.m_tiles * a.n_tiles;
-    if (n_wg <= 0) return hipSuccess;
     if (R * (lda > ldb ? lda : ldb) * 2 >= kMaxDmaBytes) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(gemm_kgrp_kernel, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a);
-    return hipGetLastError();
+    return launch_kgrp(a, nchunk, st);
 }
 
 hipError_t launch_grouped_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
@@ -671,15 +766,9 @@ hipError_t launch_grouped_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* 
     a.A = A; a.B = B; a.C = C; a.offsets = offsets;
     a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.c_stride = c_stride;
     a.M = M; a.R = R; a.N = N; a.E = E;
-    a.m_tiles = (M + BM - 1) / BM;
-    a.n_tiles = (N + BN - 1) / BN;
-    const int64_t n_wg = (int64_t)E * a.m_tiles * a.n_tiles;
-    if (n_wg <= 0) return hipSuccess;
     // DMA descriptors span an expert's rows of both operands
     if (R * (lda > ldb ? lda : ldb) * 2 >= kMaxDmaBytes) return hipErrorInvalidValue;
-    if (n_wg > 0x7fffffff) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(gemm_kgrp_kernel, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a);
-    return hipGetLastError();
+    return launch_kgrp(a, E, st);
 }
 
 }  // namespace moe

@@ -2,11 +2,11 @@
 // logits): the direct global -> LDS copy ring, the LDS operand layouts and
 // their MFMA fragment reads.
 //
-// A workgroup has kWaves = 8 wavefronts and contracts BK = 64 elements per
-// ring stage.  An operand tile lives in LDS in one of two layouts:
-//   row layout  [rows][64 k], from a K-contiguous source, fragments read with
+// A workgroup has kWaves = 8 wavefronts and contracts KD = 64 (default) or 32
+// elements per ring stage.  An operand tile lives in LDS in one of two layouts:
+//   row layout  [rows][KD k], from a K-contiguous source, fragments read with
 //               ds_read_b128;
-//   col layout  [64 k][cols], from an M/N-contiguous source, fragments read
+//   col layout  [KD k][cols], from an M/N-contiguous source, fragments read
 //               with the gfx950 LDS transpose read ds_read_b64_tr_b16.
 #pragma once
 
@@ -33,6 +33,12 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 // measured as a 2-way conflict (LDS bank-conflict counter, 16-row fragment
 // read pattern).
 __device__ __forceinline__ int rswz(int r) { return r & 7; }
+// For 32 k per row (64-byte rows, 4 chunks) the conflict-free swizzle of the
+// same 16-row fragment read is chunk c of row r at c ^ ((r >> 1) & 3): the
+// eight 16-byte reads of rows r .. r+1 and r+8 .. r+9 land in distinct bank
+// groups (measured with the LDS bank-conflict counter).
+template <int KD>
+__device__ __forceinline__ int rswz_k(int r) { return KD == 64 ? (r & 7) : ((r >> 1) & 3); }
 
 // ---- col layout: [64 k][cols], cols/8 chunks per k-row; chunk pairs XOR-swizzled
 // so the 8 rows {k..k+3, k+8..k+11} read together by ds_read_b64_tr_b16 hit
@@ -77,13 +83,12 @@ __device__ __forceinline__ void stage_barrier() {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Wait until at most N vector-memory operations of this wave are in flight
+// (an immediate operand: N < 64).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
-    if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-    else if constexpr (N == 6) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
-    else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else static_assert(N == 0, "unsupported vmcnt");
+    static_assert(N >= 0 && N < 64, "vmcnt out of range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
 // Per-lane DMA slots of one operand tile.  Slot i of a wave covers LDS bytes
@@ -99,10 +104,10 @@ __device__ __forceinline__ void wait_vmcnt() {
 //   a k tile (KTAIL) is cut per chunk at issue time.
 // Col layout (M/N-contiguous source, element (k, c) at src[k*ld + c]): k rows
 //   [k_begin, k_end), columns [x0, x_hi).
-template <bool ROWL, int EXT>
+template <bool ROWL, int EXT, int KD = BK>
 struct DmaTile {
-    static constexpr int kCPR = ROWL ? 8 : EXT / 8;       // chunks per LDS row
-    static constexpr int kSlots = EXT * 8 / 64 / kWaves;  // 1 KB slots per wave
+    static constexpr int kCPR = ROWL ? KD / 8 : EXT / 8;       // chunks per LDS row
+    static constexpr int kSlots = EXT * KD * 2 / 1024 / kWaves;  // 1 KB slots per wave
     i32x4 rs;                // wave-uniform
     uint32_t kstep;          // bytes per k tile, wave-uniform
     uint32_t off[kSlots];
@@ -114,11 +119,11 @@ struct DmaTile {
             const int64_t x_end = (x0 + EXT) < x_hi ? (x0 + EXT) : x_hi;
             const int64_t rows = x_end > x0 ? x_end - x0 : 0;
             rs = buf_rsrc(src + x0 * ld + k_begin, (uint32_t)(rows * ld * 2));
-            kstep = BK * 2;
+            kstep = KD * 2;
         } else {
             const int64_t krows = k_end > k_begin ? k_end - k_begin : 0;
             rs = buf_rsrc(src + k_begin * ld + x0, (uint32_t)(krows > 0 ? krows * ld * 2 - x0 * 2 : 0));
-            kstep = (uint32_t)(BK * ld * 2);
+            kstep = (uint32_t)(KD * ld * 2);
         }
 #pragma unroll
         for (int i = 0; i < kSlots; ++i) {
@@ -126,7 +131,7 @@ struct DmaTile {
             const int row = p / kCPR;
             int c = p % kCPR;
             if (ROWL) {
-                c ^= rswz(row);
+                c ^= rswz_k<KD>(row);
                 kpos[i] = c * 8;
                 off[i] = (uint32_t)((row * ld + c * 8) * 2);
             } else {
@@ -156,10 +161,11 @@ struct DmaTile {
 // base offsets below are computed once, everything else is an immediate.
 //
 // Row layout: lane reads row (row0 + lane%16), chunk (4*kk + lane/16) ^ rswz.
+template <int KD = BK>
 __device__ __forceinline__ uint32_t row_base(int row0, int kk, int lane) {
     const int r = row0 + (lane & 15);
     const int c = kk * 4 + (lane >> 4);
-    return (uint32_t)((r * 8 + (c ^ rswz(r))) * 16);
+    return (uint32_t)((r * (KD / 8) + (c ^ rswz_k<KD>(r))) * 16);
 }
 // Col layout: lane 16g + 4r + q points at k-row 8g + r (+32 kk, +4 for the
 // second read), columns col0 + 4q .. +3; each 16-lane group then receives one
