@@ -67,8 +67,14 @@ def parse():
 # start-up (a copy reads and writes exactly 1 GiB).  The summary records a
 # digest of the GEMM sources; once they change, `traffic` is reported as null.
 GEMM_SOURCES = ("gemm.hip", "tile_dma.h", "kernels.h", "common.h")
-KERNEL_NAME = {"grouped_up": "gemm_rows_kernel<false, 1, false>",
-               "grouped_down": "gemm_rows_kernel<false, 0, false>"}
+# The grouped GEMM's symbol carries its tile type first; a launch's epilogue
+# and operand layout pick it out (up: squared-ReLU epilogue; down: plain bf16).
+KERNEL_NAME = {"grouped_up": ("gemm_rows_kernel<", ", false, 1, false>"),
+               "grouped_down": ("gemm_rows_kernel<", ", false, 0, false>")}
+
+
+def kernel_match(kernel, name):
+    return all(part in name for part in KERNEL_NAME[kernel])
 
 
 def gemm_digest():
@@ -114,7 +120,7 @@ def per_dispatch(rows, counter, match):
 
 
 def write_traffic(d_fetch, d_write, workload, kernel, calib_bytes):
-    out = {"kernel": kernel, "kernel_symbol": KERNEL_NAME[kernel], "workload": workload,
+    out = {"kernel": kernel, "kernel_symbol": "...".join(KERNEL_NAME[kernel]), "workload": workload,
            "gemm_sources_sha256": gemm_digest()}
     total = 0.0
     for d, counter in ((d_fetch, "FETCH_SIZE"), (d_write, "WRITE_SIZE")):
@@ -123,9 +129,9 @@ def write_traffic(d_fetch, d_write, workload, kernel, calib_bytes):
         if not cal:
             raise SystemExit(f"{d}: no device copy dispatch to calibrate {counter}")
         factor = calib_bytes / (max(cal) * 1024.0)
-        ks = per_dispatch(rows, counter, lambda n: KERNEL_NAME[kernel] in n)
+        ks = per_dispatch(rows, counter, lambda n: kernel_match(kernel, n))
         if not ks:
-            raise SystemExit(f"{d}: no {KERNEL_NAME[kernel]} dispatches")
+            raise SystemExit(f"{d}: no {kernel} dispatches")
         kib = sum(ks) / len(ks)
         out[counter] = {"kib_per_dispatch": round(kib, 1), "dispatches": len(ks),
                         "copy_kib": round(max(cal), 1), "factor": round(factor, 4),
