@@ -291,13 +291,15 @@ struct RowsTile {
 };
 
 template <int BM>
-__device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, int m_total, int w) {
+__device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, int m_count, int w, int m_base) {
+    // item w of the m-tiles [m_base, m_base + m_count) x all n-tiles, taken 8
+    // m-tiles at a time across all n-tiles
     const int width = kGroupM * p.n_tiles;
     const int group = w / width;
     const int first_m = group * kGroupM;
-    const int gsz = (m_total - first_m) < kGroupM ? (m_total - first_m) : kGroupM;
+    const int gsz = (m_count - first_m) < kGroupM ? (m_count - first_m) : kGroupM;
     const int in = w - group * width;
-    const int mt = __builtin_amdgcn_readfirstlane(first_m + in % gsz);
+    const int mt = __builtin_amdgcn_readfirstlane(m_base + first_m + in % gsz);
     const int nt = in / gsz;
     RowsTile t;
     if (p.tiles != nullptr) {
@@ -466,15 +468,22 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 2, wn = wave & 3;
 
-    // This workgroup's work items: w = first + j * G, j = 0 .. n_mine - 1,
-    // where the G / 8 workgroups of one XCD take consecutive items.
+    // Each XCD's G / 8 workgroups (workgroups go to XCDs round-robin) take a
+    // contiguous eighth of the m-tiles, all n-tiles, in group-M order; this
+    // workgroup takes items w = lx + j * (G / 8) of its XCD's share.  The
+    // tile list is expert-major, so an expert's weights stream through one
+    // XCD's L2 (two where a share boundary splits the expert) instead of
+    // every XCD whose m-tile groups touch it.
     const int m_total = p.mtile_total != nullptr
                             ? *(const __attribute__((address_space(4))) int32_t*)p.mtile_total
                             : p.m_tiles;
-    const int n_work = m_total * p.n_tiles;
-    const int G = gridDim.x;
-    const int first = (int)(blockIdx.x % kXcds) * (G / kXcds) + (int)(blockIdx.x / kXcds);
-    const int n_mine = first < n_work ? (n_work - first + G - 1) / G : 0;
+    const int G = gridDim.x;   // a multiple of kXcds
+    const int Gx = G / kXcds;
+    const int xcd = (int)(blockIdx.x % kXcds), lx = (int)(blockIdx.x / kXcds);
+    const int m_base = (int)((int64_t)m_total * xcd / kXcds);
+    const int m_count = (int)((int64_t)m_total * (xcd + 1) / kXcds) - m_base;
+    const int n_work = m_count * p.n_tiles;
+    const int n_mine = lx < n_work ? (n_work - lx + Gx - 1) / Gx : 0;
     const int nk = (p.Kd + KD - 1) / KD;
     const int g_total = n_mine * nk;  // (tile, k step) pairs
     if (g_total == 0) return;
@@ -488,7 +497,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     constexpr int kSA = DmaTile<true, BM, KD>::kSlots, kSB = DmaTile<B_K, BN, KD>::kSlots;
     constexpr int kPerStage = kSA + kSB;
     auto dma_tile = [&](int j) {
-        const RowsTile t = rows_tile<BM>(p, m_total, first + j * G);
+        const RowsTile t = rows_tile<BM>(p, m_count, lx + j * Gx, m_base);
         da.init(p.A, p.lda, t.row0, t.row_hi, 0, p.Kd, wave, lane);
         db.init(p.B + (int64_t)t.e * p.b_stride, p.ldb, t.n0, (int64_t)p.N, 0, p.Kd, wave, lane);
     };
@@ -512,7 +521,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
 
     int kc = 0;   // k step of the tile being computed
     int jc = 0;   // its index in this workgroup's list
-    RowsTile cur = rows_tile<BM>(p, m_total, first);
+    RowsTile cur = rows_tile<BM>(p, m_count, lx, m_base);
     u32x2 uu[MI][4];   // dgrad: the tile's pre-activations
 
     auto step = [&](auto stage_c, int g) {
@@ -549,7 +558,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
             zero_acc(acc);
             kc = 0;
             ++jc;
-            if (jc < n_mine) cur = rows_tile<BM>(p, m_total, first + jc * G);
+            if (jc < n_mine) cur = rows_tile<BM>(p, m_count, lx + jc * Gx, m_base);
         } else {
             ++kc;
         }
