@@ -67,10 +67,11 @@ def parse():
 # start-up (a copy reads and writes exactly 1 GiB).  The summary records a
 # digest of the GEMM sources; once they change, `traffic` is reported as null.
 GEMM_SOURCES = ("gemm.hip", "tile_dma.h", "kernels.h", "common.h")
-# The grouped GEMM's symbol carries its tile type first; a launch's epilogue
-# and operand layout pick it out (up: squared-ReLU epilogue; down: plain bf16).
-KERNEL_NAME = {"grouped_up": ("gemm_rows_kernel<", ", false, 1, false>"),
-               "grouped_down": ("gemm_rows_kernel<", ", false, 0, false>")}
+# The grouped GEMM's symbol carries its operand layout, epilogue and k-tail
+# flag (up: squared-ReLU epilogue; down: plain bf16); the tile height is
+# chosen inside the kernel.
+KERNEL_NAME = {"grouped_up": ("gemm_rows_kernel<false, 1, false>",),
+               "grouped_down": ("gemm_rows_kernel<false, 0, false>",)}
 
 
 def kernel_match(kernel, name):

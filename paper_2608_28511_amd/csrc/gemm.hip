@@ -100,8 +100,10 @@ struct GemmArgs {
     const uint16_t* aux_in;   // EPI_DRELU2: pre-activation u, same layout as C
     uint16_t* aux_out;        // EPI_RELU2: pre-activation u (may be null)
     const int32_t* offsets;   // [E+1] expert row segments (KGRP mode)
-    const int4* tiles;        // ROWS mode: per BM-row tile {expert, row0, row_end, 0}; null = dense
-    const int32_t* mtile_total;  // ROWS mode with tiles: device count of valid m-tiles
+    const int4* tiles;        // ROWS mode: per 128-row tile {expert, row0, row_end, 0}; null = dense
+    const int32_t* mtile_total;  // ROWS mode with tiles: device count of valid 128-row m-tiles
+    const int4* tiles_l;      // the same for 256-row tiles
+    const int32_t* mtile_total_l;
     int64_t lda, ldb, ldc;
     int64_t b_stride;         // elements between experts' B (ROWS mode)
     int64_t c_stride;         // elements between experts' C (KGRP mode)
@@ -110,6 +112,7 @@ struct GemmArgs {
     int64_t R;                // rows of the activation buffers: segments are clamped to [0, R)
     int N, Kd, E;
     int m_tiles, n_tiles;
+    int m_tiles_l;            // ROWS mode: m-tiles of 256 rows (dense) or their static bound
     int accumulate;           // EPI_F32: C += product instead of C = product
 };
 
@@ -291,7 +294,8 @@ struct RowsTile {
 };
 
 template <int BM>
-__device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, int m_count, int w, int m_base) {
+__device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, const int4* tiles, int m_count, int w,
+                                              int m_base) {
     // item w of the m-tiles [m_base, m_base + m_count) x all n-tiles, taken 8
     // m-tiles at a time across all n-tiles
     const int width = kGroupM * p.n_tiles;
@@ -302,11 +306,11 @@ __device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, int m_count, in
     const int mt = __builtin_amdgcn_readfirstlane(m_base + first_m + in % gsz);
     const int nt = in / gsz;
     RowsTile t;
-    if (p.tiles != nullptr) {
+    if (tiles != nullptr) {
         // the table is written by an earlier launch and read-only here: a
         // scalar load through the constant address space
         const __attribute__((address_space(4))) int32_t* ti =
-            (const __attribute__((address_space(4))) int32_t*)(p.tiles + mt);
+            (const __attribute__((address_space(4))) int32_t*)(tiles + mt);
         t.e = ti[0];
         t.row0 = ti[1];
         t.row_hi = ti[2];
@@ -456,12 +460,13 @@ __device__ __forceinline__ void f32_store(const f32x4 (&acc)[MI][4], float* C, i
 }
 
 // C[r, n] = sum_k A[r, k] B_e[k, n] over the grid-wide list of output tiles
-// (expert segments from the tile table, or all M rows when it is null).
-// A is K-contiguous (ROW layout); B is N-contiguous (B_K false: weights stored
-// [Kd, N]) or K-contiguous (B_K true: transposed weights of the dgrads).
+// (expert segments from the tile table `tiles` with m_total valid m-tiles,
+// or all M rows when it is null), in tiles of T::BM rows.  A is K-contiguous
+// (ROW layout); B is N-contiguous (B_K false: weights stored [Kd, N]) or
+// K-contiguous (B_K true: transposed weights of the dgrads).  KTAIL: Kd is
+// not a multiple of 64.
 template <class T, bool B_K, int EPI, bool KTAIL>
-__global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) {
-    __shared__ __attribute__((aligned(1024))) char smem[T::kRingBytes + kEpiBytes];
+__device__ __forceinline__ void rows_body(const GemmArgs& p, char* smem, const int4* tiles, int m_total) {
     constexpr int BM = T::BM, MI = T::MI, KD = T::KD, kStages = T::kStages;
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -474,9 +479,6 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     // tile list is expert-major, so an expert's weights stream through one
     // XCD's L2 (two where a share boundary splits the expert) instead of
     // every XCD whose m-tile groups touch it.
-    const int m_total = p.mtile_total != nullptr
-                            ? *(const __attribute__((address_space(4))) int32_t*)p.mtile_total
-                            : p.m_tiles;
     const int G = gridDim.x;   // a multiple of kXcds
     const int Gx = G / kXcds;
     const int xcd = (int)(blockIdx.x % kXcds), lx = (int)(blockIdx.x / kXcds);
@@ -497,7 +499,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     constexpr int kSA = DmaTile<true, BM, KD>::kSlots, kSB = DmaTile<B_K, BN, KD>::kSlots;
     constexpr int kPerStage = kSA + kSB;
     auto dma_tile = [&](int j) {
-        const RowsTile t = rows_tile<BM>(p, m_count, lx + j * Gx, m_base);
+        const RowsTile t = rows_tile<BM>(p, tiles, m_count, lx + j * Gx, m_base);
         da.init(p.A, p.lda, t.row0, t.row_hi, 0, p.Kd, wave, lane);
         db.init(p.B + (int64_t)t.e * p.b_stride, p.ldb, t.n0, (int64_t)p.N, 0, p.Kd, wave, lane);
     };
@@ -521,7 +523,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
 
     int kc = 0;   // k step of the tile being computed
     int jc = 0;   // its index in this workgroup's list
-    RowsTile cur = rows_tile<BM>(p, m_count, lx, m_base);
+    RowsTile cur = rows_tile<BM>(p, tiles, m_count, lx, m_base);
     u32x2 uu[MI][4];   // dgrad: the tile's pre-activations
 
     auto step = [&](auto stage_c, int g) {
@@ -558,13 +560,51 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
             zero_acc(acc);
             kc = 0;
             ++jc;
-            if (jc < n_mine) cur = rows_tile<BM>(p, m_count, lx + jc * Gx, m_base);
+            if (jc < n_mine) cur = rows_tile<BM>(p, tiles, m_count, lx + jc * Gx, m_base);
         } else {
             ++kc;
         }
     };
 
     for (int g = 0; g < g_total; g += kStages) ring_round<kStages>(step, g, g_total);
+}
+
+// Relative time of one 256-row tile against two 128-row tiles: the tall tile
+// moves a third fewer operand bytes per product (measured 0.91 over the five
+// layer shapes' real routing counts).
+constexpr int kTallTileCostPct = 91;
+
+// The tile height of a launch, from the m-tile counts of both heights: the
+// busiest XCD's rounds of each (ceil(m / 8) m-tiles times n_tiles items over
+// G / 8 workgroups), tall tiles when their rounds cost less.  Every
+// workgroup reads the same counts, so the whole grid takes the same body.
+__device__ __forceinline__ bool take_tall_tiles(int m_small, int m_tall, int n_tiles, int G) {
+    const int Gx = G / kXcds;
+    const int r_small = ((m_small + kXcds - 1) / kXcds * n_tiles + Gx - 1) / Gx;
+    const int r_tall = ((m_tall + kXcds - 1) / kXcds * n_tiles + Gx - 1) / Gx;
+    return 2 * r_tall * kTallTileCostPct < 100 * r_small;
+}
+
+constexpr int kRowsSmemBytes =
+    (TileS::kRingBytes > TileL::kRingBytes ? TileS::kRingBytes : TileL::kRingBytes) + kEpiBytes;
+
+// The ROWS launch: one body per tile height, chosen on the device from the
+// tile schedule's counts (known only after routing).  Products with k-major
+// weights (the dgrads) always take 128-row tiles: measured on the same five
+// shapes, the tall tile never won for them.
+template <bool B_K, int EPI, bool KTAIL>
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) {
+    __shared__ __attribute__((aligned(1024))) char smem[kRowsSmemBytes];
+    typedef const __attribute__((address_space(4))) int32_t* cnt_ptr;
+    const int m_small = p.mtile_total != nullptr ? *(cnt_ptr)p.mtile_total : p.m_tiles;
+    if constexpr (!B_K) {
+        const int m_tall = p.mtile_total_l != nullptr ? *(cnt_ptr)p.mtile_total_l : p.m_tiles_l;
+        if (take_tall_tiles(m_small, m_tall, p.n_tiles, (int)gridDim.x)) {
+            rows_body<TileL, B_K, EPI, KTAIL>(p, smem, p.tiles_l, m_tall);
+            return;
+        }
+    }
+    rows_body<TileS, B_K, EPI, KTAIL>(p, smem, p.tiles, m_small);
 }
 
 // Device-side tile schedules of the grouped GEMM for expert segments
@@ -672,10 +712,7 @@ static int64_t persistent_grid() {
     return G < kXcds ? kXcds : G;
 }
 
-// Tall tiles only when the launch holds at least this many rounds of them.
-constexpr int64_t kMinRoundsLarge = 6;
-
-template <class T, bool B_K, int EPI>
+template <bool B_K, int EPI>
 static hipError_t launch_rows(const GemmArgs& a, hipStream_t st) {
     // never more workgroups than the static bound on the number of output tiles
     const int64_t bound = (int64_t)a.m_tiles * a.n_tiles;
@@ -683,23 +720,22 @@ static hipError_t launch_rows(const GemmArgs& a, hipStream_t st) {
     int64_t G = persistent_grid();
     const int64_t need = (bound + kXcds - 1) / kXcds * kXcds;
     if (need < G) G = need;
-    if (a.Kd % T::KD != 0)
-        hipLaunchKernelGGL((gemm_rows_kernel<T, B_K, EPI, true>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
+    if (a.Kd % TileS::KD != 0)
+        hipLaunchKernelGGL((gemm_rows_kernel<B_K, EPI, true>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
     else
-        hipLaunchKernelGGL((gemm_rows_kernel<T, B_K, EPI, false>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
+        hipLaunchKernelGGL((gemm_rows_kernel<B_K, EPI, false>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
     return hipGetLastError();
 }
 
-template <class T>
 static hipError_t launch_rows_epi(const GemmArgs& a, bool b_kmajor, int epi, hipStream_t st) {
     if (!b_kmajor) {
-        if (epi == EPI_BF16) return launch_rows<T, false, EPI_BF16>(a, st);
-        if (epi == EPI_RELU2) return launch_rows<T, false, EPI_RELU2>(a, st);
-        if (epi == EPI_F32) return launch_rows<T, false, EPI_F32>(a, st);
+        if (epi == EPI_BF16) return launch_rows<false, EPI_BF16>(a, st);
+        if (epi == EPI_RELU2) return launch_rows<false, EPI_RELU2>(a, st);
+        if (epi == EPI_F32) return launch_rows<false, EPI_F32>(a, st);
     } else {
-        if (epi == EPI_BF16) return launch_rows<T, true, EPI_BF16>(a, st);
-        if (epi == EPI_DRELU2) return launch_rows<T, true, EPI_DRELU2>(a, st);
-        if (epi == EPI_F32) return launch_rows<T, true, EPI_F32>(a, st);
+        if (epi == EPI_BF16) return launch_rows<true, EPI_BF16>(a, st);
+        if (epi == EPI_DRELU2) return launch_rows<true, EPI_DRELU2>(a, st);
+        if (epi == EPI_F32) return launch_rows<true, EPI_F32>(a, st);
     }
     return hipErrorInvalidValue;
 }
@@ -723,20 +759,20 @@ hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B
     a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.b_stride = b_stride;
     a.M = R; a.R = R; a.N = N; a.Kd = Kd; a.E = E;
     a.n_tiles = (N + BN - 1) / BN;
-    // tall tiles when the launch is long enough (bound on their count)
-    const int64_t large_tiles =
-        (sched ? mtiles_bound(R, E, TileL::BM) : (R + TileL::BM - 1) / TileL::BM) * a.n_tiles;
-    const bool large = large_tiles >= kMinRoundsLarge * persistent_grid();
-    const int BMr = large ? TileL::BM : TileS::BM;
+    // both tile heights' tables; the kernel picks one from their counts
     if (sched != nullptr) {
-        const SchedPart sp = sched_part((void*)sched, E, R, large);
-        a.tiles = sp.tiles;
-        a.mtile_total = sp.mtile_start + E;  // mtile_start[E]
-        a.m_tiles = sp.max_tiles;
+        const SchedPart ss = sched_part((void*)sched, E, R, false), sl = sched_part((void*)sched, E, R, true);
+        a.tiles = ss.tiles;
+        a.mtile_total = ss.mtile_start + E;  // mtile_start[E]
+        a.m_tiles = ss.max_tiles;
+        a.tiles_l = sl.tiles;
+        a.mtile_total_l = sl.mtile_start + E;
+        a.m_tiles_l = sl.max_tiles;
     } else {
-        a.m_tiles = (int)((R + BMr - 1) / BMr);
+        a.m_tiles = (int)((R + TileS::BM - 1) / TileS::BM);
+        a.m_tiles_l = (int)((R + TileL::BM - 1) / TileL::BM);
     }
-    return large ? launch_rows_epi<TileL>(a, b_kmajor, epi, st) : launch_rows_epi<TileS>(a, b_kmajor, epi, st);
+    return launch_rows_epi(a, b_kmajor, epi, st);
 }
 
 // KGRP launches: tall tiles when there are enough workgroups to fill the
