@@ -692,7 +692,7 @@ static SchedPart sched_part(void* sched, int E, int64_t R, bool large) {
 }
 
 // Compute units of the current device, read once per device.
-static int cu_count() {
+int cu_count() {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
     static std::once_flag once[64];

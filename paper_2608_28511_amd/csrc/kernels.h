@@ -11,6 +11,9 @@ namespace moe {
 
 enum { EPI_BF16 = 0, EPI_RELU2 = 1, EPI_DRELU2 = 2, EPI_F32 = 3 };
 
+// Compute units of the current device (read once per device).
+int cu_count();
+
 // Router workspace: the three bf16 planes [3][E][D] of the split router weight.
 size_t router_ws_bytes(int D, int E);
 hipError_t launch_router_logits(const moe_bf16* x, const float* Wr, const float* bias, int64_t S,

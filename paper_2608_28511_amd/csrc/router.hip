@@ -14,13 +14,15 @@
 //   router_split_kernel   Wr [D, E] fp32 -> three bf16 planes [3][E][D]
 //                         (transposed through LDS, so each plane is
 //                         K-contiguous like x);
-//   router_logits_kernel  64 tokens x 64 experts per workgroup, 8 waves of
-//                         32 tokens x 16 experts; x and the three planes are
-//                         copied global -> LDS by a 4-stage DMA ring (32 KB
-//                         per 64-wide d step), every fragment is one
-//                         conflict-free ds_read_b128, and every output is one
-//                         fixed-order fp32 MFMA chain (lo, mid, hi per 32-wide
-//                         d step), so results are deterministic.
+//   router_logits_kernel  64 tokens x RE experts per workgroup (RE = 64, or
+//                         32 when 64-wide tiles would leave compute units
+//                         idle), RE / 8 waves of 32 tokens x 16 experts; x
+//                         and the three planes are copied global -> LDS by a
+//                         4-stage DMA ring (8 KB + 3 x RE x 128 B per 64-wide
+//                         d step), every fragment is one conflict-free
+//                         ds_read_b128, and every output is one fixed-order
+//                         fp32 MFMA chain (lo, mid, hi per 32-wide d step),
+//                         so results are deterministic.
 #include <type_traits>
 
 #include "common.h"
@@ -30,10 +32,8 @@
 namespace moe {
 
 constexpr int kRT = 64;                      // tokens per workgroup
-constexpr int kRE = 64;                      // experts per workgroup
 constexpr int kRStages = 4;
-constexpr int kRTile = 64 * BK * 2;          // one 64 x 64 bf16 tile: 8 KB
-constexpr int kRStage = 4 * kRTile;          // x, hi, mid, lo: 32 KB
+constexpr int kRTile = 64 * BK * 2;          // the 64-token x tile of one d step: 8 KB
 
 // ---- split: one 64 (d) x 64 (e) block per 256-thread workgroup ----------
 __global__ __launch_bounds__(256) void router_split_kernel(const float* __restrict__ Wr, int D, int E,
@@ -81,33 +81,39 @@ __global__ __launch_bounds__(256) void router_split_kernel(const float* __restri
 }
 
 // ---- logits --------------------------------------------------------------
-template <bool KTAIL>
-__global__ __launch_bounds__(kWaves * 64, 1) void router_logits_kernel(const uint16_t* __restrict__ x,
+template <bool KTAIL, int RE>
+__global__ __launch_bounds__(RE / 8 * 64, 1) void router_logits_kernel(const uint16_t* __restrict__ x,
                                                                        const uint16_t* __restrict__ w3,
                                                                        const float* __restrict__ bias,
                                                                        int64_t S, int D, int E,
                                                                        float* __restrict__ logits,
                                                                        bool vec_out) {
-    __shared__ __attribute__((aligned(1024))) char smem[kRStages * kRStage];  // 128 KB
+    constexpr int kW = RE / 8;                     // waves: 2 (tokens) x RE / 16 (experts)
+    constexpr int kWTile = RE * BK * 2;            // one plane's RE x 64 tile
+    constexpr int kStage = kRTile + 3 * kWTile;    // x, hi, mid, lo
+    __shared__ __attribute__((aligned(1024))) char smem[kRStages * kStage];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave >> 2, wn = wave & 3;
+    const int wm = wave / (RE / 16), wn = wave % (RE / 16);
     const int64_t t0 = (int64_t)blockIdx.x * kRT;
-    const int e0 = blockIdx.y * kRE;
+    const int e0 = blockIdx.y * RE;
     const int64_t plane = (int64_t)E * D;
 
-    DmaTile<true, 64> dx, dw[3];
+    DmaTile<true, 64, BK, kW> dx;
+    DmaTile<true, RE, BK, kW> dw[3];
+    constexpr int kSX = DmaTile<true, 64, BK, kW>::kSlots, kSW = DmaTile<true, RE, BK, kW>::kSlots;
     dx.init(x, D, t0, S, 0, D, wave, lane);
 #pragma unroll
     for (int s = 0; s < 3; ++s) dw[s].init(w3 + s * plane, D, e0, E, 0, D, wave, lane);
 
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char*)smem;
     auto issue = [&](int stage, int64_t rem) {
-        const uint32_t b = lds0 + (uint32_t)stage * kRStage;
-        dx.template issue<KTAIL, 0, 1>(b, rem, wave);
+        const uint32_t b = lds0 + (uint32_t)stage * kStage;
+        dx.template issue<KTAIL, 0, kSX>(b, rem, wave);
 #pragma unroll
-        for (int s = 0; s < 3; ++s) dw[s].template issue<KTAIL, 0, 1>(b + (1 + s) * kRTile, rem, wave);
+        for (int s = 0; s < 3; ++s) dw[s].template issue<KTAIL, 0, kSW>(b + kRTile + s * kWTile, rem, wave);
     };
+    constexpr int kPerStage = kSX + 3 * kSW;   // copies per wave per stage
 
     uint32_t xb[2], wb[2];
 #pragma unroll
@@ -121,8 +127,8 @@ __global__ __launch_bounds__(kWaves * 64, 1) void router_logits_kernel(const uin
 
     auto step = [&](auto stage_c, int kt) {
         constexpr int S = decltype(stage_c)::value;
-        if (kt + 2 < nk) wait_vmcnt<8>();
-        else if (kt + 1 < nk) wait_vmcnt<4>();
+        if (kt + 2 < nk) wait_vmcnt<2 * kPerStage>();
+        else if (kt + 1 < nk) wait_vmcnt<kPerStage>();
         else wait_vmcnt<0>();
         stage_barrier();
         if (kt + 3 < nk) issue((S + 3) % kRStages, (int64_t)D - (int64_t)(kt + 3) * BK);
@@ -130,9 +136,9 @@ __global__ __launch_bounds__(kWaves * 64, 1) void router_logits_kernel(const uin
         for (int kk = 0; kk < 2; ++kk) {
             bf16x8 af[2], wf[3];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) af[i] = lds_b128(xb[kk] + S * kRStage + i * 2048);
+            for (int i = 0; i < 2; ++i) af[i] = lds_b128(xb[kk] + S * kStage + i * 2048);
 #pragma unroll
-            for (int s = 0; s < 3; ++s) wf[s] = lds_b128(wb[kk] + S * kRStage + s * kRTile);
+            for (int s = 0; s < 3; ++s) wf[s] = lds_b128(wb[kk] + S * kStage + s * kWTile);
 #pragma unroll
             for (int s = 2; s >= 0; --s)   // lo, mid, hi: smaller terms first
 #pragma unroll
@@ -183,15 +189,20 @@ hipError_t launch_router_logits(const moe_bf16* x, const float* Wr, const float*
                        dim3(256), 0, st, Wr, D, E, w3);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess || S == 0) return err;
-    dim3 grid(grid_for(S, kRT), (unsigned)((E + kRE - 1) / kRE));
     // 16-byte output stores only where every row start is 16-byte aligned
     const bool vec_out = (E % 4) == 0 && ((uintptr_t)logits % 16) == 0;
-    if (D % BK != 0)
-        hipLaunchKernelGGL(router_logits_kernel<true>, grid, dim3(kWaves * 64), 0, st, (const uint16_t*)x,
-                           w3, bias, S, D, E, logits, vec_out);
-    else
-        hipLaunchKernelGGL(router_logits_kernel<false>, grid, dim3(kWaves * 64), 0, st, (const uint16_t*)x,
-                           w3, bias, S, D, E, logits, vec_out);
+    // 32-expert tiles when 64-wide ones would not give every compute unit a workgroup
+    const int64_t wide = (int64_t)grid_for(S, kRT) * ((E + 63) / 64);
+    const bool narrow = wide < cu_count();
+#define MOE_ROUTER_LAUNCH(KT, RE)                                                                        \
+    hipLaunchKernelGGL((router_logits_kernel<KT, RE>), dim3(grid_for(S, kRT), (unsigned)((E + RE - 1) / RE)), \
+                       dim3(RE / 8 * 64), 0, st, (const uint16_t*)x, w3, bias, S, D, E, logits, vec_out)
+    if (D % BK != 0) {
+        if (narrow) MOE_ROUTER_LAUNCH(true, 32); else MOE_ROUTER_LAUNCH(true, 64);
+    } else {
+        if (narrow) MOE_ROUTER_LAUNCH(false, 32); else MOE_ROUTER_LAUNCH(false, 64);
+    }
+#undef MOE_ROUTER_LAUNCH
     return hipGetLastError();
 }
 

@@ -80,7 +80,8 @@ __device__ __forceinline__ void dma16(const i32x4& rs, uint32_t off, uint32_t ld
 // DMA stage with wait_vmcnt first; every LDS read of the previous stage has
 // been consumed by an MFMA before a wave can arrive here.
 __device__ __forceinline__ void stage_barrier() {
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), visible to the compiler's wait tracking
+    asm volatile("s_barrier" ::: "memory");
 }
 
 // Wait until at most N vector-memory operations of this wave are in flight
@@ -104,10 +105,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 //   a k tile (KTAIL) is cut per chunk at issue time.
 // Col layout (M/N-contiguous source, element (k, c) at src[k*ld + c]): k rows
 //   [k_begin, k_end), columns [x0, x_hi).
-template <bool ROWL, int EXT, int KD = BK>
+template <bool ROWL, int EXT, int KD = BK, int WAVES = kWaves>
 struct DmaTile {
     static constexpr int kCPR = ROWL ? KD / 8 : EXT / 8;       // chunks per LDS row
-    static constexpr int kSlots = EXT * KD * 2 / 1024 / kWaves;  // 1 KB slots per wave
+    static constexpr int kSlots = EXT * KD * 2 / 1024 / WAVES;  // 1 KB slots per wave
+    static_assert(kSlots * WAVES * 1024 == EXT * KD * 2, "the tile must split into whole slots per wave");
     i32x4 rs;                // wave-uniform
     uint32_t kstep;          // bytes per k tile, wave-uniform
     uint32_t off[kSlots];
