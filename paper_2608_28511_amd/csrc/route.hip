@@ -4,8 +4,9 @@
 // experts; the grouped-GEMM experts then need the S*K routed rows in
 // expert-contiguous order (fused permutation, Section 5.2).  Three launches:
 //
-//   route_topk     32 tokens per workgroup, 8 per wavefront, all loaded up
-//                  front.  Per token, K rounds of: wave-wide max of the
+//   route_topk     32 tokens per workgroup, 2 per wavefront (16 waves, so
+//                  each SIMD has several waves whose dependent max and
+//                  ballot chains overlap), all loaded up front.  Per token, K rounds of: wave-wide max of the
 //                  orderable 32-bit score codes of the experts not yet picked
 //                  (DPP within rows of 16 lanes, then the 4 row maxima), and
 //                  a ballot for the lowest expert id holding that code (ties
@@ -32,8 +33,8 @@
 namespace moe {
 
 constexpr int kRouteTok = 32;  // tokens per block (one bit each in the masks)
-constexpr int kRouteThreads = 256;
-constexpr int kTokPerWave = kRouteTok / (kRouteThreads / kWave);  // 8
+constexpr int kRouteThreads = 1024;
+constexpr int kTokPerWave = kRouteTok / (kRouteThreads / kWave);  // 2
 constexpr int kScanCols = 4;    // experts per route_colscan workgroup
 constexpr int kScanThreads = 256;
 

@@ -12,8 +12,7 @@
 //
 // Two launches:
 //   router_split_kernel   Wr [D, E] fp32 -> three bf16 planes [3][E][D]
-//                         (transposed through LDS, so each plane is
-//                         K-contiguous like x);
+//                         (transposed: each plane is K-contiguous like x);
 //   router_logits_kernel  64 tokens x RE experts per workgroup (RE = 64, or
 //                         32 when 64-wide tiles would leave compute units
 //                         idle), RE / 8 waves of 32 tokens x 16 experts; x
@@ -35,49 +34,42 @@ constexpr int kRT = 64;                      // tokens per workgroup
 constexpr int kRStages = 4;
 constexpr int kRTile = 64 * BK * 2;          // the 64-token x tile of one d step: 8 KB
 
-// ---- split: one 64 (d) x 64 (e) block per 256-thread workgroup ----------
+// ---- split: one lane per (expert, 8-wide d chunk) -------------------------
+// Lanes of a wave take 64 consecutive experts, so each of the 8 loads is one
+// contiguous 256-byte row segment of Wr; each lane then stores its 8 d values
+// of every plane as one 16-byte chunk.  No LDS, no barrier: the launch is a
+// single load-split-store step for D/8 x E lanes.
 __global__ __launch_bounds__(256) void router_split_kernel(const float* __restrict__ Wr, int D, int E,
                                                            uint16_t* __restrict__ w3) {
-    __shared__ float t[64][65];
-    const int tid = threadIdx.x;
-    const int d0 = blockIdx.x * 64, e0 = blockIdx.y * 64;
+    const int lane = threadIdx.x & 63;
+    const int d = (blockIdx.x * 4 + (threadIdx.x >> 6)) * 8;
+    const int e = blockIdx.y * 64 + lane;
+    if (e >= E || d >= D) return;            // D is a multiple of 8: chunks are whole
+    float w[8];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-        const int dl = (tid >> 6) + 4 * q, el = tid & 63;
-        const int d = d0 + dl, e = e0 + el;
-        t[dl][el] = (d < D && e < E) ? Wr[(int64_t)d * E + e] : 0.f;
-    }
-    __syncthreads();
-    const int el = tid >> 2, seg = (tid & 3) * 16;
-    const int e = e0 + el;
-    if (e >= E) return;
-    const int64_t plane = (int64_t)E * D;
+    for (int q = 0; q < 8; ++q) w[q] = Wr[(int64_t)(d + q) * E + e];
+    uint32_t hb[4], mb[4], lb[4];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {          // two 8-wide chunks of d
-        const int d = d0 + seg + 8 * h;
-        if (d >= D) break;                 // D is a multiple of 8: chunks are whole
-        uint32_t hb[4], mb[4], lb[4];
+    for (int u = 0; u < 4; ++u) {
+        uint32_t p[3][2];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            uint32_t p[3][2];
-#pragma unroll
-            for (int v = 0; v < 2; ++v) {
-                const float w = t[seg + 8 * h + 2 * u + v][el];
-                const uint32_t hi = f32_to_bf16(w);
-                const float r1 = w - __uint_as_float(hi << 16);
-                const uint32_t mid = f32_to_bf16(r1);
-                const uint32_t lo = f32_to_bf16(r1 - __uint_as_float(mid << 16));
-                p[0][v] = hi; p[1][v] = mid; p[2][v] = lo;
-            }
-            hb[u] = p[0][0] | (p[0][1] << 16);
-            mb[u] = p[1][0] | (p[1][1] << 16);
-            lb[u] = p[2][0] | (p[2][1] << 16);
+        for (int v = 0; v < 2; ++v) {
+            const float x = w[2 * u + v];
+            const uint32_t hi = f32_to_bf16(x);
+            const float r1 = x - __uint_as_float(hi << 16);
+            const uint32_t mid = f32_to_bf16(r1);
+            const uint32_t lo = f32_to_bf16(r1 - __uint_as_float(mid << 16));
+            p[0][v] = hi; p[1][v] = mid; p[2][v] = lo;
         }
-        uint16_t* dst = w3 + (int64_t)e * D + d;
-        *(uint4*)dst = make_uint4(hb[0], hb[1], hb[2], hb[3]);
-        *(uint4*)(dst + plane) = make_uint4(mb[0], mb[1], mb[2], mb[3]);
-        *(uint4*)(dst + 2 * plane) = make_uint4(lb[0], lb[1], lb[2], lb[3]);
+        hb[u] = p[0][0] | (p[0][1] << 16);
+        mb[u] = p[1][0] | (p[1][1] << 16);
+        lb[u] = p[2][0] | (p[2][1] << 16);
     }
+    const int64_t plane = (int64_t)E * D;
+    uint16_t* dst = w3 + (int64_t)e * D + d;
+    *(uint4*)dst = make_uint4(hb[0], hb[1], hb[2], hb[3]);
+    *(uint4*)(dst + plane) = make_uint4(mb[0], mb[1], mb[2], mb[3]);
+    *(uint4*)(dst + 2 * plane) = make_uint4(lb[0], lb[1], lb[2], lb[3]);
 }
 
 // ---- logits --------------------------------------------------------------
@@ -185,7 +177,7 @@ size_t router_ws_bytes(int D, int E) { return ((size_t)3 * E * D * 2 + 255) / 25
 hipError_t launch_router_logits(const moe_bf16* x, const float* Wr, const float* bias, int64_t S,
                                 int D, int E, float* logits, void* ws, hipStream_t st) {
     uint16_t* w3 = (uint16_t*)ws;
-    hipLaunchKernelGGL(router_split_kernel, dim3((unsigned)((D + 63) / 64), (unsigned)((E + 63) / 64)),
+    hipLaunchKernelGGL(router_split_kernel, dim3((unsigned)((D / 8 + 3) / 4), (unsigned)((E + 63) / 64)),
                        dim3(256), 0, st, Wr, D, E, w3);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess || S == 0) return err;
