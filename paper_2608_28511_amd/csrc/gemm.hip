@@ -323,7 +323,6 @@ __device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, const int4* til
     return t;
 }
 
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;

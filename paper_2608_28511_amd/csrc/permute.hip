@@ -16,36 +16,46 @@ namespace moe {
 constexpr int kRowThreads = 256;               // 4 tokens per block
 constexpr int kRowTok = kRowThreads / kWave;
 constexpr int kCPL = 4;                        // 16-byte chunks per lane per pass
+// Dispatch payloads above this take non-temporal stores: the 256 MiB last-
+// level cache cannot hold them (measured: 617 MB 148 -> 120 us; 201 MB is
+// faster with regular stores, 36 vs 41 us).
+constexpr uint64_t kDispatchNtBytes = 224ull << 20;
 
-__global__ __launch_bounds__(kRowThreads) void dispatch_kernel(const uint4* __restrict__ x,
-                                                               const float* __restrict__ prob,
-                                                               const int32_t* __restrict__ inv_perm,
-                                                               int64_t S, int D8, int K,
-                                                               uint4* __restrict__ x_disp,
-                                                               float* __restrict__ p_disp) {
-    const int lane = threadIdx.x & 63;
-    const int64_t t = (int64_t)blockIdx.x * kRowTok + (threadIdx.x >> 6);
-    if (t >= S) return;
+// One workgroup per token, one lane per 16-byte chunk of its row (blocks of
+// 64..1024 lanes, looping for rows beyond 16 KB): each chunk is read once and
+// written to the token's K routed rows.  NT: non-temporal stores, for
+// payloads larger than the last-level cache (there regular stores evict what
+// the next launch reads; below it they keep x_disp resident for the grouped
+// GEMM that follows).
+template <bool NT>
+__global__ __launch_bounds__(1024) void dispatch_kernel(const uint4* __restrict__ x,
+                                                        const float* __restrict__ prob,
+                                                        const int32_t* __restrict__ inv_perm,
+                                                        int64_t S, int D8, int K,
+                                                        uint4* __restrict__ x_disp,
+                                                        float* __restrict__ p_disp) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int64_t t = blockIdx.x;
     const int64_t R = S * K;
     int pos_l = lane < K ? inv_perm[t * K + lane] : 0;
     if ((uint32_t)pos_l >= (uint64_t)R) pos_l = -1;  // out-of-range entries are not written
-    if (p_disp != nullptr && lane < K && pos_l >= 0) p_disp[pos_l] = prob[t * K + lane];
+    if (tid < K && p_disp != nullptr && pos_l >= 0) p_disp[pos_l] = prob[t * K + lane];
     const uint4* src = x + t * D8;
-    for (int c0 = 0; c0 < D8; c0 += kWave * kCPL) {
-        uint4 v[kCPL];
-#pragma unroll
-        for (int i = 0; i < kCPL; ++i) {
-            const int c = c0 + lane + kWave * i;
-            if (c < D8) v[i] = src[c];
-        }
+    // the loop bound is wave-uniform, so every lane takes part in the
+    // shuffles; only the chunk accesses are masked
+    for (int cw = tid - lane; cw < D8; cw += blockDim.x) {
+        const int c = cw + lane;
+        const bool on = c < D8;
+        uint4 v = {};
+        if (on) v = src[c];
         for (int k = 0; k < K; ++k) {
             const int64_t pos = __shfl(pos_l, k);
-            if (pos < 0) continue;
-            uint4* dst = x_disp + pos * D8;
-#pragma unroll
-            for (int i = 0; i < kCPL; ++i) {
-                const int c = c0 + lane + kWave * i;
-                if (c < D8) dst[c] = v[i];
+            if (pos < 0 || !on) continue;
+            if constexpr (NT) {
+                const u32x4 w = {v.x, v.y, v.z, v.w};
+                __builtin_nontemporal_store(w, (u32x4*)(x_disp + pos * D8 + c));
+            } else {
+                x_disp[pos * D8 + c] = v;
             }
         }
     }
@@ -201,52 +211,52 @@ __device__ __forceinline__ uint4 pack8(const float* a) {
     return o;
 }
 
-// y[t] = bf16(sum_k w_k * y_disp[pos_k]); w_k = p_disp[pos_k] or 1.
-__global__ __launch_bounds__(kRowThreads) void combine_kernel(const uint4* __restrict__ y_disp,
-                                                              const float* __restrict__ p_disp,
-                                                              const int32_t* __restrict__ inv_perm,
-                                                              int64_t S, int D8, int K,
-                                                              const float4* __restrict__ add,
-                                                              uint4* __restrict__ y) {
-    const int lane = threadIdx.x & 63;
-    const int64_t t = (int64_t)blockIdx.x * kRowTok + (threadIdx.x >> 6);
-    if (t >= S) return;
+// y[t] = bf16(sum_k w_k * y_disp[pos_k]); w_k = p_disp[pos_k] or 1.  One
+// workgroup per token, one lane per 16-byte chunk; the loads of four slots
+// are issued before their products, which are added in slot order.
+__global__ __launch_bounds__(1024) void combine_kernel(const uint4* __restrict__ y_disp,
+                                                       const float* __restrict__ p_disp,
+                                                       const int32_t* __restrict__ inv_perm,
+                                                       int64_t S, int D8, int K,
+                                                       const float4* __restrict__ add,
+                                                       uint4* __restrict__ y) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int64_t t = blockIdx.x;
     const int64_t R = S * K;
     int pos_l = lane < K ? inv_perm[t * K + lane] : 0;
     if ((uint32_t)pos_l >= (uint64_t)R) pos_l = -1;  // out-of-range entries contribute nothing
     const float w_l = (lane < K && pos_l >= 0) ? (p_disp != nullptr ? p_disp[pos_l] : 1.f) : 0.f;
-    for (int c0 = 0; c0 < D8; c0 += kWave * kCPL) {
-        float acc[kCPL][8];
+    // the loop bound is wave-uniform, so every lane takes part in the
+    // shuffles; only the chunk accesses are masked
+    for (int cw = tid - lane; cw < D8; cw += blockDim.x) {
+        const int c = cw + lane;
+        const bool on = c < D8;
+        float acc[8];
 #pragma unroll
-        for (int i = 0; i < kCPL; ++i)
+        for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+        for (int k0 = 0; k0 < K; k0 += 4) {
+            uint4 v[4];
+            float w[4];
+            bool ok[4];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) acc[i][q] = 0.f;
-        for (int k = 0; k < K; ++k) {
-            const int64_t pos = __shfl(pos_l, k);
-            const float w = __shfl(w_l, k);
-            if (pos < 0) continue;
-            const uint4* src = y_disp + pos * D8;
-            uint4 v[kCPL];
-#pragma unroll
-            for (int i = 0; i < kCPL; ++i) {
-                const int c = c0 + lane + kWave * i;
-                if (c < D8) v[i] = src[c];
+            for (int u = 0; u < 4; ++u) {
+                const int k = k0 + u;
+                const int64_t pos = __shfl(pos_l, k < K ? k : 0);
+                w[u] = __shfl(w_l, k < K ? k : 0);
+                ok[u] = k < K && pos >= 0 && on;
+                if (ok[u]) v[u] = y_disp[pos * D8 + c];
             }
 #pragma unroll
-            for (int i = 0; i < kCPL; ++i)
-                if (c0 + lane + kWave * i < D8) fma8(acc[i], w, v[i]);
+            for (int u = 0; u < 4; ++u)
+                if (ok[u]) fma8(acc, w[u], v[u]);
         }
-#pragma unroll
-        for (int i = 0; i < kCPL; ++i) {
-            const int c = c0 + lane + kWave * i;
-            if (c >= D8) continue;
-            if (add != nullptr) {  // fp32 addend, summed after the K rows, before the rounding
-                const float4 a0 = add[(t * D8 + c) * 2], a1 = add[(t * D8 + c) * 2 + 1];
-                acc[i][0] += a0.x; acc[i][1] += a0.y; acc[i][2] += a0.z; acc[i][3] += a0.w;
-                acc[i][4] += a1.x; acc[i][5] += a1.y; acc[i][6] += a1.z; acc[i][7] += a1.w;
-            }
-            y[t * D8 + c] = pack8(acc[i]);
+        if (!on) continue;
+        if (add != nullptr) {  // fp32 addend, summed after the K rows, before the rounding
+            const float4 a0 = add[(t * D8 + c) * 2], a1 = add[(t * D8 + c) * 2 + 1];
+            acc[0] += a0.x; acc[1] += a0.y; acc[2] += a0.z; acc[3] += a0.w;
+            acc[4] += a1.x; acc[5] += a1.y; acc[6] += a1.z; acc[7] += a1.w;
         }
+        y[t * D8 + c] = pack8(acc);
     }
 }
 
@@ -311,16 +321,24 @@ __global__ __launch_bounds__(kRowThreads) void combine_bwd_kernel(
 hipError_t launch_dispatch(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S,
                            int D, int K, moe_bf16* x_disp, float* p_disp, hipStream_t st) {
     if (S == 0) return hipSuccess;
-    hipLaunchKernelGGL(dispatch_kernel, dim3(grid_for(S, kRowTok)), dim3(kRowThreads), 0, st,
-                       (const uint4*)x, prob, inv_perm, S, D / 8, K, (uint4*)x_disp, p_disp);
+    const int d8 = D / 8;
+    const int nthr = d8 >= 1024 ? 1024 : (d8 + 63) / 64 * 64;
+    const bool nt = (uint64_t)S * K * D * 2 > kDispatchNtBytes;
+    if (nt)
+        hipLaunchKernelGGL(dispatch_kernel<true>, dim3((unsigned)S), dim3(nthr), 0, st, (const uint4*)x, prob,
+                           inv_perm, S, d8, K, (uint4*)x_disp, p_disp);
+    else
+        hipLaunchKernelGGL(dispatch_kernel<false>, dim3((unsigned)S), dim3(nthr), 0, st, (const uint4*)x, prob,
+                           inv_perm, S, d8, K, (uint4*)x_disp, p_disp);
     return hipGetLastError();
 }
 
 hipError_t launch_combine(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_perm,
                           int64_t S, int D, int K, const float* add, moe_bf16* y, hipStream_t st) {
     if (S == 0) return hipSuccess;
-    hipLaunchKernelGGL(combine_kernel, dim3(grid_for(S, kRowTok)), dim3(kRowThreads), 0, st,
-                       (const uint4*)y_disp, p_disp, inv_perm, S, D / 8, K, (const float4*)add, (uint4*)y);
+    const int d8 = D / 8;
+    hipLaunchKernelGGL(combine_kernel, dim3((unsigned)S), dim3(d8 >= 1024 ? 1024 : (d8 + 63) / 64 * 64), 0, st,
+                       (const uint4*)y_disp, p_disp, inv_perm, S, d8, K, (const float4*)add, (uint4*)y);
     return hipGetLastError();
 }
 
