@@ -107,6 +107,45 @@ def test_grouped_ffn_full_size_sampled(name):
     assert_bf16_close(np64(yd[sel]), y_ref[ref_order], f"{name} y_disp")
 
 
+def _takes_tall_tiles(counts, N, cus):
+    """The rows kernel's tile-height rule, restated: the busiest XCD's rounds
+    of 128-row and of 256-row tiles; tall tiles when 2 * rounds_tall * 0.91 <
+    rounds_small.  The grid is one workgroup per CU (a multiple of 8), capped
+    by the static bound on the number of output tiles."""
+    def cdiv(a, b):
+        return -(-a // b)
+    R, E = int(sum(counts)), len(counts)
+    m_small = int(sum(cdiv(int(c), 128) for c in counts))
+    m_tall = int(sum(cdiv(int(c), 256) for c in counts))
+    nt = cdiv(N, 256)
+    bound = (cdiv(R, 128) + min(R, E)) * nt          # static bound on the output tiles
+    G = min(cus // 8 * 8, cdiv(bound, 8) * 8)
+    r_small = cdiv(cdiv(m_small, 8) * nt, G // 8)
+    r_tall = cdiv(cdiv(m_tall, 8) * nt, G // 8)
+    return 2 * r_tall * 91 < 100 * r_small
+
+
+def test_grouped_ffn_exact_tall_tiles():
+    """Both projections on 256-row tiles (long launch, few large experts with
+    ragged last tiles): bit-exact like the 128-row shapes above."""
+    R, D, F, E = 24576, 512, 1024, 4
+    off = make_segments(R, E, seed=R + E)
+    counts = np.diff(npi(off))
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    if not (_takes_tall_tiles(counts, F, cus) and _takes_tall_tiles(counts, D, cus)):
+        pytest.skip(f"this device ({cus} CUs) keeps 128-row tiles for the shape")
+    assert all(c % 256 for c in counts)   # every expert ends in a partly filled tall tile
+    x = make_sparse_sign_rows(R, D, 16, seed=R).to(torch.bfloat16)
+    W1 = _sign_weights(E, D, F, seed=D, density=1.0)
+    W2 = _sign_weights(E, F, D, seed=F, density=min(1.0, 4.0 / F))
+    h, u, yd = layer.grouped_ffn(x.to(DEV), off.to(DEV), W1.to(DEV), W2.to(DEV), save_u=True)
+    torch.cuda.synchronize()
+    u_ref, h_ref, y_ref = O.expert_ffn(np64(x), npi(off), np64(W1), np64(W2))
+    assert np.array_equal(np64(u), u_ref)
+    assert np.array_equal(np64(h), h_ref)
+    assert np.array_equal(np64(yd), y_ref)
+
+
 @pytest.mark.parametrize("R,D,F,E,empty,skew", SHAPES[1:5])
 def test_grouped_gemm_single_launches_match_ffn(R, D, F, E, empty, skew):
     """moe_grouped_schedule + two moe_grouped_gemm launches reproduce
