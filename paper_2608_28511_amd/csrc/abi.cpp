@@ -423,10 +423,12 @@ int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
         MOE_HIP(moe::launch_dispatch_mx(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_q, b.x_scale, b.p_disp, stream));
         MOE_HIP(moe::launch_dequant_mx(b.x_q, b.x_scale, R, D, b.x_disp, stream));
     } else {
-        MOE_HIP(moe::launch_dispatch(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_disp, b.p_disp, stream));
+        // the dispatch launch also builds the grouped GEMM's tile tables
+        MOE_HIP(moe::launch_dispatch(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_disp, b.p_disp, stream,
+                                     R > 0 ? b.offsets : nullptr, E, R > 0 ? b.sched : nullptr));
     }
     if (R > 0) {
-        MOE_HIP(moe::launch_tile_schedule(b.offsets, E, R, b.sched, stream));
+        if (a->payload == MOE_PAYLOAD_MXFP8) MOE_HIP(moe::launch_tile_schedule(b.offsets, E, R, b.sched, stream));
         MOE_HIP(moe::launch_grouped_rows(b.x_disp, D, a->W1, F, (int64_t)D * F, false, b.h, F,
                                          moe::EPI_RELU2, nullptr, a->u_save, b.sched, E, R, F, D, stream));
         MOE_HIP(moe::launch_grouped_rows(b.h, F, a->W2, D, (int64_t)F * D, false, b.y_disp, D,

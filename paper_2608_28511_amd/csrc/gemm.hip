@@ -66,6 +66,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "schedule.h"
 #include "tile_dma.h"
 
 namespace moe {
@@ -606,88 +607,17 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     rows_body<TileS, B_K, EPI, KTAIL>(p, smem, p.tiles, m_small);
 }
 
-// Device-side tile schedules of the grouped GEMM for expert segments
-// offsets[0..E] (clamped to [0, R)), one per tile height BM in {128, 256}:
-//   mtile_start[0] = 0, mtile_start[e+1] = sum_{e' <= e} ceil(count[e'] / BM)
-//   tiles[mt] = {e, row0, row_end, 0} for every BM-row tile mt of expert e,
-//               {-1, 0, 0, 0} for mt in [total, max_tiles) (the static grid bound).
-struct SchedPart {
-    int32_t* mtile_start;
-    int4* tiles;
-    int max_tiles;
-};
-
-__device__ void fill_schedule(const int32_t* seg_lo, const int32_t* seg_hi, int32_t* s, int E, int BMr,
-                              const SchedPart& sp, int tid) {
-    s[tid] = (seg_hi[tid] - seg_lo[tid] + BMr - 1) / BMr;
-    __syncthreads();
-    for (int d = 1; d < 1024; d <<= 1) {
-        const int add = tid >= d ? s[tid - d] : 0;
-        __syncthreads();
-        s[tid] += add;
-        __syncthreads();
-    }
-    if (tid < E) sp.mtile_start[tid + 1] = s[tid];
-    if (tid == 0) sp.mtile_start[0] = 0;
-    const int total = s[E - 1];
-    for (int mt = tid; mt < sp.max_tiles; mt += 1024) {
-        int4 v = make_int4(-1, 0, 0, 0);
-        if (mt < total) {
-            int a = 0, b = E - 1;  // first e with s[e] > mt
-            while (a < b) {
-                const int m = (a + b) >> 1;
-                if (s[m] > mt) b = m; else a = m + 1;
-            }
-            const int row0 = seg_lo[a] + (mt - (a ? s[a - 1] : 0)) * BMr;
-            const int row_end = row0 + BMr < seg_hi[a] ? row0 + BMr : seg_hi[a];
-            v = make_int4(a, row0, row_end, 0);
-        }
-        sp.tiles[mt] = v;
-    }
-    __syncthreads();
-}
+static_assert(kSchedBM[0] == TileS::BM && kSchedBM[1] == TileL::BM, "schedule tile heights");
 
 __global__ __launch_bounds__(1024) void tile_schedule_kernel(const int32_t* __restrict__ offsets, int E, int R,
                                                               SchedPart small, SchedPart large) {
-    __shared__ int32_t s[1024];
-    __shared__ int32_t seg_lo[1024], seg_hi[1024];
-    const int tid = threadIdx.x;
-    int lo = 0, hi = 0;
-    if (tid < E) {
-        lo = offsets[tid];
-        hi = offsets[tid + 1];
-        lo = lo < 0 ? 0 : (lo > R ? R : lo);
-        hi = hi < lo ? lo : (hi > R ? R : hi);
-    }
-    seg_lo[tid] = lo;
-    seg_hi[tid] = hi;
-    fill_schedule(seg_lo, seg_hi, s, E, TileS::BM, small, tid);
-    fill_schedule(seg_lo, seg_hi, s, E, TileL::BM, large, tid);
+    build_tile_schedule(offsets, E, R, small, large);
 }
 
 int gemm_tile_m() { return TileS::BM; }
 
-static int64_t mtiles_bound(int64_t R, int E, int BMr) {
-    // sum_e ceil(c_e / BM) <= ceil(R / BM) + (number of non-empty experts)
-    const int64_t nonempty = R < E ? R : E;
-    return (R + BMr - 1) / BMr + nonempty;
-}
-
-// Schedule buffer: for 128-row then 256-row tiles, mtile_start [E+1] int32
-// then (16-byte aligned) the tile table; each part 256-byte aligned.
-static size_t sched_table_offset(int E) { return (size_t)((E + 1) * 4 + 15) / 16 * 16; }
-static size_t sched_part_bytes(int E, int64_t R, int BMr) {
-    return (sched_table_offset(E) + (size_t)mtiles_bound(R, E, BMr) * 16 + 255) / 256 * 256;
-}
-
 size_t gemm_schedule_bytes(int E, int64_t R) {
     return sched_part_bytes(E, R, TileS::BM) + sched_part_bytes(E, R, TileL::BM);
-}
-
-static SchedPart sched_part(void* sched, int E, int64_t R, bool large) {
-    char* base = (char*)sched + (large ? sched_part_bytes(E, R, TileS::BM) : 0);
-    return SchedPart{(int32_t*)base, (int4*)(base + sched_table_offset(E)),
-                     (int)mtiles_bound(R, E, large ? TileL::BM : TileS::BM)};
 }
 
 // Compute units of the current device, read once per device.

@@ -55,8 +55,12 @@ hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* t
                         int32_t* inv_perm, void* ws, hipStream_t st, bool sigmoid = false,
                         const float* sel_bias = nullptr);
 
+// With sched (and the expert offsets sched_offsets [E+1] of the same
+// routing), the launch also builds the grouped GEMM's tile tables in sched,
+// as launch_tile_schedule would.
 hipError_t launch_dispatch(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S,
-                           int D, int K, moe_bf16* x_disp, float* p_disp, hipStream_t st);
+                           int D, int K, moe_bf16* x_disp, float* p_disp, hipStream_t st,
+                           const int32_t* sched_offsets = nullptr, int E = 0, void* sched = nullptr);
 // MX-FP8 payload (D a multiple of 32): codes [S*K, D] and E8M0 scales
 // [S*K, D/32] of each token row at its K routed rows; decode to bf16.
 hipError_t launch_dispatch_mx(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S, int D,

@@ -10,6 +10,7 @@
 // atomics and is deterministic.
 #include "common.h"
 #include "kernels.h"
+#include "schedule.h"
 
 namespace moe {
 
@@ -27,16 +28,25 @@ constexpr uint64_t kDispatchNtBytes = 224ull << 20;
 // payloads larger than the last-level cache (there regular stores evict what
 // the next launch reads; below it they keep x_disp resident for the grouped
 // GEMM that follows).
+// With sched_offsets, one more workgroup (the last) builds the grouped
+// GEMM's tile tables from the expert offsets, so the layer needs no launch
+// of its own for them.
 template <bool NT>
 __global__ __launch_bounds__(1024) void dispatch_kernel(const uint4* __restrict__ x,
                                                         const float* __restrict__ prob,
                                                         const int32_t* __restrict__ inv_perm,
                                                         int64_t S, int D8, int K,
                                                         uint4* __restrict__ x_disp,
-                                                        float* __restrict__ p_disp) {
+                                                        float* __restrict__ p_disp,
+                                                        const int32_t* __restrict__ sched_offsets, int E,
+                                                        SchedPart sched_small, SchedPart sched_large) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int64_t t = blockIdx.x;
     const int64_t R = S * K;
+    if (t >= S) {
+        build_tile_schedule(sched_offsets, E, (int)R, sched_small, sched_large);
+        return;
+    }
     int pos_l = lane < K ? inv_perm[t * K + lane] : 0;
     if ((uint32_t)pos_l >= (uint64_t)R) pos_l = -1;  // out-of-range entries are not written
     if (tid < K && p_disp != nullptr && pos_l >= 0) p_disp[pos_l] = prob[t * K + lane];
@@ -319,17 +329,22 @@ __global__ __launch_bounds__(kRowThreads) void combine_bwd_kernel(
 }
 
 hipError_t launch_dispatch(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S,
-                           int D, int K, moe_bf16* x_disp, float* p_disp, hipStream_t st) {
+                           int D, int K, moe_bf16* x_disp, float* p_disp, hipStream_t st,
+                           const int32_t* sched_offsets, int E, void* sched) {
     if (S == 0) return hipSuccess;
     const int d8 = D / 8;
     const int nthr = d8 >= 1024 ? 1024 : (d8 + 63) / 64 * 64;
     const bool nt = (uint64_t)S * K * D * 2 > kDispatchNtBytes;
+    const int64_t R = S * K;
+    const SchedPart ss = sched ? sched_part(sched, E, R, false) : SchedPart{};
+    const SchedPart sl = sched ? sched_part(sched, E, R, true) : SchedPart{};
+    const unsigned grid = (unsigned)S + (sched ? 1u : 0u);
     if (nt)
-        hipLaunchKernelGGL(dispatch_kernel<true>, dim3((unsigned)S), dim3(nthr), 0, st, (const uint4*)x, prob,
-                           inv_perm, S, d8, K, (uint4*)x_disp, p_disp);
+        hipLaunchKernelGGL(dispatch_kernel<true>, dim3(grid), dim3(nthr), 0, st, (const uint4*)x, prob, inv_perm, S,
+                           d8, K, (uint4*)x_disp, p_disp, sched_offsets, E, ss, sl);
     else
-        hipLaunchKernelGGL(dispatch_kernel<false>, dim3((unsigned)S), dim3(nthr), 0, st, (const uint4*)x, prob,
-                           inv_perm, S, d8, K, (uint4*)x_disp, p_disp);
+        hipLaunchKernelGGL(dispatch_kernel<false>, dim3(grid), dim3(nthr), 0, st, (const uint4*)x, prob, inv_perm, S,
+                           d8, K, (uint4*)x_disp, p_disp, sched_offsets, E, ss, sl);
     return hipGetLastError();
 }
 
