@@ -2,12 +2,13 @@
 // hidden dispatch, probability dispatch and hidden combine (Section 4.1
 // footnote), whose per-row payloads Eq. 1 counts.
 //
-// All four kernels are HBM-bound row copies.  One wavefront owns one token:
-// it reads the token's row once with 16-byte loads (8 bf16 per lane) and
-// writes it to (dispatch) or gathers it from (combine) the token's K rows of
-// the expert-contiguous buffer, each a contiguous D*2-byte row.  The combine
-// sums in fp32 in ascending slot order inside the wave, so it needs no
-// atomics and is deterministic.
+// All kernels are HBM-bound row copies.  Dispatch, its MX-FP8 form and the
+// combine take one workgroup per token, one lane per 16-byte chunk of the
+// row (8 bf16); the combine's transpose takes one wavefront per token.  A
+// token's row is read once and written to (dispatch) or gathered from
+// (combine) its K rows of the expert-contiguous buffer, each a contiguous
+// row.  The combine sums each chunk in fp32 in ascending slot order, so it
+// needs no atomics and is deterministic.
 #include "common.h"
 #include "kernels.h"
 #include "schedule.h"
@@ -128,56 +129,51 @@ __device__ __forceinline__ uint32_t bf16_mag_max8(const uint4& v) {
 
 // One wavefront per token: the row is encoded once and its codes and block
 // scales are written to the token's K routed rows.
-__global__ __launch_bounds__(kRowThreads) void dispatch_mx_kernel(const uint4* __restrict__ x,
-                                                                  const float* __restrict__ prob,
-                                                                  const int32_t* __restrict__ inv_perm,
-                                                                  int64_t S, int D8, int K,
-                                                                  uint2* __restrict__ x_q,
-                                                                  uint8_t* __restrict__ x_scale,
-                                                                  float* __restrict__ p_disp) {
-    const int lane = threadIdx.x & 63;
-    const int64_t t = (int64_t)blockIdx.x * kRowTok + (threadIdx.x >> 6);
-    if (t >= S) return;
+// One workgroup per token, one lane per 16-byte chunk (8 elements) of its
+// row; a 32-element block is 4 adjacent lanes of one wavefront.
+__global__ __launch_bounds__(1024) void dispatch_mx_kernel(const uint4* __restrict__ x,
+                                                           const float* __restrict__ prob,
+                                                           const int32_t* __restrict__ inv_perm,
+                                                           int64_t S, int D8, int K,
+                                                           uint2* __restrict__ x_q,
+                                                           uint8_t* __restrict__ x_scale,
+                                                           float* __restrict__ p_disp) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int64_t t = blockIdx.x;
     const int64_t R = S * K;
     const int D32 = D8 / 4;
     int pos_l = lane < K ? inv_perm[t * K + lane] : 0;
     if ((uint32_t)pos_l >= (uint64_t)R) pos_l = -1;  // out-of-range entries are not written
-    if (p_disp != nullptr && lane < K && pos_l >= 0) p_disp[pos_l] = prob[t * K + lane];
+    if (tid < K && p_disp != nullptr && pos_l >= 0) p_disp[pos_l] = prob[t * K + lane];
     const uint4* src = x + t * D8;
-    for (int c0 = 0; c0 < D8; c0 += kWave * kCPL) {
-        uint2 q[kCPL];
-        uint32_t sc[kCPL];
+    // the loop bound is wave-uniform, so every lane takes part in the
+    // shuffles; only the chunk accesses are masked (D8 is a multiple of 4:
+    // whole blocks per lane group)
+    for (int cw = tid - lane; cw < D8; cw += blockDim.x) {
+        const int c = cw + lane;
+        const bool on = c < D8;
+        const uint4 v = on ? src[c] : make_uint4(0, 0, 0, 0);
+        uint32_t am = bf16_mag_max8(v);
+        am = max(am, (uint32_t)__shfl_xor((int)am, 1));
+        am = max(am, (uint32_t)__shfl_xor((int)am, 2));
+        const int ef = (int)(am >> 7);            // bf16 exponent field of the block maximum
+        const int sh = ef == 0 ? -127 : max(ef - 127 - 8, -127);
+        const uint32_t sc = (uint32_t)(sh + 127);
+        const float inv = __uint_as_float((uint32_t)(127 - sh) << 23);  // 2^-s, a normal fp32
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        uint32_t b[2] = {0u, 0u};
 #pragma unroll
-        for (int i = 0; i < kCPL; ++i) {
-            const int c = c0 + lane + kWave * i;      // D8 is a multiple of 4: whole blocks per lane group
-            const uint4 v = c < D8 ? src[c] : make_uint4(0, 0, 0, 0);
-            uint32_t am = bf16_mag_max8(v);
-            am = max(am, (uint32_t)__shfl_xor((int)am, 1));
-            am = max(am, (uint32_t)__shfl_xor((int)am, 2));
-            const int ef = (int)(am >> 7);            // bf16 exponent field of the block maximum
-            const int sh = ef == 0 ? -127 : max(ef - 127 - 8, -127);
-            sc[i] = (uint32_t)(sh + 127);
-            const float inv = __uint_as_float((uint32_t)(127 - sh) << 23);  // 2^-s, a normal fp32
-            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-            uint32_t b[2] = {0u, 0u};
-#pragma unroll
-            for (int h = 0; h < 4; ++h) {
-                const uint32_t lo = e4m3_rne_sat(bf16_lo(w[h]) * inv);
-                const uint32_t hi = e4m3_rne_sat(bf16_hi(w[h]) * inv);
-                b[h >> 1] |= (lo | (hi << 8)) << (16 * (h & 1));
-            }
-            q[i] = make_uint2(b[0], b[1]);
+        for (int h = 0; h < 4; ++h) {
+            const uint32_t lo = e4m3_rne_sat(bf16_lo(w[h]) * inv);
+            const uint32_t hi = e4m3_rne_sat(bf16_hi(w[h]) * inv);
+            b[h >> 1] |= (lo | (hi << 8)) << (16 * (h & 1));
         }
+        const uint2 q = make_uint2(b[0], b[1]);
         for (int k = 0; k < K; ++k) {
             const int64_t pos = __shfl(pos_l, k);
-            if (pos < 0) continue;
-#pragma unroll
-            for (int i = 0; i < kCPL; ++i) {
-                const int c = c0 + lane + kWave * i;
-                if (c >= D8) continue;
-                x_q[pos * D8 + c] = q[i];
-                if ((lane & 3) == 0) x_scale[pos * D32 + c / 4] = (uint8_t)sc[i];
-            }
+            if (pos < 0 || !on) continue;
+            x_q[pos * D8 + c] = q;
+            if ((lane & 3) == 0) x_scale[pos * D32 + c / 4] = (uint8_t)sc;
         }
     }
 }
@@ -374,7 +370,9 @@ namespace moe {
 hipError_t launch_dispatch_mx(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S, int D,
                               int K, uint8_t* x_q, uint8_t* x_scale, float* p_disp, hipStream_t st) {
     if (S == 0) return hipSuccess;
-    hipLaunchKernelGGL(dispatch_mx_kernel, dim3(grid_for(S, kRowTok)), dim3(kRowThreads), 0, st, (const uint4*)x,
+    const int d8 = D / 8;
+    hipLaunchKernelGGL(dispatch_mx_kernel, dim3((unsigned)S), dim3(d8 >= 1024 ? 1024 : (d8 + 63) / 64 * 64), 0, st,
+                       (const uint4*)x,
                        prob, inv_perm, S, D / 8, K, (uint2*)x_q, x_scale, p_disp);
     return hipGetLastError();
 }
