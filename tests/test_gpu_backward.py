@@ -81,8 +81,12 @@ def assert_within(got, ref, bound, what):
     assert float(np.mean(d)) <= 1e-2 * rms, f"{what}: mean error {np.mean(d):.3e} vs rms {rms:.3e}"
 
 
+# the last expert is dead (-inf logits) in every case: (1, 8, 2, 1, 8) is one
+# token on one live expert; (7, 72, 3, 2, 24) sends every token to every live
+# expert; (64, 136, 1024, 32, 40) is the largest E and K the ABI takes
 @pytest.mark.parametrize("S,D,E,K,F", [(64, 64, 4, 2, 64), (300, 136, 9, 3, 200), (512, 256, 8, 2, 512),
-                                       (1024, 512, 32, 8, 256)])
+                                       (1024, 512, 32, 8, 256), (1, 8, 2, 1, 8), (7, 72, 3, 2, 24),
+                                       (64, 136, 1024, 32, 40)])
 def test_backward_small(S, D, E, K, F):
     g = torch.Generator().manual_seed(S + D + E)
     x = torch.randn((S, D), generator=g).to(torch.bfloat16)
