@@ -2,9 +2,9 @@
 // hidden dispatch, probability dispatch and hidden combine (Section 4.1
 // footnote), whose per-row payloads Eq. 1 counts.
 //
-// All kernels are HBM-bound row copies.  Dispatch, its MX-FP8 form and the
-// combine take one workgroup per token, one lane per 16-byte chunk of the
-// row (8 bf16); the combine's transpose takes one wavefront per token.  A
+// All kernels are HBM-bound row copies.  Dispatch, its MX-FP8 form, the
+// combine and its transpose take one workgroup per token, one lane per
+// 16-byte chunk of the row (8 bf16).  A
 // token's row is read once and written to (dispatch) or gathered from
 // (combine) its K rows of the expert-contiguous buffer, each a contiguous
 // row.  The combine sums each chunk in fp32 in ascending slot order, so it
@@ -15,9 +15,6 @@
 
 namespace moe {
 
-constexpr int kRowThreads = 256;               // 4 tokens per block
-constexpr int kRowTok = kRowThreads / kWave;
-constexpr int kCPL = 4;                        // 16-byte chunks per lane per pass
 // Dispatch payloads above this take non-temporal stores: the 256 MiB last-
 // level cache cannot hold them (measured: 617 MB 148 -> 120 us; 201 MB is
 // faster with regular stores, 36 vs 41 us).
@@ -267,60 +264,74 @@ __global__ __launch_bounds__(1024) void combine_kernel(const uint4* __restrict__
 }
 
 // dy_disp[pos_k] = bf16(w_k * dy[t]);  dp[t,k] = <dy[t], y_disp[pos_k]>.
-__global__ __launch_bounds__(kRowThreads) void combine_bwd_kernel(
+// One workgroup per token, one lane per 16-byte chunk; each dot is summed in
+// a fixed order: a lane's chunks in order, a wave butterfly, then the waves'
+// partials in wave order.
+constexpr int kCbMaxWaves = 16;
+__global__ __launch_bounds__(1024) void combine_bwd_kernel(
     const uint4* __restrict__ dy, const uint4* __restrict__ y_disp, const float* __restrict__ p_disp,
     const int32_t* __restrict__ inv_perm, int64_t S, int D8, int K, uint4* __restrict__ dy_disp,
     float* __restrict__ dp) {
-    const int lane = threadIdx.x & 63;
-    const int64_t t = (int64_t)blockIdx.x * kRowTok + (threadIdx.x >> 6);
-    if (t >= S) return;
+    __shared__ float part[32][kCbMaxWaves];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t t = blockIdx.x;
     const int64_t R = S * K;
     int pos_l = lane < K ? inv_perm[t * K + lane] : 0;
     if ((uint32_t)pos_l >= (uint64_t)R) pos_l = -1;  // out-of-range entries are skipped
     const float w_l = (lane < K && pos_l >= 0) ? (p_disp != nullptr ? p_disp[pos_l] : 1.f) : 0.f;
     const uint4* g = dy + t * D8;
-    for (int k = 0; k < K; ++k) {
-        const int64_t pos = __shfl(pos_l, k);
-        const float w = __shfl(w_l, k);
-        if (pos < 0) continue;
-        const uint4* yd = y_disp + pos * D8;
-        uint4* out = dy_disp + pos * D8;
-        float dot = 0.f;
-        for (int c0 = 0; c0 < D8; c0 += kWave * kCPL) {
-            uint4 gv[kCPL], yv[kCPL];
+    float dot[32];
 #pragma unroll
-            for (int i = 0; i < kCPL; ++i) {
-                const int c = c0 + lane + kWave * i;
-                if (c < D8) {
-                    gv[i] = g[c];
-                    yv[i] = yd[c];
-                }
-            }
-#pragma unroll
-            for (int i = 0; i < kCPL; ++i) {
-                const int c = c0 + lane + kWave * i;
-                if (c < D8) {
-                    float a[8], b[8];
-                    a[0] = bf16_lo(gv[i].x); a[1] = bf16_hi(gv[i].x);
-                    a[2] = bf16_lo(gv[i].y); a[3] = bf16_hi(gv[i].y);
-                    a[4] = bf16_lo(gv[i].z); a[5] = bf16_hi(gv[i].z);
-                    a[6] = bf16_lo(gv[i].w); a[7] = bf16_hi(gv[i].w);
-                    b[0] = bf16_lo(yv[i].x); b[1] = bf16_hi(yv[i].x);
-                    b[2] = bf16_lo(yv[i].y); b[3] = bf16_hi(yv[i].y);
-                    b[4] = bf16_lo(yv[i].z); b[5] = bf16_hi(yv[i].z);
-                    b[6] = bf16_lo(yv[i].w); b[7] = bf16_hi(yv[i].w);
-#pragma unroll
-                    for (int q = 0; q < 8; ++q) {
-                        dot = fmaf(a[q], b[q], dot);
-                        a[q] *= w;
-                    }
-                    out[c] = pack8(a);
-                }
-            }
+    for (int k = 0; k < 32; ++k) dot[k] = 0.f;
+    // the loop bound is wave-uniform, so every lane takes part in the
+    // shuffles; only the chunk accesses are masked
+    for (int cw = tid - lane; cw < D8; cw += blockDim.x) {
+        const int c = cw + lane;
+        const bool on = c < D8;
+        float a[8];
+        {
+            const uint4 gv = on ? g[c] : make_uint4(0, 0, 0, 0);
+            a[0] = bf16_lo(gv.x); a[1] = bf16_hi(gv.x);
+            a[2] = bf16_lo(gv.y); a[3] = bf16_hi(gv.y);
+            a[4] = bf16_lo(gv.z); a[5] = bf16_hi(gv.z);
+            a[6] = bf16_lo(gv.w); a[7] = bf16_hi(gv.w);
         }
 #pragma unroll
-        for (int m = 32; m > 0; m >>= 1) dot += __shfl_xor(dot, m);
-        if (dp != nullptr && lane == 0) dp[t * K + k] = dot;
+        for (int k = 0; k < 32; ++k) {
+            if (k >= K) break;
+            const int64_t pos = __shfl(pos_l, k);
+            const float w = __shfl(w_l, k);
+            if (pos < 0 || !on) continue;
+            const uint4 yv = y_disp[pos * D8 + c];
+            float b[8];
+            b[0] = bf16_lo(yv.x); b[1] = bf16_hi(yv.x);
+            b[2] = bf16_lo(yv.y); b[3] = bf16_hi(yv.y);
+            b[4] = bf16_lo(yv.z); b[5] = bf16_hi(yv.z);
+            b[6] = bf16_lo(yv.w); b[7] = bf16_hi(yv.w);
+            float o[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                dot[k] = fmaf(a[q], b[q], dot[k]);
+                o[q] = a[q] * w;
+            }
+            dy_disp[pos * D8 + c] = pack8(o);
+        }
+    }
+    if (dp == nullptr) return;
+#pragma unroll
+    for (int k = 0; k < 32; ++k) {
+        if (k >= K) break;
+        float v = dot[k];
+#pragma unroll
+        for (int m = 32; m > 0; m >>= 1) v += __shfl_xor(v, m);
+        if (lane == 0) part[k][wave] = v;
+    }
+    __syncthreads();
+    const int nw = blockDim.x >> 6;
+    if (tid < K) {
+        float v = 0.f;
+        for (int q = 0; q < nw; ++q) v += part[tid][q];
+        dp[t * K + tid] = v;
     }
 }
 
@@ -357,7 +368,8 @@ hipError_t launch_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const 
                               const int32_t* inv_perm, int64_t S, int D, int K, moe_bf16* dy_disp,
                               float* dp, hipStream_t st) {
     if (S == 0) return hipSuccess;
-    hipLaunchKernelGGL(combine_bwd_kernel, dim3(grid_for(S, kRowTok)), dim3(kRowThreads), 0, st,
+    const int d8 = D / 8;
+    hipLaunchKernelGGL(combine_bwd_kernel, dim3((unsigned)S), dim3(d8 >= 1024 ? 1024 : (d8 + 63) / 64 * 64), 0, st,
                        (const uint4*)dy, (const uint4*)y_disp, p_disp, inv_perm, S, D / 8, K,
                        (uint4*)dy_disp, dp);
     return hipGetLastError();
