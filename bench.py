@@ -19,6 +19,7 @@ import argparse
 import json
 import math
 import os
+import statistics
 import sys
 import time
 from pathlib import Path
@@ -187,6 +188,34 @@ def time_region(fn, reps, stream):
     return start.elapsed_time(end) / reps * 1e-3   # seconds
 
 
+def step_times(fn, reps, stream):
+    """Durations (us) of reps back-to-back calls fn(i), one HIP event pair
+    per call on `stream`."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    torch.cuda.synchronize()
+    for i in range(reps):
+        ev[i][0].record(stream)
+        fn(i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) * 1e3 for a, b in ev]
+
+
+def filtered_mean(xs):
+    """Mean after iteratively dropping samples above mean + 1.5 standard
+    deviations, until none is dropped."""
+    xs = list(xs)
+    while len(xs) > 2:
+        m = sum(xs) / len(xs)
+        sd = (sum((x - m) ** 2 for x in xs) / len(xs)) ** 0.5
+        kept = [x for x in xs if x <= m + 1.5 * sd]
+        if len(kept) == len(xs):
+            break
+        xs = kept
+    return sum(xs) / len(xs)
+
+
 def time_layer_gemms(_lib, sets, out, s, reps, stream, ws_router, ws_route, r_bufs, xd, pd, h, yd):
     """Average durations (s) of the up and down grouped GEMM launches inside
     the layer's launch sequence, one HIP event pair per launch on `stream`."""
@@ -323,6 +352,10 @@ def main():
     t_layer = time_region(step, args.steps, stream)
     slots = s.S * s.K
     value = slots / t_layer
+    # the same steps once more, each with its own events, for the paper's
+    # per-step statistics (median and the mean after iteratively dropping
+    # samples above mean + 1.5 sigma); not part of the timed region above
+    per_step = step_times(step, args.steps, stream)
 
     # ---- per-stage timings on the same stream, same launch configuration ----
     out = lf.out
@@ -515,6 +548,9 @@ def main():
                    **({"score": s.score, "Fs": s.Fs, "seq_len": s.seq_len, "aux_coeff": s.aux_coeff}
                       if prod else {})},
         "roofline": roofline, "stages": stages, "cpu_baseline": cpu,
+        "layer_step_us": {"n": len(per_step), "median": round(statistics.median(per_step), 2),
+                          "filtered_mean": round(filtered_mean(per_step), 2),
+                          "min": round(min(per_step), 2), "max": round(max(per_step), 2)},
         # Eq. 1: forward dispatch payload with bf16 and with MX-FP8 hidden elements
         "payload": {"timed": args.payload, "eq1_dispatch_bytes_bf16": _lib.moe_payload_bytes(s.S, s.K, s.D),
                     "eq1_dispatch_bytes_mxfp8": _lib.moe_mx_payload_bytes(s.S, s.K, s.D),
