@@ -54,6 +54,9 @@ def parse():
     p.add_argument("--cpu-tokens", type=int, default=0,
                    help="tokens of the batch the CPU oracle runs (0: the whole batch)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--ep-share", type=int, default=0, metavar="G",
+                   help="also time the expert-local grouped GEMMs one GPU would run under expert "
+                        "parallelism over G GPUs (E/G experts, the same S*K rows); reported apart")
     p.add_argument("--calib-bytes", type=int, default=1 << 30,
                    help="size of the plain copy run once for counter calibration")
     p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -214,6 +217,38 @@ def filtered_mean(xs):
             break
         xs = kept
     return sum(xs) / len(xs)
+
+
+def ep_share(_lib, s, G, reps, stream, dev):
+    """Up and down grouped GEMM of one GPU's share under expert parallelism
+    over G GPUs: its E/G experts receive, on balanced routing, all S*K rows
+    (each of the G GPUs sends it S*K/G).  Seeded balanced segments, fresh
+    weights of the workload's widths."""
+    import torch
+    from paper_2608_28511_amd.workloads import make_segments
+    if s.E % G:
+        return {"G": G, "skipped": f"E = {s.E} is not a multiple of G"}
+    E_loc, R = s.E // G, s.S * s.K
+    g = torch.Generator(device=dev).manual_seed(s.seed)
+    off = make_segments(R, E_loc, seed=s.seed).to(dev)
+    x = torch.randn((R, s.D), generator=g, device=dev).to(torch.bfloat16)
+    W1 = [(torch.randn((E_loc, s.D, s.F), generator=g, device=dev) / math.sqrt(s.D)).to(torch.bfloat16)
+          for _ in range(2)]
+    W2 = [(torch.randn((E_loc, s.F, s.D), generator=g, device=dev) / math.sqrt(s.F)).to(torch.bfloat16)
+          for _ in range(2)]
+    h = torch.empty((R, s.F), dtype=torch.bfloat16, device=dev)
+    y = torch.empty((R, s.D), dtype=torch.bfloat16, device=dev)
+    sched = torch.empty(_lib.moe_grouped_schedule_bytes(E_loc, R) // 4 + 1, dtype=torch.int32, device=dev)
+    _lib.moe_grouped_schedule(off, E_loc, R, sched)
+    up = lambda i: _lib.moe_grouped_gemm(x, sched, E_loc, R, s.D, s.F, W1[i % 2], 1, h, None)
+    down = lambda i: _lib.moe_grouped_gemm(h, sched, E_loc, R, s.F, s.D, W2[i % 2], 0, y, None)
+    for i in range(3):
+        up(i); down(i)
+    t_up, t_down = time_region(up, reps, stream), time_region(down, reps, stream)
+    fl = 2.0 * R * s.D * s.F
+    return {"G": G, "E_local": E_loc, "rows": R, "rows_per_expert": R // E_loc,
+            "up_us": round(t_up * 1e6, 1), "down_us": round(t_down * 1e6, 1),
+            "up_TFLOPs": round(fl / t_up / 1e12, 1), "down_TFLOPs": round(fl / t_down / 1e12, 1)}
 
 
 def time_layer_gemms(_lib, sets, out, s, reps, stream, ws_router, ws_route, r_bufs, xd, pd, h, yd):
@@ -548,6 +583,7 @@ def main():
                    **({"score": s.score, "Fs": s.Fs, "seq_len": s.seq_len, "aux_coeff": s.aux_coeff}
                       if prod else {})},
         "roofline": roofline, "stages": stages, "cpu_baseline": cpu,
+        **({"ep_share": ep_share(_lib, s, args.ep_share, reps, stream, dev)} if args.ep_share > 1 else {}),
         "layer_step_us": {"n": len(per_step), "median": round(statistics.median(per_step), 2),
                           "filtered_mean": round(filtered_mean(per_step), 2),
                           "min": round(min(per_step), 2), "max": round(max(per_step), 2)},
