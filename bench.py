@@ -41,8 +41,8 @@ def log(*a):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--settle-seconds", type=float, default=0.3,
                    help="run the layer this long before the warm-up steps, so the GPU is at its "
                         "sustained clock when the timed steps start")
