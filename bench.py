@@ -79,7 +79,8 @@ GEMM_SOURCES = ("gemm.hip", "tile_dma.h", "kernels.h", "common.h")
 # flag (up: squared-ReLU epilogue; down: plain bf16); the tile height is
 # chosen inside the kernel.
 KERNEL_NAME = {"grouped_up": ("gemm_rows_kernel<false, 1, false>",),
-               "grouped_down": ("gemm_rows_kernel<false, 0, false>",)}
+               "grouped_down": ("gemm_rows_kernel<false, 0, false>",),
+               "grouped_up_mxfp8": ("gemm_rows_mx_kernel<1, false>",)}
 
 
 def kernel_match(kernel, name):
@@ -251,9 +252,10 @@ def ep_share(_lib, s, G, reps, stream, dev):
             "up_TFLOPs": round(fl / t_up / 1e12, 1), "down_TFLOPs": round(fl / t_down / 1e12, 1)}
 
 
-def time_layer_gemms(_lib, sets, out, s, reps, stream, ws_router, ws_route, r_bufs, xd, pd, h, yd):
+def time_layer_gemms(_lib, sets, out, s, reps, stream, ws_router, ws_route, r_bufs, xd, pd, h, yd, mx=None):
     """Average durations (s) of the up and down grouped GEMM launches inside
-    the layer's launch sequence, one HIP event pair per launch on `stream`."""
+    the layer's launch sequence, one HIP event pair per launch on `stream`.
+    mx = (codes, scales): the MX-FP8 payload, read as sent by the up GEMM."""
     import torch
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
     lg = torch.empty_like(out["logits"])
@@ -265,10 +267,16 @@ def time_layer_gemms(_lib, sets, out, s, reps, stream, ws_router, ws_route, r_bu
         _lib.moe_router_logits(inp["x"], inp["Wr"], inp["bias"], s.S, s.D, s.E, lg, ws_router)
         _lib.moe_route_topk(lg, s.S, s.E, s.K, r_bufs["topk_idx"], r_bufs["topk_prob"], r_bufs["counts"],
                             r_bufs["offsets"], r_bufs["perm"], r_bufs["inv_perm"], ws_route)
-        _lib.moe_dispatch(inp["x"], r_bufs["topk_prob"], r_bufs["inv_perm"], s.S, s.D, s.K, xd, pd)
+        if mx is None:
+            _lib.moe_dispatch(inp["x"], r_bufs["topk_prob"], r_bufs["inv_perm"], s.S, s.D, s.K, xd, pd)
+        else:
+            _lib.moe_dispatch_mxfp8(inp["x"], r_bufs["topk_prob"], r_bufs["inv_perm"], s.S, s.D, s.K, *mx, pd)
         _lib.moe_grouped_schedule(r_bufs["offsets"], s.E, s.R, sched)
         ev[i][0].record(stream)
-        _lib.moe_grouped_gemm(xd, sched, s.E, s.R, s.D, s.F, inp["W1"], 1, h, None)
+        if mx is None:
+            _lib.moe_grouped_gemm(xd, sched, s.E, s.R, s.D, s.F, inp["W1"], 1, h, None)
+        else:
+            _lib.moe_grouped_gemm_mxfp8(*mx, sched, s.E, s.R, s.D, s.F, inp["W1"], 1, h, None)
         ev[i][1].record(stream)
         ev[i][2].record(stream)
         _lib.moe_grouped_gemm(h, sched, s.E, s.R, s.F, s.D, inp["W2"], 0, yd, None)
@@ -356,6 +364,9 @@ def main():
     sets = [make_inputs(s, device=dev, seed=s.seed + 1000 * i) for i in range(args.sets)]
     modes = dict(score=s.score, Fs=s.Fs, seq_len=s.seq_len, aux_coeff=s.aux_coeff)
     lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, payload=args.payload, **modes)
+    mx_run = args.payload == "mxfp8"
+    if mx_run:
+        lf.out["x_disp"] = None   # the up projection reads the payload as sent: no decode pass
 
     # a plain device copy of known size, once, so hardware byte counters can be
     # calibrated against it in profiler runs of this same command
@@ -425,7 +436,7 @@ def main():
         st["seq_aux_loss"] = time_region(
             lambda i: _lib.moe_seq_aux_loss(out["logits"], out["topk_idx"], s.S, s.E, s.K, s.seq_len, s.aux_coeff,
                                             loss2, cnt2, ws_aux), reps, stream)
-    xd2 = torch.empty_like(out["x_disp"])
+    xd2 = torch.empty((s.R, s.D), dtype=torch.bfloat16, device=dev)
     pd2 = torch.empty_like(out["p_disp"])
     x_r = [(st_["x"] if not s.H else out["x_lat"]) for st_ in sets]
     st["dispatch"] = time_region(
@@ -433,13 +444,19 @@ def main():
                                     s.K, xd2, pd2), reps, stream)
     if s.D % 32 == 0:
         xq2 = torch.empty((s.R, s.D), dtype=torch.uint8, device=dev)
-        xs2 = torch.empty((s.R, s.D // 32), dtype=torch.uint8, device=dev)
+        xs2 = layer.mx_scales(s.R, s.D, dev)
         st["dispatch_mxfp8"] = time_region(
             lambda i: _lib.moe_dispatch_mxfp8(x_r[i % len(x_r)], out["topk_prob"], out["inv_perm"], s.S, s.D, s.K,
                                               xq2, xs2, pd2), reps, stream)
         st["mxfp8_dequant"] = time_region(lambda i: _lib.moe_mxfp8_dequant(xq2, xs2, s.R, s.D, xd2), reps, stream)
     sched = layer.grouped_schedule(out["offsets"], s.E, s.R)
     h2 = torch.empty_like(out["h"])
+    if s.D % 32 == 0:
+        # the up projection reading the MX-FP8 payload as sent (decode in its operand path)
+        _lib.moe_dispatch_mxfp8(x_r[0], out["topk_prob"], out["inv_perm"], s.S, s.D, s.K, xq2, xs2, pd2)
+        st["grouped_up_mxfp8"] = time_region(
+            lambda i: _lib.moe_grouped_gemm_mxfp8(xq2, xs2, sched, s.E, s.R, s.D, s.F, sets[i % len(sets)]["W1"],
+                                                  1, h2, None), reps, stream)
     yd2 = torch.empty_like(out["y_disp"])
     # the two grouped GEMMs inside the layer's own launch sequence (router,
     # route, dispatch, schedule, up, down, combine per input set), each GEMM
@@ -447,11 +464,15 @@ def main():
     # clock conditions of the timed layer steps
     if not prod and not s.H:
         st["grouped_up"], st["grouped_down"] = time_layer_gemms(
-            _lib, sets, out, s, reps, stream, ws_router, ws_route, r_bufs, xd2, pd2, h2, yd2)
+            _lib, sets, out, s, reps, stream, ws_router, ws_route, r_bufs, xd2, pd2, h2, yd2,
+            mx=(xq2, xs2) if mx_run else None)
     else:
-        st["grouped_up"] = time_region(
-            lambda i: _lib.moe_grouped_gemm(out["x_disp"], sched, s.E, s.R, s.D, s.F,
-                                            sets[i % len(sets)]["W1"], 1, h2, None), reps, stream)
+        if mx_run:
+            st["grouped_up"] = st["grouped_up_mxfp8"]
+        else:
+            st["grouped_up"] = time_region(
+                lambda i: _lib.moe_grouped_gemm(out["x_disp"], sched, s.E, s.R, s.D, s.F,
+                                                sets[i % len(sets)]["W1"], 1, h2, None), reps, stream)
         st["grouped_down"] = time_region(
             lambda i: _lib.moe_grouped_gemm(out["h"], sched, s.E, s.R, s.F, s.D,
                                             sets[i % len(sets)]["W2"], 0, yd2, None), reps, stream)
@@ -562,9 +583,11 @@ def main():
 
     dom = max(("grouped_up", "grouped_down"), key=lambda k: st[k])
     achieved = gemm_flops / st[dom] / 1e12
-    roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1),
+    # on the MX payload the timed up projection is the kernel that decodes it
+    dom_kernel = "grouped_up_mxfp8" if mx_run and dom == "grouped_up" else dom
+    roofline = {"bound": "mfma", "kernel": dom_kernel, "achieved": round(achieved, 1),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": load_traffic(dom, s.name),
+                "traffic": load_traffic(dom_kernel, s.name),
                 "per_launch": f"2*R*D*F = {gemm_flops:.4g} flop per launch (R = S*K = {s.R})"}
 
     cpu = None

@@ -254,7 +254,8 @@ typedef struct {
     /* Dispatch payload precision (Section 1's precision lever on b_x). */
     int32_t payload;           /* MOE_PAYLOAD_BF16 or MOE_PAYLOAD_MXFP8 (D a multiple of 32) */
     uint8_t* x_q;              /* [S*K, D] MX-FP8 codes, exported or NULL */
-    uint8_t* x_scale;          /* [S*K, D/32] their E8M0 block scales, exported or NULL */
+    uint8_t* x_scale;          /* [S*K, D/32] their E8M0 block scales, exported (in an allocation
+                                  of moe_mx_scale_alloc_bytes(S*K, D) bytes) or NULL */
 } moe_layer_fwd_args;
 
 enum { MOE_PAYLOAD_BF16 = 0, MOE_PAYLOAD_MXFP8 = 1 };
@@ -268,8 +269,10 @@ size_t moe_layer_fwd_workspace_bytes(const moe_layer_fwd_args* a);
 /* [x_lat = bf16(x @ Wdown)] -> logits -> route -> dispatch -> experts ->
  * combine -> [y = bf16(y_lat @ Wup)], all enqueued on `stream`.
  * With payload = MOE_PAYLOAD_MXFP8 the dispatch sends MX-FP8 rows
- * (moe_dispatch_mxfp8) and the experts read their decoded bf16 values
- * (moe_mxfp8_dequant into x_disp).
+ * (moe_dispatch_mxfp8) and the up projection reads them as sent
+ * (moe_grouped_gemm_mxfp8: the decoded bf16 values, decoded in its operand
+ * path); x_disp, if exported, receives the decoded rows (moe_mxfp8_dequant)
+ * and is not written otherwise.
  * With score_fn = MOE_SCORE_SIGMOID the route is moe_route_sigmoid (with
  * sel_bias); seq_len > 0 adds moe_seq_aux_loss; Fs > 0 runs the shared
  * expert and adds its fp32 output in the combine, before the one bf16
@@ -388,6 +391,29 @@ int moe_dispatch_mxfp8(const moe_bf16* x, const float* topk_prob, const int32_t*
  * bf16's normal range rounded to nearest even).  out [R, D] bf16. */
 int moe_mxfp8_dequant(const uint8_t* x_q, const uint8_t* x_scale, int64_t R, int32_t D, moe_bf16* out,
                       hipStream_t stream);
+
+/* Bytes to allocate for R rows of E8M0 scales of D-element rows when the
+ * grouped GEMM below reads them: R * D/32 rounded up to a multiple of 4 (it
+ * reads whole 4-byte words; the pad bytes are never used).  0 if D is not a
+ * positive multiple of 32. */
+uint64_t moe_mx_scale_alloc_bytes(int64_t R, int32_t D);
+
+/* moe_grouped_gemm with the MX-FP8 payload as its A operand, decoded inside
+ * the operand path (the up projection reading the dispatch payload as sent,
+ * with no separate decode pass):
+ *   C[r, :] = epi( decode(x_q, x_scale)[r, :] @ W[e] ),  r in expert e's segment
+ * where decode is exactly moe_mxfp8_dequant, so C (and u_save) are
+ * bit-identical to moe_mxfp8_dequant followed by moe_grouped_gemm.
+ *   x_q [R, Kd] uint8 codes (16-byte aligned), Kd a multiple of 32;
+ *   x_scale [R, Kd/32] uint8 scales as written by moe_dispatch_mxfp8, in an
+ *   allocation of at least moe_mx_scale_alloc_bytes(R, Kd) bytes;
+ *   sched, W, epilogue, C, u_save as in moe_grouped_gemm.
+ * The codes must be ones the encoder emits (no E4M3 NaN code; scale bytes
+ * at most 246), as every payload of moe_dispatch_mxfp8 is.
+ * Errors: as moe_grouped_gemm, plus Kd % 32 != 0 (MOE_ERR_SHAPE). */
+int moe_grouped_gemm_mxfp8(const uint8_t* x_q, const uint8_t* x_scale, const void* sched, int32_t E, int64_t R,
+                           int32_t Kd, int32_t N, const moe_bf16* W, int32_t epilogue, moe_bf16* C,
+                           moe_bf16* u_save, hipStream_t stream);
 
 /* ---------------------------------------------------------------------- */
 /* The paper's production router and shared expert (Section 5.2): sigmoid  */

@@ -96,6 +96,8 @@ _PROTOS = {
     "moe_mx_payload_bytes": (C.c_uint64, [i64, i32, i32]),
     "moe_dispatch_mxfp8": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp, vp, vp]),
     "moe_mxfp8_dequant": (C.c_int, [vp, vp, i64, i32, vp, vp]),
+    "moe_mx_scale_alloc_bytes": (C.c_uint64, [i64, i32]),
+    "moe_grouped_gemm_mxfp8": (C.c_int, [vp, vp, vp, i32, i64, i32, i32, vp, i32, vp, vp, vp]),
     "moe_shared_expert_bwd": (C.c_int, [vp, vp, vp, vp, vp, vp, i64, i32, i32, vp, i32, vp, vp, vp, sz, vp]),
 }
 
@@ -398,3 +400,17 @@ def moe_dispatch_mxfp8(x, topk_prob, inv_perm, S, D, K, x_q, x_scale, p_disp):
 def moe_mxfp8_dequant(x_q, x_scale, R, D, out):
     _check(load().moe_mxfp8_dequant(_ptr(x_q, U8, "x_q"), _ptr(x_scale, U8, "x_scale"), R, D,
                                     _ptr(out, BF16, "out"), _stream()), "moe_mxfp8_dequant")
+
+
+def moe_mx_scale_alloc_bytes(R, D) -> int:
+    return load().moe_mx_scale_alloc_bytes(R, D)
+
+
+def moe_grouped_gemm_mxfp8(x_q, x_scale, sched, E, R, Kd, N, W, epilogue, Cout, u_save):
+    if x_scale is not None and (x_scale.untyped_storage().nbytes() - x_scale.storage_offset()
+                                < moe_mx_scale_alloc_bytes(R, Kd)):
+        raise ValueError("x_scale's allocation must hold moe_mx_scale_alloc_bytes(R, Kd) bytes")
+    _check(load().moe_grouped_gemm_mxfp8(_ptr(x_q, U8, "x_q"), _ptr(x_scale, U8, "x_scale"),
+                                         _ptr(sched, None, "sched"), E, R, Kd, N, _ptr(W, BF16, "W"), epilogue,
+                                         _ptr(Cout, BF16, "C"), _ptr(u_save, BF16, "u_save"), _stream()),
+           "moe_grouped_gemm_mxfp8")

@@ -249,6 +249,33 @@ int moe_grouped_gemm(const moe_bf16* A, const void* sched, int32_t E, int64_t R,
                                                u_save, sched, E, R, N, Kd, stream));
 }
 
+uint64_t moe_mx_scale_alloc_bytes(int64_t R, int32_t D) {
+    if (R < 0 || D < 32 || D % 32 != 0) return 0;
+    return ((uint64_t)R * (uint64_t)(D / 32) + 3) / 4 * 4;
+}
+
+int moe_grouped_gemm_mxfp8(const uint8_t* x_q, const uint8_t* x_scale, const void* sched, int32_t E, int64_t R,
+                           int32_t Kd, int32_t N, const moe_bf16* W, int32_t epilogue, moe_bf16* C,
+                           moe_bf16* u_save, hipStream_t stream) {
+    if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(Kd) || !dim_ok(N) || Kd % 32 != 0)
+        return MOE_ERR_SHAPE;
+    if (epilogue != 0 && epilogue != 1) return MOE_ERR_UNSUPPORTED;
+    if (!weight_ok(Kd, N)) return MOE_ERR_UNSUPPORTED;
+    if ((int64_t)moe_mx_scale_alloc_bytes(R, Kd) >= kMaxOperandBytes) return MOE_ERR_UNSUPPORTED;
+    if (epilogue == 0 && u_save != nullptr) return MOE_ERR_SHAPE;
+    MOE_TRY(need(x_q, (uint64_t)R * Kd, 16));
+    MOE_TRY(need(x_scale, moe_mx_scale_alloc_bytes(R, Kd), 1));
+    if (sched == nullptr) return MOE_ERR_NULL;
+    MOE_TRY(opt(sched, 16));
+    MOE_TRY(need(W, (uint64_t)E * Kd * N * 2, 16));
+    MOE_TRY(need(C, (uint64_t)R * N * 2, 16));
+    MOE_TRY(opt(u_save, 16));
+    if (R == 0) return MOE_OK;
+    return hip_status(moe::launch_grouped_rows_mx(x_q, x_scale, W, N, (int64_t)Kd * N, C, N,
+                                                  epilogue == 1 ? moe::EPI_RELU2 : moe::EPI_BF16, u_save, sched,
+                                                  E, R, N, Kd, stream));
+}
+
 int moe_latent_proj(const moe_bf16* A, const moe_bf16* W, int64_t M, int32_t Kd, int32_t N, moe_bf16* C,
                     hipStream_t stream) {
     if (M < 0 || M >= kMaxRows || !dim_ok(Kd) || !dim_ok(N)) return MOE_ERR_SHAPE;
@@ -337,7 +364,10 @@ size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
     b->offsets = pick(a->offsets, (size_t)(E + 1) * 4);
     b->perm = pick(a->perm, (size_t)R * 4);
     b->inv_perm = pick(a->inv_perm, (size_t)R * 4);
-    b->x_disp = pick(a->x_disp, (size_t)R * D * 2);
+    const bool mx = a->payload == MOE_PAYLOAD_MXFP8;
+    // the MX payload feeds the up projection as sent; x_disp (its decode)
+    // exists only when the caller exports it
+    b->x_disp = mx ? a->x_disp : pick(a->x_disp, (size_t)R * D * 2);
     b->p_disp = pick(a->p_disp, (size_t)R * 4);
     b->h = pick(a->h, (size_t)R * F * 2);
     b->y_disp = pick(a->y_disp, (size_t)R * D * 2);
@@ -351,9 +381,8 @@ size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
         b->aux_ws = c.take(moe::seq_aux_ws_bytes(S, E, a->seq_len));
         b->seq_counts = pick(a->seq_counts, (size_t)(S / a->seq_len) * E * 4);
     }
-    const bool mx = a->payload == MOE_PAYLOAD_MXFP8;
     b->x_q = mx ? pick(a->x_q, (size_t)R * D) : nullptr;
-    b->x_scale = mx ? pick(a->x_scale, (size_t)R * (D / 32)) : nullptr;
+    b->x_scale = mx ? pick(a->x_scale, (size_t)moe_mx_scale_alloc_bytes(R, D)) : nullptr;
     b->h_s = a->Fs ? pick(a->h_s, (size_t)S * a->Fs * 2) : nullptr;
     b->y_s = a->Fs ? pick(a->y_s, (size_t)S * D * 4) : nullptr;
     return c.used;
@@ -419,18 +448,23 @@ int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
                                          aux_coef(a->aux_coeff, S, E, K, a->seq_len), a->aux_loss,
                                          b.seq_counts, b.aux_ws, stream));
     }
-    if (a->payload == MOE_PAYLOAD_MXFP8) {
-        MOE_HIP(moe::launch_dispatch_mx(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_q, b.x_scale, b.p_disp, stream));
-        MOE_HIP(moe::launch_dequant_mx(b.x_q, b.x_scale, R, D, b.x_disp, stream));
+    // the dispatch launch also builds the grouped GEMM's tile tables
+    const bool mx = a->payload == MOE_PAYLOAD_MXFP8;
+    if (mx) {
+        MOE_HIP(moe::launch_dispatch_mx(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_q, b.x_scale, b.p_disp, stream,
+                                        R > 0 ? b.offsets : nullptr, E, R > 0 ? b.sched : nullptr));
+        if (b.x_disp != nullptr) MOE_HIP(moe::launch_dequant_mx(b.x_q, b.x_scale, R, D, b.x_disp, stream));
     } else {
-        // the dispatch launch also builds the grouped GEMM's tile tables
         MOE_HIP(moe::launch_dispatch(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_disp, b.p_disp, stream,
                                      R > 0 ? b.offsets : nullptr, E, R > 0 ? b.sched : nullptr));
     }
     if (R > 0) {
-        if (a->payload == MOE_PAYLOAD_MXFP8) MOE_HIP(moe::launch_tile_schedule(b.offsets, E, R, b.sched, stream));
-        MOE_HIP(moe::launch_grouped_rows(b.x_disp, D, a->W1, F, (int64_t)D * F, false, b.h, F,
-                                         moe::EPI_RELU2, nullptr, a->u_save, b.sched, E, R, F, D, stream));
+        if (mx)
+            MOE_HIP(moe::launch_grouped_rows_mx(b.x_q, b.x_scale, a->W1, F, (int64_t)D * F, b.h, F, moe::EPI_RELU2,
+                                                a->u_save, b.sched, E, R, F, D, stream));
+        else
+            MOE_HIP(moe::launch_grouped_rows(b.x_disp, D, a->W1, F, (int64_t)D * F, false, b.h, F,
+                                             moe::EPI_RELU2, nullptr, a->u_save, b.sched, E, R, F, D, stream));
         MOE_HIP(moe::launch_grouped_rows(b.h, F, a->W2, D, (int64_t)F * D, false, b.y_disp, D,
                                          moe::EPI_BF16, nullptr, nullptr, b.sched, E, R, D, F, stream));
     }

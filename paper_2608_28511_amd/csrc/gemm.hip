@@ -78,21 +78,89 @@ constexpr int kEpiBytes = kWaves * kEpiWaveBytes;  // 16 KB
 constexpr int kGroupM = 8;
 
 // Block tile BM x BN with KD contraction elements per ring stage and a ring
-// of STAGES stages.
-template <int BM_, int KD_, int STAGES_>
+// of STAGES stages.  AMX: A is MX-FP8 (codes, one byte per element, and the
+// stage's block scales; see MxDma) instead of bf16.
+template <int BM_, int KD_, int STAGES_, bool AMX_ = false>
 struct Tile {
     static constexpr int BM = BM_, KD = KD_, kStages = STAGES_;
+    static constexpr bool kAmx = AMX_;
     static constexpr int MI = BM / 32;          // A fragments (16 rows) per wave: waves cover BM/2 rows
     static constexpr int kKK = KD / 32;         // MFMA k steps per stage
-    static constexpr int kABytes = BM * KD * 2, kBBytes = BN * KD * 2;
+    static constexpr int kCodeBytes = BM * KD;  // AMX: the stage's codes, then its scale words
+    static constexpr int kSclBytes = AMX_ ? kWaves * 64 * 4 : 0;
+    static constexpr int kABytes = AMX_ ? kCodeBytes + kSclBytes : BM * KD * 2;
+    static constexpr int kBBytes = BN * KD * 2;
     static constexpr int kStageBytes = kABytes + kBBytes;
     static constexpr int kRingBytes = kStages * kStageBytes;
     static constexpr int kFrag = 16 * KD * 2;   // bytes between 16-row fragments of the row layout
+    static constexpr int kFragA = AMX_ ? 16 * KD : kFrag;
 };
 using TileS = Tile<128, 64, 3>;   // 144 KB ring (+16 KB epilogue staging)
 using TileL = Tile<256, 32, 4>;   // 128 KB ring
-static_assert(TileS::kRingBytes + kEpiBytes <= 160 * 1024 && TileL::kRingBytes + kEpiBytes <= 160 * 1024,
+using TileSX = Tile<128, 64, 3, true>;   // MX-FP8 A: 126 KB ring
+using TileLX = Tile<256, 32, 4, true>;   // 104 KB ring
+static_assert(TileS::kRingBytes + kEpiBytes <= 160 * 1024 && TileL::kRingBytes + kEpiBytes <= 160 * 1024 &&
+                  TileSX::kRingBytes + kEpiBytes <= 160 * 1024 && TileLX::kRingBytes + kEpiBytes <= 160 * 1024,
               "LDS budget");
+
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// MX-FP8 A operand (codes [R, Kd] uint8, E8M0 scales [R, Kd / 32] uint8):
+// per stage each wave copies one 16-byte chunk of codes (rows of KD bytes,
+// fp8 row layout) and one scale word.  A row's scale bytes are not 4-byte
+// aligned, so every row gets a window of kLPR words starting at the aligned
+// word at or below its first block of the stage; the fragment read takes its
+// byte at offset (row * nb + kb) & 3 of the window.  The scale descriptor
+// spans the whole array rounded up to 4 bytes: rows past R read zero, and
+// rows past a tile's end (zero codes) read other rows' finite scales.
+template <class T>
+struct MxDma {
+    static constexpr int kLPR = kWaves * 64 / T::BM;   // scale words per row
+    static_assert(kLPR * T::BM == kWaves * 64 && 3 + T::kKK <= 4 * kLPR, "scale window");
+    static constexpr int kSlots = 2;                     // copies per wave and stage
+    DmaTile<true, T::BM, T::KD / 2, kWaves, 1> codes;    // code pairs as 16-bit elements
+    static_assert(decltype(codes)::kSlots == 1, "one code chunk per wave and stage");
+    i32x4 srs;       // wave-uniform
+    uint32_t srow;   // (row0 + this lane's window row) * nb
+    uint32_t sword;  // byte of this lane's word in the window
+    uint32_t kb;     // first block of the next stage
+
+    __device__ __forceinline__ void init(const uint8_t* q, const uint8_t* scale, uint32_t scale_bytes,
+                                         int64_t row0, int64_t row_hi, int Kd, int wave, int lane) {
+        codes.init((const uint16_t*)q, Kd / 2, row0, row_hi, 0, Kd / 2, wave, lane);
+        srs = buf_rsrc(scale, scale_bytes);
+        const int p = wave * 64 + lane;
+        srow = (uint32_t)((row0 + p / kLPR) * (Kd / 32));
+        sword = (uint32_t)(4 * (p % kLPR));
+        kb = 0;
+    }
+    template <bool KTAIL, int I0, int I1>
+    __device__ __forceinline__ void issue(uint32_t tile_lds, int64_t k_rem, int wave) {
+        codes.template issue<KTAIL, 0, 1>(tile_lds, k_rem / 2, wave);
+        dma4(srs, ((srow + kb) & ~3u) + sword, tile_lds + T::kCodeBytes + (uint32_t)wave * 256u);
+        kb += T::kKK;
+    }
+};
+
+// bf16 MFMA fragment of 8 MX-FP8 codes sharing one E8M0 scale byte s8:
+// code * 2^(s8 - 127).  v_cvt_scalef32_pk_bf16_fp8 takes the scale from the
+// exponent field of an fp32 operand; for every finite code at every scale
+// byte up to 246 (the largest the encoder emits) its result equals the exact
+// decode, bf16 subnormals included (checked exhaustively on gfx950).
+__device__ __forceinline__ bf16x8 mx_frag(u32x2 c, uint32_t s8) {
+    const float sc = __uint_as_float(s8 << 23);
+    const bf16x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c[0], sc, false);
+    const bf16x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c[0], sc, true);
+    const bf16x2 p2 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c[1], sc, false);
+    const bf16x2 p3 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c[1], sc, true);
+    const u32x4 w = {__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1),
+                     __builtin_bit_cast(uint32_t, p2), __builtin_bit_cast(uint32_t, p3)};
+    return __builtin_bit_cast(bf16x8, w);
+}
 
 struct GemmArgs {
     const uint16_t* A;
@@ -105,6 +173,8 @@ struct GemmArgs {
     const int32_t* mtile_total;  // ROWS mode with tiles: device count of valid 128-row m-tiles
     const int4* tiles_l;      // the same for 256-row tiles
     const int32_t* mtile_total_l;
+    const uint8_t* A_scale;   // MX-FP8 A: E8M0 scales [R, Kd / 32]
+    uint32_t scale_bytes;     // R * Kd / 32 rounded up to a multiple of 4
     int64_t lda, ldb, ldc;
     int64_t b_stride;         // elements between experts' B (ROWS mode)
     int64_t c_stride;         // elements between experts' C (KGRP mode)
@@ -137,10 +207,12 @@ __device__ __forceinline__ void wait_stage(int cur, int total) {
 // ahead (half of B after the second k step's reads when a stage has two),
 // and accumulate.  `next` says whether there is a stage to copy; nrem is the
 // contraction length left from its start.
+// AMX: sb is the lane's scale byte of the stage's first block in slot 0.
 template <class T, bool A_K, bool B_K, bool KTAIL, int S, class DA, class DB, int NA, int NB>
 __device__ __forceinline__ void mma_stage(f32x4 (&acc)[T::MI][4], const uint32_t (&abase)[NA],
                                           const uint32_t (&bbase)[2][NB], DA& da, DB& db, bool next,
-                                          int64_t nrem, uint32_t ldsA, uint32_t ldsB, int wave) {
+                                          int64_t nrem, uint32_t ldsA, uint32_t ldsB, int wave,
+                                          uint32_t sb = 0) {
     constexpr int NS = (S + T::kStages - 1) % T::kStages;
     constexpr int kSA = DA::kSlots, kSB = DB::kSlots;
 #pragma unroll
@@ -148,8 +220,20 @@ __device__ __forceinline__ void mma_stage(f32x4 (&acc)[T::MI][4], const uint32_t
         bf16x8 af[T::MI], bfg[4];
 #pragma unroll
         for (int i = 0; i < T::MI; ++i) {
-            if constexpr (A_K) af[i] = lds_b128(abase[kk] + S * T::kABytes + i * T::kFrag);
-            else af[i] = lds_tr_pair(abase[i] + S * T::kABytes + kk * 64 * T::BM, 8 * T::BM);
+            if constexpr (T::kAmx) {
+                // volatile: the compiler would pair these reads (512 bytes
+                // apart) into ds_read2st64_b64, whose two addresses per lane
+                // share banks (measured: 2.6x the LDS cycles)
+                const u32x2 c =
+                    *(const volatile lds_u32x2*)(uintptr_t)(abase[kk] + S * T::kABytes + i * T::kFragA);
+                const uint32_t s8 =
+                    *(const lds_u8*)(uintptr_t)(sb + S * T::kABytes + i * 16 * 4 * MxDma<T>::kLPR + kk);
+                af[i] = mx_frag(c, s8);
+            } else if constexpr (A_K) {
+                af[i] = lds_b128(abase[kk] + S * T::kABytes + i * T::kFrag);
+            } else {
+                af[i] = lds_tr_pair(abase[i] + S * T::kABytes + kk * 64 * T::BM, 8 * T::BM);
+            }
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -182,8 +266,9 @@ __device__ __forceinline__ void frag_bases(uint32_t (&abase)[NA], uint32_t (&bba
                                            uint32_t ldsB, int wm, int wn, int lane) {
 #pragma unroll
     for (int i = 0; i < NA; ++i)
-        abase[i] = ldsA + (A_K ? row_base<T::KD>(wm * (T::BM / 2), i, lane)
-                               : col_base<T::BM>(wm * (T::BM / 2) + i * 16, lane));
+        abase[i] = ldsA + (T::kAmx ? mx_row_base<T::KD>(wm * (T::BM / 2), i, lane)
+                           : A_K  ? row_base<T::KD>(wm * (T::BM / 2), i, lane)
+                                  : col_base<T::BM>(wm * (T::BM / 2) + i * 16, lane));
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
         const uint32_t o = B_K ? row_base<T::KD>(wn * 64, j, lane) : col_base<BN>(wn * 64 + j * 16, lane);
@@ -323,10 +408,6 @@ __device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, const int4* til
     t.n0 = nt * BN;
     return t;
 }
-
-typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
-typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
 // Buffer descriptor over rows [row0, row0 + nrows) of a row-major bf16 matrix:
 // accesses at byte offsets >= nrows * ldc * 2 are dropped (stores) or read as
@@ -494,13 +575,17 @@ __device__ __forceinline__ void rows_body(const GemmArgs& p, char* smem, const i
     const uint32_t ldsB = lds0, ldsA = lds0 + kStages * T::kBBytes;
     const uint32_t ep = lds0 + T::kRingBytes + (uint32_t)wave * kEpiWaveBytes;
 
-    DmaTile<true, BM, KD> da;
+    using DA = std::conditional_t<T::kAmx, MxDma<T>, DmaTile<true, BM, KD>>;
+    DA da;
     DmaTile<B_K, BN, KD> db;
-    constexpr int kSA = DmaTile<true, BM, KD>::kSlots, kSB = DmaTile<B_K, BN, KD>::kSlots;
+    constexpr int kSA = DA::kSlots, kSB = DmaTile<B_K, BN, KD>::kSlots;
     constexpr int kPerStage = kSA + kSB;
     auto dma_tile = [&](int j) {
         const RowsTile t = rows_tile<BM>(p, tiles, m_count, lx + j * Gx, m_base);
-        da.init(p.A, p.lda, t.row0, t.row_hi, 0, p.Kd, wave, lane);
+        if constexpr (T::kAmx)
+            da.init((const uint8_t*)p.A, p.A_scale, p.scale_bytes, t.row0, t.row_hi, p.Kd, wave, lane);
+        else
+            da.init(p.A, p.lda, t.row0, t.row_hi, 0, p.Kd, wave, lane);
         db.init(p.B + (int64_t)t.e * p.b_stride, p.ldb, t.n0, (int64_t)p.N, 0, p.Kd, wave, lane);
     };
 
@@ -510,6 +595,16 @@ __device__ __forceinline__ void rows_body(const GemmArgs& p, char* smem, const i
 
     f32x4 acc[MI][4];
     zero_acc(acc);
+
+    // AMX: the lane's rows are r0 + 16 i; their scale windows sit 4 * kLPR
+    // bytes apart, and all share the in-window byte offset (row * nb + kb) & 3.
+    const int nb = p.Kd / 32;
+    const int r0_lane = wm * (BM / 2) + (lane & 15);
+    uint32_t sbase = 0, rnb = 0;
+    if constexpr (T::kAmx) {
+        sbase = ldsA + T::kCodeBytes + (uint32_t)r0_lane * 4u * MxDma<T>::kLPR;
+        rnb = (uint32_t)(r0_lane * nb);
+    }
 
     // DMA of the first kStages - 1 steps; kd / jd track the next step to send.
     int kd = 0, jd = 0;
@@ -540,7 +635,10 @@ __device__ __forceinline__ void rows_body(const GemmArgs& p, char* smem, const i
                             cur.row_hi - (cur.row0 + wm * (BM / 2)), cur.n0 + wn * 64, lane);
         const bool next = g + kStages - 1 < g_total;
         if (next && kd == 0) dma_tile(jd);
-        mma_stage<T, true, B_K, KTAIL, S>(acc, abase, bbase, da, db, next, p.Kd - kd * KD, ldsA, ldsB, wave);
+        uint32_t sb = 0;
+        if constexpr (T::kAmx) sb = sbase + (((uint32_t)(cur.row0 * nb + kc * T::kKK) + rnb) & 3u);
+        mma_stage<T, true, B_K, KTAIL, S>(acc, abase, bbase, da, db, next, p.Kd - kd * KD, ldsA, ldsB, wave,
+                                          sb);
         if (++kd == nk) { kd = 0; ++jd; }
         if (kc == nk - 1) {
             const int rbase = cur.row0 + wm * (BM / 2);
@@ -607,6 +705,25 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) 
     rows_body<TileS, B_K, EPI, KTAIL>(p, smem, p.tiles, m_small);
 }
 
+constexpr int kRowsMxSmemBytes =
+    (TileSX::kRingBytes > TileLX::kRingBytes ? TileSX::kRingBytes : TileLX::kRingBytes) + kEpiBytes;
+
+// The ROWS launch over an MX-FP8 A (the up projection reading the dispatch
+// payload as sent): the same bodies with the codes and scales in the ring
+// and the decode in the fragment read; the tile height is chosen as above.
+template <int EPI, bool KTAIL>
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_mx_kernel(GemmArgs p) {
+    __shared__ __attribute__((aligned(1024))) char smem[kRowsMxSmemBytes];
+    typedef const __attribute__((address_space(4))) int32_t* cnt_ptr;
+    const int m_small = p.mtile_total != nullptr ? *(cnt_ptr)p.mtile_total : p.m_tiles;
+    const int m_tall = p.mtile_total_l != nullptr ? *(cnt_ptr)p.mtile_total_l : p.m_tiles_l;
+    if (take_tall_tiles(m_small, m_tall, p.n_tiles, (int)gridDim.x)) {
+        rows_body<TileLX, false, EPI, KTAIL>(p, smem, p.tiles_l, m_tall);
+        return;
+    }
+    rows_body<TileSX, false, EPI, KTAIL>(p, smem, p.tiles, m_small);
+}
+
 static_assert(kSchedBM[0] == TileS::BM && kSchedBM[1] == TileL::BM, "schedule tile heights");
 
 __global__ __launch_bounds__(1024) void tile_schedule_kernel(const int32_t* __restrict__ offsets, int E, int R,
@@ -641,18 +758,35 @@ static int64_t persistent_grid() {
     return G < kXcds ? kXcds : G;
 }
 
+// Workgroups of a ROWS launch: never more than the static bound on the
+// number of output tiles (0: nothing to do).
+static int64_t rows_grid(const GemmArgs& a) {
+    const int64_t bound = (int64_t)a.m_tiles * a.n_tiles;
+    if (bound <= 0) return 0;
+    const int64_t G = persistent_grid();
+    const int64_t need = (bound + kXcds - 1) / kXcds * kXcds;
+    return need < G ? need : G;
+}
+
 template <bool B_K, int EPI>
 static hipError_t launch_rows(const GemmArgs& a, hipStream_t st) {
-    // never more workgroups than the static bound on the number of output tiles
-    const int64_t bound = (int64_t)a.m_tiles * a.n_tiles;
-    if (bound <= 0) return hipSuccess;
-    int64_t G = persistent_grid();
-    const int64_t need = (bound + kXcds - 1) / kXcds * kXcds;
-    if (need < G) G = need;
+    const int64_t G = rows_grid(a);
+    if (G == 0) return hipSuccess;
     if (a.Kd % TileS::KD != 0)
         hipLaunchKernelGGL((gemm_rows_kernel<B_K, EPI, true>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
     else
         hipLaunchKernelGGL((gemm_rows_kernel<B_K, EPI, false>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
+    return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t launch_rows_mx(const GemmArgs& a, hipStream_t st) {
+    const int64_t G = rows_grid(a);
+    if (G == 0) return hipSuccess;
+    if (a.Kd % TileS::KD != 0)
+        hipLaunchKernelGGL((gemm_rows_mx_kernel<EPI, true>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
+    else
+        hipLaunchKernelGGL((gemm_rows_mx_kernel<EPI, false>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
     return hipGetLastError();
 }
 
@@ -675,20 +809,14 @@ hipError_t launch_tile_schedule(const int32_t* offsets, int E, int64_t R, void* 
     return hipGetLastError();
 }
 
-hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
-                               int64_t b_stride, bool b_kmajor, void* C, int64_t ldc, int epi,
-                               const moe_bf16* aux_in, moe_bf16* aux_out, const void* sched,
-                               int E, int64_t R, int N, int Kd, hipStream_t st, bool accumulate) {
-    if (R == 0) return hipSuccess;
-    // the DMA descriptor of an N-contiguous B spans its whole contraction
-    if (!b_kmajor && (int64_t)Kd * ldb * 2 >= kMaxDmaBytes) return hipErrorInvalidValue;
-    GemmArgs a{};
-    a.A = A; a.B = B; a.C = C; a.aux_in = aux_in; a.aux_out = aux_out;
-    a.accumulate = accumulate ? 1 : 0;
-    a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.b_stride = b_stride;
+// The operand-independent part of a ROWS launch: B, C, sizes and both tile
+// heights' schedule tables (the kernel picks one from their counts).
+static void rows_args(GemmArgs& a, const moe_bf16* B, int64_t ldb, int64_t b_stride, void* C, int64_t ldc,
+                      moe_bf16* aux_out, const void* sched, int E, int64_t R, int N, int Kd) {
+    a.B = B; a.C = C; a.aux_out = aux_out;
+    a.ldb = ldb; a.ldc = ldc; a.b_stride = b_stride;
     a.M = R; a.R = R; a.N = N; a.Kd = Kd; a.E = E;
     a.n_tiles = (N + BN - 1) / BN;
-    // both tile heights' tables; the kernel picks one from their counts
     if (sched != nullptr) {
         const SchedPart ss = sched_part((void*)sched, E, R, false), sl = sched_part((void*)sched, E, R, true);
         a.tiles = ss.tiles;
@@ -701,8 +829,42 @@ hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B
         a.m_tiles = (int)((R + TileS::BM - 1) / TileS::BM);
         a.m_tiles_l = (int)((R + TileL::BM - 1) / TileL::BM);
     }
+}
+
+hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
+                               int64_t b_stride, bool b_kmajor, void* C, int64_t ldc, int epi,
+                               const moe_bf16* aux_in, moe_bf16* aux_out, const void* sched,
+                               int E, int64_t R, int N, int Kd, hipStream_t st, bool accumulate) {
+    if (R == 0) return hipSuccess;
+    // the DMA descriptor of an N-contiguous B spans its whole contraction
+    if (!b_kmajor && (int64_t)Kd * ldb * 2 >= kMaxDmaBytes) return hipErrorInvalidValue;
+    GemmArgs a{};
+    a.A = A; a.aux_in = aux_in;
+    a.accumulate = accumulate ? 1 : 0;
+    a.lda = lda;
+    rows_args(a, B, ldb, b_stride, C, ldc, aux_out, sched, E, R, N, Kd);
     return launch_rows_epi(a, b_kmajor, epi, st);
 }
+
+hipError_t launch_grouped_rows_mx(const uint8_t* Aq, const uint8_t* A_scale, const moe_bf16* B, int64_t ldb,
+                                  int64_t b_stride, void* C, int64_t ldc, int epi, moe_bf16* aux_out,
+                                  const void* sched, int E, int64_t R, int N, int Kd, hipStream_t st) {
+    if (R == 0) return hipSuccess;
+    if (Kd <= 0 || Kd % 32 != 0 || ((uintptr_t)Aq & 15u) != 0) return hipErrorInvalidValue;
+    if ((int64_t)Kd * ldb * 2 >= kMaxDmaBytes) return hipErrorInvalidValue;
+    const int64_t scale_bytes = (R * (Kd / 32) + 3) / 4 * 4;
+    if (scale_bytes >= kMaxDmaBytes) return hipErrorInvalidValue;
+    GemmArgs a{};
+    a.A = (const uint16_t*)Aq;
+    a.A_scale = A_scale;
+    a.scale_bytes = (uint32_t)scale_bytes;
+    a.lda = Kd;
+    rows_args(a, B, ldb, b_stride, C, ldc, aux_out, sched, E, R, N, Kd);
+    if (epi == EPI_BF16) return launch_rows_mx<EPI_BF16>(a, st);
+    if (epi == EPI_RELU2) return launch_rows_mx<EPI_RELU2>(a, st);
+    return hipErrorInvalidValue;
+}
+
 
 // KGRP launches: tall tiles when there are enough workgroups to fill the
 // device a few times over.

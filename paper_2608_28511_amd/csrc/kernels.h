@@ -62,9 +62,11 @@ hipError_t launch_dispatch(const moe_bf16* x, const float* prob, const int32_t* 
                            int D, int K, moe_bf16* x_disp, float* p_disp, hipStream_t st,
                            const int32_t* sched_offsets = nullptr, int E = 0, void* sched = nullptr);
 // MX-FP8 payload (D a multiple of 32): codes [S*K, D] and E8M0 scales
-// [S*K, D/32] of each token row at its K routed rows; decode to bf16.
+// [S*K, D/32] of each token row at its K routed rows (with sched: the tile
+// tables as in launch_dispatch); decode to bf16.
 hipError_t launch_dispatch_mx(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S, int D,
-                              int K, uint8_t* x_q, uint8_t* x_scale, float* p_disp, hipStream_t st);
+                              int K, uint8_t* x_q, uint8_t* x_scale, float* p_disp, hipStream_t st,
+                              const int32_t* sched_offsets = nullptr, int E = 0, void* sched = nullptr);
 hipError_t launch_dequant_mx(const uint8_t* x_q, const uint8_t* x_scale, int64_t R, int D, moe_bf16* out,
                              hipStream_t st);
 // y[t] = bf16(sum_k w_k y_disp[pos_k] (+ add[t], fp32 [S,D], after the sum; NULL for none))
@@ -86,6 +88,13 @@ hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B
                                int64_t b_stride, bool b_kmajor, void* C, int64_t ldc, int epi,
                                const moe_bf16* aux_in, moe_bf16* aux_out, const void* sched,
                                int E, int64_t R, int N, int Kd, hipStream_t st, bool accumulate = false);
+// ROWS mode over an MX-FP8 A: codes Aq [R, Kd] uint8 (16-byte aligned, Kd a
+// multiple of 32) and E8M0 scales A_scale [R, Kd / 32] (allocation rounded up
+// to 4 bytes), decoded in the operand path; B N-contiguous; epi EPI_BF16 or
+// EPI_RELU2.  Bit-identical to launch_grouped_rows on the decoded bf16 A.
+hipError_t launch_grouped_rows_mx(const uint8_t* Aq, const uint8_t* A_scale, const moe_bf16* B, int64_t ldb,
+                                  int64_t b_stride, void* C, int64_t ldc, int epi, moe_bf16* aux_out,
+                                  const void* sched, int E, int64_t R, int N, int Kd, hipStream_t st);
 // KGRP mode: C_e[m, n] = sum over expert e's rows r of A[r, m] * B[r, n]  (fp32 out).
 // KGRP over a dense contraction cut into nchunk row ranges of kchunk rows:
 // C + c*c_stride = A[rows of chunk c]^T @ B[rows of chunk c]  (fp32 partials).

@@ -124,20 +124,27 @@ __device__ __forceinline__ uint32_t bf16_mag_max8(const uint4& v) {
     return max(m, max(max(v.z & 0x7fffu, v.z >> 16 & 0x7fffu), max(v.w & 0x7fffu, v.w >> 16 & 0x7fffu)));
 }
 
-// One wavefront per token: the row is encoded once and its codes and block
-// scales are written to the token's K routed rows.
 // One workgroup per token, one lane per 16-byte chunk (8 elements) of its
-// row; a 32-element block is 4 adjacent lanes of one wavefront.
+// row; a 32-element block is 4 adjacent lanes of one wavefront.  The row is
+// encoded once and its codes and block scales are written to the token's K
+// routed rows.  With sched_offsets, the last workgroup builds the grouped
+// GEMM's tile tables (as in dispatch_kernel).
 __global__ __launch_bounds__(1024) void dispatch_mx_kernel(const uint4* __restrict__ x,
                                                            const float* __restrict__ prob,
                                                            const int32_t* __restrict__ inv_perm,
                                                            int64_t S, int D8, int K,
                                                            uint2* __restrict__ x_q,
                                                            uint8_t* __restrict__ x_scale,
-                                                           float* __restrict__ p_disp) {
+                                                           float* __restrict__ p_disp,
+                                                           const int32_t* __restrict__ sched_offsets, int E,
+                                                           SchedPart sched_small, SchedPart sched_large) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int64_t t = blockIdx.x;
     const int64_t R = S * K;
+    if (t >= S) {
+        build_tile_schedule(sched_offsets, E, (int)R, sched_small, sched_large);
+        return;
+    }
     const int D32 = D8 / 4;
     int pos_l = lane < K ? inv_perm[t * K + lane] : 0;
     if ((uint32_t)pos_l >= (uint64_t)R) pos_l = -1;  // out-of-range entries are not written
@@ -380,12 +387,17 @@ hipError_t launch_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const 
 namespace moe {
 
 hipError_t launch_dispatch_mx(const moe_bf16* x, const float* prob, const int32_t* inv_perm, int64_t S, int D,
-                              int K, uint8_t* x_q, uint8_t* x_scale, float* p_disp, hipStream_t st) {
+                              int K, uint8_t* x_q, uint8_t* x_scale, float* p_disp, hipStream_t st,
+                              const int32_t* sched_offsets, int E, void* sched) {
     if (S == 0) return hipSuccess;
     const int d8 = D / 8;
-    hipLaunchKernelGGL(dispatch_mx_kernel, dim3((unsigned)S), dim3(d8 >= 1024 ? 1024 : (d8 + 63) / 64 * 64), 0, st,
-                       (const uint4*)x,
-                       prob, inv_perm, S, D / 8, K, (uint2*)x_q, x_scale, p_disp);
+    const int64_t R = S * K;
+    const SchedPart ss = sched ? sched_part(sched, E, R, false) : SchedPart{};
+    const SchedPart sl = sched ? sched_part(sched, E, R, true) : SchedPart{};
+    const unsigned grid = (unsigned)S + (sched ? 1u : 0u);
+    hipLaunchKernelGGL(dispatch_mx_kernel, dim3(grid), dim3(d8 >= 1024 ? 1024 : (d8 + 63) / 64 * 64), 0, st,
+                       (const uint4*)x, prob, inv_perm, S, d8, K, (uint2*)x_q, x_scale, p_disp, sched_offsets, E,
+                       ss, sl);
     return hipGetLastError();
 }
 

@@ -40,6 +40,13 @@ __device__ __forceinline__ int rswz(int r) { return r & 7; }
 template <int KD>
 __device__ __forceinline__ int rswz_k(int r) { return KD == 64 ? (r & 7) : ((r >> 1) & 3); }
 
+// ---- fp8 row layout: [rows][KDB bytes] of MX-FP8 codes (KDB = 64 or 32:
+// 4 or 2 chunks of 16 codes); a lane's fragment is 8 codes, read with
+// ds_read_b64.  Chunk c of row r is stored at c ^ mxswz<KDB>(r), so that the
+// 16 rows x 2 eight-byte pieces each half-wave reads fall in distinct banks.
+template <int KDB>
+__device__ __forceinline__ int mxswz(int r) { return KDB == 64 ? ((r >> 2) & 3) : ((r >> 3) & 1); }
+
 // ---- col layout: [64 k][cols], cols/8 chunks per k-row; chunk pairs XOR-swizzled
 // so the 8 rows {k..k+3, k+8..k+11} read together by ds_read_b64_tr_b16 hit
 // distinct 32-byte bank groups.  cswz depends on k mod 16 only, so rows k + 4
@@ -75,6 +82,18 @@ __device__ __forceinline__ void dma16(const i32x4& rs, uint32_t off, uint32_t ld
                  : "memory", "m0");
 }
 
+// 4-byte buffer -> LDS copy for the whole wave: lane l's dword lands at
+// lds_addr + 4*l (same ordering rules as dma16).
+__device__ __forceinline__ void dma4(const i32x4& rs, uint32_t off, uint32_t lds_addr) {
+    const i32x4 srs = {__builtin_amdgcn_readfirstlane(rs[0]), __builtin_amdgcn_readfirstlane(rs[1]),
+                       __builtin_amdgcn_readfirstlane(rs[2]), __builtin_amdgcn_readfirstlane(rs[3])};
+    const uint32_t sdst = __builtin_amdgcn_readfirstlane(lds_addr);
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dword %0, %1, 0 offen lds"
+                 :
+                 : "v"(off), "s"(srs), "s"(sdst)
+                 : "memory", "m0");
+}
+
 // Workgroup barrier without the memory fence of __syncthreads (whose release
 // fence would drain every in-flight DMA stage).  Callers wait for their own
 // DMA stage with wait_vmcnt first; every LDS read of the previous stage has
@@ -102,10 +121,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 //
 // Row layout (K-contiguous source, element (r, k) at src[r*ld + k]): rows
 //   [x0, min(x_hi, x0 + EXT)), k from k_begin.  A contraction that ends inside
-//   a k tile (KTAIL) is cut per chunk at issue time.
+//   a k tile (KTAIL) is cut per chunk at issue time.  SW = 1: the fp8 row
+//   swizzle (rows of 2*KD code bytes) instead of the bf16 one.
 // Col layout (M/N-contiguous source, element (k, c) at src[k*ld + c]): k rows
 //   [k_begin, k_end), columns [x0, x_hi).
-template <bool ROWL, int EXT, int KD = BK, int WAVES = kWaves>
+template <bool ROWL, int EXT, int KD = BK, int WAVES = kWaves, int SW = 0>
 struct DmaTile {
     static constexpr int kCPR = ROWL ? KD / 8 : EXT / 8;       // chunks per LDS row
     static constexpr int kSlots = EXT * KD * 2 / 1024 / WAVES;  // 1 KB slots per wave
@@ -133,7 +153,7 @@ struct DmaTile {
             const int row = p / kCPR;
             int c = p % kCPR;
             if (ROWL) {
-                c ^= rswz_k<KD>(row);
+                c ^= SW ? mxswz<KD * 2>(row) : rswz_k<KD>(row);
                 kpos[i] = c * 8;
                 off[i] = (uint32_t)((row * ld + c * 8) * 2);
             } else {
@@ -168,6 +188,14 @@ __device__ __forceinline__ uint32_t row_base(int row0, int kk, int lane) {
     const int r = row0 + (lane & 15);
     const int c = kk * 4 + (lane >> 4);
     return (uint32_t)((r * (KD / 8) + (c ^ rswz_k<KD>(r))) * 16);
+}
+// fp8 row layout: lane reads row (row0 + lane%16), codes
+// [32*kk + 8*(lane/16), +8) of a KDB-byte row.
+template <int KDB>
+__device__ __forceinline__ uint32_t mx_row_base(int row0, int kk, int lane) {
+    const int r = row0 + (lane & 15);
+    const int g = kk * 4 + (lane >> 4);   // 8-byte piece of the row
+    return (uint32_t)(r * KDB + (((g >> 1) ^ mxswz<KDB>(r)) * 16) + (g & 1) * 8);
 }
 // Col layout: lane 16g + 4r + q points at k-row 8g + r (+32 kk, +4 for the
 // second read), columns col0 + 4q .. +3; each 16-lane group then receives one

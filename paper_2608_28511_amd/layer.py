@@ -50,12 +50,18 @@ def dispatch(x: torch.Tensor, topk_prob: Optional[torch.Tensor], inv_perm: torch
     return x_disp, p_disp
 
 
+def mx_scales(R: int, D: int, device) -> torch.Tensor:
+    """uint8 [R, D/32] scale rows in an allocation padded as the MX grouped GEMM reads it."""
+    nbytes = max(L.moe_mx_scale_alloc_bytes(R, D), 1)
+    return _empty((nbytes,), torch.uint8, device)[: R * (D // 32)].view(R, D // 32)
+
+
 def dispatch_mxfp8(x: torch.Tensor, topk_prob: Optional[torch.Tensor], inv_perm: torch.Tensor, K: int):
     """(x_q uint8 [S*K, D], x_scale uint8 [S*K, D/32], p_disp fp32 or None)."""
     S, D = x.shape
     dev = x.device
     x_q = _empty((S * K, D), torch.uint8, dev)
-    x_scale = _empty((S * K, D // 32), torch.uint8, dev)
+    x_scale = mx_scales(S * K, D, dev)
     p_disp = _empty((S * K,), F32, dev) if topk_prob is not None else None
     L.moe_dispatch_mxfp8(x, topk_prob, inv_perm, S, D, K, x_q, x_scale, p_disp)
     return x_q, x_scale, p_disp
@@ -94,6 +100,16 @@ def grouped_gemm(A: torch.Tensor, sched: torch.Tensor, W: torch.Tensor, epilogue
     E, _, N = W.shape
     C = out if out is not None else _empty((R, N), BF16, A.device)
     L.moe_grouped_gemm(A, sched, E, R, Kd, N, W, epilogue, C, u_save)
+    return C
+
+
+def grouped_gemm_mxfp8(x_q: torch.Tensor, x_scale: torch.Tensor, sched: torch.Tensor, W: torch.Tensor,
+                       epilogue: int, out: Optional[torch.Tensor] = None, u_save: Optional[torch.Tensor] = None):
+    """grouped_gemm with the MX-FP8 payload (x_scale from mx_scales) as A."""
+    R, Kd = x_q.shape
+    E, _, N = W.shape
+    C = out if out is not None else _empty((R, N), BF16, x_q.device)
+    L.moe_grouped_gemm_mxfp8(x_q, x_scale, sched, E, R, Kd, N, W, epilogue, C, u_save)
     return C
 
 
@@ -297,7 +313,7 @@ class LayerFwd:
                 self.out["seq_counts"] = _empty((S // seq_len, E), I32, dev)
         if payload == "mxfp8" and export:
             self.out["x_q"] = _empty((R, D), torch.uint8, dev)
-            self.out["x_scale"] = _empty((R, D // 32), torch.uint8, dev)
+            self.out["x_scale"] = mx_scales(R, D, dev)
         if Fs:
             if export:
                 self.out["h_s"] = _empty((S, Fs), BF16, dev)

@@ -100,3 +100,21 @@ def check_permutation_props(idx, counts, offsets, perm, inv_perm, E, K):
     tok = perm // K
     same = np.diff(e_of_pos) == 0
     assert np.all(np.diff(tok)[same] > 0)
+
+
+def takes_tall_tiles(counts, N, cus):
+    """The rows kernel's tile-height rule, restated: the busiest XCD's rounds
+    of 128-row and of 256-row tiles; tall tiles when 2 * rounds_tall * 0.91 <
+    rounds_small.  The grid is one workgroup per CU (a multiple of 8), capped
+    by the static bound on the number of output tiles."""
+    def cdiv(a, b):
+        return -(-a // b)
+    R, E = int(sum(counts)), len(counts)
+    m_small = int(sum(cdiv(int(c), 128) for c in counts))
+    m_tall = int(sum(cdiv(int(c), 256) for c in counts))
+    nt = cdiv(N, 256)
+    bound = (cdiv(R, 128) + min(R, E)) * nt          # static bound on the output tiles
+    G = min(cus // 8 * 8, cdiv(bound, 8) * 8)
+    r_small = cdiv(cdiv(m_small, 8) * nt, G // 8)
+    r_tall = cdiv(cdiv(m_tall, 8) * nt, G // 8)
+    return 2 * r_tall * 91 < 100 * r_small

@@ -15,7 +15,7 @@ from paper_2608_28511_amd import layer
 from paper_2608_28511_amd.workloads import (WORKLOADS, make_inputs, make_logits, make_segments,
                                             make_sparse_sign_rows)
 
-from gpu_helpers import LazyExperts, assert_bf16_close, np64, npi
+from gpu_helpers import LazyExperts, assert_bf16_close, np64, npi, takes_tall_tiles
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -107,24 +107,6 @@ def test_grouped_ffn_full_size_sampled(name):
     assert_bf16_close(np64(yd[sel]), y_ref[ref_order], f"{name} y_disp")
 
 
-def _takes_tall_tiles(counts, N, cus):
-    """The rows kernel's tile-height rule, restated: the busiest XCD's rounds
-    of 128-row and of 256-row tiles; tall tiles when 2 * rounds_tall * 0.91 <
-    rounds_small.  The grid is one workgroup per CU (a multiple of 8), capped
-    by the static bound on the number of output tiles."""
-    def cdiv(a, b):
-        return -(-a // b)
-    R, E = int(sum(counts)), len(counts)
-    m_small = int(sum(cdiv(int(c), 128) for c in counts))
-    m_tall = int(sum(cdiv(int(c), 256) for c in counts))
-    nt = cdiv(N, 256)
-    bound = (cdiv(R, 128) + min(R, E)) * nt          # static bound on the output tiles
-    G = min(cus // 8 * 8, cdiv(bound, 8) * 8)
-    r_small = cdiv(cdiv(m_small, 8) * nt, G // 8)
-    r_tall = cdiv(cdiv(m_tall, 8) * nt, G // 8)
-    return 2 * r_tall * 91 < 100 * r_small
-
-
 def test_grouped_ffn_exact_tall_tiles():
     """Both projections on 256-row tiles (long launch, few large experts with
     ragged last tiles): bit-exact like the 128-row shapes above."""
@@ -132,7 +114,7 @@ def test_grouped_ffn_exact_tall_tiles():
     off = make_segments(R, E, seed=R + E)
     counts = np.diff(npi(off))
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    if not (_takes_tall_tiles(counts, F, cus) and _takes_tall_tiles(counts, D, cus)):
+    if not (takes_tall_tiles(counts, F, cus) and takes_tall_tiles(counts, D, cus)):
         pytest.skip(f"this device ({cus} CUs) keeps 128-row tiles for the shape")
     assert all(c % 256 for c in counts)   # every expert ends in a partly filled tall tile
     x = make_sparse_sign_rows(R, D, 16, seed=R).to(torch.bfloat16)

@@ -1,16 +1,18 @@
 """GPU parity of the MX-FP8 dispatch payload (Section 1's precision lever on
 b_x): codes, block scales and the decoded rows are integer/byte work and
-must match the oracle bit for bit; the layer with the MX payload is held to
-the bf16 output bar against the oracle's chain on the same payload."""
+must match the oracle bit for bit; the up projection that decodes the
+payload in its operand path must equal decode-then-GEMM bit for bit (and
+the oracle to the bf16 bar); the layer with the MX payload is held to the
+bf16 output bar against the oracle's chain on the same payload."""
 import numpy as np
 import pytest
 import torch
 
 from oracle import moe_oracle as O
 from paper_2608_28511_amd import layer
-from paper_2608_28511_amd.workloads import WORKLOADS, make_inputs
+from paper_2608_28511_amd.workloads import WORKLOADS, make_inputs, make_segments
 
-from gpu_helpers import LazyExperts, assert_bf16_close, np64, npi
+from gpu_helpers import LazyExperts, assert_bf16_close, np64, npi, takes_tall_tiles
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -112,3 +114,104 @@ def test_layer_fwd_mxfp8(name, n_samples):
     ok = np.all(idx == ref["topk_idx"], axis=1)
     assert ok.mean() > 0.99
     assert_bf16_close(np64(out["y"][torch.as_tensor(tok[ok], device=DEV)]), ref["y"][ok], f"{name} y (mxfp8)")
+
+
+# (rows kind, S, K, D = Kd, E, empty experts, N): Kd / 32 odd leaves half a
+# 64-wide stage at the end of the contraction, and R * Kd / 32 not a multiple
+# of 4 puts the last scale bytes in the allocation's padded word; the last
+# case is long enough for the 256-row tiles.
+_GEMM_MX_CASES = [
+    ("normal", 37, 3, 96, 5, 1, 72),
+    ("normal", 256, 6, 2048, 8, 0, 1024),
+    ("wide", 100, 7, 2688, 16, 3, 264),
+    ("tiny", 513, 8, 128, 64, 20, 1032),
+    ("edge", 201, 3, 160, 3, 0, 256),
+    ("normal", 4096, 6, 512, 4, 0, 1024),
+]
+
+
+def _bits(t):
+    return t.view(torch.int16)
+
+
+@pytest.mark.parametrize("kind,S,K,D,E,empty,N", _GEMM_MX_CASES)
+def test_grouped_gemm_mxfp8_equals_decode_then_gemm(kind, S, K, D, E, empty, N):
+    seed = S + 7 * D + N
+    R = S * K
+    x = _rows(kind, S, D, seed)
+    inv = _random_inv(S, K, seed + 1)
+    xq, xs, _ = layer.dispatch_mxfp8(x.to(DEV), None, inv.to(DEV), K)
+    off = make_segments(R, E, seed=seed + 2, empty=empty)
+    sched = layer.grouped_schedule(off.to(DEV), E, R)
+    g = torch.Generator().manual_seed(seed + 3)
+    W = (torch.randn((E, D, N), generator=g) * D ** -0.5).to(torch.bfloat16).to(DEV)
+    xd = layer.mxfp8_dequant(xq, xs)
+    if (S, D) == (4096, 512):
+        cus = torch.cuda.get_device_properties(0).multi_processor_count
+        assert takes_tall_tiles(np.diff(npi(off)), N, cus), "the case must take the 256-row tiles"
+    for epi in (1, 0):
+        u_f = torch.empty((R, N), dtype=torch.bfloat16, device=DEV) if epi else None
+        u_r = torch.empty((R, N), dtype=torch.bfloat16, device=DEV) if epi else None
+        c_f = layer.grouped_gemm_mxfp8(xq, xs, sched, W, epi, u_save=u_f)
+        c_r = layer.grouped_gemm(xd, sched, W, epi, u_save=u_r)
+        torch.cuda.synchronize()
+        assert torch.equal(_bits(c_f), _bits(c_r)), f"epilogue {epi}: C differs from decode-then-GEMM"
+        if epi:
+            assert torch.equal(_bits(u_f), _bits(u_r)), "u_save differs from decode-then-GEMM"
+    if kind == "normal" and R * D <= 1 << 20:
+        # and the oracle's chain: its own encoding, decode and expert FFN
+        cd, sc, _ = O.dispatch_mxfp8(np64(x), None, inv.numpy(), K)
+        xd_ref = O.round_bf16(O.mxfp8_dequantize(cd, sc))
+        zero_w2 = [np.zeros((N, 8))] * E
+        u_ref, _, _ = O.expert_ffn(xd_ref, npi(off), LazyExperts(W), zero_w2, round_payload=False)
+        assert_bf16_close(np64(c_f), u_ref, f"{kind} u")   # epilogue 0: the plain product
+
+
+def test_grouped_gemm_mxfp8_oracle_h():
+    """The fused up projection's squared-ReLU output against the oracle."""
+    S, K, D, E, N = 64, 4, 224, 6, 320
+    R = S * K
+    x = _rows("normal", S, D, 11)
+    inv = _random_inv(S, K, 12)
+    xq, xs, _ = layer.dispatch_mxfp8(x.to(DEV), None, inv.to(DEV), K)
+    off = make_segments(R, E, seed=13, empty=1)
+    sched = layer.grouped_schedule(off.to(DEV), E, R)
+    W = (torch.randn((E, D, N), generator=torch.Generator().manual_seed(14)) * D ** -0.5).to(torch.bfloat16)
+    W = W.to(DEV)
+    u = torch.empty((R, N), dtype=torch.bfloat16, device=DEV)
+    h = layer.grouped_gemm_mxfp8(xq, xs, sched, W, 1, u_save=u)
+    torch.cuda.synchronize()
+    cd, sc, _ = O.dispatch_mxfp8(np64(x), None, inv.numpy(), K)
+    xd_ref = O.round_bf16(O.mxfp8_dequantize(cd, sc))
+    u_ref, h_ref, _ = O.expert_ffn(xd_ref, npi(off), LazyExperts(W), [np.zeros((N, 8))] * E, round_payload=False)
+    assert_bf16_close(np64(u), u_ref, "u")
+    assert_bf16_close(np64(h), h_ref, "h")
+
+
+def test_grouped_gemm_mxfp8_rejects_bad_shapes():
+    from paper_2608_28511_amd import _lib as L
+    R, D, E, N = 64, 48, 2, 64   # D not a multiple of 32
+    xq = torch.zeros((R, D), dtype=torch.uint8, device=DEV)
+    xs = layer.mx_scales(R, 64, DEV)
+    off = make_segments(R, E, seed=1)
+    sched = layer.grouped_schedule(off.to(DEV), E, R)
+    W = torch.zeros((E, D, N), dtype=torch.bfloat16, device=DEV)
+    C = torch.empty((R, N), dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(RuntimeError):
+        L.moe_grouped_gemm_mxfp8(xq, xs, sched, E, R, D, N, W, 0, C, None)
+    with pytest.raises(ValueError):   # scale allocation not padded to whole words
+        L.moe_grouped_gemm_mxfp8(xq[:, :32].contiguous(), torch.zeros(R * 1 - 1, dtype=torch.uint8, device=DEV),
+                                 sched, E, R, 32, N, W[:, :32].contiguous(), 0, C, None)
+
+
+def test_layer_fwd_mxfp8_without_decoded_export():
+    """The MX layer that decodes only inside the up projection (x_disp not
+    exported, no decode pass) gives the same outputs as with the export."""
+    s = WORKLOADS["tiny_s512_d256_e8_k2"]
+    inp = make_inputs(s, device=DEV)
+    a = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, export=True, payload="mxfp8")
+    b = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, export=False, payload="mxfp8")
+    ya = a(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"])["y"].clone()
+    yb = b(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"])["y"]
+    torch.cuda.synchronize()
+    assert torch.equal(_bits(ya), _bits(yb))
