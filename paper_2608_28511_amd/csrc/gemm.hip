@@ -356,18 +356,33 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) 
         for (int kt = 0; kt < nk; kt += T::kStages) ring_round<T::kStages>(step, kt, nk);
     }
 
-    // lane holds C[m][n .. n+3] for each (i, j)
+    // Epilogue through LDS (the ring is free once every wave has passed the
+    // barrier): per 16-row block the wave's 16 x 64 fp32 go to its 4 KB
+    // slice (16-byte chunk c of row r at c ^ r) and come back as whole
+    // 256-byte row pieces, 4 rows per store instruction, written
+    // non-temporally: the gradient is not read here, and full lines keep the
+    // bypassing writes efficient while the operand rows stay in L2.
+    __syncthreads();
     const int64_t c_base = (int64_t)e * p.c_stride;
+    const uint32_t ep = lds0 + (uint32_t)wave * 4096u;
+    const int r = lane & 15;
+    const int rq = lane >> 4, c = lane & 15;
+    const int64_t ncol = n0 + wn * 64 + c * 4;
 #pragma unroll
     for (int i = 0; i < T::MI; ++i) {
-        const int64_t m = row0 + wm * (T::BM / 2) + i * 16 + (lane & 15);
-        if (m >= row_hi) continue;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int64_t n = n0 + wn * 64 + j * 16 + 4 * (lane >> 4);
-            if (n >= p.N) continue;
-            const f32x4 a = acc[i][j];
-            *(float4*)((float*)p.C + c_base + m * p.ldc + n) = make_float4(a[0], a[1], a[2], a[3]);
+            const int ch = (j * 4 + (lane >> 4)) ^ r;
+            *(__attribute__((address_space(3))) f32x4*)(uintptr_t)(ep + (uint32_t)(r * 256 + ch * 16)) = acc[i][j];
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int rr = q * 4 + rq;
+            const f32x4 v =
+                *(const __attribute__((address_space(3))) f32x4*)(uintptr_t)(ep + (uint32_t)(rr * 256 + ((c ^ rr) * 16)));
+            const int64_t m = row0 + wm * (T::BM / 2) + i * 16 + rr;
+            if (m < row_hi && ncol < p.N)
+                __builtin_nontemporal_store(v, (f32x4*)((float*)p.C + c_base + m * p.ldc + ncol));
         }
     }
 }
