@@ -436,15 +436,17 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void* base, in
 
 constexpr uint32_t kDropOffset = 0x80000000u;  // beyond any descriptor's range
 
-// Staged epilogue of one 64 x 64 wave tile (EPI_BF16 / EPI_RELU2): per 16-row
-// block, the accumulators go to the wave's LDS slice as bf16 (chunk c of row
-// r at c ^ (r & 7)), come back as 16-byte row pieces and leave as two
-// buffer_store_dwordx4 of 8 rows x 128 bytes each.  OUT: 0 = the product
-// (squared-ReLU applied for EPI_RELU2), 1 = the raw product (pre-activation).
+// Staged epilogue of one 64 x 64 wave tile (EPI_BF16 / EPI_RELU2 /
+// EPI_DRELU2): per 16-row block, the accumulators go to the wave's LDS slice
+// as bf16 (chunk c of row r at c ^ (r & 7)), come back as 16-byte row pieces
+// and leave as two buffer_store_dwordx4 of 8 rows x 128 bytes each.  OUT:
+// 0 = the product (squared-ReLU applied for EPI_RELU2; times 2 max(u, 0),
+// u from uu at the accumulators' positions, for EPI_DRELU2), 1 = the raw
+// product (pre-activation).
 template <int EPI, int OUT, int MI>
 __device__ __forceinline__ void staged_store(const f32x4 (&acc)[MI][4], void* C, int64_t ldc, int N,
                                              int64_t rbase, int64_t nrows, int64_t cbase,
-                                             uint32_t ep, int lane) {
+                                             uint32_t ep, int lane, const u32x2 (*uu)[4] = nullptr) {
     const __amdgpu_buffer_rsrc_t rs = rows_rsrc(C, rbase, nrows, ldc);
     const int r = lane & 15;
     const uint32_t wr = ep + (uint32_t)(r * 128 + (lane >> 4 & 1) * 8);
@@ -459,6 +461,13 @@ __device__ __forceinline__ void staged_store(const f32x4 (&acc)[MI][4], void* C,
             if constexpr (EPI == EPI_RELU2 && OUT == 0) {
                 v0 = fmaxf(v0, 0.f); v1 = fmaxf(v1, 0.f); v2 = fmaxf(v2, 0.f); v3 = fmaxf(v3, 0.f);
                 v0 *= v0; v1 *= v1; v2 *= v2; v3 *= v3;
+            }
+            if constexpr (EPI == EPI_DRELU2) {
+                const u32x2 u = uu[i][j];
+                v0 = v0 * 2.f * fmaxf(bf16_lo(u[0]), 0.f);
+                v1 = v1 * 2.f * fmaxf(bf16_hi(u[0]), 0.f);
+                v2 = v2 * 2.f * fmaxf(bf16_lo(u[1]), 0.f);
+                v3 = v3 * 2.f * fmaxf(bf16_hi(u[1]), 0.f);
             }
             const int ch = 2 * j + (lane >> 5);
             const u32x2 w = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
@@ -476,11 +485,11 @@ __device__ __forceinline__ void staged_store(const f32x4 (&acc)[MI][4], void* C,
 }
 
 // dgrad epilogue: C = bf16(acc * 2 max(u, 0)) with u read from aux_in at the
-// accumulators' own positions (8 bytes per lane and fragment).  The sixteen
-// u loads are issued by drelu2_load at the tile's first k step (right after
-// its barrier, before that step's operand copies), so they have long
-// completed when drelu2_store uses them: its waits never reach the copies
-// in flight at the tile's end.
+// accumulators' own positions (8 bytes per lane and fragment), written by
+// staged_store.  The sixteen u loads are issued by drelu2_load at the tile's
+// first k step (right after its barrier, before that step's operand
+// copies), so they have long completed when the epilogue uses them: its
+// waits never reach the copies in flight at the tile's end.
 template <int MI>
 __device__ __forceinline__ void drelu2_load(u32x2 (&uu)[MI][4], const uint16_t* aux_in, int64_t ldc, int N,
                                             int64_t rbase, int64_t nrows, int64_t cbase, int lane) {
@@ -493,30 +502,6 @@ __device__ __forceinline__ void drelu2_load(u32x2 (&uu)[MI][4], const uint16_t* 
             const int64_t col = cbase + j * 16 + 4 * (lane >> 4);
             const uint32_t off = (row < nrows && col < N) ? (uint32_t)((row * ldc + col) * 2) : kDropOffset;
             uu[i][j] = __builtin_amdgcn_raw_buffer_load_b64(ru, off, 0, 0);
-        }
-    }
-}
-
-template <int MI>
-__device__ __forceinline__ void drelu2_store(const f32x4 (&acc)[MI][4], const u32x2 (&uu)[MI][4], void* C,
-                                             int64_t ldc, int N, int64_t rbase, int64_t nrows, int64_t cbase,
-                                             int lane) {
-    const __amdgpu_buffer_rsrc_t rc = rows_rsrc(C, rbase, nrows, ldc);
-#pragma unroll
-    for (int i = 0; i < MI; ++i) {
-        const int64_t row = i * 16 + (lane & 15);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t col = cbase + j * 16 + 4 * (lane >> 4);
-            const uint32_t off = (row < nrows && col < N) ? (uint32_t)((row * ldc + col) * 2) : kDropOffset;
-            const u32x2 u = uu[i][j];
-            const f32x4 a = acc[i][j];
-            const float g0 = a[0] * 2.f * fmaxf(bf16_lo(u[0]), 0.f);
-            const float g1 = a[1] * 2.f * fmaxf(bf16_hi(u[0]), 0.f);
-            const float g2 = a[2] * 2.f * fmaxf(bf16_lo(u[1]), 0.f);
-            const float g3 = a[3] * 2.f * fmaxf(bf16_hi(u[1]), 0.f);
-            const u32x2 w = {pack_bf16x2(g0, g1), pack_bf16x2(g2, g3)};
-            __builtin_amdgcn_raw_buffer_store_b64(w, rc, off, 0, 0);
         }
     }
 }
@@ -661,7 +646,7 @@ __device__ __forceinline__ void rows_body(const GemmArgs& p, char* smem, const i
             const int cbase = cur.n0 + wn * 64;
             if constexpr (EPI == EPI_DRELU2) {
                 if constexpr (MI > 4) drelu2_load(uu, p.aux_in, p.ldc, p.N, rbase, nrows, cbase, lane);
-                drelu2_store(acc, uu, p.C, p.ldc, p.N, rbase, nrows, cbase, lane);
+                staged_store<EPI, 0, MI>(acc, p.C, p.ldc, p.N, rbase, nrows, cbase, ep, lane, uu);
             } else if constexpr (EPI == EPI_F32) {
                 f32_store(acc, (float*)p.C, p.ldc, p.N, rbase, nrows, cbase, p.accumulate != 0, lane);
             } else {
