@@ -57,6 +57,9 @@ def parse():
     p.add_argument("--ep-share", type=int, default=0, metavar="G",
                    help="also time the expert-local grouped GEMMs one GPU would run under expert "
                         "parallelism over G GPUs (E/G experts, the same S*K rows); reported apart")
+    p.add_argument("--route-sweep", action="store_true",
+                   help="also time the route alone over token counts 1K..128K (the workload's E and K) "
+                        "and report its algorithmic GB/s; reported apart")
     p.add_argument("--calib-bytes", type=int, default=1 << 30,
                    help="size of the plain copy run once for counter calibration")
     p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -218,6 +221,31 @@ def filtered_mean(xs):
             break
         xs = kept
     return sum(xs) / len(xs)
+
+
+def route_sweep(_lib, s, reps, stream, dev):
+    """The route (top-K, histogram and scan, permutation) alone over token
+    counts S = 1K .. 128K with the workload's E and K: duration and
+    algorithmic bytes (read S*E*4, write R*16 + (2E+1)*4) per S, to show where
+    its three launches stop being latency-bound."""
+    import torch
+    out = []
+    for S in (1 << k for k in range(10, 18)):
+        R = S * s.K
+        g = torch.Generator(device=dev).manual_seed(S)
+        logits = torch.randn((S, s.E), generator=g, device=dev)
+        bufs = [torch.empty((S, s.K), dtype=torch.int32, device=dev), torch.empty((S, s.K), device=dev),
+                torch.empty((s.E,), dtype=torch.int32, device=dev),
+                torch.empty((s.E + 1,), dtype=torch.int32, device=dev),
+                torch.empty((R,), dtype=torch.int32, device=dev), torch.empty((R,), dtype=torch.int32, device=dev)]
+        ws = torch.empty(max(1, _lib.moe_route_workspace_bytes(S, s.E, s.K)), dtype=torch.uint8, device=dev)
+        fn = lambda i: _lib.moe_route_topk(logits, S, s.E, s.K, *bufs, ws)
+        for i in range(3):
+            fn(i)
+        t = time_region(fn, reps, stream)
+        nbytes = S * s.E * 4 + R * 16 + (2 * s.E + 1) * 4
+        out.append({"S": S, "us": round(t * 1e6, 2), "bytes": nbytes, "GBps": round(nbytes / t / 1e9, 1)})
+    return out
 
 
 def ep_share(_lib, s, G, reps, stream, dev):
@@ -607,6 +635,7 @@ def main():
                       if prod else {})},
         "roofline": roofline, "stages": stages, "cpu_baseline": cpu,
         **({"ep_share": ep_share(_lib, s, args.ep_share, reps, stream, dev)} if args.ep_share > 1 else {}),
+        **({"route_sweep": route_sweep(_lib, s, reps, stream, dev)} if args.route_sweep else {}),
         "layer_step_us": {"n": len(per_step), "median": round(statistics.median(per_step), 2),
                           "filtered_mean": round(filtered_mean(per_step), 2),
                           "min": round(min(per_step), 2), "max": round(max(per_step), 2)},
