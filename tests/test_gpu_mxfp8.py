@@ -10,7 +10,7 @@ import torch
 
 from oracle import moe_oracle as O
 from paper_2608_28511_amd import layer
-from paper_2608_28511_amd.workloads import WORKLOADS, make_inputs, make_segments
+from paper_2608_28511_amd.workloads import PRODUCTION, WORKLOADS, make_inputs, make_segments
 
 from gpu_helpers import LazyExperts, assert_bf16_close, np64, npi, takes_tall_tiles
 
@@ -215,3 +215,45 @@ def test_layer_fwd_mxfp8_without_decoded_export():
     yb = b(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"])["y"]
     torch.cuda.synchronize()
     assert torch.equal(_bits(ya), _bits(yb))
+
+
+def _mx_layer_vs_oracle(s, inp, out, n_samples, **oracle_kw):
+    """y of sampled tokens against the oracle's chain on the MX payload; tokens
+    whose routing the oracle decides differently (near-ties) are left out,
+    and may be at most one in fifty."""
+    x = np64(inp["x"])
+    rng = np.random.default_rng(s.seed)
+    tok = np.arange(s.S) if n_samples is None else np.sort(rng.choice(s.S, n_samples, replace=False))
+    ref = O.layer_fwd(x[tok], np64(inp["Wr"]), LazyExperts(inp["W1"]), LazyExperts(inp["W2"]), s.K,
+                      round_payload=False, payload="mxfp8", **oracle_kw)
+    ok = np.all(npi(out["topk_idx"])[tok] == ref["topk_idx"], axis=1)
+    assert ok.sum() >= len(tok) - max(1, len(tok) // 50)
+    assert_bf16_close(np64(out["y"][torch.as_tensor(tok[ok], device=DEV)]), ref["y"][ok], f"{s.name} y (mxfp8)")
+
+
+@pytest.mark.parametrize("name,n_samples", [("prod_tiny_s512_d256_e8_k2", None), ("prod_s16384_d2688_e192_k7", 8)])
+def test_prod_layer_fwd_mxfp8(name, n_samples):
+    """The paper's production variant (sigmoid routing with a selection bias,
+    shared expert, balance loss) on the MX payload."""
+    s = PRODUCTION[name]
+    inp = make_inputs(s, device=DEV)
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, export=False, payload="mxfp8", score="sigmoid", Fs=s.Fs,
+                        seq_len=s.seq_len, aux_coeff=s.aux_coeff)
+    lf.out["topk_idx"] = torch.empty((s.S, s.K), dtype=torch.int32, device=DEV)
+    out = lf(inp["x"], inp["Wr"], inp["W1"], inp["W2"], sel_bias=inp["sel_bias"], Ws1=inp["Ws1"], Ws2=inp["Ws2"])
+    torch.cuda.synchronize()
+    _mx_layer_vs_oracle(s, inp, out, n_samples, score="sigmoid", sel_bias=np64(inp["sel_bias"]),
+                        Ws1=np64(inp["Ws1"]), Ws2=np64(inp["Ws2"]))
+
+
+def test_latent_layer_fwd_mxfp8():
+    """The latent (LatentMoE-style) layer on the MX payload: the dispatch
+    encodes the latent rows."""
+    s = WORKLOADS["latent_s16384_h4096_d1024_e128_k6"]
+    inp = make_inputs(s, device=DEV)
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, export=False, payload="mxfp8")
+    lf.out["topk_idx"] = torch.empty((s.S, s.K), dtype=torch.int32, device=DEV)
+    out = lf(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"], Wdown=inp["Wdown"], Wup=inp["Wup"])
+    torch.cuda.synchronize()
+    _mx_layer_vs_oracle(s, inp, out, 16, bias=None if inp["bias"] is None else np64(inp["bias"]),
+                        Wdown=np64(inp["Wdown"]), Wup=np64(inp["Wup"]))
