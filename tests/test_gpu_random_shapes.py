@@ -1,0 +1,80 @@
+"""Seeded random layer shapes on the GPU against the oracle, every token
+compared: model and expert widths that are any multiple of 8 (k and n tails
+in every GEMM), expert counts from 1 to 300, top-K up to 12, token counts
+from 1 up, router biases that unbalance or empty experts, the MX-FP8 payload
+and the production variant (sigmoid routing, shared expert, balance loss).
+The checks are those of the fixed-shape layer tests: exact routing for
+tokens away from score ties, valid routing for the rest, and the bf16
+output bar."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_28511_amd import layer
+from paper_2608_28511_amd.workloads import PRODUCTION, WORKLOADS, make_inputs
+
+from gpu_helpers import np64
+from test_gpu_layer import DEV, check_layer, run_layer
+from test_gpu_mxfp8 import _mx_layer_vs_oracle
+from test_gpu_production import check_prod_layer, run_prod_layer
+
+pytestmark = pytest.mark.gpu
+
+
+def _shape(i, mx=False):
+    rng = np.random.default_rng(7000 + i)
+    E = int(rng.integers(1, 301))
+    bias = ["none", "normal", "zipf"][i % 3] if E >= 18 else "none"
+    K = int(rng.integers(1, min(E - (5 if bias == "zipf" else 0), 12) + 1))
+    S = int(rng.integers(1, 301))
+    D = 32 * int(rng.integers(1, 25)) if mx else 8 * int(rng.integers(1, 97))
+    F = 8 * int(rng.integers(1, 97))
+    return WORKLOADS["tiny_s512_d256_e8_k2"].scaled(name=f"random{i}", S=S, D=D, E=E, K=K, F=F, bias=bias,
+                                                    seed=100 + i)
+
+
+def _ids(i, mx=False):
+    s = _shape(i, mx)
+    return f"s{s.S}_d{s.D}_e{s.E}_k{s.K}_f{s.F}_{s.bias}"
+
+
+@pytest.mark.parametrize("i", range(24), ids=lambda i: _ids(i))
+def test_random_layer_fwd(i):
+    s = _shape(i)
+    inp = make_inputs(s, device=DEV)
+    out = run_layer(s, inp)
+    n_amb = check_layer(s, inp, out, None, seed=i)
+    assert n_amb <= max(2, s.S // 8)
+
+
+@pytest.mark.parametrize("i", range(8), ids=lambda i: _ids(i, mx=True))
+def test_random_layer_fwd_mxfp8(i):
+    s = _shape(i, mx=True)
+    inp = make_inputs(s, device=DEV)
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, export=True, payload="mxfp8")
+    out = lf(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"])
+    torch.cuda.synchronize()
+    _mx_layer_vs_oracle(s, inp, out, None, bias=None if inp["bias"] is None else np64(inp["bias"]))
+
+
+def _prod_shape(i):
+    rng = np.random.default_rng(9000 + i)
+    E = int(rng.integers(2, 129))
+    K = int(rng.integers(1, min(E, 8) + 1))
+    T = 8 * int(rng.integers(1, 17))
+    S = T * int(rng.integers(1, 5))
+    D = 8 * int(rng.integers(1, 65))
+    F = 8 * int(rng.integers(1, 65))
+    Fs = 8 * int(rng.integers(1, 65))
+    return PRODUCTION["prod_tiny_s512_d256_e8_k2"].scaled(name=f"prod_random{i}", S=S, D=D, E=E, K=K, F=F, Fs=Fs,
+                                                          seq_len=T, seed=200 + i)
+
+
+@pytest.mark.parametrize("i", range(8), ids=lambda i: "s{S}_t{seq_len}_d{D}_e{E}_k{K}_f{F}_fs{Fs}".format(
+    **_prod_shape(i).__dict__))
+def test_random_prod_layer_fwd(i):
+    s = _prod_shape(i)
+    inp = make_inputs(s, device=DEV)
+    out = run_prod_layer(s, inp)
+    n_amb = check_prod_layer(s, inp, out, None, s.aux_coeff)
+    assert n_amb <= max(2, s.S // 8)
