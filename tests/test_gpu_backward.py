@@ -45,7 +45,7 @@ def oracle_chain(x, logits, W1, W2, dy, K, E):
     dxd, dW1, dW2, du = O.expert_ffn_bwd(xd, u, h, dyd, off, W1, W2, round_payload=False)
     dx = O.dispatch_bwd(dxd, inv, S, K)
     return dict(counts=counts, y=y, dp=dp, dx=dx, dW1=dW1, dW2=dW2, off=off, xd=xd, u=u, h=h,
-                dyd=dyd, dxd=dxd, inv=inv)
+                dyd=dyd, dxd=dxd, inv=inv, yd=yd, pd=pd)
 
 
 def assert_grad_close(got, ref, what):
@@ -72,6 +72,23 @@ def bwd_bounds(xd, u, h, dyd, dxd, W1e, W2e):
     return np.abs(xd).T @ b_du, 4 * EPS_BF16 * (np.abs(h).T @ np.abs(dyd)), b_dxd
 
 
+def y_bound(R, W2, S, K, E):
+    """Elementwise bound on |y_gpu - y| from the three bf16 roundings the
+    forward defines (h, the down projection's input; y_disp; y):
+        |dy_disp| <= EPS_BF16 * (|h| @ |W2_e|) + EPS_BF16 * |y_disp|
+        |dy|      <= sum_k p_k |dy_disp| + EPS_BF16 * |y|
+    with a factor 1.25 of room for fp32 accumulation.  A max-relative bar
+    cannot stand in for it when the down projection sums few large terms
+    that cancel."""
+    b_yd = np.zeros_like(R["yd"])
+    off = R["off"]
+    for e in range(E):
+        a, b = int(off[e]), int(off[e + 1])
+        if a < b:
+            b_yd[a:b] = EPS_BF16 * (np.abs(R["h"][a:b]) @ np.abs(W2[e])) + EPS_BF16 * np.abs(R["yd"][a:b])
+    return 1.25 * (O.combine(b_yd, np.abs(R["pd"]), R["inv"], S, K) + EPS_BF16 * np.abs(R["y"]))
+
+
 def assert_within(got, ref, bound, what):
     d = np.abs(got - ref)
     bad = d > bound
@@ -88,7 +105,13 @@ def assert_within(got, ref, bound, what):
                                        (1024, 512, 32, 8, 256), (1, 8, 2, 1, 8), (7, 72, 3, 2, 24),
                                        (64, 136, 1024, 32, 40)])
 def test_backward_small(S, D, E, K, F):
-    g = torch.Generator().manual_seed(S + D + E)
+    check_backward_case(S, D, E, K, F, seed=S + D + E)
+
+
+def check_backward_case(S, D, E, K, F, seed):
+    """Forward and backward chain of one seeded case (the last expert dead)
+    against the oracle, with elementwise bounds on every gradient."""
+    g = torch.Generator().manual_seed(seed)
     x = torch.randn((S, D), generator=g).to(torch.bfloat16)
     logits = torch.randn((S, E), generator=g)
     logits[:, E - 1] = float("-inf")          # one dead expert
@@ -98,7 +121,7 @@ def test_backward_small(S, D, E, K, F):
     G = gpu_chain(x.to(DEV), logits.to(DEV), W1.to(DEV), W2.to(DEV), dy.to(DEV), K)
     R = oracle_chain(np64(x), logits.numpy(), np64(W1), np64(W2), np64(dy), K, E)
     assert np.array_equal(npi(G["r"]["counts"]), R["counts"])
-    assert_bf16_close(np64(G["y"]), R["y"], "y")
+    assert_within(np64(G["y"]), R["y"], y_bound(R, np64(W2), S, K, E), "y")
     assert_grad_close(np64(G["dp"]), R["dp"], "dp")
     gW1, gW2 = np64(G["dW1"]), np64(G["dW2"])
     off = R["off"]

@@ -5,7 +5,8 @@ from 1 up, router biases that unbalance or empty experts, the MX-FP8 payload
 and the production variant (sigmoid routing, shared expert, balance loss).
 The checks are those of the fixed-shape layer tests: exact routing for
 tokens away from score ties, valid routing for the rest, and the bf16
-output bar."""
+output bar; the backward chain (combine^T, both dgrads and wgrads,
+dispatch^T) is held to its elementwise bounds."""
 import numpy as np
 import pytest
 import torch
@@ -14,6 +15,7 @@ from paper_2608_28511_amd import layer
 from paper_2608_28511_amd.workloads import PRODUCTION, WORKLOADS, make_inputs
 
 from gpu_helpers import np64
+from test_gpu_backward import check_backward_case
 from test_gpu_layer import DEV, check_layer, run_layer
 from test_gpu_mxfp8 import _mx_layer_vs_oracle
 from test_gpu_production import check_prod_layer, run_prod_layer
@@ -78,3 +80,19 @@ def test_random_prod_layer_fwd(i):
     out = run_prod_layer(s, inp)
     n_amb = check_prod_layer(s, inp, out, None, s.aux_coeff)
     assert n_amb <= max(2, s.S // 8)
+
+
+def _bwd_shape(i):
+    rng = np.random.default_rng(11000 + i)
+    E = int(rng.integers(2, 201))
+    K = int(rng.integers(1, min(E - 1, 10) + 1))
+    S = int(rng.integers(1, 301))
+    D = 8 * int(rng.integers(1, 65))
+    F = 8 * int(rng.integers(1, 65))
+    return S, D, E, K, F
+
+
+@pytest.mark.parametrize("i", range(12), ids=lambda i: "s{}_d{}_e{}_k{}_f{}".format(*_bwd_shape(i)))
+def test_random_backward(i):
+    S, D, E, K, F = _bwd_shape(i)
+    check_backward_case(S, D, E, K, F, seed=300 + i)
