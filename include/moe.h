@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 3
+#define MOE_ABI_VERSION 4
 
 typedef uint16_t moe_bf16; /* bit pattern of a bfloat16 value (b_x = 2 bytes) */
 

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_status_payload(lib):
-    assert L.moe_abi_version() == 3
+    assert L.moe_abi_version() == 4
     assert L.moe_status_string(0) == "ok"
     for code in range(-6, 0):
         assert L.moe_status_string(code) not in ("ok", "unknown status")
@@ -49,6 +49,10 @@ def test_version_status_payload(lib):
     # MX-FP8 hidden payload: b_x = 1 + 1/32
     assert L.moe_mx_payload_bytes(8192, 6, 2048) == 8192 * 6 * (2048 + 64 + 4) == 104_005_632
     assert L.moe_mx_payload_bytes(8192, 6, 2040) == 0
+    # scale allocation read by the MX up projection: whole 4-byte words
+    assert L.moe_mx_scale_alloc_bytes(3, 96) == 12 and L.moe_mx_scale_alloc_bytes(111, 96) == 336
+    assert L.moe_mx_scale_alloc_bytes(49152, 2048) == 49152 * 64
+    assert L.moe_mx_scale_alloc_bytes(4, 48) == 0 and L.moe_mx_scale_alloc_bytes(-1, 64) == 0
 
 
 def test_workspace_queries(lib):
@@ -194,6 +198,17 @@ def test_production_validation_errors(lib):
     assert lib.moe_dispatch_mxfp8(FAKE, None, FAKE, 4, 64, 2, FAKE, FAKE, FAKE, st) == -1
     assert lib.moe_mxfp8_dequant(FAKE, FAKE, 4, 40, FAKE, st) == -2
     assert lib.moe_mxfp8_dequant(FAKE, None, 4, 64, FAKE, st) == -1
+    # MX-FP8 up projection: Kd a multiple of 32, 16-byte aligned codes, scale
+    # and schedule given, epilogue 0 or 1, weights within the descriptor range
+    assert lib.moe_grouped_gemm_mxfp8(FAKE, FAKE, FAKE, 2, 4, 48, 16, FAKE, 1, FAKE, None, st) == -2
+    assert lib.moe_grouped_gemm_mxfp8(C.c_void_p(0x10008), FAKE, FAKE, 2, 4, 64, 16, FAKE, 1, FAKE, None,
+                                      st) == -3
+    assert lib.moe_grouped_gemm_mxfp8(FAKE, None, FAKE, 2, 4, 64, 16, FAKE, 1, FAKE, None, st) == -1
+    assert lib.moe_grouped_gemm_mxfp8(FAKE, FAKE, None, 2, 4, 64, 16, FAKE, 1, FAKE, None, st) == -1
+    assert lib.moe_grouped_gemm_mxfp8(FAKE, FAKE, FAKE, 2, 4, 64, 16, FAKE, 2, FAKE, None, st) == -6
+    assert lib.moe_grouped_gemm_mxfp8(FAKE, FAKE, FAKE, 2, 4, 64, 16, FAKE, 0, FAKE, FAKE, st) == -2
+    assert lib.moe_grouped_gemm_mxfp8(FAKE, FAKE, FAKE, 2, 4, 65536, 16384, FAKE, 0, FAKE, None, st) == -6
+    assert lib.moe_grouped_gemm_mxfp8(FAKE, FAKE, FAKE, 2, 0, 64, 16, FAKE, 1, FAKE, None, st) == 0
     assert lib.moe_route_sigmoid(FAKE, None, 4, 8, 9, *[FAKE] * 6, FAKE, 1 << 20, st) == -2
     assert lib.moe_route_sigmoid(FAKE, ODD, 4, 8, 2, *[FAKE] * 6, FAKE, 1 << 20, st) == -3
     assert lib.moe_route_sigmoid(FAKE, None, 4, 8, 2, *[FAKE] * 6, FAKE, 4, st) == -4
