@@ -312,7 +312,16 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) 
     const int per = p.m_tiles * p.n_tiles;
     const int e = lid / per;
     const int in = lid - e * per;
-    const int mt = in % p.m_tiles, nt = in / p.m_tiles;
+    // Two m-tiles at a time across all n-tiles: the ~32 items an XCD runs
+    // together then share two m-tiles of A rows and a run of n-tiles of B
+    // rows, which fit its L2 (all m-tiles at a time did not: the 31.5B
+    // shape's wgrad 3286 -> ~3100 us; groups of 4 and 8 fell in between).
+    constexpr int kKgM = 2;
+    const int width = kKgM * p.n_tiles;
+    const int grp = in / width, first_m = grp * kKgM;
+    const int gsz = (p.m_tiles - first_m) < kKgM ? (p.m_tiles - first_m) : kKgM;
+    const int in2 = in - grp * width;
+    const int mt = first_m + in2 % gsz, nt = in2 / gsz;
     const int64_t row0 = (int64_t)mt * T::BM;
     const int64_t row_hi = (row0 + T::BM) < p.M ? (row0 + T::BM) : p.M;
     int64_t k_begin = p.offsets != nullptr ? (int64_t)p.offsets[e] : (int64_t)e * p.kchunk;
