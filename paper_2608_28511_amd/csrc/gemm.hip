@@ -17,11 +17,13 @@
 //   256 x 256, 32 k per stage, 4-stage ring of 32 KB stages -- one third
 //   fewer operand bytes per product, for launches long enough that the
 //   coarser tile count does not leave the last round of CUs half idle.
-// The operand copies into LDS, not the MFMAs, bound the 128-row tile (the
-// per-CU texture-data return path measured 82% busy at 0.42 of the MFMA
-// rate); the 256-row tile moves a third less per flop.  One workgroup fills
-// a CU's LDS, so each SIMD runs two wavefronts: one wave's address
-// arithmetic, barrier and LDS latency overlap the other's MFMAs.
+// Neither the MFMAs nor copy bandwidth bound the kernel: the per-CU
+// texture-data return path reads 82% busy at 0.42 of the MFMA rate while a
+// plain stream of the same copies reaches ~4x these bytes per clock, so the
+// waits are on copy latency (a quarter of the operand reads miss L2); the
+// 256-row tile moves a third less per flop.  One workgroup fills a CU's LDS,
+// so each SIMD runs two wavefronts: one wave's address arithmetic, barrier
+// and LDS latency overlap the other's MFMAs.
 //
 // Operands never pass through registers on their way to LDS: every 16-byte
 // chunk is copied by a buffer load with an LDS destination into the LDS
@@ -50,9 +52,19 @@
 // store is 16 contiguous bytes and one store instruction covers 8 whole
 // 128-byte rows; stores go through a range-checked buffer descriptor, so
 // rows past the tile's end and columns past N are dropped by the hardware.
-// Squared-ReLU (up projection) is fused there; the dgrad epilogue that
-// multiplies by the activation derivative reads the saved pre-activation
-// directly.
+// Squared-ReLU (up projection) is fused there, and so is the dgrad's
+// product with the activation derivative, whose saved pre-activation each
+// lane loads at its accumulators' positions.
+//
+// The up projection can also read its A operand as the MX-FP8 dispatch
+// payload (gemm_rows_mx_kernel): codes and block scales travel through the
+// same ring and each lane decodes its fragment right before the MFMA, with a
+// result identical to decoding first (see MxDma and mx_frag).
+//
+// KGRP mode (weight gradients) runs one workgroup per (expert, m-tile,
+// n-tile) item, two m-tiles at a time across all n-tiles so that the items
+// an XCD runs together keep their operand rows in its L2, and writes its fp32
+// tile through LDS as whole 256-byte row pieces with non-temporal stores.
 //
 // Expert segments are located through device-side tile tables (expert,
 // first row, end row of every 128-row and every 256-row tile, built from the
