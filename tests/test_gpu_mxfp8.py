@@ -121,6 +121,9 @@ def test_layer_fwd_mxfp8(name, n_samples):
 # of 4 puts the last scale bytes in the allocation's padded word; the last
 # case is long enough for the 256-row tiles.
 _GEMM_MX_CASES = [
+    ("normal", 1, 1, 32, 1, 0, 8),         # one row, one 32-element block, N = 8
+    ("wide", 19, 2, 32, 3, 1, 24),         # Kd = 32: the only stage is half a stage
+    ("tiny", 40, 4, 64, 7, 2, 264),        # Kd = 64: exactly one stage
     ("normal", 37, 3, 96, 5, 1, 72),
     ("normal", 256, 6, 2048, 8, 0, 1024),
     ("wide", 100, 7, 2688, 16, 3, 264),
