@@ -96,3 +96,28 @@ def _bwd_shape(i):
 def test_random_backward(i):
     S, D, E, K, F = _bwd_shape(i)
     check_backward_case(S, D, E, K, F, seed=300 + i)
+
+
+def _latent_shape(i):
+    rng = np.random.default_rng(13000 + i)
+    E = int(rng.integers(1, 97))
+    K = int(rng.integers(1, min(E, 8) + 1))
+    S = int(rng.integers(1, 257))
+    H = 8 * int(rng.integers(1, 97))
+    D = 8 * int(rng.integers(1, 65))
+    F = 8 * int(rng.integers(1, 65))
+    return WORKLOADS["latent_s16384_h4096_d1024_e128_k6"].scaled(name=f"latent_random{i}", S=S, H=H, D=D, E=E,
+                                                                 K=K, F=F, seed=400 + i)
+
+
+@pytest.mark.parametrize("i", range(6), ids=lambda i: "s{S}_h{H}_d{D}_e{E}_k{K}_f{F}".format(
+    **_latent_shape(i).__dict__))
+def test_random_latent_layer_fwd(i):
+    """The latent layer (dense projections H -> D before routing and D -> H
+    after the combine) at random widths: x_lat within its fp32/bf16 bound,
+    routing from the GPU's own latent rows, y against the oracle."""
+    s = _latent_shape(i)
+    inp = make_inputs(s, device=DEV)
+    out = run_layer(s, inp)
+    n_amb = check_layer(s, inp, out, None, seed=i)
+    assert n_amb <= max(2, s.S // 8)
