@@ -276,16 +276,20 @@ __global__ __launch_bounds__(256) void router_dx_kernel(const float* __restrict_
     int e_l = lane < K ? topk_idx[t * K + lane] : -1;
     if (e_l >= E) e_l = -1;
     const float w_l = e_l >= 0 ? ds[t * E + e_l] : 0.f;
-    for (int c = lane; c < D4; c += 64) {
+    // the loop bound is wave-uniform, so every lane takes part in the
+    // shuffles of lanes 0 .. K-1; only the column accesses are masked
+    for (int cw = 0; cw < D4; cw += 64) {
+        const int c = cw + lane;
+        const bool on = c < D4;
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
         for (int k = 0; k < K; ++k) {
             const int ek = __shfl(e_l, k);
             const float w = __shfl(w_l, k);
-            if (ek < 0) continue;
+            if (ek < 0 || !on) continue;
             const float4 r = WrT[(int64_t)ek * D4 + c];
             acc.x += w * r.x; acc.y += w * r.y; acc.z += w * r.z; acc.w += w * r.w;
         }
-        dx[t * D4 + c] = acc;
+        if (on) dx[t * D4 + c] = acc;
     }
 }
 

@@ -19,6 +19,8 @@ from test_gpu_backward import check_backward_case
 from test_gpu_layer import DEV, check_layer, run_layer
 from test_gpu_mxfp8 import _mx_layer_vs_oracle
 from test_gpu_production import check_prod_layer, run_prod_layer
+from test_gpu_router_bwd import test_latent_proj_bwd_matches_oracle as _latent_bwd_case
+from test_gpu_router_bwd import test_router_bwd_matches_oracle as _router_bwd_case
 
 pytestmark = pytest.mark.gpu
 
@@ -121,3 +123,27 @@ def test_random_latent_layer_fwd(i):
     out = run_layer(s, inp)
     n_amb = check_layer(s, inp, out, None, seed=i)
     assert n_amb <= max(2, s.S // 8)
+
+
+def _router_bwd_shape(i):
+    rng = np.random.default_rng(15000 + i)
+    E = int(rng.integers(2, 301))
+    return (int(rng.integers(1, 601)), 8 * int(rng.integers(1, 129)), E, int(rng.integers(1, min(E, 12) + 1)))
+
+
+@pytest.mark.parametrize("i", range(8), ids=lambda i: "s{}_d{}_e{}_k{}".format(*_router_bwd_shape(i)))
+def test_random_router_bwd(i):
+    """Router backward (softmax renormalisation gradient, dWr, dbias, dx_r)
+    at random shapes, with the fixed-shape test's elementwise bounds."""
+    _router_bwd_case(*_router_bwd_shape(i))
+
+
+def _latent_bwd_shape(i):
+    rng = np.random.default_rng(17000 + i)
+    return int(rng.integers(1, 801)), 8 * int(rng.integers(1, 129)), 8 * int(rng.integers(1, 129))
+
+
+@pytest.mark.parametrize("i", range(6), ids=lambda i: "m{}_k{}_n{}".format(*_latent_bwd_shape(i)))
+def test_random_latent_proj_bwd(i):
+    """Latent projection backward (dx_in, dW) at random shapes."""
+    _latent_bwd_case(*_latent_bwd_shape(i))

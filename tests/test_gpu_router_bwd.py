@@ -43,8 +43,11 @@ def _route_inputs(S, D, E, K, seed, bias=False):
     return x, Wr, idx, p, dp
 
 
+# (309, 264, 146, 6): D/4 = 66 columns of float4, so the second 64-column
+# chunk has 2 active lanes, fewer than K -- a regression case for dx_r, whose
+# shuffles of the K picks once ran inside that divergent chunk loop
 @pytest.mark.parametrize("S,D,E,K", [(64, 64, 4, 2), (300, 136, 37, 5), (1024, 512, 64, 6),
-                                     (777, 2048, 256, 8)])
+                                     (777, 2048, 256, 8), (309, 264, 146, 6)])
 def test_router_bwd_matches_oracle(S, D, E, K):
     x, Wr, idx, p, dp = _route_inputs(S, D, E, K, seed=S + D + E)
     G = layer.router_bwd(x.to(DEV), Wr.to(DEV), torch.as_tensor(idx).to(DEV), torch.as_tensor(p).to(DEV),
