@@ -19,6 +19,21 @@ from test_gpu_backward import check_backward_case
 from test_gpu_layer import DEV, check_layer, run_layer
 from test_gpu_mxfp8 import _mx_layer_vs_oracle
 from test_gpu_production import check_prod_layer, run_prod_layer
+from test_gpu_ffn import test_grouped_ffn_exact as _ffn_exact_case
+from test_gpu_ffn import test_grouped_ffn_random as _ffn_random_case
+from test_gpu_ffn import test_latent_proj as _latent_proj_case
+from test_gpu_mxfp8 import test_dispatch_mxfp8_bit_exact as _mx_dispatch_case
+from test_gpu_permute import test_combine_bwd_matches_oracle as _combine_bwd_case
+from test_gpu_permute import test_combine_matches_oracle as _combine_case
+from test_gpu_permute import test_dispatch_bit_exact_and_eq1_bytes as _dispatch_case
+from test_gpu_production import test_combine_add as _combine_add_case
+from test_gpu_production import test_route_sigmoid_suites as _route_sigmoid_case
+from test_gpu_production import test_router_bwd_sigmoid_matches_oracle as _router_bwd_sigmoid_case
+from test_gpu_production import test_seq_aux_loss as _seq_aux_case
+from test_gpu_production import test_shared_expert_bwd as _shared_bwd_case
+from test_gpu_production import test_shared_expert_fwd as _shared_fwd_case
+from test_gpu_route import test_route_suites as _route_case
+from test_gpu_route import test_router_logits as _router_logits_case
 from test_gpu_router_bwd import test_latent_proj_bwd_matches_oracle as _latent_bwd_case
 from test_gpu_router_bwd import test_router_bwd_matches_oracle as _router_bwd_case
 
@@ -147,3 +162,74 @@ def _latent_bwd_shape(i):
 def test_random_latent_proj_bwd(i):
     """Latent projection backward (dx_in, dW) at random shapes."""
     _latent_bwd_case(*_latent_bwd_shape(i))
+
+
+# Every other entry point with shape arguments, at seeded random shapes that
+# keep each test's own rules (widths multiples of 8, MX widths of 32, K <= E,
+# sequences that divide the tokens).
+def _r(i, salt):
+    return np.random.default_rng(19000 + 100 * salt + i)
+
+
+def _w(rng, hi):
+    return 8 * int(rng.integers(1, hi + 1))
+
+
+def _stage_cases():
+    cases = []
+    kinds = ["normal", "quantised", "equal", "signed0", "masked"]
+    for i in range(5):
+        rng = _r(i, 1)
+        E = int(rng.integers(1, 1025)); S = int(rng.integers(1, 3001))
+        cases.append(("route", (kinds[i], S, E, int(rng.integers(1, min(E, 32) + 1)))))
+        rng = _r(i, 2)
+        E = int(rng.integers(1, 1025)); S = int(rng.integers(1, 3001))
+        cases.append(("route_sigmoid", (kinds[i], S, E, int(rng.integers(1, min(E, 32) + 1)), bool(i % 2))))
+    for i in range(4):
+        rng = _r(i, 3)
+        cases.append(("router_logits", (int(rng.integers(1, 2001)), _w(rng, 300), int(rng.integers(1, 300)),
+                                        bool(i % 2))))
+        rng = _r(i, 4)
+        T = int(rng.integers(1, 400)); E = int(rng.integers(1, 400))
+        cases.append(("seq_aux", (T * int(rng.integers(1, 6)), E, int(rng.integers(1, min(E, 12) + 1)), T)))
+        rng = _r(i, 5)
+        T = int(rng.integers(1, 300)); E = int(rng.integers(2, 300))
+        cases.append(("router_bwd_sigmoid", (T * int(rng.integers(1, 4)), _w(rng, 200), E,
+                                             int(rng.integers(1, min(E, 8) + 1)), T, bool(i % 2))))
+        rng = _r(i, 6)
+        cases.append(("shared_fwd", (int(rng.integers(1, 1500)), _w(rng, 200), _w(rng, 200))))
+        rng = _r(i, 7)
+        cases.append(("shared_bwd", (int(rng.integers(1, 1500)), _w(rng, 200), _w(rng, 200))))
+        rng = _r(i, 8)
+        cases.append(("combine_add", (int(rng.integers(1, 1500)), _w(rng, 300), int(rng.integers(1, 13)))))
+        for name, salt in (("dispatch", 9), ("combine", 10), ("combine_bwd", 11)):
+            rng = _r(i, salt)
+            E = int(rng.integers(1, 300))
+            cases.append((name, (int(rng.integers(1, 1500)), _w(rng, 300), E, int(rng.integers(1, min(E, 12) + 1)))))
+        rng = _r(i, 12)
+        E = int(rng.integers(1, 200))
+        cases.append(("ffn_exact" if i % 2 else "ffn_random",
+                      (int(rng.integers(1, 4000)), _w(rng, 80), _w(rng, 80), E, int(rng.integers(0, E)),
+                       float(rng.choice([0.0, 1.5])))))
+        rng = _r(i, 13)
+        cases.append(("latent_proj", (int(rng.integers(1, 3000)), _w(rng, 200), _w(rng, 200))))
+        rng = _r(i, 14)
+        D = 32 * int(rng.integers(4, 60))
+        cases.append(("mx_dispatch", (["normal", "wide", "tiny", "edge"][i], int(rng.integers(1, 800)), D,
+                                      int(rng.integers(1, 9)))))
+    return cases
+
+
+_STAGES = {"route": _route_case, "route_sigmoid": _route_sigmoid_case, "router_logits": _router_logits_case,
+           "seq_aux": _seq_aux_case, "router_bwd_sigmoid": _router_bwd_sigmoid_case,
+           "shared_fwd": _shared_fwd_case, "shared_bwd": _shared_bwd_case, "combine_add": _combine_add_case,
+           "dispatch": _dispatch_case, "combine": _combine_case, "combine_bwd": _combine_bwd_case,
+           "ffn_exact": _ffn_exact_case, "ffn_random": _ffn_random_case, "latent_proj": _latent_proj_case,
+           "mx_dispatch": _mx_dispatch_case}
+_STAGE_CASES = _stage_cases()
+
+
+@pytest.mark.parametrize("name,args", _STAGE_CASES,
+                         ids=[f"{n}-" + "_".join(str(a) for a in args) for n, args in _STAGE_CASES])
+def test_random_stage(name, args):
+    _STAGES[name](*args)
