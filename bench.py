@@ -620,7 +620,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        log(f"cpu baseline: oracle on {args.cpu_tokens} tokens")
+        log(f"cpu baseline: oracle on {args.cpu_tokens or s.S} tokens")
         cpu = cpu_baseline(s, sets[0], args.cpu_tokens, args.payload)
 
     rec = {
