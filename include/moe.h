@@ -31,6 +31,10 @@
  *   - Outputs must not alias inputs.  Results are deterministic: the same
  *     inputs give bit-identical outputs on every call.
  *   - S == 0 (or R == 0) is valid and enqueues nothing.
+ *   - Debugging only: with MOE_DEBUG_SYNC=1 in the environment (read once per
+ *     process) every launch is followed by a synchronisation of `stream` and
+ *     an error check, so a kernel fault is reported as MOE_ERR_HIP by the
+ *     entry point that enqueued it.  Off by default.
  *   - Limits: 1 <= E <= 1024, 1 <= K <= min(E, 32), D and F multiples of 8
  *     in [8, 65536], S*K < 2^31.  The grouped GEMM copies its
  *     operands through range-checked buffer descriptors of at most 2^31
@@ -49,7 +53,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 4
+#define MOE_ABI_VERSION 5
 
 typedef uint16_t moe_bf16; /* bit pattern of a bfloat16 value (b_x = 2 bytes) */
 
@@ -208,7 +212,9 @@ int moe_latent_proj(const moe_bf16* A, const moe_bf16* W, int64_t M, int32_t Kd,
 /* Whole layer forward on one stream, no host synchronisation.             */
 /* ---------------------------------------------------------------------- */
 typedef struct {
-    uint32_t struct_size;      /* sizeof(moe_layer_fwd_args) */
+    uint32_t struct_size;      /* sizeof(moe_layer_fwd_args), or MOE_LAYER_FWD_ARGS_BASE_SIZE for a
+                                  caller that fills only the fields up to ws_bytes (every later
+                                  field then reads as zero / NULL) */
     int64_t S;
     int32_t H;                 /* 0: no latent projection (x is [S, D]) */
     int32_t D, E, K, F;
@@ -221,7 +227,6 @@ typedef struct {
     const moe_bf16* Wup;       /* [D, H] when H > 0, else NULL */
     moe_bf16* y;               /* [S, H] if H > 0 else [S, D] */
     /* Optional exported intermediates: NULL means "keep in workspace". */
-    moe_bf16* x_lat;           /* [S, D]  (H > 0 only) */
     float* logits;             /* [S, E] */
     int32_t* topk_idx;         /* [S, K] */
     float* topk_prob;          /* [S, K] */
@@ -234,9 +239,11 @@ typedef struct {
     moe_bf16* h;               /* [S*K, F] */
     moe_bf16* u_save;          /* [S*K, F] pre-activation; NULL = not saved */
     moe_bf16* y_disp;          /* [S*K, D] */
-    moe_bf16* y_lat;           /* [S, D]  (H > 0 only) */
     void* ws;                  /* workspace, >= moe_layer_fwd_workspace_bytes */
     size_t ws_bytes;
+    /* ---- extensions after the base layout (read only when struct_size covers them) ---- */
+    moe_bf16* x_lat;           /* [S, D] exported latent router/dispatch input (H > 0 only) */
+    moe_bf16* y_lat;           /* [S, D] exported latent combine output (H > 0 only) */
     /* The paper's production variant (Section 5.2); all zero / NULL gives
      * the softmax layer above.  See the production-router section below. */
     int32_t score_fn;          /* MOE_SCORE_SOFTMAX or MOE_SCORE_SIGMOID */
@@ -257,6 +264,11 @@ typedef struct {
     uint8_t* x_scale;          /* [S*K, D/32] their E8M0 block scales, exported (in an allocation
                                   of moe_mx_scale_alloc_bytes(S*K, D) bytes) or NULL */
 } moe_layer_fwd_args;
+
+/* Size of the base layout: struct_size for callers that fill only the fields
+ * from struct_size through ws_bytes (the plain softmax layer with a bf16
+ * payload; a latent layer then keeps x_lat and y_lat in the workspace). */
+#define MOE_LAYER_FWD_ARGS_BASE_SIZE offsetof(moe_layer_fwd_args, x_lat)
 
 enum { MOE_PAYLOAD_BF16 = 0, MOE_PAYLOAD_MXFP8 = 1 };
 
@@ -308,15 +320,19 @@ int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const mo
                         moe_bf16* dx_disp, float* dW1, float* dW2,
                         void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* dx[t] = bf16( sum_{k<K} dx_disp[inv_perm[t*K+k]]  (+ dx_add[t]) ), the
- * transpose of moe_dispatch (an unweighted combine): the K rows are summed in
- * fp32 in ascending k, the optional fp32 addend (the router's contribution
- * to the input gradient, moe_router_bwd's dx_r) is added after them, and the
- * result is rounded once.
- *   dx_disp [S*K, D] bf16;  dx_add [S, D] fp32 (16-byte aligned) or NULL;
- *   dx [S, D] bf16 */
-int moe_dispatch_bwd(const moe_bf16* dx_disp, const int32_t* inv_perm, const float* dx_add,
-                     int64_t S, int32_t D, int32_t K, moe_bf16* dx, hipStream_t stream);
+/* dx[t] = bf16( sum_{k<K} dx_disp[inv_perm[t*K+k]] ), the transpose of
+ * moe_dispatch (an unweighted combine): the K rows are summed in fp32 in
+ * ascending k and the sum is rounded once.
+ *   dx_disp [S*K, D] bf16;  inv_perm [S*K] int32;  dx [S, D] bf16 */
+int moe_dispatch_bwd(const moe_bf16* dx_disp, const int32_t* inv_perm, int64_t S, int32_t D, int32_t K,
+                     moe_bf16* dx, hipStream_t stream);
+
+/* moe_dispatch_bwd with an fp32 addend: dx[t] = bf16( sum_k dx_disp[pos_k] +
+ * dx_add[t] ), the addend (the router's contribution to the input gradient,
+ * moe_router_bwd's dx_r, or the shared expert's) added after the K rows and
+ * before the one rounding.  dx_add [S, D] fp32, 16-byte aligned. */
+int moe_dispatch_bwd_add(const moe_bf16* dx_disp, const int32_t* inv_perm, const float* dx_add, int64_t S,
+                         int32_t D, int32_t K, moe_bf16* dx, hipStream_t stream);
 
 /* ---------------------------------------------------------------------- */
 /* Router backward (the learned router of Section 5.2) with the expert     */
@@ -333,7 +349,7 @@ size_t moe_router_bwd_workspace_bytes(int64_t S, int32_t D, int32_t E);
  *                                the MFMA as three bf16 terms)
  *   dbias = sum_t dlogits[t]     [E] fp32, or NULL
  *   dx_r  = dlogits Wr^T         [S, D] fp32 (the K nonzero terms, fp32 FMA),
- *                                or NULL; pass it to moe_dispatch_bwd as dx_add
+ *                                or NULL; pass it to moe_dispatch_bwd_add as dx_add
  * Every sum has a fixed order (deterministic).
  *   x_r [S, D] bf16;  Wr [D, E] fp32;  topk_idx, topk_prob, dp [S, K];
  *   dlogits [S, E] fp32 or NULL (then kept in the workspace).
@@ -506,7 +522,7 @@ size_t moe_shared_expert_bwd_workspace_bytes(int64_t S, int32_t D, int32_t Fs);
  *   du   = bf16( (dy @ Ws2^T) * 2 max(u_s, 0) )      (workspace)
  *   dx   = du @ Ws1^T  fp32 [S, D]; with accumulate_dx, added to what dx
  *          holds (e.g. moe_router_bwd*'s dx_r, then pass it as dx_add to
- *          moe_dispatch_bwd); dx may be NULL
+ *          moe_dispatch_bwd_add); dx may be NULL
  *   dWs1 = x^T du  [D, Fs] fp32;   dWs2 = h_s^T dy  [Fs, D] fp32
  *   (fixed-order sums over row chunks).
  * Errors: as moe_shared_expert_fwd; MOE_ERR_UNSUPPORTED if S*max(D, Fs)*2

@@ -33,17 +33,29 @@ class MoeError(RuntimeError):
         self.code = code
 
 
+# Fields of moe_layer_fwd_args up to ws_bytes (the base layout).
+LAYER_FWD_BASE_FIELDS = [
+    ("struct_size", u32), ("S", i64), ("H", i32), ("D", i32), ("E", i32), ("K", i32),
+    ("F", i32),
+    ("x", vp), ("Wr", vp), ("router_bias", vp), ("Wdown", vp), ("W1", vp), ("W2", vp),
+    ("Wup", vp), ("y", vp),
+    ("logits", vp), ("topk_idx", vp), ("topk_prob", vp), ("counts", vp),
+    ("offsets", vp), ("perm", vp), ("inv_perm", vp), ("x_disp", vp), ("p_disp", vp),
+    ("h", vp), ("u_save", vp), ("y_disp", vp),
+    ("ws", vp), ("ws_bytes", sz),
+]
+
+
+class LayerFwdBaseArgs(C.Structure):
+    """Mirror of the base layout of moe_layer_fwd_args (struct_size =
+    MOE_LAYER_FWD_ARGS_BASE_SIZE)."""
+    _fields_ = LAYER_FWD_BASE_FIELDS
+
+
 class LayerFwdArgs(C.Structure):
     """Mirror of moe_layer_fwd_args."""
-    _fields_ = [
-        ("struct_size", u32), ("S", i64), ("H", i32), ("D", i32), ("E", i32), ("K", i32),
-        ("F", i32),
-        ("x", vp), ("Wr", vp), ("router_bias", vp), ("Wdown", vp), ("W1", vp), ("W2", vp),
-        ("Wup", vp), ("y", vp),
-        ("x_lat", vp), ("logits", vp), ("topk_idx", vp), ("topk_prob", vp), ("counts", vp),
-        ("offsets", vp), ("perm", vp), ("inv_perm", vp), ("x_disp", vp), ("p_disp", vp),
-        ("h", vp), ("u_save", vp), ("y_disp", vp), ("y_lat", vp),
-        ("ws", vp), ("ws_bytes", sz),
+    _fields_ = LAYER_FWD_BASE_FIELDS + [
+        ("x_lat", vp), ("y_lat", vp),
         ("score_fn", i32), ("Fs", i32), ("sel_bias", vp), ("Ws1", vp), ("Ws2", vp),
         ("seq_len", i64), ("aux_coeff", C.c_float), ("aux_loss", vp), ("seq_counts", vp),
         ("h_s", vp), ("u_s", vp), ("y_s", vp),
@@ -78,7 +90,8 @@ _PROTOS = {
     "moe_grouped_ffn_bwd_workspace_bytes": (sz, [i32, i64, i32, i32]),
     "moe_grouped_ffn_bwd": (C.c_int, [vp, vp, vp, vp, vp, i32, i64, i32, i32, vp, vp, vp, vp, vp,
                                       vp, sz, vp]),
-    "moe_dispatch_bwd": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp]),
+    "moe_dispatch_bwd": (C.c_int, [vp, vp, i64, i32, i32, vp, vp]),
+    "moe_dispatch_bwd_add": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp]),
     "moe_router_bwd_workspace_bytes": (sz, [i64, i32, i32]),
     "moe_router_bwd": (C.c_int, [vp, vp, vp, vp, vp, i64, i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]),
     "moe_latent_proj_bwd_workspace_bytes": (sz, [i64, i32, i32]),
@@ -292,10 +305,15 @@ def moe_grouped_ffn_bwd(x_disp, u_save, h, dy_disp, offsets, E, R, D, F, W1, W2,
         0 if ws is None else ws.numel() * ws.element_size(), _stream()), "moe_grouped_ffn_bwd")
 
 
-def moe_dispatch_bwd(dx_disp, inv_perm, dx_add, S, D, K, dx):
-    _check(load().moe_dispatch_bwd(_ptr(dx_disp, BF16, "dx_disp"), _ptr(inv_perm, I32, "inv_perm"),
-                                   _ptr(dx_add, F32, "dx_add"), S, D, K, _ptr(dx, BF16, "dx"), _stream()),
-           "moe_dispatch_bwd")
+def moe_dispatch_bwd(dx_disp, inv_perm, S, D, K, dx):
+    _check(load().moe_dispatch_bwd(_ptr(dx_disp, BF16, "dx_disp"), _ptr(inv_perm, I32, "inv_perm"), S, D, K,
+                                   _ptr(dx, BF16, "dx"), _stream()), "moe_dispatch_bwd")
+
+
+def moe_dispatch_bwd_add(dx_disp, inv_perm, dx_add, S, D, K, dx):
+    _check(load().moe_dispatch_bwd_add(_ptr(dx_disp, BF16, "dx_disp"), _ptr(inv_perm, I32, "inv_perm"),
+                                       _ptr(dx_add, F32, "dx_add"), S, D, K, _ptr(dx, BF16, "dx"), _stream()),
+           "moe_dispatch_bwd_add")
 
 
 def moe_router_bwd_workspace_bytes(S, D, E) -> int:

@@ -2,7 +2,10 @@
 // workspace sizing and carving, and stream-ordered launch of the kernels.
 // Nothing here allocates, frees or synchronises device memory.
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
+
+#include <mutex>
 
 #include <hip/hip_runtime_api.h>
 
@@ -64,6 +67,20 @@ size_t align256(size_t b) { return (b + 255) / 256 * 256; }
     } while (0)
 
 }  // namespace
+
+namespace moe {
+
+bool debug_sync_enabled() {
+    static std::once_flag once;
+    static bool on = false;
+    std::call_once(once, [] {
+        const char* v = getenv("MOE_DEBUG_SYNC");
+        on = v != nullptr && v[0] != '\0' && strcmp(v, "0") != 0;
+    });
+    return on;
+}
+
+}  // namespace moe
 
 extern "C" {
 
@@ -319,9 +336,19 @@ int shared_fwd(const moe_bf16* x, const moe_bf16* Ws1, const moe_bf16* Ws2, int6
     return MOE_OK;
 }
 
+// The caller's arguments in the full layout: a base-layout struct (the
+// fields through ws_bytes) reads as zero / NULL beyond them.
+int widen_args(const moe_layer_fwd_args* in, moe_layer_fwd_args* out) {
+    if (in == nullptr) return MOE_ERR_NULL;
+    const uint32_t n = in->struct_size;
+    if (n != sizeof(moe_layer_fwd_args) && n != MOE_LAYER_FWD_ARGS_BASE_SIZE) return MOE_ERR_SHAPE;
+    memset(out, 0, sizeof *out);
+    memcpy(out, in, n);
+    out->struct_size = sizeof *out;
+    return MOE_OK;
+}
+
 int check_layer_args(const moe_layer_fwd_args* a) {
-    if (a == nullptr) return MOE_ERR_NULL;
-    if (a->struct_size != sizeof(moe_layer_fwd_args)) return MOE_ERR_SHAPE;
     MOE_TRY(check_route_shape(a->S, a->E, a->K));
     if (!dim_ok(a->D) || !dim_ok(a->F)) return MOE_ERR_SHAPE;
     if (a->H != 0 && !dim_ok(a->H)) return MOE_ERR_SHAPE;
@@ -390,13 +417,19 @@ size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
 
 }  // namespace
 
-size_t moe_layer_fwd_workspace_bytes(const moe_layer_fwd_args* a) {
+size_t moe_layer_fwd_workspace_bytes(const moe_layer_fwd_args* args) {
+    moe_layer_fwd_args full;
+    if (widen_args(args, &full) != MOE_OK) return 0;
+    const moe_layer_fwd_args* a = &full;
     if (check_layer_args(a) != MOE_OK) return 0;
     LayerBufs b;
     return layer_layout(a, nullptr, &b);
 }
 
-int moe_layer_fwd(const moe_layer_fwd_args* a, hipStream_t stream) {
+int moe_layer_fwd(const moe_layer_fwd_args* args, hipStream_t stream) {
+    moe_layer_fwd_args full;
+    MOE_TRY(widen_args(args, &full));
+    const moe_layer_fwd_args* a = &full;
     MOE_TRY(check_layer_args(a));
     const int64_t S = a->S, R = S * a->K;
     const int H = a->H, D = a->D, E = a->E, K = a->K, F = a->F;
@@ -536,13 +569,23 @@ int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const mo
     return MOE_OK;
 }
 
-int moe_dispatch_bwd(const moe_bf16* dx_disp, const int32_t* inv_perm, const float* dx_add, int64_t S,
-                     int32_t D, int32_t K, moe_bf16* dx, hipStream_t stream) {
+int moe_dispatch_bwd(const moe_bf16* dx_disp, const int32_t* inv_perm, int64_t S, int32_t D, int32_t K,
+                     moe_bf16* dx, hipStream_t stream) {
     if (S < 0 || !dim_ok(D) || K < 1 || K > kMaxK || S * (int64_t)K >= kMaxRows) return MOE_ERR_SHAPE;
     const uint64_t R = (uint64_t)S * K;
     MOE_TRY(need(dx_disp, R * D * 2, 16));
     MOE_TRY(need(inv_perm, R * 4, 4));
-    MOE_TRY(opt(dx_add, 16));
+    MOE_TRY(need(dx, (uint64_t)S * D * 2, 16));
+    return hip_status(moe::launch_combine(dx_disp, nullptr, inv_perm, S, D, K, nullptr, dx, stream));
+}
+
+int moe_dispatch_bwd_add(const moe_bf16* dx_disp, const int32_t* inv_perm, const float* dx_add, int64_t S,
+                         int32_t D, int32_t K, moe_bf16* dx, hipStream_t stream) {
+    if (S < 0 || !dim_ok(D) || K < 1 || K > kMaxK || S * (int64_t)K >= kMaxRows) return MOE_ERR_SHAPE;
+    const uint64_t R = (uint64_t)S * K;
+    MOE_TRY(need(dx_disp, R * D * 2, 16));
+    MOE_TRY(need(inv_perm, R * 4, 4));
+    MOE_TRY(need(dx_add, (uint64_t)S * D * 4, 16));
     MOE_TRY(need(dx, (uint64_t)S * D * 2, 16));
     return hip_status(moe::launch_combine(dx_disp, nullptr, inv_perm, S, D, K, dx_add, dx, stream));
 }

@@ -165,13 +165,15 @@ hipError_t launch_seq_aux_loss(const float* logits, const int32_t* topk_idx, int
         else if (epl <= 8) MOE_AUX_CASE(8);
         else MOE_AUX_CASE(16);
 #undef MOE_AUX_CASE
-        hipError_t err = hipGetLastError();
+        hipError_t err = launch_check(st);
         if (err != hipSuccess) return err;
     }
     hipLaunchKernelGGL(seq_aux_expert_kernel, dim3((unsigned)E), dim3(256), 0, st, w.partP, w.partC, B, w.nck, E,
                        w.term, seq_counts);
+    const hipError_t err = launch_check(st);
+    if (err != hipSuccess) return err;
     hipLaunchKernelGGL(seq_aux_final_kernel, dim3(1), dim3(1024), 0, st, w.term, E, coef, loss);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 // sel_bias[e] += rate * sign(mean(counts) - counts[e]); the sign is taken
@@ -194,7 +196,7 @@ __global__ __launch_bounds__(1024) void expert_bias_update_kernel(const int32_t*
 
 hipError_t launch_expert_bias_update(const int32_t* counts, int E, float rate, float* sel_bias, hipStream_t st) {
     hipLaunchKernelGGL(expert_bias_update_kernel, dim3(1), dim3(1024), 0, st, counts, E, rate, sel_bias);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 }  // namespace moe

@@ -33,6 +33,21 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
 }
 
+// MOE_DEBUG_SYNC=1 in the environment (read once per process).
+bool debug_sync_enabled();
+
+// Status of the launches just enqueued on st: the launch error, and with
+// MOE_DEBUG_SYNC also the outcome of running them (the stream is
+// synchronised, so a fault surfaces at the entry point that enqueued it).
+inline hipError_t launch_check(hipStream_t st) {
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && debug_sync_enabled()) {
+        e = hipStreamSynchronize(st);
+        if (e == hipSuccess) e = hipGetLastError();
+    }
+    return e;
+}
+
 // Sizes handed to every launch: grid dimension from an element count.
 inline unsigned grid_for(int64_t n, int per_block) {
     return (unsigned)((n + per_block - 1) / per_block);

@@ -359,7 +359,7 @@ hipError_t launch_dispatch(const moe_bf16* x, const float* prob, const int32_t* 
     else
         hipLaunchKernelGGL(dispatch_kernel<false>, dim3(grid), dim3(nthr), 0, st, (const uint4*)x, prob, inv_perm, S,
                            d8, K, (uint4*)x_disp, p_disp, sched_offsets, E, ss, sl);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 hipError_t launch_combine(const moe_bf16* y_disp, const float* p_disp, const int32_t* inv_perm,
@@ -368,7 +368,7 @@ hipError_t launch_combine(const moe_bf16* y_disp, const float* p_disp, const int
     const int d8 = D / 8;
     hipLaunchKernelGGL(combine_kernel, dim3((unsigned)S), dim3(d8 >= 1024 ? 1024 : (d8 + 63) / 64 * 64), 0, st,
                        (const uint4*)y_disp, p_disp, inv_perm, S, d8, K, (const float4*)add, (uint4*)y);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 hipError_t launch_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const float* p_disp,
@@ -379,7 +379,7 @@ hipError_t launch_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const 
     hipLaunchKernelGGL(combine_bwd_kernel, dim3((unsigned)S), dim3(d8 >= 1024 ? 1024 : (d8 + 63) / 64 * 64), 0, st,
                        (const uint4*)dy, (const uint4*)y_disp, p_disp, inv_perm, S, D / 8, K,
                        (uint4*)dy_disp, dp);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 }  // namespace moe
@@ -398,7 +398,7 @@ hipError_t launch_dispatch_mx(const moe_bf16* x, const float* prob, const int32_
     hipLaunchKernelGGL(dispatch_mx_kernel, dim3(grid), dim3(d8 >= 1024 ? 1024 : (d8 + 63) / 64 * 64), 0, st,
                        (const uint4*)x, prob, inv_perm, S, d8, K, (uint2*)x_q, x_scale, p_disp, sched_offsets, E,
                        ss, sl);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 hipError_t launch_dequant_mx(const uint8_t* x_q, const uint8_t* x_scale, int64_t R, int D, moe_bf16* out,
@@ -407,7 +407,7 @@ hipError_t launch_dequant_mx(const uint8_t* x_q, const uint8_t* x_scale, int64_t
     if (n8 == 0) return hipSuccess;
     hipLaunchKernelGGL(dequant_mx_kernel, dim3(grid_for(n8, 256)), dim3(256), 0, st, (const uint2*)x_q, x_scale, n8,
                        (uint4*)out);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 }  // namespace moe

@@ -283,14 +283,18 @@ hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* t
             launch_topk<true>(logits, sel_bias, S, E, K, topk_idx, topk_prob, blkcnt, inv_perm, nblk, st);
         else
             launch_topk<false>(logits, nullptr, S, E, K, topk_idx, topk_prob, blkcnt, inv_perm, nblk, st);
+        const hipError_t e1 = launch_check(st);
+        if (e1 != hipSuccess) return e1;
     }
     hipLaunchKernelGGL(route_colscan_kernel, dim3((unsigned)((E + kScanCols - 1) / kScanCols)),
                        dim3(kScanThreads), 0, st, blkcnt, nblk, E, counts);
+    const hipError_t e2 = launch_check(st);
+    if (e2 != hipSuccess) return e2;
     const int64_t R = S * K;
     // at least one workgroup, so that offsets are written even for S == 0
     hipLaunchKernelGGL(route_scatter_kernel, dim3(R > 0 ? grid_for(R, 256) : 1u), dim3(256), 0, st,
                        topk_idx, blkcnt, counts, offsets, inv_perm, perm, R, K, E);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 }  // namespace moe

@@ -179,7 +179,7 @@ hipError_t launch_router_logits(const moe_bf16* x, const float* Wr, const float*
     uint16_t* w3 = (uint16_t*)ws;
     hipLaunchKernelGGL(router_split_kernel, dim3((unsigned)((D / 8 + 3) / 4), (unsigned)((E + 63) / 64)),
                        dim3(256), 0, st, Wr, D, E, w3);
-    hipError_t err = hipGetLastError();
+    hipError_t err = launch_check(st);
     if (err != hipSuccess || S == 0) return err;
     // 16-byte output stores only where every row start is 16-byte aligned
     const bool vec_out = (E % 4) == 0 && ((uintptr_t)logits % 16) == 0;
@@ -195,7 +195,7 @@ hipError_t launch_router_logits(const moe_bf16* x, const float* Wr, const float*
         if (narrow) MOE_ROUTER_LAUNCH(false, 32); else MOE_ROUTER_LAUNCH(false, 64);
     }
 #undef MOE_ROUTER_LAUNCH
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 }  // namespace moe

@@ -316,7 +316,7 @@ hipError_t launch_sum_planes(const float* part, int nchunk, int M, int N, int P,
     if (n == 0) return hipSuccess;
     hipLaunchKernelGGL(sum_planes_kernel, dim3(grid_for(n, 256)), dim3(256), 0, st, part, nchunk, M, N, P, ldp,
                        out);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 int wgrad_chunks(int64_t rows, int M, int N) {
@@ -388,7 +388,7 @@ hipError_t launch_router_bwd_sigmoid(const moe_bf16* x_r, const float* Wr, const
         else if (epl <= 8) MOE_DS_CASE(8);
         else MOE_DS_CASE(16);
 #undef MOE_DS_CASE
-        hipError_t err = hipGetLastError();
+        hipError_t err = launch_check(st);
         if (err != hipSuccess) return err;
     }
     if (!dense) return router_linear_bwd(x_r, Wr, topk_idx, ds, w, S, D, E, K, dWr, dbias, dx_r, st);
@@ -397,7 +397,7 @@ hipError_t launch_router_bwd_sigmoid(const moe_bf16* x_r, const float* Wr, const
     // dense dx_r [S, D] = ds6 [S, 6 Ep] . W6 [D, 6 Ep]^T, fp32 out
     hipLaunchKernelGGL(wr_split6_kernel, dim3(grid_for((int64_t)D * Ep, 256)), dim3(256), 0, st, Wr, D, E, Ep,
                        w.W6);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
+    if ((err = launch_check(st)) != hipSuccess) return err;
     return launch_grouped_rows((const moe_bf16*)ds6, 6 * (int64_t)Ep, (const moe_bf16*)w.W6, 6 * (int64_t)Ep, 0,
                                true, dx_r, D, EPI_F32, nullptr, nullptr, nullptr, 1, S, D, 6 * Ep, st);
 }
@@ -420,7 +420,7 @@ hipError_t launch_router_bwd(const moe_bf16* x_r, const float* Wr, const int32_t
         else if (epl <= 8) MOE_DS_CASE(8);
         else MOE_DS_CASE(16);
 #undef MOE_DS_CASE
-        if ((err = hipGetLastError()) != hipSuccess) return err;
+        if ((err = launch_check(st)) != hipSuccess) return err;
     }
     return router_linear_bwd(x_r, Wr, topk_idx, ds, w, S, D, E, K, dWr, dbias, dx_r, st);
 }
@@ -442,16 +442,18 @@ static hipError_t router_linear_bwd(const moe_bf16* x_r, const float* Wr, const 
         const int64_t chunk_rows = (S + nch - 1) / nch;
         hipLaunchKernelGGL(colsum_partial_kernel, dim3((unsigned)((E + 63) / 64), (unsigned)nch), dim3(256), 0, st,
                            ds, S, E, chunk_rows > 0 ? chunk_rows : 1, w.colpart);
+        if ((err = launch_check(st)) != hipSuccess) return err;
         hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)((E + 255) / 256)), dim3(256), 0, st, w.colpart,
                            nch, E, dbias);
-        if ((err = hipGetLastError()) != hipSuccess) return err;
+        if ((err = launch_check(st)) != hipSuccess) return err;
     }
     if (dx_r != nullptr && S > 0) {
         hipLaunchKernelGGL(transpose_f32_kernel, dim3((unsigned)((E + 31) / 32), (unsigned)((D + 31) / 32)),
                            dim3(256), 0, st, Wr, D, E, w.WrT);
+        if ((err = launch_check(st)) != hipSuccess) return err;
         hipLaunchKernelGGL(router_dx_kernel, dim3(grid_for(S, kRbTok)), dim3(256), 0, st, ds, topk_idx,
                            (const float4*)w.WrT, S, D / 4, E, K, (float4*)dx_r);
-        if ((err = hipGetLastError()) != hipSuccess) return err;
+        if ((err = launch_check(st)) != hipSuccess) return err;
     }
     return hipSuccess;
 }

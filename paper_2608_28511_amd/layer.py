@@ -153,7 +153,10 @@ def grouped_ffn_bwd(x_disp, u_save, h, dy_disp, offsets, W1, W2):
 def dispatch_bwd(dx_disp, inv_perm, S: int, K: int, dx_add: Optional[torch.Tensor] = None):
     D = dx_disp.shape[1]
     dx = _empty((S, D), BF16, dx_disp.device)
-    L.moe_dispatch_bwd(dx_disp, inv_perm, dx_add, S, D, K, dx)
+    if dx_add is None:
+        L.moe_dispatch_bwd(dx_disp, inv_perm, S, D, K, dx)
+    else:
+        L.moe_dispatch_bwd_add(dx_disp, inv_perm, dx_add, S, D, K, dx)
     return dx
 
 

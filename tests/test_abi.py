@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_status_payload(lib):
-    assert L.moe_abi_version() == 4
+    assert L.moe_abi_version() == 5
     assert L.moe_status_string(0) == "ok"
     for code in range(-6, 0):
         assert L.moe_status_string(code) not in ("ok", "unknown status")
@@ -100,6 +100,61 @@ def test_layer_struct_layout_matches(lib):
     assert L.moe_layer_fwd_workspace_bytes(a) == 0
 
 
+# The base layout of moe_layer_fwd_args, field for field, in the order the
+# boundary of the layer forward lists them: sizes, weights, output, the
+# optional exported intermediates, then the workspace.
+BOUNDARY_LAYER_FIELDS = [
+    "struct_size", "S", "H", "D", "E", "K", "F", "x", "Wr", "router_bias", "Wdown", "W1", "W2", "Wup", "y",
+    "logits", "topk_idx", "topk_prob", "counts", "offsets", "perm", "inv_perm", "x_disp", "p_disp", "h",
+    "u_save", "y_disp", "ws", "ws_bytes"]
+
+
+def _c_offsets(tmp_path, fields):
+    """offsetof of each field of moe_layer_fwd_args, sizeof and the base size,
+    from a host C program compiled against include/moe.h."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    src = tmp_path / "off.c"
+    lines = ["#include <stdio.h>", '#include "moe.h"', "int main(void) {"]
+    for f in fields:
+        lines.append(f'  printf("{f} %zu\\n", offsetof(moe_layer_fwd_args, {f}));')
+    lines += ['  printf("sizeof %zu\\n", sizeof(moe_layer_fwd_args));',
+              '  printf("base %zu\\n", (size_t)MOE_LAYER_FWD_ARGS_BASE_SIZE);', "  return 0;", "}"]
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "off"
+    subprocess.run(["gcc", "-std=c99", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", "-I", str(ROOT / "include"),
+                    str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    return {k: int(v) for k, v in (ln.split() for ln in out if ln)}
+
+
+def test_layer_args_layout_follows_the_boundary(lib, tmp_path):
+    full = [f for f, _ in L.LayerFwdArgs._fields_]
+    assert full[:len(BOUNDARY_LAYER_FIELDS)] == BOUNDARY_LAYER_FIELDS
+    c = _c_offsets(tmp_path, full)
+    for f in full:
+        assert getattr(L.LayerFwdArgs, f).offset == c[f], f
+    assert C.sizeof(L.LayerFwdArgs) == c["sizeof"]
+    # the base layout ends at ws_bytes; every extension follows it
+    assert c["base"] == C.sizeof(L.LayerFwdBaseArgs) == L.LayerFwdArgs.x_lat.offset
+    assert [f for f, _ in L.LayerFwdBaseArgs._fields_] == BOUNDARY_LAYER_FIELDS
+    # a caller that fills only the base layout gets the plain softmax layer
+    b = L.LayerFwdBaseArgs()
+    b.struct_size = C.sizeof(L.LayerFwdBaseArgs)
+    b.S, b.H, b.D, b.E, b.K, b.F = 512, 0, 256, 8, 2, 512
+    a = L.LayerFwdArgs()
+    a.struct_size = C.sizeof(L.LayerFwdArgs)
+    a.S, a.H, a.D, a.E, a.K, a.F = 512, 0, 256, 8, 2, 512
+    pb = C.cast(C.pointer(b), C.POINTER(L.LayerFwdArgs))
+    n = lib.moe_layer_fwd_workspace_bytes(pb)
+    assert n > 0 and n == lib.moe_layer_fwd_workspace_bytes(C.byref(a))
+    b.struct_size += 8
+    assert lib.moe_layer_fwd_workspace_bytes(pb) == 0
+    assert lib.moe_layer_fwd(pb, None) == -2
+
+
 def test_validation_errors_return_before_launch(lib):
     st = None
     # route: bad shapes, null and misaligned pointers, short workspace
@@ -139,8 +194,11 @@ def test_validation_errors_return_before_launch(lib):
                                    FAKE, FAKE, FAKE, 1 << 20, st) == -1
     assert lib.moe_grouped_ffn_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 4, 16, 16, FAKE, FAKE, FAKE,
                                    FAKE, FAKE, FAKE, 8, st) == -4
-    assert lib.moe_dispatch_bwd(FAKE, FAKE, None, 4, 16, 40, FAKE, st) == -2
-    assert lib.moe_dispatch_bwd(FAKE, FAKE, ODD, 4, 16, 2, FAKE, st) == -3
+    assert lib.moe_dispatch_bwd(FAKE, FAKE, 4, 16, 40, FAKE, st) == -2
+    assert lib.moe_dispatch_bwd(FAKE, None, 4, 16, 2, FAKE, st) == -1
+    assert lib.moe_dispatch_bwd(FAKE, FAKE, 4, 16, 2, ODD, st) == -3
+    assert lib.moe_dispatch_bwd_add(FAKE, FAKE, ODD, 4, 16, 2, FAKE, st) == -3
+    assert lib.moe_dispatch_bwd_add(FAKE, FAKE, None, 4, 16, 2, FAKE, st) == -1
     # router / latent backward
     assert lib.moe_router_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, 4, 16, 8, 9, None, FAKE, None, None, FAKE,
                               1 << 20, st) == -2                       # K > E
