@@ -715,9 +715,10 @@ template <bool B_K, int EPI, bool KTAIL>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_kernel(GemmArgs p) {
     __shared__ __attribute__((aligned(1024))) char smem[kRowsSmemBytes];
     typedef const __attribute__((address_space(4))) int32_t* cnt_ptr;
-    const int m_small = p.mtile_total != nullptr ? *(cnt_ptr)p.mtile_total : p.m_tiles;
+    // the table's count, never beyond the table (the builder caps it too)
+    const int m_small = p.mtile_total != nullptr ? min(*(cnt_ptr)p.mtile_total, p.m_tiles) : p.m_tiles;
     if constexpr (!B_K) {
-        const int m_tall = p.mtile_total_l != nullptr ? *(cnt_ptr)p.mtile_total_l : p.m_tiles_l;
+        const int m_tall = p.mtile_total_l != nullptr ? min(*(cnt_ptr)p.mtile_total_l, p.m_tiles_l) : p.m_tiles_l;
         if (take_tall_tiles(m_small, m_tall, p.n_tiles, (int)gridDim.x)) {
             rows_body<TileL, B_K, EPI, KTAIL>(p, smem, p.tiles_l, m_tall);
             return;
@@ -736,8 +737,9 @@ template <int EPI, bool KTAIL>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_rows_mx_kernel(GemmArgs p) {
     __shared__ __attribute__((aligned(1024))) char smem[kRowsMxSmemBytes];
     typedef const __attribute__((address_space(4))) int32_t* cnt_ptr;
-    const int m_small = p.mtile_total != nullptr ? *(cnt_ptr)p.mtile_total : p.m_tiles;
-    const int m_tall = p.mtile_total_l != nullptr ? *(cnt_ptr)p.mtile_total_l : p.m_tiles_l;
+    // the table's count, never beyond the table (the builder caps it too)
+    const int m_small = p.mtile_total != nullptr ? min(*(cnt_ptr)p.mtile_total, p.m_tiles) : p.m_tiles;
+    const int m_tall = p.mtile_total_l != nullptr ? min(*(cnt_ptr)p.mtile_total_l, p.m_tiles_l) : p.m_tiles_l;
     if (take_tall_tiles(m_small, m_tall, p.n_tiles, (int)gridDim.x)) {
         rows_body<TileLX, false, EPI, KTAIL>(p, smem, p.tiles_l, m_tall);
         return;
@@ -797,7 +799,7 @@ static hipError_t launch_rows(const GemmArgs& a, hipStream_t st) {
         hipLaunchKernelGGL((gemm_rows_kernel<B_K, EPI, true>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
     else
         hipLaunchKernelGGL((gemm_rows_kernel<B_K, EPI, false>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 template <int EPI>
@@ -808,7 +810,7 @@ static hipError_t launch_rows_mx(const GemmArgs& a, hipStream_t st) {
         hipLaunchKernelGGL((gemm_rows_mx_kernel<EPI, true>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
     else
         hipLaunchKernelGGL((gemm_rows_mx_kernel<EPI, false>), dim3((unsigned)G), dim3(kGemmThreads), 0, st, a);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 static hipError_t launch_rows_epi(const GemmArgs& a, bool b_kmajor, int epi, hipStream_t st) {
@@ -827,7 +829,7 @@ static hipError_t launch_rows_epi(const GemmArgs& a, bool b_kmajor, int epi, hip
 hipError_t launch_tile_schedule(const int32_t* offsets, int E, int64_t R, void* sched, hipStream_t st) {
     hipLaunchKernelGGL(tile_schedule_kernel, dim3(1), dim3(1024), 0, st, offsets, E, (int)R,
                        sched_part(sched, E, R, false), sched_part(sched, E, R, true));
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 // The operand-independent part of a ROWS launch: B, C, sizes and both tile
@@ -902,7 +904,7 @@ static hipError_t launch_kgrp(GemmArgs a, int64_t groups, hipStream_t st) {
         hipLaunchKernelGGL(gemm_kgrp_kernel<TileL>, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a);
     else
         hipLaunchKernelGGL(gemm_kgrp_kernel<TileS>, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a);
-    return hipGetLastError();
+    return launch_check(st);
 }
 
 hipError_t launch_chunked_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb, float* C,

@@ -2,9 +2,12 @@
 //
 // For expert segments offsets[0..E] (clamped to [0, R)) and each tile height
 // BM in {128, 256}:
-//   mtile_start[0] = 0, mtile_start[e+1] = sum_{e' <= e} ceil(count[e'] / BM)
+//   mtile_start[0] = 0, mtile_start[e+1] = min(sum_{e' <= e} ceil(count[e'] / BM), max_tiles)
 //   tiles[mt] = {e, row0, row_end, 0} for every BM-row tile mt of expert e,
 //               {-1, 0, 0, 0} for mt in [total, max_tiles) (the static grid bound).
+// Routing offsets are monotone, so the tile count never exceeds max_tiles;
+// malformed offsets (segments that overlap after clamping) could ask for
+// more, and the cap keeps every reader of the table inside it.
 // The buffer holds the 128-row part, then the 256-row part; each part is
 // mtile_start [E+1] int32, then (16-byte aligned) the tile table, and is
 // 256-byte aligned.  The tables are built by one workgroup of any size
@@ -65,9 +68,9 @@ __device__ __forceinline__ void sched_fill_part(const int32_t* seg_lo, const int
         }
     }
     __syncthreads();
-    for (int e = tid; e < E; e += nt) sp.mtile_start[e + 1] = cnt[e];
+    for (int e = tid; e < E; e += nt) sp.mtile_start[e + 1] = cnt[e] < sp.max_tiles ? cnt[e] : sp.max_tiles;
     if (tid == 0) sp.mtile_start[0] = 0;
-    const int total = cnt[E - 1];
+    const int total = cnt[E - 1] < sp.max_tiles ? cnt[E - 1] : sp.max_tiles;
     for (int mt = tid; mt < sp.max_tiles; mt += nt) {
         int4 v = make_int4(-1, 0, 0, 0);
         if (mt < total) {
