@@ -1,15 +1,22 @@
 """Benchmark of one routed MoE layer forward on one MI355X.
 
 Prints ONE JSON line on stdout (progress goes to stderr):
-  value        routed token-slots per second of moe_layer_fwd (S*K / layer time),
-               inputs resident in HBM, input sets rotated between steps so the
-               256 MB last-level cache cannot hold a step's weights
+  value        routed token-slots per second of moe_layer_fwd (S*K / layer time)
+               on the 256-expert CE-MoE-style layer (8192 tokens, D 2048, top-8,
+               F 2688: the largest forward of the five workloads by flops and
+               weight bytes), inputs resident in HBM, input sets rotated between
+               steps so the 256 MB last-level cache cannot hold a step's weights
+  other_workloads  the same layer measurement (value, ms per step, the
+               dominant GEMM's fraction of the MFMA peak) on the other full-size
+               workloads
   roofline     the dominant kernel (the larger of the two grouped GEMMs), each
                launch timed with its own HIP events on the stream it is launched
                on, inside the layer's own launch sequence, against the dense
                bf16 MFMA peak
-  stages       per-stage times and algorithmic GB/s or TFLOP/s
-  cpu_baseline the CPU oracle on a bounded sample of the same workload
+  stages       per-stage times and algorithmic GB/s or TFLOP/s; each launch of
+               a stage is timed alone with its own events, after an untimed
+               512 MB write that evicts its inputs from the last-level cache
+  cpu_baseline the CPU oracle on the same workload, with its per-stage times
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 """
@@ -46,7 +53,12 @@ def parse():
     p.add_argument("--settle-seconds", type=float, default=0.3,
                    help="run the layer this long before the warm-up steps, so the GPU is at its "
                         "sustained clock when the timed steps start")
-    p.add_argument("--workload", default="base_s8192_d2048_e64_k6")
+    p.add_argument("--workload", default="ce_s8192_d2048_e256_k8")
+    p.add_argument("--others", default="base_s8192_d2048_e64_k6,latent_s16384_h4096_d1024_e128_k6,"
+                                       "skew_s16384_d2048_e128_k8_bwd",
+                   help="comma-separated workloads measured after the headline one (layer rate and the "
+                        "dominant GEMM only); empty for none")
+    p.add_argument("--other-steps", type=int, default=20)
     p.add_argument("--sets", type=int, default=3, help="rotating input sets")
     p.add_argument("--payload", default="bf16", choices=("bf16", "mxfp8"),
                    help="dispatch payload of the timed layer (MX-FP8: b_x = 1 + 1/32)")
@@ -60,6 +72,9 @@ def parse():
     p.add_argument("--route-sweep", action="store_true",
                    help="also time the route alone over token counts 1K..128K (the workload's E and K) "
                         "and report its algorithmic GB/s; reported apart")
+    p.add_argument("--flush-bytes", type=int, default=512 << 20,
+                   help="bytes written between stage launches so no stage reads its inputs from the "
+                        "256 MB last-level cache")
     p.add_argument("--calib-bytes", type=int, default=1 << 30,
                    help="size of the plain copy run once for counter calibration")
     p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -195,6 +210,23 @@ def time_region(fn, reps, stream):
     return start.elapsed_time(end) / reps * 1e-3   # seconds
 
 
+def time_flushed(fn, reps, stream, flush):
+    """Average duration (s) of fn(i) over reps launches, each bracketed by its
+    own HIP events on `stream`, with flush() (an untimed write of more bytes
+    than the last-level cache holds) enqueued before each, so every launch
+    reads its inputs from HBM."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    torch.cuda.synchronize()
+    for i in range(reps):
+        flush()
+        ev[i][0].record(stream)
+        fn(i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    return sum(a.elapsed_time(b) for a, b in ev) / reps * 1e-3
+
+
 def step_times(fn, reps, stream):
     """Durations (us) of reps back-to-back calls fn(i), one HIP event pair
     per call on `stream`."""
@@ -316,7 +348,24 @@ def time_layer_gemms(_lib, sets, out, s, reps, stream, ws_router, ws_route, r_bu
     return up, down
 
 
+def host_info():
+    """nproc and the CPU model of the host this runs on."""
+    model = "unknown"
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "cpu_model": model}
+
+
 def cpu_baseline(s, inp, tokens, payload="bf16", min_seconds=10.0, max_runs=8):
+    """The float64 oracle on the first `tokens` tokens (0: all) of the same
+    workload, repeated until about min_seconds of CPU work.  For the softmax
+    layers the oracle's stage functions are called one by one, in the order
+    its layer forward calls them, and each is timed."""
     import numpy as np
     import torch
     from threadpoolctl import threadpool_info
@@ -340,6 +389,7 @@ def cpu_baseline(s, inp, tokens, payload="bf16", min_seconds=10.0, max_runs=8):
     extra = {}
     if s.H:
         extra = dict(Wdown=f64(inp["Wdown"]), Wup=f64(inp["Wup"]))
+    staged = s.score == "softmax" and not s.Fs and payload == "bf16"
     if s.score == "sigmoid":
         extra.update(score="sigmoid", sel_bias=f64(inp["sel_bias"]))
         if s.seq_len and T % s.seq_len == 0:   # the balance loss needs whole sequences
@@ -348,21 +398,122 @@ def cpu_baseline(s, inp, tokens, payload="bf16", min_seconds=10.0, max_runs=8):
         extra.update(Ws1=f64(inp["Ws1"]), Ws2=f64(inp["Ws2"]))
     if payload != "bf16":
         extra["payload"] = payload
-    # whole passes over the sample until about min_seconds of CPU work
+    stage_s = {}
+
+    def timed(name, fn, *a, **kw):
+        t0 = time.perf_counter()
+        r = fn(*a, **kw)
+        stage_s[name] = stage_s.get(name, 0.0) + time.perf_counter() - t0
+        return r
+
+    def staged_layer():
+        # the oracle's layer forward, stage by stage
+        x_r = timed("latent_down", O.latent_down, x, extra["Wdown"]) if s.H else x
+        logits = timed("router_logits", O.router_logits, x_r, Wr, bias)
+        idx, prob = timed("route", O.route, logits, s.K)
+        _, off, _, inv = timed("permutation", O.expert_permutation, idx, s.E)
+        x_disp, p_disp = timed("dispatch", O.dispatch, x_r, prob, inv, s.K)
+        _, _, y_disp = timed("expert_ffn", O.expert_ffn, x_disp, off, Experts(W1c), Experts(W2c))
+        y = timed("combine", O.combine, y_disp, p_disp, inv, T, s.K)
+        if s.H:
+            timed("latent_up", O.latent_up, y, extra["Wup"])
+
     runs, dt = 0, 0.0
     while runs < max_runs and (runs == 0 or dt < min_seconds):
         t0 = time.perf_counter()
-        O.layer_fwd(x, Wr, Experts(W1c), Experts(W2c), s.K, bias=bias, **extra)
+        if staged:
+            staged_layer()
+        else:
+            O.layer_fwd(x, Wr, Experts(W1c), Experts(W2c), s.K, bias=bias, **extra)
         dt += time.perf_counter() - t0
         runs += 1
     blas = [d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"]
-    return {
+    rec = {
         "value": runs * T * s.K / dt, "unit": "slots/s", "cores": int(max(blas) if blas else 1),
         "kind": "oracle",
-        "sample": f"{runs} passes over the first {T} of {s.S} tokens of the same workload through the "
+        "sample": f"{runs} pass(es) over the first {T} of {s.S} tokens of the same workload through the "
                   f"float64 oracle layer forward ({T * s.K} routed rows per pass, {dt:.1f} s in all; BLAS "
                   f"matmuls threaded, routing and permutation single-threaded Python)",
+        **host_info(),
     }
+    if stage_s:
+        rec["stage_seconds_per_pass"] = {k: round(v / runs, 3) for k, v in stage_s.items()}
+    return rec
+
+
+def settle_and_time(step, steps, warmup, settle_seconds, stream):
+    """Run the layer for settle_seconds and `warmup` steps, then time `steps`
+    steps with one pair of HIP events: seconds per step.  A GPU that has just
+    started work runs its first tens of steps ~10% slower (measured: 0.642 ms
+    per step after 5 warm-up steps, 0.579 ms after 100); a training or
+    serving loop runs at the sustained rate."""
+    import torch
+    t_end, i = time.perf_counter() + settle_seconds, 0
+    while time.perf_counter() < t_end:
+        step(i)
+        i += 1
+        if i % 8 == 0:
+            torch.cuda.synchronize()
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    return time_region(step, steps, stream)
+
+
+def other_workload(name, args, dev, stream):
+    """Layer rate and the dominant grouped GEMM of another workload: value,
+    ms per step and the GEMM's fraction of the bf16 MFMA peak, measured as
+    for the headline (rotating input sets, sustained clock, GEMM launches
+    timed inside the layer's own launch sequence where the layer has no
+    latent projection)."""
+    import torch
+    from paper_2608_28511_amd import _lib, layer
+    from paper_2608_28511_amd.workloads import PRODUCTION, WORKLOADS, make_inputs
+    s = {**WORKLOADS, **PRODUCTION}[name]
+    log(f"other workload {name}: {args.sets} input sets")
+    sets = [make_inputs(s, device=dev, seed=s.seed + 1000 * i) for i in range(args.sets)]
+    modes = dict(score=s.score, Fs=s.Fs, seq_len=s.seq_len, aux_coeff=s.aux_coeff)
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, **modes)
+
+    def step(i):
+        inp = sets[i % len(sets)]
+        lf(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"], Wdown=inp.get("Wdown"),
+           Wup=inp.get("Wup"), sel_bias=inp.get("sel_bias"), Ws1=inp.get("Ws1"), Ws2=inp.get("Ws2"))
+
+    t_layer = settle_and_time(step, args.other_steps, args.warmup, args.settle_seconds, stream)
+    out = lf.out
+    reps = args.stage_reps
+    h2 = torch.empty_like(out["h"])
+    yd2 = torch.empty_like(out["y_disp"])
+    if s.score == "softmax" and not s.H:
+        ws_router = torch.empty(max(1, _lib.moe_router_logits_workspace_bytes(s.D, s.E)), dtype=torch.uint8,
+                                device=dev)
+        ws_route = torch.empty(max(1, _lib.moe_route_workspace_bytes(s.S, s.E, s.K)), dtype=torch.uint8,
+                               device=dev)
+        r_bufs = {k: torch.empty_like(out[k]) for k in ("topk_idx", "topk_prob", "counts", "offsets",
+                                                          "perm", "inv_perm")}
+        xd2 = torch.empty_like(out["x_disp"])
+        pd2 = torch.empty_like(out["p_disp"])
+        t_up, t_down = time_layer_gemms(_lib, sets, out, s, reps, stream, ws_router, ws_route, r_bufs, xd2, pd2,
+                                        h2, yd2)
+    else:
+        sched = layer.grouped_schedule(out["offsets"], s.E, s.R)
+        t_up = time_region(lambda i: _lib.moe_grouped_gemm(out["x_disp"], sched, s.E, s.R, s.D, s.F,
+                                                           sets[i % len(sets)]["W1"], 1, h2, None), reps, stream)
+        t_down = time_region(lambda i: _lib.moe_grouped_gemm(out["h"], sched, s.E, s.R, s.F, s.D,
+                                                             sets[i % len(sets)]["W2"], 0, yd2, None), reps, stream)
+    fl = 2.0 * s.R * s.D * s.F
+    dom, t_dom = ("grouped_up", t_up) if t_up >= t_down else ("grouped_down", t_down)
+    rec = {"value": round(s.R / t_layer, 1), "unit": "slots/s", "ms_per_step": round(t_layer * 1e3, 4),
+           "steps": args.other_steps,
+           "grouped_up_us": round(t_up * 1e6, 1), "grouped_down_us": round(t_down * 1e6, 1),
+           "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(fl / t_dom / 1e12, 1),
+                        "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                        "frac": round(fl / t_dom / 1e12 / PEAK_BF16_TFLOPS, 4)}}
+    del sets, lf, out, h2, yd2
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return rec
 
 
 def main():
@@ -410,20 +561,8 @@ def main():
         lf(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"], Wdown=inp.get("Wdown"),
            Wup=inp.get("Wup"), sel_bias=inp.get("sel_bias"), Ws1=inp.get("Ws1"), Ws2=inp.get("Ws2"))
 
-    # A GPU that has just started work runs its first tens of steps ~10%
-    # slower (measured: 0.642 ms per step after 5 warm-up steps, 0.579 ms
-    # after 100); a training or serving loop runs at the sustained rate.
     log(f"settle {args.settle_seconds} s, warmup {args.warmup}, timed {args.steps}")
-    t_end, i = time.perf_counter() + args.settle_seconds, 0
-    while time.perf_counter() < t_end:
-        step(i)
-        i += 1
-        if i % 8 == 0:
-            torch.cuda.synchronize()
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    t_layer = time_region(step, args.steps, stream)
+    t_layer = settle_and_time(step, args.steps, args.warmup, args.settle_seconds, stream)
     slots = s.S * s.K
     value = slots / t_layer
     # the same steps once more, each with its own events, for the paper's
@@ -435,48 +574,52 @@ def main():
     out = lf.out
     reps = args.stage_reps
     st = {}
+    # an untimed write of more bytes than the 256 MB last-level cache holds,
+    # enqueued before each timed launch of an HBM-bound stage
+    fbuf = torch.empty(max(1, args.flush_bytes), dtype=torch.uint8, device=dev)
+    flush = lambda: fbuf.fill_(0)  # noqa: E731
     ws_router = torch.empty(max(1, _lib.moe_router_logits_workspace_bytes(s.D, s.E)), dtype=torch.uint8,
                             device=dev)
-    st["router_logits"] = time_region(
+    st["router_logits"] = time_flushed(
         lambda i: _lib.moe_router_logits(sets[i % len(sets)]["x"] if not s.H else out["x_lat"],
                                          sets[i % len(sets)]["Wr"], sets[i % len(sets)]["bias"],
-                                         s.S, s.D, s.E, out["logits"], ws_router), reps, stream)
+                                         s.S, s.D, s.E, out["logits"], ws_router), reps, stream, flush)
     ws_route = torch.empty(max(1, _lib.moe_route_workspace_bytes(s.S, s.E, s.K)), dtype=torch.uint8,
                            device=dev)
     r_bufs = {k: torch.empty_like(out[k]) for k in ("topk_idx", "topk_prob", "counts", "offsets",
                                                       "perm", "inv_perm")}
     if prod:
-        st["route"] = time_region(
+        st["route"] = time_flushed(
             lambda i: _lib.moe_route_sigmoid(out["logits"], sets[i % len(sets)]["sel_bias"], s.S, s.E, s.K,
                                              r_bufs["topk_idx"], r_bufs["topk_prob"], r_bufs["counts"],
                                              r_bufs["offsets"], r_bufs["perm"], r_bufs["inv_perm"], ws_route),
-            reps, stream)
+            reps, stream, flush)
     else:
-        st["route"] = time_region(
+        st["route"] = time_flushed(
             lambda i: _lib.moe_route_topk(out["logits"], s.S, s.E, s.K, r_bufs["topk_idx"],
                                           r_bufs["topk_prob"], r_bufs["counts"], r_bufs["offsets"],
-                                          r_bufs["perm"], r_bufs["inv_perm"], ws_route), reps, stream)
+                                          r_bufs["perm"], r_bufs["inv_perm"], ws_route), reps, stream, flush)
     if s.seq_len:
         ws_aux = torch.empty(max(1, _lib.moe_seq_aux_loss_workspace_bytes(s.S, s.E, s.seq_len)),
                              dtype=torch.uint8, device=dev)
         loss2 = torch.empty(1, dtype=torch.float32, device=dev)
         cnt2 = torch.empty((s.S // s.seq_len, s.E), dtype=torch.int32, device=dev)
-        st["seq_aux_loss"] = time_region(
+        st["seq_aux_loss"] = time_flushed(
             lambda i: _lib.moe_seq_aux_loss(out["logits"], out["topk_idx"], s.S, s.E, s.K, s.seq_len, s.aux_coeff,
-                                            loss2, cnt2, ws_aux), reps, stream)
+                                            loss2, cnt2, ws_aux), reps, stream, flush)
     xd2 = torch.empty((s.R, s.D), dtype=torch.bfloat16, device=dev)
     pd2 = torch.empty_like(out["p_disp"])
     x_r = [(st_["x"] if not s.H else out["x_lat"]) for st_ in sets]
-    st["dispatch"] = time_region(
+    st["dispatch"] = time_flushed(
         lambda i: _lib.moe_dispatch(x_r[i % len(x_r)], out["topk_prob"], out["inv_perm"], s.S, s.D,
-                                    s.K, xd2, pd2), reps, stream)
+                                    s.K, xd2, pd2), reps, stream, flush)
     if s.D % 32 == 0:
         xq2 = torch.empty((s.R, s.D), dtype=torch.uint8, device=dev)
         xs2 = layer.mx_scales(s.R, s.D, dev)
-        st["dispatch_mxfp8"] = time_region(
+        st["dispatch_mxfp8"] = time_flushed(
             lambda i: _lib.moe_dispatch_mxfp8(x_r[i % len(x_r)], out["topk_prob"], out["inv_perm"], s.S, s.D, s.K,
-                                              xq2, xs2, pd2), reps, stream)
-        st["mxfp8_dequant"] = time_region(lambda i: _lib.moe_mxfp8_dequant(xq2, xs2, s.R, s.D, xd2), reps, stream)
+                                              xq2, xs2, pd2), reps, stream, flush)
+        st["mxfp8_dequant"] = time_flushed(lambda i: _lib.moe_mxfp8_dequant(xq2, xs2, s.R, s.D, xd2), reps, stream, flush)
     sched = layer.grouped_schedule(out["offsets"], s.E, s.R)
     h2 = torch.empty_like(out["h"])
     if s.D % 32 == 0:
@@ -512,13 +655,13 @@ def main():
             lambda i: _lib.moe_shared_expert_fwd(sets[i % len(sets)]["x"], sets[i % len(sets)]["Ws1"],
                                                  sets[i % len(sets)]["Ws2"], s.S, s.D, s.Fs, hs2, None, ys2),
             reps, stream)
-        st["combine"] = time_region(
+        st["combine"] = time_flushed(
             lambda i: _lib.moe_combine_add(out["y_disp"], out["p_disp"], out["inv_perm"], out["y_s"], s.S, s.D,
-                                           s.K, y2), reps, stream)
+                                           s.K, y2), reps, stream, flush)
     else:
-        st["combine"] = time_region(
+        st["combine"] = time_flushed(
             lambda i: _lib.moe_combine(out["y_disp"], out["p_disp"], out["inv_perm"], s.S, s.D, s.K, y2),
-            reps, stream)
+            reps, stream, flush)
     if s.H:
         st["latent_down"] = time_region(
             lambda i: _lib.moe_latent_proj(sets[i % len(sets)]["x"], sets[i % len(sets)]["Wdown"],
@@ -539,9 +682,9 @@ def main():
         dx = torch.empty((s.S, s.D), dtype=torch.bfloat16, device=dev)
         ws_bwd = torch.empty(max(1, _lib.moe_grouped_ffn_bwd_workspace_bytes(s.E, s.R, s.D, s.F)),
                              dtype=torch.uint8, device=dev)
-        st["combine_bwd"] = time_region(
+        st["combine_bwd"] = time_flushed(
             lambda i: _lib.moe_combine_bwd(dy, ob["y_disp"], ob["p_disp"], ob["inv_perm"], s.S, s.D, s.K,
-                                           dy_disp, dp), reps, stream)
+                                           dy_disp, dp), reps, stream, flush)
         st["grouped_ffn_bwd"] = time_region(
             lambda i: _lib.moe_grouped_ffn_bwd(ob["x_disp"], ob["u_save"], ob["h"], dy_disp, ob["offsets"],
                                                s.E, s.R, s.D, s.F, sets[0]["W1"], sets[0]["W2"], dx_disp,
@@ -573,8 +716,8 @@ def main():
                 lambda i: _lib.moe_shared_expert_bwd(i0["x"], ob["u_s"], ob["h_s"], dy, i0["Ws1"], i0["Ws2"], s.S,
                                                      s.D, s.Fs, dx_r, True, dWs1, dWs2, ws_sb),
                 max(2, reps // 4), stream)
-        st["dispatch_bwd"] = time_region(
-            lambda i: _lib.moe_dispatch_bwd(dx_disp, ob["inv_perm"], dx_r, s.S, s.D, s.K, dx), reps, stream)
+        st["dispatch_bwd"] = time_flushed(
+            lambda i: _lib.moe_dispatch_bwd_add(dx_disp, ob["inv_perm"], dx_r, s.S, s.D, s.K, dx), reps, stream, flush)
         del lb, ob, dy_disp, dx_disp, dW1, dW2, ws_bwd
 
     bytes_ = stage_bytes(s)
@@ -623,6 +766,16 @@ def main():
         log(f"cpu baseline: oracle on {args.cpu_tokens or s.S} tokens")
         cpu = cpu_baseline(s, sets[0], args.cpu_tokens, args.payload)
 
+    # the other full-size workloads, after the headline's buffers are freed
+    route_sw = route_sweep(_lib, s, reps, stream, dev) if args.route_sweep else None
+    ep = ep_share(_lib, s, args.ep_share, reps, stream, dev) if args.ep_share > 1 else None
+    del sets, lf, out, fbuf
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    others = {}
+    for name in [n for n in args.others.split(",") if n and n != s.name]:
+        others[name] = other_workload(name, args, dev, stream)
+
     rec = {
         "metric": METRIC, "value": round(value, 1), "unit": "slots/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t_layer * 1e3, 4),
@@ -634,8 +787,9 @@ def main():
                    **({"score": s.score, "Fs": s.Fs, "seq_len": s.seq_len, "aux_coeff": s.aux_coeff}
                       if prod else {})},
         "roofline": roofline, "stages": stages, "cpu_baseline": cpu,
-        **({"ep_share": ep_share(_lib, s, args.ep_share, reps, stream, dev)} if args.ep_share > 1 else {}),
-        **({"route_sweep": route_sweep(_lib, s, reps, stream, dev)} if args.route_sweep else {}),
+        **({"ep_share": ep} if ep is not None else {}),
+        **({"route_sweep": route_sw} if route_sw is not None else {}),
+        **({"other_workloads": others} if others else {}),
         "layer_step_us": {"n": len(per_step), "median": round(statistics.median(per_step), 2),
                           "filtered_mean": round(filtered_mean(per_step), 2),
                           "min": round(min(per_step), 2), "max": round(max(per_step), 2)},

@@ -118,3 +118,78 @@ def takes_tall_tiles(counts, N, cus):
     r_small = cdiv(cdiv(m_small, 8) * nt, G // 8)
     r_tall = cdiv(cdiv(m_tall, 8) * nt, G // 8)
     return 2 * r_tall * 91 < 100 * r_small
+
+
+def tie_candidates(scores: np.ndarray, K: int, tau: float, cap: int = 5040):
+    """Every slot-ordered top-K selection that reordering experts whose sorted
+    scores lie within 2*tau of their neighbours can give, from the oracle's
+    scores of one token: the experts sorted by (score desc, index asc) are cut
+    into runs of adjacent gaps <= 2*tau; each run covering the first K
+    positions is permuted freely and the first K experts kept.  A superset of
+    the selections a perturbation of every score by tau could produce (each
+    is then held to the pairwise 2*tau rule as well).  None if there are more
+    than ``cap`` orderings."""
+    import itertools
+    import math
+    s = np.where(np.isnan(scores), -np.inf, np.asarray(scores, np.float64))
+    order = np.lexsort((np.arange(s.size), -s))
+    runs, cur = [], [int(order[0])]
+    for a, b in zip(order[:-1], order[1:]):
+        close = s[a] == s[b] or abs(s[a] - s[b]) <= 2 * tau
+        if close:
+            cur.append(int(b))
+        else:
+            runs.append(cur)
+            cur = [int(b)]
+    runs.append(cur)
+    need, n = [], 0
+    for r in runs:
+        need.append(r)
+        n += len(r)
+        if n >= K:
+            break
+    if math.prod(math.factorial(len(r)) for r in need) > cap:
+        return None
+    out = set()
+    for combo in itertools.product(*[itertools.permutations(r) for r in need]):
+        out.add(tuple(e for r in combo for e in r)[:K])
+    return out
+
+
+def check_tie_choice(scores: np.ndarray, chosen, K: int, tau: float):
+    """The GPU's slot-ordered choice for a near-tie token is one of the
+    oracle's candidate selections and obeys the 2*tau rule pairwise: every
+    slot's score is at least every later slot's minus 2*tau, and every chosen
+    score at least every unchosen one's minus 2*tau."""
+    chosen = [int(e) for e in chosen]
+    assert len(set(chosen)) == K
+    s = np.asarray(scores, np.float64)
+    cands = tie_candidates(s, K, tau)
+    if cands is not None:
+        assert tuple(chosen) in cands, (chosen, sorted(cands)[:4])
+    cs = s[chosen]
+    for i in range(K):
+        for j in range(i + 1, K):
+            assert cs[i] >= cs[j] - 2 * tau, ("slot order", chosen)
+    rest = np.delete(s, chosen)
+    if rest.size:
+        assert cs.min() >= rest.max() - 2 * tau, ("selection", chosen)
+
+
+def guarded(shape, dtype, device, guard: int = 2):
+    """A NaN-filled buffer with `guard` extra rows (leading-dimension slices)
+    before and after; returns (buffer, interior view).  A kernel that writes
+    every element of the interior and nothing outside it leaves the guards
+    all NaN and the interior free of NaN."""
+    shape = tuple(shape)
+    buf = torch.full((shape[0] + 2 * guard,) + shape[1:], float("nan"), dtype=dtype, device=device)
+    return buf, buf[guard:guard + shape[0]]
+
+
+def check_guarded(buf: torch.Tensor, guard: int, what: str):
+    n = buf.shape[0] - 2 * guard
+    assert bool(torch.isnan(buf[:guard]).all()) and bool(torch.isnan(buf[guard + n:]).all()), \
+        f"{what}: a guard row was written"
+    inner = buf[guard:guard + n]
+    bad = int(torch.isnan(inner).sum())
+    assert bad == 0, f"{what}: {bad} elements left unwritten (still NaN)"

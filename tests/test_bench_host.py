@@ -24,3 +24,14 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_cpu_baseline_reports_stages_and_host():
+    """The CPU leg on the tiny workload: one pass of the oracle's stages, each
+    timed, with the host's core count and CPU model."""
+    from paper_2608_28511_amd.workloads import TINY, make_inputs
+    rec = bench.cpu_baseline(TINY, make_inputs(TINY), 0, min_seconds=0.0, max_runs=1)
+    assert rec["kind"] == "oracle" and rec["unit"] == "slots/s" and rec["value"] > 0
+    assert rec["nproc"] >= 1 and isinstance(rec["cpu_model"], str)
+    assert set(rec["stage_seconds_per_pass"]) == {"router_logits", "route", "permutation", "dispatch",
+                                                  "expert_ffn", "combine"}

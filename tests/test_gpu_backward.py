@@ -140,56 +140,69 @@ def check_backward_case(S, D, E, K, F, seed):
     assert torch.all(G["dW1"][E - 1] == 0) and torch.all(G["dW2"][E - 1] == 0)
 
 
-def test_backward_full_size_sampled():
-    """Zipf-skewed 16384-token workload: dx / dp on sampled tokens, dW on the
-    busiest, a median and a dead expert, against the oracle."""
+def test_backward_full_size():
+    """Zipf-skewed 16384-token workload, every output against the oracle: dx
+    and dp of every token, dW1 and dW2 of every live expert within their
+    elementwise bounds, exactly zero dW for the dead experts.  The gradients
+    are written into NaN-filled buffers with guard rows (guard experts for
+    dW), so an unwritten element or a stray write shows, and the whole
+    backward runs twice and must reproduce itself bit for bit."""
+    from paper_2608_28511_amd import _lib as L
+    from gpu_helpers import check_guarded, guarded
+
     s = WORKLOADS["skew_s16384_d2048_e128_k8_bwd"]
+    S, D, E, K, F, R = s.S, s.D, s.E, s.K, s.F, s.R
     inp = make_inputs(s, device=DEV)
-    logits = torch.randn((s.S, s.E), device=DEV,
+    logits = torch.randn((S, E), device=DEV,
                          generator=torch.Generator(device=DEV).manual_seed(2)) + inp["bias"][None, :]
-    G = gpu_chain(inp["x"], logits, inp["W1"], inp["W2"], inp["dy"], s.K)
+    r = layer.route(logits, K)
+    x_disp, p_disp = layer.dispatch(inp["x"], r["topk_prob"], r["inv_perm"], K)
+    h, u, yd = layer.grouped_ffn(x_disp, r["offsets"], inp["W1"], inp["W2"], save_u=True)
+    ws = torch.empty(L.moe_grouped_ffn_bwd_workspace_bytes(E, R, D, F), dtype=torch.uint8, device=DEV)
+    G = 2
+
+    def backward():
+        b = {}
+        b["dyd"], dyd = guarded((R, D), torch.bfloat16, DEV, G)
+        b["dp"], dp = guarded((S, K), torch.float32, DEV, G)
+        b["dxd"], dxd = guarded((R, D), torch.bfloat16, DEV, G)
+        b["dW1"], dW1 = guarded((E, D, F), torch.float32, DEV, G)
+        b["dW2"], dW2 = guarded((E, F, D), torch.float32, DEV, G)
+        b["dx"], dx = guarded((S, D), torch.bfloat16, DEV, G)
+        L.moe_combine_bwd(inp["dy"], yd, p_disp, r["inv_perm"], S, D, K, dyd, dp)
+        L.moe_grouped_ffn_bwd(x_disp, u, h, dyd, r["offsets"], E, R, D, F, inp["W1"], inp["W2"], dxd, dW1, dW2, ws)
+        L.moe_dispatch_bwd(dxd, r["inv_perm"], S, D, K, dx)
+        torch.cuda.synchronize()
+        for k, buf in b.items():
+            check_guarded(buf, G, f"backward {k}")
+        return {k: v[G:-G] for k, v in b.items()}
+
+    got = backward()
+    again = backward()
+    for k in got:
+        assert torch.equal(got[k], again[k]), f"{k} differs between two identical calls"
+    del again
+
     lg = logits.cpu().numpy()
-    idx, p = O.route(lg, s.K)
-    counts = np.bincount(idx.ravel(), minlength=s.E)
-    assert np.array_equal(npi(G["r"]["counts"]), counts)
-    W1, W2 = LazyExperts(inp["W1"]), LazyExperts(inp["W2"])
-    x = np64(inp["x"])
-    dy = np64(inp["dy"])
-    # sampled tokens: every per-row quantity of the backward
-    tok = np.sort(np.random.default_rng(5).choice(s.S, 24, replace=False))
-    sub_idx, sub_p = idx[tok], p[tok]
-    _, off, perm, inv = O.expert_permutation(sub_idx, s.E)
-    xd, pd = O.dispatch(x[tok], sub_p, inv, s.K)
-    u, h, yd = O.expert_ffn(xd, off, W1, W2, round_payload=False)
-    dyd, dp = O.combine_bwd(dy[tok], yd, pd, inv, s.K, round_payload=False)
-    dxd, _, _, _ = O.expert_ffn_bwd(xd, u, h, dyd, off, W1, W2, round_payload=False)
-    dx = O.dispatch_bwd(dxd, inv, len(tok), s.K)
-    b_dxd = np.zeros_like(dxd)
-    for e in range(s.E):
+    W1, W2 = LazyExperts(inp["W1"], cache=True), LazyExperts(inp["W2"], cache=True)
+    R_ = oracle_chain(np64(inp["x"]), lg, W1, W2, np64(inp["dy"]), K, E)
+    counts = R_["counts"]
+    assert np.array_equal(npi(r["counts"]), counts)
+    assert np.array_equal(npi(r["inv_perm"]), R_["inv"])
+    assert_grad_close(np64(got["dp"]), R_["dp"], "dp")
+    off = R_["off"]
+    b_dxd = np.zeros_like(R_["dxd"])
+    live = 0
+    for e in range(E):
         a, b = int(off[e]), int(off[e + 1])
-        if a < b:
-            b_dxd[a:b] = bwd_bounds(xd[a:b], u[a:b], h[a:b], dyd[a:b], dxd[a:b], W1[e], W2[e])[2]
-    b_dx = O.dispatch_bwd(b_dxd, inv, len(tok), s.K) + EPS_BF16 * np.abs(dx)
-    sel = torch.as_tensor(tok, device=DEV)
-    assert_within(np64(G["dx"][sel]), dx, b_dx, "dx sampled")
-    assert_grad_close(np64(G["dp"][sel]), dp, "dp sampled")
-    # sampled experts: busiest, median, dead
-    order = np.argsort(-counts, kind="stable")
-    dead = np.nonzero(counts == 0)[0]
-    assert dead.size >= 4
-    for e in (int(order[0]), int(order[len(order) // 2])):
-        t_e, k_e = np.nonzero(idx == e)
-        p_e = p[t_e, k_e].reshape(-1, 1)
-        n = len(t_e)
-        off1 = np.array([0, n])
-        inv1 = np.arange(n)
-        xd1, pd1 = O.dispatch(x[t_e], p_e, inv1, 1)
-        w1, w2 = [W1[e]], [W2[e]]
-        u1, h1, yd1 = O.expert_ffn(xd1, off1, w1, w2, round_payload=False)
-        dyd1, _ = O.combine_bwd(dy[t_e], yd1, pd1, inv1, 1, round_payload=False)
-        _, dW1, dW2, _ = O.expert_ffn_bwd(xd1, u1, h1, dyd1, off1, w1, w2, round_payload=False)
-        b1, b2, _ = bwd_bounds(xd1, u1, h1, dyd1, np.zeros_like(xd1), w1[0], w2[0])
-        assert_within(np64(G["dW1"][e]), dW1[0], b1, f"dW1[{e}] ({n} rows)")
-        assert_within(np64(G["dW2"][e]), dW2[0], b2, f"dW2[{e}] ({n} rows)")
-    for e in dead[:2]:
-        assert torch.all(G["dW1"][int(e)] == 0) and torch.all(G["dW2"][int(e)] == 0)
+        if a == b:
+            assert torch.all(got["dW1"][e] == 0) and torch.all(got["dW2"][e] == 0), f"dead expert {e}"
+            continue
+        live += 1
+        b1, b2, b_dxd[a:b] = bwd_bounds(R_["xd"][a:b], R_["u"][a:b], R_["h"][a:b], R_["dyd"][a:b],
+                                        R_["dxd"][a:b], W1[e], W2[e])
+        assert_within(np64(got["dW1"][e]), R_["dW1"][e], b1, f"dW1[{e}] ({b - a} rows)")
+        assert_within(np64(got["dW2"][e]), R_["dW2"][e], b2, f"dW2[{e}] ({b - a} rows)")
+    assert live == E - int((counts == 0).sum()) and (counts == 0).sum() >= 4
+    b_dx = O.dispatch_bwd(b_dxd, R_["inv"], S, K) + EPS_BF16 * np.abs(R_["dx"])
+    assert_within(np64(got["dx"]), R_["dx"], b_dx, "dx")
