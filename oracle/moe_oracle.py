@@ -252,7 +252,7 @@ def _expert(W, e) -> np.ndarray:
     return np.asarray(W[e], dtype=np.float64)
 
 
-def expert_ffn(x_disp, offsets, W1, W2, round_payload: bool = True):
+def expert_ffn(x_disp, offsets, W1, W2, round_payload: bool = True, round_hidden: bool = False):
     """Ungated per-expert FFN over each expert's contiguous segment
     (Section 5.2: grouped GEMM over expert segments; the activation is
     squared-ReLU for this workload since the paper does not state one).
@@ -262,7 +262,10 @@ def expert_ffn(x_disp, offsets, W1, W2, round_payload: bool = True):
         h[r] = max(u[r], 0)**2
         y_disp[r] = h[r] @ W2[e]          W2[e]: [F, D]
     y_disp is the combine payload and is rounded to bf16 (b_x) unless
-    round_payload is False.  W1/W2 may be any object indexable by expert.
+    round_payload is False.  With round_hidden the hidden activation h is
+    rounded to bf16 before the down projection reads it (the paper trains in
+    BF16, Section 5.2: h is a stored bf16 activation tensor); the returned h
+    is then the rounded one.  W1/W2 may be any object indexable by expert.
     Returns (u, h, y_disp) as float64.
     """
     x_disp = np.asarray(x_disp, np.float64)
@@ -284,6 +287,8 @@ def expert_ffn(x_disp, offsets, W1, W2, round_payload: bool = True):
             y = np.zeros((R, w2.shape[1]))
         u[a:b] = x_disp[a:b] @ w1
         h[a:b] = np.maximum(u[a:b], 0.0) ** 2
+        if round_hidden:
+            h[a:b] = round_bf16(h[a:b])
         y[a:b] = h[a:b] @ w2
     if F is None:  # no routed rows at all
         F = _expert(W1, 0).shape[1] if E else 0
@@ -326,6 +331,7 @@ def latent_up(y_lat, Wup) -> np.ndarray:
 
 def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
               logits=None, round_payload: bool = True, round_latent: bool = True,
+              round_activations: bool = False,
               score: str = "softmax", sel_bias=None, Ws1=None, Ws2=None,
               seq_len: Optional[int] = None, aux_coeff: float = 0.0, payload: str = "bf16") -> dict:
     """One routed MoE layer forward, in the paper's order (Section 4.1
@@ -336,7 +342,12 @@ def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
     If ``logits`` is given, routing uses those fp32 scores instead of the
     ones computed here.  ``round_latent`` rounds the projected activations
     (the dispatched, routed input) to bf16; ``round_payload`` rounds the
-    expert outputs sent back for the combine.
+    expert outputs sent back for the combine.  ``round_activations`` also
+    rounds to bf16 the activation tensors a BF16-trained layer stores between
+    its products (the paper trains with BF16 precision, Section 5.2): each
+    expert's hidden activation h before its down projection, and with a
+    latent projection the combined latent output y_lat before the up
+    projection.
 
     The production variant of Section 5.2: ``score="sigmoid"`` routes with
     sigmoid_route (``sel_bias`` steering selection only); ``Ws1``/``Ws2`` add
@@ -372,11 +383,13 @@ def layer_fwd(x, Wr, W1, W2, K: int, bias=None, Wdown=None, Wup=None,
         x_disp, p_disp = dispatch(x_r, prob, inv_perm, K)
     else:
         raise ValueError("payload is 'bf16' or 'mxfp8'")
-    u, h, y_disp = expert_ffn(x_disp, offsets, W1, W2, round_payload)
+    u, h, y_disp = expert_ffn(x_disp, offsets, W1, W2, round_payload, round_hidden=round_activations)
     y = combine(y_disp, p_disp, inv_perm, S, K)
     out.update(topk_idx=idx, topk_prob=prob, counts=counts, offsets=offsets, perm=perm,
                inv_perm=inv_perm, x_disp=x_disp, p_disp=p_disp, u=u, h=h, y_disp=y_disp)
     if Wup is not None:
+        if round_activations:
+            y = round_bf16(y)
         out["y_lat"] = y
         y = latent_up(y, Wup)
     if Ws1 is not None:

@@ -11,8 +11,11 @@ output are checked against the oracle's evaluation of that selection.
 Counts, offsets, perm and inv_perm are checked through the properties that
 determine them uniquely from the GPU's own top-K.  The expert activations h,
 the expert outputs y_disp (every routed row) and the layer output y (every
-token) are compared with the oracle; they are written into NaN-filled
-buffers with guard rows, so an unwritten element or a stray write shows.
+token) are compared with the oracle in the paper's training precision
+(BF16, Section 5.2: the stored activations h, y_disp and the latent combine
+output rounded to bf16, every sum in float64); they are written into
+NaN-filled buffers with guard rows, so an unwritten element or a stray write
+shows.
 Each full-size layer runs twice and must reproduce itself bit for bit.
 """
 import numpy as np
@@ -85,9 +88,10 @@ def check_layer(s, inp, out):
     assert np.all(np.abs(logits_gpu[fin] - logits_ref[fin]) <= tau[fin]), "logits"
     tau_t = np.where(fin, tau, 0).max(axis=1)
 
-    # the oracle's whole layer from its own logits and routing
+    # the oracle's whole layer from its own logits and routing, with the
+    # activations a BF16-trained layer stores rounded to bf16
     ref = O.layer_fwd(x, Wr, LazyExperts(inp["W1"]), LazyExperts(inp["W2"]), K, bias=bias, Wdown=Wd, Wup=Wu,
-                      round_payload=False)
+                      round_payload=True, round_activations=True)
     idx_ref, p_ref = ref["topk_idx"], ref["topk_prob"]
     assert np.array_equal(ref["logits"].astype(np.float64), logits_ref)
     idx_gpu = npi(out["topk_idx"])
@@ -133,10 +137,10 @@ def check_layer(s, inp, out):
         _, off_c, _, inv_c = O.expert_permutation(sel, E)
         xd_c, pd_c = O.dispatch(xr_ref[tie], p_c, inv_c, K)
         _, h_c, yd_c = O.expert_ffn(xd_c, off_c, LazyExperts(inp["W1"]), LazyExperts(inp["W2"]),
-                                    round_payload=False)
+                                    round_payload=True, round_hidden=True)
         y_c = O.combine(yd_c, pd_c, inv_c, tie.size, K)
         if s.H:
-            y_c = O.latent_up(y_c, Wu)
+            y_c = O.latent_up(O.round_bf16(y_c), Wu)
         pos_g = inv_g[tie].reshape(-1)
         assert_bf16_close(_rows(out["h"], pos_g), h_c[inv_c], f"{s.name} h (near ties)")
         assert_bf16_close(_rows(out["y_disp"], pos_g), yd_c[inv_c], f"{s.name} y_disp (near ties)")

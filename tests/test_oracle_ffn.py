@@ -80,6 +80,39 @@ def test_expert_ffn_rounds_only_the_payload():
     assert np.array_equal(y1, O.round_bf16(y0)) and not np.array_equal(y0, y1)
 
 
+def test_expert_ffn_rounds_the_hidden_activation_on_request():
+    """Hand-worked: u = 1 + 2^-5 gives h = 1 + 2^-4 + 2^-10, which bf16 (7
+    fraction bits) rounds to 1 + 2^-4; with W2 = 1 the expert output is
+    exactly that rounded h with round_hidden, and the unrounded h without."""
+    xd = np.array([[1.0, 2.0 ** -5]])
+    W1 = np.array([[[1.0], [1.0]]])
+    W2 = np.array([[[1.0, 0.0]]])
+    off = np.array([0, 1])
+    _, h, y = O.expert_ffn(xd, off, W1, W2, round_payload=False, round_hidden=True)
+    assert h[0, 0] == 1 + 2.0 ** -4 and y[0, 0] == 1 + 2.0 ** -4
+    _, h, y = O.expert_ffn(xd, off, W1, W2, round_payload=False)
+    assert h[0, 0] == 1 + 2.0 ** -4 + 2.0 ** -10 and y[0, 0] == h[0, 0]
+
+
+def test_layer_fwd_bf16_activations_round_the_latent_combine():
+    """Hand-worked latent layer: two experts share a token with equal logits
+    (p = 1/2 each), their outputs are 1 and 1 + 2^-7, so the combined latent
+    value is 1 + 2^-8, exactly half a bf16 step above 1: with BF16
+    activations it rounds to even (1) before the identity up projection;
+    without, it passes through."""
+    x = np.array([[1.0, 2.0 ** -7]])
+    I2 = np.eye(2)
+    Wr = np.zeros((2, 2))
+    W1 = np.array([[[1.0], [0.0]], [[1.0], [0.0]]])
+    W2 = np.array([[[1.0, 0.0]], [[1.0 + 2.0 ** -7, 0.0]]])
+    kw = dict(Wdown=I2, Wup=I2)
+    out = O.layer_fwd(x, Wr, W1, W2, 2, round_payload=True, round_activations=True, **kw)
+    assert np.array_equal(out["topk_prob"], np.array([[0.5, 0.5]], np.float32))
+    assert out["y_lat"][0, 0] == 1.0 and out["y"][0, 0] == 1.0
+    out = O.layer_fwd(x, Wr, W1, W2, 2, round_payload=True, **kw)
+    assert out["y"][0, 0] == 1.0 + 2.0 ** -8
+
+
 def test_expert_ffn_empty_experts():
     idx = np.array([[1], [1], [3]])
     _, offsets, perm, inv = O.expert_permutation(idx, 5)

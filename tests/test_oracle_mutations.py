@@ -52,6 +52,12 @@ MUTATIONS = [
     ('bf16_trunc',
      'r = np.rint(v / ulp) * ulp',
      'r = np.trunc(v / ulp) * ulp'),
+    ('hidden_not_rounded',
+     '            h[a:b] = round_bf16(h[a:b])',
+     '            h[a:b] = h[a:b]'),
+    ('latent_combine_not_rounded',
+     '        if round_activations:\n            y = round_bf16(y)',
+     '        if round_activations:\n            y = y'),
     ('bias_ignored',
      'z = z + np.asarray(bias, np.float64)[None, :]',
      'z = z'),
