@@ -165,6 +165,25 @@ int moe_grouped_ffn(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, i
                     moe_bf16* h, moe_bf16* u_save, moe_bf16* y_disp,
                     void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* moe_grouped_ffn without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The call allocates nothing: its only
+ * scratch, the grouped GEMM's tile schedule, lives in a fixed device array of
+ * MOE_STATIC_SCRATCH_BYTES that the library holds on each GPU it runs on until
+ * the process ends.  Outputs and their meaning are those of moe_grouped_ffn
+ * (the same kernels: the results are bit-identical).
+ * Limit: R < 2^21 rows (with E <= 1024, the schedule then fits the array);
+ * larger R returns MOE_ERR_WORKSPACE before anything is enqueued.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one
+ * GPU (on different streams, or from different threads) race and must be
+ * ordered by the caller.  The array needs no initialisation: each call
+ * rewrites the schedule it reads. */
+#define MOE_STATIC_SCRATCH_BYTES (448 * 1024)
+#define MOE_STATIC_MAX_ROWS ((int64_t)1 << 21)
+int moe_grouped_ffn_static(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, int64_t R, int32_t D,
+                           int32_t F, const moe_bf16* W1, const moe_bf16* W2, moe_bf16* h, moe_bf16* u_save,
+                           moe_bf16* y_disp, hipStream_t stream);
+
 /* The two products of moe_grouped_ffn as separate launches (for callers that
  * schedule or time them individually).
  *

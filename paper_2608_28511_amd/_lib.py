@@ -79,6 +79,7 @@ _PROTOS = {
     "moe_dispatch": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp, vp]),
     "moe_grouped_ffn_workspace_bytes": (sz, [i32, i64, i32, i32]),
     "moe_grouped_ffn": (C.c_int, [vp, vp, i32, i64, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
+    "moe_grouped_ffn_static": (C.c_int, [vp, vp, i32, i64, i32, i32, vp, vp, vp, vp, vp, vp]),
     "moe_grouped_schedule_bytes": (sz, [i32, i64]),
     "moe_grouped_schedule": (C.c_int, [vp, i32, i64, vp, sz, vp]),
     "moe_grouped_gemm": (C.c_int, [vp, vp, i32, i64, i32, i32, vp, i32, vp, vp, vp]),
@@ -217,6 +218,13 @@ def moe_grouped_ffn(x_disp, offsets, E, R, D, F, W1, W2, h, u_save, y_disp, ws):
         _ptr(W1, BF16, "W1"), _ptr(W2, BF16, "W2"), _ptr(h, BF16, "h"),
         _ptr(u_save, BF16, "u_save"), _ptr(y_disp, BF16, "y_disp"), _ptr(ws, None, "ws"),
         0 if ws is None else ws.numel() * ws.element_size(), _stream()), "moe_grouped_ffn")
+
+
+def moe_grouped_ffn_static(x_disp, offsets, E, R, D, F, W1, W2, h, u_save, y_disp):
+    _check(load().moe_grouped_ffn_static(
+        _ptr(x_disp, BF16, "x_disp"), _ptr(offsets, I32, "offsets"), E, R, D, F,
+        _ptr(W1, BF16, "W1"), _ptr(W2, BF16, "W2"), _ptr(h, BF16, "h"),
+        _ptr(u_save, BF16, "u_save"), _ptr(y_disp, BF16, "y_disp"), _stream()), "moe_grouped_ffn_static")
 
 
 def moe_grouped_schedule_bytes(E, R) -> int:

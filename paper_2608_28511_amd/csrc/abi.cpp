@@ -233,6 +233,28 @@ int moe_grouped_ffn(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, i
     return MOE_OK;
 }
 
+static_assert(moe::kStaticScratchBytes == MOE_STATIC_SCRATCH_BYTES, "static scratch size");
+
+int moe_grouped_ffn_static(const moe_bf16* x_disp, const int32_t* offsets, int32_t E, int64_t R, int32_t D,
+                           int32_t F, const moe_bf16* W1, const moe_bf16* W2, moe_bf16* h, moe_bf16* u_save,
+                           moe_bf16* y_disp, hipStream_t stream) {
+    MOE_TRY(check_ffn(x_disp, offsets, E, R, D, F, W1, W2));
+    MOE_TRY(need(h, (uint64_t)R * F * 2, 16));
+    MOE_TRY(opt(u_save, 16));
+    MOE_TRY(need(y_disp, (uint64_t)R * D * 2, 16));
+    if (R >= MOE_STATIC_MAX_ROWS || moe::gemm_schedule_bytes(E, R) > moe::kStaticScratchBytes)
+        return MOE_ERR_WORKSPACE;
+    if (R == 0) return MOE_OK;
+    void* sched = nullptr;
+    MOE_HIP(moe::static_scratch(&sched));
+    MOE_HIP(moe::launch_tile_schedule(offsets, E, R, sched, stream));
+    MOE_HIP(moe::launch_grouped_rows(x_disp, D, W1, F, (int64_t)D * F, false, h, F, moe::EPI_RELU2,
+                                     nullptr, u_save, sched, E, R, F, D, stream));
+    MOE_HIP(moe::launch_grouped_rows(h, F, W2, D, (int64_t)F * D, false, y_disp, D, moe::EPI_BF16,
+                                     nullptr, nullptr, sched, E, R, D, F, stream));
+    return MOE_OK;
+}
+
 size_t moe_grouped_schedule_bytes(int32_t E, int64_t R) {
     if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows) return 0;
     return moe::gemm_schedule_bytes(E, R);

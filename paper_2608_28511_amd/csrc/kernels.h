@@ -77,6 +77,11 @@ hipError_t launch_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const 
                               float* dp, hipStream_t st);
 
 int gemm_tile_m();
+
+// Bytes of the fixed device scratch of the entry point that allocates
+// nothing (its tile schedule), and that array's address on the current device.
+constexpr size_t kStaticScratchBytes = 448 * 1024;
+hipError_t static_scratch(void** ptr);
 // Schedule buffer of the grouped GEMM: mtile_start [E+1] then the per-tile table.
 size_t gemm_schedule_bytes(int E, int64_t R);
 hipError_t launch_tile_schedule(const int32_t* offsets, int E, int64_t R, void* sched, hipStream_t st);

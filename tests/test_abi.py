@@ -183,6 +183,10 @@ def test_validation_errors_return_before_launch(lib):
     assert lib.moe_grouped_ffn_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 1 << 20, 2048, 1024, FAKE, FAKE, FAKE,
                                    FAKE, FAKE, FAKE, 1 << 40, st) == -6
     assert lib.moe_grouped_schedule(FAKE, 4, 100, FAKE, 16, st) == -4
+    # the entry point without a workspace: rows beyond its fixed array are refused on the host
+    assert lib.moe_grouped_ffn_static(FAKE, FAKE, 4, 1 << 21, 16, 16, FAKE, FAKE, FAKE, None, FAKE, st) == -4
+    assert lib.moe_grouped_ffn_static(FAKE, FAKE, 0, 4, 16, 16, FAKE, FAKE, FAKE, None, FAKE, st) == -2
+    assert lib.moe_grouped_ffn_static(FAKE, FAKE, 4, 4, 16, 16, FAKE, FAKE, FAKE, ODD, FAKE, st) == -3
     assert lib.moe_grouped_gemm(FAKE, None, 2, 4, 16, 16, FAKE, 1, FAKE, None, st) == -1
     assert lib.moe_grouped_gemm(FAKE, FAKE, 2, 4, 16, 16, FAKE, 2, FAKE, None, st) == -6
     assert lib.moe_router_logits(FAKE, FAKE, None, 4, 16, 0, FAKE, FAKE, 4096, st) == -2
