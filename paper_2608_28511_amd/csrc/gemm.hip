@@ -415,22 +415,45 @@ struct RowsTile {
     int e, row0, row_hi, n0;  // rows and columns are below 2^31
 };
 
+static_assert(kSchedGroupM == kGroupM, "schedule runs and dense groups take the same m-tiles");
+
 template <int BM>
 __device__ __forceinline__ RowsTile rows_tile(const GemmArgs& p, const int4* tiles, int m_count, int w,
                                               int m_base) {
-    // item w of the m-tiles [m_base, m_base + m_count) x all n-tiles, taken 8
-    // m-tiles at a time across all n-tiles
-    const int width = kGroupM * p.n_tiles;
-    const int group = w / width;
-    const int first_m = group * kGroupM;
-    const int gsz = (m_count - first_m) < kGroupM ? (m_count - first_m) : kGroupM;
-    const int in = w - group * width;
-    const int mt = __builtin_amdgcn_readfirstlane(m_base + first_m + in % gsz);
-    const int nt = in / gsz;
+    typedef const __attribute__((address_space(4))) int32_t* cptr;
+    // item w of the m-tiles [m_base, m_base + m_count) x all n-tiles, taken a
+    // group of m-tiles at a time across all n-tiles: with a tile table the
+    // groups are its runs of one expert's m-tiles (cut at the share's ends),
+    // dense rows take kGroupM m-tiles at a time
+    int mt, nt;
+    if (tiles != nullptr) {
+        // item w lies in the run that holds m-tile m_base + w / n_tiles (a
+        // run of s m-tiles covers s * n_tiles consecutive items); the table
+        // is written by an earlier launch and read-only here: scalar loads
+        // through the constant address space
+        const int q = m_base + w / p.n_tiles;
+        const int packed = ((cptr)(tiles + q))[3];
+        int a = packed >> 4, b = a + (packed & 15);
+        a = a > m_base ? a : m_base;
+        b = b < m_base + m_count ? b : m_base + m_count;
+        if (a > q || b <= q) { a = q; b = q + 1; }   // an entry that does not hold q: take q alone
+        const int s = b - a;
+        const int in = w - (a - m_base) * p.n_tiles;
+        mt = a + in % s;
+        nt = in / s;
+        nt = nt < p.n_tiles ? nt : p.n_tiles - 1;
+    } else {
+        const int width = kGroupM * p.n_tiles;
+        const int group = w / width;
+        const int first_m = group * kGroupM;
+        const int gsz = (m_count - first_m) < kGroupM ? (m_count - first_m) : kGroupM;
+        const int in = w - group * width;
+        mt = m_base + first_m + in % gsz;
+        nt = in / gsz;
+    }
+    mt = __builtin_amdgcn_readfirstlane(mt);
     RowsTile t;
     if (tiles != nullptr) {
-        // the table is written by an earlier launch and read-only here: a
-        // scalar load through the constant address space
         const __attribute__((address_space(4))) int32_t* ti =
             (const __attribute__((address_space(4))) int32_t*)(tiles + mt);
         t.e = ti[0];

@@ -3,8 +3,14 @@
 // For expert segments offsets[0..E] (clamped to [0, R)) and each tile height
 // BM in {128, 256}:
 //   mtile_start[0] = 0, mtile_start[e+1] = min(sum_{e' <= e} ceil(count[e'] / BM), max_tiles)
-//   tiles[mt] = {e, row0, row_end, 0} for every BM-row tile mt of expert e,
-//               {-1, 0, 0, 0} for mt in [total, max_tiles) (the static grid bound).
+//   tiles[mt] = {e, row0, row_end, 16 * g0 + gs} for every BM-row tile mt of
+//               expert e, {-1, 0, 0, 0} for mt in [total, max_tiles) (the
+//               static grid bound).  g0 and gs place mt in its group: an
+//               expert's m-tiles are cut, from its first, into runs of at
+//               most kSchedGroupM; mt's run is [g0, g0 + gs).  The GEMM walks
+//               each run across all n-tiles before the next, so the workgroups
+//               of an XCD that run together share one expert's weight panels
+//               and row tiles in its L2.
 // Routing offsets are monotone, so the tile count never exceeds max_tiles;
 // malformed offsets (segments that overlap after clamping) could ask for
 // more, and the cap keeps every reader of the table inside it.
@@ -21,6 +27,7 @@
 namespace moe {
 
 constexpr int kSchedBM[2] = {128, 256};
+constexpr int kSchedGroupM = 8;   // m-tiles per run of one expert
 
 struct SchedPart {
     int32_t* mtile_start;
@@ -79,9 +86,12 @@ __device__ __forceinline__ void sched_fill_part(const int32_t* seg_lo, const int
                 const int m = (a + b) >> 1;
                 if (cnt[m] > mt) b = m; else a = m + 1;
             }
-            const int row0 = seg_lo[a] + (mt - (a ? cnt[a - 1] : 0)) * BMr;
+            const int first = a ? cnt[a - 1] : 0;
+            const int row0 = seg_lo[a] + (mt - first) * BMr;
             const int row_end = row0 + BMr < seg_hi[a] ? row0 + BMr : seg_hi[a];
-            v = make_int4(a, row0, row_end, 0);
+            const int g0 = first + (mt - first) / kSchedGroupM * kSchedGroupM;
+            const int gs = cnt[a] - g0 < kSchedGroupM ? cnt[a] - g0 : kSchedGroupM;
+            v = make_int4(a, row0, row_end, 16 * g0 + gs);
         }
         sp.tiles[mt] = v;
     }

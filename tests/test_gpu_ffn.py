@@ -143,8 +143,15 @@ def test_grouped_gemm_single_launches_match_ffn(R, D, F, E, empty, skew):
     y2 = layer.grouped_gemm(h2, sched, W2, 0)
     torch.cuda.synchronize()
     counts = np.diff(npi(off))
-    assert np.array_equal(np.diff(npi(sched[: E + 1])), (counts + 127) // 128)
+    ms = npi(sched[: E + 1])
+    assert np.array_equal(np.diff(ms), (counts + 127) // 128)
     assert torch.equal(h, h2) and torch.equal(u, u2) and torch.equal(yd, y2)
+    # each entry's run: the m-tiles of its expert cut into runs of at most 8 from the expert's first
+    t0 = ((E + 1) * 4 + 15) // 16 * 16 // 4      # the table follows mtile_start, 16-byte aligned
+    table = npi(sched[t0: t0 + 4 * int(ms[-1])]).reshape(-1, 4)
+    for mt, (e, r0, r1, packed) in enumerate(table):
+        g0, gs = packed >> 4, packed & 15
+        assert (g0 - ms[e]) % 8 == 0 and g0 <= mt < g0 + gs and gs == min(8, ms[e + 1] - g0), (mt, e, g0, gs)
 
 
 def test_schedule_caps_overlapping_segments():
@@ -159,6 +166,7 @@ def test_schedule_caps_overlapping_segments():
     ms = npi(sched[: E + 1])
     max_tiles = -(-R // 128) + min(R, E)
     assert ms[0] == 0 and np.all(np.diff(ms) >= 0) and ms[-1] == max_tiles
-    table = npi(sched[4: 4 + 4 * max_tiles]).reshape(max_tiles, 4)   # 16-byte entries after mtile_start
+    t0 = ((E + 1) * 4 + 15) // 16 * 16 // 4      # the table follows mtile_start, 16-byte aligned
+    table = npi(sched[t0: t0 + 4 * max_tiles]).reshape(max_tiles, 4)
     assert np.all((table[:, 0] >= 0) & (table[:, 0] < E))
     assert np.all((table[:, 1] >= 0) & (table[:, 1] < table[:, 2]) & (table[:, 2] <= R))
