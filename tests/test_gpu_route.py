@@ -38,8 +38,10 @@ def _route_and_compare(logits_cpu: torch.Tensor, K: int, probs: bool = True):
     return out
 
 
+# one to sixteen experts per lane of the top-K kernel (E up to 1024), partial
+# last token blocks, K = 1 with many token blocks
 SHAPES = [(1, 1, 1), (31, 8, 2), (33, 8, 8), (512, 8, 2), (1000, 64, 6), (777, 256, 8),
-          (300, 1024, 32), (2049, 37, 5), (64, 128, 1), (95, 65, 3)]
+          (300, 1024, 32), (2049, 37, 5), (64, 128, 1), (95, 65, 3), (100, 300, 7), (5000, 16, 1)]
 
 
 @pytest.mark.parametrize("kind", ["normal", "quantised", "equal", "signed0", "masked"])
@@ -68,6 +70,13 @@ def test_route_full_size(name):
     out = _route_and_compare(logits, s.K)
     if s.bias == "zipf":
         assert (npi(out["counts"]) == 0).sum() >= 4     # masked experts receive nothing
+
+
+@pytest.mark.parametrize("S,E,K", [(70000, 128, 4), (20000, 1024, 2)])
+def test_route_large_block_counts(S, E, K):
+    """Thousands of token blocks (the column scan walks long chunks), bit-exact
+    like the rest."""
+    _route_and_compare(make_logits("normal", S, E, seed=S + E), K)
 
 
 def test_route_deterministic_and_empty():
