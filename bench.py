@@ -314,8 +314,11 @@ def ep_share(_lib, s, G, reps, stream, dev):
 
 def time_layer_gemms(_lib, sets, out, s, reps, stream, ws_router, ws_route, r_bufs, xd, pd, h, yd, mx=None):
     """Average durations (s) of the up and down grouped GEMM launches inside
-    the layer's launch sequence, one HIP event pair per launch on `stream`.
-    mx = (codes, scales): the MX-FP8 payload, read as sent by the up GEMM."""
+    the layer's launch sequence, one HIP event pair per launch on `stream`:
+    router, route, tile schedule, up projection gathering its rows from x
+    (the dispatch fused into its operand copy, as the layer runs it), down
+    projection, combine.  mx = (codes, scales): the MX-FP8 payload instead,
+    dispatched and read as sent by the up GEMM."""
     import torch
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
     lg = torch.empty_like(out["logits"])
@@ -327,21 +330,20 @@ def time_layer_gemms(_lib, sets, out, s, reps, stream, ws_router, ws_route, r_bu
         _lib.moe_router_logits(inp["x"], inp["Wr"], inp["bias"], s.S, s.D, s.E, lg, ws_router)
         _lib.moe_route_topk(lg, s.S, s.E, s.K, r_bufs["topk_idx"], r_bufs["topk_prob"], r_bufs["counts"],
                             r_bufs["offsets"], r_bufs["perm"], r_bufs["inv_perm"], ws_route)
-        if mx is None:
-            _lib.moe_dispatch(inp["x"], r_bufs["topk_prob"], r_bufs["inv_perm"], s.S, s.D, s.K, xd, pd)
-        else:
+        if mx is not None:
             _lib.moe_dispatch_mxfp8(inp["x"], r_bufs["topk_prob"], r_bufs["inv_perm"], s.S, s.D, s.K, *mx, pd)
         _lib.moe_grouped_schedule(r_bufs["offsets"], s.E, s.R, sched)
         ev[i][0].record(stream)
         if mx is None:
-            _lib.moe_grouped_gemm(xd, sched, s.E, s.R, s.D, s.F, inp["W1"], 1, h, None)
+            _lib.moe_grouped_gemm_gather(inp["x"], r_bufs["perm"], s.S, s.K, sched, s.E, s.R, s.D, s.F, inp["W1"], 1,
+                                         h, None)
         else:
             _lib.moe_grouped_gemm_mxfp8(*mx, sched, s.E, s.R, s.D, s.F, inp["W1"], 1, h, None)
         ev[i][1].record(stream)
         ev[i][2].record(stream)
         _lib.moe_grouped_gemm(h, sched, s.E, s.R, s.F, s.D, inp["W2"], 0, yd, None)
         ev[i][3].record(stream)
-        _lib.moe_combine(yd, pd, r_bufs["inv_perm"], s.S, s.D, s.K, y)
+        _lib.moe_combine(yd, pd if mx is not None else None, r_bufs["inv_perm"], s.S, s.D, s.K, y)
     torch.cuda.synchronize()
     up = sum(e[0].elapsed_time(e[1]) for e in ev) / reps * 1e-3
     down = sum(e[2].elapsed_time(e[3]) for e in ev) / reps * 1e-3
@@ -473,15 +475,17 @@ def other_workload(name, args, dev, stream):
     log(f"other workload {name}: {args.sets} input sets")
     sets = [make_inputs(s, device=dev, seed=s.seed + 1000 * i) for i in range(args.sets)]
     modes = dict(score=s.score, Fs=s.Fs, seq_len=s.seq_len, aux_coeff=s.aux_coeff)
-    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, **modes)
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=False, **modes)
 
-    def step(i):
+    def call(l, i):
         inp = sets[i % len(sets)]
-        lf(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"], Wdown=inp.get("Wdown"),
-           Wup=inp.get("Wup"), sel_bias=inp.get("sel_bias"), Ws1=inp.get("Ws1"), Ws2=inp.get("Ws2"))
+        return l(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"], Wdown=inp.get("Wdown"),
+                 Wup=inp.get("Wup"), sel_bias=inp.get("sel_bias"), Ws1=inp.get("Ws1"), Ws2=inp.get("Ws2"))
 
-    t_layer = settle_and_time(step, args.other_steps, args.warmup, args.settle_seconds, stream)
-    out = lf.out
+    t_layer = settle_and_time(lambda i: call(lf, i), args.other_steps, args.warmup, args.settle_seconds, stream)
+    # the intermediates the GEMM timings read, from one exporting call
+    lfx = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, **modes)
+    out = call(lfx, 0)
     reps = args.stage_reps
     h2 = torch.empty_like(out["h"])
     yd2 = torch.empty_like(out["y_disp"])
@@ -510,7 +514,7 @@ def other_workload(name, args, dev, stream):
            "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(fl / t_dom / 1e12, 1),
                         "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                         "frac": round(fl / t_dom / 1e12 / PEAK_BF16_TFLOPS, 4)}}
-    del sets, lf, out, h2, yd2
+    del sets, lf, lfx, out, h2, yd2
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     return rec
@@ -542,10 +546,15 @@ def main():
     log(f"generating {args.sets} input sets for {s.name}")
     sets = [make_inputs(s, device=dev, seed=s.seed + 1000 * i) for i in range(args.sets)]
     modes = dict(score=s.score, Fs=s.Fs, seq_len=s.seq_len, aux_coeff=s.aux_coeff)
-    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, payload=args.payload, **modes)
+    # the timed layer exports nothing but y, as a training or serving step
+    # would call it (with the bf16 payload the dispatch is then fused into the
+    # up projection's operand copy); stage timings read the intermediates of
+    # one more, exporting call
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=False, payload=args.payload, **modes)
+    lfx = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, device=dev, export=True, payload=args.payload, **modes)
     mx_run = args.payload == "mxfp8"
     if mx_run:
-        lf.out["x_disp"] = None   # the up projection reads the payload as sent: no decode pass
+        lfx.out["x_disp"] = None   # the up projection reads the payload as sent: no decode pass
 
     # a plain device copy of known size, once, so hardware byte counters can be
     # calibrated against it in profiler runs of this same command
@@ -571,7 +580,9 @@ def main():
     per_step = step_times(step, args.steps, stream)
 
     # ---- per-stage timings on the same stream, same launch configuration ----
-    out = lf.out
+    i0 = sets[0]
+    out = lfx(i0["x"], i0["Wr"], i0["W1"], i0["W2"], bias=i0["bias"], Wdown=i0.get("Wdown"), Wup=i0.get("Wup"),
+              sel_bias=i0.get("sel_bias"), Ws1=i0.get("Ws1"), Ws2=i0.get("Ws2"))
     reps = args.stage_reps
     st = {}
     # an untimed write of more bytes than the 256 MB last-level cache holds,
@@ -769,7 +780,7 @@ def main():
     # the other full-size workloads, after the headline's buffers are freed
     route_sw = route_sweep(_lib, s, reps, stream, dev) if args.route_sweep else None
     ep = ep_share(_lib, s, args.ep_share, reps, stream, dev) if args.ep_share > 1 else None
-    del sets, lf, out, fbuf
+    del sets, lf, lfx, out, fbuf
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     others = {}

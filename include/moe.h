@@ -208,6 +208,19 @@ int moe_grouped_gemm(const moe_bf16* A, const void* sched, int32_t E, int64_t R,
                      const moe_bf16* W, int32_t epilogue, moe_bf16* C, moe_bf16* u_save,
                      hipStream_t stream);
 
+/* moe_grouped_gemm with the dispatch fused into its A operand (the
+ * permutation fused into the expert GEMM, Section 5.2): row r of expert e's
+ * segment is x[perm[r] / K, :] instead of a materialised x_disp row, so
+ *   C[r, :] = epi( x[perm[r] / K, :] @ W[e] ),
+ * bit-identical to moe_dispatch followed by moe_grouped_gemm on x_disp.
+ *   x [S, Kd] bf16 (S * Kd * 2 < 2^31);  perm [R] int32 from moe_route_topk
+ *   (R = S * K);  sched, W, epilogue, C, u_save as in moe_grouped_gemm.
+ * Errors: as moe_grouped_gemm, plus MOE_ERR_UNSUPPORTED if S * Kd * 2
+ * reaches 2^31 and MOE_ERR_SHAPE if R != S * K. */
+int moe_grouped_gemm_gather(const moe_bf16* x, const int32_t* perm, int64_t S, int32_t K, const void* sched,
+                            int32_t E, int64_t R, int32_t Kd, int32_t N, const moe_bf16* W, int32_t epilogue,
+                            moe_bf16* C, moe_bf16* u_save, hipStream_t stream);
+
 /* ---------------------------------------------------------------------- */
 /* Combine: probability-weighted sum back to token order (the hidden       */
 /* combine of Section 4.1's footnote; D*b_x per routed row, Eq. 1).        */
@@ -299,6 +312,11 @@ size_t moe_layer_fwd_workspace_bytes(const moe_layer_fwd_args* a);
 
 /* [x_lat = bf16(x @ Wdown)] -> logits -> route -> dispatch -> experts ->
  * combine -> [y = bf16(y_lat @ Wup)], all enqueued on `stream`.
+ * With the bf16 payload and x_disp not exported, the dispatch is fused into
+ * the up projection's operand copy (it gathers each routed row from the
+ * router input through perm; the route also writes p_disp), so the
+ * dispatched rows are never materialised; the results are bit-identical to
+ * the materialised path, which runs when the caller exports x_disp.
  * With payload = MOE_PAYLOAD_MXFP8 the dispatch sends MX-FP8 rows
  * (moe_dispatch_mxfp8) and the up projection reads them as sent
  * (moe_grouped_gemm_mxfp8: the decoded bf16 values, decoded in its operand

@@ -83,6 +83,7 @@ _PROTOS = {
     "moe_grouped_schedule_bytes": (sz, [i32, i64]),
     "moe_grouped_schedule": (C.c_int, [vp, i32, i64, vp, sz, vp]),
     "moe_grouped_gemm": (C.c_int, [vp, vp, i32, i64, i32, i32, vp, i32, vp, vp, vp]),
+    "moe_grouped_gemm_gather": (C.c_int, [vp, vp, i64, i32, vp, i32, i64, i32, i32, vp, i32, vp, vp, vp]),
     "moe_combine": (C.c_int, [vp, vp, vp, i64, i32, i32, vp, vp]),
     "moe_latent_proj": (C.c_int, [vp, vp, i64, i32, i32, vp, vp]),
     "moe_layer_fwd_workspace_bytes": (sz, [C.POINTER(LayerFwdArgs)]),
@@ -241,6 +242,12 @@ def moe_grouped_gemm(A, sched, E, R, Kd, N, W, epilogue, Cout, u_save):
     _check(load().moe_grouped_gemm(_ptr(A, BF16, "A"), _ptr(sched, None, "sched"), E, R, Kd, N,
                                    _ptr(W, BF16, "W"), epilogue, _ptr(Cout, BF16, "C"),
                                    _ptr(u_save, BF16, "u_save"), _stream()), "moe_grouped_gemm")
+
+
+def moe_grouped_gemm_gather(x, perm, S, K, sched, E, R, Kd, N, W, epilogue, Cout, u_save):
+    _check(load().moe_grouped_gemm_gather(_ptr(x, BF16, "x"), _ptr(perm, I32, "perm"), S, K, _ptr(sched, None, "sched"),
+                                          E, R, Kd, N, _ptr(W, BF16, "W"), epilogue, _ptr(Cout, BF16, "C"),
+                                          _ptr(u_save, BF16, "u_save"), _stream()), "moe_grouped_gemm_gather")
 
 
 def moe_combine(y_disp, p_disp, inv_perm, S, D, K, y):

@@ -288,6 +288,27 @@ int moe_grouped_gemm(const moe_bf16* A, const void* sched, int32_t E, int64_t R,
                                                u_save, sched, E, R, N, Kd, stream));
 }
 
+int moe_grouped_gemm_gather(const moe_bf16* x, const int32_t* perm, int64_t S, int32_t K, const void* sched,
+                            int32_t E, int64_t R, int32_t Kd, int32_t N, const moe_bf16* W, int32_t epilogue,
+                            moe_bf16* C, moe_bf16* u_save, hipStream_t stream) {
+    if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(Kd) || !dim_ok(N)) return MOE_ERR_SHAPE;
+    if (S < 0 || K < 1 || K > kMaxK || S * (int64_t)K != R) return MOE_ERR_SHAPE;
+    if (epilogue != 0 && epilogue != 1) return MOE_ERR_UNSUPPORTED;
+    if (!weight_ok(Kd, N) || !weight_ok(S, Kd)) return MOE_ERR_UNSUPPORTED;
+    if (epilogue == 0 && u_save != nullptr) return MOE_ERR_SHAPE;
+    MOE_TRY(need(x, (uint64_t)S * Kd * 2, 16));
+    MOE_TRY(need(perm, (uint64_t)R * 4, 4));
+    if (sched == nullptr) return MOE_ERR_NULL;
+    MOE_TRY(opt(sched, 16));
+    MOE_TRY(need(W, (uint64_t)E * Kd * N * 2, 16));
+    MOE_TRY(need(C, (uint64_t)R * N * 2, 16));
+    MOE_TRY(opt(u_save, 16));
+    if (R == 0) return MOE_OK;
+    return hip_status(moe::launch_grouped_rows_gather(x, Kd, S, perm, K, W, N, (int64_t)Kd * N, C, N,
+                                                      epilogue == 1 ? moe::EPI_RELU2 : moe::EPI_BF16, u_save, sched,
+                                                      E, R, N, Kd, stream));
+}
+
 uint64_t moe_mx_scale_alloc_bytes(int64_t R, int32_t D) {
     if (R < 0 || D < 32 || D % 32 != 0) return 0;
     return ((uint64_t)R * (uint64_t)(D / 32) + 3) / 4 * 4;
@@ -388,6 +409,16 @@ int check_layer_args(const moe_layer_fwd_args* a) {
     return MOE_OK;
 }
 
+// The bf16 payload with x_disp not exported: the route also writes p_disp
+// and the tile tables, and the up projection gathers its rows from the
+// router input through perm, so no dispatch kernel runs and the dispatched
+// rows are never materialised (Section 5.2's permute fusion).  The gather's
+// descriptor spans the router input, so it must stay below 2^31 bytes.
+bool fused_dispatch(const moe_layer_fwd_args* a) {
+    return a->payload == MOE_PAYLOAD_BF16 && a->x_disp == nullptr &&
+           a->S * (int64_t)a->D * 2 < kMaxOperandBytes;
+}
+
 // Lays the non-exported intermediates out in the workspace (or, with base
 // == nullptr, only counts the bytes).  Pointers the caller exported win.
 struct LayerBufs {
@@ -414,9 +445,11 @@ size_t layer_layout(const moe_layer_fwd_args* a, char* base, LayerBufs* b) {
     b->perm = pick(a->perm, (size_t)R * 4);
     b->inv_perm = pick(a->inv_perm, (size_t)R * 4);
     const bool mx = a->payload == MOE_PAYLOAD_MXFP8;
-    // the MX payload feeds the up projection as sent; x_disp (its decode)
-    // exists only when the caller exports it
-    b->x_disp = mx ? a->x_disp : pick(a->x_disp, (size_t)R * D * 2);
+    // the MX payload feeds the up projection as sent, and with the bf16
+    // payload the up projection gathers its rows from the router input
+    // (permutation fused into its operand copy): x_disp (the decode, or the
+    // dispatched rows) exists only when the caller exports it
+    b->x_disp = (mx || fused_dispatch(a)) ? a->x_disp : pick(a->x_disp, (size_t)R * D * 2);
     b->p_disp = pick(a->p_disp, (size_t)R * 4);
     b->h = pick(a->h, (size_t)R * F * 2);
     b->y_disp = pick(a->y_disp, (size_t)R * D * 2);
@@ -496,8 +529,10 @@ int moe_layer_fwd(const moe_layer_fwd_args* args, hipStream_t stream) {
     }
     MOE_HIP(moe::launch_router_logits(x_r, a->Wr, a->router_bias, S, D, E, b.logits, b.router_ws, stream));
     const bool sig = a->score_fn == MOE_SCORE_SIGMOID;
+    const bool fused = fused_dispatch(a);
     MOE_HIP(moe::launch_route(b.logits, S, E, K, b.topk_idx, b.topk_prob, b.counts, b.offsets, b.perm,
-                              b.inv_perm, b.route_ws, stream, sig, a->sel_bias));
+                              b.inv_perm, b.route_ws, stream, sig, a->sel_bias, fused ? b.p_disp : nullptr,
+                              fused && R > 0 ? b.sched : nullptr));
     if (a->seq_len > 0) {
         MOE_HIP(moe::launch_seq_aux_loss(b.logits, b.topk_idx, S, E, K, a->seq_len,
                                          aux_coef(a->aux_coeff, S, E, K, a->seq_len), a->aux_loss,
@@ -509,7 +544,7 @@ int moe_layer_fwd(const moe_layer_fwd_args* args, hipStream_t stream) {
         MOE_HIP(moe::launch_dispatch_mx(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_q, b.x_scale, b.p_disp, stream,
                                         R > 0 ? b.offsets : nullptr, E, R > 0 ? b.sched : nullptr));
         if (b.x_disp != nullptr) MOE_HIP(moe::launch_dequant_mx(b.x_q, b.x_scale, R, D, b.x_disp, stream));
-    } else {
+    } else if (!fused) {
         MOE_HIP(moe::launch_dispatch(x_r, b.topk_prob, b.inv_perm, S, D, K, b.x_disp, b.p_disp, stream,
                                      R > 0 ? b.offsets : nullptr, E, R > 0 ? b.sched : nullptr));
     }
@@ -517,6 +552,9 @@ int moe_layer_fwd(const moe_layer_fwd_args* args, hipStream_t stream) {
         if (mx)
             MOE_HIP(moe::launch_grouped_rows_mx(b.x_q, b.x_scale, a->W1, F, (int64_t)D * F, b.h, F, moe::EPI_RELU2,
                                                 a->u_save, b.sched, E, R, F, D, stream));
+        else if (fused)
+            MOE_HIP(moe::launch_grouped_rows_gather(x_r, D, S, b.perm, K, a->W1, F, (int64_t)D * F, b.h, F,
+                                                    moe::EPI_RELU2, a->u_save, b.sched, E, R, F, D, stream));
         else
             MOE_HIP(moe::launch_grouped_rows(b.x_disp, D, a->W1, F, (int64_t)D * F, false, b.h, F,
                                              moe::EPI_RELU2, nullptr, a->u_save, b.sched, E, R, F, D, stream));

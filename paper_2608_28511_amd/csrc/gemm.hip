@@ -185,6 +185,9 @@ struct GemmArgs {
     const int32_t* mtile_total;  // ROWS mode with tiles: device count of valid 128-row m-tiles
     const int4* tiles_l;      // the same for 256-row tiles
     const int32_t* mtile_total_l;
+    const int32_t* a_perm;    // ROWS mode, bf16 A gathered: row r of the product is A row a_perm[r] / a_div
+    int a_div;
+    int64_t a_src_rows;       // rows of the gathered A
     const uint8_t* A_scale;   // MX-FP8 A: E8M0 scales [R, Kd / 32]
     uint32_t scale_bytes;     // R * Kd / 32 rounded up to a multiple of 4
     int64_t lda, ldb, ldc;
@@ -628,6 +631,8 @@ __device__ __forceinline__ void rows_body(const GemmArgs& p, char* smem, const i
         const RowsTile t = rows_tile<BM>(p, tiles, m_count, lx + j * Gx, m_base);
         if constexpr (T::kAmx)
             da.init((const uint8_t*)p.A, p.A_scale, p.scale_bytes, t.row0, t.row_hi, p.Kd, wave, lane);
+        else if (p.a_perm != nullptr)
+            da.init_gather(p.A, p.lda, p.a_perm, p.a_div, p.a_src_rows, t.row0, t.row_hi, wave, lane);
         else
             da.init(p.A, p.lda, t.row0, t.row_hi, 0, p.Kd, wave, lane);
         db.init(p.B + (int64_t)t.e * p.b_stride, p.ldb, t.n0, (int64_t)p.N, 0, p.Kd, wave, lane);
@@ -890,6 +895,23 @@ hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B
     a.lda = lda;
     rows_args(a, B, ldb, b_stride, C, ldc, aux_out, sched, E, R, N, Kd);
     return launch_rows_epi(a, b_kmajor, epi, st);
+}
+
+hipError_t launch_grouped_rows_gather(const moe_bf16* X, int64_t ldx, int64_t x_rows, const int32_t* perm, int div,
+                                      const moe_bf16* B, int64_t ldb, int64_t b_stride, void* C, int64_t ldc, int epi,
+                                      moe_bf16* aux_out, const void* sched, int E, int64_t R, int N, int Kd,
+                                      hipStream_t st) {
+    if (R == 0) return hipSuccess;
+    if ((int64_t)Kd * ldb * 2 >= kMaxDmaBytes || x_rows * ldx * 2 >= kMaxDmaBytes || div < 1)
+        return hipErrorInvalidValue;
+    GemmArgs a{};
+    a.A = X;
+    a.lda = ldx;
+    a.a_perm = perm;
+    a.a_div = div;
+    a.a_src_rows = x_rows;
+    rows_args(a, B, ldb, b_stride, C, ldc, aux_out, sched, E, R, N, Kd);
+    return launch_rows_epi(a, false, epi, st);
 }
 
 hipError_t launch_grouped_rows_mx(const uint8_t* Aq, const uint8_t* A_scale, const moe_bf16* B, int64_t ldb,

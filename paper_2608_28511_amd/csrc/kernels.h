@@ -49,11 +49,13 @@ int wgrad_chunks(int64_t rows, int M, int N);
 size_t route_ws_bytes(int64_t S, int E);
 // sigmoid: the production router (sigmoid scores, selection by score +
 // sel_bias (nullable), weights = picked sigmoids over their sum); otherwise
-// the softmax router.
+// the softmax router.  With p_disp, each routed row's probability is also
+// written at its position (p_disp[inv_perm[t*K+k]] = topk_prob[t, k]); with
+// sched, the launch also builds the grouped GEMM's tile tables.
 hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* topk_idx,
                         float* topk_prob, int32_t* counts, int32_t* offsets, int32_t* perm,
                         int32_t* inv_perm, void* ws, hipStream_t st, bool sigmoid = false,
-                        const float* sel_bias = nullptr);
+                        const float* sel_bias = nullptr, float* p_disp = nullptr, void* sched = nullptr);
 
 // With sched (and the expert offsets sched_offsets [E+1] of the same
 // routing), the launch also builds the grouped GEMM's tile tables in sched,
@@ -93,6 +95,14 @@ hipError_t launch_grouped_rows(const moe_bf16* A, int64_t lda, const moe_bf16* B
                                int64_t b_stride, bool b_kmajor, void* C, int64_t ldc, int epi,
                                const moe_bf16* aux_in, moe_bf16* aux_out, const void* sched,
                                int E, int64_t R, int N, int Kd, hipStream_t st, bool accumulate = false);
+// ROWS mode with the dispatch fused into the A copy: row r of expert
+// segment e is X[perm[r] / div, :] (X [x_rows, Kd] bf16, ldx elements per
+// row; perm as moe_route_topk writes it, div = K), B N-contiguous.  Equal to
+// launch_grouped_rows on the dispatched rows, without materialising them.
+hipError_t launch_grouped_rows_gather(const moe_bf16* X, int64_t ldx, int64_t x_rows, const int32_t* perm, int div,
+                                      const moe_bf16* B, int64_t ldb, int64_t b_stride, void* C, int64_t ldc, int epi,
+                                      moe_bf16* aux_out, const void* sched, int E, int64_t R, int N, int Kd,
+                                      hipStream_t st);
 // ROWS mode over an MX-FP8 A: codes Aq [R, Kd] uint8 (16-byte aligned, Kd a
 // multiple of 32) and E8M0 scales A_scale [R, Kd / 32] (allocation rounded up
 // to 4 bytes), decoded in the operand path; B N-contiguous; epi EPI_BF16 or

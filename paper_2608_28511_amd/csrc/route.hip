@@ -22,13 +22,18 @@
 //   route_scatter  one thread per routed row; every workgroup first rebuilds
 //                  offsets = exclusive scan of counts in LDS (the first one
 //                  also stores it), then pos = offsets[e] + block base + rank
-//                  gives perm and inv_perm.
+//                  gives perm and inv_perm.  In the fused layer it also
+//                  writes each routed row's probability p_disp[pos] (the
+//                  probability half of the dispatch payload), and one extra
+//                  workgroup builds the grouped GEMM's tile tables from the
+//                  offsets it holds, so the layer needs no dispatch launch.
 //
 // No step depends on the order in which atomics land (the LDS OR is
 // commutative and ranks come from popcounts), so the permutation is
 // bit-for-bit deterministic.
 #include "common.h"
 #include "kernels.h"
+#include "schedule.h"
 
 namespace moe {
 
@@ -208,8 +213,10 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
                                                             int32_t* __restrict__ offsets,
                                                             int32_t* __restrict__ inv_perm,
                                                             int32_t* __restrict__ perm, int64_t R,
-                                                            int K, int E) {
-    __shared__ int32_t off[1024];
+                                                            int K, int E, const float* __restrict__ prob,
+                                                            float* __restrict__ p_disp, int sched_wg,
+                                                            SchedPart sched_small, SchedPart sched_large) {
+    __shared__ int32_t off[1024], seg_hi[1024];
     __shared__ int32_t wsum[4];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // exclusive scan of counts[0..E): each thread owns 4 consecutive experts
@@ -237,6 +244,22 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
         base += v[u];
     }
     __syncthreads();
+    if ((int)blockIdx.x == sched_wg) {
+        // the tile tables from the segments [off[e], off[e+1]) held here,
+        // clamped to [0, R) as the standalone builder clamps them
+        const int total = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+        for (int e = tid; e < E; e += 256) seg_hi[e] = e + 1 < E ? off[e + 1] : total;
+        __syncthreads();
+        for (int e = tid; e < E; e += 256) {
+            const int lo = off[e] < (int)R ? off[e] : (int)R;
+            const int hi = seg_hi[e];
+            off[e] = lo;
+            seg_hi[e] = hi < lo ? lo : (hi > (int)R ? (int)R : hi);
+        }
+        __syncthreads();
+        build_tile_schedule_lds(off, seg_hi, E, sched_small, sched_large);
+        return;
+    }
     if (blockIdx.x == 0) {
         for (int e = tid; e < E; e += 256) offsets[e] = off[e];
         if (tid == 0) offsets[E] = wsum[0] + wsum[1] + wsum[2] + wsum[3];
@@ -251,6 +274,7 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
     if ((uint32_t)pos >= (uint64_t)R) return;  // unreachable for consistent counts
     perm[pos] = (int32_t)i;
     inv_perm[i] = pos;
+    if (p_disp != nullptr) p_disp[pos] = prob[i];
 }
 
 size_t route_ws_bytes(int64_t S, int E) {
@@ -275,7 +299,8 @@ static void launch_topk(const float* logits, const float* sel_bias, int64_t S, i
 
 hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* topk_idx,
                         float* topk_prob, int32_t* counts, int32_t* offsets, int32_t* perm,
-                        int32_t* inv_perm, void* ws, hipStream_t st, bool sigmoid, const float* sel_bias) {
+                        int32_t* inv_perm, void* ws, hipStream_t st, bool sigmoid, const float* sel_bias,
+                        float* p_disp, void* sched) {
     const int nblk = (int)((S + kRouteTok - 1) / kRouteTok);
     int32_t* blkcnt = (int32_t*)ws;
     if (S > 0) {
@@ -291,9 +316,13 @@ hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* t
     const hipError_t e2 = launch_check(st);
     if (e2 != hipSuccess) return e2;
     const int64_t R = S * K;
-    // at least one workgroup, so that offsets are written even for S == 0
-    hipLaunchKernelGGL(route_scatter_kernel, dim3(R > 0 ? grid_for(R, 256) : 1u), dim3(256), 0, st,
-                       topk_idx, blkcnt, counts, offsets, inv_perm, perm, R, K, E);
+    // at least one workgroup, so that offsets are written even for S == 0;
+    // with sched, one more (the last) builds the tile tables
+    const unsigned grid = R > 0 ? grid_for(R, 256) : 1u;
+    const SchedPart ss = sched ? sched_part(sched, E, R, false) : SchedPart{};
+    const SchedPart sl = sched ? sched_part(sched, E, R, true) : SchedPart{};
+    hipLaunchKernelGGL(route_scatter_kernel, dim3(grid + (sched ? 1u : 0u)), dim3(256), 0, st, topk_idx, blkcnt,
+                       counts, offsets, inv_perm, perm, R, K, E, topk_prob, p_disp, sched ? (int)grid : -1, ss, sl);
     return launch_check(st);
 }
 

@@ -98,6 +98,15 @@ __device__ __forceinline__ void sched_fill_part(const int32_t* seg_lo, const int
     __syncthreads();   // cnt is reused by the next part
 }
 
+// Both tile heights' tables from segment bounds a workgroup already holds in
+// LDS (seg_lo, seg_hi: E entries each, within [0, R), monotone).
+__device__ __forceinline__ void build_tile_schedule_lds(const int32_t* seg_lo, const int32_t* seg_hi, int E,
+                                                        const SchedPart& small, const SchedPart& large) {
+    __shared__ int32_t cnt[1024];
+    sched_fill_part(seg_lo, seg_hi, cnt, E, kSchedBM[0], small);
+    sched_fill_part(seg_lo, seg_hi, cnt, E, kSchedBM[1], large);
+}
+
 // Both tile heights' tables for segments offsets[0..E] (1 <= E <= 1024).
 __device__ __forceinline__ void build_tile_schedule(const int32_t* __restrict__ offsets, int E, int R,
                                                     const SchedPart& small, const SchedPart& large) {

@@ -163,6 +163,30 @@ struct DmaTile {
             }
         }
     }
+    // Row layout with gathered rows (the permutation fused into the copy):
+    // tile row r of [x0, x_hi) is source row rows_idx[x0 + r] / div of a
+    // K-contiguous source of src_rows rows (the token of routed row x0 + r),
+    // k from 0; rows past x_hi, or whose index is out of range, read as zero.
+    // The descriptor spans the whole source (src_rows * ld * 2 < 2^31).
+    __device__ __forceinline__ void init_gather(const uint16_t* __restrict__ src, int64_t ld,
+                                                const int32_t* __restrict__ rows_idx, int div, int64_t src_rows,
+                                                int64_t x0, int64_t x_hi, int wave, int lane) {
+        static_assert(ROWL, "gathered rows need the row layout");
+        rs = buf_rsrc(src, (uint32_t)(src_rows * ld * 2));
+        kstep = KD * 2;
+#pragma unroll
+        for (int i = 0; i < kSlots; ++i) {
+            const int p = (wave * kSlots + i) * 64 + lane;
+            const int row = p / kCPR;
+            const int c = (p % kCPR) ^ (SW ? mxswz<KD * 2>(row) : rswz_k<KD>(row));
+            kpos[i] = c * 8;
+            off[i] = kDmaDrop;
+            if (x0 + row < x_hi) {
+                const int tok = rows_idx[x0 + row] / div;
+                if (tok >= 0 && tok < src_rows) off[i] = (uint32_t)((tok * ld + c * 8) * 2);
+            }
+        }
+    }
     // Issue this wave's slots [I0, I1) of the next tile in k order, then
     // advance.  KTAIL (row layout): chunks at or past k_rem, the contraction
     // left from this tile's start, read as zero.

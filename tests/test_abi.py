@@ -92,7 +92,9 @@ def test_layer_struct_layout_matches(lib):
     a.S, a.H, a.D, a.E, a.K, a.F = 512, 0, 256, 8, 2, 512
     n = L.moe_layer_fwd_workspace_bytes(a)
     R = 512 * 2
-    assert n >= R * 256 * 2 * 2 + R * 512 * 2   # x_disp + y_disp + h at least
+    # y_disp + h at least; x_disp is not carved: with it unexported the dispatch
+    # is fused into the up projection, which gathers from x
+    assert R * 256 * 2 + R * 512 * 2 <= n < R * 256 * 2 * 2 + R * 512 * 2
     a.struct_size += 8
     assert L.moe_layer_fwd_workspace_bytes(a) == 0
     a.struct_size -= 8
@@ -188,6 +190,11 @@ def test_validation_errors_return_before_launch(lib):
     assert lib.moe_grouped_ffn_static(FAKE, FAKE, 0, 4, 16, 16, FAKE, FAKE, FAKE, None, FAKE, st) == -2
     assert lib.moe_grouped_ffn_static(FAKE, FAKE, 4, 4, 16, 16, FAKE, FAKE, FAKE, ODD, FAKE, st) == -3
     assert lib.moe_grouped_gemm(FAKE, None, 2, 4, 16, 16, FAKE, 1, FAKE, None, st) == -1
+    # the gathering up projection: R must be S * K; the router input must fit one descriptor
+    assert lib.moe_grouped_gemm_gather(FAKE, FAKE, 4, 2, FAKE, 2, 9, 16, 16, FAKE, 1, FAKE, None, st) == -2
+    assert lib.moe_grouped_gemm_gather(FAKE, FAKE, 1 << 20, 2, FAKE, 2, 1 << 21, 2048, 16, FAKE, 1, FAKE, None,
+                                       st) == -6
+    assert lib.moe_grouped_gemm_gather(FAKE, None, 4, 2, FAKE, 2, 8, 16, 16, FAKE, 1, FAKE, None, st) == -1
     assert lib.moe_grouped_gemm(FAKE, FAKE, 2, 4, 16, 16, FAKE, 2, FAKE, None, st) == -6
     assert lib.moe_router_logits(FAKE, FAKE, None, 4, 16, 0, FAKE, FAKE, 4096, st) == -2
     assert lib.moe_router_logits(FAKE, FAKE, ODD, 4, 16, 4, FAKE, FAKE, 4096, st) == -3

@@ -154,6 +154,29 @@ def test_grouped_gemm_single_launches_match_ffn(R, D, F, E, empty, skew):
         assert (g0 - ms[e]) % 8 == 0 and g0 <= mt < g0 + gs and gs == min(8, ms[e + 1] - g0), (mt, e, g0, gs)
 
 
+@pytest.mark.parametrize("S,D,F,E,K", [(1, 8, 8, 1, 1), (300, 136, 200, 5, 2), (2048, 256, 512, 64, 6),
+                                       (777, 264, 392, 9, 3)])
+def test_grouped_gemm_gather_matches_dispatched(S, D, F, E, K):
+    """The up projection gathering its rows from x through perm equals the
+    dispatch followed by the grouped GEMM on the dispatched rows, bit for bit
+    (u saved too), on ragged experts and k / n tails."""
+    from paper_2608_28511_amd import _lib as L
+    g = torch.Generator().manual_seed(S + D + E)
+    x = torch.randn((S, D), generator=g).to(torch.bfloat16).to(DEV)
+    W1 = (torch.randn((E, D, F), generator=g) / np.sqrt(D)).to(torch.bfloat16).to(DEV)
+    r = layer.route(make_logits("normal", S, E, seed=S + E).to(DEV), K)
+    R = S * K
+    xd, _ = layer.dispatch(x, None, r["inv_perm"], K)
+    sched = layer.grouped_schedule(r["offsets"], E, R)
+    u_ref = torch.empty((R, F), dtype=torch.bfloat16, device=DEV)
+    h_ref = layer.grouped_gemm(xd, sched, W1, 1, u_save=u_ref)
+    h = torch.full((R, F), float("nan"), dtype=torch.bfloat16, device=DEV)
+    u = torch.full((R, F), float("nan"), dtype=torch.bfloat16, device=DEV)
+    L.moe_grouped_gemm_gather(x, r["perm"], S, K, sched, E, R, D, F, W1, 1, h, u)
+    torch.cuda.synchronize()
+    assert torch.equal(h, h_ref) and torch.equal(u, u_ref)
+
+
 def test_schedule_caps_overlapping_segments():
     """Offsets that are not monotone give segments that overlap after
     clamping and ask for more tiles than the table holds (here 8 + 4 > 8 + 3);

@@ -164,6 +164,13 @@ def test_layer_fwd(name):
     again = run_layer(s, inp)
     for k, v in first.items():
         assert torch.equal(v, again[k]), f"{name}: {k} differs between two identical calls"
+    # without exported intermediates the dispatch is fused into the up
+    # projection (rows gathered through perm): the same y, bit for bit
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, H=s.H, export=False)
+    y = lf(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"], Wdown=inp.get("Wdown"),
+           Wup=inp.get("Wup"))["y"]
+    torch.cuda.synchronize()
+    assert torch.equal(y, first["y"]), f"{name}: the fused dispatch changes y"
 
 
 # Degenerate and extreme shapes, every token compared: one token and one

@@ -64,6 +64,11 @@ def test_random_layer_fwd(i):
     out = run_layer(s, inp)
     n_amb = check_layer(s, inp, out)
     assert n_amb <= max(2, s.S // 8)
+    # the fused dispatch (no exported intermediates) gives the same y bit for bit
+    lf = layer.LayerFwd(s.S, s.D, s.E, s.K, s.F, export=False)
+    y = lf(inp["x"], inp["Wr"], inp["W1"], inp["W2"], bias=inp["bias"])["y"]
+    torch.cuda.synchronize()
+    assert torch.equal(y, out["y"])
 
 
 @pytest.mark.parametrize("i", range(8), ids=lambda i: _ids(i, mx=True))
