@@ -340,7 +340,8 @@ int moe_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const float* p_d
                     const int32_t* inv_perm, int64_t S, int32_t D, int32_t K,
                     moe_bf16* dy_disp, float* dp, hipStream_t stream);
 
-/* Workspace bytes moe_grouped_ffn_bwd needs (includes the [R, F] bf16 du). */
+/* Workspace bytes moe_grouped_ffn_bwd needs (the [R, F] bf16 du, the tile
+ * schedule and the experts' order by row count). */
 size_t moe_grouped_ffn_bwd_workspace_bytes(int32_t E, int64_t R, int32_t D, int32_t F);
 
 /* Per expert e over its rows (chain rule of moe_grouped_ffn):

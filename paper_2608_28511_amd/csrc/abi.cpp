@@ -591,7 +591,7 @@ int moe_combine_bwd(const moe_bf16* dy, const moe_bf16* y_disp, const float* p_d
 
 size_t moe_grouped_ffn_bwd_workspace_bytes(int32_t E, int64_t R, int32_t D, int32_t F) {
     if (E < 1 || E > kMaxE || R < 0 || R >= kMaxRows || !dim_ok(D) || !dim_ok(F)) return 0;
-    return align256((size_t)R * F * 2) + moe::gemm_schedule_bytes(E, R);
+    return align256((size_t)R * F * 2) + moe::gemm_schedule_bytes(E, R) + align256((size_t)E * 4);
 }
 
 int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const moe_bf16* h,
@@ -607,11 +607,14 @@ int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const mo
     MOE_TRY(need(dW1, (uint64_t)E * D * F * 4, 16));
     MOE_TRY(need(dW2, (uint64_t)E * F * D * 4, 16));
     const size_t du_bytes = align256((size_t)R * F * 2);
-    const size_t wsn = du_bytes + moe::gemm_schedule_bytes(E, R);
+    const size_t sched_bytes = moe::gemm_schedule_bytes(E, R);
+    const size_t wsn = du_bytes + sched_bytes + align256((size_t)E * 4);
     if (ws == nullptr || ws_bytes < wsn) return MOE_ERR_WORKSPACE;
     MOE_TRY(opt(ws, 256));
     moe_bf16* du = (moe_bf16*)ws;
     void* sched = (char*)ws + du_bytes;
+    int32_t* order = (int32_t*)((char*)ws + du_bytes + sched_bytes);
+    MOE_HIP(moe::launch_expert_order(offsets, E, R, order, stream));
     if (R > 0) {
         MOE_HIP(moe::launch_tile_schedule(offsets, E, R, sched, stream));
         // du = (dy_disp @ W2[e]^T) * 2 max(u, 0): W2[e] is [F, D], read K(=D)-contiguous
@@ -622,10 +625,9 @@ int moe_grouped_ffn_bwd(const moe_bf16* x_disp, const moe_bf16* u_save, const mo
                                          nullptr, nullptr, sched, E, R, D, F, stream));
     }
     // dW2[e] = h_e^T @ dy_disp_e  ([F, D]);  dW1[e] = x_disp_e^T @ du_e  ([D, F])
-    MOE_HIP(moe::launch_grouped_wgrad(h, F, dy_disp, D, dW2, D, (int64_t)F * D, offsets, E, F, D,
-                                      R, stream));
-    MOE_HIP(moe::launch_grouped_wgrad(x_disp, D, du, F, dW1, F, (int64_t)D * F, offsets, E, D, F,
-                                      R, stream));
+    // both in one launch, the experts with the most rows first
+    MOE_HIP(moe::launch_grouped_wgrad2(h, F, dy_disp, D, dW2, D, (int64_t)F * D, F, D, x_disp, D, du, F, dW1, F,
+                                       (int64_t)D * F, D, F, offsets, order, E, R, stream));
     return MOE_OK;
 }
 

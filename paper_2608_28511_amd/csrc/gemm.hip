@@ -181,6 +181,7 @@ struct GemmArgs {
     const uint16_t* aux_in;   // EPI_DRELU2: pre-activation u, same layout as C
     uint16_t* aux_out;        // EPI_RELU2: pre-activation u (may be null)
     const int32_t* offsets;   // [E+1] expert row segments (KGRP mode)
+    const int32_t* order;     // KGRP mode: experts by descending row count (the item order), or null
     const int4* tiles;        // ROWS mode: per 128-row tile {expert, row0, row_end, 0}; null = dense
     const int32_t* mtile_total;  // ROWS mode with tiles: device count of valid 128-row m-tiles
     const int4* tiles_l;      // the same for 256-row tiles
@@ -316,17 +317,65 @@ __device__ __forceinline__ void ring_round(F&& step, int g0, int total) {
 // KGRP mode (wgrad): C_e[m, n] = sum over expert e's rows r of A[r, m] B[r, n],
 // fp32 output.  One workgroup per (expert, m-tile, n-tile).
 template <class T>
+__device__ __forceinline__ void kgrp_item(const GemmArgs& p, int e, int in, char* smem);
+
+// One launch: (expert, m-tile, n-tile) items.  Item `in` of expert slot
+// `slot`; an expert's items run consecutively on one XCD, so they share its
+// rows in that XCD's L2.  Without an order, each XCD takes a contiguous range
+// of slots.  With one (order[r] = the expert with the r-th most rows), slot r
+// goes to XCD r % 8, so every XCD starts on its share of the longest
+// contractions instead of the launch ending after them; the grid then holds
+// ceil(E / 8) * 8 slots.
+template <class T>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) {
     __shared__ __attribute__((aligned(1024))) char smem[T::kRingBytes];
+    const int per = p.m_tiles * p.n_tiles;
+    int slot, in;
+    if (p.order != nullptr) {
+        const int x = (int)(blockIdx.x % kXcds), j = (int)(blockIdx.x / kXcds);
+        slot = x + kXcds * (j / per);
+        in = j - (j / per) * per;
+        if (slot >= p.E) return;
+    } else {
+        const int lid = xcd_remap(blockIdx.x, gridDim.x);
+        slot = lid / per;
+        in = lid - slot * per;
+    }
+    int e = slot;
+    if (p.order != nullptr) {
+        const int eo = ((const __attribute__((address_space(4))) int32_t*)p.order)[slot];
+        e = (eo >= 0 && eo < p.E) ? eo : slot;
+    }
+    kgrp_item<T>(p, e, in, smem);
+}
 
+// Two weight gradients over the same expert segments in one launch: slot
+// 2r + q holds problem q's items of the expert with the r-th most rows
+// (order), dealt to XCDs as above, so each gradient's long contractions
+// overlap the other's instead of each launch ending on its own tail.
+template <class T>
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp2_kernel(GemmArgs p0, GemmArgs p1) {
+    __shared__ __attribute__((aligned(1024))) char smem[T::kRingBytes];
+    const int per0 = p0.m_tiles * p0.n_tiles, per1 = p1.m_tiles * p1.n_tiles;
+    const int per = per0 > per1 ? per0 : per1;
+    const int x = (int)(blockIdx.x % kXcds), j = (int)(blockIdx.x / kXcds);
+    const int slot = x + kXcds * (j / per);
+    const int in = j - (j / per) * per;
+    if (slot >= 2 * p0.E) return;
+    const int q = slot & 1, r = slot >> 1;
+    const GemmArgs& p = q ? p1 : p0;
+    if (in >= (q ? per1 : per0)) return;
+    const int eo = ((const __attribute__((address_space(4))) int32_t*)p0.order)[r];
+    const int e = (eo >= 0 && eo < p0.E) ? eo : r;
+    kgrp_item<T>(p, e, in, smem);
+}
+
+// Item `in` (an m-tile, n-tile pair) of expert (or row chunk) e.
+template <class T>
+__device__ __forceinline__ void kgrp_item(const GemmArgs& p, int e, int in, char* smem) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar LDS offsets
     const int wm = wave >> 2, wn = wave & 3;
-    const int lid = xcd_remap(blockIdx.x, gridDim.x);
-
-    const int per = p.m_tiles * p.n_tiles;
-    const int e = lid / per;
-    const int in = lid - e * per;
     // Two m-tiles at a time across all n-tiles: the ~32 items an XCD runs
     // together then share two m-tiles of A rows and a run of n-tiles of B
     // rows, which fit its L2 (all m-tiles at a time did not: the 31.5B
@@ -942,13 +991,55 @@ static hipError_t launch_kgrp(GemmArgs a, int64_t groups, hipStream_t st) {
     const bool large = groups * mt_l * nt >= 2 * persistent_grid();
     a.m_tiles = (int)(large ? mt_l : (a.M + TileS::BM - 1) / TileS::BM);
     a.n_tiles = (int)nt;
-    const int64_t n_wg = groups * a.m_tiles * a.n_tiles;
+    // with an expert order, whole XCD rounds of expert slots (see gemm_kgrp_kernel)
+    const int64_t slots = a.order != nullptr ? (groups + kXcds - 1) / kXcds * kXcds : groups;
+    const int64_t n_wg = slots * a.m_tiles * a.n_tiles;
     if (n_wg <= 0) return hipSuccess;
     if (n_wg > 0x7fffffff) return hipErrorInvalidConfiguration;
     if (large)
         hipLaunchKernelGGL(gemm_kgrp_kernel<TileL>, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a);
     else
         hipLaunchKernelGGL(gemm_kgrp_kernel<TileS>, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a);
+    return launch_check(st);
+}
+
+// Both weight gradients of the expert FFN in one launch (gemm_kgrp2_kernel),
+// items of the experts with the most rows first.
+hipError_t launch_grouped_wgrad2(const moe_bf16* A0, int64_t lda0, const moe_bf16* B0, int64_t ldb0, float* C0,
+                                 int64_t ldc0, int64_t c_stride0, int M0, int N0, const moe_bf16* A1, int64_t lda1,
+                                 const moe_bf16* B1, int64_t ldb1, float* C1, int64_t ldc1, int64_t c_stride1, int M1,
+                                 int N1, const int32_t* offsets, const int32_t* order, int E, int64_t R,
+                                 hipStream_t st) {
+    if (R * (lda0 > ldb0 ? lda0 : ldb0) * 2 >= kMaxDmaBytes || R * (lda1 > ldb1 ? lda1 : ldb1) * 2 >= kMaxDmaBytes)
+        return hipErrorInvalidValue;
+    if (order == nullptr || E < 1) return hipErrorInvalidValue;
+    GemmArgs a[2] = {};
+    const moe_bf16* As[2] = {A0, A1};
+    const moe_bf16* Bs[2] = {B0, B1};
+    float* Cs[2] = {C0, C1};
+    const int64_t lda[2] = {lda0, lda1}, ldb[2] = {ldb0, ldb1}, ldc[2] = {ldc0, ldc1}, cs[2] = {c_stride0, c_stride1};
+    const int Ms[2] = {M0, M1}, Ns[2] = {N0, N1};
+    int64_t items_l = 0;
+    for (int q = 0; q < 2; ++q) {
+        a[q].A = As[q]; a[q].B = Bs[q]; a[q].C = Cs[q]; a[q].offsets = offsets; a[q].order = order;
+        a[q].lda = lda[q]; a[q].ldb = ldb[q]; a[q].ldc = ldc[q]; a[q].c_stride = cs[q];
+        a[q].M = Ms[q]; a[q].R = R; a[q].N = Ns[q]; a[q].E = E;
+        items_l += (int64_t)E * ((Ms[q] + TileL::BM - 1) / TileL::BM) * ((Ns[q] + BN - 1) / BN);
+    }
+    // tall tiles when both gradients have enough items to fill the device a few times over
+    const bool large = items_l >= 4 * persistent_grid();
+    int per = 0;
+    for (int q = 0; q < 2; ++q) {
+        a[q].m_tiles = (int)((Ms[q] + (large ? TileL::BM : TileS::BM) - 1) / (large ? TileL::BM : TileS::BM));
+        a[q].n_tiles = (Ns[q] + BN - 1) / BN;
+        per = a[q].m_tiles * a[q].n_tiles > per ? a[q].m_tiles * a[q].n_tiles : per;
+    }
+    const int64_t n_wg = (int64_t)((2 * E + kXcds - 1) / kXcds * kXcds) * per;
+    if (n_wg > 0x7fffffff) return hipErrorInvalidConfiguration;
+    if (large)
+        hipLaunchKernelGGL(gemm_kgrp2_kernel<TileL>, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a[0], a[1]);
+    else
+        hipLaunchKernelGGL(gemm_kgrp2_kernel<TileS>, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a[0], a[1]);
     return launch_check(st);
 }
 
@@ -963,11 +1054,37 @@ hipError_t launch_chunked_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* 
     return launch_kgrp(a, nchunk, st);
 }
 
+// Experts ranked by row count, most first (ties to the lower index):
+// order[rank] = e.  One workgroup; each thread counts, for its experts, the
+// experts that come before them.
+__global__ __launch_bounds__(1024) void expert_order_kernel(const int32_t* __restrict__ offsets, int E, int R,
+                                                            int32_t* __restrict__ order) {
+    __shared__ int32_t cnt[1024];
+    for (int e = threadIdx.x; e < E; e += 1024) {
+        int lo = offsets[e], hi = offsets[e + 1];
+        lo = lo < 0 ? 0 : (lo > R ? R : lo);
+        hi = hi < lo ? lo : (hi > R ? R : hi);
+        cnt[e] = hi - lo;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += 1024) {
+        const int c = cnt[e];
+        int rank = 0;
+        for (int f = 0; f < E; ++f) rank += (cnt[f] > c || (cnt[f] == c && f < e)) ? 1 : 0;
+        order[rank] = e;
+    }
+}
+
+hipError_t launch_expert_order(const int32_t* offsets, int E, int64_t R, int32_t* order, hipStream_t st) {
+    hipLaunchKernelGGL(expert_order_kernel, dim3(1), dim3(1024), 0, st, offsets, E, (int)R, order);
+    return launch_check(st);
+}
+
 hipError_t launch_grouped_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
                                 float* C, int64_t ldc, int64_t c_stride, const int32_t* offsets,
-                                int E, int M, int N, int64_t R, hipStream_t st) {
+                                int E, int M, int N, int64_t R, hipStream_t st, const int32_t* order) {
     GemmArgs a{};
-    a.A = A; a.B = B; a.C = C; a.offsets = offsets;
+    a.A = A; a.B = B; a.C = C; a.offsets = offsets; a.order = order;
     a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.c_stride = c_stride;
     a.M = M; a.R = R; a.N = N; a.E = E;
     // DMA descriptors span an expert's rows of both operands
