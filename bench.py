@@ -80,6 +80,8 @@ def parse():
     p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                    help="summarise two rocprofv3 counter passes into profiles/ and exit")
     p.add_argument("--traffic-kernel", default="grouped_down", choices=sorted(KERNEL_NAME))
+    p.add_argument("--traffic-bench-args", default="--others= --no-cpu-baseline --steps 10 --warmup 2 --stage-reps 5",
+                   help="the bench arguments the two counter passes ran with (recorded in the summary)")
     return p.parse_args()
 
 
@@ -147,7 +149,7 @@ def per_dispatch(rows, counter, match):
     return list(vals.values())
 
 
-def write_traffic(d_fetch, d_write, workload, kernel, calib_bytes):
+def write_traffic(d_fetch, d_write, workload, kernel, calib_bytes, bench_args):
     out = {"kernel": kernel, "kernel_symbol": "...".join(KERNEL_NAME[kernel]), "workload": workload,
            "gemm_sources_sha256": gemm_digest()}
     total = 0.0
@@ -167,9 +169,14 @@ def write_traffic(d_fetch, d_write, workload, kernel, calib_bytes):
         total += kib * 1024.0 * factor
     out["bytes_per_launch"] = round(total)
     p = traffic_path(kernel, workload)
+    cmd = f"python3 -u bench.py --workload {workload} {bench_args}"
+    out["commands"] = [f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {d_fetch} -o f -- {cmd}",
+                       f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {d_write} -o wr -- {cmd}",
+                       f"python bench.py --traffic-from {d_fetch} {d_write} --workload {workload} "
+                       f"--traffic-kernel {kernel}"]
     p.write_text(f"HBM traffic of {kernel} on {workload} from rocprofv3 FETCH_SIZE / WRITE_SIZE "
-                 f"passes of `python bench.py --no-cpu-baseline --workload {workload}`, scaled by "
-                 f"a 1 GiB device copy (see bench.py)\n" + json.dumps(out, indent=1) + "\n")
+                 f"passes (commands below), each scaled by what it reads for a 1 GiB device copy\n"
+                 + json.dumps(out, indent=1) + "\n")
     print(p.read_text())
 
 
@@ -523,7 +530,8 @@ def other_workload(name, args, dev, stream):
 def main():
     args = parse()
     if args.traffic_from:
-        write_traffic(*args.traffic_from, args.workload, args.traffic_kernel, args.calib_bytes)
+        write_traffic(*args.traffic_from, args.workload, args.traffic_kernel, args.calib_bytes,
+                      args.traffic_bench_args)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
