@@ -181,7 +181,7 @@ struct GemmArgs {
     const uint16_t* aux_in;   // EPI_DRELU2: pre-activation u, same layout as C
     uint16_t* aux_out;        // EPI_RELU2: pre-activation u (may be null)
     const int32_t* offsets;   // [E+1] expert row segments (KGRP mode)
-    const int32_t* order;     // KGRP mode: experts by descending row count (the item order), or null
+    const int32_t* order;     // KGRP pair launch: experts by descending row count (the item order)
     const int4* tiles;        // ROWS mode: per 128-row tile {expert, row0, row_end, 0}; null = dense
     const int32_t* mtile_total;  // ROWS mode with tiles: device count of valid 128-row m-tiles
     const int4* tiles_l;      // the same for 256-row tiles
@@ -319,55 +319,104 @@ __device__ __forceinline__ void ring_round(F&& step, int g0, int total) {
 template <class T>
 __device__ __forceinline__ void kgrp_item(const GemmArgs& p, int e, int in, char* smem);
 
-// One launch: (expert, m-tile, n-tile) items.  Item `in` of expert slot
-// `slot`; an expert's items run consecutively on one XCD, so they share its
-// rows in that XCD's L2.  Without an order, each XCD takes a contiguous range
-// of slots.  With one (order[r] = the expert with the r-th most rows), slot r
-// goes to XCD r % 8, so every XCD starts on its share of the longest
-// contractions instead of the launch ending after them; the grid then holds
-// ceil(E / 8) * 8 slots.
+// The pair launch's items are those of the expert order (slot r = the
+// expert with the r-th most rows), each slot holding problem 0's items, then
+// problem 1's.  Workgroups go to XCDs round-robin, so workgroup b is the
+// (b / 8)-th of XCD b % 8, and every XCD runs its items in the order below:
+//   heavy slots (the leading ones, at most 8, whose expert holds more than
+//   R / 16 rows: its two gradients are then over half an XCD's fair share)
+//   are cut into chunks of kKgChunk consecutive items, chunk c going to XCD
+//   c % 8, so every XCD holds an equal share of the longest contractions
+//   (whole units left the XCD with the busiest experts of a Zipf routing
+//   at ~1.2x its share);
+//   the other slots' units (one expert, one problem) follow whole, dealt
+//   in rounds of 8 that alternate direction (unit 8k + i to XCD i, or 7 - i
+//   when k is odd, counted from the XCD after the last heavy chunk), so
+//   the units' decreasing sizes even out across XCDs, and the items an XCD
+//   runs together keep one expert's operand rows in its L2 (cutting them
+//   too cost 2.6% on a balanced routing).
+// Each XCD's share is padded to the same length; the padding comes last.
+constexpr int kKgChunk = 8;
+
+struct KgItem {
+    int r, q, in;   // slot, problem, item; r < 0: padding
+};
+
+// Slots whose expert holds more than R / 16 rows: a prefix of the order.
+__device__ __forceinline__ int heavy_slots(const GemmArgs& p) {
+    typedef const __attribute__((address_space(4))) int32_t* cptr;
+    const cptr ord = (cptr)p.order, off = (cptr)p.offsets;
+    const int n = p.E < kXcds ? p.E : kXcds;
+    const int R = (int)p.R;
+    int h = 0;
+    for (; h < n; ++h) {
+        int e = ord[h];
+        e = (e >= 0 && e < p.E) ? e : h;
+        int lo = off[e], hi = off[e + 1];
+        lo = lo < 0 ? 0 : (lo > R ? R : lo);
+        hi = hi < lo ? lo : (hi > R ? R : hi);
+        if ((int64_t)(hi - lo) * 16 <= p.R) break;
+    }
+    return h;
+}
+
+__device__ __forceinline__ KgItem kg_item(unsigned b, int E, int per0, int per1, int H) {
+    const int per = per0 + per1, perm = per0 > per1 ? per0 : per1;
+    const int64_t heavy = (int64_t)H * per;
+    const int n_hc = (int)((heavy + kKgChunk - 1) / kKgChunk);
+    const int x = (int)(b % kXcds), j = (int)(b / kXcds);
+    const int nhx = n_hc > x ? (n_hc - x + kXcds - 1) / kXcds : 0;   // heavy chunks on XCD x
+    KgItem it{-1, 0, 0};
+    if (perm == 0) return it;
+    if (j < nhx * kKgChunk) {
+        const int64_t g = (int64_t)(x + kXcds * (j / kKgChunk)) * kKgChunk + j % kKgChunk;
+        if (g >= heavy) return it;
+        it.r = (int)(g / per);
+        const int rem = (int)(g - (int64_t)it.r * per);
+        it.q = rem >= per0 ? 1 : 0;
+        it.in = rem - it.q * per0;
+        return it;
+    }
+    const int jj = j - nhx * kKgChunk, k = jj / perm;
+    const int xp = ((x - n_hc) % kXcds + kXcds) % kXcds;
+    const int u = kXcds * k + ((k & 1) ? kXcds - 1 - xp : xp);
+    const int r = H + u / 2, q = u & 1, in = jj - k * perm;
+    if (r >= E || in >= (q ? per1 : per0)) return it;
+    return KgItem{r, q, in};
+}
+
+// The pair launch's grid: every XCD's longest possible share (8 heavy slots).
+inline int64_t kg_grid(int E, int64_t per0, int64_t per1) {
+    const int64_t per = per0 + per1, perm = per0 > per1 ? per0 : per1;
+    const int64_t n_hc = ((E < kXcds ? E : kXcds) * per + kKgChunk - 1) / kKgChunk;
+    return kXcds * ((n_hc + kXcds - 1) / kXcds * kKgChunk + (2 * (int64_t)E + kXcds - 1) / kXcds * perm);
+}
+
+// One launch: (row chunk, m-tile, n-tile) items, item `in` of chunk e.  Each
+// XCD takes a contiguous range of chunks, so a chunk's items run
+// consecutively on one XCD and share its rows in that XCD's L2.
 template <class T>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp_kernel(GemmArgs p) {
     __shared__ __attribute__((aligned(1024))) char smem[T::kRingBytes];
     const int per = p.m_tiles * p.n_tiles;
-    int slot, in;
-    if (p.order != nullptr) {
-        const int x = (int)(blockIdx.x % kXcds), j = (int)(blockIdx.x / kXcds);
-        slot = x + kXcds * (j / per);
-        in = j - (j / per) * per;
-        if (slot >= p.E) return;
-    } else {
-        const int lid = xcd_remap(blockIdx.x, gridDim.x);
-        slot = lid / per;
-        in = lid - slot * per;
-    }
-    int e = slot;
-    if (p.order != nullptr) {
-        const int eo = ((const __attribute__((address_space(4))) int32_t*)p.order)[slot];
-        e = (eo >= 0 && eo < p.E) ? eo : slot;
-    }
+    const int lid = xcd_remap(blockIdx.x, gridDim.x);
+    const int e = lid / per;
+    const int in = lid - e * per;
     kgrp_item<T>(p, e, in, smem);
 }
 
-// Two weight gradients over the same expert segments in one launch: slot
-// 2r + q holds problem q's items of the expert with the r-th most rows
-// (order), dealt to XCDs as above, so each gradient's long contractions
-// overlap the other's instead of each launch ending on its own tail.
+// Two weight gradients over the same expert segments in one launch, items
+// placed as above, so each gradient's long contractions overlap the other's
+// instead of each launch ending on its own tail.
 template <class T>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kgrp2_kernel(GemmArgs p0, GemmArgs p1) {
     __shared__ __attribute__((aligned(1024))) char smem[T::kRingBytes];
-    const int per0 = p0.m_tiles * p0.n_tiles, per1 = p1.m_tiles * p1.n_tiles;
-    const int per = per0 > per1 ? per0 : per1;
-    const int x = (int)(blockIdx.x % kXcds), j = (int)(blockIdx.x / kXcds);
-    const int slot = x + kXcds * (j / per);
-    const int in = j - (j / per) * per;
-    if (slot >= 2 * p0.E) return;
-    const int q = slot & 1, r = slot >> 1;
-    const GemmArgs& p = q ? p1 : p0;
-    if (in >= (q ? per1 : per0)) return;
-    const int eo = ((const __attribute__((address_space(4))) int32_t*)p0.order)[r];
-    const int e = (eo >= 0 && eo < p0.E) ? eo : r;
-    kgrp_item<T>(p, e, in, smem);
+    const KgItem it = kg_item(blockIdx.x, p0.E, p0.m_tiles * p0.n_tiles, p1.m_tiles * p1.n_tiles, heavy_slots(p0));
+    if (it.r < 0) return;
+    const GemmArgs& p = it.q ? p1 : p0;
+    const int eo = ((const __attribute__((address_space(4))) int32_t*)p0.order)[it.r];
+    const int e = (eo >= 0 && eo < p0.E) ? eo : it.r;
+    kgrp_item<T>(p, e, it.in, smem);
 }
 
 // Item `in` (an m-tile, n-tile pair) of expert (or row chunk) e.
@@ -991,9 +1040,7 @@ static hipError_t launch_kgrp(GemmArgs a, int64_t groups, hipStream_t st) {
     const bool large = groups * mt_l * nt >= 2 * persistent_grid();
     a.m_tiles = (int)(large ? mt_l : (a.M + TileS::BM - 1) / TileS::BM);
     a.n_tiles = (int)nt;
-    // with an expert order, whole XCD rounds of expert slots (see gemm_kgrp_kernel)
-    const int64_t slots = a.order != nullptr ? (groups + kXcds - 1) / kXcds * kXcds : groups;
-    const int64_t n_wg = slots * a.m_tiles * a.n_tiles;
+    const int64_t n_wg = groups * a.m_tiles * a.n_tiles;
     if (n_wg <= 0) return hipSuccess;
     if (n_wg > 0x7fffffff) return hipErrorInvalidConfiguration;
     if (large)
@@ -1028,13 +1075,12 @@ hipError_t launch_grouped_wgrad2(const moe_bf16* A0, int64_t lda0, const moe_bf1
     }
     // tall tiles when both gradients have enough items to fill the device a few times over
     const bool large = items_l >= 4 * persistent_grid();
-    int per = 0;
     for (int q = 0; q < 2; ++q) {
         a[q].m_tiles = (int)((Ms[q] + (large ? TileL::BM : TileS::BM) - 1) / (large ? TileL::BM : TileS::BM));
         a[q].n_tiles = (Ns[q] + BN - 1) / BN;
-        per = a[q].m_tiles * a[q].n_tiles > per ? a[q].m_tiles * a[q].n_tiles : per;
     }
-    const int64_t n_wg = (int64_t)((2 * E + kXcds - 1) / kXcds * kXcds) * per;
+    const int64_t n_wg =
+        kg_grid(E, (int64_t)a[0].m_tiles * a[0].n_tiles, (int64_t)a[1].m_tiles * a[1].n_tiles);
     if (n_wg > 0x7fffffff) return hipErrorInvalidConfiguration;
     if (large)
         hipLaunchKernelGGL(gemm_kgrp2_kernel<TileL>, dim3((unsigned)n_wg), dim3(kGemmThreads), 0, st, a[0], a[1]);
@@ -1080,16 +1126,5 @@ hipError_t launch_expert_order(const int32_t* offsets, int E, int64_t R, int32_t
     return launch_check(st);
 }
 
-hipError_t launch_grouped_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
-                                float* C, int64_t ldc, int64_t c_stride, const int32_t* offsets,
-                                int E, int M, int N, int64_t R, hipStream_t st, const int32_t* order) {
-    GemmArgs a{};
-    a.A = A; a.B = B; a.C = C; a.offsets = offsets; a.order = order;
-    a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.c_stride = c_stride;
-    a.M = M; a.R = R; a.N = N; a.E = E;
-    // DMA descriptors span an expert's rows of both operands
-    if (R * (lda > ldb ? lda : ldb) * 2 >= kMaxDmaBytes) return hipErrorInvalidValue;
-    return launch_kgrp(a, E, st);
-}
 
 }  // namespace moe

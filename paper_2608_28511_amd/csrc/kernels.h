@@ -116,13 +116,10 @@ hipError_t launch_grouped_rows_mx(const uint8_t* Aq, const uint8_t* A_scale, con
 hipError_t launch_chunked_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb, float* C,
                                 int64_t ldc, int64_t c_stride, int nchunk, int64_t kchunk, int M, int N,
                                 int64_t R, hipStream_t st);
-// order (optional, from launch_expert_order): the experts' items are
-// dispatched in that order, the largest contractions first.
-hipError_t launch_grouped_wgrad(const moe_bf16* A, int64_t lda, const moe_bf16* B, int64_t ldb,
-                                float* C, int64_t ldc, int64_t c_stride, const int32_t* offsets,
-                                int E, int M, int N, int64_t R, hipStream_t st, const int32_t* order = nullptr);
 // Two KGRP products over the same expert segments in one launch (the expert
-// FFN's dW2 and dW1), items ordered by `order` (required) across both.
+// FFN's dW2 and dW1): the experts' items in `order` (required, from
+// launch_expert_order), the largest contractions first, dealt evenly to the
+// XCDs in chunks of consecutive items.
 hipError_t launch_grouped_wgrad2(const moe_bf16* A0, int64_t lda0, const moe_bf16* B0, int64_t ldb0, float* C0,
                                  int64_t ldc0, int64_t c_stride0, int M0, int N0, const moe_bf16* A1, int64_t lda1,
                                  const moe_bf16* B1, int64_t ldb1, float* C1, int64_t ldc1, int64_t c_stride1, int M1,
