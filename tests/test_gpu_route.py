@@ -93,8 +93,10 @@ def test_route_deterministic_and_empty():
 
 @pytest.mark.parametrize("S,D,E,bias", [(1, 8, 1, False), (100, 264, 37, True), (512, 256, 8, False),
                                         (1000, 2048, 64, False), (777, 2048, 256, True),
-                                        (513, 1024, 128, False)])
+                                        (513, 1024, 128, False), (8142, 2040, 250, True)])
 def test_router_logits(S, D, E, bias):
+    """The last case takes the 128-token x 64-expert tile with ragged tokens,
+    experts and contraction."""
     g = torch.Generator().manual_seed(S + D + E)
     x = torch.randn((S, D), generator=g).to(torch.bfloat16)
     Wr = torch.randn((D, E), generator=g) / np.sqrt(D)
