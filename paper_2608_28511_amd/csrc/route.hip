@@ -6,11 +6,13 @@
 //
 //   route_topk     32 tokens per workgroup, 2 per wavefront (16 waves, so
 //                  each SIMD has several waves whose dependent max and
-//                  ballot chains overlap), all loaded up front.  Per token, K rounds of: wave-wide max of the
-//                  orderable 32-bit score codes of the experts not yet picked
-//                  (DPP within rows of 16 lanes, then the 4 row maxima), and
-//                  a ballot for the lowest expert id holding that code (ties
-//                  go to the lower id, NaN ranks below -inf).  Then the
+//                  ballot chains overlap), all loaded up front.  K rounds,
+//                  each over the wave's two tokens together (two independent
+//                  chains), of: wave-wide max of the orderable 32-bit score
+//                  codes of the experts not yet picked (DPP within rows of 16
+//                  lanes, then the 4 row maxima), a ballot for the lowest
+//                  expert id holding that code (ties go to the lower id, NaN
+//                  ranks below -inf), and clearing the winner's code.  Then the
 //                  softmax renormalised over the K winners (or, for sigmoid
 //                  scores, the winners' sigmoids over their sum), and a per-block
 //                  LDS bitmask per expert that gives each (token, slot) its
@@ -44,9 +46,11 @@ constexpr int kScanCols = 4;    // experts per route_colscan workgroup
 constexpr int kScanThreads = 256;
 
 // Monotone map of an fp32 score to uint32 (larger score -> larger code).
-// -0 is folded onto +0 and NaN maps to 0, below the code of -inf.
+// -0 is folded onto +0 and NaN maps to 1, below the code of -inf (0x007fffff,
+// the smallest code of a number); 0 is left for experts already picked or
+// past E, so that removing a pick is clearing its code.
 __device__ __forceinline__ uint32_t score_code(float f) {
-    if (f != f) return 0u;
+    if (f != f) return 1u;
     uint32_t u = __float_as_uint(f);
     if (u == 0x80000000u) u = 0u;
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
@@ -111,41 +115,48 @@ __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
     }
     __syncthreads();
 
+    // K rounds for the wave's tokens together (independent chains the
+    // scheduler interleaves).  Every code of an expert not yet picked is >= 1
+    // and K <= E, so a round's maximum is never a cleared code (a token past
+    // S has only cleared codes; its picks are never stored).  Lane k keeps
+    // the k-th pick of each token and its code.
+    int my_e[kTokPerWave] = {};
+    uint32_t my_c[kTokPerWave] = {};
+    for (int k = 0; k < K; ++k) {
+#pragma unroll
+        for (int j = 0; j < kTokPerWave; ++j) {
+            uint32_t m = code[j][0];
+#pragma unroll
+            for (int i = 1; i < EPL; ++i) m = max(m, code[j][i]);
+            m = wave_max_u32(m);
+            // the lowest expert id holding m: the lowest slot i with a
+            // match, then its lowest lane
+            int e_sel = 0;
+#pragma unroll
+            for (int i = EPL - 1; i >= 0; --i) {
+                const uint64_t b = __ballot(code[j][i] == m);
+                if (b != 0) e_sel = kWave * i + (__ffsll((unsigned long long)b) - 1);
+            }
+            const bool own = lane == (e_sel & (kWave - 1));
+#pragma unroll
+            for (int i = 0; i < EPL; ++i)
+                if (own && i == (e_sel >> 6)) code[j][i] = 0u;
+            if (lane == k) {
+                my_e[j] = e_sel;
+                my_c[j] = m;
+            }
+        }
+    }
+
 #pragma unroll
     for (int j = 0; j < kTokPerWave; ++j) {
         const int jt = wave * kTokPerWave + j;
         const int64_t t = t_base + jt;
         if (t >= S) break;
-        uint32_t taken = 0;  // bit i: expert lane + 64 i picked (or beyond E)
-#pragma unroll
-        for (int i = 0; i < EPL; ++i)
-            if (lane + kWave * i >= E) taken |= 1u << i;
-        int my_e = 0;
-        float my_s = 0.f;
-        for (int k = 0; k < K; ++k) {
-            uint32_t m = 0;
-#pragma unroll
-            for (int i = 0; i < EPL; ++i)
-                if (!(taken >> i & 1u)) m = max(m, code[j][i]);
-            m = wave_max_u32(m);
-            int e_sel = 0;
-#pragma unroll
-            for (int i = 0; i < EPL; ++i) {
-                const uint64_t b = __ballot(!(taken >> i & 1u) && code[j][i] == m);
-                if (b != 0) {
-                    e_sel = kWave * i + (__ffsll((unsigned long long)b) - 1);
-                    break;
-                }
-            }
-            if (lane == (e_sel & (kWave - 1))) taken |= 1u << (e_sel / kWave);
-            if (lane == k) {
-                my_e = e_sel;
-                my_s = code_score(m);
-            }
-        }
+        const float my_s = code_score(my_c[j]);
         float z;
         if constexpr (SIG) {
-            z = (lane < K) ? sigmoid_f32(logits[t * E + my_e]) : 0.f;
+            z = (lane < K) ? sigmoid_f32(logits[t * E + my_e[j]]) : 0.f;
         } else {
             const float s0 = __shfl(my_s, 0);
             z = (lane < K) ? expf(my_s - s0) : 0.f;
@@ -154,10 +165,10 @@ __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
 #pragma unroll
         for (int msk = 32; msk > 0; msk >>= 1) sum += __shfl_xor(sum, msk);
         if (lane < K) {
-            topk_idx[t * K + lane] = my_e;
+            topk_idx[t * K + lane] = my_e[j];
             topk_prob[t * K + lane] = z / sum;
-            sel[jt][lane] = (int16_t)my_e;
-            atomicOr(&mask[my_e], 1u << jt);
+            sel[jt][lane] = (int16_t)my_e[j];
+            atomicOr(&mask[my_e[j]], 1u << jt);
         }
     }
     __syncthreads();
