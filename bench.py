@@ -11,8 +11,10 @@ Prints ONE JSON line on stdout (progress goes to stderr):
                workloads
   roofline     the dominant kernel (the larger of the two grouped GEMMs), each
                launch timed with its own HIP events on the stream it is launched
-               on, inside the layer's own launch sequence, against the dense
-               bf16 MFMA peak
+               on, inside the layer's own launch sequence, against the roofline
+               that bounds it: HBM (8 TB/s) when its flops per algorithmic byte
+               fall below the ridge (312.5), else the dense bf16 MFMA peak; both
+               fractions are reported
   stages       per-stage times and algorithmic GB/s or TFLOP/s; each launch of
                a stage is timed alone with its own events, after an untimed
                512 MB write that evicts its inputs from the last-level cache
@@ -178,6 +180,33 @@ def write_traffic(d_fetch, d_write, workload, kernel, calib_bytes, bench_args):
                  f"passes (commands below), each scaled by what it reads for a 1 GiB device copy\n"
                  + json.dumps(out, indent=1) + "\n")
     print(p.read_text())
+
+
+def gemm_bytes(s, e_used):
+    """Algorithmic bytes of one grouped-GEMM launch (either projection): the
+    A rows read, the output rows written and the weights of the experts that
+    received rows, R*Kd*2 + R*N*2 + E_used*Kd*N*2 with {Kd, N} = {D, F}."""
+    return s.R * s.D * 2 + s.R * s.F * 2 + e_used * s.D * s.F * 2
+
+
+def gemm_roofline(kernel, flops, nbytes, t, traffic=None, per_launch=""):
+    """The dominant grouped GEMM against the roofline that bounds it: an
+    algorithmic intensity (flops per algorithmic byte) below the ridge (peak
+    MFMA rate over peak HBM bandwidth, 312.5 flop/B) bounds it by HBM, above
+    it by the MFMA pipes.  Both fractions are reported."""
+    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    ai = flops / nbytes
+    tf, gbs = flops / t / 1e12, nbytes / t / 1e9
+    if ai < ridge:
+        r = {"bound": "hbm", "kernel": kernel, "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+             "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    else:
+        r = {"bound": "mfma", "kernel": kernel, "achieved": round(tf, 1), "peak": PEAK_BF16_TFLOPS,
+             "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
+    r.update(traffic=traffic, intensity_flop_per_byte=round(ai, 1), ridge_flop_per_byte=round(ridge, 1),
+             mfma_frac=round(tf / PEAK_BF16_TFLOPS, 4), hbm_frac=round(gbs / PEAK_HBM_GBS, 4),
+             algorithmic_bytes=int(nbytes), flops=flops, per_launch=per_launch)
+    return r
 
 
 def stage_bytes(s):
@@ -514,13 +543,12 @@ def other_workload(name, args, dev, stream):
         t_down = time_region(lambda i: _lib.moe_grouped_gemm(out["h"], sched, s.E, s.R, s.F, s.D,
                                                              sets[i % len(sets)]["W2"], 0, yd2, None), reps, stream)
     fl = 2.0 * s.R * s.D * s.F
+    e_used = int((out["counts"] > 0).sum().item())
     dom, t_dom = ("grouped_up", t_up) if t_up >= t_down else ("grouped_down", t_down)
     rec = {"value": round(s.R / t_layer, 1), "unit": "slots/s", "ms_per_step": round(t_layer * 1e3, 4),
            "steps": args.other_steps,
            "grouped_up_us": round(t_up * 1e6, 1), "grouped_down_us": round(t_down * 1e6, 1),
-           "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(fl / t_dom / 1e12, 1),
-                        "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                        "frac": round(fl / t_dom / 1e12 / PEAK_BF16_TFLOPS, 4)}}
+           "roofline": gemm_roofline(dom, fl, gemm_bytes(s, e_used), t_dom)}
     del sets, lf, lfx, out, h2, yd2
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
@@ -772,13 +800,14 @@ def main():
         stages[k] = e
 
     dom = max(("grouped_up", "grouped_down"), key=lambda k: st[k])
-    achieved = gemm_flops / st[dom] / 1e12
     # on the MX payload the timed up projection is the kernel that decodes it
     dom_kernel = "grouped_up_mxfp8" if mx_run and dom == "grouped_up" else dom
-    roofline = {"bound": "mfma", "kernel": dom_kernel, "achieved": round(achieved, 1),
-                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": load_traffic(dom_kernel, s.name),
-                "per_launch": f"2*R*D*F = {gemm_flops:.4g} flop per launch (R = S*K = {s.R})"}
+    e_used = int((out["counts"] > 0).sum().item())
+    gb = gemm_bytes(s, e_used)
+    roofline = gemm_roofline(
+        dom_kernel, gemm_flops, gb, st[dom], traffic=load_traffic(dom_kernel, s.name),
+        per_launch=(f"2*R*D*F = {gemm_flops:.4g} flop and R*D*2 + R*F*2 + E_used*D*F*2 = {gb:.4g} bytes "
+                    f"per launch (R = S*K = {s.R}, E_used = {e_used})"))
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -35,3 +35,23 @@ def test_cpu_baseline_reports_stages_and_host():
     assert rec["nproc"] >= 1 and isinstance(rec["cpu_model"], str)
     assert set(rec["stage_seconds_per_pass"]) == {"router_logits", "route", "permutation", "dispatch",
                                                   "expert_ffn", "combine"}
+
+
+def test_gemm_roofline_takes_the_bound_of_its_intensity():
+    """The grouped GEMM's roofline: below the ridge (2500 TFLOP/s over 8 TB/s =
+    312.5 flop per byte) HBM bounds it, above it the MFMA pipes; the 256-expert
+    layer's projection (2.8 GB of weights for 65,536 rows) falls below, the
+    64-expert one above."""
+    from paper_2608_28511_amd.workloads import WORKLOADS
+    ce, base = WORKLOADS["ce_s8192_d2048_e256_k8"], WORKLOADS["base_s8192_d2048_e64_k6"]
+    fl = 2.0 * ce.R * ce.D * ce.F
+    nb = bench.gemm_bytes(ce, ce.E)
+    assert nb == ce.R * (ce.D + ce.F) * 2 + ce.E * ce.D * ce.F * 2
+    r = bench.gemm_roofline("grouped_up", fl, nb, 1e-3)
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert abs(r["achieved"] - nb / 1e-3 / 1e9) < 0.1 and abs(r["frac"] - r["hbm_frac"]) < 1e-9
+    assert r["intensity_flop_per_byte"] < 312.5 == r["ridge_flop_per_byte"]
+    assert abs(r["mfma_frac"] - fl / 1e-3 / 2.5e15) < 1e-4
+    fl_b = 2.0 * base.R * base.D * base.F
+    r = bench.gemm_roofline("grouped_up", fl_b, bench.gemm_bytes(base, base.E), 2e-4)
+    assert r["bound"] == "mfma" and r["unit"] == "TFLOP/s" and abs(r["frac"] - r["mfma_frac"]) < 1e-9
