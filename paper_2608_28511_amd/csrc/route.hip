@@ -2,7 +2,7 @@
 //
 // Dropless top-K routing (Section 1) sends every token to exactly K distinct
 // experts; the grouped-GEMM experts then need the S*K routed rows in
-// expert-contiguous order (fused permutation, Section 5.2).  Three launches:
+// expert-contiguous order (fused permutation, Section 5.2).  Two launches:
 //
 //   route_topk     32 tokens per workgroup, 2 per wavefront (16 waves, so
 //                  each SIMD has several waves whose dependent max and
@@ -17,18 +17,21 @@
 //                  scores, the winners' sigmoids over their sum), and a per-block
 //                  LDS bitmask per expert that gives each (token, slot) its
 //                  rank among the block's rows of that expert and the block's
-//                  per-expert count.
-//   route_colscan  per expert (parallel over experts): exclusive scan of the
-//                  block counts along blocks, in place; the total is
-//                  counts[e].
-//   route_scatter  one thread per routed row; every workgroup first rebuilds
-//                  offsets = exclusive scan of counts in LDS (the first one
-//                  also stores it), then pos = offsets[e] + block base + rank
-//                  gives perm and inv_perm.  In the fused layer it also
-//                  writes each routed row's probability p_disp[pos] (the
-//                  probability half of the dispatch payload), and one extra
-//                  workgroup builds the grouped GEMM's tile tables from the
-//                  offsets it holds, so the layer needs no dispatch launch.
+//                  per-expert count, stored as one byte (at most 32) in an
+//                  expert-major count matrix [E][blocks].
+//   route_scatter  each workgroup first sums, for every expert, its row of
+//                  the count matrix in full (counts, then offsets by an
+//                  exclusive scan in LDS; the first workgroup stores both)
+//                  and up to its own first token block (the expert's rows in
+//                  earlier blocks), four bytes per dot-product instruction;
+//                  then pos = offsets[e] + rows in earlier blocks + rank
+//                  gives perm and inv_perm for the rows of its blocks.  In the
+//                  fused layer it also writes each routed row's probability
+//                  p_disp[pos] (the probability half of the dispatch payload),
+//                  and one extra workgroup builds the grouped GEMM's tile
+//                  tables from the offsets it holds, so the layer needs no
+//                  dispatch launch.  Every workgroup reads the whole count
+//                  matrix, so the blocks are dealt to at most 256 workgroups.
 //
 // No step depends on the order in which atomics land (the LDS OR is
 // commutative and ranks come from popcounts), so the permutation is
@@ -42,8 +45,12 @@ namespace moe {
 constexpr int kRouteTok = 32;  // tokens per block (one bit each in the masks)
 constexpr int kRouteThreads = 1024;
 constexpr int kTokPerWave = kRouteTok / (kRouteThreads / kWave);  // 2
-constexpr int kScanCols = 4;    // experts per route_colscan workgroup
-constexpr int kScanThreads = 256;
+constexpr int kScatThreads = 256;
+constexpr int kScatMaxWg = 256;   // scatter workgroups (each reads the whole count matrix)
+
+// Row length in bytes of the expert-major count matrix: the token blocks
+// rounded up to whole 16-byte chunks (the padding bytes are zero).
+inline __host__ __device__ int64_t cnt_row_bytes(int64_t nblk) { return (nblk + 15) / 16 * 16; }
 
 // Monotone map of an fp32 score to uint32 (larger score -> larger code).
 // -0 is folded onto +0 and NaN maps to 1, below the code of -inf (0x007fffff,
@@ -83,8 +90,8 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 template <int EPL, bool SIG>
 __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
     const float* __restrict__ logits, const float* __restrict__ sel_bias, int64_t S, int E, int K,
-    int32_t* __restrict__ topk_idx, float* __restrict__ topk_prob, int32_t* __restrict__ blkcnt,
-    int32_t* __restrict__ rank_out) {
+    int32_t* __restrict__ topk_idx, float* __restrict__ topk_prob, uint8_t* __restrict__ blkcnt,
+    int64_t nbp, int32_t* __restrict__ rank_out) {
     __shared__ uint32_t mask[1024];
     __shared__ int16_t sel[kRouteTok][32];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -180,65 +187,103 @@ __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
         rank_out[(t_base + j) * K + k] = __popc(mask[e] & ((1u << j) - 1u));
     }
     for (int e = tid; e < E; e += kRouteThreads)
-        blkcnt[(int64_t)blockIdx.x * E + e] = __popc(mask[e]);
+        blkcnt[(int64_t)e * nbp + blockIdx.x] = (uint8_t)__popc(mask[e]);
+    // the last block also zeroes every row's padding bytes
+    const int64_t nblk = gridDim.x;
+    if ((int64_t)blockIdx.x == nblk - 1) {
+        const int pad = (int)(nbp - nblk);
+        for (int q = tid; q < E * pad; q += kRouteThreads)
+            blkcnt[(int64_t)(q / pad) * nbp + nblk + q % pad] = 0;
+    }
 }
 
-// blkcnt[b*E+e] (rows of expert e in token block b) is replaced in place by
-// the rows of e in blocks before b; counts[e] = all rows of e.  A workgroup
-// takes kScanCols experts; its 256 threads split the blocks into 64 chunks.
-__global__ __launch_bounds__(kScanThreads) void route_colscan_kernel(int32_t* __restrict__ blkcnt, int nblk,
-                                                                     int E, int32_t* __restrict__ counts) {
-    constexpr int kChunks = kScanThreads / kScanCols;  // 64
-    __shared__ int32_t part[kChunks][kScanCols];
-    const int tid = threadIdx.x;
-    const int c = tid % kScanCols, q = tid / kScanCols;
-    const int e = blockIdx.x * kScanCols + c;
-    const int chunk = (nblk + kChunks - 1) / kChunks;
-    const int b0 = q * chunk;
-    const int b1 = (b0 + chunk) < nblk ? (b0 + chunk) : nblk;
-    int s = 0;
-    if (e < E)
-        for (int b = b0; b < b1; ++b) s += blkcnt[(int64_t)b * E + e];
-    part[q][c] = s;
-    __syncthreads();
-    if (e >= E) return;
-    int before = 0, total = 0;
-    for (int r = 0; r < kChunks; ++r) {
-        const int v = part[r][c];
-        before += r < q ? v : 0;
-        total += v;
+// Sum of the 16 count bytes of a chunk, and of its bytes before position lim.
+__device__ __forceinline__ uint32_t bytes_sum(const uint4& c) {
+    uint32_t s = __builtin_amdgcn_udot4(c.x, 0x01010101u, 0u, false);
+    s = __builtin_amdgcn_udot4(c.y, 0x01010101u, s, false);
+    s = __builtin_amdgcn_udot4(c.z, 0x01010101u, s, false);
+    return __builtin_amdgcn_udot4(c.w, 0x01010101u, s, false);
+}
+__device__ __forceinline__ uint32_t bytes_sum_below(const uint4& c, int lim) {
+    const uint32_t w[4] = {c.x, c.y, c.z, c.w};
+    uint32_t s = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int n = lim - 4 * q;   // bytes of word q below lim
+        const uint32_t m = n >= 4 ? 0xffffffffu : (n <= 0 ? 0u : (1u << (8 * n)) - 1u);
+        s = __builtin_amdgcn_udot4(w[q] & m, 0x01010101u, s, false);
     }
-    int run = before;
-    for (int b = b0; b < b1; ++b) {
-        const int64_t ix = (int64_t)b * E + e;
-        const int v = blkcnt[ix];
-        blkcnt[ix] = run;
-        run += v;
-    }
-    if (q == 0) counts[e] = total;
+    return s;
 }
 
-__global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __restrict__ topk_idx,
-                                                            const int32_t* __restrict__ blkbase,
-                                                            const int32_t* __restrict__ counts,
-                                                            int32_t* __restrict__ offsets,
-                                                            int32_t* __restrict__ inv_perm,
-                                                            int32_t* __restrict__ perm, int64_t R,
-                                                            int K, int E, const float* __restrict__ prob,
-                                                            float* __restrict__ p_disp, int sched_wg,
-                                                            SchedPart sched_small, SchedPart sched_large) {
-    __shared__ int32_t off[1024], seg_hi[1024];
+// Workgroup w takes token blocks [w * bpw, min((w + 1) * bpw, nblk)).
+__global__ __launch_bounds__(kScatThreads) void route_scatter_kernel(
+    const int32_t* __restrict__ topk_idx, const uint8_t* __restrict__ blkcnt, int64_t nblk, int64_t nbp, int bpw,
+    int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int32_t* __restrict__ inv_perm,
+    int32_t* __restrict__ perm, int64_t S, int K, int E, const float* __restrict__ prob,
+    float* __restrict__ p_disp, int sched_wg, SchedPart sched_small, SchedPart sched_large) {
+    __shared__ int32_t off[1024], run[1024], seg_hi[1024];
     __shared__ int32_t wsum[4];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // exclusive scan of counts[0..E): each thread owns 4 consecutive experts
-    int v[4], run = 0;
+    const bool sched = (int)blockIdx.x == sched_wg;
+    const int64_t b0 = sched ? 0 : (int64_t)blockIdx.x * bpw;
+    const int64_t b1 = sched ? 0 : (b0 + bpw < nblk ? b0 + bpw : nblk);
+
+    // 1. per expert: rows in all blocks (-> seg_hi for now) and in blocks
+    // before b0 (-> run).  tpe adjacent lanes share an expert's row (E <=
+    // 128) and combine their sums with xor shuffles; above 128 experts each
+    // lane takes whole rows.
+    const int64_t nchunk = nbp / 16;
+    const int64_t cb0 = b0 / 16;
+    const int lim0 = (int)(b0 % 16);
+    if (E <= 128) {
+        int tpe = 64;
+        while (tpe * E > kScatThreads) tpe >>= 1;
+        const int e = tid / tpe, part = tid % tpe;
+        uint32_t tot = 0, pre = 0;
+        if (e < E) {
+            const uint4* row = (const uint4*)(blkcnt + (int64_t)e * nbp);
+            for (int64_t c = part; c < nchunk; c += tpe) {
+                const uint4 v = row[c];
+                const uint32_t s = bytes_sum(v);
+                tot += s;
+                pre += c < cb0 ? s : (c == cb0 ? bytes_sum_below(v, lim0) : 0u);
+            }
+        }
+        for (int m = 1; m < tpe; m <<= 1) {
+            tot += __shfl_xor(tot, m);
+            pre += __shfl_xor(pre, m);
+        }
+        if (e < E && part == 0) {
+            seg_hi[e] = (int32_t)tot;
+            run[e] = (int32_t)pre;
+        }
+    } else {
+        for (int e = tid; e < E; e += kScatThreads) {
+            const uint4* row = (const uint4*)(blkcnt + (int64_t)e * nbp);
+            uint32_t tot = 0, pre = 0;
+            for (int64_t c = 0; c < nchunk; ++c) {
+                const uint4 v = row[c];
+                const uint32_t s = bytes_sum(v);
+                tot += s;
+                pre += c < cb0 ? s : (c == cb0 ? bytes_sum_below(v, lim0) : 0u);
+            }
+            seg_hi[e] = (int32_t)tot;
+            run[e] = (int32_t)pre;
+        }
+    }
+    __syncthreads();
+
+    // 2. offsets = exclusive scan of the counts: each thread owns 4
+    // consecutive experts
+    int v[4], acc = 0;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
         const int e = tid * 4 + u;
-        v[u] = e < E ? counts[e] : 0;
-        run += v[u];
+        v[u] = e < E ? seg_hi[e] : 0;
+        acc += v[u];
     }
-    int incl = run;  // inclusive scan of the per-thread sums within the wave
+    int incl = acc;  // inclusive scan of the per-thread sums within the wave
 #pragma unroll
     for (int d = 1; d < kWave; d <<= 1) {
         const int o = __shfl_up(incl, d);
@@ -246,7 +291,7 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
     }
     if (lane == kWave - 1) wsum[wave] = incl;
     __syncthreads();
-    int base = incl - run;
+    int base = incl - acc;
     for (int w = 0; w < wave; ++w) base += wsum[w];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -254,14 +299,15 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
         if (e < E) off[e] = base;
         base += v[u];
     }
+    const int total = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    const int64_t R = S * K;
     __syncthreads();
-    if ((int)blockIdx.x == sched_wg) {
-        // the tile tables from the segments [off[e], off[e+1]) held here,
-        // clamped to [0, R) as the standalone builder clamps them
-        const int total = wsum[0] + wsum[1] + wsum[2] + wsum[3];
-        for (int e = tid; e < E; e += 256) seg_hi[e] = e + 1 < E ? off[e + 1] : total;
+    if (sched) {
+        // the tile tables from the segments [off[e], off[e] + count) held
+        // here, clamped to [0, R) as the standalone builder clamps them
+        for (int e = tid; e < E; e += kScatThreads) seg_hi[e] = e + 1 < E ? off[e + 1] : total;
         __syncthreads();
-        for (int e = tid; e < E; e += 256) {
+        for (int e = tid; e < E; e += kScatThreads) {
             const int lo = off[e] < (int)R ? off[e] : (int)R;
             const int hi = seg_hi[e];
             off[e] = lo;
@@ -272,34 +318,47 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
         return;
     }
     if (blockIdx.x == 0) {
-        for (int e = tid; e < E; e += 256) offsets[e] = off[e];
-        if (tid == 0) offsets[E] = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+        for (int e = tid; e < E; e += kScatThreads) {
+            offsets[e] = off[e];
+            counts[e] = seg_hi[e];
+        }
+        if (tid == 0) offsets[E] = total;
     }
 
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + tid;
-    if (i >= R) return;
-    const int64_t t = i / K;
-    const int e = topk_idx[i];
-    const int64_t b = t / kRouteTok;
-    const int pos = off[e] + blkbase[b * E + e] + inv_perm[i];
-    if ((uint32_t)pos >= (uint64_t)R) return;  // unreachable for consistent counts
-    perm[pos] = (int32_t)i;
-    inv_perm[i] = pos;
-    if (p_disp != nullptr) p_disp[pos] = prob[i];
+    // 3. the rows of blocks b0 .. b1 - 1, one block at a time: run[e] holds
+    // the rows of e in the blocks before the current one
+    for (int64_t b = b0; b < b1; ++b) {
+        const int64_t r0 = b * kRouteTok * K;
+        const int64_t t1 = (b + 1) * kRouteTok < S ? (b + 1) * kRouteTok : S;
+        for (int64_t i = r0 + tid; i < t1 * K; i += kScatThreads) {
+            const int e = topk_idx[i];
+            if ((unsigned)e >= (unsigned)E) continue;   // unreachable: top-K writes ids below E
+            const int pos = off[e] + run[e] + inv_perm[i];
+            if ((uint64_t)(uint32_t)pos >= (uint64_t)R) continue;  // unreachable for consistent counts
+            perm[pos] = (int32_t)i;
+            inv_perm[i] = pos;
+            if (p_disp != nullptr) p_disp[pos] = prob[i];
+        }
+        if (b + 1 < b1) {
+            __syncthreads();
+            for (int e = tid; e < E; e += kScatThreads) run[e] += blkcnt[(int64_t)e * nbp + b];
+            __syncthreads();
+        }
+    }
 }
 
 size_t route_ws_bytes(int64_t S, int E) {
     const int64_t nblk = (S + kRouteTok - 1) / kRouteTok;
-    return (size_t)(((nblk * E * 4) + 255) / 256 * 256);
+    return (size_t)((cnt_row_bytes(nblk) * E + 255) / 256 * 256);
 }
 
 template <bool SIG>
 static void launch_topk(const float* logits, const float* sel_bias, int64_t S, int E, int K, int32_t* topk_idx,
-                        float* topk_prob, int32_t* blkcnt, int32_t* rank, int nblk, hipStream_t st) {
+                        float* topk_prob, uint8_t* blkcnt, int64_t nbp, int32_t* rank, int nblk, hipStream_t st) {
     const int epl = (E + kWave - 1) / kWave;
 #define MOE_ROUTE_CASE(N)                                                                          \
     hipLaunchKernelGGL((route_topk_kernel<N, SIG>), dim3(nblk), dim3(kRouteThreads), 0, st, logits, \
-                       sel_bias, S, E, K, topk_idx, topk_prob, blkcnt, rank)
+                       sel_bias, S, E, K, topk_idx, topk_prob, blkcnt, nbp, rank)
     if (epl <= 1) MOE_ROUTE_CASE(1);
     else if (epl <= 2) MOE_ROUTE_CASE(2);
     else if (epl <= 4) MOE_ROUTE_CASE(4);
@@ -312,28 +371,27 @@ hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* t
                         float* topk_prob, int32_t* counts, int32_t* offsets, int32_t* perm,
                         int32_t* inv_perm, void* ws, hipStream_t st, bool sigmoid, const float* sel_bias,
                         float* p_disp, void* sched) {
-    const int nblk = (int)((S + kRouteTok - 1) / kRouteTok);
-    int32_t* blkcnt = (int32_t*)ws;
+    const int64_t nblk = (S + kRouteTok - 1) / kRouteTok;
+    const int64_t nbp = cnt_row_bytes(nblk);
+    uint8_t* blkcnt = (uint8_t*)ws;
     if (S > 0) {
         if (sigmoid)
-            launch_topk<true>(logits, sel_bias, S, E, K, topk_idx, topk_prob, blkcnt, inv_perm, nblk, st);
+            launch_topk<true>(logits, sel_bias, S, E, K, topk_idx, topk_prob, blkcnt, nbp, inv_perm, (int)nblk, st);
         else
-            launch_topk<false>(logits, nullptr, S, E, K, topk_idx, topk_prob, blkcnt, inv_perm, nblk, st);
+            launch_topk<false>(logits, nullptr, S, E, K, topk_idx, topk_prob, blkcnt, nbp, inv_perm, (int)nblk, st);
         const hipError_t e1 = launch_check(st);
         if (e1 != hipSuccess) return e1;
     }
-    hipLaunchKernelGGL(route_colscan_kernel, dim3((unsigned)((E + kScanCols - 1) / kScanCols)),
-                       dim3(kScanThreads), 0, st, blkcnt, nblk, E, counts);
-    const hipError_t e2 = launch_check(st);
-    if (e2 != hipSuccess) return e2;
+    // at least one workgroup, so that counts and offsets are written even
+    // for S == 0; with sched, one more (the last) builds the tile tables
+    const int bpw = (int)((nblk + kScatMaxWg - 1) / kScatMaxWg > 1 ? (nblk + kScatMaxWg - 1) / kScatMaxWg : 1);
+    const int64_t nwg = nblk > 0 ? (nblk + bpw - 1) / bpw : 1;
     const int64_t R = S * K;
-    // at least one workgroup, so that offsets are written even for S == 0;
-    // with sched, one more (the last) builds the tile tables
-    const unsigned grid = R > 0 ? grid_for(R, 256) : 1u;
     const SchedPart ss = sched ? sched_part(sched, E, R, false) : SchedPart{};
     const SchedPart sl = sched ? sched_part(sched, E, R, true) : SchedPart{};
-    hipLaunchKernelGGL(route_scatter_kernel, dim3(grid + (sched ? 1u : 0u)), dim3(256), 0, st, topk_idx, blkcnt,
-                       counts, offsets, inv_perm, perm, R, K, E, topk_prob, p_disp, sched ? (int)grid : -1, ss, sl);
+    hipLaunchKernelGGL(route_scatter_kernel, dim3((unsigned)(nwg + (sched ? 1 : 0))), dim3(kScatThreads), 0, st,
+                       topk_idx, blkcnt, nblk, nbp, bpw, counts, offsets, inv_perm, perm, S, K, E, topk_prob, p_disp,
+                       sched ? (int)nwg : -1, ss, sl);
     return launch_check(st);
 }
 

@@ -23,7 +23,9 @@ DEV = "cuda:0"
 # (R, D, F, E, empty experts, skew)
 SHAPES = [(1, 8, 8, 1, 0, 0.0), (100, 16, 24, 3, 0, 0.0), (1000, 264, 200, 5, 1, 0.0),
           (777, 136, 392, 9, 2, 1.5), (4096, 256, 512, 8, 0, 0.0), (300, 512, 128, 64, 20, 0.0),
-          (2500, 192, 64, 2, 0, 2.0)]
+          (2500, 192, 64, 2, 0, 2.0),
+          # widths that 384-column tiles cover with less padding (up: F; down: D)
+          (1500, 392, 1096, 7, 1, 1.0), (900, 2688, 360, 5, 1, 0.0), (640, 200, 360, 6, 1, 0.5)]
 
 
 def _sign_weights(E, a, b, seed, density):
