@@ -84,6 +84,24 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     return max(max(a, b), max(c, d));
 }
 
+// Sum of v over the 64 lanes (all active), wave-uniform, in a fixed order:
+// sums within rows of 16 lanes (pairs, quads, half rows, rows), then
+// row_bcast:15 into rows 1 and 3 and row_bcast:31 into rows 2 and 3 (lanes
+// of rows outside a broadcast's row mask add 0), so lane 63 holds the total.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_add(float x) {
+    return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROWS, 0xf, false));
+}
+__device__ __forceinline__ float wave_sum_f32(float v) {
+    v = dpp_add<0xB1, 0xf>(v);    // quad_perm 1,0,3,2
+    v = dpp_add<0x4E, 0xf>(v);    // quad_perm 2,3,0,1
+    v = dpp_add<0x141, 0xf>(v);   // row_half_mirror
+    v = dpp_add<0x140, 0xf>(v);   // row_mirror
+    v = dpp_add<0x142, 0xa>(v);   // row_bcast:15 into rows 1 and 3
+    v = dpp_add<0x143, 0xc>(v);   // row_bcast:31 into rows 2 and 3
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
 // SIG false: selection by the logits, weights = softmax over the K picked.
 // SIG true: selection by sigmoid(logit) + sel_bias (bias may be null), weights
 // = the picked sigmoids over their sum; the bias only steers selection.
@@ -98,13 +116,16 @@ __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
     const int64_t t_base = (int64_t)blockIdx.x * kRouteTok;
     for (int e = tid; e < E; e += kRouteThreads) mask[e] = 0u;
 
-    // this wave's tokens t_base + wave*8 + j: every score code loaded up front
+    // this wave's tokens t_base + wave * kTokPerWave + j: every score loaded
+    // up front, all loads issued before any is used (entries past S or E
+    // read element 0, which exists, and are masked afterwards)
     uint32_t code[kTokPerWave][EPL];
-    float bias[EPL];
+    float l[kTokPerWave][EPL], bias[EPL];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
         const int e = lane + kWave * i;
-        bias[i] = (SIG && sel_bias != nullptr && e < E) ? sel_bias[e] : 0.f;
+        bias[i] = 0.f;
+        if constexpr (SIG) bias[i] = sel_bias != nullptr ? sel_bias[e < E ? e : 0] : 0.f;
     }
 #pragma unroll
     for (int j = 0; j < kTokPerWave; ++j) {
@@ -112,12 +133,17 @@ __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
 #pragma unroll
         for (int i = 0; i < EPL; ++i) {
             const int e = lane + kWave * i;
-            if (t < S && e < E) {
-                const float l = logits[t * E + e];
-                code[j][i] = score_code(SIG ? sigmoid_f32(l) + bias[i] : l);
-            } else {
-                code[j][i] = 0u;
-            }
+            l[j][i] = logits[(t < S && e < E) ? t * E + e : 0];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < kTokPerWave; ++j) {
+        const int64_t t = t_base + wave * kTokPerWave + j;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) {
+            const int e = lane + kWave * i;
+            const uint32_t c = score_code(SIG ? sigmoid_f32(l[j][i]) + bias[i] : l[j][i]);
+            code[j][i] = (t < S && e < E) ? c : 0u;
         }
     }
     __syncthreads();
@@ -160,17 +186,14 @@ __global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
         const int jt = wave * kTokPerWave + j;
         const int64_t t = t_base + jt;
         if (t >= S) break;
-        const float my_s = code_score(my_c[j]);
         float z;
         if constexpr (SIG) {
             z = (lane < K) ? sigmoid_f32(logits[t * E + my_e[j]]) : 0.f;
         } else {
-            const float s0 = __shfl(my_s, 0);
-            z = (lane < K) ? expf(my_s - s0) : 0.f;
+            const float s0 = code_score((uint32_t)__builtin_amdgcn_readlane((int)my_c[j], 0));
+            z = (lane < K) ? expf(code_score(my_c[j]) - s0) : 0.f;
         }
-        float sum = z;
-#pragma unroll
-        for (int msk = 32; msk > 0; msk >>= 1) sum += __shfl_xor(sum, msk);
+        const float sum = wave_sum_f32(z);
         if (lane < K) {
             topk_idx[t * K + lane] = my_e[j];
             topk_prob[t * K + lane] = z / sum;
@@ -216,23 +239,82 @@ __device__ __forceinline__ uint32_t bytes_sum_below(const uint4& c, int lim) {
     return s;
 }
 
-// Workgroup w takes token blocks [w * bpw, min((w + 1) * bpw, nblk)).
+// Chunks c = c0, c0 + step, ... < nchunk of one count row: tot += all their
+// bytes, pre += the bytes of blocks before chunk cb0's byte lim0.  Eight
+// chunks are loaded before any is summed, so the loads overlap.
+__device__ __forceinline__ void row_sums(const uint8_t* row8, int64_t c0, int step, int64_t nchunk, int64_t cb0,
+                                         int lim0, uint32_t& tot, uint32_t& pre) {
+    constexpr int kU = 8;
+    const uint4* row = (const uint4*)row8;
+    for (int64_t cb = c0; cb < nchunk; cb += (int64_t)kU * step) {
+        uint4 v[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int64_t c = cb + (int64_t)u * step;
+            v[u] = c < nchunk ? row[c] : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int64_t c = cb + (int64_t)u * step;
+            const uint32_t s = bytes_sum(v[u]);
+            tot += s;
+            pre += c < cb0 ? s : (c == cb0 ? bytes_sum_below(v[u], lim0) : 0u);
+        }
+    }
+}
+
+// Inclusive prefix sums out[e] = v(0) + ... + v(e) over e < E <= 1024, by a
+// workgroup of kScatThreads threads (4 consecutive entries each); returns the
+// total.  wsum is LDS scratch of 4 entries; out may be read after the call.
+template <class V>
+__device__ __forceinline__ int wg_incl_scan(V v, int E, int32_t* out, int32_t* wsum) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int x[4], acc = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int e = tid * 4 + u;
+        x[u] = e < E ? v(e) : 0;
+        acc += x[u];
+    }
+    int incl = acc;  // inclusive scan of the per-thread sums within the wave
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const int o = __shfl_up(incl, d);
+        if (lane >= d) incl += o;
+    }
+    __syncthreads();   // earlier readers of wsum are done
+    if (lane == kWave - 1) wsum[wave] = incl;
+    __syncthreads();
+    int base = incl - acc;
+    for (int w = 0; w < wave; ++w) base += wsum[w];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int e = tid * 4 + u;
+        base += x[u];
+        if (e < E) out[e] = base;
+    }
+    const int total = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    __syncthreads();
+    return total;
+}
+
+// Workgroup w takes token blocks [w * bpw, min((w + 1) * bpw, nblk)).  With
+// the tile tables requested (sched_small.tiles != null), every workgroup also
+// writes its slice of both tables.
 __global__ __launch_bounds__(kScatThreads) void route_scatter_kernel(
     const int32_t* __restrict__ topk_idx, const uint8_t* __restrict__ blkcnt, int64_t nblk, int64_t nbp, int bpw,
     int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int32_t* __restrict__ inv_perm,
     int32_t* __restrict__ perm, int64_t S, int K, int E, const float* __restrict__ prob,
-    float* __restrict__ p_disp, int sched_wg, SchedPart sched_small, SchedPart sched_large) {
-    __shared__ int32_t off[1024], run[1024], seg_hi[1024];
+    float* __restrict__ p_disp, SchedPart sched_small, SchedPart sched_large) {
+    __shared__ int32_t cnt[1024], off[1024], run[1024], seg_lo[1024], seg_hi[1024];
     __shared__ int32_t wsum[4];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const bool sched = (int)blockIdx.x == sched_wg;
-    const int64_t b0 = sched ? 0 : (int64_t)blockIdx.x * bpw;
-    const int64_t b1 = sched ? 0 : (b0 + bpw < nblk ? b0 + bpw : nblk);
+    const int tid = threadIdx.x;
+    const int64_t b0 = (int64_t)blockIdx.x * bpw;
+    const int64_t b1 = b0 + bpw < nblk ? b0 + bpw : nblk;
 
-    // 1. per expert: rows in all blocks (-> seg_hi for now) and in blocks
-    // before b0 (-> run).  tpe adjacent lanes share an expert's row (E <=
-    // 128) and combine their sums with xor shuffles; above 128 experts each
-    // lane takes whole rows.
+    // 1. per expert: rows in all blocks (cnt) and in blocks before b0 (run).
+    // tpe adjacent lanes share an expert's row (E <= 128) and combine their
+    // sums with xor shuffles; above 128 experts each lane takes whole rows.
     const int64_t nchunk = nbp / 16;
     const int64_t cb0 = b0 / 16;
     const int lim0 = (int)(b0 % 16);
@@ -241,88 +323,60 @@ __global__ __launch_bounds__(kScatThreads) void route_scatter_kernel(
         while (tpe * E > kScatThreads) tpe >>= 1;
         const int e = tid / tpe, part = tid % tpe;
         uint32_t tot = 0, pre = 0;
-        if (e < E) {
-            const uint4* row = (const uint4*)(blkcnt + (int64_t)e * nbp);
-            for (int64_t c = part; c < nchunk; c += tpe) {
-                const uint4 v = row[c];
-                const uint32_t s = bytes_sum(v);
-                tot += s;
-                pre += c < cb0 ? s : (c == cb0 ? bytes_sum_below(v, lim0) : 0u);
-            }
-        }
+        if (e < E) row_sums(blkcnt + (int64_t)e * nbp, part, tpe, nchunk, cb0, lim0, tot, pre);
         for (int m = 1; m < tpe; m <<= 1) {
             tot += __shfl_xor(tot, m);
             pre += __shfl_xor(pre, m);
         }
         if (e < E && part == 0) {
-            seg_hi[e] = (int32_t)tot;
+            cnt[e] = (int32_t)tot;
             run[e] = (int32_t)pre;
         }
     } else {
         for (int e = tid; e < E; e += kScatThreads) {
-            const uint4* row = (const uint4*)(blkcnt + (int64_t)e * nbp);
             uint32_t tot = 0, pre = 0;
-            for (int64_t c = 0; c < nchunk; ++c) {
-                const uint4 v = row[c];
-                const uint32_t s = bytes_sum(v);
-                tot += s;
-                pre += c < cb0 ? s : (c == cb0 ? bytes_sum_below(v, lim0) : 0u);
-            }
-            seg_hi[e] = (int32_t)tot;
+            row_sums(blkcnt + (int64_t)e * nbp, 0, 1, nchunk, cb0, lim0, tot, pre);
+            cnt[e] = (int32_t)tot;
             run[e] = (int32_t)pre;
         }
     }
     __syncthreads();
 
-    // 2. offsets = exclusive scan of the counts: each thread owns 4
-    // consecutive experts
-    int v[4], acc = 0;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int e = tid * 4 + u;
-        v[u] = e < E ? seg_hi[e] : 0;
-        acc += v[u];
-    }
-    int incl = acc;  // inclusive scan of the per-thread sums within the wave
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        const int o = __shfl_up(incl, d);
-        if (lane >= d) incl += o;
-    }
-    if (lane == kWave - 1) wsum[wave] = incl;
-    __syncthreads();
-    int base = incl - acc;
-    for (int w = 0; w < wave; ++w) base += wsum[w];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int e = tid * 4 + u;
-        if (e < E) off[e] = base;
-        base += v[u];
-    }
-    const int total = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    // 2. offsets = exclusive scan of the counts (seg_hi holds the inclusive one)
+    const int total = wg_incl_scan([&](int e) { return cnt[e]; }, E, seg_hi, wsum);
+    for (int e = tid; e < E; e += kScatThreads) off[e] = seg_hi[e] - cnt[e];
     const int64_t R = S * K;
+    if (blockIdx.x == 0) {
+        for (int e = tid; e < E; e += kScatThreads) {
+            offsets[e] = seg_hi[e] - cnt[e];
+            counts[e] = cnt[e];
+        }
+        if (tid == 0) offsets[E] = total;
+    }
     __syncthreads();
-    if (sched) {
-        // the tile tables from the segments [off[e], off[e] + count) held
-        // here, clamped to [0, R) as the standalone builder clamps them
-        for (int e = tid; e < E; e += kScatThreads) seg_hi[e] = e + 1 < E ? off[e + 1] : total;
-        __syncthreads();
+
+    // the tile tables: segments clamped to [0, R) as the standalone builder
+    // clamps them; each height's tile counts scanned into cnt, then this
+    // workgroup's slice of the table
+    if (sched_small.tiles != nullptr) {
         for (int e = tid; e < E; e += kScatThreads) {
             const int lo = off[e] < (int)R ? off[e] : (int)R;
             const int hi = seg_hi[e];
-            off[e] = lo;
+            seg_lo[e] = lo;
             seg_hi[e] = hi < lo ? lo : (hi > (int)R ? (int)R : hi);
         }
         __syncthreads();
-        build_tile_schedule_lds(off, seg_hi, E, sched_small, sched_large);
-        return;
-    }
-    if (blockIdx.x == 0) {
-        for (int e = tid; e < E; e += kScatThreads) {
-            offsets[e] = off[e];
-            counts[e] = seg_hi[e];
+        const int nwg = (int)gridDim.x;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const SchedPart& sp = h ? sched_large : sched_small;
+            const int bm = kSchedBM[h];
+            wg_incl_scan([&](int e) { return (seg_hi[e] - seg_lo[e] + bm - 1) / bm; }, E, cnt, wsum);
+            const int per = (sp.max_tiles + nwg - 1) / nwg;
+            const int mt0 = (int)blockIdx.x * per;
+            sched_fill_slice(seg_lo, seg_hi, cnt, E, bm, sp, mt0, mt0 + per, blockIdx.x == 0);
+            __syncthreads();   // cnt is rescanned for the next height
         }
-        if (tid == 0) offsets[E] = total;
     }
 
     // 3. the rows of blocks b0 .. b1 - 1, one block at a time: run[e] holds
@@ -383,15 +437,14 @@ hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* t
         if (e1 != hipSuccess) return e1;
     }
     // at least one workgroup, so that counts and offsets are written even
-    // for S == 0; with sched, one more (the last) builds the tile tables
+    // for S == 0
     const int bpw = (int)((nblk + kScatMaxWg - 1) / kScatMaxWg > 1 ? (nblk + kScatMaxWg - 1) / kScatMaxWg : 1);
     const int64_t nwg = nblk > 0 ? (nblk + bpw - 1) / bpw : 1;
     const int64_t R = S * K;
     const SchedPart ss = sched ? sched_part(sched, E, R, false) : SchedPart{};
     const SchedPart sl = sched ? sched_part(sched, E, R, true) : SchedPart{};
-    hipLaunchKernelGGL(route_scatter_kernel, dim3((unsigned)(nwg + (sched ? 1 : 0))), dim3(kScatThreads), 0, st,
-                       topk_idx, blkcnt, nblk, nbp, bpw, counts, offsets, inv_perm, perm, S, K, E, topk_prob, p_disp,
-                       sched ? (int)nwg : -1, ss, sl);
+    hipLaunchKernelGGL(route_scatter_kernel, dim3((unsigned)nwg), dim3(kScatThreads), 0, st, topk_idx, blkcnt, nblk,
+                       nbp, bpw, counts, offsets, inv_perm, perm, S, K, E, topk_prob, p_disp, ss, sl);
     return launch_check(st);
 }
 

@@ -98,6 +98,39 @@ __device__ __forceinline__ void sched_fill_part(const int32_t* seg_lo, const int
     __syncthreads();   // cnt is reused by the next part
 }
 
+// Entries [mt0, mt1) of one tile height's table (and, with starts, its
+// mtile_start array) from segments seg_lo / seg_hi and the inclusive prefix
+// sums incl[e] of their tile counts, all in LDS: lets every workgroup of a
+// launch write its own slice.
+__device__ __forceinline__ void sched_fill_slice(const int32_t* seg_lo, const int32_t* seg_hi, const int32_t* incl,
+                                                 int E, int BMr, const SchedPart& sp, int mt0, int mt1,
+                                                 bool starts) {
+    const int tid = threadIdx.x, nt = blockDim.x;
+    if (starts) {
+        for (int e = tid; e < E; e += nt) sp.mtile_start[e + 1] = incl[e] < sp.max_tiles ? incl[e] : sp.max_tiles;
+        if (tid == 0) sp.mtile_start[0] = 0;
+    }
+    const int total = incl[E - 1] < sp.max_tiles ? incl[E - 1] : sp.max_tiles;
+    mt1 = mt1 < sp.max_tiles ? mt1 : sp.max_tiles;
+    for (int mt = mt0 + tid; mt < mt1; mt += nt) {
+        int4 v = make_int4(-1, 0, 0, 0);
+        if (mt < total) {
+            int a = 0, b = E - 1;  // first e with incl[e] > mt
+            while (a < b) {
+                const int m = (a + b) >> 1;
+                if (incl[m] > mt) b = m; else a = m + 1;
+            }
+            const int first = a ? incl[a - 1] : 0;
+            const int row0 = seg_lo[a] + (mt - first) * BMr;
+            const int row_end = row0 + BMr < seg_hi[a] ? row0 + BMr : seg_hi[a];
+            const int g0 = first + (mt - first) / kSchedGroupM * kSchedGroupM;
+            const int gs = incl[a] - g0 < kSchedGroupM ? incl[a] - g0 : kSchedGroupM;
+            v = make_int4(a, row0, row_end, 16 * g0 + gs);
+        }
+        sp.tiles[mt] = v;
+    }
+}
+
 // Both tile heights' tables from segment bounds a workgroup already holds in
 // LDS (seg_lo, seg_hi: E entries each, within [0, R), monotone).
 __device__ __forceinline__ void build_tile_schedule_lds(const int32_t* seg_lo, const int32_t* seg_hi, int E,
