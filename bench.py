@@ -295,7 +295,7 @@ def route_sweep(_lib, s, reps, stream, dev):
     """The route (top-K, histogram and scan, permutation) alone over token
     counts S = 1K .. 128K with the workload's E and K: duration and
     algorithmic bytes (read S*E*4, write R*16 + (2E+1)*4) per S, to show where
-    its three launches stop being latency-bound."""
+    its two launches stop being latency-bound."""
     import torch
     out = []
     for S in (1 << k for k in range(10, 18)):

@@ -74,7 +74,7 @@ def test_route_full_size(name):
 
 @pytest.mark.parametrize("S,E,K", [(70000, 128, 4), (20000, 1024, 2)])
 def test_route_large_block_counts(S, E, K):
-    """Thousands of token blocks (the column scan walks long chunks), bit-exact
+    """Thousands of token blocks (several per scatter workgroup), bit-exact
     like the rest."""
     _route_and_compare(make_logits("normal", S, E, seed=S + E), K)
 
