@@ -28,10 +28,11 @@
 //                  gives perm and inv_perm for the rows of its blocks.  In the
 //                  fused layer it also writes each routed row's probability
 //                  p_disp[pos] (the probability half of the dispatch payload),
-//                  and one extra workgroup builds the grouped GEMM's tile
-//                  tables from the offsets it holds, so the layer needs no
-//                  dispatch launch.  Every workgroup reads the whole count
-//                  matrix, so the blocks are dealt to at most 256 workgroups.
+//                  and eight extra workgroups each write a slice of the
+//                  grouped GEMM's tile tables from the offsets they hold, so
+//                  the layer needs no dispatch launch.  Every workgroup reads
+//                  the whole count matrix, so the blocks are dealt to at most
+//                  256 workgroups.
 //
 // No step depends on the order in which atomics land (the LDS OR is
 // commutative and ranks come from popcounts), so the permutation is
@@ -298,19 +299,21 @@ __device__ __forceinline__ int wg_incl_scan(V v, int E, int32_t* out, int32_t* w
     return total;
 }
 
-// Workgroup w takes token blocks [w * bpw, min((w + 1) * bpw, nblk)).  With
-// the tile tables requested (sched_small.tiles != null), every workgroup also
-// writes its slice of both tables.
+// Workgroup w < nrow takes token blocks [w * bpw, min((w + 1) * bpw, nblk)).
+// With the tile tables requested (sched_small.tiles != null), the workgroups
+// nrow .. gridDim.x - 1 each write one slice of both tables instead, while
+// the others place rows.
 __global__ __launch_bounds__(kScatThreads) void route_scatter_kernel(
     const int32_t* __restrict__ topk_idx, const uint8_t* __restrict__ blkcnt, int64_t nblk, int64_t nbp, int bpw,
-    int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int32_t* __restrict__ inv_perm,
+    int nrow, int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int32_t* __restrict__ inv_perm,
     int32_t* __restrict__ perm, int64_t S, int K, int E, const float* __restrict__ prob,
     float* __restrict__ p_disp, SchedPart sched_small, SchedPart sched_large) {
     __shared__ int32_t cnt[1024], off[1024], run[1024], seg_lo[1024], seg_hi[1024];
     __shared__ int32_t wsum[4];
     const int tid = threadIdx.x;
-    const int64_t b0 = (int64_t)blockIdx.x * bpw;
-    const int64_t b1 = b0 + bpw < nblk ? b0 + bpw : nblk;
+    const bool tab = (int)blockIdx.x >= nrow;
+    const int64_t b0 = tab ? 0 : (int64_t)blockIdx.x * bpw;
+    const int64_t b1 = tab ? 0 : (b0 + bpw < nblk ? b0 + bpw : nblk);
 
     // 1. per expert: rows in all blocks (cnt) and in blocks before b0 (run).
     // tpe adjacent lanes share an expert's row (E <= 128) and combine their
@@ -358,7 +361,7 @@ __global__ __launch_bounds__(kScatThreads) void route_scatter_kernel(
     // the tile tables: segments clamped to [0, R) as the standalone builder
     // clamps them; each height's tile counts scanned into cnt, then this
     // workgroup's slice of the table
-    if (sched_small.tiles != nullptr) {
+    if (tab) {
         for (int e = tid; e < E; e += kScatThreads) {
             const int lo = off[e] < (int)R ? off[e] : (int)R;
             const int hi = seg_hi[e];
@@ -366,17 +369,18 @@ __global__ __launch_bounds__(kScatThreads) void route_scatter_kernel(
             seg_hi[e] = hi < lo ? lo : (hi > (int)R ? (int)R : hi);
         }
         __syncthreads();
-        const int nwg = (int)gridDim.x;
+        const int ntab = (int)gridDim.x - nrow, slice = (int)blockIdx.x - nrow;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const SchedPart& sp = h ? sched_large : sched_small;
             const int bm = kSchedBM[h];
             wg_incl_scan([&](int e) { return (seg_hi[e] - seg_lo[e] + bm - 1) / bm; }, E, cnt, wsum);
-            const int per = (sp.max_tiles + nwg - 1) / nwg;
-            const int mt0 = (int)blockIdx.x * per;
-            sched_fill_slice(seg_lo, seg_hi, cnt, E, bm, sp, mt0, mt0 + per, blockIdx.x == 0);
+            const int per = (sp.max_tiles + ntab - 1) / ntab;
+            const int mt0 = slice * per;
+            sched_fill_slice(seg_lo, seg_hi, cnt, E, bm, sp, mt0, mt0 + per, slice == 0);
             __syncthreads();   // cnt is rescanned for the next height
         }
+        return;
     }
 
     // 3. the rows of blocks b0 .. b1 - 1, one block at a time: run[e] holds
@@ -443,8 +447,11 @@ hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* t
     const int64_t R = S * K;
     const SchedPart ss = sched ? sched_part(sched, E, R, false) : SchedPart{};
     const SchedPart sl = sched ? sched_part(sched, E, R, true) : SchedPart{};
-    hipLaunchKernelGGL(route_scatter_kernel, dim3((unsigned)nwg), dim3(kScatThreads), 0, st, topk_idx, blkcnt, nblk,
-                       nbp, bpw, counts, offsets, inv_perm, perm, S, K, E, topk_prob, p_disp, ss, sl);
+    // with the tile tables, kSchedWg more workgroups each write a slice of them
+    constexpr int kSchedWg = 8;
+    const int64_t grid = nwg + (sched ? kSchedWg : 0);
+    hipLaunchKernelGGL(route_scatter_kernel, dim3((unsigned)grid), dim3(kScatThreads), 0, st, topk_idx, blkcnt, nblk,
+                       nbp, bpw, (int)nwg, counts, offsets, inv_perm, perm, S, K, E, topk_prob, p_disp, ss, sl);
     return launch_check(st);
 }
 
