@@ -72,10 +72,16 @@ def test_route_full_size(name):
         assert (npi(out["counts"]) == 0).sum() >= 4     # masked experts receive nothing
 
 
-@pytest.mark.parametrize("S,E,K", [(70000, 128, 4), (20000, 1024, 2)])
+@pytest.mark.parametrize("S,E,K", [(70000, 128, 4), (20000, 1024, 2),
+                                   # 257 blocks: the first count with two blocks per scatter workgroup
+                                   (8220, 64, 6),
+                                   # 513 blocks, more than 128 experts (whole count rows per lane)
+                                   (16401, 200, 8),
+                                   # 1,032 blocks, 32 lanes sharing each expert's count row
+                                   (33001, 8, 2)])
 def test_route_large_block_counts(S, E, K):
-    """Thousands of token blocks (several per scatter workgroup), bit-exact
-    like the rest."""
+    """Hundreds to thousands of token blocks (several per scatter workgroup,
+    a ragged last one), bit-exact like the rest."""
     _route_and_compare(make_logits("normal", S, E, seed=S + E), K)
 
 
