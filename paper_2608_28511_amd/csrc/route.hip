@@ -18,14 +18,19 @@
 //                  LDS bitmask per expert that gives each (token, slot) its
 //                  rank among the block's rows of that expert and the block's
 //                  per-expert count, stored as one byte (at most 32) in an
-//                  expert-major count matrix [E][blocks].
+//                  expert-major count matrix [E][blocks].  For E <= 64 and
+//                  K <= 16, route_topk_rows_kernel takes one token per row of
+//                  16 lanes instead (four tokens per wave, every reduction
+//                  a DPP step within the row).
 //   route_scatter  each workgroup first sums, for every expert, its row of
 //                  the count matrix in full (counts, then offsets by an
 //                  exclusive scan in LDS; the first workgroup stores both)
 //                  and up to its own first token block (the expert's rows in
 //                  earlier blocks), four bytes per dot-product instruction;
 //                  then pos = offsets[e] + rows in earlier blocks + rank
-//                  gives perm and inv_perm for the rows of its blocks.  In the
+//                  gives perm and inv_perm for the rows of its blocks (all
+//                  of them in one pass when their per-block prefixes fit in
+//                  LDS).  In the
 //                  fused layer it also writes each routed row's probability
 //                  p_disp[pos] (the probability half of the dispatch payload),
 //                  and eight extra workgroups each write a slice of the
@@ -48,6 +53,7 @@ constexpr int kRouteThreads = 1024;
 constexpr int kTokPerWave = kRouteTok / (kRouteThreads / kWave);  // 2
 constexpr int kScatThreads = 256;
 constexpr int kScatMaxWg = 256;   // scatter workgroups (each reads the whole count matrix)
+constexpr int kPfxInts = 8192;    // LDS per-block prefixes of a scatter workgroup (blocks x experts)
 
 // Row length in bytes of the expert-major count matrix: the token blocks
 // rounded up to whole 16-byte chunks (the padding bytes are zero).
@@ -264,6 +270,126 @@ __device__ __forceinline__ void row_sums(const uint8_t* row8, int64_t c0, int st
     }
 }
 
+// Row form for E <= 64 and K <= 16: one token per row of 16 lanes, so a
+// wave holds four tokens and one instruction stream serves all four.  Lane r
+// of a row holds experts r + 16 i (slot i < EPR); the row maximum and the
+// lowest expert id holding it are both DPP reductions within the row (no
+// readlane, no scalar chain).  Same selection order, same block counts and
+// ranks as route_topk_kernel.
+constexpr int kRowThreads = kRouteTok * 16;   // 512: 8 waves of 4 tokens
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xf, 0xf, false);
+}
+__device__ __forceinline__ uint32_t row_max_u32(uint32_t v) {
+    v = max(v, dpp_u32<0xB1>(v));    // quad_perm 1,0,3,2
+    v = max(v, dpp_u32<0x4E>(v));    // quad_perm 2,3,0,1
+    v = max(v, dpp_u32<0x141>(v));   // row_half_mirror
+    return max(v, dpp_u32<0x140>(v));   // row_mirror
+}
+__device__ __forceinline__ uint32_t row_min_u32(uint32_t v) {
+    v = min(v, dpp_u32<0xB1>(v));
+    v = min(v, dpp_u32<0x4E>(v));
+    v = min(v, dpp_u32<0x141>(v));
+    return min(v, dpp_u32<0x140>(v));
+}
+__device__ __forceinline__ float row_sum_f32(float v) {
+    v = dpp_add<0xB1, 0xf>(v);
+    v = dpp_add<0x4E, 0xf>(v);
+    v = dpp_add<0x141, 0xf>(v);
+    return dpp_add<0x140, 0xf>(v);
+}
+
+template <int EPR, bool SIG>
+__global__ __launch_bounds__(kRowThreads) void route_topk_rows_kernel(
+    const float* __restrict__ logits, const float* __restrict__ sel_bias, int64_t S, int E, int K,
+    int32_t* __restrict__ topk_idx, float* __restrict__ topk_prob, uint8_t* __restrict__ blkcnt,
+    int64_t nbp, int32_t* __restrict__ rank_out) {
+    __shared__ uint32_t mask[64];
+    __shared__ int16_t sel[kRouteTok][16];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int r = lane & 15, jt = wave * 4 + (lane >> 4);
+    const int64_t t_base = (int64_t)blockIdx.x * kRouteTok;
+    const int64_t t = t_base + jt;
+    if (tid < 64) mask[tid] = 0u;
+
+    // every score loaded before any is used (entries past S or E read
+    // element 0, which exists, and are masked afterwards)
+    float l[EPR], bias[EPR];
+    uint32_t code[EPR];
+#pragma unroll
+    for (int i = 0; i < EPR; ++i) {
+        const int e = r + 16 * i;
+        bias[i] = 0.f;
+        if constexpr (SIG) bias[i] = sel_bias != nullptr ? sel_bias[e < E ? e : 0] : 0.f;
+        l[i] = logits[(t < S && e < E) ? t * E + e : 0];
+    }
+#pragma unroll
+    for (int i = 0; i < EPR; ++i) {
+        const int e = r + 16 * i;
+        const uint32_t c = score_code(SIG ? sigmoid_f32(l[i]) + bias[i] : l[i]);
+        code[i] = (t < S && e < E) ? c : 0u;
+    }
+    __syncthreads();
+
+    // K rounds: the row's maximum code (never a cleared one: K <= E), the
+    // lowest expert id holding it (a lane's lowest matching slot, then the
+    // row minimum), and clearing it.  Lane k of the row keeps the k-th pick.
+    int my_e = 0;
+    uint32_t my_c = 0u;
+    for (int k = 0; k < K; ++k) {
+        uint32_t m = code[0];
+#pragma unroll
+        for (int i = 1; i < EPR; ++i) m = max(m, code[i]);
+        m = row_max_u32(m);
+        uint32_t cand = 0xffffu;
+#pragma unroll
+        for (int i = EPR - 1; i >= 0; --i) cand = code[i] == m ? (uint32_t)(r + 16 * i) : cand;
+        const int e_sel = (int)row_min_u32(cand);
+        const bool own = r == (e_sel & 15);
+#pragma unroll
+        for (int i = 0; i < EPR; ++i)
+            if (own && i == (e_sel >> 4)) code[i] = 0u;
+        if (r == k) {
+            my_e = e_sel;
+            my_c = m;
+        }
+    }
+
+    float z;
+    if constexpr (SIG) {
+        z = (r < K && t < S) ? sigmoid_f32(logits[t * E + my_e]) : 0.f;
+    } else {
+        const float s0 = code_score((uint32_t)__shfl((int)my_c, lane & 48));
+        z = r < K ? expf(code_score(my_c) - s0) : 0.f;
+    }
+    const float sum = row_sum_f32(z);
+    if (r < K && t < S) {
+        topk_idx[t * K + r] = my_e;
+        topk_prob[t * K + r] = z / sum;
+        sel[jt][r] = (int16_t)my_e;
+        atomicOr(&mask[my_e], 1u << jt);
+    }
+    __syncthreads();
+
+    const int n_tok = (int)((S - t_base) < kRouteTok ? (S - t_base) : kRouteTok);
+    for (int q = tid; q < n_tok * K; q += kRowThreads) {
+        const int j = q / K, k = q - j * K;
+        const int e = sel[j][k];
+        rank_out[(t_base + j) * K + k] = __popc(mask[e] & ((1u << j) - 1u));
+    }
+    for (int e = tid; e < E; e += kRowThreads)
+        blkcnt[(int64_t)e * nbp + blockIdx.x] = (uint8_t)__popc(mask[e]);
+    // the last block also zeroes every row's padding bytes
+    const int64_t nblk = gridDim.x;
+    if ((int64_t)blockIdx.x == nblk - 1) {
+        const int pad = (int)(nbp - nblk);
+        for (int q = tid; q < E * pad; q += kRowThreads)
+            blkcnt[(int64_t)(q / pad) * nbp + nblk + q % pad] = 0;
+    }
+}
+
 // Inclusive prefix sums out[e] = v(0) + ... + v(e) over e < E <= 1024, by a
 // workgroup of kScatThreads threads (4 consecutive entries each); returns the
 // total.  wsum is LDS scratch of 4 entries; out may be read after the call.
@@ -309,6 +435,7 @@ __global__ __launch_bounds__(kScatThreads) void route_scatter_kernel(
     int32_t* __restrict__ perm, int64_t S, int K, int E, const float* __restrict__ prob,
     float* __restrict__ p_disp, SchedPart sched_small, SchedPart sched_large) {
     __shared__ int32_t cnt[1024], off[1024], run[1024], seg_lo[1024], seg_hi[1024];
+    __shared__ int32_t pfx[kPfxInts];
     __shared__ int32_t wsum[4];
     const int tid = threadIdx.x;
     const bool tab = (int)blockIdx.x >= nrow;
@@ -383,8 +510,33 @@ __global__ __launch_bounds__(kScatThreads) void route_scatter_kernel(
         return;
     }
 
-    // 3. the rows of blocks b0 .. b1 - 1, one block at a time: run[e] holds
-    // the rows of e in the blocks before the current one
+    // 3. the rows of blocks b0 .. b1 - 1.  When their per-block prefixes fit
+    // in LDS (pfx[(b - b0) * E + e] = rows of e in blocks before b), all rows
+    // are placed in one pass; else one block at a time, run[e] holding the
+    // rows of e in the blocks before the current one.
+    const int nb = (int)(b1 - b0);
+    if (nb > 1 && nb * E <= kPfxInts) {
+        for (int e = tid; e < E; e += kScatThreads) {
+            int acc = run[e];
+            for (int q = 0; q < nb; ++q) {
+                pfx[q * E + e] = acc;
+                acc += blkcnt[(int64_t)e * nbp + b0 + q];
+            }
+        }
+        __syncthreads();
+        const int64_t t1 = b1 * kRouteTok < S ? b1 * kRouteTok : S;
+        for (int64_t i = b0 * kRouteTok * K + tid; i < t1 * K; i += kScatThreads) {
+            const int e = topk_idx[i];
+            if ((unsigned)e >= (unsigned)E) continue;   // unreachable: top-K writes ids below E
+            const int q = (int)(i / K / kRouteTok - b0);
+            const int pos = off[e] + pfx[q * E + e] + inv_perm[i];
+            if ((uint64_t)(uint32_t)pos >= (uint64_t)R) continue;  // unreachable for consistent counts
+            perm[pos] = (int32_t)i;
+            inv_perm[i] = pos;
+            if (p_disp != nullptr) p_disp[pos] = prob[i];
+        }
+        return;
+    }
     for (int64_t b = b0; b < b1; ++b) {
         const int64_t r0 = b * kRouteTok * K;
         const int64_t t1 = (b + 1) * kRouteTok < S ? (b + 1) * kRouteTok : S;
@@ -413,6 +565,17 @@ size_t route_ws_bytes(int64_t S, int E) {
 template <bool SIG>
 static void launch_topk(const float* logits, const float* sel_bias, int64_t S, int E, int K, int32_t* topk_idx,
                         float* topk_prob, uint8_t* blkcnt, int64_t nbp, int32_t* rank, int nblk, hipStream_t st) {
+    if (E <= 64 && K <= 16) {
+        const int epr = (E + 15) / 16;
+#define MOE_ROUTE_ROWS(N)                                                                           \
+    hipLaunchKernelGGL((route_topk_rows_kernel<N, SIG>), dim3(nblk), dim3(kRowThreads), 0, st, logits, \
+                       sel_bias, S, E, K, topk_idx, topk_prob, blkcnt, nbp, rank)
+        if (epr <= 1) MOE_ROUTE_ROWS(1);
+        else if (epr <= 2) MOE_ROUTE_ROWS(2);
+        else MOE_ROUTE_ROWS(4);
+#undef MOE_ROUTE_ROWS
+        return;
+    }
     const int epl = (E + kWave - 1) / kWave;
 #define MOE_ROUTE_CASE(N)                                                                          \
     hipLaunchKernelGGL((route_topk_kernel<N, SIG>), dim3(nblk), dim3(kRouteThreads), 0, st, logits, \
