@@ -16,9 +16,10 @@
 // more, and the cap keeps every reader of the table inside it.
 // The buffer holds the 128-row part, then the 256-row part; each part is
 // mtile_start [E+1] int32, then (16-byte aligned) the tile table, and is
-// 256-byte aligned.  The tables are built by one workgroup of any size
-// (a multiple of 64 threads), so the builder runs either as its own launch
-// or as an extra workgroup of a launch that runs after the routing.
+// 256-byte aligned.  The tables are built either by one workgroup of any
+// size (a multiple of 64 threads: its own launch, or an extra workgroup of a
+// launch that runs after the routing), or a slice per workgroup by several
+// workgroups that each hold the segment bounds (sched_fill_slice).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -129,15 +130,6 @@ __device__ __forceinline__ void sched_fill_slice(const int32_t* seg_lo, const in
         }
         sp.tiles[mt] = v;
     }
-}
-
-// Both tile heights' tables from segment bounds a workgroup already holds in
-// LDS (seg_lo, seg_hi: E entries each, within [0, R), monotone).
-__device__ __forceinline__ void build_tile_schedule_lds(const int32_t* seg_lo, const int32_t* seg_hi, int E,
-                                                        const SchedPart& small, const SchedPart& large) {
-    __shared__ int32_t cnt[1024];
-    sched_fill_part(seg_lo, seg_hi, cnt, E, kSchedBM[0], small);
-    sched_fill_part(seg_lo, seg_hi, cnt, E, kSchedBM[1], large);
 }
 
 // Both tile heights' tables for segments offsets[0..E] (1 <= E <= 1024).
