@@ -37,10 +37,19 @@ __device__ __forceinline__ uint4 ld_nt(const uint4* p) {
     return make_uint4(q[0], q[1], q[2], q[3]);
 }
 
-// Two fp32 -> one dword holding (lo, hi) bf16.
+// Two fp32 -> one dword holding (lo, hi) bf16, both rounded to nearest even
+// by one v_cvt_pk_bf16_f32 (converting them one at a time costs a shift and
+// an or per pair on top of two conversions).
+typedef __bf16 bf16x2_cvt __attribute__((ext_vector_type(2)));
+typedef float f32x2_cvt __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_cvt){lo, hi}, bf16x2_cvt));
 }
+
+// max(x, 0) as one integer max of the bit pattern: every negative value and
+// -0 map to +0, non-negative values pass unchanged (a NaN with the sign bit
+// clear passes too).  fmaxf costs a NaN-quieting max on top.
+__device__ __forceinline__ float relu_f32(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
 
 // MOE_DEBUG_SYNC=1 in the environment (read once per process).
 bool debug_sync_enabled();

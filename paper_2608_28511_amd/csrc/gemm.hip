@@ -604,15 +604,15 @@ __device__ __forceinline__ void staged_store(const f32x4 (&acc)[MI][4], void* C,
             const f32x4 a = acc[i][j];
             float v0 = a[0], v1 = a[1], v2 = a[2], v3 = a[3];
             if constexpr (EPI == EPI_RELU2 && OUT == 0) {
-                v0 = fmaxf(v0, 0.f); v1 = fmaxf(v1, 0.f); v2 = fmaxf(v2, 0.f); v3 = fmaxf(v3, 0.f);
+                v0 = relu_f32(v0); v1 = relu_f32(v1); v2 = relu_f32(v2); v3 = relu_f32(v3);
                 v0 *= v0; v1 *= v1; v2 *= v2; v3 *= v3;
             }
             if constexpr (EPI == EPI_DRELU2) {
                 const u32x2 u = uu[i][j];
-                v0 = v0 * 2.f * fmaxf(bf16_lo(u[0]), 0.f);
-                v1 = v1 * 2.f * fmaxf(bf16_hi(u[0]), 0.f);
-                v2 = v2 * 2.f * fmaxf(bf16_lo(u[1]), 0.f);
-                v3 = v3 * 2.f * fmaxf(bf16_hi(u[1]), 0.f);
+                v0 = v0 * 2.f * relu_f32(bf16_lo(u[0]));
+                v1 = v1 * 2.f * relu_f32(bf16_hi(u[0]));
+                v2 = v2 * 2.f * relu_f32(bf16_lo(u[1]));
+                v3 = v3 * 2.f * relu_f32(bf16_hi(u[1]));
             }
             const int ch = 2 * j + (lane >> 5);
             const u32x2 w = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
