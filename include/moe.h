@@ -31,10 +31,15 @@
  *   - Outputs must not alias inputs.  Results are deterministic: the same
  *     inputs give bit-identical outputs on every call.
  *   - S == 0 (or R == 0) is valid and enqueues nothing.
+ *   - Every entry point enqueues kernels only (no allocation, copy, memset or
+ *     host synchronisation), so a call made while `stream` is being captured
+ *     records the whole call into the graph; replays read the buffers' contents
+ *     at replay time.
  *   - Debugging only: with MOE_DEBUG_SYNC=1 in the environment (read once per
  *     process) every launch is followed by a synchronisation of `stream` and
  *     an error check, so a kernel fault is reported as MOE_ERR_HIP by the
- *     entry point that enqueued it.  Off by default.
+ *     entry point that enqueued it; a stream under graph capture is not
+ *     synchronised.  Off by default.
  *   - Limits: 1 <= E <= 1024, 1 <= K <= min(E, 32), D and F multiples of 8
  *     in [8, 65536], S*K < 2^31.  The grouped GEMM copies its
  *     operands through range-checked buffer descriptors of at most 2^31

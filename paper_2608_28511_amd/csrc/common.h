@@ -57,11 +57,19 @@ bool debug_sync_enabled();
 // Status of the launches just enqueued on st: the launch error, and with
 // MOE_DEBUG_SYNC also the outcome of running them (the stream is
 // synchronised, so a fault surfaces at the entry point that enqueued it).
+// A stream that is being captured into a graph is never synchronised.
 inline hipError_t launch_check(hipStream_t st) {
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && debug_sync_enabled()) {
-        e = hipStreamSynchronize(st);
-        if (e == hipSuccess) e = hipGetLastError();
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(st, &cs) != hipSuccess) {
+            (void)hipGetLastError();   // e.g. the null stream under a global capture: do not synchronise
+            return hipSuccess;
+        }
+        if (cs == hipStreamCaptureStatusNone) {
+            e = hipStreamSynchronize(st);
+            if (e == hipSuccess) e = hipGetLastError();
+        }
     }
     return e;
 }
