@@ -8,8 +8,9 @@ every exported output: the outputs are overwritten with NaN / sentinel values
 before each replay, eager layer calls on the same buffers run between
 replays, and after new input values are copied into the captured input
 buffer the replay must give the new eager result.  Covered: the plain layer
-(materialised and fused dispatch), the MX-FP8 payload, the latent layer and
-the production layer (sigmoid routing, shared expert, sequence loss).
+(materialised and fused dispatch), the MX-FP8 payload, the latent layer, the
+production layer (sigmoid routing, shared expert, sequence loss) and a whole
+forward and backward step through the separate entry points.
 """
 import pytest
 import torch
@@ -108,3 +109,63 @@ def test_layer_graph_replay(name):
     g.replay()
     torch.cuda.synchronize()
     _assert_same(lf.out, ref2, f"{name}: replay with new x")
+
+
+SKEW = MoEShape("graph_skew_s2048_d512_e32_k4_bwd", S=2048, D=512, E=32, K=4, F=384, bias="zipf",
+                backward=True, seed=24)
+
+
+def _train_step(inp, K):
+    """Router, route, dispatch, experts, combine and the whole backward
+    (combine^T, expert dgrads and wgrads, router backward, dispatch^T with the
+    router's input gradient added), on the current stream, no host sync."""
+    x, Wr, W1, W2, dy = inp["x"], inp["Wr"], inp["W1"], inp["W2"], inp["dy"]
+    S = x.shape[0]
+    logits = layer.router_logits(x, Wr, inp["bias"])
+    r = layer.route(logits, K)
+    x_disp, p_disp = layer.dispatch(x, r["topk_prob"], r["inv_perm"], K)
+    h, u, yd = layer.grouped_ffn(x_disp, r["offsets"], W1, W2, save_u=True)
+    y = layer.combine(yd, p_disp, r["inv_perm"], S, K)
+    dyd, dp = layer.combine_bwd(dy, yd, p_disp, r["inv_perm"], K)
+    dxd, dW1, dW2 = layer.grouped_ffn_bwd(x_disp, u, h, dyd, r["offsets"], W1, W2)
+    rb = layer.router_bwd(x, Wr, r["topk_idx"], r["topk_prob"], dp)
+    dx = layer.dispatch_bwd(dxd, r["inv_perm"], S, K, dx_add=rb["dx_r"])
+    return dict(logits=logits, topk_idx=r["topk_idx"], perm=r["perm"], y=y, dp=dp, dW1=dW1, dW2=dW2,
+                dWr=rb["dWr"], dbias=rb["dbias"], dx=dx)
+
+
+def test_train_step_graph_replay():
+    """A forward and backward step on Zipf routing (dead experts included)
+    captured once: every replay equals the eager step bit for bit, also after
+    new x and dy are copied into the captured inputs."""
+    s = SKEW
+    inp = make_inputs(s, device=DEV)
+    ref = _snapshot(_train_step(inp, s.K))
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        _train_step(inp, s.K)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        out = _train_step(inp, s.K)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        _clobber(out)
+        g.replay()
+        torch.cuda.synchronize()
+        _assert_same(out, ref, f"train step: replay {rep}")
+        _train_step(inp, s.K)   # eager work between the replays
+        torch.cuda.synchronize()
+    new = make_inputs(s.scaled(seed=s.seed + 100), device=DEV, with_experts=False)
+    inp["x"].copy_(new["x"])
+    inp["dy"].copy_(new["dy"])
+    ref2 = _snapshot(_train_step(inp, s.K))
+    torch.cuda.synchronize()
+    assert not torch.equal(ref2["dW1"], ref["dW1"])
+    _clobber(out)
+    g.replay()
+    torch.cuda.synchronize()
+    _assert_same(out, ref2, "train step: replay with new x and dy")
