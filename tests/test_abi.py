@@ -313,3 +313,19 @@ def test_binding_refuses_host_tensors():
         L._ptr(torch.zeros(4), torch.float32, "x")
     with pytest.raises(TypeError):
         L._ptr([1, 2], torch.float32, "x")
+
+
+def test_c_consumer_reports_the_header_abi_version(lib):
+    """The plain C consumer (tests/c_abi/layer_fwd_c.c, gcc, no Python) links
+    against libmoe.so and reads the same ABI version as its header (no GPU
+    call on this path)."""
+    import importlib.util
+    import subprocess
+
+    spec = importlib.util.spec_from_file_location("c_abi_build", ROOT / "tests" / "c_abi" / "build.py")
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    exe = mod.ensure_built()
+    r = subprocess.run([str(exe), "--abi"], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.split() == [str(L.moe_abi_version())] * 2
