@@ -30,9 +30,9 @@
 //                  then pos = offsets[e] + rows in earlier blocks + rank
 //                  gives perm and inv_perm for the rows of its blocks (all
 //                  of them in one pass when their per-block prefixes fit in
-//                  LDS).  In the
-//                  fused layer it also writes each routed row's probability
-//                  p_disp[pos] (the probability half of the dispatch payload),
+//                  LDS).  In the fused layer it also writes each routed
+//                  row's probability p_disp[pos] (the probability half of
+//                  the dispatch payload),
 //                  and eight extra workgroups each write a slice of the
 //                  grouped GEMM's tile tables from the offsets they hold, so
 //                  the layer needs no dispatch launch.  Every workgroup reads
