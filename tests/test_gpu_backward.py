@@ -53,29 +53,51 @@ def assert_grad_close(got, ref, what):
 
 
 EPS_BF16 = 2.0 ** -8   # relative error of one round-to-nearest to bf16 (8 significant bits)
+U32 = 2.0 ** -24       # unit roundoff of fp32
+
+
+def u_bound(xd, W1e):
+    """|u_gpu - u| of the up projection's fp32 accumulation over D products
+    (before any bf16 rounding): (D + 8) U |x_disp| @ |W1_e|.  Where u cancels
+    (|u| much smaller than its terms) this dominates the relative error of u
+    and of h = max(u, 0)^2."""
+    return (xd.shape[1] + 8) * U32 * (np.abs(xd) @ np.abs(W1e))
+
+
+def h_u_bound(u, b_u):
+    """|max(u_gpu, 0)^2 - max(u, 0)^2| from |u_gpu - u| <= b_u (a sign flip
+    near zero included): 2 max(u, 0) b_u + b_u^2."""
+    return 2 * np.maximum(u, 0) * b_u + b_u ** 2
 
 
 def bwd_bounds(xd, u, h, dyd, dxd, W1e, W2e):
     """Elementwise error bounds for one expert segment of the backward.
 
-    The GPU rounds dy_disp, u_save and du to bf16 (each <= EPS_BF16 relative)
-    before they enter fp32-accumulated products.  With mag_dh = |dy_disp| @
-    |W2^T| bounding |dh| and its error, |du_gpu - du| <= 3 * EPS_BF16 *
-    2*max(u,0) * mag_dh (one rounding each in dy_disp, u, du), so
+    The GPU's forward carries u's fp32 accumulation error b_u (u_bound) into
+    u_save and h; then it rounds dy_disp, u_save and du to bf16 (each <=
+    EPS_BF16 relative) before they enter fp32-accumulated products.  With
+    mag_dh = |dy_disp| @ |W2^T| bounding |dh| and its error,
+        |du_gpu - du|       <= (4 EPS_BF16 2 max(u,0) + 2 (1 + EPS_BF16) b_u) mag_dh
+                               (one rounding each in dy_disp, u, du, room for
+                               fp32 accumulation; u_save off by b_u as well)
         |dW1_gpu - dW1|     <= |x_disp|^T @ b_du
-        |dW2_gpu - dW2|     <= 3 * EPS_BF16 * |h|^T @ |dy_disp|   (h, dy_disp rounded)
-        |dx_disp_gpu - ref| <= b_du @ |W1^T| + EPS_BF16 * |dx_disp|  (final rounding)
-    A factor 4 instead of 3 leaves room for fp32 accumulation."""
+        |dW2_gpu - dW2|     <= 4 EPS_BF16 |h|^T @ |dy_disp| + (1 + 4 EPS_BF16) h_u^T @ |dy_disp|
+                               (h and dy_disp rounded; h_u = h_u_bound, h's
+                               error from u's)
+        |dx_disp_gpu - ref| <= b_du @ |W1^T| + EPS_BF16 * |dx_disp|  (final rounding)"""
+    b_u = u_bound(xd, W1e)
     mag_dh = np.abs(dyd) @ np.abs(W2e).T
-    b_du = 4 * EPS_BF16 * 2 * np.maximum(u, 0) * mag_dh
+    b_du = (4 * EPS_BF16 * 2 * np.maximum(u, 0) + 2 * (1 + EPS_BF16) * b_u) * mag_dh
     b_dxd = b_du @ np.abs(W1e).T + EPS_BF16 * np.abs(dxd)
-    return np.abs(xd).T @ b_du, 4 * EPS_BF16 * (np.abs(h).T @ np.abs(dyd)), b_dxd
+    b_dw2 = 4 * EPS_BF16 * (np.abs(h).T @ np.abs(dyd)) + (1 + 4 * EPS_BF16) * (h_u_bound(u, b_u).T @ np.abs(dyd))
+    return np.abs(xd).T @ b_du, b_dw2, b_dxd
 
 
-def y_bound(R, W2, S, K, E):
-    """Elementwise bound on |y_gpu - y| from the three bf16 roundings the
-    forward defines (h, the down projection's input; y_disp; y):
-        |dy_disp| <= EPS_BF16 * (|h| @ |W2_e|) + EPS_BF16 * |y_disp|
+def y_bound(R, W1, W2, S, K, E):
+    """Elementwise bound on |y_gpu - y| from the forward's fp32 accumulation
+    of u (carried into h, h_u_bound) and its three bf16 roundings (h, the
+    down projection's input; y_disp; y):
+        |dy_disp| <= (EPS_BF16 |h| + h_u) @ |W2_e| + EPS_BF16 * |y_disp|
         |dy|      <= sum_k p_k |dy_disp| + EPS_BF16 * |y|
     with a factor 1.25 of room for fp32 accumulation.  A max-relative bar
     cannot stand in for it when the down projection sums few large terms
@@ -85,7 +107,9 @@ def y_bound(R, W2, S, K, E):
     for e in range(E):
         a, b = int(off[e]), int(off[e + 1])
         if a < b:
-            b_yd[a:b] = EPS_BF16 * (np.abs(R["h"][a:b]) @ np.abs(W2[e])) + EPS_BF16 * np.abs(R["yd"][a:b])
+            h_u = h_u_bound(R["u"][a:b], u_bound(R["xd"][a:b], W1[e]))
+            b_yd[a:b] = ((EPS_BF16 * np.abs(R["h"][a:b]) + h_u) @ np.abs(W2[e])
+                         + EPS_BF16 * np.abs(R["yd"][a:b]))
     return 1.25 * (O.combine(b_yd, np.abs(R["pd"]), R["inv"], S, K) + EPS_BF16 * np.abs(R["y"]))
 
 
@@ -108,6 +132,15 @@ def test_backward_small(S, D, E, K, F):
     check_backward_case(S, D, E, K, F, seed=S + D + E)
 
 
+def test_backward_cancelling_u():
+    """A seeded random case (two rows on expert 43) where one pre-activation
+    nearly cancels (u = 4.8e-6 against sum |x||W1| = 7.4): u's fp32
+    accumulation error is then over 1% of u, so h = max(u, 0)^2 and that
+    row of dW2 miss a bound that budgets only the bf16 roundings; the
+    bounds carry the forward accumulation term (u_bound)."""
+    check_backward_case(91, 120, 53, 2, 336, seed=343)
+
+
 def check_backward_case(S, D, E, K, F, seed):
     """Forward and backward chain of one seeded case (the last expert dead)
     against the oracle, with elementwise bounds on every gradient."""
@@ -121,7 +154,7 @@ def check_backward_case(S, D, E, K, F, seed):
     G = gpu_chain(x.to(DEV), logits.to(DEV), W1.to(DEV), W2.to(DEV), dy.to(DEV), K)
     R = oracle_chain(np64(x), logits.numpy(), np64(W1), np64(W2), np64(dy), K, E)
     assert np.array_equal(npi(G["r"]["counts"]), R["counts"])
-    assert_within(np64(G["y"]), R["y"], y_bound(R, np64(W2), S, K, E), "y")
+    assert_within(np64(G["y"]), R["y"], y_bound(R, np64(W1), np64(W2), S, K, E), "y")
     assert_grad_close(np64(G["dp"]), R["dp"], "dp")
     gW1, gW2 = np64(G["dW1"]), np64(G["dW2"])
     off = R["off"]
