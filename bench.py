@@ -506,8 +506,8 @@ def other_workload(name, args, dev, stream):
     latent projection)."""
     import torch
     from paper_2608_28511_amd import _lib, layer
-    from paper_2608_28511_amd.workloads import PRODUCTION, WORKLOADS, make_inputs
-    s = {**WORKLOADS, **PRODUCTION}[name]
+    from paper_2608_28511_amd.workloads import PAPER_SHAPES, PRODUCTION, WORKLOADS, make_inputs
+    s = {**WORKLOADS, **PRODUCTION, **PAPER_SHAPES}[name]
     log(f"other workload {name}: {args.sets} input sets")
     sets = [make_inputs(s, device=dev, seed=s.seed + 1000 * i) for i in range(args.sets)]
     modes = dict(score=s.score, Fs=s.Fs, seq_len=s.seq_len, aux_coeff=s.aux_coeff)
@@ -568,13 +568,13 @@ def main():
     import torch
 
     from paper_2608_28511_amd import _lib, layer
-    from paper_2608_28511_amd.workloads import PRODUCTION, WORKLOADS, make_inputs
+    from paper_2608_28511_amd.workloads import PAPER_SHAPES, PRODUCTION, WORKLOADS, make_inputs
 
     if not torch.cuda.is_available():
         print("bench.py needs a HIP device", file=sys.stderr)
         sys.exit(1)
     _lib.load(build_if_missing=True)
-    s = {**WORKLOADS, **PRODUCTION}[args.workload]
+    s = {**WORKLOADS, **PRODUCTION, **PAPER_SHAPES}[args.workload]
     prod = s.score == "sigmoid"
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()

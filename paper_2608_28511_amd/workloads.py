@@ -104,6 +104,18 @@ PRODUCTION: Dict[str, MoEShape] = {
                                           F=3520, backward=True, seed=7, score="sigmoid",
                                           sel_bias_std=0.05, Fs=3520, seq_len=8192, aux_coeff=1e-4),
 }
+# The paper's own latent layers at the 31.5B scale (Table 2): hidden 2688
+# projected to the dispatch width d_latent, with LatentMoE's 512 experts
+# top-22 (expert width 1856) and CE-LatentMoE's 640 experts top-24 (expert
+# width 3712), over two sequences of 8192 tokens; softmax routing as in the
+# latent workload above.
+PAPER_SHAPES: Dict[str, MoEShape] = {
+    "latentmoe_s16384_h2688_d672_e512_k22": MoEShape("latentmoe_s16384_h2688_d672_e512_k22", S=16384, D=672,
+                                                     E=512, K=22, F=1856, H=2688, seed=8),
+    "celatent_s16384_h2688_d768_e640_k24": MoEShape("celatent_s16384_h2688_d768_e640_k24", S=16384, D=768,
+                                                    E=640, K=24, F=3712, H=2688, seed=9),
+}
+
 PROD_TINY = PRODUCTION["prod_tiny_s512_d256_e8_k2"]
 PROD = PRODUCTION["prod_s16384_d2688_e192_k7"]
 
