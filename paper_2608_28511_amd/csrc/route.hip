@@ -4,24 +4,20 @@
 // experts; the grouped-GEMM experts then need the S*K routed rows in
 // expert-contiguous order (fused permutation, Section 5.2).  Two launches:
 //
-//   route_topk     32 tokens per workgroup, 2 per wavefront (16 waves, so
-//                  each SIMD has several waves whose dependent max and
-//                  ballot chains overlap), all loaded up front.  K rounds,
-//                  each over the wave's two tokens together (two independent
-//                  chains), of: wave-wide max of the orderable 32-bit score
-//                  codes of the experts not yet picked (DPP within rows of 16
-//                  lanes, then the 4 row maxima), a ballot for the lowest
-//                  expert id holding that code (ties go to the lower id, NaN
-//                  ranks below -inf), and clearing the winner's code.  Then the
-//                  softmax renormalised over the K winners (or, for sigmoid
-//                  scores, the winners' sigmoids over their sum), and a per-block
-//                  LDS bitmask per expert that gives each (token, slot) its
-//                  rank among the block's rows of that expert and the block's
-//                  per-expert count, stored as one byte (at most 32) in an
-//                  expert-major count matrix [E][blocks].  For E <= 64 and
-//                  K <= 16, route_topk_rows_kernel takes one token per row of
-//                  16 lanes instead (four tokens per wave, every reduction
-//                  a DPP step within the row).
+//   route_topk     32 tokens per workgroup, one per row of 16 lanes (four per
+//                  wavefront), all scores loaded up front; lane r of a row
+//                  holds experts r + 16 i.  K rounds of: the row maximum of
+//                  the orderable 32-bit score codes of the experts not yet
+//                  picked (DPP within the row), the lowest expert id holding
+//                  it (ties go to the lower id, NaN ranks below -inf; a
+//                  lane's lowest matching slot, then the row minimum), and
+//                  clearing the winner's code.  Then the softmax renormalised
+//                  over the K winners (or, for sigmoid scores, the winners'
+//                  sigmoids over their sum), and a per-block LDS bitmask per
+//                  expert that gives each (token, slot) its rank among the
+//                  block's rows of that expert and the block's per-expert
+//                  count, stored as one byte (at most 32) in an expert-major
+//                  count matrix [E][blocks].
 //   route_scatter  each workgroup first sums, for every expert, its row of
 //                  the count matrix in full (counts, then offsets by an
 //                  exclusive scan in LDS; the first workgroup stores both)
@@ -32,12 +28,11 @@
 //                  of them in one pass when their per-block prefixes fit in
 //                  LDS).  In the fused layer it also writes each routed
 //                  row's probability p_disp[pos] (the probability half of
-//                  the dispatch payload),
-//                  and eight extra workgroups each write a slice of the
-//                  grouped GEMM's tile tables from the offsets they hold, so
-//                  the layer needs no dispatch launch.  Every workgroup reads
-//                  the whole count matrix, so the blocks are dealt to at most
-//                  256 workgroups.
+//                  the dispatch payload), and eight extra workgroups each
+//                  write a slice of the grouped GEMM's tile tables from the
+//                  offsets they hold, so the layer needs no dispatch launch.
+//                  Every workgroup reads the whole count matrix, so the
+//                  blocks are dealt to at most 256 workgroups.
 //
 // No step depends on the order in which atomics land (the LDS OR is
 // commutative and ranks come from popcounts), so the permutation is
@@ -49,8 +44,6 @@
 namespace moe {
 
 constexpr int kRouteTok = 32;  // tokens per block (one bit each in the masks)
-constexpr int kRouteThreads = 1024;
-constexpr int kTokPerWave = kRouteTok / (kRouteThreads / kWave);  // 2
 constexpr int kScatThreads = 256;
 constexpr int kScatMaxWg = 256;   // scatter workgroups (each reads the whole count matrix)
 constexpr int kPfxInts = 8192;    // LDS per-block prefixes of a scatter workgroup (blocks x experts)
@@ -79,152 +72,10 @@ __device__ __forceinline__ float code_score(uint32_t c) {
 // sigmoid in fp32 (-inf -> 0, +inf -> 1).
 __device__ __forceinline__ float sigmoid_f32(float l) { return 1.f / (1.f + expf(-l)); }
 
-// Maximum of v over the 64 lanes (all active), returned wave-uniform.
-__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
-    // pairs, quads, half rows, rows of 16 lanes: full permutations within a row
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xf, 0xf, false));   // quad_perm 1,0,3,2
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xf, 0xf, false));   // quad_perm 2,3,0,1
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xf, 0xf, false));  // row_half_mirror
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xf, 0xf, false));  // row_mirror
-    const uint32_t a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);
-    const uint32_t c = __builtin_amdgcn_readlane(v, 32), d = __builtin_amdgcn_readlane(v, 48);
-    return max(max(a, b), max(c, d));
-}
-
-// Sum of v over the 64 lanes (all active), wave-uniform, in a fixed order:
-// sums within rows of 16 lanes (pairs, quads, half rows, rows), then
-// row_bcast:15 into rows 1 and 3 and row_bcast:31 into rows 2 and 3 (lanes
-// of rows outside a broadcast's row mask add 0), so lane 63 holds the total.
+// v plus its DPP-permuted copy (lanes of rows outside the row mask add 0).
 template <int CTRL, int ROWS>
 __device__ __forceinline__ float dpp_add(float x) {
     return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROWS, 0xf, false));
-}
-__device__ __forceinline__ float wave_sum_f32(float v) {
-    v = dpp_add<0xB1, 0xf>(v);    // quad_perm 1,0,3,2
-    v = dpp_add<0x4E, 0xf>(v);    // quad_perm 2,3,0,1
-    v = dpp_add<0x141, 0xf>(v);   // row_half_mirror
-    v = dpp_add<0x140, 0xf>(v);   // row_mirror
-    v = dpp_add<0x142, 0xa>(v);   // row_bcast:15 into rows 1 and 3
-    v = dpp_add<0x143, 0xc>(v);   // row_bcast:31 into rows 2 and 3
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
-}
-
-// SIG false: selection by the logits, weights = softmax over the K picked.
-// SIG true: selection by sigmoid(logit) + sel_bias (bias may be null), weights
-// = the picked sigmoids over their sum; the bias only steers selection.
-template <int EPL, bool SIG>
-__global__ __launch_bounds__(kRouteThreads) void route_topk_kernel(
-    const float* __restrict__ logits, const float* __restrict__ sel_bias, int64_t S, int E, int K,
-    int32_t* __restrict__ topk_idx, float* __restrict__ topk_prob, uint8_t* __restrict__ blkcnt,
-    int64_t nbp, int32_t* __restrict__ rank_out) {
-    __shared__ uint32_t mask[1024];
-    __shared__ int16_t sel[kRouteTok][32];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t t_base = (int64_t)blockIdx.x * kRouteTok;
-    for (int e = tid; e < E; e += kRouteThreads) mask[e] = 0u;
-
-    // this wave's tokens t_base + wave * kTokPerWave + j: every score loaded
-    // up front, all loads issued before any is used (entries past S or E
-    // read element 0, which exists, and are masked afterwards)
-    uint32_t code[kTokPerWave][EPL];
-    float l[kTokPerWave][EPL], bias[EPL];
-#pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-        const int e = lane + kWave * i;
-        bias[i] = 0.f;
-        if constexpr (SIG) bias[i] = sel_bias != nullptr ? sel_bias[e < E ? e : 0] : 0.f;
-    }
-#pragma unroll
-    for (int j = 0; j < kTokPerWave; ++j) {
-        const int64_t t = t_base + wave * kTokPerWave + j;
-#pragma unroll
-        for (int i = 0; i < EPL; ++i) {
-            const int e = lane + kWave * i;
-            l[j][i] = logits[(t < S && e < E) ? t * E + e : 0];
-        }
-    }
-#pragma unroll
-    for (int j = 0; j < kTokPerWave; ++j) {
-        const int64_t t = t_base + wave * kTokPerWave + j;
-#pragma unroll
-        for (int i = 0; i < EPL; ++i) {
-            const int e = lane + kWave * i;
-            const uint32_t c = score_code(SIG ? sigmoid_f32(l[j][i]) + bias[i] : l[j][i]);
-            code[j][i] = (t < S && e < E) ? c : 0u;
-        }
-    }
-    __syncthreads();
-
-    // K rounds for the wave's tokens together (independent chains the
-    // scheduler interleaves).  Every code of an expert not yet picked is >= 1
-    // and K <= E, so a round's maximum is never a cleared code (a token past
-    // S has only cleared codes; its picks are never stored).  Lane k keeps
-    // the k-th pick of each token and its code.
-    int my_e[kTokPerWave] = {};
-    uint32_t my_c[kTokPerWave] = {};
-    for (int k = 0; k < K; ++k) {
-#pragma unroll
-        for (int j = 0; j < kTokPerWave; ++j) {
-            uint32_t m = code[j][0];
-#pragma unroll
-            for (int i = 1; i < EPL; ++i) m = max(m, code[j][i]);
-            m = wave_max_u32(m);
-            // the lowest expert id holding m: the lowest slot i with a
-            // match, then its lowest lane
-            int e_sel = 0;
-#pragma unroll
-            for (int i = EPL - 1; i >= 0; --i) {
-                const uint64_t b = __ballot(code[j][i] == m);
-                if (b != 0) e_sel = kWave * i + (__ffsll((unsigned long long)b) - 1);
-            }
-            const bool own = lane == (e_sel & (kWave - 1));
-#pragma unroll
-            for (int i = 0; i < EPL; ++i)
-                if (own && i == (e_sel >> 6)) code[j][i] = 0u;
-            if (lane == k) {
-                my_e[j] = e_sel;
-                my_c[j] = m;
-            }
-        }
-    }
-
-#pragma unroll
-    for (int j = 0; j < kTokPerWave; ++j) {
-        const int jt = wave * kTokPerWave + j;
-        const int64_t t = t_base + jt;
-        if (t >= S) break;
-        float z;
-        if constexpr (SIG) {
-            z = (lane < K) ? sigmoid_f32(logits[t * E + my_e[j]]) : 0.f;
-        } else {
-            const float s0 = code_score((uint32_t)__builtin_amdgcn_readlane((int)my_c[j], 0));
-            z = (lane < K) ? expf(code_score(my_c[j]) - s0) : 0.f;
-        }
-        const float sum = wave_sum_f32(z);
-        if (lane < K) {
-            topk_idx[t * K + lane] = my_e[j];
-            topk_prob[t * K + lane] = z / sum;
-            sel[jt][lane] = (int16_t)my_e[j];
-            atomicOr(&mask[my_e[j]], 1u << jt);
-        }
-    }
-    __syncthreads();
-
-    const int n_tok = (int)((S - t_base) < kRouteTok ? (S - t_base) : kRouteTok);
-    for (int q = tid; q < n_tok * K; q += kRouteThreads) {
-        const int j = q / K, k = q - j * K;
-        const int e = sel[j][k];
-        rank_out[(t_base + j) * K + k] = __popc(mask[e] & ((1u << j) - 1u));
-    }
-    for (int e = tid; e < E; e += kRouteThreads)
-        blkcnt[(int64_t)e * nbp + blockIdx.x] = (uint8_t)__popc(mask[e]);
-    // the last block also zeroes every row's padding bytes
-    const int64_t nblk = gridDim.x;
-    if ((int64_t)blockIdx.x == nblk - 1) {
-        const int pad = (int)(nbp - nblk);
-        for (int q = tid; q < E * pad; q += kRouteThreads)
-            blkcnt[(int64_t)(q / pad) * nbp + nblk + q % pad] = 0;
-    }
 }
 
 // Sum of the 16 count bytes of a chunk, and of its bytes before position lim.
@@ -270,12 +121,11 @@ __device__ __forceinline__ void row_sums(const uint8_t* row8, int64_t c0, int st
     }
 }
 
-// Row form for E <= 64 and K <= 16: one token per row of 16 lanes, so a
-// wave holds four tokens and one instruction stream serves all four.  Lane r
-// of a row holds experts r + 16 i (slot i < EPR); the row maximum and the
-// lowest expert id holding it are both DPP reductions within the row (no
-// readlane, no scalar chain).  Same selection order, same block counts and
-// ranks as route_topk_kernel.
+// Row form: one token per row of 16 lanes, so a wave holds four tokens and
+// one instruction stream serves all four.  Lane r of a row holds experts
+// r + 16 i (slot i < EPR); the row maximum and the lowest expert id holding
+// it are both DPP reductions within the row (no readlane, no scalar chain),
+// and lane r keeps picks r and r + 16 (K <= 32).
 constexpr int kRowThreads = kRouteTok * 16;   // 512: 8 waves of 4 tokens
 
 template <int CTRL>
@@ -306,38 +156,41 @@ __global__ __launch_bounds__(kRowThreads) void route_topk_rows_kernel(
     const float* __restrict__ logits, const float* __restrict__ sel_bias, int64_t S, int E, int K,
     int32_t* __restrict__ topk_idx, float* __restrict__ topk_prob, uint8_t* __restrict__ blkcnt,
     int64_t nbp, int32_t* __restrict__ rank_out) {
-    __shared__ uint32_t mask[64];
-    __shared__ int16_t sel[kRouteTok][16];
+    __shared__ uint32_t mask[1024];
+    __shared__ int16_t sel[kRouteTok][32];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int r = lane & 15, jt = wave * 4 + (lane >> 4);
     const int64_t t_base = (int64_t)blockIdx.x * kRouteTok;
     const int64_t t = t_base + jt;
-    if (tid < 64) mask[tid] = 0u;
+    for (int e = tid; e < E; e += kRowThreads) mask[e] = 0u;
 
     // every score loaded before any is used (entries past S or E read
     // element 0, which exists, and are masked afterwards)
-    float l[EPR], bias[EPR];
     uint32_t code[EPR];
+    {
+        float l[EPR], bias[EPR];
 #pragma unroll
-    for (int i = 0; i < EPR; ++i) {
-        const int e = r + 16 * i;
-        bias[i] = 0.f;
-        if constexpr (SIG) bias[i] = sel_bias != nullptr ? sel_bias[e < E ? e : 0] : 0.f;
-        l[i] = logits[(t < S && e < E) ? t * E + e : 0];
-    }
+        for (int i = 0; i < EPR; ++i) {
+            const int e = r + 16 * i;
+            bias[i] = 0.f;
+            if constexpr (SIG) bias[i] = sel_bias != nullptr ? sel_bias[e < E ? e : 0] : 0.f;
+            l[i] = logits[(t < S && e < E) ? t * E + e : 0];
+        }
 #pragma unroll
-    for (int i = 0; i < EPR; ++i) {
-        const int e = r + 16 * i;
-        const uint32_t c = score_code(SIG ? sigmoid_f32(l[i]) + bias[i] : l[i]);
-        code[i] = (t < S && e < E) ? c : 0u;
+        for (int i = 0; i < EPR; ++i) {
+            const int e = r + 16 * i;
+            const uint32_t c = score_code(SIG ? sigmoid_f32(l[i]) + bias[i] : l[i]);
+            code[i] = (t < S && e < E) ? c : 0u;
+        }
     }
     __syncthreads();
 
     // K rounds: the row's maximum code (never a cleared one: K <= E), the
     // lowest expert id holding it (a lane's lowest matching slot, then the
-    // row minimum), and clearing it.  Lane k of the row keeps the k-th pick.
-    int my_e = 0;
-    uint32_t my_c = 0u;
+    // row minimum), and clearing it.  Lane k % 16 of the row keeps the k-th
+    // pick, in its slot k / 16.
+    int my_e[2] = {0, 0};
+    uint32_t my_c[2] = {0u, 0u};
     for (int k = 0; k < K; ++k) {
         uint32_t m = code[0];
 #pragma unroll
@@ -351,25 +204,41 @@ __global__ __launch_bounds__(kRowThreads) void route_topk_rows_kernel(
 #pragma unroll
         for (int i = 0; i < EPR; ++i)
             if (own && i == (e_sel >> 4)) code[i] = 0u;
-        if (r == k) {
-            my_e = e_sel;
-            my_c = m;
+        if (r == (k & 15)) {
+            if (k < 16) {
+                my_e[0] = e_sel;
+                my_c[0] = m;
+            } else {
+                my_e[1] = e_sel;
+                my_c[1] = m;
+            }
         }
     }
 
-    float z;
+    const bool has0 = r < K, has1 = r + 16 < K;
+    float z0, z1;
     if constexpr (SIG) {
-        z = (r < K && t < S) ? sigmoid_f32(logits[t * E + my_e]) : 0.f;
+        z0 = (has0 && t < S) ? sigmoid_f32(logits[t * E + my_e[0]]) : 0.f;
+        z1 = (has1 && t < S) ? sigmoid_f32(logits[t * E + my_e[1]]) : 0.f;
     } else {
-        const float s0 = code_score((uint32_t)__shfl((int)my_c, lane & 48));
-        z = r < K ? expf(code_score(my_c) - s0) : 0.f;
+        const float s0 = code_score((uint32_t)__shfl((int)my_c[0], lane & 48));
+        z0 = has0 ? expf(code_score(my_c[0]) - s0) : 0.f;
+        z1 = has1 ? expf(code_score(my_c[1]) - s0) : 0.f;
     }
-    const float sum = row_sum_f32(z);
-    if (r < K && t < S) {
-        topk_idx[t * K + r] = my_e;
-        topk_prob[t * K + r] = z / sum;
-        sel[jt][r] = (int16_t)my_e;
-        atomicOr(&mask[my_e], 1u << jt);
+    const float sum = row_sum_f32(z0 + z1);
+    if (t < S) {
+        if (has0) {
+            topk_idx[t * K + r] = my_e[0];
+            topk_prob[t * K + r] = z0 / sum;
+            sel[jt][r] = (int16_t)my_e[0];
+            atomicOr(&mask[my_e[0]], 1u << jt);
+        }
+        if (has1) {
+            topk_idx[t * K + r + 16] = my_e[1];
+            topk_prob[t * K + r + 16] = z1 / sum;
+            sel[jt][r + 16] = (int16_t)my_e[1];
+            atomicOr(&mask[my_e[1]], 1u << jt);
+        }
     }
     __syncthreads();
 
@@ -565,27 +434,21 @@ size_t route_ws_bytes(int64_t S, int E) {
 template <bool SIG>
 static void launch_topk(const float* logits, const float* sel_bias, int64_t S, int E, int K, int32_t* topk_idx,
                         float* topk_prob, uint8_t* blkcnt, int64_t nbp, int32_t* rank, int nblk, hipStream_t st) {
-    if (E <= 64 && K <= 16) {
-        const int epr = (E + 15) / 16;
+    const int epr = (E + 15) / 16;   // E <= 1024: at most 64 slots per lane
 #define MOE_ROUTE_ROWS(N)                                                                           \
     hipLaunchKernelGGL((route_topk_rows_kernel<N, SIG>), dim3(nblk), dim3(kRowThreads), 0, st, logits, \
                        sel_bias, S, E, K, topk_idx, topk_prob, blkcnt, nbp, rank)
-        if (epr <= 1) MOE_ROUTE_ROWS(1);
-        else if (epr <= 2) MOE_ROUTE_ROWS(2);
-        else MOE_ROUTE_ROWS(4);
+    if (epr <= 1) MOE_ROUTE_ROWS(1);
+    else if (epr <= 2) MOE_ROUTE_ROWS(2);
+    else if (epr <= 4) MOE_ROUTE_ROWS(4);
+    else if (epr <= 8) MOE_ROUTE_ROWS(8);
+    else if (epr <= 16) MOE_ROUTE_ROWS(16);
+    else if (epr <= 24) MOE_ROUTE_ROWS(24);
+    else if (epr <= 32) MOE_ROUTE_ROWS(32);
+    else if (epr <= 40) MOE_ROUTE_ROWS(40);
+    else if (epr <= 48) MOE_ROUTE_ROWS(48);
+    else MOE_ROUTE_ROWS(64);
 #undef MOE_ROUTE_ROWS
-        return;
-    }
-    const int epl = (E + kWave - 1) / kWave;
-#define MOE_ROUTE_CASE(N)                                                                          \
-    hipLaunchKernelGGL((route_topk_kernel<N, SIG>), dim3(nblk), dim3(kRouteThreads), 0, st, logits, \
-                       sel_bias, S, E, K, topk_idx, topk_prob, blkcnt, nbp, rank)
-    if (epl <= 1) MOE_ROUTE_CASE(1);
-    else if (epl <= 2) MOE_ROUTE_CASE(2);
-    else if (epl <= 4) MOE_ROUTE_CASE(4);
-    else if (epl <= 8) MOE_ROUTE_CASE(8);
-    else MOE_ROUTE_CASE(16);
-#undef MOE_ROUTE_CASE
 }
 
 hipError_t launch_route(const float* logits, int64_t S, int E, int K, int32_t* topk_idx,
